@@ -1,0 +1,462 @@
+/*
+ * soma_oracle.c -- plain, slow CPU oracle for the SOMA SPSA step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg use it.  It shares no code, header, table or constant
+ * generator with the HIP path: both sides implement the same published
+ * definitions independently.
+ *
+ * What it computes (paper, arXiv 2609.37899):
+ *   - the central-difference SPSA estimator
+ *       g_hat = (1/P) sum_j [(L(theta + eps z_j) - L(theta - eps z_j)) / (2 eps)] z_j
+ *     (Section 4, Eq. main-spsa; Appendix E, Eq. localspsa), with every
+ *     direction and both signs evaluated on one shared batch (Section 4);
+ *   - the separable per-expert loss: expert e is estimated from its own L_e
+ *     only (Section 4; Appendix F, Eq. separable-training-objective), or, in
+ *     SUMMED mode, from sum_e L_e (Appendix J, independent-vs-summed losses);
+ *   - the next-byte cross entropy L_CE(h) = log sum_v exp(w_v . h) - w_y . h
+ *     (Appendix E), averaged over all targets, in nats;
+ *   - a plain stacked LSTM byte model: embedding -> LSTM_1 -> ... -> LSTM_L ->
+ *     linear head (the experts' recurrent body, Section 3 and Appendix C),
+ *     bias-free as in Appendix C, gates in the order i, f, g, o;
+ *   - the update theta' = theta - lr * g_hat (plain SGD step on g_hat).
+ *
+ * Probe law: z ~ N(0,1) per parameter, drawn by counter-based Philox4x32-10
+ * (Salmon, Moraes, Dror, Shaw, SC'11, "Parallel random numbers: as easy as
+ * 1, 2, 3") and the Box-Muller transform.  The logarithm and the sine/cosine
+ * used by Box-Muller are computed by this file's own fp32 routines (series
+ * below) so that the result is a fixed sequence of correctly rounded IEEE
+ * operations, reproducible bit for bit on any conforming machine.
+ *
+ * Precision: perturbed weights are formed in fp32 with one rounding
+ * (fmaf(+-eps, z, theta)); the forward pass, the losses, the coefficients and
+ * the update sum are carried in fp64; theta' is rounded once to fp32.
+ *
+ * Build: cc -O2 -std=c11 -fopenmp -ffp-contract=off -fno-fast-math -shared
+ *        -fPIC -o liboracle.so soma_oracle.c -lm
+ * (contraction must stay off: the RNG is specified operation by operation).
+ */
+#define _POSIX_C_SOURCE 200809L
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Model configuration (the oracle's own definition).                        */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_experts; /* N */
+  int32_t n_layers;  /* L */
+  int32_t embed;     /* E */
+  int32_t hidden;    /* H */
+  int32_t batch;     /* B sequences per expert */
+  int32_t seq_len;   /* T bytes per sequence -> T-1 targets */
+  int32_t n_pairs;   /* P antithetic pairs (directions) per expert */
+  int32_t loss_mode; /* 0: independent per-expert losses, 1: summed loss */
+} oracle_cfg;
+
+#define VOCAB 256
+
+/* Canonical flat layout of one expert's parameter vector:
+ *   Emb[V][E]; for l = 1..L: W_l[4H][in_l + H] (rows: gate blocks i,f,g,o;
+ *   columns: [input | recurrent]), in_1 = E, in_l = H; Whead[V][H].          */
+static int64_t in_dim(const oracle_cfg *c, int l) { return l == 0 ? c->embed : c->hidden; }
+
+static int64_t off_layer(const oracle_cfg *c, int l) {
+  int64_t off = (int64_t)VOCAB * c->embed;
+  for (int i = 0; i < l; ++i) off += 4LL * c->hidden * (in_dim(c, i) + c->hidden);
+  return off;
+}
+
+int64_t oracle_param_count(const oracle_cfg *c) {
+  return off_layer(c, c->n_layers) + (int64_t)VOCAB * c->hidden;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (SC'11).  One round maps (c0,c1,c2,c3) with key (k0,k1) to  */
+/*   (hi(M1*c2) ^ c1 ^ k0, lo(M1*c2), hi(M0*c0) ^ c3 ^ k1, lo(M0*c0));        */
+/* the key is advanced by the Weyl constants between rounds.                 */
+/* ------------------------------------------------------------------------ */
+#define PHILOX_M0 0xD2511F53u
+#define PHILOX_M1 0xCD9E8D57u
+#define PHILOX_W0 0x9E3779B9u
+#define PHILOX_W1 0xBB67AE85u
+
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += PHILOX_W0;
+      k1 += PHILOX_W1;
+    }
+    uint64_t p0 = (uint64_t)PHILOX_M0 * (uint64_t)x0;
+    uint64_t p1 = (uint64_t)PHILOX_M1 * (uint64_t)x2;
+    uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    uint32_t y1 = (uint32_t)p1;
+    uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    uint32_t y3 = (uint32_t)p0;
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+  }
+  out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Own fp32 elementary functions for Box-Muller.                              */
+/*                                                                            */
+/* Series coefficients are the fp32 values nearest to the exact reals        */
+/*   S_n = (-1)^((n-1)/2) (pi/2)^n / n!  (n odd)   -- sin(pi/2 r)            */
+/*   C_n = (-1)^(n/2)     (pi/2)^n / n!  (n even)  -- cos(pi/2 r)            */
+/* computed here from that definition in double and rounded once.            */
+/* ------------------------------------------------------------------------ */
+static float g_sin_c[6];  /* S1, S3, S5, S7, S9, S11 */
+static float g_cos_c[7];  /* C0, C2, ..., C12 */
+
+__attribute__((constructor)) static void oracle_init_constants(void) {
+  const double half_pi = 1.57079632679489661923132169163975144;
+  for (int i = 0; i < 6; ++i) {
+    int n = 2 * i + 1;
+    double v = 1.0;
+    for (int m = 1; m <= n; ++m) v = v * half_pi / (double)m;
+    g_sin_c[i] = (float)((i & 1) ? -v : v);
+  }
+  for (int i = 0; i < 7; ++i) {
+    int n = 2 * i;
+    double v = 1.0;
+    for (int m = 1; m <= n; ++m) v = v * half_pi / (double)m;
+    g_cos_c[i] = (float)((i & 1) ? -v : v);
+  }
+}
+
+/* Expose the coefficient table for the pin test (S1..S11 then C0..C12). */
+void oracle_series_constants(float out[13]) {
+  for (int i = 0; i < 6; ++i) out[i] = g_sin_c[i];
+  for (int i = 0; i < 7; ++i) out[6 + i] = g_cos_c[i];
+}
+
+/* ln(m * 2^-24) for integer m in [1, 2^24], in fp32.
+ * Method: write m 2^-24 = 2^n f with f in (sqrt(1/2), sqrt(2)]; then
+ * ln f = 2 atanh(s), s = (f-1)/(f+1), |s| <= 0.1716, and
+ * 2 atanh(s) = 2s (1 + s^2/3 + s^4/5 + s^6/7 + s^8/9 + s^10/11 + ...).
+ * ln 2 is split Cody-Waite style into a 16-bit head (exact products n*hi)
+ * and a tail. */
+float oracle_ln_u24(uint32_t m) {
+  int e = 31 - __builtin_clz(m);           /* floor(log2 m), 0..24 */
+  float f = ldexpf((float)m, -e);          /* exact, in [1, 2) */
+  if (f > 0x1.6a09e6p+0f) {                /* fp32 nearest to sqrt(2) */
+    f = f * 0.5f;
+    e = e + 1;
+  }
+  const float n = (float)(e - 24);
+  const float ln2_hi = 0.693145751953125f;                               /* 0x3F317200 */
+  const float ln2_lo = (float)(0.69314718055994530942 - 0.693145751953125);
+  float s = (f - 1.0f) / (f + 1.0f);
+  float s2 = s * s;
+  float q = fmaf(s2, 1.0f / 11.0f, 1.0f / 9.0f);
+  q = fmaf(s2, q, 1.0f / 7.0f);
+  q = fmaf(s2, q, 1.0f / 5.0f);
+  q = fmaf(s2, q, 1.0f / 3.0f);
+  q = q * s2;
+  float two_s = s + s;
+  float lnf = fmaf(two_s, q, two_s);
+  return fmaf(n, ln2_hi, fmaf(n, ln2_lo, lnf));
+}
+
+/* cos and sin of 2 pi i 2^-24 for integer i in [0, 2^24).
+ * Quarter-turn reduction is exact: 4 i 2^-24 = qd + r with qd the nearest
+ * integer (ties up) and r in [-1/2, 1/2); angle = pi/2 (qd + r).            */
+void oracle_sincos_2pi_u24(uint32_t i, float *c_out, float *s_out) {
+  uint32_t qd = (i + (1u << 21)) >> 22;               /* 0..4 */
+  int32_t rem = (int32_t)i - (int32_t)(qd << 22);     /* [-2^21, 2^21) */
+  float r = (float)rem * 0x1p-22f;                    /* exact */
+  float r2 = r * r;
+  float sp = fmaf(r2, g_sin_c[5], g_sin_c[4]);
+  sp = fmaf(r2, sp, g_sin_c[3]);
+  sp = fmaf(r2, sp, g_sin_c[2]);
+  sp = fmaf(r2, sp, g_sin_c[1]);
+  sp = fmaf(r2, sp, g_sin_c[0]);
+  float sn = sp * r;                                  /* sin(pi/2 r) */
+  float cp = fmaf(r2, g_cos_c[6], g_cos_c[5]);
+  cp = fmaf(r2, cp, g_cos_c[4]);
+  cp = fmaf(r2, cp, g_cos_c[3]);
+  cp = fmaf(r2, cp, g_cos_c[2]);
+  cp = fmaf(r2, cp, g_cos_c[1]);
+  float cs = fmaf(r2, cp, g_cos_c[0]);                /* cos(pi/2 r) */
+  float c, s;
+  switch (qd & 3u) {
+    case 0: c = cs;  s = sn;  break;
+    case 1: c = -sn; s = cs;  break;
+    case 2: c = -cs; s = -sn; break;
+    default: c = sn; s = -cs; break;
+  }
+  *c_out = c;
+  *s_out = s;
+}
+
+/* Box-Muller on one pair of Philox words (wa, wb):
+ *   u1 = ((wa >> 8) + 1) 2^-24 in (0, 1],  u2 = (wb >> 8) 2^-24 in [0, 1),
+ *   r = sqrt(-2 ln u1),  za = r cos(2 pi u2),  zb = r sin(2 pi u2).         */
+void oracle_box_muller(uint32_t wa, uint32_t wb, float *za, float *zb) {
+  float lnu = oracle_ln_u24((wa >> 8) + 1u);
+  float r = sqrtf(-2.0f * lnu);
+  float c, s;
+  oracle_sincos_2pi_u24(wb >> 8, &c, &s);
+  *za = r * c;
+  *zb = r * s;
+}
+
+/* Array forms of the two routines above, for the exhaustive pin tests. */
+void oracle_ln_u24_array(const uint32_t *m, int64_t n, float *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) out[i] = oracle_ln_u24(m[i]);
+}
+
+void oracle_sincos_2pi_u24_array(const uint32_t *idx, int64_t n, float *c, float *s) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) oracle_sincos_2pi_u24(idx[i], &c[i], &s[i]);
+}
+
+/* The four Gaussians z[4q .. 4q+3] of direction `pair` at SPSA step `step`
+ * for an expert whose stream seed is `seed`.
+ *   key     = (lo32(seed), hi32(seed) ^ hi32(step))
+ *   counter = (lo32(q), pair, lo32(step), hi32(q))
+ *   (w0, w1) -> z[4q], z[4q+1];  (w2, w3) -> z[4q+2], z[4q+3].            */
+static void gaussian_quad(uint64_t seed, uint64_t step, uint32_t pair, uint64_t q, float z[4]) {
+  uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32) ^ (uint32_t)(step >> 32)};
+  uint32_t ctr[4] = {(uint32_t)q, pair, (uint32_t)step, (uint32_t)(q >> 32)};
+  uint32_t w[4];
+  oracle_philox4x32_10(ctr, key, w);
+  oracle_box_muller(w[0], w[1], &z[0], &z[1]);
+  oracle_box_muller(w[2], w[3], &z[2], &z[3]);
+}
+
+void oracle_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+                     float *out) {
+  for (uint64_t i = 0; i < count; ++i) {
+    uint64_t k = k0 + i;
+    float z[4];
+    gaussian_quad(seed, step, pair, k >> 2, z);
+    out[i] = z[k & 3];
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Forward pass and loss, fp64.                                               */
+/* ------------------------------------------------------------------------ */
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/* Sum of next-byte cross entropies of one sequence (T-1 targets). */
+static double sequence_ce_sum(const oracle_cfg *c, const double *w, const uint8_t *seq,
+                              double *scratch) {
+  const int L = c->n_layers, E = c->embed, H = c->hidden, T = c->seq_len;
+  double *h = scratch;                 /* [L][H] */
+  double *cs = h + (size_t)L * H;      /* [L][H] */
+  double *x = cs + (size_t)L * H;      /* [max(E,H)] */
+  double *a = x + (E > H ? E : H);     /* [4H] */
+  double *logits = a + 4 * (size_t)H;  /* [V] */
+  memset(h, 0, sizeof(double) * 2 * (size_t)L * H);
+  const double *emb = w;
+  const double *head = w + off_layer(c, L);
+  double total = 0.0;
+  for (int t = 0; t + 1 < T; ++t) {
+    const double *erow = emb + (size_t)seq[t] * E;
+    for (int k = 0; k < E; ++k) x[k] = erow[k];
+    int xin = E;
+    for (int l = 0; l < L; ++l) {
+      const double *W = w + off_layer(c, l);
+      const int cols = xin + H;
+      double *hl = h + (size_t)l * H, *cl = cs + (size_t)l * H;
+      for (int r = 0; r < 4 * H; ++r) {
+        const double *wr = W + (size_t)r * cols;
+        double acc = 0.0;
+        for (int k = 0; k < xin; ++k) acc += wr[k] * x[k];
+        for (int k = 0; k < H; ++k) acc += wr[xin + k] * hl[k];
+        a[r] = acc;
+      }
+      for (int u = 0; u < H; ++u) {
+        double ig = sigmoid(a[u]);
+        double fg = sigmoid(a[H + u]);
+        double gg = tanh(a[2 * H + u]);
+        double og = sigmoid(a[3 * H + u]);
+        cl[u] = fg * cl[u] + ig * gg;
+        hl[u] = og * tanh(cl[u]);
+      }
+      for (int u = 0; u < H; ++u) x[u] = hl[u];
+      xin = H;
+    }
+    double mx = -INFINITY;
+    for (int v = 0; v < VOCAB; ++v) {
+      const double *wr = head + (size_t)v * H;
+      double acc = 0.0;
+      for (int k = 0; k < H; ++k) acc += wr[k] * x[k];
+      logits[v] = acc;
+      if (acc > mx) mx = acc;
+    }
+    double se = 0.0;
+    for (int v = 0; v < VOCAB; ++v) se += exp(logits[v] - mx);
+    total += log(se) + mx - logits[seq[t + 1]];
+  }
+  return total;
+}
+
+static size_t scratch_doubles(const oracle_cfg *c) {
+  const size_t L = c->n_layers, E = c->embed, H = c->hidden;
+  return 2 * L * H + (E > H ? E : H) + 4 * H + VOCAB;
+}
+
+/* Mean cross entropy (nats per target byte) of one model with fp64 weights
+ * over its B sequences of T bytes.  Sequences are independent forwards and
+ * may run in parallel; their sums are added in sequence order. */
+double oracle_forward_loss_f64(const oracle_cfg *c, const double *w, const uint8_t *bytes) {
+  const int B = c->batch, T = c->seq_len;
+  double *seq_sum = (double *)malloc(sizeof(double) * (size_t)B);
+  const size_t ns = scratch_doubles(c);
+#pragma omp parallel
+  {
+    double *scratch = (double *)malloc(sizeof(double) * ns);
+#pragma omp for schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) seq_sum[b] = sequence_ce_sum(c, w, bytes + (size_t)b * T, scratch);
+    free(scratch);
+  }
+  double total = 0.0;
+  for (int b = 0; b < B; ++b) total += seq_sum[b];
+  free(seq_sum);
+  return total / ((double)B * (double)(T - 1));
+}
+
+double oracle_forward_loss(const oracle_cfg *c, const float *w32, const uint8_t *bytes) {
+  const int64_t d = oracle_param_count(c);
+  double *w = (double *)malloc(sizeof(double) * (size_t)d);
+  for (int64_t k = 0; k < d; ++k) w[k] = (double)w32[k];
+  double loss = oracle_forward_loss_f64(c, w, bytes);
+  free(w);
+  return loss;
+}
+
+/* w = fl32(theta + s*eps*z_pair) with one rounding, s*eps passed as sign_eps. */
+void oracle_perturb(const oracle_cfg *c, const float *theta, uint64_t seed, uint64_t step,
+                    uint32_t pair, float sign_eps, float *w_out) {
+  const int64_t d = oracle_param_count(c);
+  for (int64_t q = 0; 4 * q < d; ++q) {
+    float z[4];
+    gaussian_quad(seed, step, pair, (uint64_t)q, z);
+    for (int i = 0; i < 4 && 4 * q + i < d; ++i) {
+      int64_t k = 4 * q + i;
+      w_out[k] = fmaf(sign_eps, z[i], theta[k]);
+    }
+  }
+}
+
+/* L(theta + sign*eps*z_pair) for one expert. */
+double oracle_perturbed_loss(const oracle_cfg *c, const float *theta, uint64_t seed, uint64_t step,
+                             uint32_t pair, int sign, float eps, const uint8_t *bytes) {
+  const int64_t d = oracle_param_count(c);
+  float *w = (float *)malloc(sizeof(float) * (size_t)d);
+  oracle_perturb(c, theta, seed, step, pair, sign >= 0 ? eps : -eps, w);
+  double loss = oracle_forward_loss(c, w, bytes);
+  free(w);
+  return loss;
+}
+
+/* ------------------------------------------------------------------------ */
+/* SPSA step.                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Given per-direction coefficients coef[j] = (L+ - L-)/(2 eps P), return
+ *   theta'[k] = fl32(theta[k] - lr * sum_j coef[j] z_j[k])   (sum in j order),
+ * for the listed coordinates ks[0..nk) (or all when ks == NULL), and the
+ * estimate g_hat[k] = sum_j coef[j] z_j[k] when ghat != NULL. */
+void oracle_apply_update(const oracle_cfg *c, const float *theta, uint64_t seed, uint64_t step,
+                         float lr, const double *coef, const int64_t *ks, int64_t nk,
+                         float *theta_out, double *ghat) {
+  const int P = c->n_pairs;
+  const int64_t n = ks ? nk : oracle_param_count(c);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t k = ks ? ks[i] : i;
+    double g = 0.0;
+    for (int j = 0; j < P; ++j) {
+      float z[4];
+      gaussian_quad(seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
+      g += coef[j] * (double)z[k & 3];
+    }
+    theta_out[i] = (float)((double)theta[k] - (double)lr * g);
+    if (ghat) ghat[i] = g;
+  }
+}
+
+/* One SPSA step for all experts.
+ *   theta   [N][d]   fp32, read only
+ *   seeds   [N]      per-expert Philox stream seeds
+ *   bytes   [N][B][T]
+ *   losses  [N][P][2] out: [e][j][0] = L(theta_e + eps z), [1] = L(theta_e - eps z)
+ *   coef    [N][P]    out (may be NULL): the coefficient applied to z_{e,j}
+ *   theta_out [N][d]  out
+ *   ghat    [N][d]    out (may be NULL): the estimate, fp64
+ * Returns 0, or -1 on an invalid configuration. */
+int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *seeds, uint64_t step,
+                     float eps, float lr, const uint8_t *bytes, float *losses, double *coef,
+                     float *theta_out, double *ghat) {
+  const int N = c->n_experts, P = c->n_pairs;
+  if (N < 1 || P < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
+      c->seq_len < 2)
+    return -1;
+  const int64_t d = oracle_param_count(c);
+  const size_t bstride = (size_t)c->batch * c->seq_len;
+  double *L = (double *)malloc(sizeof(double) * (size_t)N * P * 2);
+  /* 1-4: perturbed forwards, each on its expert's own batch. */
+  for (int e = 0; e < N; ++e)
+    for (int j = 0; j < P; ++j)
+      for (int s = 0; s < 2; ++s)
+        L[((size_t)e * P + j) * 2 + s] =
+            oracle_perturbed_loss(c, theta + (size_t)e * d, seeds[e], step, (uint32_t)j,
+                                  s == 0 ? +1 : -1, eps, bytes + (size_t)e * bstride);
+  /* 5: coefficients. */
+  double *cf = (double *)malloc(sizeof(double) * (size_t)N * P);
+  const double denom = 2.0 * (double)eps * (double)P;
+  for (int e = 0; e < N; ++e)
+    for (int j = 0; j < P; ++j) {
+      double diff;
+      if (c->loss_mode == 1) {
+        diff = 0.0;
+        for (int e2 = 0; e2 < N; ++e2)
+          diff += L[((size_t)e2 * P + j) * 2 + 0] - L[((size_t)e2 * P + j) * 2 + 1];
+      } else {
+        diff = L[((size_t)e * P + j) * 2 + 0] - L[((size_t)e * P + j) * 2 + 1];
+      }
+      cf[(size_t)e * P + j] = diff / denom;
+    }
+  /* 6: update. */
+  for (int e = 0; e < N; ++e)
+    oracle_apply_update(c, theta + (size_t)e * d, seeds[e], step, lr, cf + (size_t)e * P, NULL, 0,
+                        theta_out + (size_t)e * d, ghat ? ghat + (size_t)e * d : NULL);
+  /* 7: outputs. */
+  for (size_t i = 0; i < (size_t)N * P * 2; ++i) losses[i] = (float)L[i];
+  if (coef)
+    for (size_t i = 0; i < (size_t)N * P; ++i) coef[i] = cf[i];
+  free(cf);
+  free(L);
+  return 0;
+}
+
+/* Unperturbed mean cross entropy of every expert on its own batch. */
+int oracle_eval_loss(const oracle_cfg *c, const float *theta, const uint8_t *bytes, double *loss) {
+  const int64_t d = oracle_param_count(c);
+  const size_t bstride = (size_t)c->batch * c->seq_len;
+  for (int e = 0; e < c->n_experts; ++e)
+    loss[e] = oracle_forward_loss(c, theta + (size_t)e * d, bytes + (size_t)e * bstride);
+  return 0;
+}
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

@@ -1,0 +1,63 @@
+"""The workloads the SPSA step is measured and checked on.
+
+Shapes follow the paper's setting (Section 4: byte vocabulary, antithetic
++-eps directions on one shared batch, n_pert = 64, B = 64; Appendix C for the
+recurrent experts) at the sizes below.  ``n_pairs`` counts directions; each is
+evaluated at +eps and -eps, so an expert runs 2 * n_pairs perturbed forwards.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field, replace
+
+from .synth import param_count
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n_experts: int
+    n_layers: int
+    embed: int
+    hidden: int
+    batch: int
+    seq_len: int
+    n_pairs: int
+    eps: float = 1e-3
+    lr: float = 1e-3
+    loss_mode: int = 0          # 0 independent per-expert losses, 1 summed
+    cluster_seeds: tuple = field(default=())
+    pool_clusters: bool = False
+    init_seed: int = 0
+
+    @property
+    def params_per_expert(self) -> int:
+        return param_count(self.n_layers, self.embed, self.hidden)
+
+    @property
+    def flops_per_token(self) -> int:
+        """Contraction work per target token of one perturbed forward:
+        2 * sum_l (in_l + H) * 4H + 2 * H * V (elementwise work excluded)."""
+        f = 0
+        for l in range(self.n_layers):
+            f += 2 * ((self.embed if l == 0 else self.hidden) + self.hidden) * 4 * self.hidden
+        return f + 2 * self.hidden * 256
+
+    @property
+    def perturbed_tokens(self) -> int:
+        """Expert x perturbation x target-token count of one SPSA step."""
+        return self.n_experts * 2 * self.n_pairs * self.batch * (self.seq_len - 1)
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+TINY = Workload("tiny_n1_h64", 1, 1, 32, 64, 8, 64, 4, eps=1e-3, lr=1e-2, cluster_seeds=(1,))
+SOMA_N2 = Workload("soma_n2_l2_h512", 2, 2, 512, 512, 64, 256, 32, cluster_seeds=(1000, 1001))
+SOMA_N4 = Workload("soma_n4_l2_h384", 4, 2, 384, 384, 32, 512, 32,
+                   cluster_seeds=(1000, 1001, 1002, 1003))
+MONOLITH = Workload("monolith_l2_h704", 1, 2, 704, 704, 64, 256, 128,
+                    cluster_seeds=(1000, 1001), pool_clusters=True)
+SOMA_N256 = Workload("soma_n256_l1_h64", 256, 1, 32, 64, 16, 256, 32,
+                     cluster_seeds=tuple(1000 + c for c in range(256)))
+
+ALL = {w.name: w for w in (TINY, SOMA_N2, SOMA_N4, MONOLITH, SOMA_N256)}
