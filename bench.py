@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Benchmark of the SOMA SPSA step (one GPU).
+
+A step is one pass of the whole hot path for every expert: 2P antithetic
+perturbed forwards on the expert's own batch (probes regenerated in the weight
+tiles), the cross entropies, the loss reduction, the coefficients and the
+regenerate-and-update of every parameter.  Inputs (weights, byte batches,
+seeds) are resident in device memory before the timed region starts.
+
+Prints ONE JSON line.  ``value`` is the whole-job perturbed-token rate,
+N * 2P * B * (T - 1) / seconds per step; ``steps_per_sec`` is 1 / seconds per
+step.  ``roofline`` reports the dominant kernel's algorithmic FLOP rate,
+measured with HIP events recorded by the library between its launches on the
+step's stream, against the fp32 MFMA peak.  ``cpu_baseline`` times the CPU
+oracle on a bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "perturbed forward tokens/sec (expert×pert×token) + SPSA steps/sec, 1 GPU"
+PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="soma_n2_l2_h512")
+    ap.add_argument("--pairs", type=int, default=0, help="override the workload's directions per expert")
+    ap.add_argument("--pair-chunk", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="per-kernel HBM bytes from rocprofv3 counter runs (JSON), if present")
+    return ap.parse_args()
+
+
+def kernel_flops(w):
+    """Algorithmic contraction FLOPs per step, by kernel class."""
+    N, P, B, T, E, H, L = (w.n_experts, w.n_pairs, w.batch, w.seq_len, w.embed, w.hidden,
+                           w.n_layers)
+    fwd = N * 2 * P                  # perturbed forwards
+    tok = B * (T - 1)                # target tokens per forward
+    rec = fwd * tok * L * 2 * H * 4 * H
+    proj = fwd * tok * (L - 1) * 2 * H * 4 * H
+    emb_in = fwd * tok * 2 * E * 4 * H     # layer-1 input contraction (executed once per byte value)
+    head = fwd * tok * 2 * H * 256
+    return {"rec": rec, "proj": proj, "fold": emb_in, "head": head}
+
+
+def cpu_baseline(w, theta, data, seeds):
+    """Time the oracle on a bounded sample of the workload."""
+    import numpy as np
+
+    import oracle
+    cfg = oracle.cfg_from(w)
+    threads = oracle.num_threads()
+    if w.perturbed_tokens * w.flops_per_token < 2e10:
+        t0 = time.perf_counter()
+        oracle.spsa_step(cfg, theta, seeds, 0, w.eps, w.lr, data)
+        dt = time.perf_counter() - t0
+        tokens = w.perturbed_tokens
+        sample = f"full step of {w.name}"
+    else:
+        t0 = time.perf_counter()
+        for s in (+1, -1):
+            oracle.perturbed_loss(cfg, theta[0], int(seeds[0]), 0, 0, s, w.eps, data[0])
+        dt = time.perf_counter() - t0
+        tokens = 2 * w.batch * (w.seq_len - 1)
+        sample = (f"expert 0, direction 0, both signs at full B={w.batch}, T={w.seq_len} "
+                  f"({tokens} perturbed tokens of {w.perturbed_tokens} per step; "
+                  f"full step extrapolates to {dt * w.perturbed_tokens / tokens:.0f} s)")
+    return {"value": tokens / dt, "unit": "perturbed tokens/s", "cores": threads, "kind": "oracle",
+            "sample": sample, "seconds": dt}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; "
+                                   f"--gpus {args.gpus} is not supported (experts shard across "
+                                   "GPUs with no communication; see DESIGN.md)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_37899_amd import soma, synth, workloads
+
+    w = workloads.ALL[args.workload]
+    if args.pairs:
+        w = w.with_(n_pairs=args.pairs)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    shape = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
+                       w.loss_mode, args.pair_chunk)
+    theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
+    nb = max(1, min(args.steps + args.warmup, 3))
+    batches = [synth.expert_batches(w.cluster_seeds, w.batch, w.seq_len, data_seed=i,
+                                    pool=w.pool_clusters) for i in range(nb)]
+    seeds_np = synth.expert_seeds(w.n_experts)
+
+    ctx = soma.Context(shape, device=dev)
+    theta = torch.from_numpy(theta0.copy()).to(dev)
+    seeds = soma.seeds_tensor(seeds_np, dev)
+    dbatches = [torch.from_numpy(b).to(dev) for b in batches]
+    losses = torch.zeros((w.n_experts, w.n_pairs, 2), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        ctx.spsa_step(theta, seeds, i, w.eps, w.lr, dbatches[i % nb], losses)
+    torch.cuda.synchronize()
+
+    ctx.set_phase_timing(True)
+    phases = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ctx.spsa_step(theta, seeds, args.warmup + i, w.eps, w.lr, dbatches[(args.warmup + i) % nb], losses)
+        pt = ctx.phase_times()          # waits for this step's last event
+        for k, v in pt.items():
+            phases[k] = phases.get(k, 0) + v
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_phase_timing(False)
+    sec = (t1 - t0) / args.steps
+    lv = losses.cpu().numpy()
+    assert np.all(np.isfinite(lv)), "non-finite losses"
+
+    # Dominant kernel and its roofline.
+    fl = kernel_flops(w)
+    K = args.steps
+    ms = {"rec": phases["rec_ms"] / K, "proj": phases["proj_ms"] / K, "fold": phases["fold_ms"] / K,
+          "head": phases["head_ms"] / K, "reduce": phases["reduce_ms"] / K,
+          "update": phases["update_ms"] / K}
+    launches = {"rec": phases["rec_launches"] / K, "proj": max(phases["proj_launches"] / K, 1),
+                "fold": 1, "head": 1}
+    dom = max(("rec", "proj", "fold", "head"), key=lambda k: ms[k])
+    per_launch_flops = fl[dom] / launches[dom]
+    avg_launch_s = ms[dom] / 1e3 / launches[dom]
+    achieved = per_launch_flops / avg_launch_s / 1e12
+    traffic = None
+    kname = {"rec": "k_rec_step", "proj": "k_proj", "fold": "k_fold", "head": "k_head_ce"}[dom]
+    if os.path.exists(args.traffic):
+        try:
+            tj = json.load(open(args.traffic))
+            ent = tj.get(w.name, {}).get(kname)
+            if ent and ent.get("source_hash") == tj.get("current_hash", {}).get(kname):
+                traffic = ent["bytes_per_launch"]
+        except Exception:
+            traffic = None
+    roof = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 3),
+            "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_FP32_MFMA_TFLOPS, 4), "traffic": traffic,
+            "flops_per_launch": per_launch_flops, "avg_launch_ms": round(avg_launch_s * 1e3, 4),
+            "launches_per_step": launches[dom]}
+    total_flops = w.perturbed_tokens * w.flops_per_token
+    out = {
+        "metric": METRIC,
+        "value": round(w.perturbed_tokens / sec, 1),
+        "unit": "perturbed tokens/s",
+        "steps_per_sec": round(1.0 / sec, 4),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic: order-2 Markov byte chains, Dirichlet(0.1) rows, one chain per expert",
+        "config": {"workload": w.name, "n_experts": w.n_experts, "n_layers": w.n_layers,
+                   "embed": w.embed, "hidden": w.hidden, "batch": w.batch, "seq_len": w.seq_len,
+                   "n_pairs": w.n_pairs, "forwards_per_expert": 2 * w.n_pairs,
+                   "params_per_expert": w.params_per_expert, "eps": w.eps, "lr": w.lr,
+                   "loss_mode": "summed" if w.loss_mode else "independent",
+                   "parallelism": "single GPU, all experts and directions in each launch"},
+        "algorithmic_tflops": round(total_flops / sec / 1e12, 3),
+        "phase_ms": {k: round(v, 3) for k, v in ms.items()},
+        "roofline": roof,
+        "mean_loss": float(np.mean(lv)),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, theta0, batches[0], seeds_np)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

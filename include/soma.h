@@ -1,0 +1,188 @@
+/*
+ * soma.h -- C ABI of the MI355X (gfx950) SOMA SPSA hot path.
+ *
+ * SOMA (arXiv 2609.37899) trains an ensemble of N byte-level LSTM experts
+ * with zero-order SPSA.  One step of the method, for every expert e:
+ *
+ *   1. draw P directions z_{e,j} ~ N(0, I) over all d parameters of e;
+ *   2. evaluate the antithetic losses L_{e,j,+-} = L_e(theta_e +- eps z_{e,j})
+ *      on the expert's own batch, all directions and both signs sharing it
+ *      (Section 4; Appendix E, Eq. localspsa);
+ *   3. form the coefficients c_{e,j} = (L_{e,j,+} - L_{e,j,-}) / (2 eps P)
+ *      (Section 4, Eq. main-spsa), or in SUMMED mode
+ *      c_j = sum_e (L_{e,j,+} - L_{e,j,-}) / (2 eps P) for every expert
+ *      (Appendix J, independent vs summed losses);
+ *   4. apply theta_e <- theta_e - lr * sum_j c_{e,j} z_{e,j}, regenerating
+ *      every z_{e,j} from its counter instead of storing it.
+ *
+ * The model (Section 3 and Appendix C, bias-free) is: byte embedding
+ * Emb[256][E] -> L stacked LSTM layers (gate order i, f, g, o; h0 = c0 = 0
+ * per sequence) -> linear head Whead[256][H] -> softmax cross entropy over
+ * the 256 byte values (Appendix E, L_CE).  A sequence of T bytes gives T-1
+ * (input, target) pairs; L is the mean over all B(T-1) targets, in nats.
+ *
+ * Parameter layout (one expert, fp32, flat, canonical index k):
+ *   Emb[256][E]; for l = 1..L: W_l[4H][in_l + H] with rows in gate blocks
+ *   i, f, g, o and columns [input | recurrent], in_1 = E, in_l = H;
+ *   Whead[256][H].  d = 256 E + sum_l 4H (in_l + H) + 256 H.
+ *
+ * Probe stream (exact, reproducible bit for bit): z_{e,j}[k] is element
+ * k & 3 of the Gaussian quad for q = k >> 2, obtained from
+ *   Philox4x32-10 (Salmon et al., SC'11) with
+ *     key     = (lo32(seed_e), hi32(seed_e) ^ hi32(step)),
+ *     counter = (lo32(q), j, lo32(step), hi32(q)),
+ *   and Box-Muller on the word pairs (w0, w1) -> z[4q], z[4q+1] and
+ *   (w2, w3) -> z[4q+2], z[4q+3]:
+ *     u1 = ((wa >> 8) + 1) 2^-24, u2 = (wb >> 8) 2^-24,
+ *     za = sqrt(-2 ln u1) cos(2 pi u2), zb = sqrt(-2 ln u1) sin(2 pi u2),
+ *   where ln, cos and sin are fixed fp32 series evaluations (an atanh series
+ *   for ln, Taylor series of sin and cos of (pi/2) r after an exact
+ *   quarter-turn reduction) with correctly rounded +, *, /, fma and sqrt.
+ *   Perturbed weights are fmaf(+-eps, z, theta) (one rounding).
+ *
+ * Conventions for every entry point:
+ *   - Pointers named *_dev are device pointers (HIP), caller owned, and must
+ *     stay valid until the work enqueued on `stream` has finished.  Other
+ *     pointers are host pointers read before the call returns.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is
+ *     asynchronous; the caller synchronises.
+ *   - The library allocates no device memory: scratch space is the caller's
+ *     workspace buffer, sized by soma_workspace_size().
+ *   - Return value: SOMA_OK or a negative error code; on error nothing is
+ *     enqueued and no output is modified.  soma_last_error() returns a
+ *     thread-local description of the last error.
+ */
+#ifndef SOMA_H_
+#define SOMA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SOMA_VOCAB 256
+
+enum soma_status {
+  SOMA_OK = 0,
+  SOMA_EINVAL = -1,     /* null pointer, bad scalar (eps <= 0, non-finite lr), bad mode */
+  SOMA_ESHAPE = -2,     /* unsupported shape (see soma_config) */
+  SOMA_EDEVICE = -3,    /* a HIP call or kernel launch failed */
+  SOMA_EWORKSPACE = -4  /* workspace missing, misaligned or too small */
+};
+
+enum soma_loss_mode {
+  SOMA_LOSS_INDEPENDENT = 0, /* c_{e,j} from expert e's own losses (Section 4) */
+  SOMA_LOSS_SUMMED = 1       /* c_j from the summed loss, applied to all experts (Appendix J) */
+};
+
+/* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;
+ * embed and hidden positive multiples of 16; batch >= 1; seq_len >= 2;
+ * pair_chunk in [0, n_pairs] (0 picks a chunk that keeps the workspace
+ * under 24 GiB; the step processes the P directions in chunks of this many,
+ * which changes memory use but not the result). */
+typedef struct soma_config {
+  int32_t n_experts;  /* N */
+  int32_t n_layers;   /* L */
+  int32_t embed;      /* E */
+  int32_t hidden;     /* H */
+  int32_t batch;      /* B sequences per expert */
+  int32_t seq_len;    /* T bytes per sequence */
+  int32_t n_pairs;    /* P antithetic directions per expert (2P forwards) */
+  int32_t loss_mode;  /* enum soma_loss_mode */
+  int32_t pair_chunk; /* directions evaluated per pass; 0 = automatic */
+  int32_t reserved;   /* must be 0 */
+} soma_config;
+
+typedef struct soma_ctx soma_ctx;
+
+/* d, the number of parameters of one expert (layout above).  Pure. */
+int soma_param_count(const soma_config* cfg, int64_t* per_expert);
+
+/* Bytes of device workspace soma_create() needs for this shape.  Pure. */
+int soma_workspace_size(const soma_config* cfg, size_t* bytes);
+
+/* Bind a shape to a caller-owned device workspace of at least
+ * soma_workspace_size() bytes, 256-byte aligned.  The context is host
+ * memory owned by the library until soma_destroy(); one context must not be
+ * used by two streams at once (its workspace is shared). */
+int soma_create(const soma_config* cfg, void* workspace_dev, size_t workspace_bytes,
+                soma_ctx** out);
+void soma_destroy(soma_ctx* ctx);
+
+/* One SPSA step (Section 4, Eq. main-spsa; Appendix E, Eq. localspsa, with
+ * a plain step theta <- theta - lr g_hat in place of Adam).
+ *   theta_dev  [N][d] fp32, updated in place.  It is written only by the
+ *              final update kernel, after every loss of the step exists.
+ *   seeds_dev  [N] uint64, the per-expert probe stream seeds.
+ *   step       the step counter that keys the probe stream.
+ *   eps        perturbation radius, finite and > 0.
+ *   lr         learning rate, finite.
+ *   bytes_dev  [N][B][T] uint8, expert e's batch (shared by all its
+ *              directions and both signs).
+ *   losses_dev [N][P][2] fp32 out: [e][j][0] = L(theta_e + eps z_{e,j}),
+ *              [e][j][1] = L(theta_e - eps z_{e,j}), mean nats per target.
+ * The coefficients of the step stay in the workspace until the next call
+ * and can be read with soma_coefficients(). */
+int soma_spsa_step(soma_ctx* ctx, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,
+                   float eps, float lr, const uint8_t* bytes_dev, float* losses_dev, void* stream);
+
+/* Unperturbed mean cross entropy of every expert on its own batch
+ * (Appendix E, L_CE; the expert validation loss of Section 6).
+ *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8, loss_dev [N] fp32 out. */
+int soma_eval_loss(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev,
+                   float* loss_dev, void* stream);
+
+/* Copy the coefficients c[N][P] (fp32) of the last soma_spsa_step on this
+ * context into coef_dev (device-to-device, on `stream`). */
+int soma_coefficients(soma_ctx* ctx, float* coef_dev, void* stream);
+
+/* The update of step 4 alone, for given coefficients:
+ *   theta_e[k] <- theta_e[k] - lr * sum_{j<P} coef[e][j] z_{e,j}[k]
+ * (sum in j order, fp32).  coef_dev [N][P] fp32 (device).  This is the
+ * kernel soma_spsa_step ends with; it is exposed so that the update can be
+ * checked and reused on its own (e.g. to replay a step from stored losses). */
+int soma_apply_update(soma_ctx* ctx, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,
+                      float lr, const float* coef_dev, void* stream);
+
+/* The probe values z_{seed,step,pair}[k] for k in [k0, k0 + count), written
+ * to out_dev [count] fp32.  k0 + count must not exceed 2^40. */
+int soma_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+                  float* out_dev, void* stream);
+
+/* Philox4x32-10 on n (counter, key) pairs: ctr_dev [n][4], key_dev [n][2],
+ * out_dev [n][4], all uint32 device arrays. */
+int soma_philox(const uint32_t* ctr_dev, const uint32_t* key_dev, uint32_t* out_dev, uint64_t n,
+                void* stream);
+
+/* Per-phase device time of the last soma_spsa_step on a context, from HIP
+ * events recorded on the step's stream between its kernel launches (off by
+ * default; enabling adds one event record per phase boundary).  Times are
+ * summed over direction chunks. */
+typedef struct soma_phase_times {
+  float fold_ms;          /* layer-1 gate inputs per byte value (k_fold) */
+  float proj_ms;          /* input projections of layers >= 2 (k_proj) */
+  float rec_ms;           /* recurrent time steps of all layers (k_rec_step) */
+  float head_ms;          /* head + softmax cross entropy (k_head_ce) */
+  float reduce_ms;        /* loss sums and coefficients */
+  float update_ms;        /* regenerate-and-update (k_update) */
+  int32_t rec_launches;   /* k_rec_step launches in the step */
+  int32_t proj_launches;  /* k_proj launches in the step */
+} soma_phase_times;
+
+/* Turn phase timing on (enable != 0) or off for later steps on ctx. */
+int soma_set_phase_timing(soma_ctx* ctx, int enable);
+
+/* Wait for the last timed step's events and report its phase times.
+ * Returns SOMA_EINVAL if no step ran with timing enabled. */
+int soma_get_phase_times(soma_ctx* ctx, soma_phase_times* out);
+
+/* Thread-local description of the last error ("" if none). */
+const char* soma_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOMA_H_ */

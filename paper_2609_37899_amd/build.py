@@ -1,0 +1,47 @@
+"""Build ``libsoma.so`` (the HIP library behind include/soma.h) for gfx950.
+
+Run ``python -m paper_2609_37899_amd.build`` (or ``__graft_entry__.build()``).
+The library is built in-tree next to this file.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+SRC = os.path.join(PKG, "csrc", "soma_api.hip")
+DEPS = [os.path.join(PKG, "csrc", f) for f in ("soma_api.hip", "soma_kernels.hpp", "soma_rng.hpp")] + \
+       [os.path.join(ROOT, "include", "soma.h")]
+LIB = os.path.join(PKG, "libsoma.so")
+ARCH = os.environ.get("SOMA_OFFLOAD_ARCH", "gfx950")
+
+HIPCC_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    # The probe generator is specified operation by operation: no contraction.
+    "-ffp-contract=off",
+    # Packed fp32 VALU instructions stay off (build notes).
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-command-line-argument",
+]
+
+
+def hipcc() -> str:
+    return shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+
+
+def build(verbose: bool = False) -> str:
+    tmp = LIB + ".tmp%d" % os.getpid()
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
+           "-o", tmp, SRC]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd, cwd="/tmp")
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

@@ -1,0 +1,533 @@
+// soma_api.hip -- C ABI of the SOMA SPSA hot path on gfx950 (see soma.h).
+//
+// One step enqueues, per chunk of directions (all experts at once):
+//   k_fold        layer-1 gate inputs per byte value, both signs
+//   per layer l:  k_proj (l >= 2) then T-1 launches of k_rec_step
+//   k_head_ce     head + softmax cross entropy, per-tile sums
+//   k_loss_reduce fixed-order sums -> L_{e,j,+-}
+// and then, once for the step:
+//   k_coef        c_{e,j} (independent) or c_j (summed)
+//   k_update      theta -= lr sum_j c_j z_j, regenerating every z_j
+// The step writes theta only in k_update, after every loss exists.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "soma.h"
+#include "soma_kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return SOMA_OK;
+}
+
+constexpr size_t kAlign = 256;
+constexpr size_t kAutoBudget = size_t(24) << 30;  // automatic pair_chunk keeps the workspace below this
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  int64_t d = 0;
+  int64_t off_layer[64] = {};
+  int64_t off_head = 0;
+  int pc = 0;          // directions per pass
+  int row_tiles = 0;   // head tiles per slot
+  size_t coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, total = 0;
+};
+
+int64_t param_count_of(const soma_config& c) {
+  int64_t d = int64_t(SOMA_VOCAB) * c.embed;
+  for (int l = 0; l < c.n_layers; ++l)
+    d += 4LL * c.hidden * ((l == 0 ? c.embed : c.hidden) + c.hidden);
+  return d + int64_t(SOMA_VOCAB) * c.hidden;
+}
+
+int validate(const soma_config* c) {
+  if (!c) return fail(SOMA_EINVAL, "config is NULL");
+  if (c->n_experts < 1 || c->n_layers < 1 || c->n_pairs < 1 || c->batch < 1)
+    return fail(SOMA_ESHAPE, "n_experts, n_layers, n_pairs and batch must be >= 1");
+  if (c->n_layers > 64) return fail(SOMA_ESHAPE, "at most 64 layers");
+  if (c->seq_len < 2) return fail(SOMA_ESHAPE, "seq_len must be >= 2 (T-1 targets)");
+  if (c->embed < 16 || c->embed % 16 || c->hidden < 16 || c->hidden % 16)
+    return fail(SOMA_ESHAPE, "embed and hidden must be positive multiples of 16 (got %d, %d)",
+                c->embed, c->hidden);
+  if (c->loss_mode != SOMA_LOSS_INDEPENDENT && c->loss_mode != SOMA_LOSS_SUMMED)
+    return fail(SOMA_EINVAL, "loss_mode must be 0 (independent) or 1 (summed)");
+  if (c->pair_chunk < 0 || c->pair_chunk > c->n_pairs)
+    return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs]");
+  if (c->reserved != 0) return fail(SOMA_EINVAL, "reserved must be 0");
+  const int64_t d = param_count_of(*c);
+  if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
+  const int64_t rows = int64_t(c->seq_len - 1) * c->batch;
+  if (rows >= (int64_t(1) << 31)) return fail(SOMA_ESHAPE, "B (T-1) must stay below 2^31");
+  return SOMA_OK;
+}
+
+Layout layout_for(const soma_config& c, int pc) {
+  Layout L;
+  L.d = param_count_of(c);
+  int64_t off = int64_t(SOMA_VOCAB) * c.embed;
+  for (int l = 0; l < c.n_layers; ++l) {
+    L.off_layer[l] = off;
+    off += 4LL * c.hidden * ((l == 0 ? c.embed : c.hidden) + c.hidden);
+  }
+  L.off_head = off;
+  L.pc = pc;
+  const size_t N = c.n_experts, H = c.hidden, B = c.batch, R = size_t(c.seq_len - 1) * B;
+  L.row_tiles = int((R + 63) / 64);
+  const size_t slots = N * size_t(pc) * 2;
+  size_t at = 0;
+  L.coef = at; at += round_up(sizeof(float) * N * c.n_pairs);
+  L.lossd = at; at += round_up(sizeof(double) * N * c.n_pairs * 2);
+  L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
+  L.U = at;    at += round_up(sizeof(float) * slots * SOMA_VOCAB * 4 * H);
+  L.hseq = at; at += round_up(sizeof(float) * slots * R * H);
+  L.cst = at;  at += round_up(sizeof(float) * slots * B * H);
+  L.gin = at;
+  if (c.n_layers > 1) at += round_up(sizeof(float) * slots * R * 4 * H);
+  L.total = at;
+  return L;
+}
+
+int choose_chunk(const soma_config& c) {
+  if (c.pair_chunk > 0) return c.pair_chunk;
+  int pc = c.n_pairs;
+  while (pc > 1 && layout_for(c, pc).total > kAutoBudget) --pc;
+  return pc;
+}
+
+}  // namespace
+
+enum Phase { kPhaseStart = -1, kPhaseFold, kPhaseProj, kPhaseRec, kPhaseHead, kPhaseReduce, kPhaseUpdate };
+
+struct soma_ctx {
+  soma_config cfg;
+  Layout lay;
+  char* ws;
+  size_t ws_bytes;
+  bool have_coef;
+  // phase timing
+  bool timing;
+  bool have_times;
+  std::vector<hipEvent_t> events;   // pool, grows on demand
+  std::vector<int> phase;           // phase closed by events[i]
+  size_t nmarks;
+  int rec_launches, proj_launches;
+};
+
+namespace soma {
+
+// z values for a contiguous index range (probe dump).
+__global__ void k_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+                           float* out) {
+  const uint64_t q = (k0 >> 2) + blockIdx.x * uint64_t(blockDim.x) + threadIdx.x;
+  const uint64_t qend = (k0 + count + 3) >> 2;
+  if (q >= qend) return;
+  const float4 z = gauss_quad(stream_key(seed, step), pair, static_cast<uint32_t>(step), q);
+  const float zz[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint64_t k = 4 * q + i;
+    if (k >= k0 && k < k0 + count) out[k - k0] = zz[i];
+  }
+}
+
+__global__ void k_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out, uint64_t n) {
+  const uint64_t i = blockIdx.x * uint64_t(blockDim.x) + threadIdx.x;
+  if (i >= n) return;
+  const uint4 r = philox4x32_10(make_uint4(ctr[4 * i], ctr[4 * i + 1], ctr[4 * i + 2], ctr[4 * i + 3]),
+                                make_uint2(key[2 * i], key[2 * i + 1]));
+  out[4 * i] = r.x;
+  out[4 * i + 1] = r.y;
+  out[4 * i + 2] = r.z;
+  out[4 * i + 3] = r.w;
+}
+
+// L[e][j0 + jl][s] = (sum over tiles in order) / (B (T-1)), accumulated in
+// fp64; the fp64 mean is kept (lossd) so that the antithetic difference is
+// taken before any rounding to fp32.  One thread per slot.
+__global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs, int PC, int NS,
+                              int P, int j0, double inv_rows, float* losses, double* lossd) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N * pcs * NS) return;
+  const int s = i % NS, jl = (i / NS) % pcs, e = i / (NS * pcs);
+  const double* p = part + ((int64_t(e) * PC + jl) * NS + s) * row_tiles;
+  double tot = 0.0;
+  for (int k = 0; k < row_tiles; ++k) tot += p[k];
+  const int64_t o = (int64_t(e) * P + j0 + jl) * NS + s;
+  losses[o] = static_cast<float>(tot * inv_rows);
+  if (lossd) lossd[o] = tot * inv_rows;
+}
+
+// c[e][j] = (L+ - L-) / (2 eps P) from the fp64 means, rounded once to fp32;
+// summed mode: the differences of all experts added in expert order, the
+// same coefficient for every expert.
+__global__ void k_coef(const double* lossd, int N, int P, int summed, double inv_denom, float* coef) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N * P) return;
+  const int j = i % P, e = i / P;
+  double diff;
+  if (summed) {
+    diff = 0.0;
+    for (int e2 = 0; e2 < N; ++e2) diff += lossd[(int64_t(e2) * P + j) * 2] - lossd[(int64_t(e2) * P + j) * 2 + 1];
+  } else {
+    diff = lossd[(int64_t(e) * P + j) * 2] - lossd[(int64_t(e) * P + j) * 2 + 1];
+  }
+  coef[i] = static_cast<float>(diff * inv_denom);
+}
+
+// theta[e][k] -= lr * sum_{j<P} coef[e][j] z_{e,j}[k], one probe quad per
+// thread and direction; the sum runs in j order in fp32.
+__global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* seeds, uint64_t step,
+                                                 float lr, const float* coef, int64_t d, int P) {
+  const int e = blockIdx.y;
+  const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
+  if (4 * q >= d) return;
+  const uint2 key = stream_key(seeds[e], step);
+  const uint32_t step_lo = static_cast<uint32_t>(step);
+  const float* c = coef + int64_t(e) * P;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < P; ++j) {
+    const float cj = c[j];
+    const float4 z = gauss_quad(key, static_cast<uint32_t>(j), step_lo, static_cast<uint64_t>(q));
+    acc = fma4(cj, z, acc);
+  }
+  float* t = theta + int64_t(e) * d + 4 * q;
+  if (4 * q + 4 <= d) {
+    float4 v = *reinterpret_cast<float4*>(t);
+    v = fma4(-lr, acc, v);
+    *reinterpret_cast<float4*>(t) = v;
+  } else {
+    const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
+    for (int i = 0; 4 * q + i < d; ++i) t[i] = __builtin_fmaf(-lr, a4[i], t[i]);
+  }
+}
+
+}  // namespace soma
+
+namespace {
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SOMA_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+  return SOMA_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Record a phase boundary on the stream (no-op unless timing is on).
+int mark(soma_ctx* ctx, int phase, hipStream_t st) {
+  if (!ctx->timing) return SOMA_OK;
+  if (ctx->nmarks == ctx->events.size()) {
+    hipEvent_t ev;
+    const hipError_t e = hipEventCreate(&ev);
+    if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipEventCreate: %s", hipGetErrorString(e));
+    ctx->events.push_back(ev);
+    ctx->phase.push_back(phase);
+  }
+  ctx->phase[ctx->nmarks] = phase;
+  const hipError_t e = hipEventRecord(ctx->events[ctx->nmarks], st);
+  if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipEventRecord: %s", hipGetErrorString(e));
+  ++ctx->nmarks;
+  return SOMA_OK;
+}
+
+template <bool kPert>
+int launch_rec(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
+  const int B = a.B;
+  if (B <= 16)
+    hipLaunchKernelGGL((soma::k_rec_step<1, kPert>), grid, dim3(soma::kThreads), 0, st, a);
+  else if (B <= 32)
+    hipLaunchKernelGGL((soma::k_rec_step<2, kPert>), grid, dim3(soma::kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((soma::k_rec_step<4, kPert>), grid, dim3(soma::kThreads), 0, st, a);
+  return SOMA_OK;
+}
+
+int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
+
+// Forward passes of `pcs` directions starting at j0 (kPert) or of the
+// unperturbed experts (!kPert, pcs = 1), ending with per-tile loss sums.
+template <bool kPert>
+int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, float eps,
+                const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
+  const soma_config& c = ctx->cfg;
+  const Layout& L = ctx->lay;
+  soma::FwdArgs a{};
+  a.theta = theta;
+  a.bytes = bytes;
+  a.seeds = seeds;
+  a.U = reinterpret_cast<float*>(ctx->ws + L.U);
+  a.gin = reinterpret_cast<float*>(ctx->ws + L.gin);
+  a.hseq = reinterpret_cast<float*>(ctx->ws + L.hseq);
+  a.cst = reinterpret_cast<float*>(ctx->ws + L.cst);
+  a.part = reinterpret_cast<double*>(ctx->ws + L.part);
+  a.d = L.d;
+  a.off_head = L.off_head;
+  a.step = step;
+  a.eps = eps;
+  a.N = c.n_experts;
+  a.E = c.embed;
+  a.H = c.hidden;
+  a.B = c.batch;
+  a.T = c.seq_len;
+  a.PC = kPert ? L.pc : 1;
+  a.j0 = j0;
+  a.pcs = pcs;
+  a.row_tiles = L.row_tiles;
+  const int H = c.hidden, N = c.n_experts;
+  const int64_t R = int64_t(c.seq_len - 1) * c.batch;
+
+  a.layer = 0;
+  a.in_l = c.embed;
+  a.off_l = L.off_layer[0];
+  hipLaunchKernelGGL((soma::k_fold<kPert>), dim3(4 * H / 64, SOMA_VOCAB / 64, N * pcs),
+                     dim3(soma::kThreads), 0, st, a);
+  if (int rc = check_launch("k_fold")) return rc;
+  if (int rc = mark(ctx, kPhaseFold, st)) return rc;
+  const int rb = rec_row_block(c.batch);
+  const int bgroups = (c.batch + rb - 1) / rb;
+  for (int l = 0; l < c.n_layers; ++l) {
+    a.layer = l;
+    a.in_l = l == 0 ? c.embed : c.hidden;
+    a.off_l = L.off_layer[l];
+    if (l > 0) {
+      hipLaunchKernelGGL((soma::k_proj<kPert>),
+                         dim3(4 * H / 64, unsigned((R + 127) / 128), N * pcs),
+                         dim3(soma::kThreads), 0, st, a);
+      if (int rc = check_launch("k_proj")) return rc;
+      if (int rc = mark(ctx, kPhaseProj, st)) return rc;
+      ++ctx->proj_launches;
+    }
+    const dim3 grid((H / 16) * bgroups, pcs, N);
+    for (int t = 0; t + 1 < c.seq_len; ++t) {
+      a.t = t;
+      launch_rec<kPert>(a, grid, st);
+    }
+    if (int rc = check_launch("k_rec_step")) return rc;
+    if (int rc = mark(ctx, kPhaseRec, st)) return rc;
+    ctx->rec_launches += c.seq_len - 1;
+  }
+  hipLaunchKernelGGL((soma::k_head_ce<kPert>), dim3(L.row_tiles, N * pcs), dim3(soma::kThreads), 0,
+                     st, a);
+  if (int rc = check_launch("k_head_ce")) return rc;
+  return mark(ctx, kPhaseHead, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* soma_last_error(void) { return g_last_error.c_str(); }
+
+int soma_param_count(const soma_config* cfg, int64_t* per_expert) {
+  if (int rc = validate(cfg)) return rc;
+  if (!per_expert) return fail(SOMA_EINVAL, "per_expert is NULL");
+  *per_expert = param_count_of(*cfg);
+  return ok();
+}
+
+int soma_workspace_size(const soma_config* cfg, size_t* bytes) {
+  if (int rc = validate(cfg)) return rc;
+  if (!bytes) return fail(SOMA_EINVAL, "bytes is NULL");
+  *bytes = layout_for(*cfg, choose_chunk(*cfg)).total;
+  return ok();
+}
+
+int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_ctx** out) {
+  if (int rc = validate(cfg)) return rc;
+  if (!out) return fail(SOMA_EINVAL, "out is NULL");
+  const Layout L = layout_for(*cfg, choose_chunk(*cfg));
+  if (!workspace) return fail(SOMA_EWORKSPACE, "workspace is NULL");
+  if (!aligned(workspace, kAlign)) return fail(SOMA_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < L.total)
+    return fail(SOMA_EWORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, L.total);
+  soma_ctx* ctx = new (std::nothrow) soma_ctx;
+  if (!ctx) return fail(SOMA_EINVAL, "out of host memory");
+  ctx->cfg = *cfg;
+  ctx->lay = L;
+  ctx->ws = static_cast<char*>(workspace);
+  ctx->ws_bytes = ws_bytes;
+  ctx->have_coef = false;
+  ctx->timing = false;
+  ctx->have_times = false;
+  ctx->nmarks = 0;
+  ctx->rec_launches = ctx->proj_launches = 0;
+  *out = ctx;
+  return ok();
+}
+
+void soma_destroy(soma_ctx* ctx) {
+  if (!ctx) return;
+  for (hipEvent_t ev : ctx->events) (void)hipEventDestroy(ev);
+  delete ctx;
+}
+
+int soma_set_phase_timing(soma_ctx* ctx, int enable) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  ctx->timing = enable != 0;
+  return ok();
+}
+
+int soma_get_phase_times(soma_ctx* ctx, soma_phase_times* out) {
+  if (!ctx || !out) return fail(SOMA_EINVAL, "NULL argument");
+  if (!ctx->have_times || ctx->nmarks < 2) return fail(SOMA_EINVAL, "no timed step on this context");
+  hipError_t e = hipEventSynchronize(ctx->events[ctx->nmarks - 1]);
+  if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipEventSynchronize: %s", hipGetErrorString(e));
+  float acc[6] = {0, 0, 0, 0, 0, 0};
+  for (size_t i = 1; i < ctx->nmarks; ++i) {
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, ctx->events[i - 1], ctx->events[i]);
+    if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipEventElapsedTime: %s", hipGetErrorString(e));
+    const int p = ctx->phase[i];
+    if (p >= 0 && p < 6) acc[p] += ms;
+  }
+  out->fold_ms = acc[kPhaseFold];
+  out->proj_ms = acc[kPhaseProj];
+  out->rec_ms = acc[kPhaseRec];
+  out->head_ms = acc[kPhaseHead];
+  out->reduce_ms = acc[kPhaseReduce];
+  out->update_ms = acc[kPhaseUpdate];
+  out->rec_launches = ctx->rec_launches;
+  out->proj_launches = ctx->proj_launches;
+  return ok();
+}
+
+int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, float eps,
+                   float lr, const uint8_t* bytes, float* losses, void* stream) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (!theta || !seeds || !bytes || !losses) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
+  if (!aligned(seeds, 8) || !aligned(losses, 4)) return fail(SOMA_EINVAL, "misaligned seeds or losses");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(SOMA_EINVAL, "eps must be finite and > 0");
+  if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
+  const soma_config& c = ctx->cfg;
+  const Layout& L = ctx->lay;
+  const hipStream_t st = as_stream(stream);
+  ctx->nmarks = 0;
+  ctx->rec_launches = ctx->proj_launches = 0;
+  ctx->have_times = false;
+  if (int rc = mark(ctx, kPhaseStart, st)) return rc;
+  for (int j0 = 0; j0 < c.n_pairs; j0 += L.pc) {
+    const int pcs = std::min(L.pc, c.n_pairs - j0);
+    if (int rc = run_forward<true>(ctx, theta, seeds, step, eps, bytes, j0, pcs, st)) return rc;
+    const int n = c.n_experts * pcs * 2;
+    const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
+    hipLaunchKernelGGL(soma::k_loss_reduce, dim3((n + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts,
+                       pcs, L.pc, 2, c.n_pairs, j0, inv_rows, losses,
+                       reinterpret_cast<double*>(ctx->ws + L.lossd));
+    if (int rc = check_launch("k_loss_reduce")) return rc;
+    if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
+  }
+  float* coef = reinterpret_cast<float*>(ctx->ws + L.coef);
+  const int nc = c.n_experts * c.n_pairs;
+  const double inv_denom = 1.0 / (2.0 * double(eps) * double(c.n_pairs));
+  hipLaunchKernelGGL(soma::k_coef, dim3((nc + 255) / 256), dim3(256), 0, st,
+                     reinterpret_cast<const double*>(ctx->ws + L.lossd), c.n_experts, c.n_pairs,
+                     c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, inv_denom, coef);
+  if (int rc = check_launch("k_coef")) return rc;
+  if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
+  const int64_t quads = (L.d + 3) / 4;
+  hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
+                     st, theta, seeds, step, lr, coef, L.d, c.n_pairs);
+  if (int rc = check_launch("k_update")) return rc;
+  if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
+  ctx->have_coef = true;
+  ctx->have_times = ctx->timing;
+  return ok();
+}
+
+int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, float* loss,
+                   void* stream) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (!theta || !bytes || !loss) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
+  const soma_config& c = ctx->cfg;
+  const Layout& L = ctx->lay;
+  const hipStream_t st = as_stream(stream);
+  const bool timing = ctx->timing;
+  ctx->timing = false;  // evaluation is not part of the step's phase record
+  const int rc0 = run_forward<false>(ctx, theta, nullptr, 0, 0.0f, bytes, 0, 1, st);
+  ctx->timing = timing;
+  if (rc0) return rc0;
+  const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
+  hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
+                     reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1,
+                     1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr));
+  if (int rc = check_launch("k_loss_reduce")) return rc;
+  return ok();
+}
+
+int soma_coefficients(soma_ctx* ctx, float* coef, void* stream) {
+  if (!ctx || !coef) return fail(SOMA_EINVAL, "NULL argument");
+  if (!ctx->have_coef) return fail(SOMA_EINVAL, "no step has run on this context");
+  const size_t n = size_t(ctx->cfg.n_experts) * ctx->cfg.n_pairs;
+  const hipError_t e = hipMemcpyAsync(coef, ctx->ws + ctx->lay.coef, n * sizeof(float),
+                                      hipMemcpyDeviceToDevice, as_stream(stream));
+  if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipMemcpyAsync: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int soma_apply_update(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, float lr,
+                      const float* coef, void* stream) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (!theta || !seeds || !coef) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
+  if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
+  const soma_config& c = ctx->cfg;
+  const int64_t quads = (ctx->lay.d + 3) / 4;
+  hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
+                     as_stream(stream), theta, seeds, step, lr, coef, ctx->lay.d, c.n_pairs);
+  if (int rc = check_launch("k_update")) return rc;
+  return ok();
+}
+
+int soma_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+                  float* out, void* stream) {
+  if (!out) return fail(SOMA_EINVAL, "out is NULL");
+  if (count == 0) return ok();
+  if (k0 + count > (uint64_t(1) << 40) || k0 + count < k0)
+    return fail(SOMA_EINVAL, "k0 + count must not exceed 2^40");
+  const uint64_t quads = ((k0 + count + 3) >> 2) - (k0 >> 2);
+  hipLaunchKernelGGL(soma::k_gaussian, dim3(unsigned((quads + 255) / 256)), dim3(256), 0,
+                     as_stream(stream), seed, step, pair, k0, count, out);
+  if (int rc = check_launch("k_gaussian")) return rc;
+  return ok();
+}
+
+int soma_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out, uint64_t n, void* stream) {
+  if (!ctr || !key || !out) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (n == 0) return ok();
+  if (n > (uint64_t(1) << 32)) return fail(SOMA_EINVAL, "n too large");
+  hipLaunchKernelGGL(soma::k_philox, dim3(unsigned((n + 255) / 256)), dim3(256), 0,
+                     as_stream(stream), ctr, key, out, n);
+  if (int rc = check_launch("k_philox")) return rc;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,518 @@
+// soma_kernels.hpp -- gfx950 kernels of the SOMA SPSA step.
+//
+// Data layout in HBM (fp32 unless noted; "slot" = (expert e, direction jl of
+// the current chunk, sign s), slot = (e * PC + jl) * NS + s with NS = 2 signs
+// in a step and 1 in evaluation):
+//   theta [N][d]                 canonical parameter order (see soma.h)
+//   bytes [N][B][T] uint8
+//   U     [slot][256][4H]        layer-1 gate inputs per byte value:
+//                                U[v] = Emb[v] W_1x^T (the embedding row times
+//                                the input half of W_1, re-associated once per
+//                                slot instead of once per token)
+//   gin   [slot][T-1][B][4H]     gate inputs of layers >= 2 (x_t W_lx^T)
+//   hseq  [slot][T-1][B][H]      hidden states of the current layer
+//   cst   [slot][B][H]           cell state of the current layer
+//   part  [slot][row tiles]      per-tile sums of cross entropy (fp64)
+// The last axis of U and gin is gate-interleaved: column 4u + g holds gate g
+// (i, f, g, o) of unit u, so that one MFMA output lane holds the four gates
+// of one unit.
+//
+// Matrix cores: V_MFMA_F32_16X16X4_F32.  For A (16 x 4), B (4 x 16) and
+// D (16 x 16), lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16] and
+// receives D[4 (l / 16) + r][l % 16] in accumulator register r.  Every
+// contraction here is D = W x^T with the perturbed weight W in the A slot
+// (rows = gate rows or vocabulary rows) and activations in the B slot
+// (columns = batch rows).  A lane loads W[m][k .. k+3] and x[n][k .. k+3] as
+// float4 along k and feeds component s to the s-th of four MFMAs, which
+// permutes the order of k inside a 16-wide group identically on both
+// operands.  The four consecutive k of one W row are exactly one Philox
+// counter, so each lane draws its own probe quad in registers: the probe is
+// generated where the weight tile is loaded and never stored.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "soma_rng.hpp"
+
+namespace soma {
+
+constexpr int kVocab = 256;
+constexpr int kThreads = 256;  // 4 waves of 64
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// acc += W(float4 along k) . X(float4 along k) over one 16-wide k group.
+__device__ __forceinline__ f32x4 mfma_k16(const float4& w, const float4& x, f32x4 acc) {
+  acc = mfma4(w.x, x.x, acc);
+  acc = mfma4(w.y, x.y, acc);
+  acc = mfma4(w.z, x.z, acc);
+  acc = mfma4(w.w, x.w, acc);
+  return acc;
+}
+
+__device__ __forceinline__ float4 fma4(float a, const float4& z, const float4& t) {
+  return make_float4(__builtin_fmaf(a, z.x, t.x), __builtin_fmaf(a, z.y, t.y),
+                     __builtin_fmaf(a, z.z, t.z), __builtin_fmaf(a, z.w, t.w));
+}
+
+__device__ __forceinline__ float sigmoid_f(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-x));
+}
+
+__device__ __forceinline__ float tanh_f(float x) {
+  // 1 - 2 / (e^{2x} + 1), saturating correctly for large |x|.
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * x) + 1.0f);
+}
+
+// Shape and workspace pointers shared by the forward kernels.
+struct FwdArgs {
+  const float* theta;     // [N][d]
+  const uint8_t* bytes;   // [N][B][T]
+  const uint64_t* seeds;  // [N]
+  float* U;
+  float* gin;
+  float* hseq;
+  float* cst;
+  double* part;
+  int64_t d;        // parameters per expert
+  int64_t off_l;    // canonical offset of W_l (current layer)
+  int64_t off_head; // canonical offset of Whead
+  uint64_t step;
+  float eps;
+  int N, E, H, B, T, PC;  // PC = slot stride in directions
+  int pcs;                // directions in this pass (grid extent)
+  int j0;                 // first direction of the chunk
+  int layer;              // current layer (0-based)
+  int in_l;               // input width of the current layer
+  int t;                  // time step (rec kernel)
+  int row_tiles;          // head row tiles per slot
+};
+
+// ---------------------------------------------------------------------------
+// Layer-1 gate inputs per byte value (the vocabulary fold).
+//   U[slot][v][4u+g] = sum_{k<E} Emb+-[v][k] W_1+-[g H + u][k]
+// Both operands are perturbed (same direction, same sign).  Grid:
+// (4H/64 gate-row tiles, 4 vocabulary tiles, N * chunk).  Each wave owns 16
+// gate rows; the 64 embedding rows of the tile are perturbed cooperatively
+// into LDS, both signs from one probe quad.
+// ---------------------------------------------------------------------------
+template <bool kPert>
+__global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
+  constexpr int NS = kPert ? 2 : 1;
+  constexpr int KC = 64, LDK = KC + 4;
+  __shared__ float es[NS][64][LDK];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int mtile = blockIdx.x, v0 = blockIdx.y * 64;
+  const int e = blockIdx.z / a.pcs, jl = blockIdx.z % a.pcs;
+  const int E = a.E, H = a.H;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const int prow = mtile * 64 + wave * 16 + lr;
+  const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (E + H);
+
+  f32x4 acc[NS][4];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < E; k0 += KC) {
+    const int kc = min(KC, E - k0);
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 64 * (kc / 4); idx += kThreads) {
+      const int n = idx / (kc / 4), c4 = idx % (kc / 4);
+      const int64_t kk = static_cast<int64_t>(v0 + n) * E + k0 + 4 * c4;
+      const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
+      if (kPert) {
+        const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
+        *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = fma4(a.eps, z, t4);
+        *reinterpret_cast<float4*>(&es[NS - 1][n][4 * c4]) = fma4(-a.eps, z, t4);
+      } else {
+        *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = t4;
+      }
+    }
+    __syncthreads();
+    for (int g = 0; g < kc / 16; ++g) {
+      const int64_t kw = wrow + k0 + 16 * g + 4 * lg;
+      const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
+      float4 w[NS];
+      if (kPert) {
+        const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
+        w[0] = fma4(a.eps, z, t4);
+        w[NS - 1] = fma4(-a.eps, z, t4);
+      } else {
+        w[0] = t4;
+      }
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          const float4 x = *reinterpret_cast<const float4*>(&es[s][nb * 16 + lr][16 * g + 4 * lg]);
+          acc[s][nb] = mfma_k16(w[s], x, acc[s][nb]);
+        }
+    }
+  }
+  const int p = mtile * 64 + wave * 16 + 4 * lg;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * NS + s;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      const int v = v0 + nb * 16 + lr;
+      float* dst = a.U + (slot * kVocab + v) * (4 * static_cast<int64_t>(H)) + p;
+      *reinterpret_cast<float4*>(dst) =
+          make_float4(acc[s][nb][0], acc[s][nb][1], acc[s][nb][2], acc[s][nb][3]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Input projection of layer l >= 2, time-parallel over all B(T-1) rows:
+//   gin[slot][row][4u+g] = sum_{k<H} W_l+-[g H + u][k] h_{l-1}[slot][row][k]
+// Grid: (4H/64 gate-row tiles, ceil(R/128) row tiles, N * chunk).  One probe
+// quad per lane and k group serves both signs and 128 rows per sign.
+// ---------------------------------------------------------------------------
+template <bool kPert>
+__global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
+  constexpr int NS = kPert ? 2 : 1;
+  constexpr int NBP = 8;            // 16-row blocks per sign
+  constexpr int KC = 32, LDK = KC + 4;
+  __shared__ float xs[NS][NBP * 16][LDK];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int mtile = blockIdx.x, r0 = blockIdx.y * NBP * 16;
+  const int e = blockIdx.z / a.pcs, jl = blockIdx.z % a.pcs;
+  const int H = a.H, in = a.in_l;
+  const int64_t R = static_cast<int64_t>(a.T - 1) * a.B;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const int prow = mtile * 64 + wave * 16 + lr;
+  const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H);
+  const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * NS;
+
+  f32x4 acc[NS][NBP];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NBP; ++nb) acc[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < in; k0 += KC) {
+    const int kc = min(KC, in - k0);
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < NS * NBP * 16 * (kc / 4); idx += kThreads) {
+      const int c4 = idx % (kc / 4), n = (idx / (kc / 4)) % (NBP * 16), s = idx / ((kc / 4) * NBP * 16);
+      const int64_t row = r0 + n;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (row < R) v = *reinterpret_cast<const float4*>(a.hseq + ((slot0 + s) * R + row) * H + k0 + 4 * c4);
+      *reinterpret_cast<float4*>(&xs[s][n][4 * c4]) = v;
+    }
+    __syncthreads();
+    for (int g = 0; g < kc / 16; ++g) {
+      const int64_t kw = wrow + k0 + 16 * g + 4 * lg;
+      const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
+      float4 w[NS];
+      if (kPert) {
+        const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
+        w[0] = fma4(a.eps, z, t4);
+        w[NS - 1] = fma4(-a.eps, z, t4);
+      } else {
+        w[0] = t4;
+      }
+#pragma unroll
+      for (int nb = 0; nb < NBP; ++nb)
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          const float4 x = *reinterpret_cast<const float4*>(&xs[s][nb * 16 + lr][16 * g + 4 * lg]);
+          acc[s][nb] = mfma_k16(w[s], x, acc[s][nb]);
+        }
+    }
+  }
+  const int p = mtile * 64 + wave * 16 + 4 * lg;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NBP; ++nb) {
+      const int64_t row = r0 + nb * 16 + lr;
+      if (row < R) {
+        float* dst = a.gin + ((slot0 + s) * R + row) * (4 * static_cast<int64_t>(H)) + p;
+        *reinterpret_cast<float4*>(dst) =
+            make_float4(acc[s][nb][0], acc[s][nb][1], acc[s][nb][2], acc[s][nb][3]);
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// One time step t of the recurrence of one layer, all directions and signs:
+//   a = gin_t + h_{t-1} W_lh+-^T;  i,f,o = sigma, g = tanh;
+//   c_t = f c_{t-1} + i g;  h_t = o tanh(c_t)          (h_{-1} = c_{-1} = 0)
+// Grid: (H/16 unit tiles * batch groups of 16 NB rows, chunk, N).  A block
+// owns 16 units (64 gate rows, 16 per wave) for both signs and NB*16 batch
+// rows; each lane ends with the four gates of one unit for one row and
+// applies the cell update in registers.  The recurrent weights are
+// re-perturbed from their probe counters every step.
+// ---------------------------------------------------------------------------
+template <int NB, bool kPert>
+__global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
+  constexpr int NS = kPert ? 2 : 1;
+  constexpr int KC = 64, LDK = KC + 4;
+  __shared__ float hs[NS][NB * 16][LDK];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T, in = a.in_l, t = a.t;
+  const int ntile = H / 16;
+  const int utile = blockIdx.x % ntile, b0 = (blockIdx.x / ntile) * NB * 16;
+  const int jl = blockIdx.y, e = blockIdx.z;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const int64_t R = static_cast<int64_t>(T - 1) * B;
+  const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * NS;
+
+  f32x4 acc[NS][NB];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (t > 0) {
+    const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
+    const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+    const int prow = utile * 64 + wave * 16 + lr;
+    const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H) + in;
+    for (int k0 = 0; k0 < H; k0 += KC) {
+      const int kc = min(KC, H - k0);
+      __syncthreads();
+      for (int idx = threadIdx.x; idx < NS * NB * 16 * (kc / 4); idx += kThreads) {
+        const int c4 = idx % (kc / 4), n = (idx / (kc / 4)) % (NB * 16), s = idx / ((kc / 4) * NB * 16);
+        const int b = b0 + n;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (b < B)
+          v = *reinterpret_cast<const float4*>(
+              a.hseq + ((slot0 + s) * R + static_cast<int64_t>(t - 1) * B + b) * H + k0 + 4 * c4);
+        *reinterpret_cast<float4*>(&hs[s][n][4 * c4]) = v;
+      }
+      __syncthreads();
+      for (int g = 0; g < kc / 16; ++g) {
+        const int64_t kw = wrow + k0 + 16 * g + 4 * lg;
+        const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
+        float4 w[NS];
+        if (kPert) {
+          const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
+          w[0] = fma4(a.eps, z, t4);
+          w[NS - 1] = fma4(-a.eps, z, t4);
+        } else {
+          w[0] = t4;
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            const float4 x = *reinterpret_cast<const float4*>(&hs[s][nb * 16 + lr][16 * g + 4 * lg]);
+            acc[s][nb] = mfma_k16(w[s], x, acc[s][nb]);
+          }
+      }
+    }
+  }
+
+  const int unit = utile * 16 + wave * 4 + lg;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int b = b0 + nb * 16 + lr;
+      if (b >= B) continue;
+      const int64_t slot = slot0 + s;
+      float4 gi;
+      if (a.layer == 0) {
+        const int v = a.bytes[(static_cast<int64_t>(e) * B + b) * T + t];
+        gi = *reinterpret_cast<const float4*>(a.U + (slot * kVocab + v) * (4 * static_cast<int64_t>(H)) + 4 * unit);
+      } else {
+        gi = *reinterpret_cast<const float4*>(
+            a.gin + (slot * R + static_cast<int64_t>(t) * B + b) * (4 * static_cast<int64_t>(H)) + 4 * unit);
+      }
+      const float ai = acc[s][nb][0] + gi.x, af = acc[s][nb][1] + gi.y;
+      const float ag = acc[s][nb][2] + gi.z, ao = acc[s][nb][3] + gi.w;
+      float* cp = a.cst + (slot * B + b) * static_cast<int64_t>(H) + unit;
+      const float cprev = t > 0 ? *cp : 0.0f;
+      const float c = sigmoid_f(af) * cprev + sigmoid_f(ai) * tanh_f(ag);
+      *cp = c;
+      a.hseq[(slot * R + static_cast<int64_t>(t) * B + b) * H + unit] = sigmoid_f(ao) * tanh_f(c);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Head and fused softmax cross entropy over 256 byte values.
+//   logits[row][v] = sum_k Whead+-[v][k] h[slot][row][k];
+//   ce = log sum_v exp(logits - max) + max - logits[target]
+// Grid: (ceil(R/64) row tiles, N * chunk).  Waves own 64 vocabulary rows
+// each (four 16-row MFMA blocks); row maxima and sums meet across the four
+// lane groups by shuffles and across waves through LDS in a fixed order.
+// part[slot][tile] receives the tile's sum of ce in fp64 (deterministic order).
+// ---------------------------------------------------------------------------
+template <bool kPert>
+__global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
+  constexpr int NS = kPert ? 2 : 1;
+  constexpr int NBH = 4;  // 64 rows per sign
+  constexpr int KC = 32, LDK = KC + 4;
+  __shared__ float xs[NS][NBH * 16][LDK];
+  __shared__ float red[4][NS][NBH * 16];
+  __shared__ float tgt[NS][NBH * 16];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T;
+  const int64_t R = static_cast<int64_t>(T - 1) * B;
+  const int tile = blockIdx.x;
+  const int64_t r0 = static_cast<int64_t>(tile) * NBH * 16;
+  const int e = blockIdx.y / a.pcs, jl = blockIdx.y % a.pcs;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * NS;
+
+  f32x4 acc[4][NS][NBH];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int nb = 0; nb < NBH; ++nb) acc[mb][s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = 0; k0 < H; k0 += KC) {
+    const int kc = min(KC, H - k0);
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < NS * NBH * 16 * (kc / 4); idx += kThreads) {
+      const int c4 = idx % (kc / 4), n = (idx / (kc / 4)) % (NBH * 16), s = idx / ((kc / 4) * NBH * 16);
+      const int64_t row = r0 + n;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (row < R) v = *reinterpret_cast<const float4*>(a.hseq + ((slot0 + s) * R + row) * H + k0 + 4 * c4);
+      *reinterpret_cast<float4*>(&xs[s][n][4 * c4]) = v;
+    }
+    __syncthreads();
+    for (int g = 0; g < kc / 16; ++g) {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const int v = wave * 64 + mb * 16 + lr;
+        const int64_t kw = a.off_head + static_cast<int64_t>(v) * H + k0 + 16 * g + 4 * lg;
+        const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
+        float4 w[NS];
+        if (kPert) {
+          const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
+          w[0] = fma4(a.eps, z, t4);
+          w[NS - 1] = fma4(-a.eps, z, t4);
+        } else {
+          w[0] = t4;
+        }
+#pragma unroll
+        for (int nb = 0; nb < NBH; ++nb)
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            const float4 x = *reinterpret_cast<const float4*>(&xs[s][nb * 16 + lr][16 * g + 4 * lg]);
+            acc[mb][s][nb] = mfma_k16(w[s], x, acc[mb][s][nb]);
+          }
+      }
+    }
+  }
+
+  // Row maxima: lane-local over 16 logits, then across the 4 lane groups.
+  float mx[NS][NBH];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NBH; ++nb) {
+      float m = acc[0][s][nb][0];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) m = fmaxf(m, acc[mb][s][nb][r]);
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      mx[s][nb] = m;
+    }
+  __syncthreads();
+  if (lg == 0) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int nb = 0; nb < NBH; ++nb) red[wave][s][nb * 16 + lr] = mx[s][nb];
+  }
+  // target logits: the lane holding v = target writes it
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NBH; ++nb) {
+      const int64_t row = r0 + nb * 16 + lr;
+      if (row < R) {
+        const int64_t tt = row / B, b = row % B;
+        const int y = a.bytes[(static_cast<int64_t>(e) * B + b) * T + tt + 1];
+        if ((y >> 6) == wave && ((y >> 2) & 3) == lg) {
+          const int ymb = (y >> 4) & 3, yr = y & 3;
+          float v = 0.0f;
+#pragma unroll
+          for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (mb == ymb && r == yr) v = acc[mb][s][nb][r];
+          tgt[s][nb * 16 + lr] = v;
+        }
+      }
+    }
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NBH; ++nb) {
+      const int n = nb * 16 + lr;
+      mx[s][nb] = fmaxf(fmaxf(red[0][s][n], red[1][s][n]), fmaxf(red[2][s][n], red[3][s][n]));
+    }
+  float se[NS][NBH];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NBH; ++nb) {
+      float sum = 0.0f;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sum += __expf(acc[mb][s][nb][r] - mx[s][nb]);
+      sum += __shfl_xor(sum, 16);
+      sum += __shfl_xor(sum, 32);
+      se[s][nb] = sum;
+    }
+  __syncthreads();
+  if (lg == 0) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int nb = 0; nb < NBH; ++nb) red[wave][s][nb * 16 + lr] = se[s][nb];
+  }
+  __syncthreads();
+  // Every lane now holds the row maxima (mx) of its rows; `red` holds the
+  // per-wave sums.  Lane group 0 of wave 0 forms ce for the tile's rows.
+  __shared__ float ces[NS][NBH * 16];
+  if (wave == 0 && lg == 0) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int nb = 0; nb < NBH; ++nb) {
+        const int n = nb * 16 + lr;
+        const int64_t row = r0 + n;
+        float ce = 0.0f;
+        if (row < R) {
+          const float sum = ((red[0][s][n] + red[1][s][n]) + red[2][s][n]) + red[3][s][n];
+          ce = __logf(sum) + mx[s][nb] - tgt[s][n];
+        }
+        ces[s][n] = ce;
+      }
+  }
+  __syncthreads();
+  if (threadIdx.x < NS) {
+    const int s = threadIdx.x;
+    double tot = 0.0;
+    for (int n = 0; n < NBH * 16; ++n) tot += static_cast<double>(ces[s][n]);
+    a.part[(slot0 + s) * a.row_tiles + tile] = tot;
+  }
+}
+
+}  // namespace soma

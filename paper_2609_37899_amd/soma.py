@@ -1,0 +1,211 @@
+"""Thin Python binding of ``libsoma.so`` (include/soma.h): argument marshalling only.
+
+Every step of the SPSA hot path runs in the HIP library.  torch supplies
+device memory and the stream; nothing here computes.  If the library is not
+built (``python -m paper_2609_37899_amd.build``), every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsoma.so")
+
+SOMA_OK, SOMA_EINVAL, SOMA_ESHAPE, SOMA_EDEVICE, SOMA_EWORKSPACE = 0, -1, -2, -3, -4
+LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
+
+EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
+           "soma_spsa_step", "soma_eval_loss", "soma_coefficients", "soma_apply_update",
+           "soma_gaussian", "soma_philox", "soma_set_phase_timing", "soma_get_phase_times",
+           "soma_last_error")
+
+
+class SomaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"soma error {code}: {msg}")
+        self.code = code
+
+
+class PhaseTimes(ctypes.Structure):
+    _fields_ = [("fold_ms", ctypes.c_float), ("proj_ms", ctypes.c_float),
+                ("rec_ms", ctypes.c_float), ("head_ms", ctypes.c_float),
+                ("reduce_ms", ctypes.c_float), ("update_ms", ctypes.c_float),
+                ("rec_launches", ctypes.c_int32), ("proj_launches", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
+        "pair_chunk", "reserved")]
+
+
+_lib = None
+
+
+def load():
+    """Load libsoma.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_37899_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, cp = ctypes.c_void_p, ctypes.POINTER(Config)
+        u64, u32, f32, i64p = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_float, ctypes.POINTER(ctypes.c_int64)
+        sig = {
+            "soma_param_count": (ctypes.c_int, [cp, i64p]),
+            "soma_workspace_size": (ctypes.c_int, [cp, ctypes.POINTER(ctypes.c_size_t)]),
+            "soma_create": (ctypes.c_int, [cp, vp, ctypes.c_size_t, ctypes.POINTER(vp)]),
+            "soma_destroy": (None, [vp]),
+            "soma_spsa_step": (ctypes.c_int, [vp, vp, vp, u64, f32, f32, vp, vp, vp]),
+            "soma_eval_loss": (ctypes.c_int, [vp, vp, vp, vp, vp]),
+            "soma_coefficients": (ctypes.c_int, [vp, vp, vp]),
+            "soma_apply_update": (ctypes.c_int, [vp, vp, vp, u64, f32, vp, vp]),
+            "soma_gaussian": (ctypes.c_int, [u64, u64, u32, u64, u64, vp, vp]),
+            "soma_philox": (ctypes.c_int, [vp, vp, vp, u64, vp]),
+            "soma_set_phase_timing": (ctypes.c_int, [vp, ctypes.c_int]),
+            "soma_get_phase_times": (ctypes.c_int, [vp, ctypes.POINTER(PhaseTimes)]),
+            "soma_last_error": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != SOMA_OK:
+        raise SomaError(rc, load().soma_last_error().decode())
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dptr(t, dtype=None, name="tensor"):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+@dataclass
+class Shape:
+    n_experts: int
+    n_layers: int
+    embed: int
+    hidden: int
+    batch: int
+    seq_len: int
+    n_pairs: int
+    loss_mode: int = LOSS_INDEPENDENT
+    pair_chunk: int = 0
+
+    def cfg(self) -> Config:
+        return Config(self.n_experts, self.n_layers, self.embed, self.hidden, self.batch,
+                      self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, 0)
+
+
+def param_count(shape: Shape) -> int:
+    out = ctypes.c_int64()
+    _check(load().soma_param_count(ctypes.byref(shape.cfg()), ctypes.byref(out)))
+    return out.value
+
+
+def workspace_size(shape: Shape) -> int:
+    out = ctypes.c_size_t()
+    _check(load().soma_workspace_size(ctypes.byref(shape.cfg()), ctypes.byref(out)))
+    return out.value
+
+
+class Context:
+    """A shape bound to a device workspace (a torch uint8 tensor)."""
+
+    def __init__(self, shape: Shape, device="cuda"):
+        import torch
+        self.shape = shape
+        self._cfg = shape.cfg()
+        nbytes = workspace_size(shape)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        h = ctypes.c_void_p()
+        _check(load().soma_create(ctypes.byref(self._cfg), ctypes.c_void_p(self.workspace.data_ptr()),
+                                  nbytes, ctypes.byref(h)))
+        self._h = h
+        self.d = param_count(shape)
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            load().soma_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def spsa_step(self, theta, seeds, step: int, eps: float, lr: float, bytes_, losses,
+                  stream=None):
+        import torch
+        _check(load().soma_spsa_step(self._h, _dptr(theta, torch.float32, "theta"),
+                                     _dptr(seeds, torch.int64, "seeds"), int(step), float(eps),
+                                     float(lr), _dptr(bytes_, torch.uint8, "bytes"),
+                                     _dptr(losses, torch.float32, "losses"), _stream(stream)))
+
+    def set_phase_timing(self, enable: bool = True):
+        _check(load().soma_set_phase_timing(self._h, 1 if enable else 0))
+
+    def phase_times(self) -> dict:
+        out = PhaseTimes()
+        _check(load().soma_get_phase_times(self._h, ctypes.byref(out)))
+        return out.as_dict()
+
+    def eval_loss(self, theta, bytes_, loss, stream=None):
+        import torch
+        _check(load().soma_eval_loss(self._h, _dptr(theta, torch.float32, "theta"),
+                                     _dptr(bytes_, torch.uint8, "bytes"),
+                                     _dptr(loss, torch.float32, "loss"), _stream(stream)))
+
+    def coefficients(self, coef, stream=None):
+        import torch
+        _check(load().soma_coefficients(self._h, _dptr(coef, torch.float32, "coef"), _stream(stream)))
+
+    def apply_update(self, theta, seeds, step: int, lr: float, coef, stream=None):
+        import torch
+        _check(load().soma_apply_update(self._h, _dptr(theta, torch.float32, "theta"),
+                                        _dptr(seeds, torch.int64, "seeds"), int(step), float(lr),
+                                        _dptr(coef, torch.float32, "coef"), _stream(stream)))
+
+
+def gaussian(seed: int, step: int, pair: int, k0: int, out, stream=None):
+    import torch
+    _check(load().soma_gaussian(int(seed) & (2**64 - 1), int(step), int(pair), int(k0), out.numel(),
+                                _dptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def philox(ctr, key, out, stream=None):
+    import torch
+    n = ctr.shape[0]
+    _check(load().soma_philox(_dptr(ctr, torch.int32, "ctr"), _dptr(key, torch.int32, "key"),
+                              _dptr(out, torch.int32, "out"), n, _stream(stream)))
+
+
+def seeds_tensor(seeds, device="cuda"):
+    """uint64 seeds as the int64 device tensor the library reads bit for bit."""
+    import numpy as np
+    import torch
+    a = np.ascontiguousarray(seeds, dtype=np.uint64).view(np.int64)
+    return torch.from_numpy(a.copy()).to(device)

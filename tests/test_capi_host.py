@@ -1,0 +1,99 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/soma.h declares, and rejects bad arguments with the
+documented codes before enqueuing anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_37899_amd import soma, workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "soma.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(soma_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(soma.LIB_PATH):
+        from paper_2609_37899_amd import build
+        build.build()
+    return soma.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(soma.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def shape_of(w, **kw):
+    s = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
+                   w.loss_mode)
+    for k, v in kw.items():
+        setattr(s, k, v)
+    return s
+
+
+def test_param_counts_match_layout(lib):
+    for w in workloads.ALL.values():
+        assert soma.param_count(shape_of(w)) == w.params_per_expert
+
+
+def test_workspace_size_and_auto_chunk(lib):
+    s = shape_of(workloads.SOMA_N2)
+    ws = soma.workspace_size(s)
+    assert 0 < ws < 24 * 2**30
+    s1 = shape_of(workloads.SOMA_N2, pair_chunk=1)
+    assert soma.workspace_size(s1) < ws
+    big = shape_of(workloads.MONOLITH.with_(n_pairs=512))
+    assert soma.workspace_size(big) <= 24 * 2**30
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("embed", 24, soma.SOMA_ESHAPE), ("hidden", 0, soma.SOMA_ESHAPE), ("seq_len", 1, soma.SOMA_ESHAPE),
+    ("n_pairs", 0, soma.SOMA_ESHAPE), ("loss_mode", 2, soma.SOMA_EINVAL),
+    ("pair_chunk", 99, soma.SOMA_ESHAPE), ("reserved", 1, soma.SOMA_EINVAL)])
+def test_invalid_shapes_are_rejected(lib, field, value, code):
+    s = shape_of(workloads.TINY)
+    cfg = s.cfg()
+    setattr(cfg, field, value)
+    out = ctypes.c_size_t()
+    assert lib.soma_workspace_size(ctypes.byref(cfg), ctypes.byref(out)) == code
+    assert lib.soma_last_error()
+
+
+def test_create_checks_workspace(lib):
+    cfg = shape_of(workloads.TINY).cfg()
+    need = soma.workspace_size(shape_of(workloads.TINY))
+    h = ctypes.c_void_p()
+    assert lib.soma_create(ctypes.byref(cfg), None, need, ctypes.byref(h)) == soma.SOMA_EWORKSPACE
+    assert lib.soma_create(ctypes.byref(cfg), ctypes.c_void_p(0x1000 + 8), need, ctypes.byref(h)) == soma.SOMA_EWORKSPACE
+    assert lib.soma_create(ctypes.byref(cfg), ctypes.c_void_p(0x100000), need - 1, ctypes.byref(h)) == soma.SOMA_EWORKSPACE
+
+
+def test_step_rejects_bad_scalars_before_enqueueing(lib):
+    # A context over a fake (never dereferenced) workspace address: every call
+    # below fails validation on the host, so no device work is issued.
+    cfg = shape_of(workloads.TINY).cfg()
+    need = soma.workspace_size(shape_of(workloads.TINY))
+    h = ctypes.c_void_p()
+    assert lib.soma_create(ctypes.byref(cfg), ctypes.c_void_p(0x100000), need, ctypes.byref(h)) == 0
+    p = ctypes.c_void_p(0x200000)
+    try:
+        for eps in (0.0, -1e-3, float("nan"), float("inf")):
+            assert lib.soma_spsa_step(h, p, p, 0, eps, 1e-2, p, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_spsa_step(h, p, p, 0, 1e-3, float("nan"), p, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_spsa_step(h, None, p, 0, 1e-3, 1e-2, p, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_spsa_step(h, ctypes.c_void_p(0x200004), p, 0, 1e-3, 1e-2, p, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_coefficients(h, p, None) == soma.SOMA_EINVAL   # no step ran yet
+        assert lib.soma_gaussian(0, 0, 0, 2**40, 1, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_gaussian(0, 0, 0, 0, 1, None, None) == soma.SOMA_EINVAL
+    finally:
+        lib.soma_destroy(h)
