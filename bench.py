@@ -99,15 +99,17 @@ def main():
     w = workloads.ALL[args.workload]
     if args.pairs:
         w = w.with_(n_pairs=args.pairs)
+    # Inputs are drawn (with a worker pool) before anything touches the GPU.
+    theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
+    nb = max(1, min(args.steps + args.warmup, 3))
+    batches = [synth.expert_batches(w.cluster_seeds, w.batch, w.seq_len, data_seed=i,
+                                    pool=w.pool_clusters, workers=synth.default_workers())
+               for i in range(nb)]
+    seeds_np = synth.expert_seeds(w.n_experts)
     dev = "cuda:0"
     torch.cuda.set_device(0)
     shape = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
                        w.loss_mode, args.pair_chunk)
-    theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
-    nb = max(1, min(args.steps + args.warmup, 3))
-    batches = [synth.expert_batches(w.cluster_seeds, w.batch, w.seq_len, data_seed=i,
-                                    pool=w.pool_clusters) for i in range(nb)]
-    seeds_np = synth.expert_seeds(w.n_experts)
 
     ctx = soma.Context(shape, device=dev)
     theta = torch.from_numpy(theta0.copy()).to(dev)
