@@ -156,6 +156,12 @@ int soma_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint
 int soma_philox(const uint32_t* ctr_dev, const uint32_t* key_dev, uint32_t* out_dev, uint64_t n,
                 void* stream);
 
+/* The Box-Muller transform of the probe stream on n word pairs:
+ * (za[i], zb[i]) from (wa[i], wb[i]) as defined above.  wa_dev, wb_dev [n]
+ * uint32, za_dev, zb_dev [n] fp32, all device arrays. */
+int soma_box_muller(const uint32_t* wa_dev, const uint32_t* wb_dev, float* za_dev, float* zb_dev,
+                    uint64_t n, void* stream);
+
 /* Per-phase device time of the last soma_spsa_step on a context, from HIP
  * events recorded on the step's stream between its kernel launches (off by
  * default; enabling adds one event record per phase boundary).  Times are

@@ -60,6 +60,7 @@ def _load():
                 "oracle_ln_u24_array": (None, [u32p, ctypes.c_int64, f32p]),
                 "oracle_sincos_2pi_u24_array": (None, [u32p, ctypes.c_int64, f32p, f32p]),
                 "oracle_box_muller": (None, [ctypes.c_uint32, ctypes.c_uint32, f32p, f32p]),
+                "oracle_box_muller_array": (None, [u32p, u32p, ctypes.c_int64, f32p, f32p]),
                 "oracle_gaussian": (None, [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
                                            ctypes.c_uint64, ctypes.c_uint64, f32p]),
                 "oracle_forward_loss_f64": (ctypes.c_double, [cfgp, f64p, u8p]),
@@ -153,6 +154,16 @@ def box_muller(wa: int, wb: int):
     a, b = ctypes.c_float(), ctypes.c_float()
     _load().oracle_box_muller(int(wa), int(wb), ctypes.byref(a), ctypes.byref(b))
     return np.float32(a.value), np.float32(b.value)
+
+
+def box_muller_array(wa: np.ndarray, wb: np.ndarray):
+    a = np.ascontiguousarray(wa, dtype=np.uint32)
+    b = np.ascontiguousarray(wb, dtype=np.uint32)
+    za = np.empty(a.size, dtype=np.float32)
+    zb = np.empty(a.size, dtype=np.float32)
+    _load().oracle_box_muller_array(_ptr(a, ctypes.c_uint32), _ptr(b, ctypes.c_uint32), a.size,
+                                    _ptr(za, ctypes.c_float), _ptr(zb, ctypes.c_float))
+    return za, zb
 
 
 def gaussian(seed: int, step: int, pair: int, k0: int, count: int) -> np.ndarray:

@@ -221,6 +221,12 @@ void oracle_sincos_2pi_u24_array(const uint32_t *idx, int64_t n, float *c, float
   for (int64_t i = 0; i < n; ++i) oracle_sincos_2pi_u24(idx[i], &c[i], &s[i]);
 }
 
+void oracle_box_muller_array(const uint32_t *wa, const uint32_t *wb, int64_t n, float *za,
+                             float *zb) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) oracle_box_muller(wa[i], wb[i], &za[i], &zb[i]);
+}
+
 /* The four Gaussians z[4q .. 4q+3] of direction `pair` at SPSA step `step`
  * for an expert whose stream seed is `seed`.
  *   key     = (lo32(seed), hi32(seed) ^ hi32(step))

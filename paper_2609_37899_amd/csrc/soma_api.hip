@@ -165,6 +165,14 @@ __global__ void k_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out
   out[4 * i + 3] = r.w;
 }
 
+__global__ void k_box_muller(const uint32_t* wa, const uint32_t* wb, float* za, float* zb, uint64_t n) {
+  const uint64_t i = blockIdx.x * uint64_t(blockDim.x) + threadIdx.x;
+  if (i >= n) return;
+  const float2 z = box_muller(wa[i], wb[i]);
+  za[i] = z.x;
+  zb[i] = z.y;
+}
+
 // L[e][j0 + jl][s] = (sum over tiles in order) / (B (T-1)), accumulated in
 // fp64; the fp64 mean is kept (lossd) so that the antithetic difference is
 // taken before any rounding to fp32.  One thread per slot.
@@ -527,6 +535,17 @@ int soma_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out, uint64_
   hipLaunchKernelGGL(soma::k_philox, dim3(unsigned((n + 255) / 256)), dim3(256), 0,
                      as_stream(stream), ctr, key, out, n);
   if (int rc = check_launch("k_philox")) return rc;
+  return ok();
+}
+
+int soma_box_muller(const uint32_t* wa, const uint32_t* wb, float* za, float* zb, uint64_t n,
+                    void* stream) {
+  if (!wa || !wb || !za || !zb) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (n == 0) return ok();
+  if (n > (uint64_t(1) << 32)) return fail(SOMA_EINVAL, "n too large");
+  hipLaunchKernelGGL(soma::k_box_muller, dim3(unsigned((n + 255) / 256)), dim3(256), 0,
+                     as_stream(stream), wa, wb, za, zb, n);
+  if (int rc = check_launch("k_box_muller")) return rc;
   return ok();
 }
 

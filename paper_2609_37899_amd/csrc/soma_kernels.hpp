@@ -173,6 +173,96 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Shared main loop of the contractions D = W x^T with a perturbed weight.
+//
+// Each wave owns MB blocks of 16 weight rows (canonical row starts wrow[mb]);
+// a lane regenerates the probe quad of W[m][k .. k+3] for its row m = lane%16
+// and k = 16 g + 4 (lane/16) and forms both signs in registers.  The
+// activations (NS signs x NBR*16 rows x 32 k) are prefetched into registers
+// one chunk ahead and staged through a double-buffered LDS tile (one barrier
+// per chunk).  act(s, n, k) returns the float4 x[s][n][k .. k+3] or zeros.
+// ---------------------------------------------------------------------------
+constexpr int kChunk = 32;            // k per LDS chunk (two 16-wide groups)
+constexpr int kLdk = kChunk + 4;      // padded LDS row: conflict-free b128 reads
+
+template <int NS, int NBR>
+using StageTile = float[2][NS][NBR * 16][kLdk];
+
+template <int NS, int MB, int NBR, bool kPert, class Act>
+__device__ __forceinline__ void perturbed_mainloop(f32x4 (&acc)[MB][NS][NBR], StageTile<NS, NBR>& lds,
+                                                   const float* __restrict__ th,
+                                                   const int64_t (&wrow)[MB], int K, uint2 key,
+                                                   uint32_t pair, uint32_t step_lo, float eps,
+                                                   const Act& act) {
+  constexpr int ROWS = NBR * 16;
+  constexpr int F4 = NS * ROWS * (kChunk / 4);
+  constexpr int PT = (F4 + kThreads - 1) / kThreads;
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int nch = (K + kChunk - 1) / kChunk;
+  float4 pre[PT];
+
+  auto gload = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kThreads;
+      const int c4 = idx & 7, n = (idx >> 3) % ROWS, sg = idx / (8 * ROWS);
+      const int k = c * kChunk + 4 * c4;
+      pre[i] = (idx < F4 && k < K) ? act(sg, n, k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kThreads;
+      if (idx < F4) {
+        const int c4 = idx & 7, n = (idx >> 3) % ROWS, sg = idx / (8 * ROWS);
+        *reinterpret_cast<float4*>(&lds[buf][sg][n][4 * c4]) = pre[i];
+      }
+    }
+  };
+
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) gload(c + 1);
+    const int buf = c & 1;
+#pragma unroll
+    for (int g = 0; g < kChunk / 16; ++g) {
+      const int k = c * kChunk + 16 * g;
+      const bool valid = (g == 0) || (k < K);   // the second group of a tail chunk may be empty
+      const int kk = (valid ? k : c * kChunk) + 4 * lg;
+      float4 w[MB][NS];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const float4 t4 = *reinterpret_cast<const float4*>(th + wrow[mb] + kk);
+        if (kPert) {
+          const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(wrow[mb] + kk) >> 2);
+          w[mb][0] = fma4(eps, z, t4);
+          w[mb][NS - 1] = fma4(-eps, z, t4);
+        } else {
+          w[mb][0] = t4;
+        }
+        if (!valid) {
+#pragma unroll
+          for (int s = 0; s < NS; ++s) w[mb][s] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+#pragma unroll
+      for (int nb = 0; nb < NBR; ++nb)
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          const float4 x = *reinterpret_cast<const float4*>(&lds[buf][s][nb * 16 + lr][16 * g + 4 * lg]);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) acc[mb][s][nb] = mfma_k16(w[mb][s], x, acc[mb][s][nb]);
+        }
+    }
+    if (c + 1 < nch) sstore(buf ^ 1);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Input projection of layer l >= 2, time-parallel over all B(T-1) rows:
 //   gin[slot][row][4u+g] = sum_{k<H} W_l+-[g H + u][k] h_{l-1}[slot][row][k]
 // Grid: (4H/64 gate-row tiles, ceil(R/128) row tiles, N * chunk).  One probe
@@ -181,11 +271,11 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
 template <bool kPert>
 __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
   constexpr int NS = kPert ? 2 : 1;
-  constexpr int NBP = 8;            // 16-row blocks per sign
-  constexpr int KC = 32, LDK = KC + 4;
-  __shared__ float xs[NS][NBP * 16][LDK];
+  constexpr int NBP = 8;  // 16-row blocks per sign
+  __shared__ StageTile<NS, NBP> xs;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
-  const int mtile = blockIdx.x, r0 = blockIdx.y * NBP * 16;
+  const int mtile = blockIdx.x;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * NBP * 16;
   const int e = blockIdx.z / a.pcs, jl = blockIdx.z % a.pcs;
   const int H = a.H, in = a.in_l;
   const int64_t R = static_cast<int64_t>(a.T - 1) * a.B;
@@ -193,46 +283,23 @@ __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
   const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
   const int prow = mtile * 64 + wave * 16 + lr;
-  const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H);
+  const int64_t wrow[1] = {a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H)};
   const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * NS;
+  const float* hin = a.hseq;
 
-  f32x4 acc[NS][NBP];
+  f32x4 acc[1][NS][NBP];
 #pragma unroll
   for (int s = 0; s < NS; ++s)
 #pragma unroll
-    for (int nb = 0; nb < NBP; ++nb) acc[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NBP; ++nb) acc[0][s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = 0; k0 < in; k0 += KC) {
-    const int kc = min(KC, in - k0);
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < NS * NBP * 16 * (kc / 4); idx += kThreads) {
-      const int c4 = idx % (kc / 4), n = (idx / (kc / 4)) % (NBP * 16), s = idx / ((kc / 4) * NBP * 16);
-      const int64_t row = r0 + n;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (row < R) v = *reinterpret_cast<const float4*>(a.hseq + ((slot0 + s) * R + row) * H + k0 + 4 * c4);
-      *reinterpret_cast<float4*>(&xs[s][n][4 * c4]) = v;
-    }
-    __syncthreads();
-    for (int g = 0; g < kc / 16; ++g) {
-      const int64_t kw = wrow + k0 + 16 * g + 4 * lg;
-      const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
-      float4 w[NS];
-      if (kPert) {
-        const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
-        w[0] = fma4(a.eps, z, t4);
-        w[NS - 1] = fma4(-a.eps, z, t4);
-      } else {
-        w[0] = t4;
-      }
-#pragma unroll
-      for (int nb = 0; nb < NBP; ++nb)
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          const float4 x = *reinterpret_cast<const float4*>(&xs[s][nb * 16 + lr][16 * g + 4 * lg]);
-          acc[s][nb] = mfma_k16(w[s], x, acc[s][nb]);
-        }
-    }
-  }
+  auto act = [&](int s, int n, int k) {
+    const int64_t row = r0 + n;
+    return row < R ? *reinterpret_cast<const float4*>(hin + ((slot0 + s) * R + row) * H + k)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  perturbed_mainloop<NS, 1, NBP, kPert>(acc, xs, th, wrow, in, key, pair, step_lo, a.eps, act);
+
   const int p = mtile * 64 + wave * 16 + 4 * lg;
 #pragma unroll
   for (int s = 0; s < NS; ++s)
@@ -242,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
       if (row < R) {
         float* dst = a.gin + ((slot0 + s) * R + row) * (4 * static_cast<int64_t>(H)) + p;
         *reinterpret_cast<float4*>(dst) =
-            make_float4(acc[s][nb][0], acc[s][nb][1], acc[s][nb][2], acc[s][nb][3]);
+            make_float4(acc[0][s][nb][0], acc[0][s][nb][1], acc[0][s][nb][2], acc[0][s][nb][3]);
       }
     }
 }
@@ -260,8 +327,7 @@ __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
 template <int NB, bool kPert>
 __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
   constexpr int NS = kPert ? 2 : 1;
-  constexpr int KC = 64, LDK = KC + 4;
-  __shared__ float hs[NS][NB * 16][LDK];
+  __shared__ StageTile<NS, NB> hs;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T, in = a.in_l, t = a.t;
   const int ntile = H / 16;
@@ -271,50 +337,24 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
   const int64_t R = static_cast<int64_t>(T - 1) * B;
   const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * NS;
 
-  f32x4 acc[NS][NB];
+  f32x4 acc[1][NS][NB];
 #pragma unroll
   for (int s = 0; s < NS; ++s)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb) acc[0][s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   if (t > 0) {
     const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
     const int prow = utile * 64 + wave * 16 + lr;
-    const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H) + in;
-    for (int k0 = 0; k0 < H; k0 += KC) {
-      const int kc = min(KC, H - k0);
-      __syncthreads();
-      for (int idx = threadIdx.x; idx < NS * NB * 16 * (kc / 4); idx += kThreads) {
-        const int c4 = idx % (kc / 4), n = (idx / (kc / 4)) % (NB * 16), s = idx / ((kc / 4) * NB * 16);
-        const int b = b0 + n;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (b < B)
-          v = *reinterpret_cast<const float4*>(
-              a.hseq + ((slot0 + s) * R + static_cast<int64_t>(t - 1) * B + b) * H + k0 + 4 * c4);
-        *reinterpret_cast<float4*>(&hs[s][n][4 * c4]) = v;
-      }
-      __syncthreads();
-      for (int g = 0; g < kc / 16; ++g) {
-        const int64_t kw = wrow + k0 + 16 * g + 4 * lg;
-        const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
-        float4 w[NS];
-        if (kPert) {
-          const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
-          w[0] = fma4(a.eps, z, t4);
-          w[NS - 1] = fma4(-a.eps, z, t4);
-        } else {
-          w[0] = t4;
-        }
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-          for (int s = 0; s < NS; ++s) {
-            const float4 x = *reinterpret_cast<const float4*>(&hs[s][nb * 16 + lr][16 * g + 4 * lg]);
-            acc[s][nb] = mfma_k16(w[s], x, acc[s][nb]);
-          }
-      }
-    }
+    const int64_t wrow[1] = {a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H) + in};
+    const float* hprev = a.hseq + static_cast<int64_t>(t - 1) * B * H;
+    auto act = [&](int s, int n, int k) {
+      const int b = b0 + n;
+      return b < B ? *reinterpret_cast<const float4*>(hprev + ((slot0 + s) * R + b) * H + k)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    perturbed_mainloop<NS, 1, NB, kPert>(acc, hs, th, wrow, H, key, pair, step_lo, a.eps, act);
   }
 
   const int unit = utile * 16 + wave * 4 + lg;
@@ -333,8 +373,8 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
         gi = *reinterpret_cast<const float4*>(
             a.gin + (slot * R + static_cast<int64_t>(t) * B + b) * (4 * static_cast<int64_t>(H)) + 4 * unit);
       }
-      const float ai = acc[s][nb][0] + gi.x, af = acc[s][nb][1] + gi.y;
-      const float ag = acc[s][nb][2] + gi.z, ao = acc[s][nb][3] + gi.w;
+      const float ai = acc[0][s][nb][0] + gi.x, af = acc[0][s][nb][1] + gi.y;
+      const float ag = acc[0][s][nb][2] + gi.z, ao = acc[0][s][nb][3] + gi.w;
       float* cp = a.cst + (slot * B + b) * static_cast<int64_t>(H) + unit;
       const float cprev = t > 0 ? *cp : 0.0f;
       const float c = sigmoid_f(af) * cprev + sigmoid_f(ai) * tanh_f(ag);
@@ -356,10 +396,10 @@ template <bool kPert>
 __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
   constexpr int NS = kPert ? 2 : 1;
   constexpr int NBH = 4;  // 64 rows per sign
-  constexpr int KC = 32, LDK = KC + 4;
-  __shared__ float xs[NS][NBH * 16][LDK];
+  __shared__ StageTile<NS, NBH> xs;
   __shared__ float red[4][NS][NBH * 16];
   __shared__ float tgt[NS][NBH * 16];
+  __shared__ float ces[NS][NBH * 16];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T;
   const int64_t R = static_cast<int64_t>(T - 1) * B;
@@ -379,41 +419,16 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NBH; ++nb) acc[mb][s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = 0; k0 < H; k0 += KC) {
-    const int kc = min(KC, H - k0);
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < NS * NBH * 16 * (kc / 4); idx += kThreads) {
-      const int c4 = idx % (kc / 4), n = (idx / (kc / 4)) % (NBH * 16), s = idx / ((kc / 4) * NBH * 16);
-      const int64_t row = r0 + n;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (row < R) v = *reinterpret_cast<const float4*>(a.hseq + ((slot0 + s) * R + row) * H + k0 + 4 * c4);
-      *reinterpret_cast<float4*>(&xs[s][n][4 * c4]) = v;
-    }
-    __syncthreads();
-    for (int g = 0; g < kc / 16; ++g) {
+  int64_t wrow[4];
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        const int v = wave * 64 + mb * 16 + lr;
-        const int64_t kw = a.off_head + static_cast<int64_t>(v) * H + k0 + 16 * g + 4 * lg;
-        const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
-        float4 w[NS];
-        if (kPert) {
-          const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
-          w[0] = fma4(a.eps, z, t4);
-          w[NS - 1] = fma4(-a.eps, z, t4);
-        } else {
-          w[0] = t4;
-        }
-#pragma unroll
-        for (int nb = 0; nb < NBH; ++nb)
-#pragma unroll
-          for (int s = 0; s < NS; ++s) {
-            const float4 x = *reinterpret_cast<const float4*>(&xs[s][nb * 16 + lr][16 * g + 4 * lg]);
-            acc[mb][s][nb] = mfma_k16(w[s], x, acc[mb][s][nb]);
-          }
-      }
-    }
-  }
+  for (int mb = 0; mb < 4; ++mb) wrow[mb] = a.off_head + static_cast<int64_t>(wave * 64 + mb * 16 + lr) * H;
+  const float* hin = a.hseq;
+  auto act = [&](int s, int n, int k) {
+    const int64_t row = r0 + n;
+    return row < R ? *reinterpret_cast<const float4*>(hin + ((slot0 + s) * R + row) * H + k)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  perturbed_mainloop<NS, 4, NBH, kPert>(acc, xs, th, wrow, H, key, pair, step_lo, a.eps, act);
 
   // Row maxima: lane-local over 16 logits, then across the 4 lane groups.
   float mx[NS][NBH];
@@ -430,7 +445,6 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
       m = fmaxf(m, __shfl_xor(m, 32));
       mx[s][nb] = m;
     }
-  __syncthreads();
   if (lg == 0) {
 #pragma unroll
     for (int s = 0; s < NS; ++s)
@@ -488,9 +502,8 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
       for (int nb = 0; nb < NBH; ++nb) red[wave][s][nb * 16 + lr] = se[s][nb];
   }
   __syncthreads();
-  // Every lane now holds the row maxima (mx) of its rows; `red` holds the
+  // Every lane holds the row maxima (mx) of its rows; `red` holds the
   // per-wave sums.  Lane group 0 of wave 0 forms ce for the tile's rows.
-  __shared__ float ces[NS][NBH * 16];
   if (wave == 0 && lg == 0) {
 #pragma unroll
     for (int s = 0; s < NS; ++s)

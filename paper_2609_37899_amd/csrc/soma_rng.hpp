@@ -32,9 +32,11 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 x, uint2 k) {
   constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t hi0 = __umulhi(kM0, x.x), lo0 = kM0 * x.x;
-    const uint32_t hi1 = __umulhi(kM1, x.z), lo1 = kM1 * x.z;
-    x = make_uint4(hi1 ^ x.y ^ k.x, lo1, hi0 ^ x.w ^ k.y, lo0);
+    // One 32x32->64 product per multiplier (a single v_mad_u64_u32).
+    const uint64_t p0 = static_cast<uint64_t>(kM0) * x.x;
+    const uint64_t p1 = static_cast<uint64_t>(kM1) * x.z;
+    x = make_uint4(static_cast<uint32_t>(p1 >> 32) ^ x.y ^ k.x, static_cast<uint32_t>(p1),
+                   static_cast<uint32_t>(p0 >> 32) ^ x.w ^ k.y, static_cast<uint32_t>(p0));
     k.x += kW0;
     k.y += kW1;
   }
@@ -45,8 +47,11 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 x, uint2 k) {
 // ln f = 2 atanh(s) = 2s (1 + s^2/3 + s^4/5 + ... + s^10/11), s = (f-1)/(f+1);
 // ln 2 = hi + lo with a 16-bit hi so that n * hi is exact.
 __device__ __forceinline__ float ln_u24(uint32_t m) {
-  int e = 31 - __clz(static_cast<int>(m));
-  float f = ldexpf(static_cast<float>(m), -e);
+  // m <= 2^24 converts exactly; its exponent field is floor(log2 m) and its
+  // mantissa field with a zero exponent is f = m 2^-floor(log2 m) in [1, 2).
+  const uint32_t mb = __float_as_uint(static_cast<float>(m));
+  int e = static_cast<int>(mb >> 23) - 127;
+  float f = __uint_as_float((mb & 0x007FFFFFu) | 0x3F800000u);
   if (f > 0x1.6a09e6p+0f) {  // fp32 nearest to sqrt(2)
     f = f * 0.5f;
     e = e + 1;
@@ -95,9 +100,25 @@ __device__ __forceinline__ void sincos_2pi_u24(uint32_t i, float& c_out, float& 
   s_out = (qm >= 2u) ? -sm : sm;
 }
 
+// Correctly rounded sqrt for y = +-0 or a positive normal fp32 number: the
+// hardware estimate s (within 1 ulp) is replaced by its neighbour when the
+// exact residual y - s'^2 of a neighbour s' shows it to be the rounded root.
+// (The general lowering adds a rescale for tiny inputs and a special-value
+// path; y = -2 ln u1 is never tiny, infinite or NaN.)
+__device__ __forceinline__ float sqrt_rn_normal(float y) {
+  const float s = __builtin_amdgcn_sqrtf(y);
+  const float sm = __uint_as_float(__float_as_uint(s) - 1u);
+  const float sp = __uint_as_float(__float_as_uint(s) + 1u);
+  const float rm = __builtin_fmaf(-sm, s, y);
+  const float rp = __builtin_fmaf(-sp, s, y);
+  float r = (rm <= 0.0f) ? sm : s;
+  r = (rp > 0.0f) ? sp : r;
+  return r;
+}
+
 __device__ __forceinline__ float2 box_muller(uint32_t wa, uint32_t wb) {
   const float lnu = ln_u24((wa >> 8) + 1u);
-  const float r = __builtin_sqrtf(-2.0f * lnu);
+  const float r = sqrt_rn_normal(-2.0f * lnu);
   float c, s;
   sincos_2pi_u24(wb >> 8, c, s);
   return make_float2(r * c, r * s);

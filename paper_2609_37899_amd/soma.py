@@ -18,7 +18,8 @@ LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_eval_loss", "soma_coefficients", "soma_apply_update",
-           "soma_gaussian", "soma_philox", "soma_set_phase_timing", "soma_get_phase_times",
+           "soma_gaussian", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
+           "soma_get_phase_times",
            "soma_last_error")
 
 
@@ -68,6 +69,7 @@ def load():
             "soma_apply_update": (ctypes.c_int, [vp, vp, vp, u64, f32, vp, vp]),
             "soma_gaussian": (ctypes.c_int, [u64, u64, u32, u64, u64, vp, vp]),
             "soma_philox": (ctypes.c_int, [vp, vp, vp, u64, vp]),
+            "soma_box_muller": (ctypes.c_int, [vp, vp, vp, vp, u64, vp]),
             "soma_set_phase_timing": (ctypes.c_int, [vp, ctypes.c_int]),
             "soma_get_phase_times": (ctypes.c_int, [vp, ctypes.POINTER(PhaseTimes)]),
             "soma_last_error": (ctypes.c_char_p, []),
@@ -201,6 +203,13 @@ def philox(ctr, key, out, stream=None):
     n = ctr.shape[0]
     _check(load().soma_philox(_dptr(ctr, torch.int32, "ctr"), _dptr(key, torch.int32, "key"),
                               _dptr(out, torch.int32, "out"), n, _stream(stream)))
+
+
+def box_muller(wa, wb, za, zb, stream=None):
+    import torch
+    _check(load().soma_box_muller(_dptr(wa, torch.int32, "wa"), _dptr(wb, torch.int32, "wb"),
+                                  _dptr(za, torch.float32, "za"), _dptr(zb, torch.float32, "zb"),
+                                  wa.numel(), _stream(stream)))
 
 
 def seeds_tensor(seeds, device="cuda"):

@@ -42,3 +42,27 @@ def test_gaussian_bit_exact(oracle_mod, seed, step, pair, k0, count):
     ref = oracle_mod.gaussian(seed, step, pair, k0, count)
     mism = np.flatnonzero(got.view(np.uint32) != ref.view(np.uint32))
     assert mism.size == 0, f"{mism.size} mismatches, first at {mism[:5]}: {got[mism[:5]]} vs {ref[mism[:5]]}"
+
+
+def test_box_muller_exhaustive(oracle_mod):
+    """Every radius input (all 2^24 values of wa >> 8) and every angle input
+    (all 2^24 values of wb >> 8), bit for bit."""
+    torch = require_gpu()
+    from paper_2609_37899_amd import soma
+    n = 1 << 24
+    idx = np.arange(n, dtype=np.uint32)
+    rng = np.random.default_rng(3)
+    for wa, wb in ((idx << 8, np.full(n, 0x12345678, np.uint32)),
+                   (rng.integers(0, 2**32, n, dtype=np.uint64).astype(np.uint32), idx << 8)):
+        wa = wa | rng.integers(0, 256, n, dtype=np.uint32)    # low bits must not matter
+        da = torch.from_numpy(wa.view(np.int32).copy()).cuda()
+        db = torch.from_numpy(wb.view(np.int32).copy()).cuda()
+        za = torch.empty(n, dtype=torch.float32, device="cuda")
+        zb = torch.empty(n, dtype=torch.float32, device="cuda")
+        soma.box_muller(da, db, za, zb)
+        torch.cuda.synchronize()
+        ra, rb = oracle_mod.box_muller_array(wa, wb)
+        ga, gb = za.cpu().numpy(), zb.cpu().numpy()
+        bad = np.flatnonzero((ga.view(np.uint32) != ra.view(np.uint32)) |
+                             (gb.view(np.uint32) != rb.view(np.uint32)))
+        assert bad.size == 0, f"{bad.size} mismatches, e.g. wa={wa[bad[:3]]} wb={wb[bad[:3]]}"
