@@ -152,6 +152,8 @@ def main():
     achieved = per_launch_flops / avg_launch_s / 1e12
     traffic = None
     kname = {"rec": "k_rec_step", "proj": "k_proj", "fold": "k_fold", "head": "k_head_ce"}[dom]
+    if dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
+        kname = "k_rec_persist"   # one persistent launch per layer and direction chunk
     if os.path.exists(args.traffic):
         try:
             tj = json.load(open(args.traffic))

@@ -77,11 +77,18 @@ enum soma_loss_mode {
   SOMA_LOSS_SUMMED = 1       /* c_j from the summed loss, applied to all experts (Appendix J) */
 };
 
+/* Execution flags (soma_config.flags). */
+enum soma_flags {
+  /* Run the recurrence as one launch per time step even where the persistent
+   * kernel applies (the result is the same up to fp32 rounding order). */
+  SOMA_FLAG_PER_STEP_RECURRENCE = 1
+};
+
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;
  * embed and hidden positive multiples of 16; batch >= 1; seq_len >= 2;
  * pair_chunk in [0, n_pairs] (0 picks a chunk that keeps the workspace
  * under 24 GiB; the step processes the P directions in chunks of this many,
- * which changes memory use but not the result). */
+ * which changes memory use but not the result); flags: enum soma_flags. */
 typedef struct soma_config {
   int32_t n_experts;  /* N */
   int32_t n_layers;   /* L */
@@ -92,7 +99,7 @@ typedef struct soma_config {
   int32_t n_pairs;    /* P antithetic directions per expert (2P forwards) */
   int32_t loss_mode;  /* enum soma_loss_mode */
   int32_t pair_chunk; /* directions evaluated per pass; 0 = automatic */
-  int32_t reserved;   /* must be 0 */
+  int32_t flags;      /* enum soma_flags, 0 by default */
 } soma_config;
 
 typedef struct soma_ctx soma_ctx;
@@ -113,6 +120,11 @@ void soma_destroy(soma_ctx* ctx);
 
 /* One SPSA step (Section 4, Eq. main-spsa; Appendix E, Eq. localspsa, with
  * a plain step theta <- theta - lr g_hat in place of Adam).
+ * Where the shape allows (H <= 512, B <= 64, a device that supports
+ * cooperative launches), each layer's recurrence runs as one persistent
+ * launch whose blocks synchronise per time step through bounded waits; if a
+ * wait ever times out, the step's losses are NaN and theta is left
+ * unchanged.
  *   theta_dev  [N][d] fp32, updated in place.  It is written only by the
  *              final update kernel, after every loss of the step exists.
  *   seeds_dev  [N] uint64, the per-expert probe stream seeds.

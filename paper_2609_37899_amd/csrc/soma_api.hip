@@ -44,6 +44,8 @@ int ok() {
 }
 
 constexpr size_t kAlign = 256;
+constexpr int kMaxGroups = 1024;              // persistent-recurrence groups (counters in the workspace)
+constexpr unsigned kSpinLimit = 1u << 20;     // polls (~1 s) before a persistent launch gives up
 constexpr size_t kAutoBudget = size_t(24) << 30;  // automatic pair_chunk keeps the workspace below this
 
 size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -54,7 +56,7 @@ struct Layout {
   int64_t off_head = 0;
   int pc = 0;          // directions per pass
   int row_tiles = 0;   // head tiles per slot
-  size_t coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, total = 0;
+  size_t sync = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, total = 0;
 };
 
 int64_t param_count_of(const soma_config& c) {
@@ -77,7 +79,7 @@ int validate(const soma_config* c) {
     return fail(SOMA_EINVAL, "loss_mode must be 0 (independent) or 1 (summed)");
   if (c->pair_chunk < 0 || c->pair_chunk > c->n_pairs)
     return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs]");
-  if (c->reserved != 0) return fail(SOMA_EINVAL, "reserved must be 0");
+  if (c->flags & ~SOMA_FLAG_PER_STEP_RECURRENCE) return fail(SOMA_EINVAL, "unknown flags");
   const int64_t d = param_count_of(*c);
   if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
   const int64_t rows = int64_t(c->seq_len - 1) * c->batch;
@@ -99,6 +101,7 @@ Layout layout_for(const soma_config& c, int pc) {
   L.row_tiles = int((R + 63) / 64);
   const size_t slots = N * size_t(pc) * 2;
   size_t at = 0;
+  L.sync = at; at += round_up(sizeof(unsigned) * (kMaxGroups + 1));
   L.coef = at; at += round_up(sizeof(float) * N * c.n_pairs);
   L.lossd = at; at += round_up(sizeof(double) * N * c.n_pairs * 2);
   L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
@@ -131,6 +134,8 @@ struct soma_ctx {
   // phase timing
   bool timing;
   bool have_times;
+  // device facts for the persistent recurrence
+  int coop_blocks;                  // co-resident k_rec_persist blocks (0: path unavailable)
   std::vector<hipEvent_t> events;   // pool, grows on demand
   std::vector<int> phase;           // phase closed by events[i]
   size_t nmarks;
@@ -177,13 +182,15 @@ __global__ void k_box_muller(const uint32_t* wa, const uint32_t* wb, float* za, 
 // fp64; the fp64 mean is kept (lossd) so that the antithetic difference is
 // taken before any rounding to fp32.  One thread per slot.
 __global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs, int PC, int NS,
-                              int P, int j0, double inv_rows, float* losses, double* lossd) {
+                              int P, int j0, double inv_rows, float* losses, double* lossd,
+                              const unsigned* err) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= N * pcs * NS) return;
   const int s = i % NS, jl = (i / NS) % pcs, e = i / (NS * pcs);
   const double* p = part + ((int64_t(e) * PC + jl) * NS + s) * row_tiles;
   double tot = 0.0;
   for (int k = 0; k < row_tiles; ++k) tot += p[k];
+  if (err && *err) tot = __builtin_nan("");   // an aborted persistent launch voids the step
   const int64_t o = (int64_t(e) * P + j0 + jl) * NS + s;
   losses[o] = static_cast<float>(tot * inv_rows);
   if (lossd) lossd[o] = tot * inv_rows;
@@ -209,10 +216,12 @@ __global__ void k_coef(const double* lossd, int N, int P, int summed, double inv
 // theta[e][k] -= lr * sum_{j<P} coef[e][j] z_{e,j}[k], one probe quad per
 // thread and direction; the sum runs in j order in fp32.
 __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* seeds, uint64_t step,
-                                                 float lr, const float* coef, int64_t d, int P) {
+                                                 float lr, const float* coef, int64_t d, int P,
+                                                 const unsigned* err) {
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
+  if (err && *err) return;   // the step was aborted: theta stays as it was
   const uint2 key = stream_key(seeds[e], step);
   const uint32_t step_lo = static_cast<uint32_t>(step);
   const float* c = coef + int64_t(e) * P;
@@ -278,6 +287,55 @@ int launch_rec(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
 
 int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 
+// Groups of H/16 blocks that the persistent recurrence can run at once
+// (0 when the shape or the device rules it out).
+int persistent_groups(const soma_ctx* ctx, int jobs) {
+  const soma_config& c = ctx->cfg;
+  if (c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) return 0;
+  if (ctx->coop_blocks <= 0 || c.hidden > 16 * soma::kRecMaxKq || c.hidden % soma::kRecChunk != 0 ||
+      c.batch > 64)
+    return 0;
+  const int ut = c.hidden / 16;
+  int groups = std::min(ctx->coop_blocks / ut, jobs);
+  groups = std::min(groups, kMaxGroups);
+  return groups >= 1 ? groups : 0;
+}
+
+template <int NB, int NCH>
+const void* persist_kernel() {
+  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH>);
+}
+
+template <int NB>
+const void* persist_kernel_for(int nch) {
+  switch (nch) {
+    case 1: return persist_kernel<NB, 1>();
+    case 2: return persist_kernel<NB, 2>();
+    case 3: return persist_kernel<NB, 3>();
+    case 4: return persist_kernel<NB, 4>();
+    case 5: return persist_kernel<NB, 5>();
+    case 6: return persist_kernel<NB, 6>();
+    case 7: return persist_kernel<NB, 7>();
+    case 8: return persist_kernel<NB, 8>();
+    default: return nullptr;
+  }
+}
+
+// The persistent recurrence kernel for batch B and hidden width H (H % 64 == 0, H <= 512).
+const void* persist_kernel_for(int B, int H) {
+  const int nch = H / soma::kRecChunk;
+  if (B <= 16) return persist_kernel_for<1>(nch);
+  if (B <= 32) return persist_kernel_for<2>(nch);
+  return persist_kernel_for<4>(nch);
+}
+
+int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, hipStream_t st) {
+  void* args[] = {const_cast<soma::PersistArgs*>(&p)};
+  const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(soma::kPersistThreads), args, 0, st);
+  if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipLaunchCooperativeKernel: %s", hipGetErrorString(e));
+  return SOMA_OK;
+}
+
 // Forward passes of `pcs` directions starting at j0 (kPert) or of the
 // unperturbed experts (!kPert, pcs = 1), ending with per-tile loss sums.
 template <bool kPert>
@@ -331,14 +389,32 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       if (int rc = mark(ctx, kPhaseProj, st)) return rc;
       ++ctx->proj_launches;
     }
-    const dim3 grid((H / 16) * bgroups, pcs, N);
-    for (int t = 0; t + 1 < c.seq_len; ++t) {
-      a.t = t;
-      launch_rec<kPert>(a, grid, st);
+    const int groups = kPert ? persistent_groups(ctx, N * pcs) : 0;
+    if (groups > 0) {
+      soma::PersistArgs p{};
+      p.a = a;
+      p.bar = reinterpret_cast<unsigned*>(ctx->ws + L.sync);
+      p.err = p.bar + kMaxGroups;
+      p.groups = groups;
+      p.jobs = N * pcs;
+      p.spin_limit = kSpinLimit;
+      // Counters restart at zero for every launch; the abort flag is kept
+      // (zeroed once per step) so that a failure anywhere in the step sticks.
+      hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
+      if (int rc = check_launch("k_zero_u32")) return rc;
+      const int blocks = groups * (H / 16);
+      if (int rc = launch_persist(persist_kernel_for(c.batch, H), p, blocks, st)) return rc;
+      ctx->rec_launches += 1;
+    } else {
+      const dim3 grid((H / 16) * bgroups, pcs, N);
+      for (int t = 0; t + 1 < c.seq_len; ++t) {
+        a.t = t;
+        launch_rec<kPert>(a, grid, st);
+      }
+      if (int rc = check_launch("k_rec_step")) return rc;
+      ctx->rec_launches += c.seq_len - 1;
     }
-    if (int rc = check_launch("k_rec_step")) return rc;
     if (int rc = mark(ctx, kPhaseRec, st)) return rc;
-    ctx->rec_launches += c.seq_len - 1;
   }
   hipLaunchKernelGGL((soma::k_head_ce<kPert>), dim3(L.row_tiles, N * pcs), dim3(soma::kThreads), 0,
                      st, a);
@@ -381,6 +457,25 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
   ctx->ws = static_cast<char*>(workspace);
   ctx->ws_bytes = ws_bytes;
   ctx->have_coef = false;
+  ctx->coop_blocks = 0;
+  {
+    // Co-resident blocks for the persistent recurrence on the current device.
+    int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
+    hipFuncAttributes fa{};
+    const bool shape_ok = cfg->hidden % soma::kRecChunk == 0 && cfg->hidden <= 16 * soma::kRecMaxKq &&
+                          cfg->batch <= 64;
+    const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden) : nullptr;
+    if (kern && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
+        hipFuncGetAttributes(&fa, kern) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, soma::kPersistThreads, 0) == hipSuccess &&
+        coop && size_t(lds_max) >= fa.sharedSizeBytes && per_cu >= 1) {
+      ctx->coop_blocks = cus * per_cu;
+    }
+    (void)hipGetLastError();  // a failed query only disables the persistent path
+  }
   ctx->timing = false;
   ctx->have_times = false;
   ctx->nmarks = 0;
@@ -440,6 +535,9 @@ int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t 
   ctx->rec_launches = ctx->proj_launches = 0;
   ctx->have_times = false;
   if (int rc = mark(ctx, kPhaseStart, st)) return rc;
+  unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
+  hipLaunchKernelGGL(soma::k_zero_u32, dim3(1), dim3(64), 0, st, err, 1);
+  if (int rc = check_launch("k_zero_u32")) return rc;
   for (int j0 = 0; j0 < c.n_pairs; j0 += L.pc) {
     const int pcs = std::min(L.pc, c.n_pairs - j0);
     if (int rc = run_forward<true>(ctx, theta, seeds, step, eps, bytes, j0, pcs, st)) return rc;
@@ -448,7 +546,7 @@ int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t 
     hipLaunchKernelGGL(soma::k_loss_reduce, dim3((n + 255) / 256), dim3(256), 0, st,
                        reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts,
                        pcs, L.pc, 2, c.n_pairs, j0, inv_rows, losses,
-                       reinterpret_cast<double*>(ctx->ws + L.lossd));
+                       reinterpret_cast<double*>(ctx->ws + L.lossd), err);
     if (int rc = check_launch("k_loss_reduce")) return rc;
     if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
   }
@@ -462,7 +560,7 @@ int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t 
   if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
   const int64_t quads = (L.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
-                     st, theta, seeds, step, lr, coef, L.d, c.n_pairs);
+                     st, theta, seeds, step, lr, coef, L.d, c.n_pairs, err);
   if (int rc = check_launch("k_update")) return rc;
   if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
   ctx->have_coef = true;
@@ -486,7 +584,8 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
   const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
   hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
                      reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1,
-                     1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr));
+                     1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr),
+                     static_cast<const unsigned*>(nullptr));
   if (int rc = check_launch("k_loss_reduce")) return rc;
   return ok();
 }
@@ -510,7 +609,8 @@ int soma_apply_update(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
-                     as_stream(stream), theta, seeds, step, lr, coef, ctx->lay.d, c.n_pairs);
+                     as_stream(stream), theta, seeds, step, lr, coef, ctx->lay.d, c.n_pairs,
+                     static_cast<const unsigned*>(nullptr));
   if (int rc = check_launch("k_update")) return rc;
   return ok();
 }

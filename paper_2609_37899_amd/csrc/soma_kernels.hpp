@@ -528,4 +528,251 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent recurrence of one layer (perturbed step only).
+//
+// A block of 8 waves owns 16 units (64 gate rows) of one (expert, direction)
+// for both signs: wave w keeps the perturbed recurrent weights of gate rows
+// [16 (w % 4), +16) for sign w / 4 IN REGISTERS for the whole sequence --
+// the probes are drawn once per (expert, direction) instead of once per
+// time step.  A group
+// of H/16 co-resident blocks carries one (expert, direction) through time:
+// after step t every block publishes its slice of h_t and arrives on the
+// group's counter; before step t+1 it waits for all H/16 arrivals.  Groups
+// take (expert, direction) jobs round-robin; the cell state stays in
+// registers.  One block per CU (two waves per SIMD).
+//
+// h is exchanged with device-coherent (sc1) stores and loads, so no cache
+// writeback or invalidation is needed: a block's stores complete
+// (s_waitcnt vmcnt(0)) before its arrival is counted, and readers load h
+// only after observing every arrival.
+//
+// Every wait is bounded: a block that polls longer than spin_limit sets the
+// sticky abort flag, and every block that sees the flag leaves, so the grid
+// always drains; the update kernel then leaves theta untouched and the
+// losses read NaN.
+// ---------------------------------------------------------------------------
+constexpr int kPersistThreads = 512;   // 8 waves: 4 gate-row blocks x 2 signs
+constexpr int kRecMaxKq = 32;          // H/16 <= 32, i.e. H <= 512
+constexpr int kRecChunk = 64;          // k per staged h chunk
+constexpr int kRecLdk = kRecChunk + 4;
+constexpr int kCoherent = 16;          // cache policy: device scope (sc1)
+constexpr int kZpiece = 256;           // k per cooperatively drawn probe piece
+
+struct PersistArgs {
+  FwdArgs a;
+  unsigned* bar;         // [groups] arrival counters, zero at launch
+  unsigned* err;         // sticky abort flag, zero at the start of the step
+  int groups;            // concurrent groups
+  int jobs;              // N * directions in this pass
+  unsigned spin_limit;   // polls before giving up
+};
+
+__device__ __forceinline__ void wait_stores() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): every memory access of this wave has completed
+}
+
+__device__ __forceinline__ void group_arrive(unsigned* bar) {
+  wait_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Returns true when the block must abort.
+__device__ __forceinline__ bool group_wait(unsigned* bar, unsigned target, unsigned* err,
+                                           unsigned spin_limit, unsigned* flag) {
+  if (threadIdx.x == 0) {
+    unsigned polls = 0, bad = 0;
+    while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) {
+        bad = 1;
+        break;
+      }
+      if (++polls > spin_limit) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        bad = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    *flag = bad;
+  }
+  __syncthreads();
+  return *flag != 0u;
+}
+
+// Buffer resource over [base, base + bytes) (bytes < 2^32); reads past the
+// end return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, static_cast<int>(bytes), 0x00020000);
+}
+
+template <int NB, int NCH>
+__global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
+  constexpr int KQ = 4 * NCH;                           // 16-wide k groups: H = 64 NCH
+  constexpr int ROWS = NB * 16;
+  constexpr int CH4 = 2 * ROWS * (kRecChunk / 4);       // float4 per staged chunk (both signs)
+  constexpr int PT = (CH4 + kPersistThreads - 1) / kPersistThreads;
+  // staging for h chunks, also holding one probe piece at the start of a job
+  constexpr int HS_ROWS = (ROWS * 2 * 2 * kRecLdk >= 64 * (kZpiece + 4))
+                              ? ROWS : (64 * (kZpiece + 4) + 4 * kRecLdk - 1) / (4 * kRecLdk);
+  __shared__ float hs[2][2][HS_ROWS][kRecLdk];
+  __shared__ unsigned abort_flag;
+  const FwdArgs& a = p.a;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int wb = wave & 3, sg = wave >> 2;              // gate-row block and sign of this wave
+  const int H = a.H, B = a.B, T = a.T, in = a.in_l;
+  const int UT = H / 16;
+  const int g = blockIdx.x % p.groups;
+  const int utile = blockIdx.x / p.groups;              // < UT: the grid is groups * UT blocks
+  const int64_t R = static_cast<int64_t>(T - 1) * B;
+  const int64_t H4 = 4 * static_cast<int64_t>(H);
+  const int prow = utile * 64 + wb * 16 + lr;           // A-operand gate row (interleaved order)
+  const int64_t crow = static_cast<int64_t>((prow & 3) * H + (prow >> 2));
+  const int unit = utile * 16 + wb * 4 + lg;            // output unit of this lane
+  const float seps = sg == 0 ? a.eps : -a.eps;
+  const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));
+  unsigned* bar = p.bar + g;
+  unsigned done = 0;                                    // steps this block has published
+
+  for (int job = g; job < p.jobs; job += p.groups) {
+    const int e = job / a.pcs, jl = job % a.pcs;
+    const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+    const uint2 key = stream_key(a.seeds[e], a.step);
+    const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+    const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * 2;
+    const int64_t slot = slot0 + sg;
+    const int64_t wrow = a.off_l + crow * (in + H) + in;
+    const __amdgpu_buffer_rsrc_t hbuf[2] = {buffer_of(a.hseq + slot0 * R * H, slot_bytes),
+                                            buffer_of(a.hseq + (slot0 + 1) * R * H, slot_bytes)};
+
+    // Perturbed recurrent weights of this lane (one sign), drawn once for the
+    // sequence: the block draws the probes of its 64 gate rows cooperatively,
+    // 256 k at a time, into the (idle) staging LDS; each lane then forms its
+    // row's weights from them.
+    float4 w[KQ];
+    float* zs = &hs[0][0][0][0];                       // [64][kZpiece + 4] floats
+#pragma unroll
+    for (int piece = 0; piece < (KQ + 15) / 16; ++piece) {
+      const int kq0 = piece * 16;
+      const int nq = (KQ - kq0 < 16 ? KQ - kq0 : 16);
+      __syncthreads();
+      for (int q = threadIdx.x; q < 64 * nq * 4; q += kPersistThreads) {
+        const int m = q / (nq * 4), k4 = q % (nq * 4);
+        const int pr = utile * 64 + m;
+        const int64_t kk = a.off_l + static_cast<int64_t>((pr & 3) * H + (pr >> 2)) * (in + H) + in +
+                           16 * kq0 + 4 * k4;
+        *reinterpret_cast<float4*>(&zs[m * (kZpiece + 4) + 4 * k4]) =
+            gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int c2 = 0; c2 < 16; ++c2) {
+        const int c = kq0 + c2;
+        if (c < KQ) {
+          const int64_t kk = wrow + 16 * c + 4 * lg;
+          const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
+          const float4 z = *reinterpret_cast<const float4*>(&zs[(wb * 16 + lr) * (kZpiece + 4) + 16 * c2 + 4 * lg]);
+          w[c] = fma4(seps, z, t4);
+        }
+      }
+    }
+    __syncthreads();
+    float cs[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) cs[nb] = 0.0f;
+
+    for (int t = 0; t + 1 < T; ++t) {
+      float4 gi[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int b = nb * 16 + lr;
+        gi[nb] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (b < B) {
+          if (a.layer == 0) {
+            const int v = a.bytes[(static_cast<int64_t>(e) * B + b) * T + t];
+            gi[nb] = *reinterpret_cast<const float4*>(a.U + (slot * kVocab + v) * H4 + 4 * unit);
+          } else {
+            gi[nb] = *reinterpret_cast<const float4*>(
+                a.gin + (slot * R + static_cast<int64_t>(t) * B + b) * H4 + 4 * unit);
+          }
+        }
+      }
+      f32x4 acc[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+      if (t > 0) {
+        if (group_wait(bar, static_cast<unsigned>(UT) * done, p.err, p.spin_limit, &abort_flag)) return;
+        const int row0 = (t - 1) * B;                    // rows of h_{t-1} in each slot
+        float4 pre[PT];
+        auto gload = [&](int cc) {
+#pragma unroll
+          for (int i = 0; i < PT; ++i) {
+            const int idx = threadIdx.x + i * kPersistThreads;
+            const int c4 = idx % (kRecChunk / 4), n = (idx / (kRecChunk / 4)) % ROWS;
+            const int s2 = idx / ((kRecChunk / 4) * ROWS);
+            pre[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (idx < CH4 && n < B) {
+              const uint32_t off = static_cast<uint32_t>(((row0 + n) * H + cc * kRecChunk + 4 * c4) * 4);
+              const f32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hbuf[s2], off, 0, kCoherent);
+              pre[i] = make_float4(v[0], v[1], v[2], v[3]);
+            }
+          }
+        };
+        auto sstore = [&](int buf) {
+#pragma unroll
+          for (int i = 0; i < PT; ++i) {
+            const int idx = threadIdx.x + i * kPersistThreads;
+            if (idx < CH4) {
+              const int c4 = idx % (kRecChunk / 4), n = (idx / (kRecChunk / 4)) % ROWS;
+              const int s2 = idx / ((kRecChunk / 4) * ROWS);
+              *reinterpret_cast<float4*>(&hs[buf][s2][n][4 * c4]) = pre[i];
+            }
+          }
+        };
+        gload(0);
+        sstore(0);
+        __syncthreads();
+#pragma unroll
+        for (int cc = 0; cc < NCH; ++cc) {
+          if (cc + 1 < NCH) gload(cc + 1);
+          const int buf = cc & 1;
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              const float4 x = *reinterpret_cast<const float4*>(&hs[buf][sg][nb * 16 + lr][16 * gq + 4 * lg]);
+              acc[nb] = mfma_k16(w[4 * cc + gq], x, acc[nb]);
+            }
+          }
+          if (cc + 1 < NCH) sstore(buf ^ 1);
+          __syncthreads();
+        }
+      }
+
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int b = nb * 16 + lr;
+        if (b < B) {
+          const float ai = acc[nb][0] + gi[nb].x, af = acc[nb][1] + gi[nb].y;
+          const float ag = acc[nb][2] + gi[nb].z, ao = acc[nb][3] + gi[nb].w;
+          const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
+          cs[nb] = c;
+          __hip_atomic_store(a.hseq + (slot * R + static_cast<int64_t>(t) * B + b) * H + unit,
+                             sigmoid_f(ao) * tanh_f(c), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+      group_arrive(bar);
+      ++done;
+    }
+  }
+}
+
+// Zero n words (barrier counters and the abort flag before a persistent launch).
+__global__ void k_zero_u32(unsigned* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
 }  // namespace soma

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_PKG, "libsoma.so")
 
 SOMA_OK, SOMA_EINVAL, SOMA_ESHAPE, SOMA_EDEVICE, SOMA_EWORKSPACE = 0, -1, -2, -3, -4
 LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
+FLAG_PER_STEP_RECURRENCE = 1
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_eval_loss", "soma_coefficients", "soma_apply_update",
@@ -42,7 +43,7 @@ class PhaseTimes(ctypes.Structure):
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "pair_chunk", "reserved")]
+        "pair_chunk", "flags")]
 
 
 _lib = None
@@ -115,10 +116,11 @@ class Shape:
     n_pairs: int
     loss_mode: int = LOSS_INDEPENDENT
     pair_chunk: int = 0
+    flags: int = 0
 
     def cfg(self) -> Config:
         return Config(self.n_experts, self.n_layers, self.embed, self.hidden, self.batch,
-                      self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, 0)
+                      self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, self.flags)
 
 
 def param_count(shape: Shape) -> int:

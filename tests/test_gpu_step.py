@@ -15,6 +15,8 @@ CASES = {
     "ragged_l2_summed": (2, 2, 48, 32, 20, 37, 3, 1e-3, 1e-2, 1, 2),
     "l3_b70": (3, 3, 16, 80, 70, 9, 2, 2e-3, 5e-3, 0, 0),
     "h512_short": (1, 2, 512, 512, 16, 6, 2, 1e-3, 1e-3, 0, 0),
+    "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
+    "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
 }
 
 
@@ -116,3 +118,32 @@ def test_chunking_does_not_change_the_result():
         outs.append((th.cpu().numpy(), losses.cpu().numpy()))
     for th, ls in outs[1:]:
         assert np.array_equal(th, outs[0][0]) and np.array_equal(ls, outs[0][1])
+
+
+@pytest.mark.parametrize("name", ["tiny", "h512_short", "b64_h128", "b40_h384"])
+def test_persistent_and_per_step_recurrence_agree_bitwise(name):
+    """The persistent recurrence (probe tile resident in LDS, group barriers)
+    and the per-step launches accumulate in the same order: identical bits."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = soma.seeds_tensor(synth.expert_seeds(N))
+    outs = []
+    for flags in (0, soma.FLAG_PER_STEP_RECURRENCE):
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags))
+        ctx.set_phase_timing(True)
+        th = torch.from_numpy(theta.copy()).cuda()
+        losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+        ctx.spsa_step(th, seeds, 2, eps, lr, torch.from_numpy(data).cuda(), losses)
+        launches = ctx.phase_times()["rec_launches"]
+        torch.cuda.synchronize()
+        outs.append((th.cpu().numpy(), losses.cpu().numpy(), launches))
+    (t0, l0, n0), (t1, l1, n1) = outs
+    chunks = (P + (pc or P) - 1) // (pc or P)
+    assert n1 == L * (T - 1) * chunks
+    assert n0 == L * chunks      # one persistent launch per layer and chunk
+    print(f"{name}: recurrence launches persistent={n0} per-step={n1}")
+    assert np.all(np.isfinite(l0))
+    assert np.array_equal(l0, l1)
+    assert np.array_equal(t0, t1)
