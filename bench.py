@@ -41,7 +41,38 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-kernel HBM bytes from rocprofv3 counter runs (JSON), if present")
+    ap.add_argument("--workers", type=int, default=0,
+                    help="processes drawing the synthetic data (0: one per core, up to 16; "
+                         "use 1 under a profiler that initialises the GPU before the program)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device copy of 1 GiB (the reference kernel whose "
+                         "FETCH_SIZE / WRITE_SIZE scale the HBM traffic counters)")
     return ap.parse_args()
+
+
+KERNEL_SOURCES = ("paper_2609_37899_amd/csrc/soma_kernels.hpp", "paper_2609_37899_amd/csrc/soma_rng.hpp")
+
+
+def kernel_source_hash() -> str:
+    """Hash of the kernel sources: stored traffic figures apply only to these."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def calibrate_copy():
+    import torch
+    n = 1 << 28                                   # 2^28 fp32 = 1 GiB per buffer
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read_per_copy": 4 * n,
+                      "bytes_written_per_copy": 4 * n, "copies": 3}), flush=True)
 
 
 def kernel_flops(w):
@@ -85,6 +116,9 @@ def cpu_baseline(w, theta, data, seeds):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; "
                                    f"--gpus {args.gpus} is not supported (experts shard across "
@@ -103,7 +137,8 @@ def main():
     theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
     nb = max(1, min(args.steps + args.warmup, 3))
     batches = [synth.expert_batches(w.cluster_seeds, w.batch, w.seq_len, data_seed=i,
-                                    pool=w.pool_clusters, workers=synth.default_workers())
+                                    pool=w.pool_clusters,
+                                    workers=args.workers or synth.default_workers())
                for i in range(nb)]
     seeds_np = synth.expert_seeds(w.n_experts)
     dev = "cuda:0"
@@ -156,17 +191,16 @@ def main():
         kname = "k_rec_persist"   # one persistent launch per layer and direction chunk
     if os.path.exists(args.traffic):
         try:
-            tj = json.load(open(args.traffic))
-            ent = tj.get(w.name, {}).get(kname)
-            if ent and ent.get("source_hash") == tj.get("current_hash", {}).get(kname):
-                traffic = ent["bytes_per_launch"]
-        except Exception:
+            ent = json.load(open(args.traffic)).get(w.name, {}).get(kname)
+            if ent and ent.get("source_hash") == kernel_source_hash():
+                traffic = ent["hbm_bytes_per_launch"]
+        except (OSError, ValueError, KeyError):
             traffic = None
     roof = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 3),
             "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_FP32_MFMA_TFLOPS, 4), "traffic": traffic,
             "flops_per_launch": per_launch_flops, "avg_launch_ms": round(avg_launch_s * 1e3, 4),
-            "launches_per_step": launches[dom]}
+            "launches_per_step": launches[dom], "kernel_source_hash": kernel_source_hash()}
     total_flops = w.perturbed_tokens * w.flops_per_token
     out = {
         "metric": METRIC,

@@ -292,10 +292,9 @@ int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 int persistent_groups(const soma_ctx* ctx, int jobs) {
   const soma_config& c = ctx->cfg;
   if (c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) return 0;
-  if (ctx->coop_blocks <= 0 || c.hidden > 16 * soma::kRecMaxKq || c.hidden % soma::kRecChunk != 0 ||
-      c.batch > 64)
+  if (ctx->coop_blocks <= 0 || c.hidden > soma::kRecMaxH || c.hidden % 64 != 0 || c.batch > 64)
     return 0;
-  const int ut = c.hidden / 16;
+  const int ut = c.hidden / soma::kRecUnits;
   int groups = std::min(ctx->coop_blocks / ut, jobs);
   groups = std::min(groups, kMaxGroups);
   return groups >= 1 ? groups : 0;
@@ -323,7 +322,7 @@ const void* persist_kernel_for(int nch) {
 
 // The persistent recurrence kernel for batch B and hidden width H (H % 64 == 0, H <= 512).
 const void* persist_kernel_for(int B, int H) {
-  const int nch = H / soma::kRecChunk;
+  const int nch = H / 64;
   if (B <= 16) return persist_kernel_for<1>(nch);
   if (B <= 32) return persist_kernel_for<2>(nch);
   return persist_kernel_for<4>(nch);
@@ -389,20 +388,20 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       if (int rc = mark(ctx, kPhaseProj, st)) return rc;
       ++ctx->proj_launches;
     }
-    const int groups = kPert ? persistent_groups(ctx, N * pcs) : 0;
+    const int groups = kPert ? persistent_groups(ctx, 2 * N * pcs) : 0;
     if (groups > 0) {
       soma::PersistArgs p{};
       p.a = a;
       p.bar = reinterpret_cast<unsigned*>(ctx->ws + L.sync);
       p.err = p.bar + kMaxGroups;
       p.groups = groups;
-      p.jobs = N * pcs;
+      p.jobs = 2 * N * pcs;   // (expert, direction, sign)
       p.spin_limit = kSpinLimit;
       // Counters restart at zero for every launch; the abort flag is kept
       // (zeroed once per step) so that a failure anywhere in the step sticks.
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
       if (int rc = check_launch("k_zero_u32")) return rc;
-      const int blocks = groups * (H / 16);
+      const int blocks = groups * (H / soma::kRecUnits);
       if (int rc = launch_persist(persist_kernel_for(c.batch, H), p, blocks, st)) return rc;
       ctx->rec_launches += 1;
     } else {
@@ -462,8 +461,7 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
     // Co-resident blocks for the persistent recurrence on the current device.
     int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
     hipFuncAttributes fa{};
-    const bool shape_ok = cfg->hidden % soma::kRecChunk == 0 && cfg->hidden <= 16 * soma::kRecMaxKq &&
-                          cfg->batch <= 64;
+    const bool shape_ok = cfg->hidden % 64 == 0 && cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
     const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden) : nullptr;
     if (kern && hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&

@@ -104,7 +104,7 @@ struct FwdArgs {
 template <bool kPert>
 __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
   constexpr int NS = kPert ? 2 : 1;
-  constexpr int KC = 64, LDK = KC + 4;
+  constexpr int KC = 64, LDK = KC + 8;
   __shared__ float es[NS][64][LDK];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int mtile = blockIdx.x, v0 = blockIdx.y * 64;
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
 // per chunk).  act(s, n, k) returns the float4 x[s][n][k .. k+3] or zeros.
 // ---------------------------------------------------------------------------
 constexpr int kChunk = 32;            // k per LDS chunk (two 16-wide groups)
-constexpr int kLdk = kChunk + 4;      // padded LDS row: conflict-free b128 reads
+constexpr int kLdk = kChunk + 8;      // padded LDS row (an odd multiple of 8 floats): conflict-free b128 reads
 
 template <int NS, int NBR>
 using StageTile = float[2][NS][NBR * 16][kLdk];
@@ -531,16 +531,17 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
 // ---------------------------------------------------------------------------
 // Persistent recurrence of one layer (perturbed step only).
 //
-// A block of 8 waves owns 16 units (64 gate rows) of one (expert, direction)
-// for both signs: wave w keeps the perturbed recurrent weights of gate rows
-// [16 (w % 4), +16) for sign w / 4 IN REGISTERS for the whole sequence --
-// the probes are drawn once per (expert, direction) instead of once per
-// time step.  A group
-// of H/16 co-resident blocks carries one (expert, direction) through time:
+// A block of 8 waves owns 32 units (128 gate rows) of one (expert, direction,
+// sign): wave w keeps the perturbed recurrent weights of gate rows
+// [16 w, +16) IN REGISTERS for the whole sequence -- the probes are drawn once
+// per (expert, direction, sign) instead of once per time step.  A group of
+// H/32 co-resident blocks carries one (expert, direction, sign) through time:
 // after step t every block publishes its slice of h_t and arrives on the
-// group's counter; before step t+1 it waits for all H/16 arrivals.  Groups
-// take (expert, direction) jobs round-robin; the cell state stays in
-// registers.  One block per CU (two waves per SIMD).
+// group's counter; before step t+1 it waits for all H/32 arrivals, then
+// stages the whole h_{t-1} of its sign (B x H) in LDS, a quarter of K at a
+// time, overlapping the next quarter's loads with the current quarter's
+// MFMAs.  Groups take jobs round-robin; the cell state stays in registers.
+// One block per CU (two waves per SIMD).
 //
 // h is exchanged with device-coherent (sc1) stores and loads, so no cache
 // writeback or invalidation is needed: a block's stores complete
@@ -552,19 +553,20 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
 // always drains; the update kernel then leaves theta untouched and the
 // losses read NaN.
 // ---------------------------------------------------------------------------
-constexpr int kPersistThreads = 512;   // 8 waves: 4 gate-row blocks x 2 signs
-constexpr int kRecMaxKq = 32;          // H/16 <= 32, i.e. H <= 512
-constexpr int kRecChunk = 64;          // k per staged h chunk
-constexpr int kRecLdk = kRecChunk + 4;
+constexpr int kPersistThreads = 512;   // 8 waves x 16 gate rows
+constexpr int kRecMaxH = 512;          // H <= 512 (h_{t-1} of one sign fits in LDS)
+constexpr int kRecUnits = 32;          // units per block (128 gate rows)
+constexpr int kHsld = kRecMaxH + 8;    // padded LDS row of staged h (odd multiple of 8 floats)
 constexpr int kCoherent = 16;          // cache policy: device scope (sc1)
 constexpr int kZpiece = 256;           // k per cooperatively drawn probe piece
+constexpr int kZld = kZpiece + 8;      // its padded LDS row
 
 struct PersistArgs {
   FwdArgs a;
   unsigned* bar;         // [groups] arrival counters, zero at launch
   unsigned* err;         // sticky abort flag, zero at the start of the step
   int groups;            // concurrent groups
-  int jobs;              // N * directions in this pass
+  int jobs;              // N * directions in this pass * 2 signs
   unsigned spin_limit;   // polls before giving up
 };
 
@@ -610,59 +612,56 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const float* base, u
 template <int NB, int NCH>
 __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
   constexpr int KQ = 4 * NCH;                           // 16-wide k groups: H = 64 NCH
+  constexpr int NQ = NCH >= 4 ? 4 : NCH;                // staging quarters of K
+  constexpr int QG = KQ / NQ;                           // k groups per quarter
   constexpr int ROWS = NB * 16;
-  constexpr int CH4 = 2 * ROWS * (kRecChunk / 4);       // float4 per staged chunk (both signs)
-  constexpr int PT = (CH4 + kPersistThreads - 1) / kPersistThreads;
-  // staging for h chunks, also holding one probe piece at the start of a job
-  constexpr int HS_ROWS = (ROWS * 2 * 2 * kRecLdk >= 64 * (kZpiece + 4))
-                              ? ROWS : (64 * (kZpiece + 4) + 4 * kRecLdk - 1) / (4 * kRecLdk);
-  __shared__ float hs[2][2][HS_ROWS][kRecLdk];
+  constexpr int QF4 = ROWS * QG * 4;                    // float4 per quarter (16 k per group = 4 float4)
+  constexpr int PT = (QF4 + kPersistThreads - 1) / kPersistThreads;
+  constexpr int LDS_FLOATS = (ROWS * kHsld > 128 * kZld) ? ROWS * kHsld : 128 * kZld;
+  __shared__ float hs[LDS_FLOATS];                      // staged h_{t-1} [ROWS][kHsld]; probe piece at job start
   __shared__ unsigned abort_flag;
   const FwdArgs& a = p.a;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
-  const int wb = wave & 3, sg = wave >> 2;              // gate-row block and sign of this wave
   const int H = a.H, B = a.B, T = a.T, in = a.in_l;
-  const int UT = H / 16;
+  const int UT = H / kRecUnits;                         // blocks per group
   const int g = blockIdx.x % p.groups;
   const int utile = blockIdx.x / p.groups;              // < UT: the grid is groups * UT blocks
   const int64_t R = static_cast<int64_t>(T - 1) * B;
   const int64_t H4 = 4 * static_cast<int64_t>(H);
-  const int prow = utile * 64 + wb * 16 + lr;           // A-operand gate row (interleaved order)
+  const int prow = utile * 128 + wave * 16 + lr;        // A-operand gate row (interleaved order)
   const int64_t crow = static_cast<int64_t>((prow & 3) * H + (prow >> 2));
-  const int unit = utile * 16 + wb * 4 + lg;            // output unit of this lane
-  const float seps = sg == 0 ? a.eps : -a.eps;
+  const int unit = utile * kRecUnits + wave * 4 + lg;   // output unit of this lane
   const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));
   unsigned* bar = p.bar + g;
   unsigned done = 0;                                    // steps this block has published
 
   for (int job = g; job < p.jobs; job += p.groups) {
-    const int e = job / a.pcs, jl = job % a.pcs;
+    const int sg = job & 1, pj = job >> 1;
+    const int e = pj / a.pcs, jl = pj % a.pcs;
     const float* th = a.theta + static_cast<int64_t>(e) * a.d;
     const uint2 key = stream_key(a.seeds[e], a.step);
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-    const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * 2;
-    const int64_t slot = slot0 + sg;
+    const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+    const float seps = sg == 0 ? a.eps : -a.eps;
     const int64_t wrow = a.off_l + crow * (in + H) + in;
-    const __amdgpu_buffer_rsrc_t hbuf[2] = {buffer_of(a.hseq + slot0 * R * H, slot_bytes),
-                                            buffer_of(a.hseq + (slot0 + 1) * R * H, slot_bytes)};
+    const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
 
-    // Perturbed recurrent weights of this lane (one sign), drawn once for the
-    // sequence: the block draws the probes of its 64 gate rows cooperatively,
-    // 256 k at a time, into the (idle) staging LDS; each lane then forms its
-    // row's weights from them.
+    // Perturbed recurrent weights of this lane, drawn once for the sequence:
+    // the block draws the probes of its 128 gate rows cooperatively, 256 k at
+    // a time, into the (idle) staging LDS; each lane then forms its row's
+    // weights from them.
     float4 w[KQ];
-    float* zs = &hs[0][0][0][0];                       // [64][kZpiece + 4] floats
 #pragma unroll
     for (int piece = 0; piece < (KQ + 15) / 16; ++piece) {
       const int kq0 = piece * 16;
       const int nq = (KQ - kq0 < 16 ? KQ - kq0 : 16);
       __syncthreads();
-      for (int q = threadIdx.x; q < 64 * nq * 4; q += kPersistThreads) {
+      for (int q = threadIdx.x; q < 128 * nq * 4; q += kPersistThreads) {
         const int m = q / (nq * 4), k4 = q % (nq * 4);
-        const int pr = utile * 64 + m;
+        const int pr = utile * 128 + m;
         const int64_t kk = a.off_l + static_cast<int64_t>((pr & 3) * H + (pr >> 2)) * (in + H) + in +
                            16 * kq0 + 4 * k4;
-        *reinterpret_cast<float4*>(&zs[m * (kZpiece + 4) + 4 * k4]) =
+        *reinterpret_cast<float4*>(&hs[m * kZld + 4 * k4]) =
             gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
       }
       __syncthreads();
@@ -672,7 +671,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         if (c < KQ) {
           const int64_t kk = wrow + 16 * c + 4 * lg;
           const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
-          const float4 z = *reinterpret_cast<const float4*>(&zs[(wb * 16 + lr) * (kZpiece + 4) + 16 * c2 + 4 * lg]);
+          const float4 z = *reinterpret_cast<const float4*>(&hs[(wave * 16 + lr) * kZld + 16 * c2 + 4 * lg]);
           w[c] = fma4(seps, z, t4);
         }
       }
@@ -704,30 +703,28 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 
       if (t > 0) {
         if (group_wait(bar, static_cast<unsigned>(UT) * done, p.err, p.spin_limit, &abort_flag)) return;
-        const int row0 = (t - 1) * B;                    // rows of h_{t-1} in each slot
+        const int row0 = (t - 1) * B;                    // rows of h_{t-1} in the slot
         float4 pre[PT];
-        auto gload = [&](int cc) {
+        auto gload = [&](int qq) {
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
             const int idx = threadIdx.x + i * kPersistThreads;
-            const int c4 = idx % (kRecChunk / 4), n = (idx / (kRecChunk / 4)) % ROWS;
-            const int s2 = idx / ((kRecChunk / 4) * ROWS);
+            const int c4 = idx % (QG * 4), n = idx / (QG * 4);
             pre[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (idx < CH4 && n < B) {
-              const uint32_t off = static_cast<uint32_t>(((row0 + n) * H + cc * kRecChunk + 4 * c4) * 4);
-              const f32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hbuf[s2], off, 0, kCoherent);
+            if (idx < QF4 && n < B) {
+              const uint32_t off = static_cast<uint32_t>(((row0 + n) * H + qq * QG * 16 + 4 * c4) * 4);
+              const f32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hbuf, off, 0, kCoherent);
               pre[i] = make_float4(v[0], v[1], v[2], v[3]);
             }
           }
         };
-        auto sstore = [&](int buf) {
+        auto sstore = [&](int qq) {
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
             const int idx = threadIdx.x + i * kPersistThreads;
-            if (idx < CH4) {
-              const int c4 = idx % (kRecChunk / 4), n = (idx / (kRecChunk / 4)) % ROWS;
-              const int s2 = idx / ((kRecChunk / 4) * ROWS);
-              *reinterpret_cast<float4*>(&hs[buf][s2][n][4 * c4]) = pre[i];
+            if (idx < QF4) {
+              const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+              *reinterpret_cast<float4*>(&hs[n * kHsld + qq * QG * 16 + 4 * c4]) = pre[i];
             }
           }
         };
@@ -735,19 +732,21 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         sstore(0);
         __syncthreads();
 #pragma unroll
-        for (int cc = 0; cc < NCH; ++cc) {
-          if (cc + 1 < NCH) gload(cc + 1);
-          const int buf = cc & 1;
+        for (int qq = 0; qq < NQ; ++qq) {
+          if (qq + 1 < NQ) gload(qq + 1);
 #pragma unroll
-          for (int gq = 0; gq < 4; ++gq) {
+          for (int gq = 0; gq < QG; ++gq) {
+            const int kq = qq * QG + gq;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
-              const float4 x = *reinterpret_cast<const float4*>(&hs[buf][sg][nb * 16 + lr][16 * gq + 4 * lg]);
-              acc[nb] = mfma_k16(w[4 * cc + gq], x, acc[nb]);
+              const float4 x = *reinterpret_cast<const float4*>(&hs[(nb * 16 + lr) * kHsld + 16 * kq + 4 * lg]);
+              acc[nb] = mfma_k16(w[kq], x, acc[nb]);
             }
           }
-          if (cc + 1 < NCH) sstore(buf ^ 1);
-          __syncthreads();
+          if (qq + 1 < NQ) {
+            sstore(qq + 1);
+            __syncthreads();
+          }
         }
       }
 
@@ -763,6 +762,8 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
                              sigmoid_f(ao) * tanh_f(c), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
       }
+      // Every wave is done reading hs (its last quarter) before the group
+      // moves on: group_arrive's barrier orders the next step's staging.
       group_arrive(bar);
       ++done;
     }
