@@ -287,13 +287,17 @@ int launch_rec(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
 
 int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 
-// Groups of H/16 blocks that the persistent recurrence can run at once
-// (0 when the shape or the device rules it out).
+// Groups of H/32 blocks that the persistent recurrence can run at once
+// (0 when the shape or the device rules it out).  The kernel addresses one
+// slot's gate inputs with 32-bit offsets, so B (T-1) 4H floats must stay
+// below 2^31 bytes.
 int persistent_groups(const soma_ctx* ctx, int jobs) {
   const soma_config& c = ctx->cfg;
   if (c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) return 0;
   if (ctx->coop_blocks <= 0 || c.hidden > soma::kRecMaxH || c.hidden % 64 != 0 || c.batch > 64)
     return 0;
+  const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
+  if (gin_slot_bytes >= (int64_t(1) << 31)) return 0;
   const int ut = c.hidden / soma::kRecUnits;
   int groups = std::min(ctx->coop_blocks / ut, jobs);
   groups = std::min(groups, kMaxGroups);

@@ -570,12 +570,12 @@ struct PersistArgs {
   unsigned spin_limit;   // polls before giving up
 };
 
-__device__ __forceinline__ void wait_stores() {
+__device__ __forceinline__ void wait_vmem() {
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): every memory access of this wave has completed
 }
 
 __device__ __forceinline__ void group_arrive(unsigned* bar) {
-  wait_stores();
+  wait_vmem();
   __syncthreads();
   if (threadIdx.x == 0) __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -585,8 +585,12 @@ __device__ __forceinline__ bool group_wait(unsigned* bar, unsigned target, unsig
                                            unsigned spin_limit, unsigned* flag) {
   if (threadIdx.x == 0) {
     unsigned polls = 0, bad = 0;
-    while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) {
+    for (;;) {
+      // Both words are read in one round trip.
+      const unsigned arrived = __hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const unsigned failed = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (arrived >= target) break;
+      if (failed != 0u) {
         bad = 1;
         break;
       }
@@ -603,11 +607,23 @@ __device__ __forceinline__ bool group_wait(unsigned* bar, unsigned target, unsig
   return *flag != 0u;
 }
 
-// Buffer resource over [base, base + bytes) (bytes < 2^32); reads past the
-// end return zeros.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const float* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, static_cast<int>(bytes), 0x00020000);
+// Buffer resource over [base, base + bytes) (bytes < 2^31); reads past the
+// end return zeros and writes past it are dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
 }
+
+// float4 load through a buffer resource (the builtin returns the bits as
+// four 32-bit integers).
+template <int kAux>
+__device__ __forceinline__ float4 buffer_load_f4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kAux);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
+
+// Batch row of lane row b (rows past the batch read the last row).
+__device__ __forceinline__ int brow_of(int b, int B) { return b < B ? b : B - 1; }
 
 template <int NB, int NCH>
 __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
@@ -631,7 +647,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
   const int prow = utile * 128 + wave * 16 + lr;        // A-operand gate row (interleaved order)
   const int64_t crow = static_cast<int64_t>((prow & 3) * H + (prow >> 2));
   const int unit = utile * kRecUnits + wave * 4 + lg;   // output unit of this lane
-  const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));
+  const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));   // < 2^31 (host check)
   unsigned* bar = p.bar + g;
   unsigned done = 0;                                    // steps this block has published
 
@@ -645,6 +661,12 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     const float seps = sg == 0 ? a.eps : -a.eps;
     const int64_t wrow = a.off_l + crow * (in + H) + in;
     const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
+    // Gate inputs of layer 1 (folded, per byte value) or of a later layer.
+    const __amdgpu_buffer_rsrc_t gbuf =
+        a.layer == 0 ? buffer_of(a.U + slot * kVocab * H4, static_cast<uint32_t>(kVocab * H4 * sizeof(float)))
+                     : buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(R * H4 * sizeof(float)));
+    const __amdgpu_buffer_rsrc_t bbuf =
+        buffer_of(a.bytes + static_cast<int64_t>(e) * B * T, static_cast<uint32_t>(B * T));
 
     // Perturbed recurrent weights of this lane, drawn once for the sequence:
     // the block draws the probes of its 128 gate rows cooperatively, 256 k at
@@ -677,31 +699,53 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       }
     }
     __syncthreads();
+    // Rows past the batch compute on the last row's inputs and h (a column
+    // of the product depends only on the same column of h, so no stored
+    // output depends on them) and are never stored.  So the step has no
+    // divergent branches: its loads issue together, and the stores of h, all
+    // at its end, are not waited on before the arrival.  (They do not read
+    // the rows that follow h_{t-1}, which are h_t and still being written:
+    // every h load happens after the wait that publishes its row.)
+    // All addresses of the step loop are 32-bit offsets into the buffers
+    // above (a few VGPRs instead of one 64-bit pointer per row).
     float cs[NB];
+    int vnext[NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) cs[nb] = 0.0f;
+    for (int nb = 0; nb < NB; ++nb) {
+      cs[nb] = 0.0f;
+      vnext[nb] = a.layer == 0
+                      ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, static_cast<uint32_t>(brow_of(nb * 16 + lr, B) * T), 0, 0)
+                      : 0;
+    }
 
     for (int t = 0; t + 1 < T; ++t) {
+      // Gate inputs of step t, loaded while the last quarter of K runs.
+      // Layer 1 reads its folded inputs by byte value; the bytes of step
+      // t + 1 (t + 1 < T) are fetched one step ahead.
       float4 gi[NB];
+      auto load_inputs = [&]() {
+        if (a.layer == 0) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int b = nb * 16 + lr;
-        gi[nb] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (b < B) {
-          if (a.layer == 0) {
-            const int v = a.bytes[(static_cast<int64_t>(e) * B + b) * T + t];
-            gi[nb] = *reinterpret_cast<const float4*>(a.U + (slot * kVocab + v) * H4 + 4 * unit);
-          } else {
-            gi[nb] = *reinterpret_cast<const float4*>(
-                a.gin + (slot * R + static_cast<int64_t>(t) * B + b) * H4 + 4 * unit);
-          }
+          for (int nb = 0; nb < NB; ++nb)
+            gi[nb] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vnext[nb] * 4 * H + 4 * unit) * 4));
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            vnext[nb] = __builtin_amdgcn_raw_buffer_load_b8(
+                bbuf, static_cast<uint32_t>(brow_of(nb * 16 + lr, B) * T + t + 1), 0, 0);
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            gi[nb] = buffer_load_f4<0>(
+                gbuf, static_cast<uint32_t>(((t * B + brow_of(nb * 16 + lr, B)) * 4 * H + 4 * unit) * 4));
         }
-      }
+      };
       f32x4 acc[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-      if (t > 0) {
+      if (t == 0) {
+        load_inputs();
+      } else {
         if (group_wait(bar, static_cast<unsigned>(UT) * done, p.err, p.spin_limit, &abort_flag)) return;
         const int row0 = (t - 1) * B;                    // rows of h_{t-1} in the slot
         float4 pre[PT];
@@ -709,12 +753,10 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
             const int idx = threadIdx.x + i * kPersistThreads;
-            const int c4 = idx % (QG * 4), n = idx / (QG * 4);
-            pre[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (idx < QF4 && n < B) {
+            const int c4 = idx % (QG * 4), n = brow_of(idx / (QG * 4), B);
+            if (idx < QF4) {
               const uint32_t off = static_cast<uint32_t>(((row0 + n) * H + qq * QG * 16 + 4 * c4) * 4);
-              const f32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hbuf, off, 0, kCoherent);
-              pre[i] = make_float4(v[0], v[1], v[2], v[3]);
+              pre[i] = buffer_load_f4<kCoherent>(hbuf, off);
             }
           }
         };
@@ -734,6 +776,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 #pragma unroll
         for (int qq = 0; qq < NQ; ++qq) {
           if (qq + 1 < NQ) gload(qq + 1);
+          if (qq + 1 == NQ) load_inputs();
 #pragma unroll
           for (int gq = 0; gq < QG; ++gq) {
             const int kq = qq * QG + gq;
@@ -750,17 +793,24 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         }
       }
 
+      // The inputs (issued a quarter of K ago) have landed: waiting for them
+      // here keeps the compiler from waiting on the h stores between rows.
+      wait_vmem();
+      float hv[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const float ai = acc[nb][0] + gi[nb].x, af = acc[nb][1] + gi[nb].y;
+        const float ag = acc[nb][2] + gi[nb].z, ao = acc[nb][3] + gi[nb].w;
+        const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
+        cs[nb] = c;
+        hv[nb] = sigmoid_f(ao) * tanh_f(c);
+      }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         const int b = nb * 16 + lr;
-        if (b < B) {
-          const float ai = acc[nb][0] + gi[nb].x, af = acc[nb][1] + gi[nb].y;
-          const float ag = acc[nb][2] + gi[nb].z, ao = acc[nb][3] + gi[nb].w;
-          const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
-          cs[nb] = c;
-          __hip_atomic_store(a.hseq + (slot * R + static_cast<int64_t>(t) * B + b) * H + unit,
-                             sigmoid_f(ao) * tanh_f(c), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+        if (b < B)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(hv[nb]), hbuf,   // the store takes bits
+                                                static_cast<uint32_t>(((t * B + b) * H + unit) * 4), 0, kCoherent);
       }
       // Every wave is done reading hs (its last quarter) before the group
       // moves on: group_arrive's barrier orders the next step's staging.
