@@ -81,7 +81,11 @@ enum soma_loss_mode {
 enum soma_flags {
   /* Run the recurrence as one launch per time step even where the persistent
    * kernel applies (the result is the same up to fp32 rounding order). */
-  SOMA_FLAG_PER_STEP_RECURRENCE = 1
+  SOMA_FLAG_PER_STEP_RECURRENCE = 1,
+  /* Run the input projection of layers 2..L as row tiles that regenerate
+   * their probes per tile, even where the streaming kernel (probes drawn once
+   * per 128 gate rows, weights held in registers) applies; same result. */
+  SOMA_FLAG_TILED_PROJECTION = 2
 };
 
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;

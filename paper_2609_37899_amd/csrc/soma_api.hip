@@ -79,7 +79,8 @@ int validate(const soma_config* c) {
     return fail(SOMA_EINVAL, "loss_mode must be 0 (independent) or 1 (summed)");
   if (c->pair_chunk < 0 || c->pair_chunk > c->n_pairs)
     return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs]");
-  if (c->flags & ~SOMA_FLAG_PER_STEP_RECURRENCE) return fail(SOMA_EINVAL, "unknown flags");
+  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_PROJECTION))
+    return fail(SOMA_EINVAL, "unknown flags");
   const int64_t d = param_count_of(*c);
   if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
   const int64_t rows = int64_t(c->seq_len - 1) * c->batch;
@@ -332,6 +333,30 @@ const void* persist_kernel_for(int B, int H) {
   return persist_kernel_for<4>(nch);
 }
 
+// The streaming input projection applies for H % 64 == 0, H <= 512 and one
+// slot's gate inputs under 2^31 bytes (32-bit offsets), unless the tiled
+// projection is asked for.
+bool stream_projection(const soma_config& c) {
+  if (c.flags & SOMA_FLAG_TILED_PROJECTION) return false;
+  const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
+  return c.hidden % 64 == 0 && c.hidden <= 512 && gin_slot_bytes < (int64_t(1) << 31);
+}
+
+void launch_proj_stream(const soma::FwdArgs& a, int nslots, hipStream_t st) {
+  const int mblocks = a.H / 32;
+  const dim3 grid(unsigned(nslots * mblocks)), block(soma::kProjThreads);
+  switch (a.H / 64) {
+    case 1: hipLaunchKernelGGL(soma::k_proj_stream<1>, grid, block, 0, st, a, mblocks, nslots); break;
+    case 2: hipLaunchKernelGGL(soma::k_proj_stream<2>, grid, block, 0, st, a, mblocks, nslots); break;
+    case 3: hipLaunchKernelGGL(soma::k_proj_stream<3>, grid, block, 0, st, a, mblocks, nslots); break;
+    case 4: hipLaunchKernelGGL(soma::k_proj_stream<4>, grid, block, 0, st, a, mblocks, nslots); break;
+    case 5: hipLaunchKernelGGL(soma::k_proj_stream<5>, grid, block, 0, st, a, mblocks, nslots); break;
+    case 6: hipLaunchKernelGGL(soma::k_proj_stream<6>, grid, block, 0, st, a, mblocks, nslots); break;
+    case 7: hipLaunchKernelGGL(soma::k_proj_stream<7>, grid, block, 0, st, a, mblocks, nslots); break;
+    default: hipLaunchKernelGGL(soma::k_proj_stream<8>, grid, block, 0, st, a, mblocks, nslots); break;
+  }
+}
+
 int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, hipStream_t st) {
   void* args[] = {const_cast<soma::PersistArgs*>(&p)};
   const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(soma::kPersistThreads), args, 0, st);
@@ -385,10 +410,15 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     a.in_l = l == 0 ? c.embed : c.hidden;
     a.off_l = L.off_layer[l];
     if (l > 0) {
-      hipLaunchKernelGGL((soma::k_proj<kPert>),
-                         dim3(4 * H / 64, unsigned((R + 127) / 128), N * pcs),
-                         dim3(soma::kThreads), 0, st, a);
-      if (int rc = check_launch("k_proj")) return rc;
+      if (kPert && stream_projection(c)) {
+        launch_proj_stream(a, 2 * N * pcs, st);
+        if (int rc = check_launch("k_proj_stream")) return rc;
+      } else {
+        hipLaunchKernelGGL((soma::k_proj<kPert>),
+                           dim3(4 * H / 64, unsigned((R + 127) / 128), N * pcs),
+                           dim3(soma::kThreads), 0, st, a);
+        if (int rc = check_launch("k_proj")) return rc;
+      }
       if (int rc = mark(ctx, kPhaseProj, st)) return rc;
       ++ctx->proj_launches;
     }

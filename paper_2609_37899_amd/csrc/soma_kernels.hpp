@@ -625,6 +625,45 @@ __device__ __forceinline__ float4 buffer_load_f4(__amdgpu_buffer_rsrc_t r, uint3
 // Batch row of lane row b (rows past the batch read the last row).
 __device__ __forceinline__ int brow_of(int b, int B) { return b < B ? b : B - 1; }
 
+// Perturbed weights of the block's 128 gate rows r0 .. r0 + 127 (interleaved
+// order, row 4u + g is gate g of unit u) over columns col0 .. col0 + 16 KQ of
+// layer matrix W_l (canonical row g H + u, row length ld), one sign:
+//   w = theta + seps z.
+// Lane (wave, lr, lg) keeps row r0 + 16 wave + lr, columns col0 + 16 c + 4 lg
+// .. + 3 in w[c].  The block draws the probes cooperatively, 256 columns at a
+// time, into the LDS scratch zs (128 x kZld floats); it is free again on return.
+template <int KQ>
+__device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, const float* th, int64_t off_l,
+                                                 int ld, int col0, int H, int r0, uint2 key, uint32_t pair,
+                                                 uint32_t step_lo, float seps) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int prow = r0 + wave * 16 + lr;
+  const int64_t wrow = off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * ld + col0;
+#pragma unroll
+  for (int piece = 0; piece < (KQ + 15) / 16; ++piece) {
+    const int kq0 = piece * 16;
+    const int nq = (KQ - kq0 < 16 ? KQ - kq0 : 16);
+    __syncthreads();
+    for (int q = threadIdx.x; q < 128 * nq * 4; q += blockDim.x) {
+      const int m = q / (nq * 4), k4 = q % (nq * 4);
+      const int pr = r0 + m;
+      const int64_t kk = off_l + static_cast<int64_t>((pr & 3) * H + (pr >> 2)) * ld + col0 + 16 * kq0 + 4 * k4;
+      *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c2 = 0; c2 < 16; ++c2) {
+      const int c = kq0 + c2;
+      if (c < KQ) {
+        const float4 t4 = *reinterpret_cast<const float4*>(th + wrow + 16 * c + 4 * lg);
+        const float4 z = *reinterpret_cast<const float4*>(&zs[(wave * 16 + lr) * kZld + 16 * c2 + 4 * lg]);
+        w[c] = fma4(seps, z, t4);
+      }
+    }
+  }
+  __syncthreads();
+}
+
 template <int NB, int NCH>
 __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
   constexpr int KQ = 4 * NCH;                           // 16-wide k groups: H = 64 NCH
@@ -644,8 +683,6 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
   const int utile = blockIdx.x / p.groups;              // < UT: the grid is groups * UT blocks
   const int64_t R = static_cast<int64_t>(T - 1) * B;
   const int64_t H4 = 4 * static_cast<int64_t>(H);
-  const int prow = utile * 128 + wave * 16 + lr;        // A-operand gate row (interleaved order)
-  const int64_t crow = static_cast<int64_t>((prow & 3) * H + (prow >> 2));
   const int unit = utile * kRecUnits + wave * 4 + lg;   // output unit of this lane
   const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));   // < 2^31 (host check)
   unsigned* bar = p.bar + g;
@@ -659,7 +696,6 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
     const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
     const float seps = sg == 0 ? a.eps : -a.eps;
-    const int64_t wrow = a.off_l + crow * (in + H) + in;
     const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
     // Gate inputs of layer 1 (folded, per byte value) or of a later layer.
     const __amdgpu_buffer_rsrc_t gbuf =
@@ -668,37 +704,9 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     const __amdgpu_buffer_rsrc_t bbuf =
         buffer_of(a.bytes + static_cast<int64_t>(e) * B * T, static_cast<uint32_t>(B * T));
 
-    // Perturbed recurrent weights of this lane, drawn once for the sequence:
-    // the block draws the probes of its 128 gate rows cooperatively, 256 k at
-    // a time, into the (idle) staging LDS; each lane then forms its row's
-    // weights from them.
+    // Perturbed recurrent weights of this lane, drawn once for the sequence.
     float4 w[KQ];
-#pragma unroll
-    for (int piece = 0; piece < (KQ + 15) / 16; ++piece) {
-      const int kq0 = piece * 16;
-      const int nq = (KQ - kq0 < 16 ? KQ - kq0 : 16);
-      __syncthreads();
-      for (int q = threadIdx.x; q < 128 * nq * 4; q += kPersistThreads) {
-        const int m = q / (nq * 4), k4 = q % (nq * 4);
-        const int pr = utile * 128 + m;
-        const int64_t kk = a.off_l + static_cast<int64_t>((pr & 3) * H + (pr >> 2)) * (in + H) + in +
-                           16 * kq0 + 4 * k4;
-        *reinterpret_cast<float4*>(&hs[m * kZld + 4 * k4]) =
-            gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int c2 = 0; c2 < 16; ++c2) {
-        const int c = kq0 + c2;
-        if (c < KQ) {
-          const int64_t kk = wrow + 16 * c + 4 * lg;
-          const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
-          const float4 z = *reinterpret_cast<const float4*>(&hs[(wave * 16 + lr) * kZld + 16 * c2 + 4 * lg]);
-          w[c] = fma4(seps, z, t4);
-        }
-      }
-    }
-    __syncthreads();
+    resident_weights<KQ>(w, hs, th, a.off_l, in + H, in, H, utile * 128, key, pair, step_lo, seps);
     // Rows past the batch compute on the last row's inputs and h (a column
     // of the product depends only on the same column of h, so no stored
     // output depends on them) and are never stored.  So the step has no
@@ -817,6 +825,131 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       group_arrive(bar);
       ++done;
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Input projection of layer l >= 2 with register-resident weights:
+//   gin[slot][row][4u+g] = sum_{k<H} W_l+-[g H + u][k] h_{l-1}[slot][row][k]
+// A block owns one job, the 128 gate rows [128 mb, +128) of one (expert,
+// direction, sign) slot: it forms their perturbed weights in registers once
+// (the probes are drawn once per job instead of once per row tile) and
+// streams all R = B (T-1) rows of the slot's h through a double-buffered LDS
+// ring of 64-row x K/4 chunks, one barrier per chunk; each lane stores the
+// four gates of one unit for its rows after every 64-row tile.
+// Grid: slots * mblocks blocks of 512 threads; where the slot count is a
+// multiple of 8 the 16 row blocks of a slot run on one XCD (blocks are dealt
+// to XCDs round-robin), so they share its L2 while streaming the same h.
+// ---------------------------------------------------------------------------
+constexpr int kProjThreads = 512;
+
+template <int NCH>
+__global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
+  constexpr int KQ = 4 * NCH;                 // 16-wide k groups: K = H = 64 NCH
+  constexpr int NQ = NCH >= 4 ? 4 : NCH;      // chunks per row tile
+  constexpr int QG = KQ / NQ;                 // k groups per chunk (<= 8)
+  constexpr int CW = QG * 16 + 8;             // padded LDS row of a chunk (an odd multiple of 8 floats)
+  constexpr int CF4 = 64 * QG * 4;            // float4 per chunk
+  constexpr int PT = (CF4 + kProjThreads - 1) / kProjThreads;
+  constexpr int LDS_FLOATS = (2 * 64 * CW > 128 * kZld) ? 2 * 64 * CW : 128 * kZld;
+  __shared__ float xs[LDS_FLOATS];            // ring [2][64][CW]; probe scratch while forming weights
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T;
+  const int R = (T - 1) * B;
+  const int H4 = 4 * H;
+
+  int ps, mb;                                 // slot of this pass, row block
+  {
+    const int b = blockIdx.x;
+    if (nslots % 8 == 0) {
+      const int i = b / 8;
+      mb = i % mblocks;
+      ps = (i / mblocks) * 8 + b % 8;
+    } else {
+      ps = b / mblocks;
+      mb = b % mblocks;
+    }
+  }
+  const int sg = ps & 1, pj = ps >> 1;
+  const int e = pj / a.pcs, jl = pj % a.pcs;
+  const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = stream_key(a.seeds[e], a.step);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const float seps = sg == 0 ? a.eps : -a.eps;
+  const int unit = mb * 32 + wave * 4 + lg;   // output unit of this lane
+  // 32-bit offsets: R 4H floats < 2^31 bytes (host check).
+  const __amdgpu_buffer_rsrc_t hbuf =
+      buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(static_cast<int64_t>(R) * H * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t gbuf =
+      buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(static_cast<int64_t>(R) * H4 * sizeof(float)));
+
+  float4 w[KQ];
+  resident_weights<KQ>(w, xs, th, a.off_l, a.in_l + H, 0, H, mb * 128, key, pair, step_lo, seps);
+
+  // Chunk c covers rows [64 (c / NQ), +64) and k [QG 16 (c % NQ), +QG 16);
+  // rows past R read row R - 1 and are never stored.
+  const int nchunks = ((R + 63) / 64) * NQ;
+  float4 pre[PT];
+  auto gload = [&](int c) {
+    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * QG * 16;
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kProjThreads;
+      if (idx < CF4) {
+        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+        const int row = r0 + n < R ? r0 + n : R - 1;
+        pre[i] = buffer_load_f4<0>(hbuf, static_cast<uint32_t>((row * H + k0 + 4 * c4) * 4));
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kProjThreads;
+      if (idx < CF4) {
+        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+        *reinterpret_cast<float4*>(&xs[(buf * 64 + n) * CW + 4 * c4]) = pre[i];
+      }
+    }
+  };
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int c = 0; c < nchunks; ++c) {
+    if (c + 1 < nchunks) gload(c + 1);
+    const int buf = c & 1, qq = c % NQ;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if (q == qq) {                           // compile-time register index into w
+#pragma unroll
+        for (int gq = 0; gq < QG; ++gq)
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) {
+            const float4 x = *reinterpret_cast<const float4*>(&xs[(buf * 64 + nb * 16 + lr) * CW + 16 * gq + 4 * lg]);
+            acc[nb] = mfma_k16(w[q * QG + gq], x, acc[nb]);
+          }
+      }
+    }
+    if (qq == NQ - 1) {
+      const int r0 = (c / NQ) * 64;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int row = r0 + nb * 16 + lr;
+        if (row < R) {
+          typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[nb]), gbuf,
+                                                 static_cast<uint32_t>((row * H4 + 4 * unit) * 4), 0, 0);
+        }
+        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    if (c + 1 < nchunks) sstore(buf ^ 1);
+    __syncthreads();
   }
 }
 

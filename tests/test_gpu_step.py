@@ -147,3 +147,29 @@ def test_persistent_and_per_step_recurrence_agree_bitwise(name):
     assert np.all(np.isfinite(l0))
     assert np.array_equal(l0, l1)
     assert np.array_equal(t0, t1)
+
+
+@pytest.mark.parametrize("name", ["h512_short", "b64_h128", "b40_h384"])
+def test_streaming_and_tiled_projection_agree_bitwise(name):
+    """The streaming input projection (weights resident in registers, probes
+    drawn once per 128 gate rows) and the tiled one (probes regenerated per
+    row tile) sum over k in the same order: identical bits.  The cases cover
+    a ragged last row tile (R = 80, 320) and slot counts that are and are not
+    a multiple of 8 (the two block-to-job mappings)."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = soma.seeds_tensor(synth.expert_seeds(N))
+    outs = []
+    for flags in (0, soma.FLAG_TILED_PROJECTION):
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags))
+        th = torch.from_numpy(theta.copy()).cuda()
+        losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+        ctx.spsa_step(th, seeds, 3, eps, lr, torch.from_numpy(data).cuda(), losses)
+        torch.cuda.synchronize()
+        outs.append((th.cpu().numpy(), losses.cpu().numpy()))
+    (t0, l0), (t1, l1) = outs
+    assert np.all(np.isfinite(l0))
+    assert np.array_equal(l0, l1)
+    assert np.array_equal(t0, t1)
