@@ -560,6 +560,7 @@ constexpr int kHsld = kRecMaxH + 8;    // padded LDS row of staged h (odd multip
 constexpr int kCoherent = 16;          // cache policy: device scope (sc1)
 constexpr int kZpiece = 256;           // k per cooperatively drawn probe piece
 constexpr int kZld = kZpiece + 8;      // its padded LDS row
+constexpr int kHtld = kRecUnits + 4;   // LDS row of the transposed h_t tile (conflict-free word writes)
 
 struct PersistArgs {
   FwdArgs a;
@@ -674,6 +675,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
   constexpr int PT = (QF4 + kPersistThreads - 1) / kPersistThreads;
   constexpr int LDS_FLOATS = (ROWS * kHsld > 128 * kZld) ? ROWS * kHsld : 128 * kZld;
   __shared__ float hs[LDS_FLOATS];                      // staged h_{t-1} [ROWS][kHsld]; probe piece at job start
+  __shared__ float ht[ROWS * kHtld];                    // h_t of the block's units, transposed for stores
   __shared__ unsigned abort_flag;
   const FwdArgs& a = p.a;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
@@ -813,15 +815,24 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         cs[nb] = c;
         hv[nb] = sigmoid_f(ao) * tanh_f(c);
       }
+      // Publish h_t: the block's 32 units of one row are one 128-byte line;
+      // transposed through LDS, each thread stores a float4 and the block
+      // writes whole lines instead of scattered words.
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int b = nb * 16 + lr;
-        if (b < B)
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(hv[nb]), hbuf,   // the store takes bits
-                                                static_cast<uint32_t>(((t * B + b) * H + unit) * 4), 0, kCoherent);
+      for (int nb = 0; nb < NB; ++nb) ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = hv[nb];
+      __syncthreads();
+      if (threadIdx.x < ROWS * 8) {
+        const int n = threadIdx.x >> 3, c4 = threadIdx.x & 7;
+        if (n < B) {
+          typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+          const float4 v = *reinterpret_cast<const float4*>(&ht[n * kHtld + 4 * c4]);
+          __builtin_amdgcn_raw_buffer_store_b128(
+              __builtin_bit_cast(u32x4, v), hbuf,
+              static_cast<uint32_t>(((t * B + n) * H + utile * kRecUnits + 4 * c4) * 4), 0, kCoherent);
+        }
       }
-      // Every wave is done reading hs (its last quarter) before the group
-      // moves on: group_arrive's barrier orders the next step's staging.
+      // Every wave is done reading hs (its last quarter) and ht before the
+      // group moves on: group_arrive's barrier orders the next step's staging.
       group_arrive(bar);
       ++done;
     }
