@@ -752,9 +752,21 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       f32x4 acc[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // Cell update of row tile nb: c_t = f c_{t-1} + i g, h_t = o tanh(c_t),
+      // written to the transposed tile that is published below.
+      auto cell = [&](int nb) {
+        const float ai = acc[nb][0] + gi[nb].x, af = acc[nb][1] + gi[nb].y;
+        const float ag = acc[nb][2] + gi[nb].z, ao = acc[nb][3] + gi[nb].w;
+        const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
+        cs[nb] = c;
+        ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = sigmoid_f(ao) * tanh_f(c);
+      };
 
       if (t == 0) {
         load_inputs();
+        wait_vmem();
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) cell(nb);
       } else {
         if (group_wait(bar, static_cast<unsigned>(UT) * done, p.err, p.spin_limit, &abort_flag)) return;
         const int row0 = (t - 1) * B;                    // rows of h_{t-1} in the slot
@@ -780,46 +792,45 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
             }
           }
         };
+        auto mfma_tile = [&](int nb, int kq) {
+          const float4 x = *reinterpret_cast<const float4*>(&hs[(nb * 16 + lr) * kHsld + 16 * kq + 4 * lg]);
+          acc[nb] = mfma_k16(w[kq], x, acc[nb]);
+        };
         gload(0);
         sstore(0);
         __syncthreads();
 #pragma unroll
         for (int qq = 0; qq < NQ; ++qq) {
-          if (qq + 1 < NQ) gload(qq + 1);
-          if (qq + 1 == NQ) load_inputs();
-#pragma unroll
-          for (int gq = 0; gq < QG; ++gq) {
-            const int kq = qq * QG + gq;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-              const float4 x = *reinterpret_cast<const float4*>(&hs[(nb * 16 + lr) * kHsld + 16 * kq + 4 * lg]);
-              acc[nb] = mfma_k16(w[kq], x, acc[nb]);
-            }
-          }
           if (qq + 1 < NQ) {
+            gload(qq + 1);
+#pragma unroll
+            for (int gq = 0; gq < QG; ++gq)
+#pragma unroll
+              for (int nb = 0; nb < NB; ++nb) mfma_tile(nb, qq * QG + gq);
             sstore(qq + 1);
             __syncthreads();
+          } else {
+            // Last quarter, row tile by row tile: the cell update of a tile
+            // overlaps the MFMAs of the next (same k order per tile).  The
+            // inputs, issued here, have landed by the first update.
+            load_inputs();
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+              for (int gq = 0; gq < QG; ++gq) mfma_tile(nb, qq * QG + gq);
+              if (nb == 1) wait_vmem();
+              if (nb >= 1) cell(nb - 1);
+            }
+            if (NB == 1) wait_vmem();
+            cell(NB - 1);
           }
         }
       }
 
-      // The inputs (issued a quarter of K ago) have landed: waiting for them
-      // here keeps the compiler from waiting on the h stores between rows.
-      wait_vmem();
-      float hv[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const float ai = acc[nb][0] + gi[nb].x, af = acc[nb][1] + gi[nb].y;
-        const float ag = acc[nb][2] + gi[nb].z, ao = acc[nb][3] + gi[nb].w;
-        const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
-        cs[nb] = c;
-        hv[nb] = sigmoid_f(ao) * tanh_f(c);
-      }
       // Publish h_t: the block's 32 units of one row are one 128-byte line;
-      // transposed through LDS, each thread stores a float4 and the block
-      // writes whole lines instead of scattered words.
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = hv[nb];
+      // transposed through LDS (cell() wrote this lane's words), each thread
+      // stores a float4 and the block writes whole lines instead of
+      // scattered words.
       __syncthreads();
       if (threadIdx.x < ROWS * 8) {
         const int n = threadIdx.x >> 3, c4 = threadIdx.x & 7;
