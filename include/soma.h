@@ -82,10 +82,12 @@ enum soma_flags {
   /* Run the recurrence as one launch per time step even where the persistent
    * kernel applies (the result is the same up to fp32 rounding order). */
   SOMA_FLAG_PER_STEP_RECURRENCE = 1,
-  /* Run the input projection of layers 2..L as row tiles that regenerate
-   * their probes per tile, even where the streaming kernel (probes drawn once
-   * per 128 gate rows, weights held in registers) applies; same result. */
-  SOMA_FLAG_TILED_PROJECTION = 2
+  /* Run the input projections of layers 2..L and the output head as row
+   * tiles that regenerate their probes per tile, even where the streaming
+   * kernels (probes drawn once per 128 weight rows, weights held in
+   * registers) apply.  The projections agree bit for bit; the head's cross
+   * entropy agrees up to fp32 rounding order. */
+  SOMA_FLAG_TILED_WEIGHTS = 2
 };
 
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;

@@ -56,7 +56,7 @@ struct Layout {
   int64_t off_head = 0;
   int pc = 0;          // directions per pass
   int row_tiles = 0;   // head tiles per slot
-  size_t sync = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, total = 0;
+  size_t sync = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, hpart = 0, htgt = 0, total = 0;
 };
 
 int64_t param_count_of(const soma_config& c) {
@@ -79,7 +79,7 @@ int validate(const soma_config* c) {
     return fail(SOMA_EINVAL, "loss_mode must be 0 (independent) or 1 (summed)");
   if (c->pair_chunk < 0 || c->pair_chunk > c->n_pairs)
     return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs]");
-  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_PROJECTION))
+  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS))
     return fail(SOMA_EINVAL, "unknown flags");
   const int64_t d = param_count_of(*c);
   if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
@@ -109,6 +109,8 @@ Layout layout_for(const soma_config& c, int pc) {
   L.U = at;    at += round_up(sizeof(float) * slots * SOMA_VOCAB * 4 * H);
   L.hseq = at; at += round_up(sizeof(float) * slots * R * H);
   L.cst = at;  at += round_up(sizeof(float) * slots * B * H);
+  L.hpart = at; at += round_up(sizeof(float) * 2 * slots * 2 * R);   // (m, s) per vocabulary half
+  L.htgt = at; at += round_up(sizeof(float) * slots * R);
   L.gin = at;
   if (c.n_layers > 1) at += round_up(sizeof(float) * slots * R * 4 * H);
   L.total = at;
@@ -333,13 +335,27 @@ const void* persist_kernel_for(int B, int H) {
   return persist_kernel_for<4>(nch);
 }
 
-// The streaming input projection applies for H % 64 == 0, H <= 512 and one
-// slot's gate inputs under 2^31 bytes (32-bit offsets), unless the tiled
-// projection is asked for.
-bool stream_projection(const soma_config& c) {
-  if (c.flags & SOMA_FLAG_TILED_PROJECTION) return false;
+// The streaming input projection and head apply for H % 64 == 0, H <= 512
+// and one slot's gate inputs under 2^31 bytes (32-bit offsets), unless the
+// tiled kernels are asked for.
+bool stream_weights(const soma_config& c) {
+  if (c.flags & SOMA_FLAG_TILED_WEIGHTS) return false;
   const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
   return c.hidden % 64 == 0 && c.hidden <= 512 && gin_slot_bytes < (int64_t(1) << 31);
+}
+
+void launch_head_stream(const soma::FwdArgs& a, int nslots, float2* hpart, float* htgt, hipStream_t st) {
+  const dim3 grid(unsigned(nslots * 2)), block(soma::kProjThreads);
+  switch (a.H / 64) {
+    case 1: hipLaunchKernelGGL(soma::k_head_stream<1>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 2: hipLaunchKernelGGL(soma::k_head_stream<2>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 3: hipLaunchKernelGGL(soma::k_head_stream<3>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 4: hipLaunchKernelGGL(soma::k_head_stream<4>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 5: hipLaunchKernelGGL(soma::k_head_stream<5>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 6: hipLaunchKernelGGL(soma::k_head_stream<6>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 7: hipLaunchKernelGGL(soma::k_head_stream<7>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    default: hipLaunchKernelGGL(soma::k_head_stream<8>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+  }
 }
 
 void launch_proj_stream(const soma::FwdArgs& a, int nslots, hipStream_t st) {
@@ -410,7 +426,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     a.in_l = l == 0 ? c.embed : c.hidden;
     a.off_l = L.off_layer[l];
     if (l > 0) {
-      if (kPert && stream_projection(c)) {
+      if (kPert && stream_weights(c)) {
         launch_proj_stream(a, 2 * N * pcs, st);
         if (int rc = check_launch("k_proj_stream")) return rc;
       } else {
@@ -449,9 +465,18 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     }
     if (int rc = mark(ctx, kPhaseRec, st)) return rc;
   }
-  hipLaunchKernelGGL((soma::k_head_ce<kPert>), dim3(L.row_tiles, N * pcs), dim3(soma::kThreads), 0,
-                     st, a);
-  if (int rc = check_launch("k_head_ce")) return rc;
+  if (kPert && stream_weights(c)) {
+    float2* hpart = reinterpret_cast<float2*>(ctx->ws + L.hpart);
+    float* htgt = reinterpret_cast<float*>(ctx->ws + L.htgt);
+    launch_head_stream(a, 2 * N * pcs, hpart, htgt, st);
+    if (int rc = check_launch("k_head_stream")) return rc;
+    hipLaunchKernelGGL(soma::k_ce_combine, dim3(L.row_tiles, 2 * N * pcs), dim3(64), 0, st, a, hpart, htgt);
+    if (int rc = check_launch("k_ce_combine")) return rc;
+  } else {
+    hipLaunchKernelGGL((soma::k_head_ce<kPert>), dim3(L.row_tiles, N * pcs), dim3(soma::kThreads), 0,
+                       st, a);
+    if (int rc = check_launch("k_head_ce")) return rc;
+  }
   return mark(ctx, kPhaseHead, st);
 }
 

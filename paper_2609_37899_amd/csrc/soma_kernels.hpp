@@ -626,20 +626,22 @@ __device__ __forceinline__ float4 buffer_load_f4(__amdgpu_buffer_rsrc_t r, uint3
 // Batch row of lane row b (rows past the batch read the last row).
 __device__ __forceinline__ int brow_of(int b, int B) { return b < B ? b : B - 1; }
 
-// Perturbed weights of the block's 128 gate rows r0 .. r0 + 127 (interleaved
-// order, row 4u + g is gate g of unit u) over columns col0 .. col0 + 16 KQ of
-// layer matrix W_l (canonical row g H + u, row length ld), one sign:
-//   w = theta + seps z.
+// Perturbed weights of the block's 128 rows r0 .. r0 + 127 over columns
+// col0 .. col0 + 16 KQ of a matrix at canonical offset off_l with row length
+// ld, one sign:  w = theta + seps z.  With kGateRows the rows are a layer's
+// gate rows in interleaved order (row 4u + g is gate g of unit u, canonical
+// row g H + u); otherwise row r is canonical row r.
 // Lane (wave, lr, lg) keeps row r0 + 16 wave + lr, columns col0 + 16 c + 4 lg
 // .. + 3 in w[c].  The block draws the probes cooperatively, 256 columns at a
 // time, into the LDS scratch zs (128 x kZld floats); it is free again on return.
-template <int KQ>
+template <int KQ, bool kGateRows = true>
 __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, const float* th, int64_t off_l,
                                                  int ld, int col0, int H, int r0, uint2 key, uint32_t pair,
                                                  uint32_t step_lo, float seps) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  auto canon = [&](int r) { return kGateRows ? (r & 3) * H + (r >> 2) : r; };
   const int prow = r0 + wave * 16 + lr;
-  const int64_t wrow = off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * ld + col0;
+  const int64_t wrow = off_l + static_cast<int64_t>(canon(prow)) * ld + col0;
 #pragma unroll
   for (int piece = 0; piece < (KQ + 15) / 16; ++piece) {
     const int kq0 = piece * 16;
@@ -648,7 +650,7 @@ __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, con
     for (int q = threadIdx.x; q < 128 * nq * 4; q += blockDim.x) {
       const int m = q / (nq * 4), k4 = q % (nq * 4);
       const int pr = r0 + m;
-      const int64_t kk = off_l + static_cast<int64_t>((pr & 3) * H + (pr >> 2)) * ld + col0 + 16 * kq0 + 4 * k4;
+      const int64_t kk = off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 16 * kq0 + 4 * k4;
       *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
     }
     __syncthreads();
@@ -972,6 +974,190 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
     }
     if (c + 1 < nchunks) sstore(buf ^ 1);
     __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Output head and cross entropy with register-resident weights, in two
+// passes.  k_head_stream: a block owns one job, one vocabulary half (128
+// rows of Whead) of one (expert, direction, sign) slot: it forms the
+// perturbed rows in registers once and streams all R rows of the slot's top
+// layer h through the same double-buffered LDS ring as k_proj_stream.  After
+// each 64-row tile it reduces the half's 128 logits of every row to
+// (m, s) = (max, sum exp(logit - max)) and the lane holding the target byte
+// stores its logit.  k_ce_combine merges the two halves of a row,
+//   ce = M + ln(s_0 e^{m_0 - M} + s_1 e^{m_1 - M}) - logit_target,
+// M = max(m_0, m_1), and sums each 64-row tile in fp64 (the per-tile sums
+// that the loss reduction reads).
+// Partials: hpart[slot][half][R] float2 (m, s); htgt[slot][R].
+// ---------------------------------------------------------------------------
+template <int NCH>
+__global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int nslots, float2* hpart, float* htgt) {
+  constexpr int KQ = 4 * NCH;
+  constexpr int NQ = NCH >= 4 ? 4 : NCH;
+  constexpr int QG = KQ / NQ;
+  constexpr int CW = QG * 16 + 8;
+  constexpr int CF4 = 64 * QG * 4;
+  constexpr int PT = (CF4 + kProjThreads - 1) / kProjThreads;
+  constexpr int LDS_FLOATS = (2 * 64 * CW > 128 * kZld) ? 2 * 64 * CW : 128 * kZld;
+  __shared__ float xs[LDS_FLOATS];
+  __shared__ float2 red[2][8][64];              // per-wave (m, s) of each row, by tile parity
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T;
+  const int R = (T - 1) * B;
+
+  int ps, vh;                                   // slot of this pass, vocabulary half
+  {
+    const int b = blockIdx.x;
+    if (nslots % 8 == 0) {
+      const int i = b / 8;
+      vh = i & 1;
+      ps = (i >> 1) * 8 + b % 8;
+    } else {
+      ps = b >> 1;
+      vh = b & 1;
+    }
+  }
+  const int sg = ps & 1, pj = ps >> 1;
+  const int e = pj / a.pcs, jl = pj % a.pcs;
+  const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = stream_key(a.seeds[e], a.step);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const float seps = sg == 0 ? a.eps : -a.eps;
+  const int vbase = vh * 128 + wave * 16 + 4 * lg;   // vocabulary rows vbase .. +3 of this lane
+  // 32-bit offsets: R H floats < 2^31 bytes (host check).
+  const __amdgpu_buffer_rsrc_t hbuf =
+      buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(static_cast<int64_t>(R) * H * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t bbuf =
+      buffer_of(a.bytes + static_cast<int64_t>(e) * B * T, static_cast<uint32_t>(B * T));
+  float2* hp = hpart + (slot * 2 + vh) * R;
+  float* tg = htgt + slot * R;
+
+  float4 w[KQ];
+  resident_weights<KQ, false>(w, xs, th, a.off_head, H, 0, H, vh * 128, key, pair, step_lo, seps);
+
+  const int nchunks = ((R + 63) / 64) * NQ;
+  float4 pre[PT];
+  auto gload = [&](int c) {
+    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * QG * 16;
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kProjThreads;
+      if (idx < CF4) {
+        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+        const int row = r0 + n < R ? r0 + n : R - 1;
+        pre[i] = buffer_load_f4<0>(hbuf, static_cast<uint32_t>((row * H + k0 + 4 * c4) * 4));
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kProjThreads;
+      if (idx < CF4) {
+        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+        *reinterpret_cast<float4*>(&xs[(buf * 64 + n) * CW + 4 * c4]) = pre[i];
+      }
+    }
+  };
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int y[4];                                     // target bytes of this lane's rows in the current tile
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int c = 0; c < nchunks; ++c) {
+    if (c + 1 < nchunks) gload(c + 1);
+    const int buf = c & 1, qq = c % NQ, r0 = (c / NQ) * 64;
+    if (qq == NQ - 1) {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int row = r0 + nb * 16 + lr < R ? r0 + nb * 16 + lr : R - 1;
+        const int tt = row / B, b = row - tt * B;
+        y[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, static_cast<uint32_t>(b * T + tt + 1), 0, 0);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if (q == qq) {                            // compile-time register index into w
+#pragma unroll
+        for (int gq = 0; gq < QG; ++gq)
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) {
+            const float4 x = *reinterpret_cast<const float4*>(&xs[(buf * 64 + nb * 16 + lr) * CW + 16 * gq + 4 * lg]);
+            acc[nb] = mfma_k16(w[q * QG + gq], x, acc[nb]);
+          }
+      }
+    }
+    if (qq == NQ - 1) {
+      // Lane (lr, lg) holds the logits of vocabulary rows vbase .. +3 for
+      // tile rows nb*16 + lr: reduce over the 4 lane groups, then over the
+      // 8 waves.
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        float m = fmaxf(fmaxf(acc[nb][0], acc[nb][1]), fmaxf(acc[nb][2], acc[nb][3]));
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        float sum = ((__expf(acc[nb][0] - m) + __expf(acc[nb][1] - m)) + __expf(acc[nb][2] - m)) +
+                    __expf(acc[nb][3] - m);
+        sum += __shfl_xor(sum, 16);
+        sum += __shfl_xor(sum, 32);
+        if (lg == 0) red[(c / NQ) & 1][wave][nb * 16 + lr] = make_float2(m, sum);
+        const int row = r0 + nb * 16 + lr;
+        const int yo = y[nb] - vbase;
+        if (row < R && yo >= 0 && yo < 4) {
+          float v = acc[nb][0];
+#pragma unroll
+          for (int r = 1; r < 4; ++r)
+            if (yo == r) v = acc[nb][r];
+          tg[row] = v;
+        }
+        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    if (c + 1 < nchunks) sstore(buf ^ 1);
+    __syncthreads();
+    if (qq == NQ - 1 && threadIdx.x < 64 && r0 + static_cast<int>(threadIdx.x) < R) {
+      // This buffer is next written two tiles on, behind the next tile's
+      // barrier, which these threads reach only after reading it.
+      const int n = threadIdx.x;
+      const float2 (&rd)[8][64] = red[(c / NQ) & 1];
+      float M = rd[0][n].x;
+#pragma unroll
+      for (int wv = 1; wv < 8; ++wv) M = fmaxf(M, rd[wv][n].x);
+      float S = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < 8; ++wv) S += rd[wv][n].y * __expf(rd[wv][n].x - M);
+      hp[r0 + n] = make_float2(M, S);
+    }
+  }
+}
+
+// ce of every row from the two vocabulary halves, summed per 64-row tile in
+// fp64.  Grid: (row tiles, slots of the pass); 64 threads.
+__global__ void k_ce_combine(FwdArgs a, const float2* hpart, const float* htgt) {
+  __shared__ float ces[64];
+  const int tile = blockIdx.x, ps = blockIdx.y;
+  const int sg = ps & 1, pj = ps >> 1;
+  const int e = pj / a.pcs, jl = pj % a.pcs;
+  const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+  const int64_t R = static_cast<int64_t>(a.T - 1) * a.B;
+  const int64_t row = static_cast<int64_t>(tile) * 64 + threadIdx.x;
+  float ce = 0.0f;
+  if (row < R) {
+    const float2 p0 = hpart[(slot * 2) * R + row], p1 = hpart[(slot * 2 + 1) * R + row];
+    const float M = fmaxf(p0.x, p1.x);
+    ce = __logf(p0.y * __expf(p0.x - M) + p1.y * __expf(p1.x - M)) + M - htgt[slot * R + row];
+  }
+  ces[threadIdx.x] = ce;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+    for (int n = 0; n < 64; ++n) tot += static_cast<double>(ces[n]);
+    a.part[slot * a.row_tiles + tile] = tot;
   }
 }
 

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_PKG, "libsoma.so")
 SOMA_OK, SOMA_EINVAL, SOMA_ESHAPE, SOMA_EDEVICE, SOMA_EWORKSPACE = 0, -1, -2, -3, -4
 LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
 FLAG_PER_STEP_RECURRENCE = 1
-FLAG_TILED_PROJECTION = 2
+FLAG_TILED_WEIGHTS = 2
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_eval_loss", "soma_coefficients", "soma_apply_update",

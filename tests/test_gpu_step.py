@@ -149,20 +149,23 @@ def test_persistent_and_per_step_recurrence_agree_bitwise(name):
     assert np.array_equal(t0, t1)
 
 
-@pytest.mark.parametrize("name", ["h512_short", "b64_h128", "b40_h384"])
-def test_streaming_and_tiled_projection_agree_bitwise(name):
-    """The streaming input projection (weights resident in registers, probes
-    drawn once per 128 gate rows) and the tiled one (probes regenerated per
-    row tile) sum over k in the same order: identical bits.  The cases cover
-    a ragged last row tile (R = 80, 320) and slot counts that are and are not
-    a multiple of 8 (the two block-to-job mappings)."""
+@pytest.mark.parametrize("name", ["tiny", "h512_short", "b64_h128", "b40_h384"])
+def test_streaming_and_tiled_weights_agree(name):
+    """The streaming projection and head (weights resident in registers,
+    probes drawn once per 128 weight rows) against the tiled kernels (probes
+    regenerated per row tile).  The projections sum over k in the same order;
+    the streaming head merges the softmax of two vocabulary halves, so the
+    cross entropies agree up to fp32 rounding order (one ulp-level term per
+    token, 1e-6 relative on the per-pair mean).  The cases cover a ragged last
+    row tile (R = 80, 320) and slot counts that are and are not a multiple of
+    8 (the two block-to-job mappings)."""
     torch = require_gpu()
     N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
     theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
     data = synth.expert_batches([100 + e for e in range(N)], B, T)
     seeds = soma.seeds_tensor(synth.expert_seeds(N))
     outs = []
-    for flags in (0, soma.FLAG_TILED_PROJECTION):
+    for flags in (0, soma.FLAG_TILED_WEIGHTS):
         ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags))
         th = torch.from_numpy(theta.copy()).cuda()
         losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
@@ -171,5 +174,6 @@ def test_streaming_and_tiled_projection_agree_bitwise(name):
         outs.append((th.cpu().numpy(), losses.cpu().numpy()))
     (t0, l0), (t1, l1) = outs
     assert np.all(np.isfinite(l0))
-    assert np.array_equal(l0, l1)
-    assert np.array_equal(t0, t1)
+    rel = np.abs(l0.astype(np.float64) - l1) / np.abs(l1)
+    assert rel.max() <= 1e-6, rel.max()
+    assert_theta_close(t0, t1)
