@@ -102,12 +102,17 @@ def cpu_baseline(w, theta, data, seeds):
         tokens = w.perturbed_tokens
         sample = f"full step of {w.name}"
     else:
+        # Directions 0, 1, ... of expert 0 (both signs each) until 10 s of
+        # oracle work, at most 8.
         t0 = time.perf_counter()
-        for s in (+1, -1):
-            oracle.perturbed_loss(cfg, theta[0], int(seeds[0]), 0, 0, s, w.eps, data[0])
+        n = 0
+        while n < min(8, w.n_pairs) and (n == 0 or time.perf_counter() - t0 < 10.0):
+            for s in (+1, -1):
+                oracle.perturbed_loss(cfg, theta[0], int(seeds[0]), 0, n, s, w.eps, data[0])
+            n += 1
         dt = time.perf_counter() - t0
-        tokens = 2 * w.batch * (w.seq_len - 1)
-        sample = (f"expert 0, direction 0, both signs at full B={w.batch}, T={w.seq_len} "
+        tokens = n * 2 * w.batch * (w.seq_len - 1)
+        sample = (f"expert 0, directions 0..{n - 1}, both signs, at full B={w.batch}, T={w.seq_len} "
                   f"({tokens} perturbed tokens of {w.perturbed_tokens} per step; "
                   f"full step extrapolates to {dt * w.perturbed_tokens / tokens:.0f} s)")
     return {"value": tokens / dt, "unit": "perturbed tokens/s", "cores": threads, "kind": "oracle",

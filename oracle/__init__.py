@@ -39,7 +39,8 @@ def build(force: bool = False) -> str:
 
 class OracleCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
-        "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode")]
+        "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
+        "probe")]
 
 
 def _load():
@@ -63,6 +64,9 @@ def _load():
                 "oracle_box_muller_array": (None, [u32p, u32p, ctypes.c_int64, f32p, f32p]),
                 "oracle_gaussian": (None, [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint32,
                                            ctypes.c_uint64, ctypes.c_uint64, f32p]),
+                "oracle_probe": (ctypes.c_int, [ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64,
+                                                ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64,
+                                                f32p]),
                 "oracle_forward_loss_f64": (ctypes.c_double, [cfgp, f64p, u8p]),
                 "oracle_forward_loss": (ctypes.c_double, [cfgp, f32p, u8p]),
                 "oracle_perturb": (None, [cfgp, f32p, ctypes.c_uint64, ctypes.c_uint64,
@@ -91,14 +95,19 @@ def _ptr(a: np.ndarray, ctype):
     return a.ctypes.data_as(ctypes.POINTER(ctype))
 
 
-def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode=0):
-    return OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode)
+PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
+
+
+def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode=0,
+             probe=PROBE_GAUSSIAN):
+    return OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe)
 
 
 def cfg_from(shape) -> OracleCfg:
     """Build the oracle's configuration from any object with the shape fields."""
     return make_cfg(shape.n_experts, shape.n_layers, shape.embed, shape.hidden, shape.batch,
-                    shape.seq_len, shape.n_pairs, getattr(shape, "loss_mode", 0))
+                    shape.seq_len, shape.n_pairs, getattr(shape, "loss_mode", 0),
+                    getattr(shape, "probe", PROBE_GAUSSIAN))
 
 
 def param_count(cfg: OracleCfg) -> int:
@@ -170,6 +179,17 @@ def gaussian(seed: int, step: int, pair: int, k0: int, count: int) -> np.ndarray
     out = np.empty(int(count), dtype=np.float32)
     _load().oracle_gaussian(int(seed), int(step), int(pair), int(k0), int(count),
                             _ptr(out, ctypes.c_float))
+    return out
+
+
+def probe(law: int, seed: int, step: int, pair: int, k0: int, count: int) -> np.ndarray:
+    """Probe values z_pair[k0 .. k0+count) under law 0 (Gaussian), 1 (sparse
+    Rademacher) or 2 (dense Rademacher)."""
+    out = np.empty(int(count), dtype=np.float32)
+    rc = _load().oracle_probe(int(law), int(seed), int(step), int(pair), int(k0), int(count),
+                              _ptr(out, ctypes.c_float))
+    if rc != 0:
+        raise ValueError(f"unknown probe law {law}")
     return out
 
 

@@ -22,12 +22,23 @@
  *     bias-free as in Appendix C, gates in the order i, f, g, o;
  *   - the update theta' = theta - lr * g_hat (plain SGD step on g_hat).
  *
- * Probe law: z ~ N(0,1) per parameter, drawn by counter-based Philox4x32-10
- * (Salmon, Moraes, Dror, Shaw, SC'11, "Parallel random numbers: as easy as
- * 1, 2, 3") and the Box-Muller transform.  The logarithm and the sine/cosine
- * used by Box-Muller are computed by this file's own fp32 routines (series
- * below) so that the result is a fixed sequence of correctly rounded IEEE
- * operations, reproducible bit for bit on any conforming machine.
+ * Probe laws (cfg.probe), all from counter-based Philox4x32-10 (Salmon,
+ * Moraes, Dror, Shaw, SC'11, "Parallel random numbers: as easy as 1, 2, 3"):
+ *   0  Gaussian: z ~ N(0,1) per parameter by the Box-Muller transform.  The
+ *      logarithm and the sine/cosine it uses are this file's own fp32
+ *      routines (series below), a fixed sequence of correctly rounded IEEE
+ *      operations, reproducible bit for bit on any conforming machine.
+ *   1  sparse Rademacher, the paper's training law (Appendix E): each
+ *      coordinate is 0 with probability 1/2 and -1 or +1 with probability
+ *      1/4 each (the paper's normalization gains, which are always +-1, do
+ *      not occur in this model).
+ *   2  dense Rademacher, the law of the paper's variance theory (Section 4,
+ *      Eq. main-spsa; Appendix F, Prop. block-variance): -1 or +1 with
+ *      probability 1/2 each.
+ *   Both Rademacher laws read a 2-bit field per coordinate (64 coordinates
+ *   per Philox block): the high bit says whether a sparse coordinate is
+ *   active, the low bit is the sign (1 = -1).  The dense law uses the sign
+ *   bit alone, so the two laws agree wherever the sparse one is nonzero.
  *
  * Precision: perturbed weights are formed in fp32 with one rounding
  * (fmaf(+-eps, z, theta)); the forward pass, the losses, the coefficients and
@@ -58,6 +69,7 @@ typedef struct {
   int32_t seq_len;   /* T bytes per sequence -> T-1 targets */
   int32_t n_pairs;   /* P antithetic pairs (directions) per expert */
   int32_t loss_mode; /* 0: independent per-expert losses, 1: summed loss */
+  int32_t probe;     /* probe law: 0 Gaussian, 1 sparse Rademacher, 2 dense Rademacher */
 } oracle_cfg;
 
 #define VOCAB 256
@@ -251,6 +263,44 @@ void oracle_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, u
   }
 }
 
+/* Rademacher probe value of coordinate k (laws 1 and 2).
+ *   key     = (lo32(seed), hi32(seed) ^ hi32(step))          (as above)
+ *   counter = (lo32(b), pair, lo32(step), hi32(b)),  b = k >> 6
+ *   field   = bits 2 (k & 15) .. +1 of word (k >> 4) & 3 of the block's output. */
+static float rademacher_value(int law, uint64_t seed, uint64_t step, uint32_t pair, uint64_t k) {
+  const uint64_t b = k >> 6;
+  uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32) ^ (uint32_t)(step >> 32)};
+  uint32_t ctr[4] = {(uint32_t)b, pair, (uint32_t)step, (uint32_t)(b >> 32)};
+  uint32_t w[4];
+  oracle_philox4x32_10(ctr, key, w);
+  const uint32_t field = (w[(k >> 4) & 3] >> (2 * (k & 15))) & 3u;
+  const float sgn = (field & 1u) ? -1.0f : 1.0f;
+  if (law == 2) return sgn;
+  return (field >> 1) ? sgn : 0.0f;
+}
+
+/* z_pair[4q .. 4q+3] under probe law `law`. */
+static void probe_quad(int law, uint64_t seed, uint64_t step, uint32_t pair, uint64_t q, float z[4]) {
+  if (law == 0) {
+    gaussian_quad(seed, step, pair, q, z);
+    return;
+  }
+  for (int i = 0; i < 4; ++i) z[i] = rademacher_value(law, seed, step, pair, 4 * q + (uint64_t)i);
+}
+
+/* count probe values z_pair[k0 .. k0+count) under law `law` (0, 1 or 2). */
+int oracle_probe(int law, uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+                 float *out) {
+  if (law < 0 || law > 2) return -1;
+  for (uint64_t i = 0; i < count; ++i) {
+    uint64_t k = k0 + i;
+    float z[4];
+    probe_quad(law, seed, step, pair, k >> 2, z);
+    out[i] = z[k & 3];
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Forward pass and loss, fp64.                                               */
 /* ------------------------------------------------------------------------ */
@@ -350,7 +400,7 @@ void oracle_perturb(const oracle_cfg *c, const float *theta, uint64_t seed, uint
   const int64_t d = oracle_param_count(c);
   for (int64_t q = 0; 4 * q < d; ++q) {
     float z[4];
-    gaussian_quad(seed, step, pair, (uint64_t)q, z);
+    probe_quad(c->probe, seed, step, pair, (uint64_t)q, z);
     for (int i = 0; i < 4 && 4 * q + i < d; ++i) {
       int64_t k = 4 * q + i;
       w_out[k] = fmaf(sign_eps, z[i], theta[k]);
@@ -388,7 +438,7 @@ void oracle_apply_update(const oracle_cfg *c, const float *theta, uint64_t seed,
     double g = 0.0;
     for (int j = 0; j < P; ++j) {
       float z[4];
-      gaussian_quad(seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
+      probe_quad(c->probe, seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
       g += coef[j] * (double)z[k & 3];
     }
     theta_out[i] = (float)((double)theta[k] - (double)lr * g);
@@ -410,7 +460,7 @@ int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *se
                      float *theta_out, double *ghat) {
   const int N = c->n_experts, P = c->n_pairs;
   if (N < 1 || P < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
-      c->seq_len < 2)
+      c->seq_len < 2 || c->probe < 0 || c->probe > 2)
     return -1;
   const int64_t d = oracle_param_count(c);
   const size_t bstride = (size_t)c->batch * c->seq_len;
