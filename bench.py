@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "perturbed forward tokens/sec (expert×pert×token) + SPSA steps/sec, 1 GPU"
 PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 PEAK_HBM_GBS = 8000.0
+PROBE_LAWS = {"gaussian": 0, "sparse": 1, "dense": 2}
 
 
 def parse():
@@ -38,6 +39,9 @@ def parse():
     ap.add_argument("--workload", default="soma_n2_l2_h512")
     ap.add_argument("--pairs", type=int, default=0, help="override the workload's directions per expert")
     ap.add_argument("--pair-chunk", type=int, default=0)
+    ap.add_argument("--probe", choices=sorted(PROBE_LAWS), default="gaussian",
+                    help="probe law: gaussian (the workload's), sparse (the paper's training law: "
+                         "0 w.p. 1/2, +-1 w.p. 1/4) or dense (+-1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-kernel HBM bytes from rocprofv3 counter runs (JSON), if present")
@@ -88,12 +92,13 @@ def kernel_flops(w):
     return {"rec": rec, "proj": proj, "fold": emb_in, "head": head}
 
 
-def cpu_baseline(w, theta, data, seeds):
+def cpu_baseline(w, theta, data, seeds, probe=0):
     """Time the oracle on a bounded sample of the workload."""
     import numpy as np
 
     import oracle
     cfg = oracle.cfg_from(w)
+    cfg.probe = probe
     threads = oracle.num_threads()
     if w.perturbed_tokens * w.flops_per_token < 2e10:
         t0 = time.perf_counter()
@@ -148,8 +153,9 @@ def main():
     seeds_np = synth.expert_seeds(w.n_experts)
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    probe = PROBE_LAWS[args.probe]
     shape = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
-                       w.loss_mode, args.pair_chunk)
+                       w.loss_mode, args.pair_chunk, probe=probe)
 
     ctx = soma.Context(shape, device=dev)
     theta = torch.from_numpy(theta0.copy()).to(dev)
@@ -226,6 +232,7 @@ def main():
                    "n_pairs": w.n_pairs, "forwards_per_expert": 2 * w.n_pairs,
                    "params_per_expert": w.params_per_expert, "eps": w.eps, "lr": w.lr,
                    "loss_mode": "summed" if w.loss_mode else "independent",
+                   "probe": args.probe,
                    "parallelism": "single GPU, all experts and directions in each launch"},
         "algorithmic_tflops": round(total_flops / sec / 1e12, 3),
         "phase_ms": {k: round(v, 3) for k, v in ms.items()},
@@ -233,7 +240,7 @@ def main():
         "mean_loss": float(np.mean(lv)),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, theta0, batches[0], seeds_np)
+        out["cpu_baseline"] = cpu_baseline(w, theta0, batches[0], seeds_np, probe)
     print(json.dumps(out), flush=True)
 
 

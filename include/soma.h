@@ -4,7 +4,8 @@
  * SOMA (arXiv 2609.37899) trains an ensemble of N byte-level LSTM experts
  * with zero-order SPSA.  One step of the method, for every expert e:
  *
- *   1. draw P directions z_{e,j} ~ N(0, I) over all d parameters of e;
+ *   1. draw P directions z_{e,j} over all d parameters of e (Gaussian, or
+ *      the paper's sparse or dense Rademacher law: soma_config.probe);
  *   2. evaluate the antithetic losses L_{e,j,+-} = L_e(theta_e +- eps z_{e,j})
  *      on the expert's own batch, all directions and both signs sharing it
  *      (Section 4; Appendix E, Eq. localspsa);
@@ -26,8 +27,8 @@
  *   i, f, g, o and columns [input | recurrent], in_1 = E, in_l = H;
  *   Whead[256][H].  d = 256 E + sum_l 4H (in_l + H) + 256 H.
  *
- * Probe stream (exact, reproducible bit for bit): z_{e,j}[k] is element
- * k & 3 of the Gaussian quad for q = k >> 2, obtained from
+ * Probe stream (exact, reproducible bit for bit), Gaussian law: z_{e,j}[k]
+ * is element k & 3 of the Gaussian quad for q = k >> 2, obtained from
  *   Philox4x32-10 (Salmon et al., SC'11) with
  *     key     = (lo32(seed_e), hi32(seed_e) ^ hi32(step)),
  *     counter = (lo32(q), j, lo32(step), hi32(q)),
@@ -38,6 +39,12 @@
  *   where ln, cos and sin are fixed fp32 series evaluations (an atanh series
  *   for ln, Taylor series of sin and cos of (pi/2) r after an exact
  *   quarter-turn reduction) with correctly rounded +, *, /, fma and sqrt.
+ * Rademacher laws: coordinate k reads the 2-bit field f at bits 2 (k & 15)
+ *   of word (k >> 4) & 3 of the Philox output for the same key and counter
+ *   (lo32(b), j, lo32(step), hi32(b)), b = k >> 6.  Sparse (the paper's
+ *   training law, Appendix E): z = 0 if f < 2, else (f & 1 ? -1 : +1), i.e.
+ *   0 w.p. 1/2 and +-1 w.p. 1/4 each.  Dense (the law of its variance theory,
+ *   Section 4 and Appendix F): z = f & 1 ? -1 : +1.
  *   Perturbed weights are fmaf(+-eps, z, theta) (one rounding).
  *
  * Conventions for every entry point:
@@ -77,6 +84,13 @@ enum soma_loss_mode {
   SOMA_LOSS_SUMMED = 1       /* c_j from the summed loss, applied to all experts (Appendix J) */
 };
 
+/* Probe laws (soma_config.probe; the stream definitions are above). */
+enum soma_probe_law {
+  SOMA_PROBE_GAUSSIAN = 0,          /* z ~ N(0, 1) */
+  SOMA_PROBE_SPARSE_RADEMACHER = 1, /* 0 w.p. 1/2, +-1 w.p. 1/4 each (Appendix E) */
+  SOMA_PROBE_RADEMACHER = 2         /* +-1 w.p. 1/2 each (Section 4; Appendix F) */
+};
+
 /* Execution flags (soma_config.flags). */
 enum soma_flags {
   /* Run the recurrence as one launch per time step even where the persistent
@@ -106,6 +120,7 @@ typedef struct soma_config {
   int32_t loss_mode;  /* enum soma_loss_mode */
   int32_t pair_chunk; /* directions evaluated per pass; 0 = automatic */
   int32_t flags;      /* enum soma_flags, 0 by default */
+  int32_t probe;      /* enum soma_probe_law, 0 (Gaussian) by default */
 } soma_config;
 
 typedef struct soma_ctx soma_ctx;
@@ -164,10 +179,17 @@ int soma_coefficients(soma_ctx* ctx, float* coef_dev, void* stream);
 int soma_apply_update(soma_ctx* ctx, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,
                       float lr, const float* coef_dev, void* stream);
 
-/* The probe values z_{seed,step,pair}[k] for k in [k0, k0 + count), written
- * to out_dev [count] fp32.  k0 + count must not exceed 2^40. */
+/* The Gaussian probe values z_{seed,step,pair}[k] for k in [k0, k0 + count),
+ * written to out_dev [count] fp32 (soma_probe with SOMA_PROBE_GAUSSIAN).
+ * k0 + count must not exceed 2^40. */
 int soma_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
                   float* out_dev, void* stream);
+
+/* The probe values z_{seed,step,pair}[k] for k in [k0, k0 + count) under
+ * probe law `law` (enum soma_probe_law), written to out_dev [count] fp32.
+ * k0 + count must not exceed 2^40; an unknown law returns SOMA_EINVAL. */
+int soma_probe(int law, uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+               float* out_dev, void* stream);
 
 /* Philox4x32-10 on n (counter, key) pairs: ctr_dev [n][4], key_dev [n][2],
  * out_dev [n][4], all uint32 device arrays. */

@@ -81,6 +81,9 @@ int validate(const soma_config* c) {
     return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs]");
   if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS))
     return fail(SOMA_EINVAL, "unknown flags");
+  if (c->probe != SOMA_PROBE_GAUSSIAN && c->probe != SOMA_PROBE_SPARSE_RADEMACHER &&
+      c->probe != SOMA_PROBE_RADEMACHER)
+    return fail(SOMA_EINVAL, "probe must be 0 (Gaussian), 1 (sparse Rademacher) or 2 (Rademacher)");
   const int64_t d = param_count_of(*c);
   if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
   const int64_t rows = int64_t(c->seq_len - 1) * c->batch;
@@ -162,6 +165,20 @@ __global__ void k_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t
   }
 }
 
+__global__ void k_probe(int law, uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count,
+                        float* out) {
+  const uint64_t q = (k0 >> 2) + blockIdx.x * uint64_t(blockDim.x) + threadIdx.x;
+  const uint64_t qend = (k0 + count + 3) >> 2;
+  if (q >= qend) return;
+  const float4 z = probe_quad(law, stream_key(seed, step), pair, static_cast<uint32_t>(step), 4 * q);
+  const float zz[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint64_t k = 4 * q + i;
+    if (k >= k0 && k < k0 + count) out[k - k0] = zz[i];
+  }
+}
+
 __global__ void k_philox(const uint32_t* ctr, const uint32_t* key, uint32_t* out, uint64_t n) {
   const uint64_t i = blockIdx.x * uint64_t(blockDim.x) + threadIdx.x;
   if (i >= n) return;
@@ -219,7 +236,7 @@ __global__ void k_coef(const double* lossd, int N, int P, int summed, double inv
 // theta[e][k] -= lr * sum_{j<P} coef[e][j] z_{e,j}[k], one probe quad per
 // thread and direction; the sum runs in j order in fp32.
 __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* seeds, uint64_t step,
-                                                 float lr, const float* coef, int64_t d, int P,
+                                                 float lr, const float* coef, int64_t d, int P, int law,
                                                  const unsigned* err) {
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
@@ -231,7 +248,7 @@ __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* se
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int j = 0; j < P; ++j) {
     const float cj = c[j];
-    const float4 z = gauss_quad(key, static_cast<uint32_t>(j), step_lo, static_cast<uint64_t>(q));
+    const float4 z = probe_quad(law, key, static_cast<uint32_t>(j), step_lo, 4 * static_cast<uint64_t>(q));
     acc = fma4(cj, z, acc);
   }
   float* t = theta + int64_t(e) * d + 4 * q;
@@ -307,32 +324,38 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
   return groups >= 1 ? groups : 0;
 }
 
-template <int NB, int NCH>
+template <int NB, int NCH, bool kRad>
 const void* persist_kernel() {
-  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH>);
+  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH, kRad>);
 }
 
-template <int NB>
+template <int NB, bool kRad>
 const void* persist_kernel_for(int nch) {
   switch (nch) {
-    case 1: return persist_kernel<NB, 1>();
-    case 2: return persist_kernel<NB, 2>();
-    case 3: return persist_kernel<NB, 3>();
-    case 4: return persist_kernel<NB, 4>();
-    case 5: return persist_kernel<NB, 5>();
-    case 6: return persist_kernel<NB, 6>();
-    case 7: return persist_kernel<NB, 7>();
-    case 8: return persist_kernel<NB, 8>();
+    case 1: return persist_kernel<NB, 1, kRad>();
+    case 2: return persist_kernel<NB, 2, kRad>();
+    case 3: return persist_kernel<NB, 3, kRad>();
+    case 4: return persist_kernel<NB, 4, kRad>();
+    case 5: return persist_kernel<NB, 5, kRad>();
+    case 6: return persist_kernel<NB, 6, kRad>();
+    case 7: return persist_kernel<NB, 7, kRad>();
+    case 8: return persist_kernel<NB, 8, kRad>();
     default: return nullptr;
   }
 }
 
-// The persistent recurrence kernel for batch B and hidden width H (H % 64 == 0, H <= 512).
+template <bool kRad>
 const void* persist_kernel_for(int B, int H) {
   const int nch = H / 64;
-  if (B <= 16) return persist_kernel_for<1>(nch);
-  if (B <= 32) return persist_kernel_for<2>(nch);
-  return persist_kernel_for<4>(nch);
+  if (B <= 16) return persist_kernel_for<1, kRad>(nch);
+  if (B <= 32) return persist_kernel_for<2, kRad>(nch);
+  return persist_kernel_for<4, kRad>(nch);
+}
+
+// The persistent recurrence kernel for batch B, hidden width H (H % 64 == 0,
+// H <= 512) and the generator family of probe law `probe`.
+const void* persist_kernel_for(int B, int H, int probe) {
+  return probe == SOMA_PROBE_GAUSSIAN ? persist_kernel_for<false>(B, H) : persist_kernel_for<true>(B, H);
 }
 
 // The streaming input projection and head apply for H % 64 == 0, H <= 512
@@ -344,33 +367,49 @@ bool stream_weights(const soma_config& c) {
   return c.hidden % 64 == 0 && c.hidden <= 512 && gin_slot_bytes < (int64_t(1) << 31);
 }
 
-void launch_head_stream(const soma::FwdArgs& a, int nslots, float2* hpart, float* htgt, hipStream_t st) {
+template <bool kRad>
+void launch_head_stream_t(const soma::FwdArgs& a, int nslots, float2* hpart, float* htgt, hipStream_t st) {
   const dim3 grid(unsigned(nslots * 2)), block(soma::kProjThreads);
   switch (a.H / 64) {
-    case 1: hipLaunchKernelGGL(soma::k_head_stream<1>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 2: hipLaunchKernelGGL(soma::k_head_stream<2>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 3: hipLaunchKernelGGL(soma::k_head_stream<3>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 4: hipLaunchKernelGGL(soma::k_head_stream<4>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 5: hipLaunchKernelGGL(soma::k_head_stream<5>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 6: hipLaunchKernelGGL(soma::k_head_stream<6>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 7: hipLaunchKernelGGL(soma::k_head_stream<7>, grid, block, 0, st, a, nslots, hpart, htgt); break;
-    default: hipLaunchKernelGGL(soma::k_head_stream<8>, grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 1: hipLaunchKernelGGL((soma::k_head_stream<1, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 2: hipLaunchKernelGGL((soma::k_head_stream<2, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 3: hipLaunchKernelGGL((soma::k_head_stream<3, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 4: hipLaunchKernelGGL((soma::k_head_stream<4, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 5: hipLaunchKernelGGL((soma::k_head_stream<5, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 6: hipLaunchKernelGGL((soma::k_head_stream<6, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 7: hipLaunchKernelGGL((soma::k_head_stream<7, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    default: hipLaunchKernelGGL((soma::k_head_stream<8, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+  }
+}
+
+void launch_head_stream(const soma::FwdArgs& a, int nslots, float2* hpart, float* htgt, hipStream_t st) {
+  if (a.probe == SOMA_PROBE_GAUSSIAN)
+    launch_head_stream_t<false>(a, nslots, hpart, htgt, st);
+  else
+    launch_head_stream_t<true>(a, nslots, hpart, htgt, st);
+}
+
+template <bool kRad>
+void launch_proj_stream_t(const soma::FwdArgs& a, int nslots, hipStream_t st) {
+  const int mblocks = a.H / 32;
+  const dim3 grid(unsigned(nslots * mblocks)), block(soma::kProjThreads);
+  switch (a.H / 64) {
+    case 1: hipLaunchKernelGGL((soma::k_proj_stream<1, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 2: hipLaunchKernelGGL((soma::k_proj_stream<2, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 3: hipLaunchKernelGGL((soma::k_proj_stream<3, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 4: hipLaunchKernelGGL((soma::k_proj_stream<4, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 5: hipLaunchKernelGGL((soma::k_proj_stream<5, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 6: hipLaunchKernelGGL((soma::k_proj_stream<6, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 7: hipLaunchKernelGGL((soma::k_proj_stream<7, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    default: hipLaunchKernelGGL((soma::k_proj_stream<8, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
   }
 }
 
 void launch_proj_stream(const soma::FwdArgs& a, int nslots, hipStream_t st) {
-  const int mblocks = a.H / 32;
-  const dim3 grid(unsigned(nslots * mblocks)), block(soma::kProjThreads);
-  switch (a.H / 64) {
-    case 1: hipLaunchKernelGGL(soma::k_proj_stream<1>, grid, block, 0, st, a, mblocks, nslots); break;
-    case 2: hipLaunchKernelGGL(soma::k_proj_stream<2>, grid, block, 0, st, a, mblocks, nslots); break;
-    case 3: hipLaunchKernelGGL(soma::k_proj_stream<3>, grid, block, 0, st, a, mblocks, nslots); break;
-    case 4: hipLaunchKernelGGL(soma::k_proj_stream<4>, grid, block, 0, st, a, mblocks, nslots); break;
-    case 5: hipLaunchKernelGGL(soma::k_proj_stream<5>, grid, block, 0, st, a, mblocks, nslots); break;
-    case 6: hipLaunchKernelGGL(soma::k_proj_stream<6>, grid, block, 0, st, a, mblocks, nslots); break;
-    case 7: hipLaunchKernelGGL(soma::k_proj_stream<7>, grid, block, 0, st, a, mblocks, nslots); break;
-    default: hipLaunchKernelGGL(soma::k_proj_stream<8>, grid, block, 0, st, a, mblocks, nslots); break;
-  }
+  if (a.probe == SOMA_PROBE_GAUSSIAN)
+    launch_proj_stream_t<false>(a, nslots, st);
+  else
+    launch_proj_stream_t<true>(a, nslots, st);
 }
 
 int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, hipStream_t st) {
@@ -400,6 +439,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   a.off_head = L.off_head;
   a.step = step;
   a.eps = eps;
+  a.probe = c.probe;
   a.N = c.n_experts;
   a.E = c.embed;
   a.H = c.hidden;
@@ -452,7 +492,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
       if (int rc = check_launch("k_zero_u32")) return rc;
       const int blocks = groups * (H / soma::kRecUnits);
-      if (int rc = launch_persist(persist_kernel_for(c.batch, H), p, blocks, st)) return rc;
+      if (int rc = launch_persist(persist_kernel_for(c.batch, H, c.probe), p, blocks, st)) return rc;
       ctx->rec_launches += 1;
     } else {
       const dim3 grid((H / 16) * bgroups, pcs, N);
@@ -521,7 +561,7 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
     int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
     hipFuncAttributes fa{};
     const bool shape_ok = cfg->hidden % 64 == 0 && cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
-    const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden) : nullptr;
+    const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden, cfg->probe) : nullptr;
     if (kern && hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
@@ -617,7 +657,7 @@ int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t 
   if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
   const int64_t quads = (L.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
-                     st, theta, seeds, step, lr, coef, L.d, c.n_pairs, err);
+                     st, theta, seeds, step, lr, coef, L.d, c.n_pairs, c.probe, err);
   if (int rc = check_launch("k_update")) return rc;
   if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
   ctx->have_coef = true;
@@ -666,7 +706,7 @@ int soma_apply_update(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
-                     as_stream(stream), theta, seeds, step, lr, coef, ctx->lay.d, c.n_pairs,
+                     as_stream(stream), theta, seeds, step, lr, coef, ctx->lay.d, c.n_pairs, c.probe,
                      static_cast<const unsigned*>(nullptr));
   if (int rc = check_launch("k_update")) return rc;
   return ok();
@@ -682,6 +722,21 @@ int soma_gaussian(uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint
   hipLaunchKernelGGL(soma::k_gaussian, dim3(unsigned((quads + 255) / 256)), dim3(256), 0,
                      as_stream(stream), seed, step, pair, k0, count, out);
   if (int rc = check_launch("k_gaussian")) return rc;
+  return ok();
+}
+
+int soma_probe(int law, uint64_t seed, uint64_t step, uint32_t pair, uint64_t k0, uint64_t count, float* out,
+               void* stream) {
+  if (law != SOMA_PROBE_GAUSSIAN && law != SOMA_PROBE_SPARSE_RADEMACHER && law != SOMA_PROBE_RADEMACHER)
+    return fail(SOMA_EINVAL, "unknown probe law %d", law);
+  if (!out) return fail(SOMA_EINVAL, "out is NULL");
+  if (count == 0) return ok();
+  if (k0 + count > (uint64_t(1) << 40) || k0 + count < k0)
+    return fail(SOMA_EINVAL, "k0 + count must not exceed 2^40");
+  const uint64_t quads = ((k0 + count + 3) >> 2) - (k0 >> 2);
+  hipLaunchKernelGGL(soma::k_probe, dim3(unsigned((quads + 255) / 256)), dim3(256), 0, as_stream(stream), law,
+                     seed, step, pair, k0, count, out);
+  if (int rc = check_launch("k_probe")) return rc;
   return ok();
 }
 

@@ -84,6 +84,7 @@ struct FwdArgs {
   int64_t off_head; // canonical offset of Whead
   uint64_t step;
   float eps;
+  int probe;              // probe law (kProbe*)
   int N, E, H, B, T, PC;  // PC = slot stride in directions
   int pcs;                // directions in this pass (grid extent)
   int j0;                 // first direction of the chunk
@@ -130,7 +131,7 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
       const int64_t kk = static_cast<int64_t>(v0 + n) * E + k0 + 4 * c4;
       const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
       if (kPert) {
-        const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
+        const float4 z = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk));
         *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = fma4(a.eps, z, t4);
         *reinterpret_cast<float4*>(&es[NS - 1][n][4 * c4]) = fma4(-a.eps, z, t4);
       } else {
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
       const float4 t4 = *reinterpret_cast<const float4*>(th + kw);
       float4 w[NS];
       if (kPert) {
-        const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kw) >> 2);
+        const float4 z = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kw));
         w[0] = fma4(a.eps, z, t4);
         w[NS - 1] = fma4(-a.eps, z, t4);
       } else {
@@ -191,7 +192,7 @@ using StageTile = float[2][NS][NBR * 16][kLdk];
 template <int NS, int MB, int NBR, bool kPert, class Act>
 __device__ __forceinline__ void perturbed_mainloop(f32x4 (&acc)[MB][NS][NBR], StageTile<NS, NBR>& lds,
                                                    const float* __restrict__ th,
-                                                   const int64_t (&wrow)[MB], int K, uint2 key,
+                                                   const int64_t (&wrow)[MB], int K, int law, uint2 key,
                                                    uint32_t pair, uint32_t step_lo, float eps,
                                                    const Act& act) {
   constexpr int ROWS = NBR * 16;
@@ -237,7 +238,7 @@ __device__ __forceinline__ void perturbed_mainloop(f32x4 (&acc)[MB][NS][NBR], St
       for (int mb = 0; mb < MB; ++mb) {
         const float4 t4 = *reinterpret_cast<const float4*>(th + wrow[mb] + kk);
         if (kPert) {
-          const float4 z = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(wrow[mb] + kk) >> 2);
+          const float4 z = probe_quad(law, key, pair, step_lo, static_cast<uint64_t>(wrow[mb] + kk));
           w[mb][0] = fma4(eps, z, t4);
           w[mb][NS - 1] = fma4(-eps, z, t4);
         } else {
@@ -298,7 +299,7 @@ __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
     return row < R ? *reinterpret_cast<const float4*>(hin + ((slot0 + s) * R + row) * H + k)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   };
-  perturbed_mainloop<NS, 1, NBP, kPert>(acc, xs, th, wrow, in, key, pair, step_lo, a.eps, act);
+  perturbed_mainloop<NS, 1, NBP, kPert>(acc, xs, th, wrow, in, a.probe, key, pair, step_lo, a.eps, act);
 
   const int p = mtile * 64 + wave * 16 + 4 * lg;
 #pragma unroll
@@ -354,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
       return b < B ? *reinterpret_cast<const float4*>(hprev + ((slot0 + s) * R + b) * H + k)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
     };
-    perturbed_mainloop<NS, 1, NB, kPert>(acc, hs, th, wrow, H, key, pair, step_lo, a.eps, act);
+    perturbed_mainloop<NS, 1, NB, kPert>(acc, hs, th, wrow, H, a.probe, key, pair, step_lo, a.eps, act);
   }
 
   const int unit = utile * 16 + wave * 4 + lg;
@@ -428,7 +429,7 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
     return row < R ? *reinterpret_cast<const float4*>(hin + ((slot0 + s) * R + row) * H + k)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   };
-  perturbed_mainloop<NS, 4, NBH, kPert>(acc, xs, th, wrow, H, key, pair, step_lo, a.eps, act);
+  perturbed_mainloop<NS, 4, NBH, kPert>(acc, xs, th, wrow, H, a.probe, key, pair, step_lo, a.eps, act);
 
   // Row maxima: lane-local over 16 logits, then across the 4 lane groups.
   float mx[NS][NBH];
@@ -634,10 +635,13 @@ __device__ __forceinline__ int brow_of(int b, int B) { return b < B ? b : B - 1;
 // Lane (wave, lr, lg) keeps row r0 + 16 wave + lr, columns col0 + 16 c + 4 lg
 // .. + 3 in w[c].  The block draws the probes cooperatively, 256 columns at a
 // time, into the LDS scratch zs (128 x kZld floats); it is free again on return.
-template <int KQ, bool kGateRows = true>
+// The generator is fixed at compile time (kRad: a Rademacher law, `law` then
+// telling sparse from dense; else Gaussian): a run-time choice between the
+// two costs these register-resident kernels spills.
+template <int KQ, bool kGateRows, bool kRad>
 __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, const float* th, int64_t off_l,
-                                                 int ld, int col0, int H, int r0, uint2 key, uint32_t pair,
-                                                 uint32_t step_lo, float seps) {
+                                                 int ld, int col0, int H, int r0, int law, uint2 key,
+                                                 uint32_t pair, uint32_t step_lo, float seps) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   auto canon = [&](int r) { return kGateRows ? (r & 3) * H + (r >> 2) : r; };
   const int prow = r0 + wave * 16 + lr;
@@ -650,8 +654,9 @@ __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, con
     for (int q = threadIdx.x; q < 128 * nq * 4; q += blockDim.x) {
       const int m = q / (nq * 4), k4 = q % (nq * 4);
       const int pr = r0 + m;
-      const int64_t kk = off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 16 * kq0 + 4 * k4;
-      *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) = gauss_quad(key, pair, step_lo, static_cast<uint64_t>(kk) >> 2);
+      const uint64_t kk = static_cast<uint64_t>(off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 16 * kq0 + 4 * k4);
+      *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) =
+          kRad ? rademacher_quad(key, pair, step_lo, kk, law == kProbeRademacher) : gauss_quad(key, pair, step_lo, kk >> 2);
     }
     __syncthreads();
 #pragma unroll
@@ -667,7 +672,7 @@ __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, con
   __syncthreads();
 }
 
-template <int NB, int NCH>
+template <int NB, int NCH, bool kRad>
 __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
   constexpr int KQ = 4 * NCH;                           // 16-wide k groups: H = 64 NCH
   constexpr int NQ = NCH >= 4 ? 4 : NCH;                // staging quarters of K
@@ -710,7 +715,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 
     // Perturbed recurrent weights of this lane, drawn once for the sequence.
     float4 w[KQ];
-    resident_weights<KQ>(w, hs, th, a.off_l, in + H, in, H, utile * 128, key, pair, step_lo, seps);
+    resident_weights<KQ, true, kRad>(w, hs, th, a.off_l, in + H, in, H, utile * 128, a.probe, key, pair, step_lo, seps);
     // Rows past the batch compute on the last row's inputs and h (a column
     // of the product depends only on the same column of h, so no stored
     // output depends on them) and are never stored.  So the step has no
@@ -867,7 +872,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 // ---------------------------------------------------------------------------
 constexpr int kProjThreads = 512;
 
-template <int NCH>
+template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
   constexpr int KQ = 4 * NCH;                 // 16-wide k groups: K = H = 64 NCH
   constexpr int NQ = NCH >= 4 ? 4 : NCH;      // chunks per row tile
@@ -909,7 +914,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
       buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(static_cast<int64_t>(R) * H4 * sizeof(float)));
 
   float4 w[KQ];
-  resident_weights<KQ>(w, xs, th, a.off_l, a.in_l + H, 0, H, mb * 128, key, pair, step_lo, seps);
+  resident_weights<KQ, true, kRad>(w, xs, th, a.off_l, a.in_l + H, 0, H, mb * 128, a.probe, key, pair, step_lo, seps);
 
   // Chunk c covers rows [64 (c / NQ), +64) and k [QG 16 (c % NQ), +QG 16);
   // rows past R read row R - 1 and are never stored.
@@ -991,7 +996,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
 // that the loss reduction reads).
 // Partials: hpart[slot][half][R] float2 (m, s); htgt[slot][R].
 // ---------------------------------------------------------------------------
-template <int NCH>
+template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int nslots, float2* hpart, float* htgt) {
   constexpr int KQ = 4 * NCH;
   constexpr int NQ = NCH >= 4 ? 4 : NCH;
@@ -1035,7 +1040,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
   float* tg = htgt + slot * R;
 
   float4 w[KQ];
-  resident_weights<KQ, false>(w, xs, th, a.off_head, H, 0, H, vh * 128, key, pair, step_lo, seps);
+  resident_weights<KQ, false, kRad>(w, xs, th, a.off_head, H, 0, H, vh * 128, a.probe, key, pair, step_lo, seps);
 
   const int nchunks = ((R + 63) / 64) * NQ;
   float4 pre[PT];

@@ -1,4 +1,4 @@
-// soma_rng.hpp -- counter-based Gaussian probe generator for gfx950.
+// soma_rng.hpp -- counter-based probe generators for gfx950.
 //
 // z[k] for parameter k of direction j at step `step` of an expert with stream
 // seed `seed` is element k & 3 of gauss_quad(stream_key(seed, step), j,
@@ -132,6 +132,40 @@ __device__ __forceinline__ float4 gauss_quad(uint2 key, uint32_t pair, uint32_t 
   const float2 a = box_muller(w.x, w.y);
   const float2 b = box_muller(w.z, w.w);
   return make_float4(a.x, a.y, b.x, b.y);
+}
+
+// Probe laws.  Gaussian; sparse Rademacher, the paper's training law (each
+// coordinate 0 w.p. 1/2, -1 or +1 w.p. 1/4, Appendix E); dense Rademacher,
+// the law of its variance theory (Section 4; Appendix F).
+enum : int { kProbeGaussian = 0, kProbeSparseRademacher = 1, kProbeRademacher = 2 };
+
+// z[k4 .. k4+3] (k4 a multiple of 4) under a Rademacher law.  Coordinate k
+// reads the 2-bit field at bits 2 (k & 15) of word (k >> 4) & 3 of Philox
+// block k >> 6, counter (lo32(k >> 6), pair, lo32(step), hi32(k >> 6)): the
+// high bit makes a sparse coordinate active, the low bit is the sign (1: -1);
+// the dense law uses the sign bit alone.
+__device__ __forceinline__ float4 rademacher_quad(uint2 key, uint32_t pair, uint32_t step_lo, uint64_t k4,
+                                                  bool dense) {
+  const uint64_t b = k4 >> 6;
+  const uint4 w = philox4x32_10(
+      make_uint4(static_cast<uint32_t>(b), pair, step_lo, static_cast<uint32_t>(b >> 32)), key);
+  const uint32_t wi = static_cast<uint32_t>(k4 >> 4) & 3u;
+  const uint32_t word = wi == 0u ? w.x : (wi == 1u ? w.y : (wi == 2u ? w.z : w.w));
+  const uint32_t f8 = word >> (2u * (static_cast<uint32_t>(k4) & 15u));   // four 2-bit fields
+  float z[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t f = (f8 >> (2 * i)) & 3u;
+    const float sgn = (f & 1u) ? -1.0f : 1.0f;
+    z[i] = (dense || (f >> 1) != 0u) ? sgn : 0.0f;
+  }
+  return make_float4(z[0], z[1], z[2], z[3]);
+}
+
+// z[k4 .. k4+3] of direction `pair` under probe law `law` (k4 a multiple of 4).
+__device__ __forceinline__ float4 probe_quad(int law, uint2 key, uint32_t pair, uint32_t step_lo, uint64_t k4) {
+  if (law == kProbeGaussian) return gauss_quad(key, pair, step_lo, k4 >> 2);
+  return rademacher_quad(key, pair, step_lo, k4, law == kProbeRademacher);
 }
 
 }  // namespace soma

@@ -15,12 +15,13 @@ LIB_PATH = os.path.join(_PKG, "libsoma.so")
 
 SOMA_OK, SOMA_EINVAL, SOMA_ESHAPE, SOMA_EDEVICE, SOMA_EWORKSPACE = 0, -1, -2, -3, -4
 LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
+PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_eval_loss", "soma_coefficients", "soma_apply_update",
-           "soma_gaussian", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
+           "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
            "soma_get_phase_times",
            "soma_last_error")
 
@@ -44,7 +45,7 @@ class PhaseTimes(ctypes.Structure):
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "pair_chunk", "flags")]
+        "pair_chunk", "flags", "probe")]
 
 
 _lib = None
@@ -70,6 +71,7 @@ def load():
             "soma_coefficients": (ctypes.c_int, [vp, vp, vp]),
             "soma_apply_update": (ctypes.c_int, [vp, vp, vp, u64, f32, vp, vp]),
             "soma_gaussian": (ctypes.c_int, [u64, u64, u32, u64, u64, vp, vp]),
+            "soma_probe": (ctypes.c_int, [ctypes.c_int, u64, u64, u32, u64, u64, vp, vp]),
             "soma_philox": (ctypes.c_int, [vp, vp, vp, u64, vp]),
             "soma_box_muller": (ctypes.c_int, [vp, vp, vp, vp, u64, vp]),
             "soma_set_phase_timing": (ctypes.c_int, [vp, ctypes.c_int]),
@@ -118,10 +120,12 @@ class Shape:
     loss_mode: int = LOSS_INDEPENDENT
     pair_chunk: int = 0
     flags: int = 0
+    probe: int = PROBE_GAUSSIAN
 
     def cfg(self) -> Config:
         return Config(self.n_experts, self.n_layers, self.embed, self.hidden, self.batch,
-                      self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, self.flags)
+                      self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, self.flags,
+                      self.probe)
 
 
 def param_count(shape: Shape) -> int:
@@ -199,6 +203,12 @@ def gaussian(seed: int, step: int, pair: int, k0: int, out, stream=None):
     import torch
     _check(load().soma_gaussian(int(seed) & (2**64 - 1), int(step), int(pair), int(k0), out.numel(),
                                 _dptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def probe(law: int, seed: int, step: int, pair: int, k0: int, out, stream=None):
+    import torch
+    _check(load().soma_probe(int(law), int(seed) & (2**64 - 1), int(step), int(pair), int(k0), out.numel(),
+                             _dptr(out, torch.float32, "out"), _stream(stream)))
 
 
 def philox(ctr, key, out, stream=None):

@@ -59,7 +59,8 @@ def test_workspace_size_and_auto_chunk(lib):
 @pytest.mark.parametrize("field,value,code", [
     ("embed", 24, soma.SOMA_ESHAPE), ("hidden", 0, soma.SOMA_ESHAPE), ("seq_len", 1, soma.SOMA_ESHAPE),
     ("n_pairs", 0, soma.SOMA_ESHAPE), ("loss_mode", 2, soma.SOMA_EINVAL),
-    ("pair_chunk", 99, soma.SOMA_ESHAPE), ("flags", 4, soma.SOMA_EINVAL)])
+    ("pair_chunk", 99, soma.SOMA_ESHAPE), ("flags", 4, soma.SOMA_EINVAL), ("probe", 3, soma.SOMA_EINVAL),
+    ("probe", -1, soma.SOMA_EINVAL)])
 def test_invalid_shapes_are_rejected(lib, field, value, code):
     s = shape_of(workloads.TINY)
     cfg = s.cfg()
@@ -95,5 +96,7 @@ def test_step_rejects_bad_scalars_before_enqueueing(lib):
         assert lib.soma_coefficients(h, p, None) == soma.SOMA_EINVAL   # no step ran yet
         assert lib.soma_gaussian(0, 0, 0, 2**40, 1, p, None) == soma.SOMA_EINVAL
         assert lib.soma_gaussian(0, 0, 0, 0, 1, None, None) == soma.SOMA_EINVAL
+        assert lib.soma_probe(3, 0, 0, 0, 0, 1, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_probe(1, 0, 0, 0, 2**40, 1, p, None) == soma.SOMA_EINVAL
     finally:
         lib.soma_destroy(h)

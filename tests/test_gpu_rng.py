@@ -44,6 +44,38 @@ def test_gaussian_bit_exact(oracle_mod, seed, step, pair, k0, count):
     assert mism.size == 0, f"{mism.size} mismatches, first at {mism[:5]}: {got[mism[:5]]} vs {ref[mism[:5]]}"
 
 
+@pytest.mark.parametrize("law", [1, 2])
+@pytest.mark.parametrize("seed,step,pair,k0,count", [
+    (0x50A10000, 0, 0, 0, 1 << 22),                         # 4M consecutive probes
+    (0x50A10001, 0, 31, 4_456_448 - 5000, 5000),            # the end of a 4.46M-parameter expert
+    (0xDEADBEEF12345678, (1 << 33) + 5, 7, (1 << 34) + 3, 4099),  # high step/counter words, odd offset
+    (1, 0, 0, 61, 10),                                      # a start inside a 64-coordinate block
+])
+def test_rademacher_probes_bit_exact(oracle_mod, law, seed, step, pair, k0, count):
+    """Sparse (law 1, the paper's training law) and dense (law 2) Rademacher
+    probes from the 2-bit Philox fields, bit for bit."""
+    torch = require_gpu()
+    from paper_2609_37899_amd import soma
+    out = torch.empty(count, dtype=torch.float32, device="cuda")
+    soma.probe(law, seed, step, pair, k0, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = oracle_mod.probe(law, seed, step, pair, k0, count)
+    mism = np.flatnonzero(got.view(np.uint32) != ref.view(np.uint32))
+    assert mism.size == 0, f"{mism.size} mismatches, first at {mism[:5]}: {got[mism[:5]]} vs {ref[mism[:5]]}"
+
+
+def test_probe_law_0_is_the_gaussian_export():
+    torch = require_gpu()
+    from paper_2609_37899_amd import soma
+    a = torch.empty(4099, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    soma.probe(0, 9, 2, 3, 17, a)
+    soma.gaussian(9, 2, 3, 17, b)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
 def test_box_muller_exhaustive(oracle_mod):
     """Every radius input (all 2^24 values of wa >> 8) and every angle input
     (all 2^24 values of wb >> 8), bit for bit."""

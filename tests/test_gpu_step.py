@@ -20,10 +20,10 @@ CASES = {
 }
 
 
-def run_case(name, distinct=True, data=None):
+def run_case(name, distinct=True, data=None, probe=0):
     torch = require_gpu()
     N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
-    shape = soma.Shape(N, L, E, H, B, T, P, mode, pc)
+    shape = soma.Shape(N, L, E, H, B, T, P, mode, pc, probe=probe)
     theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=distinct)
     if data is None:
         data = synth.expert_batches([100 + e for e in range(N)], B, T)
@@ -43,7 +43,7 @@ def run_case(name, distinct=True, data=None):
 def oracle_step(oracle_mod, r):
     s = r["shape"]
     cfg = oracle_mod.make_cfg(s.n_experts, s.n_layers, s.embed, s.hidden, s.batch, s.seq_len,
-                              s.n_pairs, s.loss_mode)
+                              s.n_pairs, s.loss_mode, s.probe)
     return oracle_mod.spsa_step(cfg, r["theta0"], r["seeds"], 0, r["eps"], r["lr"], r["data"])
 
 
@@ -56,6 +56,20 @@ def test_step_matches_oracle(oracle_mod, name):
     uerr = update_rel_error(r["theta0"], r["theta"], o["theta"])
     cerr = np.abs(r["coef"] - o["coef"]).max() / np.abs(o["coef"]).max()
     print(f"{name}: loss rel {lerr:.2e}  theta rel {terr:.2e}  update rel {uerr:.2e}  coef rel {cerr:.2e}")
+    assert not np.array_equal(r["theta"], r["theta0"])
+
+
+@pytest.mark.parametrize("probe", [1, 2])
+@pytest.mark.parametrize("name", ["tiny", "ragged_l2_summed", "l3_b70", "b64_h128", "b40_h384"])
+def test_rademacher_step_matches_oracle(oracle_mod, name, probe):
+    """Whole steps under the paper's sparse Rademacher law (1) and the dense
+    law (2): the tiled kernels (H = 32, 80), the persistent recurrence and the
+    streaming projection and head (H = 64, 128, 384)."""
+    r = run_case(name, probe=probe)
+    o = oracle_step(oracle_mod, r)
+    lerr = assert_losses_close(r["losses"], o["losses"])
+    terr = assert_theta_close(r["theta"], o["theta"])
+    print(f"{name} law {probe}: loss rel {lerr:.2e}  theta rel {terr:.2e}")
     assert not np.array_equal(r["theta"], r["theta0"])
 
 
@@ -120,8 +134,9 @@ def test_chunking_does_not_change_the_result():
         assert np.array_equal(th, outs[0][0]) and np.array_equal(ls, outs[0][1])
 
 
-@pytest.mark.parametrize("name", ["tiny", "h512_short", "b64_h128", "b40_h384"])
-def test_persistent_and_per_step_recurrence_agree_bitwise(name):
+@pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("b64_h128", 0), ("b40_h384", 0),
+                                        ("b64_h128", 1)])
+def test_persistent_and_per_step_recurrence_agree_bitwise(name, probe):
     """The persistent recurrence (probe tile resident in LDS, group barriers)
     and the per-step launches accumulate in the same order: identical bits."""
     torch = require_gpu()
@@ -131,7 +146,7 @@ def test_persistent_and_per_step_recurrence_agree_bitwise(name):
     seeds = soma.seeds_tensor(synth.expert_seeds(N))
     outs = []
     for flags in (0, soma.FLAG_PER_STEP_RECURRENCE):
-        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags))
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags, probe))
         ctx.set_phase_timing(True)
         th = torch.from_numpy(theta.copy()).cuda()
         losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
@@ -149,8 +164,9 @@ def test_persistent_and_per_step_recurrence_agree_bitwise(name):
     assert np.array_equal(t0, t1)
 
 
-@pytest.mark.parametrize("name", ["tiny", "h512_short", "b64_h128", "b40_h384"])
-def test_streaming_and_tiled_weights_agree(name):
+@pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("b64_h128", 0), ("b40_h384", 0),
+                                        ("h512_short", 1), ("b40_h384", 2)])
+def test_streaming_and_tiled_weights_agree(name, probe):
     """The streaming projection and head (weights resident in registers,
     probes drawn once per 128 weight rows) against the tiled kernels (probes
     regenerated per row tile).  The projections sum over k in the same order;
@@ -166,7 +182,7 @@ def test_streaming_and_tiled_weights_agree(name):
     seeds = soma.seeds_tensor(synth.expert_seeds(N))
     outs = []
     for flags in (0, soma.FLAG_TILED_WEIGHTS):
-        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags))
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags, probe))
         th = torch.from_numpy(theta.copy()).cuda()
         losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
         ctx.spsa_step(th, seeds, 3, eps, lr, torch.from_numpy(data).cuda(), losses)
