@@ -77,6 +77,10 @@ def _load():
                 "oracle_apply_update": (None, [cfgp, f32p, ctypes.c_uint64, ctypes.c_uint64,
                                                ctypes.c_float, f64p, i64p, ctypes.c_int64,
                                                f32p, f64p]),
+                "oracle_apply_adam": (None, [cfgp, f32p, f32p, f32p, ctypes.c_int64, ctypes.c_uint64,
+                                             ctypes.c_uint64, ctypes.c_float, f64p, ctypes.c_double,
+                                             ctypes.c_double, ctypes.c_double, ctypes.c_double, i64p,
+                                             ctypes.c_int64, f32p, f32p, f32p, f64p]),
                 "oracle_spsa_step": (ctypes.c_int, [cfgp, f32p, u64p, ctypes.c_uint64,
                                                     ctypes.c_float, ctypes.c_float, u8p, f32p,
                                                     f64p, f32p, f64p]),
@@ -242,6 +246,35 @@ def apply_update(cfg: OracleCfg, theta_e: np.ndarray, seed: int, step: int, lr: 
                                 _ptr(out, ctypes.c_float),
                                 _ptr(gh, ctypes.c_double) if want_ghat else None)
     return (out, gh) if want_ghat else out
+
+
+ADAM_DEFAULTS = dict(beta1=0.9, beta2=0.999, delta=1e-8, weight_decay=1e-4)
+
+
+def apply_adam(cfg: OracleCfg, theta_e, m_e, v_e, t: int, seed: int, step: int, lr: float, coef,
+               beta1=0.9, beta2=0.999, delta=1e-8, weight_decay=1e-4, ks=None, want_ghat=False):
+    """The paper's Adam-style update of one expert (update number t >= 1)
+    from the coefficients coef[j]; returns (theta', m', v'[, g_hat])."""
+    th = np.ascontiguousarray(theta_e, dtype=np.float32)
+    m = np.ascontiguousarray(m_e, dtype=np.float32)
+    v = np.ascontiguousarray(v_e, dtype=np.float32)
+    cf = np.ascontiguousarray(coef, dtype=np.float64)
+    if ks is None:
+        n, kp = th.size, None
+    else:
+        kk = np.ascontiguousarray(ks, dtype=np.int64)
+        n, kp = kk.size, _ptr(kk, ctypes.c_int64)
+    to = np.empty(n, np.float32)
+    mo = np.empty(n, np.float32)
+    vo = np.empty(n, np.float32)
+    gh = np.empty(n, np.float64) if want_ghat else None
+    _load().oracle_apply_adam(ctypes.byref(cfg), _ptr(th, ctypes.c_float), _ptr(m, ctypes.c_float),
+                              _ptr(v, ctypes.c_float), int(t), int(seed), int(step), float(lr),
+                              _ptr(cf, ctypes.c_double), float(beta1), float(beta2), float(delta),
+                              float(weight_decay), kp, n, _ptr(to, ctypes.c_float),
+                              _ptr(mo, ctypes.c_float), _ptr(vo, ctypes.c_float),
+                              _ptr(gh, ctypes.c_double) if want_ghat else None)
+    return (to, mo, vo, gh) if want_ghat else (to, mo, vo)
 
 
 def spsa_step(cfg: OracleCfg, theta: np.ndarray, seeds, step: int, eps: float, lr: float,

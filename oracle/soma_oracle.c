@@ -446,7 +446,41 @@ void oracle_apply_update(const oracle_cfg *c, const float *theta, uint64_t seed,
   }
 }
 
-/* One SPSA step for all experts.
+/* The paper's update (Appendix E, Eq. localspsa, with coupled weight decay):
+ *   g  = g_hat + lambda theta                    (decay added before the moments)
+ *   m' = beta1 m + (1 - beta1) g,   v' = beta2 v + (1 - beta2) g^2
+ *   theta' = theta - lr (m' / (1 - beta1^t)) / (sqrt(v' / (1 - beta2^t)) + delta)
+ * for update number t >= 1, g_hat[k] = sum_j coef[j] z_j[k] (j order).  All
+ * arithmetic in fp64; theta', m', v' rounded once to fp32.  Coordinates as
+ * in oracle_apply_update (ks / nk); ghat (may be NULL) receives g_hat. */
+void oracle_apply_adam(const oracle_cfg *c, const float *theta, const float *m, const float *v, int64_t t,
+                       uint64_t seed, uint64_t step, float lr, const double *coef, double beta1,
+                       double beta2, double delta, double lambda, const int64_t *ks, int64_t nk,
+                       float *theta_out, float *m_out, float *v_out, double *ghat) {
+  const int P = c->n_pairs;
+  const int64_t n = ks ? nk : oracle_param_count(c);
+  const double bc1 = 1.0 - pow(beta1, (double)t), bc2 = 1.0 - pow(beta2, (double)t);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t k = ks ? ks[i] : i;
+    double gh = 0.0;
+    for (int j = 0; j < P; ++j) {
+      float z[4];
+      probe_quad(c->probe, seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
+      gh += coef[j] * (double)z[k & 3];
+    }
+    const double th = (double)theta[k];
+    const double g = gh + lambda * th;
+    const double m1 = beta1 * (double)m[k] + (1.0 - beta1) * g;
+    const double v1 = beta2 * (double)v[k] + (1.0 - beta2) * g * g;
+    theta_out[i] = (float)(th - (double)lr * (m1 / bc1) / (sqrt(v1 / bc2) + delta));
+    m_out[i] = (float)m1;
+    v_out[i] = (float)v1;
+    if (ghat) ghat[i] = gh;
+  }
+}
+
+/* One SPSA step for all experts./* One SPSA step for all experts.
  *   theta   [N][d]   fp32, read only
  *   seeds   [N]      per-expert Philox stream seeds
  *   bytes   [N][B][T]
