@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--workload", default="soma_n2_l2_h512")
     ap.add_argument("--pairs", type=int, default=0, help="override the workload's directions per expert")
     ap.add_argument("--pair-chunk", type=int, default=0)
+    ap.add_argument("--optimizer", choices=("sgd", "adam"), default="sgd",
+                    help="update: the plain step on the estimate, or the paper's Adam-style update "
+                         "(beta 0.9/0.999, delta 1e-8, coupled decay 1e-4) with fp32 moments")
     ap.add_argument("--probe", choices=sorted(PROBE_LAWS), default="gaussian",
                     help="probe law: gaussian (the workload's), sparse (the paper's training law: "
                          "0 w.p. 1/2, +-1 w.p. 1/4) or dense (+-1)")
@@ -162,10 +165,21 @@ def main():
     seeds = soma.seeds_tensor(seeds_np, dev)
     dbatches = [torch.from_numpy(b).to(dev) for b in batches]
     losses = torch.zeros((w.n_experts, w.n_pairs, 2), dtype=torch.float32, device=dev)
+    if args.optimizer == "adam":
+        m_state = torch.zeros_like(theta)
+        v_state = torch.zeros_like(theta)
+        adam = soma.Adam()
+
+    def one_step(i):
+        if args.optimizer == "adam":
+            ctx.spsa_step_adam(theta, m_state, v_state, i + 1, adam, seeds, i, w.eps, w.lr,
+                               dbatches[i % nb], losses)
+        else:
+            ctx.spsa_step(theta, seeds, i, w.eps, w.lr, dbatches[i % nb], losses)
     torch.cuda.synchronize()
 
     for i in range(args.warmup):
-        ctx.spsa_step(theta, seeds, i, w.eps, w.lr, dbatches[i % nb], losses)
+        one_step(i)
     torch.cuda.synchronize()
 
     ctx.set_phase_timing(True)
@@ -173,7 +187,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        ctx.spsa_step(theta, seeds, args.warmup + i, w.eps, w.lr, dbatches[(args.warmup + i) % nb], losses)
+        one_step(args.warmup + i)
         pt = ctx.phase_times()          # waits for this step's last event
         for k, v in pt.items():
             phases[k] = phases.get(k, 0) + v
@@ -232,7 +246,7 @@ def main():
                    "n_pairs": w.n_pairs, "forwards_per_expert": 2 * w.n_pairs,
                    "params_per_expert": w.params_per_expert, "eps": w.eps, "lr": w.lr,
                    "loss_mode": "summed" if w.loss_mode else "independent",
-                   "probe": args.probe,
+                   "probe": args.probe, "optimizer": args.optimizer,
                    "parallelism": "single GPU, all experts and directions in each launch"},
         "algorithmic_tflops": round(total_flops / sec / 1e12, 3),
         "phase_ms": {k: round(v, 3) for k, v in ms.items()},

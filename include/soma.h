@@ -161,6 +161,39 @@ void soma_destroy(soma_ctx* ctx);
 int soma_spsa_step(soma_ctx* ctx, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,
                    float eps, float lr, const uint8_t* bytes_dev, float* losses_dev, void* stream);
 
+/* Adam hyperparameters of the paper's update (Appendix E, Eq. localspsa;
+ * the paper uses beta1 = 0.9, beta2 = 0.999, delta = 1e-8 and coupled weight
+ * decay 1e-4).  beta1, beta2 in [0, 1); delta finite and > 0; weight_decay
+ * finite. */
+typedef struct soma_adam {
+  float beta1;
+  float beta2;
+  float delta;         /* stabiliser added to sqrt(v_hat) */
+  float weight_decay;  /* lambda: lambda theta is added to the estimate before the moments */
+} soma_adam;
+
+/* One SPSA step with the paper's Adam-style update instead of the plain
+ * one (steps 1-3 as soma_spsa_step, then for every coordinate)
+ *   g = g_hat + lambda theta,  g_hat = sum_j c_{e,j} z_{e,j} (j order, fp32),
+ *   m <- beta1 m + (1 - beta1) g,   v <- beta2 v + (1 - beta2) g^2,
+ *   theta <- theta - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + delta).
+ *   m_dev, v_dev  [N][d] fp32 moment buffers (caller owned, 16-byte aligned,
+ *                 zero before the first update), updated in place.
+ *   t             the update number, >= 1 (the bias corrections' exponent).
+ *   hp            host pointer to the hyperparameters.
+ * Other arguments, errors and atomicity as soma_spsa_step: theta, m and v
+ * are written only by the final update kernel, and an aborted step leaves
+ * all three untouched. */
+int soma_spsa_step_adam(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_dev, int64_t t,
+                        const soma_adam* hp, const uint64_t* seeds_dev, uint64_t step, float eps, float lr,
+                        const uint8_t* bytes_dev, float* losses_dev, void* stream);
+
+/* The Adam update of soma_spsa_step_adam alone, for given coefficients
+ * coef_dev [N][P] fp32 (device). */
+int soma_apply_adam(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_dev, int64_t t,
+                    const soma_adam* hp, const uint64_t* seeds_dev, uint64_t step, float lr,
+                    const float* coef_dev, void* stream);
+
 /* Unperturbed mean cross entropy of every expert on its own batch
  * (Appendix E, L_CE; the expert validation loss of Section 6).
  *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8, loss_dev [N] fp32 out. */

@@ -233,8 +233,20 @@ __global__ void k_coef(const double* lossd, int N, int P, int summed, double inv
   coef[i] = static_cast<float>(diff * inv_denom);
 }
 
+// g_hat[4q .. 4q+3] = sum_{j<P} coef[j] z_j[4q .. 4q+3] of one expert, summed
+// in j order in fp32 (each z regenerated from its counter).
+__device__ __forceinline__ float4 estimate_quad(uint2 key, uint32_t step_lo, const float* coef, int P, int law,
+                                                int64_t q) {
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < P; ++j) {
+    const float4 z = probe_quad(law, key, static_cast<uint32_t>(j), step_lo, 4 * static_cast<uint64_t>(q));
+    acc = fma4(coef[j], z, acc);
+  }
+  return acc;
+}
+
 // theta[e][k] -= lr * sum_{j<P} coef[e][j] z_{e,j}[k], one probe quad per
-// thread and direction; the sum runs in j order in fp32.
+// thread (Section 4, Eq. main-spsa; the plain step on the estimate).
 __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* seeds, uint64_t step,
                                                  float lr, const float* coef, int64_t d, int P, int law,
                                                  const unsigned* err) {
@@ -242,15 +254,8 @@ __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* se
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
   if (err && *err) return;   // the step was aborted: theta stays as it was
-  const uint2 key = stream_key(seeds[e], step);
-  const uint32_t step_lo = static_cast<uint32_t>(step);
-  const float* c = coef + int64_t(e) * P;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < P; ++j) {
-    const float cj = c[j];
-    const float4 z = probe_quad(law, key, static_cast<uint32_t>(j), step_lo, 4 * static_cast<uint64_t>(q));
-    acc = fma4(cj, z, acc);
-  }
+  const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
+                                   coef + int64_t(e) * P, P, law, q);
   float* t = theta + int64_t(e) * d + 4 * q;
   if (4 * q + 4 <= d) {
     float4 v = *reinterpret_cast<float4*>(t);
@@ -259,6 +264,41 @@ __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* se
   } else {
     const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
     for (int i = 0; 4 * q + i < d; ++i) t[i] = __builtin_fmaf(-lr, a4[i], t[i]);
+  }
+}
+
+// Adam hyperparameters in the form the kernel uses (fp32): bc1 = 1 - beta1^t,
+// bc2 = 1 - beta2^t, omb1 = 1 - beta1, omb2 = 1 - beta2 (computed in fp64 on
+// the host, rounded once).
+struct AdamArgs {
+  float lr, beta1, beta2, omb1, omb2, bc1, bc2, delta, lambda;
+};
+
+// The paper's update with coupled weight decay (Appendix E, Eq. localspsa):
+//   g = g_hat + lambda theta;  m' = beta1 m + (1 - beta1) g;
+//   v' = beta2 v + (1 - beta2) g^2;
+//   theta' = theta - lr (m' / bc1) / (sqrt(v' / bc2) + delta).
+// theta, m, v [N][d] fp32 in place, one probe quad per thread.
+__global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, float* v, const uint64_t* seeds,
+                                                      uint64_t step, AdamArgs h, const float* coef, int64_t d,
+                                                      int P, int law, const unsigned* err) {
+  const int e = blockIdx.y;
+  const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
+  if (4 * q >= d) return;
+  if (err && *err) return;   // the step was aborted: theta, m, v stay as they were
+  const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
+                                   coef + int64_t(e) * P, P, law, q);
+  const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
+  const int64_t base = int64_t(e) * d + 4 * q;
+  for (int i = 0; i < 4 && 4 * q + i < d; ++i) {
+    const float th = theta[base + i];
+    const float g = __builtin_fmaf(h.lambda, th, a4[i]);
+    const float m1 = __builtin_fmaf(h.beta1, m[base + i], h.omb1 * g);
+    const float v1 = __builtin_fmaf(h.beta2, v[base + i], h.omb2 * (g * g));
+    const float r = (m1 / h.bc1) / (sqrtf(v1 / h.bc2) + h.delta);
+    theta[base + i] = __builtin_fmaf(-h.lr, r, th);
+    m[base + i] = m1;
+    v[base + i] = v1;
   }
 }
 
@@ -617,17 +657,28 @@ int soma_get_phase_times(soma_ctx* ctx, soma_phase_times* out) {
   return ok();
 }
 
-int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, float eps,
-                   float lr, const uint8_t* bytes, float* losses, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Arguments of a step that both updates check.
+int check_step_args(soma_ctx* ctx, const float* theta, const uint64_t* seeds, const uint8_t* bytes,
+                    const float* losses, float eps, float lr) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
   if (!theta || !seeds || !bytes || !losses) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
   if (!aligned(seeds, 8) || !aligned(losses, 4)) return fail(SOMA_EINVAL, "misaligned seeds or losses");
   if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(SOMA_EINVAL, "eps must be finite and > 0");
   if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
+  return SOMA_OK;
+}
+
+// Steps 1-3 of the method: every perturbed forward, the losses and the
+// coefficients (in the workspace).  Returns the step's abort flag.
+int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, float eps,
+                              const uint8_t* bytes, float* losses, hipStream_t st, unsigned** err_out) {
   const soma_config& c = ctx->cfg;
   const Layout& L = ctx->lay;
-  const hipStream_t st = as_stream(stream);
   ctx->nmarks = 0;
   ctx->rec_launches = ctx->proj_launches = 0;
   ctx->have_times = false;
@@ -655,6 +706,59 @@ int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t 
                      c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, inv_denom, coef);
   if (int rc = check_launch("k_coef")) return rc;
   if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
+  *err_out = err;
+  return SOMA_OK;
+}
+
+// Adam hyperparameters checked and converted for update number t.
+int adam_args(const soma_adam* hp, int64_t t, float lr, soma::AdamArgs* out) {
+  if (!hp) return fail(SOMA_EINVAL, "adam hyperparameters are NULL");
+  if (t < 1) return fail(SOMA_EINVAL, "the update number t must be >= 1");
+  if (!(hp->beta1 >= 0.0f && hp->beta1 < 1.0f) || !(hp->beta2 >= 0.0f && hp->beta2 < 1.0f))
+    return fail(SOMA_EINVAL, "beta1 and beta2 must lie in [0, 1)");
+  if (!(hp->delta > 0.0f) || !std::isfinite(hp->delta)) return fail(SOMA_EINVAL, "delta must be finite and > 0");
+  if (!std::isfinite(hp->weight_decay)) return fail(SOMA_EINVAL, "weight_decay must be finite");
+  if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
+  const double b1 = hp->beta1, b2 = hp->beta2;
+  out->lr = lr;
+  out->beta1 = hp->beta1;
+  out->beta2 = hp->beta2;
+  out->omb1 = static_cast<float>(1.0 - b1);
+  out->omb2 = static_cast<float>(1.0 - b2);
+  out->bc1 = static_cast<float>(1.0 - std::pow(b1, double(t)));
+  out->bc2 = static_cast<float>(1.0 - std::pow(b2, double(t)));
+  out->delta = hp->delta;
+  out->lambda = hp->weight_decay;
+  return SOMA_OK;
+}
+
+int check_state(const float* m, const float* v) {
+  if (!m || !v) return fail(SOMA_EINVAL, "NULL moment buffer");
+  if (!aligned(m, 16) || !aligned(v, 16)) return fail(SOMA_EINVAL, "m and v must be 16-byte aligned");
+  return SOMA_OK;
+}
+
+void launch_adam(const soma_ctx* ctx, float* theta, float* m, float* v, const uint64_t* seeds, uint64_t step,
+                 const soma::AdamArgs& h, const float* coef, const unsigned* err, hipStream_t st) {
+  const soma_config& c = ctx->cfg;
+  const int64_t quads = (ctx->lay.d + 3) / 4;
+  hipLaunchKernelGGL(soma::k_update_adam, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
+                     theta, m, v, seeds, step, h, coef, ctx->lay.d, c.n_pairs, c.probe, err);
+}
+
+}  // namespace
+
+extern "C" {
+
+int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, float eps,
+                   float lr, const uint8_t* bytes, float* losses, void* stream) {
+  if (int rc = check_step_args(ctx, theta, seeds, bytes, losses, eps, lr)) return rc;
+  const soma_config& c = ctx->cfg;
+  const Layout& L = ctx->lay;
+  const hipStream_t st = as_stream(stream);
+  unsigned* err = nullptr;
+  if (int rc = forwards_and_coefficients(ctx, theta, seeds, step, eps, bytes, losses, st, &err)) return rc;
+  const float* coef = reinterpret_cast<const float*>(ctx->ws + L.coef);
   const int64_t quads = (L.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
                      st, theta, seeds, step, lr, coef, L.d, c.n_pairs, c.probe, err);
@@ -662,6 +766,37 @@ int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t 
   if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
   ctx->have_coef = true;
   ctx->have_times = ctx->timing;
+  return ok();
+}
+
+int soma_spsa_step_adam(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, const soma_adam* hp,
+                        const uint64_t* seeds, uint64_t step, float eps, float lr, const uint8_t* bytes,
+                        float* losses, void* stream) {
+  if (int rc = check_step_args(ctx, theta, seeds, bytes, losses, eps, lr)) return rc;
+  if (int rc = check_state(m, v)) return rc;
+  soma::AdamArgs h{};
+  if (int rc = adam_args(hp, t, lr, &h)) return rc;
+  const hipStream_t st = as_stream(stream);
+  unsigned* err = nullptr;
+  if (int rc = forwards_and_coefficients(ctx, theta, seeds, step, eps, bytes, losses, st, &err)) return rc;
+  launch_adam(ctx, theta, m, v, seeds, step, h, reinterpret_cast<const float*>(ctx->ws + ctx->lay.coef), err, st);
+  if (int rc = check_launch("k_update_adam")) return rc;
+  if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
+  ctx->have_coef = true;
+  ctx->have_times = ctx->timing;
+  return ok();
+}
+
+int soma_apply_adam(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, const soma_adam* hp,
+                    const uint64_t* seeds, uint64_t step, float lr, const float* coef, void* stream) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (!theta || !seeds || !coef) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
+  if (int rc = check_state(m, v)) return rc;
+  soma::AdamArgs h{};
+  if (int rc = adam_args(hp, t, lr, &h)) return rc;
+  launch_adam(ctx, theta, m, v, seeds, step, h, coef, nullptr, as_stream(stream));
+  if (int rc = check_launch("k_update_adam")) return rc;
   return ok();
 }
 

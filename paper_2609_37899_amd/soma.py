@@ -20,7 +20,8 @@ FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
-           "soma_spsa_step", "soma_eval_loss", "soma_coefficients", "soma_apply_update",
+           "soma_spsa_step", "soma_spsa_step_adam", "soma_eval_loss", "soma_coefficients",
+           "soma_apply_update", "soma_apply_adam",
            "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
            "soma_get_phase_times",
            "soma_last_error")
@@ -40,6 +41,15 @@ class PhaseTimes(ctypes.Structure):
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class Adam(ctypes.Structure):
+    """soma_adam; the defaults are the paper's (Appendix E)."""
+    _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("delta", ctypes.c_float),
+                ("weight_decay", ctypes.c_float)]
+
+    def __init__(self, beta1=0.9, beta2=0.999, delta=1e-8, weight_decay=1e-4):
+        super().__init__(beta1, beta2, delta, weight_decay)
 
 
 class Config(ctypes.Structure):
@@ -67,6 +77,10 @@ def load():
             "soma_create": (ctypes.c_int, [cp, vp, ctypes.c_size_t, ctypes.POINTER(vp)]),
             "soma_destroy": (None, [vp]),
             "soma_spsa_step": (ctypes.c_int, [vp, vp, vp, u64, f32, f32, vp, vp, vp]),
+            "soma_spsa_step_adam": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam),
+                                                   vp, u64, f32, f32, vp, vp, vp]),
+            "soma_apply_adam": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam), vp,
+                                               u64, f32, vp, vp]),
             "soma_eval_loss": (ctypes.c_int, [vp, vp, vp, vp, vp]),
             "soma_coefficients": (ctypes.c_int, [vp, vp, vp]),
             "soma_apply_update": (ctypes.c_int, [vp, vp, vp, u64, f32, vp, vp]),
@@ -173,6 +187,23 @@ class Context:
                                      _dptr(seeds, torch.int64, "seeds"), int(step), float(eps),
                                      float(lr), _dptr(bytes_, torch.uint8, "bytes"),
                                      _dptr(losses, torch.float32, "losses"), _stream(stream)))
+
+    def spsa_step_adam(self, theta, m, v, t: int, adam, seeds, step: int, eps: float, lr: float, bytes_,
+                       losses, stream=None):
+        import torch
+        _check(load().soma_spsa_step_adam(self._h, _dptr(theta, torch.float32, "theta"),
+                                          _dptr(m, torch.float32, "m"), _dptr(v, torch.float32, "v"),
+                                          int(t), ctypes.byref(adam), _dptr(seeds, torch.int64, "seeds"),
+                                          int(step), float(eps), float(lr),
+                                          _dptr(bytes_, torch.uint8, "bytes"),
+                                          _dptr(losses, torch.float32, "losses"), _stream(stream)))
+
+    def apply_adam(self, theta, m, v, t: int, adam, seeds, step: int, lr: float, coef, stream=None):
+        import torch
+        _check(load().soma_apply_adam(self._h, _dptr(theta, torch.float32, "theta"),
+                                      _dptr(m, torch.float32, "m"), _dptr(v, torch.float32, "v"), int(t),
+                                      ctypes.byref(adam), _dptr(seeds, torch.int64, "seeds"), int(step),
+                                      float(lr), _dptr(coef, torch.float32, "coef"), _stream(stream)))
 
     def set_phase_timing(self, enable: bool = True):
         _check(load().soma_set_phase_timing(self._h, 1 if enable else 0))

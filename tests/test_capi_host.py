@@ -98,5 +98,16 @@ def test_step_rejects_bad_scalars_before_enqueueing(lib):
         assert lib.soma_gaussian(0, 0, 0, 0, 1, None, None) == soma.SOMA_EINVAL
         assert lib.soma_probe(3, 0, 0, 0, 0, 1, p, None) == soma.SOMA_EINVAL
         assert lib.soma_probe(1, 0, 0, 0, 2**40, 1, p, None) == soma.SOMA_EINVAL
+        good = soma.Adam()
+        assert lib.soma_apply_adam(h, p, p, p, 0, ctypes.byref(good), p, 0, 1e-3, p, None) == soma.SOMA_EINVAL
+        for bad in (soma.Adam(beta1=1.0), soma.Adam(beta2=-0.1), soma.Adam(delta=0.0),
+                    soma.Adam(weight_decay=float("nan"))):
+            assert lib.soma_apply_adam(h, p, p, p, 1, ctypes.byref(bad), p, 0, 1e-3, p, None) == soma.SOMA_EINVAL
+            assert lib.soma_spsa_step_adam(h, p, p, p, 1, ctypes.byref(bad), p, 0, 1e-3, 1e-3, p, p,
+                                           None) == soma.SOMA_EINVAL
+        assert lib.soma_apply_adam(h, p, None, p, 1, ctypes.byref(good), p, 0, 1e-3, p, None) == soma.SOMA_EINVAL
+        assert lib.soma_apply_adam(h, p, p, ctypes.c_void_p(0x200008), 1, ctypes.byref(good), p, 0, 1e-3, p,
+                                   None) == soma.SOMA_EINVAL
+        assert lib.soma_apply_adam(h, p, p, p, 1, None, p, 0, 1e-3, p, None) == soma.SOMA_EINVAL
     finally:
         lib.soma_destroy(h)

@@ -193,3 +193,45 @@ def test_streaming_and_tiled_weights_agree(name, probe):
     rel = np.abs(l0.astype(np.float64) - l1) / np.abs(l1)
     assert rel.max() <= 1e-6, rel.max()
     assert_theta_close(t0, t1)
+
+
+@pytest.mark.parametrize("name,probe", [("ragged_l2", 1), ("b64_h128", 0)])
+def test_adam_step_matches_oracle(oracle_mod, name, probe):
+    """A whole step with the Adam-style update from zero moments: losses and
+    coefficients against the oracle's step; theta', m', v' against the
+    oracle's update applied to the GPU's coefficients (so that fp32 forward
+    noise in L+ - L- does not enter the comparison of the update)."""
+    from test_gpu_update import _adam_compare
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
+    shape = soma.Shape(N, L, E, H, B, T, P, mode, pc, probe=probe)
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = synth.expert_seeds(N)
+    adam = soma.Adam()
+    ctx = soma.Context(shape)
+    th = torch.from_numpy(theta.copy()).cuda()
+    m = torch.zeros_like(th)
+    v = torch.zeros_like(th)
+    losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+    ctx.spsa_step_adam(th, m, v, 1, adam, soma.seeds_tensor(seeds), 0, eps, lr, torch.from_numpy(data).cuda(),
+                       losses)
+    coef = torch.zeros((N, P), dtype=torch.float32, device="cuda")
+    ctx.coefficients(coef)
+    torch.cuda.synchronize()
+    r = dict(theta0=theta, data=data, seeds=seeds, shape=shape, eps=eps, lr=lr)
+    o = oracle_step(oracle_mod, r)
+    assert_losses_close(losses.cpu().numpy(), o["losses"])
+    cg = coef.cpu().numpy()
+    assert np.abs(cg - o["coef"]).max() <= 2e-2 * np.abs(o["coef"]).max()
+    cfg = oracle_mod.cfg_from(shape)
+    hp = dict(beta1=float(adam.beta1), beta2=float(adam.beta2), delta=float(adam.delta),
+              weight_decay=float(adam.weight_decay))
+    got = [x.cpu().numpy() for x in (th, m, v)]
+    for e in range(N):
+        to, mo, vo, gh = oracle_mod.apply_adam(cfg, theta[e], np.zeros_like(theta[e]), np.zeros_like(theta[e]), 1,
+                                               int(seeds[e]), 0, float(np.float32(lr)), cg[e].astype(np.float64),
+                                               want_ghat=True, **hp)
+        g = gh + hp["weight_decay"] * theta[e].astype(np.float64)
+        _adam_compare([x[e] for x in got], (to, mo, vo), theta[e].astype(np.float64), g, float(np.float32(lr)),
+                      1, True)
