@@ -194,6 +194,50 @@ int soma_apply_adam(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_dev,
                     const soma_adam* hp, const uint64_t* seeds_dev, uint64_t step, float lr,
                     const float* coef_dev, void* stream);
 
+/* Per-expert learning rate and perturbation radius under the paper's
+ * plateau schedule (Section 4; Table experimental-setup: lr and eps start at
+ * 1e-3 and are halved together after 1,000 updates without an improvement of
+ * the expert's validation loss by more than 1e-8, never below 1e-5).  The
+ * state lives in device memory, [N] entries owned by the caller, so a
+ * training loop of steps, evaluations and schedule updates needs no host
+ * round trip. */
+typedef struct soma_schedule_entry {
+  float lr;        /* the expert's current learning rate */
+  float eps;       /* the expert's current perturbation radius */
+  float best;      /* best validation loss observed (+inf before the first) */
+  int32_t since;   /* updates since the last improvement or decay */
+} soma_schedule_entry;
+
+typedef struct soma_plateau {
+  float factor;      /* decay factor in (0, 1): 0.5 */
+  int32_t patience;  /* updates without improvement before a decay, >= 1: 1000 */
+  float threshold;   /* an improvement must lower the loss by more than this: 1e-8 */
+  float floor;       /* lr and eps are not decayed below this: 1e-5 */
+} soma_plateau;
+
+/* Set sched_dev[0..n) to (lr0, eps0, +inf, 0).  eps0 finite and > 0. */
+int soma_schedule_init(soma_schedule_entry* sched_dev, int32_t n, float lr0, float eps0, void* stream);
+
+/* One observation of the validation losses val_loss_dev [n] fp32 (device,
+ * e.g. from soma_eval_loss), `updates` updates after the previous one: for
+ * every expert, if val < best - threshold (compared in fp64) then best = val
+ * and since = 0, else since += updates; then if since >= patience, lr and eps
+ * become min(x, max(x * factor, floor)) and since = 0.  A NaN loss counts as
+ * no improvement. */
+int soma_schedule_observe(soma_schedule_entry* sched_dev, int32_t n, const float* val_loss_dev, int32_t updates,
+                          const soma_plateau* rule, void* stream);
+
+/* soma_spsa_step_adam with each expert's eps and lr read from its schedule
+ * entry, sched_dev [N] (device).  The coefficients use the expert's own
+ * radius, c_{e,j} = (L+ - L-) / (2 eps_e P); in SUMMED mode
+ * c_j = sum_e (L_{e,j,+} - L_{e,j,-}) / (2 eps_e P).  A step with an entry
+ * whose eps is not finite and > 0 or whose lr is not finite is aborted on the
+ * device: its losses read NaN and theta, m and v stay untouched. */
+int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_dev, int64_t t,
+                              const soma_adam* hp, const uint64_t* seeds_dev, uint64_t step,
+                              const soma_schedule_entry* sched_dev, const uint8_t* bytes_dev,
+                              float* losses_dev, void* stream);
+
 /* Unperturbed mean cross entropy of every expert on its own batch
  * (Appendix E, L_CE; the expert validation loss of Section 6).
  *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8, loss_dev [N] fp32 out. */

@@ -17,6 +17,8 @@ import threading
 
 import numpy as np
 
+from .plateau import Plateau  # noqa: F401  (the lr / eps schedule, plain Python)
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "soma_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")

@@ -56,7 +56,8 @@ struct Layout {
   int64_t off_head = 0;
   int pc = 0;          // directions per pass
   int row_tiles = 0;   // head tiles per slot
-  size_t sync = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, hpart = 0, htgt = 0, total = 0;
+  size_t sync = 0, rates = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, hpart = 0, htgt = 0,
+         total = 0;
 };
 
 int64_t param_count_of(const soma_config& c) {
@@ -106,6 +107,7 @@ Layout layout_for(const soma_config& c, int pc) {
   const size_t slots = N * size_t(pc) * 2;
   size_t at = 0;
   L.sync = at; at += round_up(sizeof(unsigned) * (kMaxGroups + 1));
+  L.rates = at; at += round_up(sizeof(float) * 2 * N);            // eps[N], lr[N] of a scalar-rate step
   L.coef = at; at += round_up(sizeof(float) * N * c.n_pairs);
   L.lossd = at; at += round_up(sizeof(double) * N * c.n_pairs * 2);
   L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
@@ -219,18 +221,42 @@ __global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs,
 // c[e][j] = (L+ - L-) / (2 eps P) from the fp64 means, rounded once to fp32;
 // summed mode: the differences of all experts added in expert order, the
 // same coefficient for every expert.
-__global__ void k_coef(const double* lossd, int N, int P, int summed, double inv_denom, float* coef) {
+__global__ void k_coef(const double* lossd, int N, int P, int summed, const float* eps_v, int eps_stride,
+                       float* coef) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= N * P) return;
   const int j = i % P, e = i / P;
-  double diff;
+  auto inv_denom = [&](int x) { return 1.0 / (2.0 * double(eps_v[int64_t(x) * eps_stride]) * double(P)); };
+  double c;
   if (summed) {
-    diff = 0.0;
-    for (int e2 = 0; e2 < N; ++e2) diff += lossd[(int64_t(e2) * P + j) * 2] - lossd[(int64_t(e2) * P + j) * 2 + 1];
+    c = 0.0;
+    for (int e2 = 0; e2 < N; ++e2)
+      c += (lossd[(int64_t(e2) * P + j) * 2] - lossd[(int64_t(e2) * P + j) * 2 + 1]) * inv_denom(e2);
   } else {
-    diff = lossd[(int64_t(e) * P + j) * 2] - lossd[(int64_t(e) * P + j) * 2 + 1];
+    c = (lossd[(int64_t(e) * P + j) * 2] - lossd[(int64_t(e) * P + j) * 2 + 1]) * inv_denom(e);
   }
-  coef[i] = static_cast<float>(diff * inv_denom);
+  coef[i] = static_cast<float>(c);
+}
+
+// Per-expert rates of a step given as scalars: eps_v[e] = eps, lr_v[e] = lr.
+__global__ void k_fill_rates(float* eps_v, float* lr_v, int N, float eps, float lr) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < N) {
+    eps_v[e] = eps;
+    lr_v[e] = lr;
+  }
+}
+
+// A step whose per-expert radius is not finite and > 0, or whose learning
+// rate is not finite, is aborted (the sticky flag; losses read NaN and the
+// parameters stay as they were).
+__global__ void k_check_rates(const float* eps_v, int eps_stride, const float* lr_v, int lr_stride, int N,
+                              unsigned* err) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= N) return;
+  const float eps = eps_v[int64_t(e) * eps_stride], lr = lr_v[int64_t(e) * lr_stride];
+  if (!(eps > 0.0f) || !__builtin_isfinite(eps) || !__builtin_isfinite(lr))
+    __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // g_hat[4q .. 4q+3] = sum_{j<P} coef[j] z_j[4q .. 4q+3] of one expert, summed
@@ -248,14 +274,15 @@ __device__ __forceinline__ float4 estimate_quad(uint2 key, uint32_t step_lo, con
 // theta[e][k] -= lr * sum_{j<P} coef[e][j] z_{e,j}[k], one probe quad per
 // thread (Section 4, Eq. main-spsa; the plain step on the estimate).
 __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* seeds, uint64_t step,
-                                                 float lr, const float* coef, int64_t d, int P, int law,
-                                                 const unsigned* err) {
+                                                 const float* lr_v, int lr_stride, const float* coef, int64_t d,
+                                                 int P, int law, const unsigned* err) {
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
   if (err && *err) return;   // the step was aborted: theta stays as it was
   const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
                                    coef + int64_t(e) * P, P, law, q);
+  const float lr = lr_v[int64_t(e) * lr_stride];
   float* t = theta + int64_t(e) * d + 4 * q;
   if (4 * q + 4 <= d) {
     float4 v = *reinterpret_cast<float4*>(t);
@@ -271,7 +298,7 @@ __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* se
 // bc2 = 1 - beta2^t, omb1 = 1 - beta1, omb2 = 1 - beta2 (computed in fp64 on
 // the host, rounded once).
 struct AdamArgs {
-  float lr, beta1, beta2, omb1, omb2, bc1, bc2, delta, lambda;
+  float beta1, beta2, omb1, omb2, bc1, bc2, delta, lambda;
 };
 
 // The paper's update with coupled weight decay (Appendix E, Eq. localspsa):
@@ -280,8 +307,9 @@ struct AdamArgs {
 //   theta' = theta - lr (m' / bc1) / (sqrt(v' / bc2) + delta).
 // theta, m, v [N][d] fp32 in place, one probe quad per thread.
 __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, float* v, const uint64_t* seeds,
-                                                      uint64_t step, AdamArgs h, const float* coef, int64_t d,
-                                                      int P, int law, const unsigned* err) {
+                                                      uint64_t step, AdamArgs h, const float* lr_v, int lr_stride,
+                                                      const float* coef, int64_t d, int P, int law,
+                                                      const unsigned* err) {
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
@@ -289,6 +317,7 @@ __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, flo
   const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
                                    coef + int64_t(e) * P, P, law, q);
   const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
+  const float lr = lr_v[int64_t(e) * lr_stride];
   const int64_t base = int64_t(e) * d + 4 * q;
   for (int i = 0; i < 4 && 4 * q + i < d; ++i) {
     const float th = theta[base + i];
@@ -296,10 +325,37 @@ __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, flo
     const float m1 = __builtin_fmaf(h.beta1, m[base + i], h.omb1 * g);
     const float v1 = __builtin_fmaf(h.beta2, v[base + i], h.omb2 * (g * g));
     const float r = (m1 / h.bc1) / (sqrtf(v1 / h.bc2) + h.delta);
-    theta[base + i] = __builtin_fmaf(-h.lr, r, th);
+    theta[base + i] = __builtin_fmaf(-lr, r, th);
     m[base + i] = m1;
     v[base + i] = v1;
   }
+}
+
+// The plateau schedule (Section 4; Table experimental-setup): an expert's
+// learning rate and perturbation radius decay together, by `factor`, after
+// `patience` updates without its validation loss improving by more than
+// `threshold`, never below `floor` (and never upward).
+__global__ void k_schedule_init(soma_schedule_entry* s, int n, float lr0, float eps0) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) s[i] = soma_schedule_entry{lr0, eps0, __builtin_inff(), 0};
+}
+
+__global__ void k_schedule_observe(soma_schedule_entry* s, int n, const float* val, int updates, soma_plateau rule) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  soma_schedule_entry x = s[i];
+  if (double(val[i]) < double(x.best) - double(rule.threshold)) {
+    x.best = val[i];
+    x.since = 0;
+  } else {
+    x.since += updates;
+  }
+  if (x.since >= rule.patience) {
+    x.lr = fminf(x.lr, fmaxf(x.lr * rule.factor, rule.floor));
+    x.eps = fminf(x.eps, fmaxf(x.eps * rule.factor, rule.floor));
+    x.since = 0;
+  }
+  s[i] = x;
 }
 
 }  // namespace soma
@@ -462,8 +518,8 @@ int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, h
 // Forward passes of `pcs` directions starting at j0 (kPert) or of the
 // unperturbed experts (!kPert, pcs = 1), ending with per-tile loss sums.
 template <bool kPert>
-int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, float eps,
-                const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
+int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, const float* eps_v,
+                int eps_stride, const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
   const soma_config& c = ctx->cfg;
   const Layout& L = ctx->lay;
   soma::FwdArgs a{};
@@ -478,7 +534,8 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   a.d = L.d;
   a.off_head = L.off_head;
   a.step = step;
-  a.eps = eps;
+  a.eps_v = eps_v;
+  a.eps_stride = eps_stride;
   a.probe = c.probe;
   a.N = c.n_experts;
   a.E = c.embed;
@@ -661,22 +718,53 @@ int soma_get_phase_times(soma_ctx* ctx, soma_phase_times* out) {
 
 namespace {
 
-// Arguments of a step that both updates check.
-int check_step_args(soma_ctx* ctx, const float* theta, const uint64_t* seeds, const uint8_t* bytes,
-                    const float* losses, float eps, float lr) {
+// Per-expert perturbation radius and learning rate of a step (device
+// pointers, expert e at [e * stride]).
+struct Rates {
+  const float* eps_v;
+  int eps_stride;
+  const float* lr_v;
+  int lr_stride;
+};
+
+// The scalar rates of a step, written to the workspace (no host copy).
+int scalar_rates(soma_ctx* ctx, float eps, float lr, hipStream_t st, Rates* out) {
+  float* r = reinterpret_cast<float*>(ctx->ws + ctx->lay.rates);
+  const int N = ctx->cfg.n_experts;
+  hipLaunchKernelGGL(soma::k_fill_rates, dim3((N + 255) / 256), dim3(256), 0, st, r, r + N, N, eps, lr);
+  if (int rc = check_launch("k_fill_rates")) return rc;
+  *out = Rates{r, 1, r + N, 1};
+  return SOMA_OK;
+}
+
+Rates schedule_rates(const soma_schedule_entry* sched) {
+  constexpr int kStride = int(sizeof(soma_schedule_entry) / sizeof(float));
+  static_assert(sizeof(soma_schedule_entry) % sizeof(float) == 0, "entries are whole floats");
+  return Rates{&sched->eps, kStride, &sched->lr, kStride};
+}
+
+// Arguments of a step that every update checks (rates apart).
+int check_step_ptrs(soma_ctx* ctx, const float* theta, const uint64_t* seeds, const uint8_t* bytes,
+                    const float* losses) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
   if (!theta || !seeds || !bytes || !losses) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
   if (!aligned(seeds, 8) || !aligned(losses, 4)) return fail(SOMA_EINVAL, "misaligned seeds or losses");
+  return SOMA_OK;
+}
+
+int check_scalar_rates(float eps, float lr) {
   if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(SOMA_EINVAL, "eps must be finite and > 0");
   if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
   return SOMA_OK;
 }
 
 // Steps 1-3 of the method: every perturbed forward, the losses and the
-// coefficients (in the workspace).  Returns the step's abort flag.
-int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, float eps,
-                              const uint8_t* bytes, float* losses, hipStream_t st, unsigned** err_out) {
+// coefficients (in the workspace).  Returns the step's abort flag, which an
+// invalid per-expert rate sets.
+int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step,
+                              const Rates& r, const uint8_t* bytes, float* losses, hipStream_t st,
+                              unsigned** err_out) {
   const soma_config& c = ctx->cfg;
   const Layout& L = ctx->lay;
   ctx->nmarks = 0;
@@ -686,9 +774,12 @@ int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t*
   unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
   hipLaunchKernelGGL(soma::k_zero_u32, dim3(1), dim3(64), 0, st, err, 1);
   if (int rc = check_launch("k_zero_u32")) return rc;
+  hipLaunchKernelGGL(soma::k_check_rates, dim3((c.n_experts + 255) / 256), dim3(256), 0, st, r.eps_v,
+                     r.eps_stride, r.lr_v, r.lr_stride, c.n_experts, err);
+  if (int rc = check_launch("k_check_rates")) return rc;
   for (int j0 = 0; j0 < c.n_pairs; j0 += L.pc) {
     const int pcs = std::min(L.pc, c.n_pairs - j0);
-    if (int rc = run_forward<true>(ctx, theta, seeds, step, eps, bytes, j0, pcs, st)) return rc;
+    if (int rc = run_forward<true>(ctx, theta, seeds, step, r.eps_v, r.eps_stride, bytes, j0, pcs, st)) return rc;
     const int n = c.n_experts * pcs * 2;
     const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
     hipLaunchKernelGGL(soma::k_loss_reduce, dim3((n + 255) / 256), dim3(256), 0, st,
@@ -700,10 +791,9 @@ int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t*
   }
   float* coef = reinterpret_cast<float*>(ctx->ws + L.coef);
   const int nc = c.n_experts * c.n_pairs;
-  const double inv_denom = 1.0 / (2.0 * double(eps) * double(c.n_pairs));
   hipLaunchKernelGGL(soma::k_coef, dim3((nc + 255) / 256), dim3(256), 0, st,
                      reinterpret_cast<const double*>(ctx->ws + L.lossd), c.n_experts, c.n_pairs,
-                     c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, inv_denom, coef);
+                     c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, r.eps_v, r.eps_stride, coef);
   if (int rc = check_launch("k_coef")) return rc;
   if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
   *err_out = err;
@@ -711,16 +801,14 @@ int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t*
 }
 
 // Adam hyperparameters checked and converted for update number t.
-int adam_args(const soma_adam* hp, int64_t t, float lr, soma::AdamArgs* out) {
+int adam_args(const soma_adam* hp, int64_t t, soma::AdamArgs* out) {
   if (!hp) return fail(SOMA_EINVAL, "adam hyperparameters are NULL");
   if (t < 1) return fail(SOMA_EINVAL, "the update number t must be >= 1");
   if (!(hp->beta1 >= 0.0f && hp->beta1 < 1.0f) || !(hp->beta2 >= 0.0f && hp->beta2 < 1.0f))
     return fail(SOMA_EINVAL, "beta1 and beta2 must lie in [0, 1)");
   if (!(hp->delta > 0.0f) || !std::isfinite(hp->delta)) return fail(SOMA_EINVAL, "delta must be finite and > 0");
   if (!std::isfinite(hp->weight_decay)) return fail(SOMA_EINVAL, "weight_decay must be finite");
-  if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
   const double b1 = hp->beta1, b2 = hp->beta2;
-  out->lr = lr;
   out->beta1 = hp->beta1;
   out->beta2 = hp->beta2;
   out->omb1 = static_cast<float>(1.0 - b1);
@@ -738,12 +826,43 @@ int check_state(const float* m, const float* v) {
   return SOMA_OK;
 }
 
-void launch_adam(const soma_ctx* ctx, float* theta, float* m, float* v, const uint64_t* seeds, uint64_t step,
-                 const soma::AdamArgs& h, const float* coef, const unsigned* err, hipStream_t st) {
+int launch_sgd(const soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, const Rates& r,
+               const float* coef, const unsigned* err, hipStream_t st) {
+  const soma_config& c = ctx->cfg;
+  const int64_t quads = (ctx->lay.d + 3) / 4;
+  hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st, theta,
+                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, c.n_pairs, c.probe, err);
+  return check_launch("k_update");
+}
+
+int launch_adam(const soma_ctx* ctx, float* theta, float* m, float* v, const uint64_t* seeds, uint64_t step,
+                const soma::AdamArgs& h, const Rates& r, const float* coef, const unsigned* err, hipStream_t st) {
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update_adam, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
-                     theta, m, v, seeds, step, h, coef, ctx->lay.d, c.n_pairs, c.probe, err);
+                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, c.n_pairs, c.probe, err);
+  return check_launch("k_update_adam");
+}
+
+int finish_step(soma_ctx* ctx, hipStream_t st) {
+  if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
+  ctx->have_coef = true;
+  ctx->have_times = ctx->timing;
+  return ok();
+}
+
+// The whole Adam step for given rates.
+int adam_step(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, const soma_adam* hp,
+              const uint64_t* seeds, uint64_t step, const Rates& r, const uint8_t* bytes, float* losses,
+              hipStream_t st) {
+  soma::AdamArgs h{};
+  if (int rc = adam_args(hp, t, &h)) return rc;
+  unsigned* err = nullptr;
+  if (int rc = forwards_and_coefficients(ctx, theta, seeds, step, r, bytes, losses, st, &err)) return rc;
+  if (int rc = launch_adam(ctx, theta, m, v, seeds, step, h, r,
+                           reinterpret_cast<const float*>(ctx->ws + ctx->lay.coef), err, st))
+    return rc;
+  return finish_step(ctx, st);
 }
 
 }  // namespace
@@ -752,38 +871,70 @@ extern "C" {
 
 int soma_spsa_step(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, float eps,
                    float lr, const uint8_t* bytes, float* losses, void* stream) {
-  if (int rc = check_step_args(ctx, theta, seeds, bytes, losses, eps, lr)) return rc;
-  const soma_config& c = ctx->cfg;
-  const Layout& L = ctx->lay;
+  if (int rc = check_step_ptrs(ctx, theta, seeds, bytes, losses)) return rc;
+  if (int rc = check_scalar_rates(eps, lr)) return rc;
   const hipStream_t st = as_stream(stream);
+  Rates r{};
+  if (int rc = scalar_rates(ctx, eps, lr, st, &r)) return rc;
   unsigned* err = nullptr;
-  if (int rc = forwards_and_coefficients(ctx, theta, seeds, step, eps, bytes, losses, st, &err)) return rc;
-  const float* coef = reinterpret_cast<const float*>(ctx->ws + L.coef);
-  const int64_t quads = (L.d + 3) / 4;
-  hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
-                     st, theta, seeds, step, lr, coef, L.d, c.n_pairs, c.probe, err);
-  if (int rc = check_launch("k_update")) return rc;
-  if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
-  ctx->have_coef = true;
-  ctx->have_times = ctx->timing;
-  return ok();
+  if (int rc = forwards_and_coefficients(ctx, theta, seeds, step, r, bytes, losses, st, &err)) return rc;
+  if (int rc = launch_sgd(ctx, theta, seeds, step, r, reinterpret_cast<const float*>(ctx->ws + ctx->lay.coef),
+                          err, st))
+    return rc;
+  return finish_step(ctx, st);
 }
 
 int soma_spsa_step_adam(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, const soma_adam* hp,
                         const uint64_t* seeds, uint64_t step, float eps, float lr, const uint8_t* bytes,
                         float* losses, void* stream) {
-  if (int rc = check_step_args(ctx, theta, seeds, bytes, losses, eps, lr)) return rc;
+  if (int rc = check_step_ptrs(ctx, theta, seeds, bytes, losses)) return rc;
+  if (int rc = check_scalar_rates(eps, lr)) return rc;
   if (int rc = check_state(m, v)) return rc;
   soma::AdamArgs h{};
-  if (int rc = adam_args(hp, t, lr, &h)) return rc;
+  if (int rc = adam_args(hp, t, &h)) return rc;
   const hipStream_t st = as_stream(stream);
-  unsigned* err = nullptr;
-  if (int rc = forwards_and_coefficients(ctx, theta, seeds, step, eps, bytes, losses, st, &err)) return rc;
-  launch_adam(ctx, theta, m, v, seeds, step, h, reinterpret_cast<const float*>(ctx->ws + ctx->lay.coef), err, st);
-  if (int rc = check_launch("k_update_adam")) return rc;
-  if (int rc = mark(ctx, kPhaseUpdate, st)) return rc;
-  ctx->have_coef = true;
-  ctx->have_times = ctx->timing;
+  Rates r{};
+  if (int rc = scalar_rates(ctx, eps, lr, st, &r)) return rc;
+  return adam_step(ctx, theta, m, v, t, hp, seeds, step, r, bytes, losses, st);
+}
+
+int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, const soma_adam* hp,
+                              const uint64_t* seeds, uint64_t step, const soma_schedule_entry* sched,
+                              const uint8_t* bytes, float* losses, void* stream) {
+  if (int rc = check_step_ptrs(ctx, theta, seeds, bytes, losses)) return rc;
+  if (int rc = check_state(m, v)) return rc;
+  if (!sched) return fail(SOMA_EINVAL, "schedule is NULL");
+  if (!aligned(sched, alignof(soma_schedule_entry))) return fail(SOMA_EINVAL, "misaligned schedule");
+  soma::AdamArgs h{};
+  if (int rc = adam_args(hp, t, &h)) return rc;
+  return adam_step(ctx, theta, m, v, t, hp, seeds, step, schedule_rates(sched), bytes, losses,
+                   as_stream(stream));
+}
+
+int soma_schedule_init(soma_schedule_entry* sched, int32_t n, float lr0, float eps0, void* stream) {
+  if (!sched) return fail(SOMA_EINVAL, "schedule is NULL");
+  if (n < 1) return fail(SOMA_EINVAL, "n must be >= 1");
+  if (!aligned(sched, alignof(soma_schedule_entry))) return fail(SOMA_EINVAL, "misaligned schedule");
+  if (!(eps0 > 0.0f) || !std::isfinite(eps0) || !std::isfinite(lr0))
+    return fail(SOMA_EINVAL, "eps0 must be finite and > 0, lr0 finite");
+  hipLaunchKernelGGL(soma::k_schedule_init, dim3((n + 255) / 256), dim3(256), 0, as_stream(stream), sched, n, lr0,
+                     eps0);
+  if (int rc = check_launch("k_schedule_init")) return rc;
+  return ok();
+}
+
+int soma_schedule_observe(soma_schedule_entry* sched, int32_t n, const float* val_loss, int32_t updates,
+                          const soma_plateau* rule, void* stream) {
+  if (!sched || !val_loss || !rule) return fail(SOMA_EINVAL, "NULL argument");
+  if (n < 1 || updates < 0) return fail(SOMA_EINVAL, "n must be >= 1 and updates >= 0");
+  if (!aligned(sched, alignof(soma_schedule_entry)) || !aligned(val_loss, 4))
+    return fail(SOMA_EINVAL, "misaligned schedule or losses");
+  if (!(rule->factor > 0.0f && rule->factor < 1.0f) || rule->patience < 1 || !(rule->threshold >= 0.0f) ||
+      !std::isfinite(rule->threshold) || !(rule->floor >= 0.0f) || !std::isfinite(rule->floor))
+    return fail(SOMA_EINVAL, "plateau rule: factor in (0, 1), patience >= 1, finite threshold and floor >= 0");
+  hipLaunchKernelGGL(soma::k_schedule_observe, dim3((n + 255) / 256), dim3(256), 0, as_stream(stream), sched, n,
+                     val_loss, updates, *rule);
+  if (int rc = check_launch("k_schedule_observe")) return rc;
   return ok();
 }
 
@@ -792,11 +943,14 @@ int soma_apply_adam(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, 
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
   if (!theta || !seeds || !coef) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
+  if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
   if (int rc = check_state(m, v)) return rc;
   soma::AdamArgs h{};
-  if (int rc = adam_args(hp, t, lr, &h)) return rc;
-  launch_adam(ctx, theta, m, v, seeds, step, h, coef, nullptr, as_stream(stream));
-  if (int rc = check_launch("k_update_adam")) return rc;
+  if (int rc = adam_args(hp, t, &h)) return rc;
+  const hipStream_t st = as_stream(stream);
+  Rates r{};
+  if (int rc = scalar_rates(ctx, 1.0f, lr, st, &r)) return rc;
+  if (int rc = launch_adam(ctx, theta, m, v, seeds, step, h, r, coef, nullptr, st)) return rc;
   return ok();
 }
 
@@ -810,7 +964,7 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
   const hipStream_t st = as_stream(stream);
   const bool timing = ctx->timing;
   ctx->timing = false;  // evaluation is not part of the step's phase record
-  const int rc0 = run_forward<false>(ctx, theta, nullptr, 0, 0.0f, bytes, 0, 1, st);
+  const int rc0 = run_forward<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
   ctx->timing = timing;
   if (rc0) return rc0;
   const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
@@ -838,12 +992,10 @@ int soma_apply_update(soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64
   if (!theta || !seeds || !coef) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
   if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
-  const soma_config& c = ctx->cfg;
-  const int64_t quads = (ctx->lay.d + 3) / 4;
-  hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0,
-                     as_stream(stream), theta, seeds, step, lr, coef, ctx->lay.d, c.n_pairs, c.probe,
-                     static_cast<const unsigned*>(nullptr));
-  if (int rc = check_launch("k_update")) return rc;
+  const hipStream_t st = as_stream(stream);
+  Rates r{};
+  if (int rc = scalar_rates(ctx, 1.0f, lr, st, &r)) return rc;
+  if (int rc = launch_sgd(ctx, theta, seeds, step, r, coef, nullptr, st)) return rc;
   return ok();
 }
 

@@ -83,7 +83,8 @@ struct FwdArgs {
   int64_t off_l;    // canonical offset of W_l (current layer)
   int64_t off_head; // canonical offset of Whead
   uint64_t step;
-  float eps;
+  const float* eps_v;     // perturbation radius of expert e: eps_v[e * eps_stride]
+  int eps_stride;
   int probe;              // probe law (kProbe*)
   int N, E, H, B, T, PC;  // PC = slot stride in directions
   int pcs;                // directions in this pass (grid extent)
@@ -93,6 +94,8 @@ struct FwdArgs {
   int t;                  // time step (rec kernel)
   int row_tiles;          // head row tiles per slot
 };
+
+__device__ __forceinline__ float eps_of(const FwdArgs& a, int e) { return a.eps_v[int64_t(e) * a.eps_stride]; }
 
 // ---------------------------------------------------------------------------
 // Layer-1 gate inputs per byte value (the vocabulary fold).
@@ -113,6 +116,7 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
   const int E = a.E, H = a.H;
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
+  const float eps = kPert ? eps_of(a, e) : 0.0f;
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
   const int prow = mtile * 64 + wave * 16 + lr;
   const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (E + H);
@@ -132,8 +136,8 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
       const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
       if (kPert) {
         const float4 z = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk));
-        *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = fma4(a.eps, z, t4);
-        *reinterpret_cast<float4*>(&es[NS - 1][n][4 * c4]) = fma4(-a.eps, z, t4);
+        *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = fma4(eps, z, t4);
+        *reinterpret_cast<float4*>(&es[NS - 1][n][4 * c4]) = fma4(-eps, z, t4);
       } else {
         *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = t4;
       }
@@ -145,8 +149,8 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
       float4 w[NS];
       if (kPert) {
         const float4 z = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kw));
-        w[0] = fma4(a.eps, z, t4);
-        w[NS - 1] = fma4(-a.eps, z, t4);
+        w[0] = fma4(eps, z, t4);
+        w[NS - 1] = fma4(-eps, z, t4);
       } else {
         w[0] = t4;
       }
@@ -299,7 +303,8 @@ __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
     return row < R ? *reinterpret_cast<const float4*>(hin + ((slot0 + s) * R + row) * H + k)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   };
-  perturbed_mainloop<NS, 1, NBP, kPert>(acc, xs, th, wrow, in, a.probe, key, pair, step_lo, a.eps, act);
+  perturbed_mainloop<NS, 1, NBP, kPert>(acc, xs, th, wrow, in, a.probe, key, pair, step_lo,
+        kPert ? eps_of(a, e) : 0.0f, act);
 
   const int p = mtile * 64 + wave * 16 + 4 * lg;
 #pragma unroll
@@ -355,7 +360,8 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
       return b < B ? *reinterpret_cast<const float4*>(hprev + ((slot0 + s) * R + b) * H + k)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
     };
-    perturbed_mainloop<NS, 1, NB, kPert>(acc, hs, th, wrow, H, a.probe, key, pair, step_lo, a.eps, act);
+    perturbed_mainloop<NS, 1, NB, kPert>(acc, hs, th, wrow, H, a.probe, key, pair, step_lo,
+        kPert ? eps_of(a, e) : 0.0f, act);
   }
 
   const int unit = utile * 16 + wave * 4 + lg;
@@ -429,7 +435,8 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
     return row < R ? *reinterpret_cast<const float4*>(hin + ((slot0 + s) * R + row) * H + k)
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   };
-  perturbed_mainloop<NS, 4, NBH, kPert>(acc, xs, th, wrow, H, a.probe, key, pair, step_lo, a.eps, act);
+  perturbed_mainloop<NS, 4, NBH, kPert>(acc, xs, th, wrow, H, a.probe, key, pair, step_lo,
+        kPert ? eps_of(a, e) : 0.0f, act);
 
   // Row maxima: lane-local over 16 logits, then across the 4 lane groups.
   float mx[NS][NBH];
@@ -704,7 +711,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     const uint2 key = stream_key(a.seeds[e], a.step);
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
     const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
-    const float seps = sg == 0 ? a.eps : -a.eps;
+    const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
     const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
     // Gate inputs of layer 1 (folded, per byte value) or of a later layer.
     const __amdgpu_buffer_rsrc_t gbuf =
@@ -905,7 +912,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = stream_key(a.seeds[e], a.step);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-  const float seps = sg == 0 ? a.eps : -a.eps;
+  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
   const int unit = mb * 32 + wave * 4 + lg;   // output unit of this lane
   // 32-bit offsets: R 4H floats < 2^31 bytes (host check).
   const __amdgpu_buffer_rsrc_t hbuf =
@@ -1029,7 +1036,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = stream_key(a.seeds[e], a.step);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-  const float seps = sg == 0 ? a.eps : -a.eps;
+  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
   const int vbase = vh * 128 + wave * 16 + 4 * lg;   // vocabulary rows vbase .. +3 of this lane
   // 32-bit offsets: R H floats < 2^31 bytes (host check).
   const __amdgpu_buffer_rsrc_t hbuf =

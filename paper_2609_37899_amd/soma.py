@@ -21,7 +21,8 @@ FLAG_TILED_WEIGHTS = 2
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_spsa_step_adam", "soma_eval_loss", "soma_coefficients",
-           "soma_apply_update", "soma_apply_adam",
+           "soma_apply_update", "soma_apply_adam", "soma_spsa_step_adam_sched", "soma_schedule_init",
+           "soma_schedule_observe",
            "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
            "soma_get_phase_times",
            "soma_last_error")
@@ -50,6 +51,18 @@ class Adam(ctypes.Structure):
 
     def __init__(self, beta1=0.9, beta2=0.999, delta=1e-8, weight_decay=1e-4):
         super().__init__(beta1, beta2, delta, weight_decay)
+
+
+class Plateau(ctypes.Structure):
+    """soma_plateau; the defaults are the paper's schedule."""
+    _fields_ = [("factor", ctypes.c_float), ("patience", ctypes.c_int32), ("threshold", ctypes.c_float),
+                ("floor", ctypes.c_float)]
+
+    def __init__(self, factor=0.5, patience=1000, threshold=1e-8, floor=1e-5):
+        super().__init__(factor, patience, threshold, floor)
+
+
+SCHEDULE_ENTRY_BYTES = 16   # soma_schedule_entry: lr, eps, best (fp32), since (int32)
 
 
 class Config(ctypes.Structure):
@@ -81,6 +94,11 @@ def load():
                                                    vp, u64, f32, f32, vp, vp, vp]),
             "soma_apply_adam": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam), vp,
                                                u64, f32, vp, vp]),
+            "soma_spsa_step_adam_sched": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam),
+                                                         vp, u64, vp, vp, vp, vp]),
+            "soma_schedule_init": (ctypes.c_int, [vp, ctypes.c_int32, f32, f32, vp]),
+            "soma_schedule_observe": (ctypes.c_int, [vp, ctypes.c_int32, vp, ctypes.c_int32,
+                                                     ctypes.POINTER(Plateau), vp]),
             "soma_eval_loss": (ctypes.c_int, [vp, vp, vp, vp, vp]),
             "soma_coefficients": (ctypes.c_int, [vp, vp, vp]),
             "soma_apply_update": (ctypes.c_int, [vp, vp, vp, u64, f32, vp, vp]),
@@ -198,6 +216,16 @@ class Context:
                                           _dptr(bytes_, torch.uint8, "bytes"),
                                           _dptr(losses, torch.float32, "losses"), _stream(stream)))
 
+    def spsa_step_adam_sched(self, theta, m, v, t: int, adam, seeds, step: int, sched, bytes_, losses,
+                             stream=None):
+        import torch
+        _check(load().soma_spsa_step_adam_sched(self._h, _dptr(theta, torch.float32, "theta"),
+                                                _dptr(m, torch.float32, "m"), _dptr(v, torch.float32, "v"),
+                                                int(t), ctypes.byref(adam), _dptr(seeds, torch.int64, "seeds"),
+                                                int(step), _dptr(sched, None, "schedule"),
+                                                _dptr(bytes_, torch.uint8, "bytes"),
+                                                _dptr(losses, torch.float32, "losses"), _stream(stream)))
+
     def apply_adam(self, theta, m, v, t: int, adam, seeds, step: int, lr: float, coef, stream=None):
         import torch
         _check(load().soma_apply_adam(self._h, _dptr(theta, torch.float32, "theta"),
@@ -240,6 +268,32 @@ def probe(law: int, seed: int, step: int, pair: int, k0: int, out, stream=None):
     import torch
     _check(load().soma_probe(int(law), int(seed) & (2**64 - 1), int(step), int(pair), int(k0), out.numel(),
                              _dptr(out, torch.float32, "out"), _stream(stream)))
+
+
+def schedule_tensor(n: int, device="cuda"):
+    """Device memory for n soma_schedule_entry records (int32 view, 4 words each)."""
+    import torch
+    return torch.empty((n, SCHEDULE_ENTRY_BYTES // 4), dtype=torch.int32, device=device)
+
+
+def schedule_init(sched, lr0: float, eps0: float, stream=None):
+    _check(load().soma_schedule_init(_dptr(sched, None, "schedule"), sched.shape[0], float(lr0), float(eps0),
+                                     _stream(stream)))
+
+
+def schedule_observe(sched, val_loss, updates: int, rule, stream=None):
+    import torch
+    _check(load().soma_schedule_observe(_dptr(sched, None, "schedule"), sched.shape[0],
+                                        _dptr(val_loss, torch.float32, "val_loss"), int(updates),
+                                        ctypes.byref(rule), _stream(stream)))
+
+
+def schedule_fields(sched):
+    """(lr, eps, best, since) numpy arrays of a schedule tensor (copies to the host)."""
+    import numpy as np
+    a = sched.cpu().numpy()
+    f = a.view(np.float32)
+    return f[:, 0].copy(), f[:, 1].copy(), f[:, 2].copy(), a[:, 3].copy()
 
 
 def philox(ctr, key, out, stream=None):
