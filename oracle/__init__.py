@@ -42,7 +42,7 @@ def build(force: bool = False) -> str:
 class OracleCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "probe")]
+        "probe", "accum")]
 
 
 def _load():
@@ -105,15 +105,15 @@ PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 
 
 def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode=0,
-             probe=PROBE_GAUSSIAN):
-    return OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe)
+             probe=PROBE_GAUSSIAN, accum=1):
+    return OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe, accum)
 
 
 def cfg_from(shape) -> OracleCfg:
     """Build the oracle's configuration from any object with the shape fields."""
     return make_cfg(shape.n_experts, shape.n_layers, shape.embed, shape.hidden, shape.batch,
                     shape.seq_len, shape.n_pairs, getattr(shape, "loss_mode", 0),
-                    getattr(shape, "probe", PROBE_GAUSSIAN))
+                    getattr(shape, "probe", PROBE_GAUSSIAN), getattr(shape, "accum", 1))
 
 
 def param_count(cfg: OracleCfg) -> int:
@@ -281,13 +281,15 @@ def apply_adam(cfg: OracleCfg, theta_e, m_e, v_e, t: int, seed: int, step: int, 
 
 def spsa_step(cfg: OracleCfg, theta: np.ndarray, seeds, step: int, eps: float, lr: float,
               bytes_all: np.ndarray, want_ghat: bool = False):
-    """Full oracle step.  Returns dict(losses [N,P,2] f32, coef [N,P] f64,
-    theta [N,d] f32, ghat [N,d] f64 or None)."""
-    N, P = cfg.n_experts, cfg.n_pairs
+    """Full oracle step.  bytes_all is [N][B][T], or [A][N][B][T] with A =
+    cfg.accum accumulation batches.  Returns dict(losses [N,D,2] f32, coef
+    [N,D] f64, theta [N,d] f32, ghat [N,d] f64 or None), D = A P directions."""
+    A = max(1, cfg.accum)
+    N, P = cfg.n_experts, cfg.n_pairs * A
     d = param_count(cfg)
     t = np.ascontiguousarray(theta, dtype=np.float32).reshape(N, d)
     sd = np.ascontiguousarray(seeds, dtype=np.uint64).reshape(N)
-    b = np.ascontiguousarray(bytes_all, dtype=np.uint8).reshape(N, cfg.batch, cfg.seq_len)
+    b = np.ascontiguousarray(bytes_all, dtype=np.uint8).reshape(A, N, cfg.batch, cfg.seq_len)
     losses = np.empty((N, P, 2), dtype=np.float32)
     coef = np.empty((N, P), dtype=np.float64)
     out = np.empty_like(t)

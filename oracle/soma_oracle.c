@@ -70,7 +70,11 @@ typedef struct {
   int32_t n_pairs;   /* P antithetic pairs (directions) per expert */
   int32_t loss_mode; /* 0: independent per-expert losses, 1: summed loss */
   int32_t probe;     /* probe law: 0 Gaussian, 1 sparse Rademacher, 2 dense Rademacher */
+  int32_t accum;     /* A accumulation batches per update (0 or 1: one batch) */
 } oracle_cfg;
+
+/* Directions per update: P per batch, A batches. */
+static int total_dirs(const oracle_cfg *c) { return c->n_pairs * (c->accum > 1 ? c->accum : 1); }
 
 #define VOCAB 256
 
@@ -430,7 +434,7 @@ double oracle_perturbed_loss(const oracle_cfg *c, const float *theta, uint64_t s
 void oracle_apply_update(const oracle_cfg *c, const float *theta, uint64_t seed, uint64_t step,
                          float lr, const double *coef, const int64_t *ks, int64_t nk,
                          float *theta_out, double *ghat) {
-  const int P = c->n_pairs;
+  const int P = total_dirs(c);
   const int64_t n = ks ? nk : oracle_param_count(c);
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i) {
@@ -457,7 +461,7 @@ void oracle_apply_adam(const oracle_cfg *c, const float *theta, const float *m, 
                        uint64_t seed, uint64_t step, float lr, const double *coef, double beta1,
                        double beta2, double delta, double lambda, const int64_t *ks, int64_t nk,
                        float *theta_out, float *m_out, float *v_out, double *ghat) {
-  const int P = c->n_pairs;
+  const int P = total_dirs(c);
   const int64_t n = ks ? nk : oracle_param_count(c);
   const double bc1 = 1.0 - pow(beta1, (double)t), bc2 = 1.0 - pow(beta2, (double)t);
 #pragma omp parallel for schedule(static)
@@ -480,32 +484,37 @@ void oracle_apply_adam(const oracle_cfg *c, const float *theta, const float *m, 
   }
 }
 
-/* One SPSA step for all experts./* One SPSA step for all experts.
+/* One SPSA step for all experts, accumulated over A = accum independently
+ * sampled batches (Appendix E): direction j of the D = A P directions is
+ * evaluated on batch j / P, and the estimate averages all D directions,
+ *   g_hat = (1/A) sum_a (1/P) sum_{j in batch a} ... = (1/D) sum_j ...
  *   theta   [N][d]   fp32, read only
  *   seeds   [N]      per-expert Philox stream seeds
- *   bytes   [N][B][T]
- *   losses  [N][P][2] out: [e][j][0] = L(theta_e + eps z), [1] = L(theta_e - eps z)
- *   coef    [N][P]    out (may be NULL): the coefficient applied to z_{e,j}
+ *   bytes   [A][N][B][T]
+ *   losses  [N][D][2] out: [e][j][0] = L(theta_e + eps z), [1] = L(theta_e - eps z)
+ *   coef    [N][D]    out (may be NULL): the coefficient applied to z_{e,j}
  *   theta_out [N][d]  out
  *   ghat    [N][d]    out (may be NULL): the estimate, fp64
  * Returns 0, or -1 on an invalid configuration. */
 int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *seeds, uint64_t step,
                      float eps, float lr, const uint8_t *bytes, float *losses, double *coef,
                      float *theta_out, double *ghat) {
-  const int N = c->n_experts, P = c->n_pairs;
-  if (N < 1 || P < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
-      c->seq_len < 2 || c->probe < 0 || c->probe > 2)
+  const int N = c->n_experts, P = total_dirs(c), Pb = c->n_pairs;
+  if (N < 1 || Pb < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
+      c->seq_len < 2 || c->probe < 0 || c->probe > 2 || c->accum < 0)
     return -1;
   const int64_t d = oracle_param_count(c);
   const size_t bstride = (size_t)c->batch * c->seq_len;
   double *L = (double *)malloc(sizeof(double) * (size_t)N * P * 2);
-  /* 1-4: perturbed forwards, each on its expert's own batch. */
+  /* 1-4: perturbed forwards, each on its expert's own batch (batch j / Pb of
+   * the update for direction j). */
   for (int e = 0; e < N; ++e)
     for (int j = 0; j < P; ++j)
       for (int s = 0; s < 2; ++s)
         L[((size_t)e * P + j) * 2 + s] =
             oracle_perturbed_loss(c, theta + (size_t)e * d, seeds[e], step, (uint32_t)j,
-                                  s == 0 ? +1 : -1, eps, bytes + (size_t)e * bstride);
+                                  s == 0 ? +1 : -1, eps,
+                                  bytes + ((size_t)(j / Pb) * N + e) * bstride);
   /* 5: coefficients. */
   double *cf = (double *)malloc(sizeof(double) * (size_t)N * P);
   const double denom = 2.0 * (double)eps * (double)P;
