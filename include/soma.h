@@ -106,9 +106,16 @@ enum soma_flags {
 
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;
  * embed and hidden positive multiples of 16; batch >= 1; seq_len >= 2;
- * pair_chunk in [0, n_pairs] (0 picks a chunk that keeps the workspace
- * under 24 GiB; the step processes the P directions in chunks of this many,
- * which changes memory use but not the result); flags: enum soma_flags. */
+ * accum >= 0; pair_chunk in [0, D] (0 picks a chunk that keeps the workspace
+ * under 24 GiB; the step processes its D directions in chunks of this many,
+ * which changes memory use but not the result); flags: enum soma_flags.
+ *
+ * Accumulation (Appendix E): with A = accum > 1 an update averages the
+ * estimates of A independently sampled batches, each with its own P =
+ * n_pairs directions.  The step then evaluates D = A P directions, direction
+ * j (probe stream index j) on batch j / P; bytes are [A][N][B][T], losses
+ * [N][D][2], coefficients [N][D] with c = (L+ - L-) / (2 eps D).  With A <= 1,
+ * D = P and bytes are [N][B][T]. */
 typedef struct soma_config {
   int32_t n_experts;  /* N */
   int32_t n_layers;   /* L */
@@ -121,6 +128,7 @@ typedef struct soma_config {
   int32_t pair_chunk; /* directions evaluated per pass; 0 = automatic */
   int32_t flags;      /* enum soma_flags, 0 by default */
   int32_t probe;      /* enum soma_probe_law, 0 (Gaussian) by default */
+  int32_t accum;      /* A accumulation batches per update (0 or 1: one batch), see below */
 } soma_config;
 
 typedef struct soma_ctx soma_ctx;
@@ -153,8 +161,8 @@ void soma_destroy(soma_ctx* ctx);
  *   eps        perturbation radius, finite and > 0.
  *   lr         learning rate, finite.
  *   bytes_dev  [N][B][T] uint8, expert e's batch (shared by all its
- *              directions and both signs).
- *   losses_dev [N][P][2] fp32 out: [e][j][0] = L(theta_e + eps z_{e,j}),
+ *              directions and both signs); [A][N][B][T] with accumulation.
+ *   losses_dev [N][D][2] fp32 out: [e][j][0] = L(theta_e + eps z_{e,j}),
  *              [e][j][1] = L(theta_e - eps z_{e,j}), mean nats per target.
  * The coefficients of the step stay in the workspace until the next call
  * and can be read with soma_coefficients(). */
@@ -189,7 +197,7 @@ int soma_spsa_step_adam(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_
                         const uint8_t* bytes_dev, float* losses_dev, void* stream);
 
 /* The Adam update of soma_spsa_step_adam alone, for given coefficients
- * coef_dev [N][P] fp32 (device). */
+ * coef_dev [N][D] fp32 (device). */
 int soma_apply_adam(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_dev, int64_t t,
                     const soma_adam* hp, const uint64_t* seeds_dev, uint64_t step, float lr,
                     const float* coef_dev, void* stream);
@@ -244,13 +252,13 @@ int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta_dev, float* m_dev, flo
 int soma_eval_loss(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev,
                    float* loss_dev, void* stream);
 
-/* Copy the coefficients c[N][P] (fp32) of the last soma_spsa_step on this
+/* Copy the coefficients c[N][D] (fp32) of the last soma_spsa_step on this
  * context into coef_dev (device-to-device, on `stream`). */
 int soma_coefficients(soma_ctx* ctx, float* coef_dev, void* stream);
 
 /* The update of step 4 alone, for given coefficients:
  *   theta_e[k] <- theta_e[k] - lr * sum_{j<P} coef[e][j] z_{e,j}[k]
- * (sum in j order, fp32).  coef_dev [N][P] fp32 (device).  This is the
+ * (sum in j order, fp32).  coef_dev [N][D] fp32 (device).  This is the
  * kernel soma_spsa_step ends with; it is exposed so that the update can be
  * checked and reused on its own (e.g. to replay a step from stored losses). */
 int soma_apply_update(soma_ctx* ctx, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,

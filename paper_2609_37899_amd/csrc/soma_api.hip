@@ -60,6 +60,9 @@ struct Layout {
          total = 0;
 };
 
+// Directions per update: n_pairs per accumulation batch, accum batches.
+int dirs(const soma_config& c) { return c.n_pairs * (c.accum > 1 ? c.accum : 1); }
+
 int64_t param_count_of(const soma_config& c) {
   int64_t d = int64_t(SOMA_VOCAB) * c.embed;
   for (int l = 0; l < c.n_layers; ++l)
@@ -78,8 +81,11 @@ int validate(const soma_config* c) {
                 c->embed, c->hidden);
   if (c->loss_mode != SOMA_LOSS_INDEPENDENT && c->loss_mode != SOMA_LOSS_SUMMED)
     return fail(SOMA_EINVAL, "loss_mode must be 0 (independent) or 1 (summed)");
-  if (c->pair_chunk < 0 || c->pair_chunk > c->n_pairs)
-    return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs]");
+  if (c->accum < 0) return fail(SOMA_ESHAPE, "accum must be >= 0 (0 or 1: one batch)");
+  if (int64_t(c->n_pairs) * (c->accum > 1 ? c->accum : 1) >= (int64_t(1) << 24))
+    return fail(SOMA_ESHAPE, "n_pairs * accum must stay below 2^24");
+  if (c->pair_chunk < 0 || c->pair_chunk > dirs(*c))
+    return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs * accum]");
   if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS))
     return fail(SOMA_EINVAL, "unknown flags");
   if (c->probe != SOMA_PROBE_GAUSSIAN && c->probe != SOMA_PROBE_SPARSE_RADEMACHER &&
@@ -108,8 +114,8 @@ Layout layout_for(const soma_config& c, int pc) {
   size_t at = 0;
   L.sync = at; at += round_up(sizeof(unsigned) * (kMaxGroups + 1));
   L.rates = at; at += round_up(sizeof(float) * 2 * N);            // eps[N], lr[N] of a scalar-rate step
-  L.coef = at; at += round_up(sizeof(float) * N * c.n_pairs);
-  L.lossd = at; at += round_up(sizeof(double) * N * c.n_pairs * 2);
+  L.coef = at; at += round_up(sizeof(float) * N * dirs(c));
+  L.lossd = at; at += round_up(sizeof(double) * N * dirs(c) * 2);
   L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
   L.U = at;    at += round_up(sizeof(float) * slots * SOMA_VOCAB * 4 * H);
   L.hseq = at; at += round_up(sizeof(float) * slots * R * H);
@@ -124,7 +130,7 @@ Layout layout_for(const soma_config& c, int pc) {
 
 int choose_chunk(const soma_config& c) {
   if (c.pair_chunk > 0) return c.pair_chunk;
-  int pc = c.n_pairs;
+  int pc = dirs(c);
   while (pc > 1 && layout_for(c, pc).total > kAutoBudget) --pc;
   return pc;
 }
@@ -536,6 +542,8 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   a.step = step;
   a.eps_v = eps_v;
   a.eps_stride = eps_stride;
+  a.ppb = kPert ? c.n_pairs : 1;
+  a.bstride = kPert ? int64_t(c.n_experts) * c.batch * c.seq_len : 0;
   a.probe = c.probe;
   a.N = c.n_experts;
   a.E = c.embed;
@@ -777,22 +785,23 @@ int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t*
   hipLaunchKernelGGL(soma::k_check_rates, dim3((c.n_experts + 255) / 256), dim3(256), 0, st, r.eps_v,
                      r.eps_stride, r.lr_v, r.lr_stride, c.n_experts, err);
   if (int rc = check_launch("k_check_rates")) return rc;
-  for (int j0 = 0; j0 < c.n_pairs; j0 += L.pc) {
-    const int pcs = std::min(L.pc, c.n_pairs - j0);
+  const int D = dirs(c);
+  for (int j0 = 0; j0 < D; j0 += L.pc) {
+    const int pcs = std::min(L.pc, D - j0);
     if (int rc = run_forward<true>(ctx, theta, seeds, step, r.eps_v, r.eps_stride, bytes, j0, pcs, st)) return rc;
     const int n = c.n_experts * pcs * 2;
     const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
     hipLaunchKernelGGL(soma::k_loss_reduce, dim3((n + 255) / 256), dim3(256), 0, st,
                        reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts,
-                       pcs, L.pc, 2, c.n_pairs, j0, inv_rows, losses,
+                       pcs, L.pc, 2, D, j0, inv_rows, losses,
                        reinterpret_cast<double*>(ctx->ws + L.lossd), err);
     if (int rc = check_launch("k_loss_reduce")) return rc;
     if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
   }
   float* coef = reinterpret_cast<float*>(ctx->ws + L.coef);
-  const int nc = c.n_experts * c.n_pairs;
+  const int nc = c.n_experts * D;
   hipLaunchKernelGGL(soma::k_coef, dim3((nc + 255) / 256), dim3(256), 0, st,
-                     reinterpret_cast<const double*>(ctx->ws + L.lossd), c.n_experts, c.n_pairs,
+                     reinterpret_cast<const double*>(ctx->ws + L.lossd), c.n_experts, D,
                      c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, r.eps_v, r.eps_stride, coef);
   if (int rc = check_launch("k_coef")) return rc;
   if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
@@ -831,7 +840,7 @@ int launch_sgd(const soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st, theta,
-                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, c.n_pairs, c.probe, err);
+                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), c.probe, err);
   return check_launch("k_update");
 }
 
@@ -840,7 +849,7 @@ int launch_adam(const soma_ctx* ctx, float* theta, float* m, float* v, const uin
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update_adam, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
-                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, c.n_pairs, c.probe, err);
+                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), c.probe, err);
   return check_launch("k_update_adam");
 }
 
@@ -979,7 +988,7 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
 int soma_coefficients(soma_ctx* ctx, float* coef, void* stream) {
   if (!ctx || !coef) return fail(SOMA_EINVAL, "NULL argument");
   if (!ctx->have_coef) return fail(SOMA_EINVAL, "no step has run on this context");
-  const size_t n = size_t(ctx->cfg.n_experts) * ctx->cfg.n_pairs;
+  const size_t n = size_t(ctx->cfg.n_experts) * dirs(ctx->cfg);
   const hipError_t e = hipMemcpyAsync(coef, ctx->ws + ctx->lay.coef, n * sizeof(float),
                                       hipMemcpyDeviceToDevice, as_stream(stream));
   if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipMemcpyAsync: %s", hipGetErrorString(e));

@@ -86,6 +86,8 @@ struct FwdArgs {
   const float* eps_v;     // perturbation radius of expert e: eps_v[e * eps_stride]
   int eps_stride;
   int probe;              // probe law (kProbe*)
+  int ppb;                // directions per accumulation batch (direction j reads batch j / ppb)
+  int64_t bstride;        // bytes per accumulation batch, N B T
   int N, E, H, B, T, PC;  // PC = slot stride in directions
   int pcs;                // directions in this pass (grid extent)
   int j0;                 // first direction of the chunk
@@ -96,6 +98,12 @@ struct FwdArgs {
 };
 
 __device__ __forceinline__ float eps_of(const FwdArgs& a, int e) { return a.eps_v[int64_t(e) * a.eps_stride]; }
+
+// Expert e's batch [B][T] for direction j0 + jl of the pass (its
+// accumulation batch).
+__device__ __forceinline__ const uint8_t* bytes_of(const FwdArgs& a, int e, int jl) {
+  return a.bytes + int64_t((a.j0 + jl) / a.ppb) * a.bstride + int64_t(e) * a.B * a.T;
+}
 
 // ---------------------------------------------------------------------------
 // Layer-1 gate inputs per byte value (the vocabulary fold).
@@ -374,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
       const int64_t slot = slot0 + s;
       float4 gi;
       if (a.layer == 0) {
-        const int v = a.bytes[(static_cast<int64_t>(e) * B + b) * T + t];
+        const int v = bytes_of(a, e, jl)[static_cast<int64_t>(b) * T + t];
         gi = *reinterpret_cast<const float4*>(a.U + (slot * kVocab + v) * (4 * static_cast<int64_t>(H)) + 4 * unit);
       } else {
         gi = *reinterpret_cast<const float4*>(
@@ -467,7 +475,7 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
       const int64_t row = r0 + nb * 16 + lr;
       if (row < R) {
         const int64_t tt = row / B, b = row % B;
-        const int y = a.bytes[(static_cast<int64_t>(e) * B + b) * T + tt + 1];
+        const int y = bytes_of(a, e, jl)[b * T + tt + 1];
         if ((y >> 6) == wave && ((y >> 2) & 3) == lg) {
           const int ymb = (y >> 4) & 3, yr = y & 3;
           float v = 0.0f;
@@ -718,7 +726,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         a.layer == 0 ? buffer_of(a.U + slot * kVocab * H4, static_cast<uint32_t>(kVocab * H4 * sizeof(float)))
                      : buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(R * H4 * sizeof(float)));
     const __amdgpu_buffer_rsrc_t bbuf =
-        buffer_of(a.bytes + static_cast<int64_t>(e) * B * T, static_cast<uint32_t>(B * T));
+        buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
 
     // Perturbed recurrent weights of this lane, drawn once for the sequence.
     float4 w[KQ];
@@ -1042,7 +1050,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
   const __amdgpu_buffer_rsrc_t hbuf =
       buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(static_cast<int64_t>(R) * H * sizeof(float)));
   const __amdgpu_buffer_rsrc_t bbuf =
-      buffer_of(a.bytes + static_cast<int64_t>(e) * B * T, static_cast<uint32_t>(B * T));
+      buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
   float2* hp = hpart + (slot * 2 + vh) * R;
   float* tg = htgt + slot * R;
 

@@ -68,7 +68,7 @@ SCHEDULE_ENTRY_BYTES = 16   # soma_schedule_entry: lr, eps, best (fp32), since (
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "pair_chunk", "flags", "probe")]
+        "pair_chunk", "flags", "probe", "accum")]
 
 
 _lib = None
@@ -153,11 +153,17 @@ class Shape:
     pair_chunk: int = 0
     flags: int = 0
     probe: int = PROBE_GAUSSIAN
+    accum: int = 1
 
     def cfg(self) -> Config:
         return Config(self.n_experts, self.n_layers, self.embed, self.hidden, self.batch,
                       self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, self.flags,
-                      self.probe)
+                      self.probe, self.accum)
+
+    @property
+    def directions(self) -> int:
+        """Directions per update, n_pairs per accumulation batch."""
+        return self.n_pairs * max(1, self.accum)
 
 
 def param_count(shape: Shape) -> int:

@@ -235,3 +235,29 @@ def test_adam_step_matches_oracle(oracle_mod, name, probe):
         g = gh + hp["weight_decay"] * theta[e].astype(np.float64)
         _adam_compare([x[e] for x in got], (to, mo, vo), theta[e].astype(np.float64), g, float(np.float32(lr)),
                       1, True)
+
+
+@pytest.mark.parametrize("name,A,pc", [("ragged_l2", 3, 2), ("b64_h128", 2, 0), ("tiny", 2, 3)])
+def test_accumulated_step_matches_oracle(oracle_mod, name, A, pc):
+    """Accumulation over A independently sampled batches (direction j on
+    batch j / P): the persistent and streaming kernels (b64_h128), the tiled
+    ones (ragged_l2, H = 32), and direction chunks that straddle batches
+    (P = 3 with chunks of 2; P = 4 with chunks of 3)."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, _ = CASES[name]
+    shape = soma.Shape(N, L, E, H, B, T, P, mode, pc, accum=A)
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = np.stack([synth.expert_batches([100 + e for e in range(N)], B, T, data_seed=a) for a in range(A)])
+    seeds = synth.expert_seeds(N)
+    ctx = soma.Context(shape)
+    th = torch.from_numpy(theta.copy()).cuda()
+    losses = torch.zeros((N, A * P, 2), dtype=torch.float32, device="cuda")
+    ctx.spsa_step(th, soma.seeds_tensor(seeds), 0, eps, lr, torch.from_numpy(data).cuda(), losses)
+    torch.cuda.synchronize()
+    cfg = oracle_mod.cfg_from(shape)
+    o = oracle_mod.spsa_step(cfg, theta, seeds, 0, eps, lr, data)
+    assert_losses_close(losses.cpu().numpy(), o["losses"])
+    assert_theta_close(th.cpu().numpy(), o["theta"])
+    # the batches differ, so the accumulated losses are not one batch's repeated
+    lg = losses.cpu().numpy()
+    assert not np.array_equal(lg[:, :P], lg[:, P:2 * P])
