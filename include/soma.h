@@ -287,6 +287,22 @@ int soma_philox(const uint32_t* ctr_dev, const uint32_t* key_dev, uint32_t* out_
 int soma_box_muller(const uint32_t* wa_dev, const uint32_t* wb_dev, float* za_dev, float* zb_dev,
                     uint64_t n, void* stream);
 
+/* Variance harness (Appendix estimator-iso): moments of the single-direction
+ * estimates X_j = D c_{e,j} z_{e,j} of each expert from the coefficients
+ * coef_dev [N][D] of a step taken at fixed weights (lr = 0), probes
+ * regenerated from (seeds_dev, step):
+ *   out_dev[e][0] = sum_k sum_g (sum_{j in g} X_{j,k})^2 over the consecutive
+ *                   groups g of `group` directions (group divides D),
+ *   out_dev[e][1] = sum_k (sum_j X_{j,k})^2,
+ * fp64, out_dev [N][2] (device).  With G = D / group groups and group means
+ * Y_g = (1/group) sum_{j in g} X_j, the trace of their covariance across
+ * groups is (out[0] - out[1] / G) / (group^2 (G - 1)), and the relative
+ * centered variance of an n_pert = group estimate is R_g = that / ||g||^2
+ * (for group = 1: the single-probe covariance).  The summation order of the
+ * fp64 partial sums is not fixed (atomic adds). */
+int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds_dev, uint64_t step, const float* coef_dev,
+                           int32_t group, double* out_dev, void* stream);
+
 /* Per-phase device time of the last soma_spsa_step on a context, from HIP
  * events recorded on the step's stream between its kernel launches (off by
  * default; enabling adds one event record per phase boundary).  Times are

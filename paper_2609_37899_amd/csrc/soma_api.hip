@@ -337,6 +337,64 @@ __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, flo
   }
 }
 
+// Moments of the single-direction estimates X_j = D c_j z_j of each expert
+// (the coefficients of a step at fixed weights; Appendix estimator-iso):
+//   out[e][0] += sum_k sum_g (sum_{j in g} X_jk)^2  over consecutive groups
+//                of `group` directions,
+//   out[e][1] += sum_k (sum_j X_jk)^2,
+// in fp64, z regenerated per (quad, j).  Partial sums of a block are added
+// to out with fp64 atomics (summation order is not fixed).
+__global__ __launch_bounds__(256) void k_estimator_moments(const uint64_t* seeds, uint64_t step, const float* coef,
+                                                            int64_t d, int D, int group, int law, double* out) {
+  __shared__ double red[2][256];
+  const int e = blockIdx.y;
+  const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
+  double s0 = 0.0, s1 = 0.0;
+  if (4 * q < d) {
+    const uint2 key = stream_key(seeds[e], step);
+    const uint32_t step_lo = static_cast<uint32_t>(step);
+    const float* c = coef + int64_t(e) * D;
+    double gsum[4] = {0, 0, 0, 0}, tot[4] = {0, 0, 0, 0};
+    for (int j = 0; j < D; ++j) {
+      const float4 z = probe_quad(law, key, static_cast<uint32_t>(j), step_lo, 4 * static_cast<uint64_t>(q));
+      const double x = double(D) * double(c[j]);
+      const double zz[4] = {z.x, z.y, z.z, z.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gsum[i] += x * zz[i];
+      if ((j + 1) % group == 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (4 * q + i < d) s0 += gsum[i] * gsum[i];
+          tot[i] += gsum[i];
+          gsum[i] = 0.0;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (4 * q + i < d) s1 += tot[i] * tot[i];
+  }
+  red[0][threadIdx.x] = s0;
+  red[1][threadIdx.x] = s1;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (int(threadIdx.x) < w) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + w];
+      red[1][threadIdx.x] += red[1][threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    atomicAdd(&out[2 * e], red[0][0]);
+    atomicAdd(&out[2 * e + 1], red[1][0]);
+  }
+}
+
+__global__ void k_zero_f64(double* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.0;
+}
+
 // The plateau schedule (Section 4; Table experimental-setup): an expert's
 // learning rate and perturbation radius decay together, by `factor`, after
 // `patience` updates without its validation loss improving by more than
@@ -918,6 +976,25 @@ int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta, float* m, float* v, i
   if (int rc = adam_args(hp, t, &h)) return rc;
   return adam_step(ctx, theta, m, v, t, hp, seeds, step, schedule_rates(sched), bytes, losses,
                    as_stream(stream));
+}
+
+int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds, uint64_t step, const float* coef, int32_t group,
+                           double* out, void* stream) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (!seeds || !coef || !out) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (!aligned(out, 8) || !aligned(seeds, 8)) return fail(SOMA_EINVAL, "misaligned seeds or out");
+  const soma_config& c = ctx->cfg;
+  const int D = dirs(c);
+  if (group < 1 || D % group != 0) return fail(SOMA_EINVAL, "group must divide D = %d", D);
+  const hipStream_t st = as_stream(stream);
+  hipLaunchKernelGGL(soma::k_zero_f64, dim3((2 * c.n_experts + 255) / 256), dim3(256), 0, st, out,
+                     2 * c.n_experts);
+  if (int rc = check_launch("k_zero_f64")) return rc;
+  const int64_t quads = (ctx->lay.d + 3) / 4;
+  hipLaunchKernelGGL(soma::k_estimator_moments, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
+                     seeds, step, coef, ctx->lay.d, D, group, c.probe, out);
+  if (int rc = check_launch("k_estimator_moments")) return rc;
+  return ok();
 }
 
 int soma_schedule_init(soma_schedule_entry* sched, int32_t n, float lr0, float eps0, void* stream) {

@@ -22,7 +22,7 @@ FLAG_TILED_WEIGHTS = 2
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_spsa_step_adam", "soma_eval_loss", "soma_coefficients",
            "soma_apply_update", "soma_apply_adam", "soma_spsa_step_adam_sched", "soma_schedule_init",
-           "soma_schedule_observe",
+           "soma_schedule_observe", "soma_estimator_moments",
            "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
            "soma_get_phase_times",
            "soma_last_error")
@@ -97,6 +97,7 @@ def load():
             "soma_spsa_step_adam_sched": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam),
                                                          vp, u64, vp, vp, vp, vp]),
             "soma_schedule_init": (ctypes.c_int, [vp, ctypes.c_int32, f32, f32, vp]),
+            "soma_estimator_moments": (ctypes.c_int, [vp, vp, u64, vp, ctypes.c_int32, vp, vp]),
             "soma_schedule_observe": (ctypes.c_int, [vp, ctypes.c_int32, vp, ctypes.c_int32,
                                                      ctypes.POINTER(Plateau), vp]),
             "soma_eval_loss": (ctypes.c_int, [vp, vp, vp, vp, vp]),
@@ -232,6 +233,12 @@ class Context:
                                                 _dptr(bytes_, torch.uint8, "bytes"),
                                                 _dptr(losses, torch.float32, "losses"), _stream(stream)))
 
+    def estimator_moments(self, seeds, step: int, coef, group: int, out, stream=None):
+        import torch
+        _check(load().soma_estimator_moments(self._h, _dptr(seeds, torch.int64, "seeds"), int(step),
+                                             _dptr(coef, torch.float32, "coef"), int(group),
+                                             _dptr(out, torch.float64, "out"), _stream(stream)))
+
     def apply_adam(self, theta, m, v, t: int, adam, seeds, step: int, lr: float, coef, stream=None):
         import torch
         _check(load().soma_apply_adam(self._h, _dptr(theta, torch.float32, "theta"),
@@ -314,6 +321,15 @@ def box_muller(wa, wb, za, zb, stream=None):
     _check(load().soma_box_muller(_dptr(wa, torch.int32, "wa"), _dptr(wb, torch.int32, "wb"),
                                   _dptr(za, torch.float32, "za"), _dptr(zb, torch.float32, "zb"),
                                   wa.numel(), _stream(stream)))
+
+
+def group_covariance_trace(moments, directions: int, group: int):
+    """tr Cov of the group means of `group` consecutive single-direction
+    estimates, from soma_estimator_moments' two sums (per expert)."""
+    import numpy as np
+    m = np.asarray(moments, dtype=np.float64).reshape(-1, 2)
+    G = directions // group
+    return (m[:, 0] - m[:, 1] / G) / (group * group * (G - 1))
 
 
 def seeds_tensor(seeds, device="cuda"):
