@@ -42,7 +42,7 @@ def build(force: bool = False) -> str:
 class OracleCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "probe", "accum")]
+        "probe", "accum", "arch")] + [("tied_head", ctypes.c_void_p), ("head_stride", ctypes.c_int64)]
 
 
 def _load():
@@ -88,6 +88,7 @@ def _load():
                                                     f64p, f32p, f64p]),
                 "oracle_eval_loss": (ctypes.c_int, [cfgp, f32p, u8p, f64p]),
                 "oracle_num_threads": (ctypes.c_int, []),
+                "oracle_head_delta": (ctypes.c_double, [cfgp, f32p, u8p, f64p]),
             }
             for name, (res, args) in sig.items():
                 fn = getattr(lib, name)
@@ -101,19 +102,45 @@ def _ptr(a: np.ndarray, ctype):
     return a.ctypes.data_as(ctypes.POINTER(ctype))
 
 
+VOCAB = 256
 PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 
 
+ARCH_LSTM, ARCH_PAPER_BODY = 0, 1
+
+
 def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode=0,
-             probe=PROBE_GAUSSIAN, accum=1):
-    return OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe, accum)
+             probe=PROBE_GAUSSIAN, accum=1, arch=ARCH_LSTM, tied_head=None):
+    """tied_head (arch 1): the frozen tied matrix E, [V][d] (shared by all
+    experts) or [N][V][d] (one per expert); the configuration keeps it alive."""
+    cfg = OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe, accum,
+                    arch, None, 0)
+    if tied_head is not None:
+        h = np.ascontiguousarray(tied_head, dtype=np.float32)
+        cfg._head_ref = h
+        cfg.tied_head = h.ctypes.data
+        cfg.head_stride = 0 if h.ndim == 2 else VOCAB * hidden
+    return cfg
 
 
 def cfg_from(shape) -> OracleCfg:
     """Build the oracle's configuration from any object with the shape fields."""
     return make_cfg(shape.n_experts, shape.n_layers, shape.embed, shape.hidden, shape.batch,
                     shape.seq_len, shape.n_pairs, getattr(shape, "loss_mode", 0),
-                    getattr(shape, "probe", PROBE_GAUSSIAN), getattr(shape, "accum", 1))
+                    getattr(shape, "probe", PROBE_GAUSSIAN), getattr(shape, "accum", 1),
+                    getattr(shape, "arch", ARCH_LSTM), getattr(shape, "tied_head", None))
+
+
+def head_delta(cfg: OracleCfg, theta_e, bytes_e):
+    """(mean CE, dE [V][d] fp64): the decoder-path derivative of the
+    unperturbed loss with respect to the tied matrix (arch 1; one expert,
+    cfg.tied_head pointing at its E)."""
+    t = np.ascontiguousarray(theta_e, dtype=np.float32)
+    b = np.ascontiguousarray(bytes_e, dtype=np.uint8)
+    g = np.empty((VOCAB, cfg.hidden), dtype=np.float64)
+    loss = _load().oracle_head_delta(ctypes.byref(cfg), _ptr(t, ctypes.c_float), _ptr(b, ctypes.c_uint8),
+                                     _ptr(g, ctypes.c_double))
+    return float(loss), g
 
 
 def param_count(cfg: OracleCfg) -> int:

@@ -71,6 +71,9 @@ typedef struct {
   int32_t loss_mode; /* 0: independent per-expert losses, 1: summed loss */
   int32_t probe;     /* probe law: 0 Gaussian, 1 sparse Rademacher, 2 dense Rademacher */
   int32_t accum;     /* A accumulation batches per update (0 or 1: one batch) */
+  int32_t arch;      /* 0: stacked LSTM + linear head; 1: the paper's expert body (see below) */
+  const float *tied_head; /* arch 1: the frozen tied embedding/decoder E [V][d] of expert 0 */
+  int64_t head_stride;    /* floats from one expert's E to the next (0: one shared E) */
 } oracle_cfg;
 
 /* Directions per update: P per batch, A batches. */
@@ -89,8 +92,37 @@ static int64_t off_layer(const oracle_cfg *c, int l) {
   return off;
 }
 
+/* The paper's expert body (arch 1; Section 3 and Appendix C, Fig. arch):
+ * width d = embed = hidden; D = n_layers pre-norm residual blocks, each an
+ * LSTM sublayer and a GELU MLP (hidden 4d), both bias-free, with gain-only
+ * LayerNorm; a final gain-only LayerNorm; the frozen tied matrix E embeds the
+ * input byte and decodes logits = LN(x) E^T.  E is not part of theta.
+ * Body layout (canonical k), per block l: g1[d]; W[4d][2d] (gates i,f,g,o;
+ * columns [input | recurrent]); g2[d]; W1[4d][d]; W2[d][4d]; then g_f[d]:
+ * d_body = D (16 d^2 + 2 d) + d (the paper's 16 D d_t^2 + (2D + 1) d_t).
+ * LayerNorm(x; g) = g (x - mean) / sqrt(var + 1e-5) (biased variance over
+ * the d features); GELU(u) = u Phi(u) = u (1 + erf(u / sqrt 2)) / 2. */
+#define LN_EPS 1e-5
+
+static int64_t body_block(int64_t d) { return 16 * d * d + 2 * d; }
+
 int64_t oracle_param_count(const oracle_cfg *c) {
+  if (c->arch == 1) return c->n_layers * body_block(c->hidden) + c->hidden;
   return off_layer(c, c->n_layers) + (int64_t)VOCAB * c->hidden;
+}
+
+/* Whether coordinate k of the body is a LayerNorm gain. */
+static int body_is_gain(const oracle_cfg *c, int64_t k) {
+  const int64_t d = c->hidden, blk = body_block(d);
+  if (k >= c->n_layers * blk) return 1;               /* g_f */
+  const int64_t r = k % blk;
+  return r < d || (r >= d + 8 * d * d && r < 2 * d + 8 * d * d);
+}
+
+/* The probe law of coordinate k: under the paper's sparse law its
+ * normalization gains are dense +-1 (Appendix E); otherwise the configured law. */
+static int law_of(const oracle_cfg *c, int64_t k) {
+  return (c->arch == 1 && c->probe == 1 && body_is_gain(c, k)) ? 2 : c->probe;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -364,8 +396,126 @@ static double sequence_ce_sum(const oracle_cfg *c, const double *w, const uint8_
   return total;
 }
 
+static void layer_norm(const double *x, const double *g, int d, double *out) {
+  double mu = 0.0, var = 0.0;
+  for (int k = 0; k < d; ++k) mu += x[k];
+  mu /= d;
+  for (int k = 0; k < d; ++k) var += (x[k] - mu) * (x[k] - mu);
+  var /= d;
+  const double inv = 1.0 / sqrt(var + LN_EPS);
+  for (int k = 0; k < d; ++k) out[k] = g[k] * (x[k] - mu) * inv;
+}
+
+static double gelu(double u) { return 0.5 * u * (1.0 + erf(u / sqrt(2.0))); }
+
+/* Sum of next-byte cross entropies of one sequence under the paper's body
+ * (arch 1), E the frozen tied matrix [V][d] (fp64).  When dE != NULL the
+ * decoder-path derivative (p - onehot(y)) f^T of every target, f the decoder
+ * input, is added to dE [V][d] (Appendix E, Eq. delta, before the mean). */
+static double sequence_ce_sum_body(const oracle_cfg *c, const double *w, const double *E, const uint8_t *seq,
+                                   double *scratch, double *dE) {
+  const int D = c->n_layers, d = c->hidden, T = c->seq_len;
+  const int64_t blk = body_block(d);
+  double *h = scratch;                  /* [D][d] */
+  double *cs = h + (size_t)D * d;       /* [D][d] */
+  double *x = cs + (size_t)D * d;       /* [d] */
+  double *n = x + d;                    /* [d] */
+  double *a = n + d;                    /* [4d] */
+  double *u = a + 4 * (size_t)d;        /* [4d] */
+  double *logits = u + 4 * (size_t)d;   /* [V] */
+  memset(h, 0, sizeof(double) * 2 * (size_t)D * d);
+  const double *gf = w + D * blk;
+  double total = 0.0;
+  for (int t = 0; t + 1 < T; ++t) {
+    for (int k = 0; k < d; ++k) x[k] = E[(size_t)seq[t] * d + k];
+    for (int l = 0; l < D; ++l) {
+      const double *g1 = w + l * blk, *W = g1 + d, *g2 = W + 8 * (size_t)d * d;
+      const double *W1 = g2 + d, *W2 = W1 + 4 * (size_t)d * d;
+      double *hl = h + (size_t)l * d, *cl = cs + (size_t)l * d;
+      layer_norm(x, g1, d, n);                                   /* LSTM sublayer */
+      for (int r = 0; r < 4 * d; ++r) {
+        const double *wr = W + (size_t)r * 2 * d;
+        double acc = 0.0;
+        for (int k = 0; k < d; ++k) acc += wr[k] * n[k];
+        for (int k = 0; k < d; ++k) acc += wr[d + k] * hl[k];
+        a[r] = acc;
+      }
+      for (int q = 0; q < d; ++q) {
+        const double ig = sigmoid(a[q]), fg = sigmoid(a[d + q]), gg = tanh(a[2 * d + q]),
+                     og = sigmoid(a[3 * d + q]);
+        cl[q] = fg * cl[q] + ig * gg;
+        hl[q] = og * tanh(cl[q]);
+      }
+      for (int k = 0; k < d; ++k) x[k] += hl[k];                 /* residual */
+      layer_norm(x, g2, d, n);                                   /* MLP sublayer */
+      for (int r = 0; r < 4 * d; ++r) {
+        const double *wr = W1 + (size_t)r * d;
+        double acc = 0.0;
+        for (int k = 0; k < d; ++k) acc += wr[k] * n[k];
+        u[r] = gelu(acc);
+      }
+      for (int r = 0; r < d; ++r) {
+        const double *wr = W2 + (size_t)r * 4 * d;
+        double acc = 0.0;
+        for (int k = 0; k < 4 * d; ++k) acc += wr[k] * u[k];
+        x[r] += acc;                                             /* residual */
+      }
+    }
+    layer_norm(x, gf, d, n);                                     /* decoder input f */
+    double mx = -INFINITY;
+    for (int v = 0; v < VOCAB; ++v) {
+      double acc = 0.0;
+      for (int k = 0; k < d; ++k) acc += E[(size_t)v * d + k] * n[k];
+      logits[v] = acc;
+      if (acc > mx) mx = acc;
+    }
+    double se = 0.0;
+    for (int v = 0; v < VOCAB; ++v) se += exp(logits[v] - mx);
+    const int y = seq[t + 1];
+    total += log(se) + mx - logits[y];
+    if (dE)
+      for (int v = 0; v < VOCAB; ++v) {
+        const double pv = exp(logits[v] - mx) / se - (v == y ? 1.0 : 0.0);
+        for (int k = 0; k < d; ++k) dE[(size_t)v * d + k] += pv * n[k];
+      }
+  }
+  return total;
+}
+
+static double *head_f64(const oracle_cfg *c) {
+  const size_t nE = (size_t)VOCAB * c->hidden;
+  double *E = (double *)malloc(sizeof(double) * nE);
+  for (size_t i = 0; i < nE; ++i) E[i] = (double)c->tied_head[i];
+  return E;
+}
+
+/* The decoder-path derivative of the unperturbed mean cross entropy with
+ * respect to the tied matrix (Appendix E, Eq. delta), one expert (arch 1):
+ *   dE = (1 / (B (T-1))) sum_{b,t} (p_{b,t} - onehot(y_{b,t+1})) f_{b,t}^T,
+ * holding the decoder inputs f fixed.  grad [V][d] fp64 out.  Returns the
+ * mean cross entropy, or NaN for a configuration that is not arch 1. */
+double oracle_head_delta(const oracle_cfg *c, const float *theta, const uint8_t *bytes, double *grad) {
+  if (c->arch != 1 || !c->tied_head) return NAN;
+  const int B = c->batch, T = c->seq_len, d = c->hidden;
+  const int64_t nd = oracle_param_count(c);
+  double *w = (double *)malloc(sizeof(double) * (size_t)nd);
+  for (int64_t k = 0; k < nd; ++k) w[k] = (double)theta[k];
+  double *E = head_f64(c);
+  double *scratch = (double *)malloc(sizeof(double) * (4 * (size_t)c->n_layers * d + 12 * (size_t)d + VOCAB));
+  memset(grad, 0, sizeof(double) * (size_t)VOCAB * d);
+  double total = 0.0;
+  for (int b = 0; b < B; ++b) total += sequence_ce_sum_body(c, w, E, bytes + (size_t)b * T, scratch, grad);
+  const double inv = 1.0 / ((double)B * (double)(T - 1));
+  for (size_t i = 0; i < (size_t)VOCAB * d; ++i) grad[i] *= inv;
+  free(scratch);
+  free(E);
+  free(w);
+  return total * inv;
+}
+
 static size_t scratch_doubles(const oracle_cfg *c) {
   const size_t L = c->n_layers, E = c->embed, H = c->hidden;
+  if (c->arch == 1) return 2 * L * H + 10 * H + VOCAB;
   return 2 * L * H + (E > H ? E : H) + 4 * H + VOCAB;
 }
 
@@ -376,13 +526,17 @@ double oracle_forward_loss_f64(const oracle_cfg *c, const double *w, const uint8
   const int B = c->batch, T = c->seq_len;
   double *seq_sum = (double *)malloc(sizeof(double) * (size_t)B);
   const size_t ns = scratch_doubles(c);
+  double *E = c->arch == 1 ? head_f64(c) : NULL;
 #pragma omp parallel
   {
     double *scratch = (double *)malloc(sizeof(double) * ns);
 #pragma omp for schedule(dynamic, 1)
-    for (int b = 0; b < B; ++b) seq_sum[b] = sequence_ce_sum(c, w, bytes + (size_t)b * T, scratch);
+    for (int b = 0; b < B; ++b)
+      seq_sum[b] = c->arch == 1 ? sequence_ce_sum_body(c, w, E, bytes + (size_t)b * T, scratch, NULL)
+                                : sequence_ce_sum(c, w, bytes + (size_t)b * T, scratch);
     free(scratch);
   }
+  free(E);
   double total = 0.0;
   for (int b = 0; b < B; ++b) total += seq_sum[b];
   free(seq_sum);
@@ -404,7 +558,7 @@ void oracle_perturb(const oracle_cfg *c, const float *theta, uint64_t seed, uint
   const int64_t d = oracle_param_count(c);
   for (int64_t q = 0; 4 * q < d; ++q) {
     float z[4];
-    probe_quad(c->probe, seed, step, pair, (uint64_t)q, z);
+    probe_quad(law_of(c, 4 * q), seed, step, pair, (uint64_t)q, z);
     for (int i = 0; i < 4 && 4 * q + i < d; ++i) {
       int64_t k = 4 * q + i;
       w_out[k] = fmaf(sign_eps, z[i], theta[k]);
@@ -442,7 +596,7 @@ void oracle_apply_update(const oracle_cfg *c, const float *theta, uint64_t seed,
     double g = 0.0;
     for (int j = 0; j < P; ++j) {
       float z[4];
-      probe_quad(c->probe, seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
+      probe_quad(law_of(c, k & ~(int64_t)3), seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
       g += coef[j] * (double)z[k & 3];
     }
     theta_out[i] = (float)((double)theta[k] - (double)lr * g);
@@ -470,7 +624,7 @@ void oracle_apply_adam(const oracle_cfg *c, const float *theta, const float *m, 
     double gh = 0.0;
     for (int j = 0; j < P; ++j) {
       float z[4];
-      probe_quad(c->probe, seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
+      probe_quad(law_of(c, k & ~(int64_t)3), seed, step, (uint32_t)j, (uint64_t)k >> 2, z);
       gh += coef[j] * (double)z[k & 3];
     }
     const double th = (double)theta[k];
@@ -501,20 +655,24 @@ int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *se
                      float *theta_out, double *ghat) {
   const int N = c->n_experts, P = total_dirs(c), Pb = c->n_pairs;
   if (N < 1 || Pb < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
-      c->seq_len < 2 || c->probe < 0 || c->probe > 2 || c->accum < 0)
+      c->seq_len < 2 || c->probe < 0 || c->probe > 2 || c->accum < 0 || c->arch < 0 || c->arch > 1 ||
+      (c->arch == 1 && (c->embed != c->hidden || !c->tied_head)))
     return -1;
   const int64_t d = oracle_param_count(c);
   const size_t bstride = (size_t)c->batch * c->seq_len;
   double *L = (double *)malloc(sizeof(double) * (size_t)N * P * 2);
   /* 1-4: perturbed forwards, each on its expert's own batch (batch j / Pb of
    * the update for direction j). */
-  for (int e = 0; e < N; ++e)
+  for (int e = 0; e < N; ++e) {
+    oracle_cfg ce = *c;                      /* expert e's tied head (arch 1) */
+    if (c->tied_head) ce.tied_head = c->tied_head + e * c->head_stride;
     for (int j = 0; j < P; ++j)
       for (int s = 0; s < 2; ++s)
         L[((size_t)e * P + j) * 2 + s] =
-            oracle_perturbed_loss(c, theta + (size_t)e * d, seeds[e], step, (uint32_t)j,
+            oracle_perturbed_loss(&ce, theta + (size_t)e * d, seeds[e], step, (uint32_t)j,
                                   s == 0 ? +1 : -1, eps,
                                   bytes + ((size_t)(j / Pb) * N + e) * bstride);
+  }
   /* 5: coefficients. */
   double *cf = (double *)malloc(sizeof(double) * (size_t)N * P);
   const double denom = 2.0 * (double)eps * (double)P;
@@ -547,8 +705,11 @@ int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *se
 int oracle_eval_loss(const oracle_cfg *c, const float *theta, const uint8_t *bytes, double *loss) {
   const int64_t d = oracle_param_count(c);
   const size_t bstride = (size_t)c->batch * c->seq_len;
-  for (int e = 0; e < c->n_experts; ++e)
-    loss[e] = oracle_forward_loss(c, theta + (size_t)e * d, bytes + (size_t)e * bstride);
+  for (int e = 0; e < c->n_experts; ++e) {
+    oracle_cfg ce = *c;
+    if (c->tied_head) ce.tied_head = c->tied_head + e * c->head_stride;
+    loss[e] = oracle_forward_loss(&ce, theta + (size_t)e * d, bytes + (size_t)e * bstride);
+  }
   return 0;
 }
 
