@@ -16,7 +16,8 @@
  *   4. apply theta_e <- theta_e - lr * sum_j c_{e,j} z_{e,j}, regenerating
  *      every z_{e,j} from its counter instead of storing it.
  *
- * The model (Section 3 and Appendix C, bias-free) is: byte embedding
+ * The default model (soma_config.arch = SOMA_ARCH_LSTM; the paper's own
+ * body is SOMA_ARCH_BODY, below; both bias-free) is: byte embedding
  * Emb[256][E] -> L stacked LSTM layers (gate order i, f, g, o; h0 = c0 = 0
  * per sequence) -> linear head Whead[256][H] -> softmax cross entropy over
  * the 256 byte values (Appendix E, L_CE).  A sequence of T bytes gives T-1
@@ -104,6 +105,30 @@ enum soma_flags {
   SOMA_FLAG_TILED_WEIGHTS = 2
 };
 
+/* Expert architectures (soma_config.arch). */
+enum soma_arch {
+  /* The stacked LSTM with a perturbed byte embedding and an untied linear
+   * head (the layout above). */
+  SOMA_ARCH_LSTM = 0,
+  /* The paper's expert body (Section 3; Appendix C, Fig. arch): width
+   * d = embed = hidden, D = n_layers pre-norm residual blocks
+   *   x <- x + LSTM(LN(x; g1)),  x <- x + W2 GELU(W1 LN(x; g2)),
+   * bias-free, with a final f = LN(x; g_f) and logits = f E^T, where the
+   * tied matrix E [256][d] embeds the input byte (x_0 = E[byte]) and is set
+   * with soma_set_tied_head().  E is not perturbed and not part of theta.
+   * LN(x; g) = g (x - mean) / sqrt(var + 1e-5) (biased variance over the d
+   * features); GELU(u) = u Phi(u) with the exact normal CDF.  Parameters of
+   * one expert, canonical order, per block:
+   *   g1[d]; W[4d][2d] (gate rows i, f, g, o; columns [LN input | recurrent]);
+   *   g2[d]; W1[4d][d]; W2[d][4d];
+   * then g_f[d]: d_e = D (16 d^2 + 2 d) + d (the paper's 16 D d^2 + (2D+1) d).
+   * Under the sparse Rademacher law the gains g1, g2 and g_f draw dense
+   * +-1 (Appendix E); every other coordinate follows soma_config.probe.
+   * Supported: d in {16, 32}, D in {1, 2} (one perturbed body and E fit in
+   * one compute unit's LDS); flags must be 0. */
+  SOMA_ARCH_BODY = 1
+};
+
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;
  * embed and hidden positive multiples of 16; batch >= 1; seq_len >= 2;
  * accum >= 0; pair_chunk in [0, D] (0 picks a chunk that keeps the workspace
@@ -129,6 +154,7 @@ typedef struct soma_config {
   int32_t flags;      /* enum soma_flags, 0 by default */
   int32_t probe;      /* enum soma_probe_law, 0 (Gaussian) by default */
   int32_t accum;      /* A accumulation batches per update (0 or 1: one batch), see below */
+  int32_t arch;       /* enum soma_arch, 0 (stacked LSTM) by default */
 } soma_config;
 
 typedef struct soma_ctx soma_ctx;
@@ -251,6 +277,32 @@ int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta_dev, float* m_dev, flo
  *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8, loss_dev [N] fp32 out. */
 int soma_eval_loss(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev,
                    float* loss_dev, void* stream);
+
+/* The tied matrix E of an SOMA_ARCH_BODY context (Appendix C): expert e
+ * reads E_dev + e * expert_stride, [256][d] fp32 row-major (device, 16-byte
+ * aligned, expert_stride a multiple of 4 floats; 0 = one E shared by every
+ * expert, the paper's frozen width-32 head).  The context keeps the pointer,
+ * not a copy: the memory must stay valid and unchanged while any step or
+ * evaluation that reads it runs.  Every step, evaluation and
+ * soma_head_delta() on an SOMA_ARCH_BODY context returns SOMA_EINVAL until
+ * it is set; SOMA_EINVAL on an SOMA_ARCH_LSTM context. */
+int soma_set_tied_head(soma_ctx* ctx, float* E_dev, int64_t expert_stride);
+
+/* The decoder-path delta rule of an SOMA_ARCH_BODY context (Appendix E,
+ * Eq. delta): with the decoder inputs f_{b,t} of the unperturbed body held
+ * fixed, for every expert
+ *   grad_e = (1 / (B (T-1))) sum_{b,t} (softmax(E_e f_{b,t}) - onehot(y_{b,t+1})) f_{b,t}^T,
+ * a [256][d] matrix; the indirect path through the input embedding and the
+ * body is deliberately left out.
+ *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8 (device).
+ *   lr        if nonzero, also E_e <- E_e - lr grad_e in place (plain
+ *             descent on the rule; each expert must then own its E:
+ *             expert_stride != 0 or N = 1).
+ *   grad_dev  [N][256][d] fp32 out, or NULL.
+ *   loss_dev  [N] fp32 out (the unperturbed mean cross entropy, as
+ *             soma_eval_loss), or NULL. */
+int soma_head_delta(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev, float lr, float* grad_dev,
+                    float* loss_dev, void* stream);
 
 /* Copy the coefficients c[N][D] (fp32) of the last soma_spsa_step on this
  * context into coef_dev (device-to-device, on `stream`). */

@@ -13,7 +13,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "soma_api.hip")
-DEPS = [os.path.join(PKG, "csrc", f) for f in ("soma_api.hip", "soma_kernels.hpp", "soma_rng.hpp")] + \
+DEPS = [os.path.join(PKG, "csrc", f) for f in ("soma_api.hip", "soma_kernels.hpp", "soma_body.hpp", "soma_rng.hpp")] + \
        [os.path.join(ROOT, "include", "soma.h")]
 LIB = os.path.join(PKG, "libsoma.so")
 ARCH = os.environ.get("SOMA_OFFLOAD_ARCH", "gfx950")

@@ -22,6 +22,7 @@
 
 #include "soma.h"
 #include "soma_kernels.hpp"
+#include "soma_body.hpp"
 
 namespace {
 
@@ -58,12 +59,17 @@ struct Layout {
   int row_tiles = 0;   // head tiles per slot
   size_t sync = 0, rates = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, hpart = 0, htgt = 0,
          total = 0;
+  // the paper's body (SOMA_ARCH_BODY): decoder inputs, log-sum-exps and
+  // delta-rule partials of an evaluation pass
+  size_t fdec = 0, lse = 0, dpart = 0;
+  int delta_chunks = 0;
 };
 
 // Directions per update: n_pairs per accumulation batch, accum batches.
 int dirs(const soma_config& c) { return c.n_pairs * (c.accum > 1 ? c.accum : 1); }
 
 int64_t param_count_of(const soma_config& c) {
+  if (c.arch == SOMA_ARCH_BODY) return c.n_layers * soma::body_block(c.hidden) + c.hidden;
   int64_t d = int64_t(SOMA_VOCAB) * c.embed;
   for (int l = 0; l < c.n_layers; ++l)
     d += 4LL * c.hidden * ((l == 0 ? c.embed : c.hidden) + c.hidden);
@@ -91,6 +97,17 @@ int validate(const soma_config* c) {
   if (c->probe != SOMA_PROBE_GAUSSIAN && c->probe != SOMA_PROBE_SPARSE_RADEMACHER &&
       c->probe != SOMA_PROBE_RADEMACHER)
     return fail(SOMA_EINVAL, "probe must be 0 (Gaussian), 1 (sparse Rademacher) or 2 (Rademacher)");
+  if (c->arch != SOMA_ARCH_LSTM && c->arch != SOMA_ARCH_BODY)
+    return fail(SOMA_EINVAL, "arch must be 0 (stacked LSTM) or 1 (the paper's body)");
+  if (c->arch == SOMA_ARCH_BODY) {
+    if (c->embed != c->hidden || (c->hidden != 16 && c->hidden != 32) || c->n_layers > 2)
+      return fail(SOMA_ESHAPE, "the body needs embed = hidden in {16, 32} and n_layers in {1, 2} (got %d, %d, %d)",
+                  c->embed, c->hidden, c->n_layers);
+    if (c->flags) return fail(SOMA_EINVAL, "flags select stacked-LSTM kernels and must be 0 for the body");
+    const int64_t blocks = int64_t((c->batch + soma::kBodySeqs - 1) / soma::kBodySeqs) * c->n_experts * 2 *
+                           (int64_t(c->n_pairs) * (c->accum > 1 ? c->accum : 1));
+    if (blocks >= (int64_t(1) << 31)) return fail(SOMA_ESHAPE, "too many body blocks in one step");
+  }
   const int64_t d = param_count_of(*c);
   if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
   const int64_t rows = int64_t(c->seq_len - 1) * c->batch;
@@ -98,7 +115,29 @@ int validate(const soma_config* c) {
   return SOMA_OK;
 }
 
+Layout layout_for_body(const soma_config& c, int pc) {
+  Layout L;
+  L.d = param_count_of(c);
+  L.pc = pc;
+  const size_t N = c.n_experts, R = size_t(c.seq_len - 1) * c.batch, dm = c.hidden;
+  L.row_tiles = (c.batch + soma::kBodySeqs - 1) / soma::kBodySeqs;
+  L.delta_chunks = int((R + soma::kDeltaChunk - 1) / soma::kDeltaChunk);
+  const size_t slots = N * size_t(pc) * 2;
+  size_t at = 0;
+  L.sync = at; at += round_up(sizeof(unsigned) * (kMaxGroups + 1));
+  L.rates = at; at += round_up(sizeof(float) * 2 * N);
+  L.coef = at; at += round_up(sizeof(float) * N * dirs(c));
+  L.lossd = at; at += round_up(sizeof(double) * N * dirs(c) * 2);
+  L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
+  L.fdec = at; at += round_up(sizeof(float) * N * R * dm);
+  L.lse = at; at += round_up(sizeof(float) * N * R);
+  L.dpart = at; at += round_up(sizeof(float) * N * L.delta_chunks * SOMA_VOCAB * dm);
+  L.total = at;
+  return L;
+}
+
 Layout layout_for(const soma_config& c, int pc) {
+  if (c.arch == SOMA_ARCH_BODY) return layout_for_body(c, pc);
   Layout L;
   L.d = param_count_of(c);
   int64_t off = int64_t(SOMA_VOCAB) * c.embed;
@@ -130,6 +169,7 @@ Layout layout_for(const soma_config& c, int pc) {
 
 int choose_chunk(const soma_config& c) {
   if (c.pair_chunk > 0) return c.pair_chunk;
+  if (c.arch == SOMA_ARCH_BODY) return dirs(c);   // no per-direction buffers
   int pc = dirs(c);
   while (pc > 1 && layout_for(c, pc).total > kAutoBudget) --pc;
   return pc;
@@ -150,6 +190,8 @@ struct soma_ctx {
   bool have_times;
   // device facts for the persistent recurrence
   int coop_blocks;                  // co-resident k_rec_persist blocks (0: path unavailable)
+  float* head;                      // SOMA_ARCH_BODY: the tied matrix E of expert 0 (caller owned)
+  int64_t head_stride;              // floats from one expert's E to the next
   std::vector<hipEvent_t> events;   // pool, grows on demand
   std::vector<int> phase;           // phase closed by events[i]
   size_t nmarks;
@@ -265,6 +307,24 @@ __global__ void k_check_rates(const float* eps_v, int eps_stride, const float* l
     __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The probe law of each coordinate: one law for the stacked LSTM; for the
+// paper's body under the sparse law, dense +-1 on the LayerNorm gains
+// (Appendix E).  Gain ranges are whole probe quads (d is a multiple of 4).
+struct LawMap {
+  int law;
+  int layers;
+  int64_t blk;  // parameters per body block; 0: every coordinate has `law`
+  int64_t dm;   // body width
+};
+
+__device__ __forceinline__ int law_at(const LawMap& m, int64_t k4) {
+  if (m.blk == 0 || m.law != kProbeSparseRademacher) return m.law;
+  const int64_t l = k4 / m.blk;
+  if (l >= m.layers) return kProbeRademacher;                 // g_f
+  const int64_t r = k4 - l * m.blk, w = 8 * m.dm * m.dm;
+  return (r < m.dm || (r >= m.dm + w && r < 2 * m.dm + w)) ? kProbeRademacher : m.law;   // g1, g2
+}
+
 // g_hat[4q .. 4q+3] = sum_{j<P} coef[j] z_j[4q .. 4q+3] of one expert, summed
 // in j order in fp32 (each z regenerated from its counter).
 __device__ __forceinline__ float4 estimate_quad(uint2 key, uint32_t step_lo, const float* coef, int P, int law,
@@ -281,13 +341,13 @@ __device__ __forceinline__ float4 estimate_quad(uint2 key, uint32_t step_lo, con
 // thread (Section 4, Eq. main-spsa; the plain step on the estimate).
 __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* seeds, uint64_t step,
                                                  const float* lr_v, int lr_stride, const float* coef, int64_t d,
-                                                 int P, int law, const unsigned* err) {
+                                                 int P, LawMap lm, const unsigned* err) {
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
   if (err && *err) return;   // the step was aborted: theta stays as it was
   const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
-                                   coef + int64_t(e) * P, P, law, q);
+                                   coef + int64_t(e) * P, P, law_at(lm, 4 * q), q);
   const float lr = lr_v[int64_t(e) * lr_stride];
   float* t = theta + int64_t(e) * d + 4 * q;
   if (4 * q + 4 <= d) {
@@ -314,14 +374,14 @@ struct AdamArgs {
 // theta, m, v [N][d] fp32 in place, one probe quad per thread.
 __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, float* v, const uint64_t* seeds,
                                                       uint64_t step, AdamArgs h, const float* lr_v, int lr_stride,
-                                                      const float* coef, int64_t d, int P, int law,
+                                                      const float* coef, int64_t d, int P, LawMap lm,
                                                       const unsigned* err) {
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
   if (err && *err) return;   // the step was aborted: theta, m, v stay as they were
   const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
-                                   coef + int64_t(e) * P, P, law, q);
+                                   coef + int64_t(e) * P, P, law_at(lm, 4 * q), q);
   const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
   const float lr = lr_v[int64_t(e) * lr_stride];
   const int64_t base = int64_t(e) * d + 4 * q;
@@ -345,7 +405,7 @@ __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, flo
 // in fp64, z regenerated per (quad, j).  Partial sums of a block are added
 // to out with fp64 atomics (summation order is not fixed).
 __global__ __launch_bounds__(256) void k_estimator_moments(const uint64_t* seeds, uint64_t step, const float* coef,
-                                                            int64_t d, int D, int group, int law, double* out) {
+                                                            int64_t d, int D, int group, LawMap lm, double* out) {
   __shared__ double red[2][256];
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
@@ -354,6 +414,7 @@ __global__ __launch_bounds__(256) void k_estimator_moments(const uint64_t* seeds
     const uint2 key = stream_key(seeds[e], step);
     const uint32_t step_lo = static_cast<uint32_t>(step);
     const float* c = coef + int64_t(e) * D;
+    const int law = law_at(lm, 4 * q);
     double gsum[4] = {0, 0, 0, 0}, tot[4] = {0, 0, 0, 0};
     for (int j = 0; j < D; ++j) {
       const float4 z = probe_quad(law, key, static_cast<uint32_t>(j), step_lo, 4 * static_cast<uint64_t>(q));
@@ -579,12 +640,58 @@ int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, h
   return SOMA_OK;
 }
 
+// The paper's body: one fused launch per pass (SOMA_ARCH_BODY).
+template <int DW, int D, bool kPert>
+void launch_body_t(const soma::BodyArgs& a, unsigned blocks, hipStream_t st) {
+  hipLaunchKernelGGL((soma::k_body<DW, D, kPert>), dim3(blocks), dim3(soma::kBodyThreads), 0, st, a);
+}
+
+template <bool kPert>
+int run_body(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, const float* eps_v,
+             int eps_stride, const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
+  const soma_config& c = ctx->cfg;
+  const Layout& L = ctx->lay;
+  soma::BodyArgs a{};
+  a.theta = theta;
+  a.bytes = bytes;
+  a.seeds = seeds;
+  a.E = ctx->head;
+  a.e_stride = ctx->head_stride;
+  a.part = reinterpret_cast<double*>(ctx->ws + L.part);
+  a.fdec = reinterpret_cast<float*>(ctx->ws + L.fdec);
+  a.lse = reinterpret_cast<float*>(ctx->ws + L.lse);
+  a.d = L.d;
+  a.step = step;
+  a.eps_v = eps_v;
+  a.eps_stride = eps_stride;
+  a.probe = c.probe;
+  a.ppb = kPert ? c.n_pairs : 1;
+  a.bstride = kPert ? int64_t(c.n_experts) * c.batch * c.seq_len : 0;
+  a.N = c.n_experts;
+  a.B = c.batch;
+  a.T = c.seq_len;
+  a.PC = kPert ? L.pc : 1;
+  a.pcs = pcs;
+  a.j0 = j0;
+  a.btiles = L.row_tiles;
+  const unsigned blocks = unsigned(L.row_tiles) * unsigned(c.n_experts) * unsigned(pcs) * (kPert ? 2u : 1u);
+  const bool wide = c.hidden == 32, deep = c.n_layers == 2;
+  if (wide && deep) launch_body_t<2, 2, kPert>(a, blocks, st);
+  else if (wide) launch_body_t<2, 1, kPert>(a, blocks, st);
+  else if (deep) launch_body_t<1, 2, kPert>(a, blocks, st);
+  else launch_body_t<1, 1, kPert>(a, blocks, st);
+  if (int rc = check_launch("k_body")) return rc;
+  ctx->rec_launches += 1;
+  return mark(ctx, kPhaseRec, st);
+}
+
 // Forward passes of `pcs` directions starting at j0 (kPert) or of the
 // unperturbed experts (!kPert, pcs = 1), ending with per-tile loss sums.
 template <bool kPert>
 int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, const float* eps_v,
                 int eps_stride, const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
   const soma_config& c = ctx->cfg;
+  if (c.arch == SOMA_ARCH_BODY) return run_body<kPert>(ctx, theta, seeds, step, eps_v, eps_stride, bytes, j0, pcs, st);
   const Layout& L = ctx->lay;
   soma::FwdArgs a{};
   a.theta = theta;
@@ -723,7 +830,8 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
     // Co-resident blocks for the persistent recurrence on the current device.
     int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
     hipFuncAttributes fa{};
-    const bool shape_ok = cfg->hidden % 64 == 0 && cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
+    const bool shape_ok = cfg->arch == SOMA_ARCH_LSTM && cfg->hidden % 64 == 0 &&
+                          cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
     const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden, cfg->probe) : nullptr;
     if (kern && hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
@@ -736,6 +844,8 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
     }
     (void)hipGetLastError();  // a failed query only disables the persistent path
   }
+  ctx->head = nullptr;
+  ctx->head_stride = 0;
   ctx->timing = false;
   ctx->have_times = false;
   ctx->nmarks = 0;
@@ -809,10 +919,18 @@ Rates schedule_rates(const soma_schedule_entry* sched) {
   return Rates{&sched->eps, kStride, &sched->lr, kStride};
 }
 
+// The paper's body decodes through the caller's tied matrix: it must be set.
+int check_head(const soma_ctx* ctx) {
+  if (ctx->cfg.arch == SOMA_ARCH_BODY && !ctx->head)
+    return fail(SOMA_EINVAL, "no tied matrix E: call soma_set_tied_head first");
+  return SOMA_OK;
+}
+
 // Arguments of a step that every update checks (rates apart).
 int check_step_ptrs(soma_ctx* ctx, const float* theta, const uint64_t* seeds, const uint8_t* bytes,
                     const float* losses) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (int rc = check_head(ctx)) return rc;
   if (!theta || !seeds || !bytes || !losses) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
   if (!aligned(seeds, 8) || !aligned(losses, 4)) return fail(SOMA_EINVAL, "misaligned seeds or losses");
@@ -893,12 +1011,18 @@ int check_state(const float* m, const float* v) {
   return SOMA_OK;
 }
 
+soma::LawMap law_map(const soma_config& c) {
+  soma::LawMap m{c.probe, c.n_layers, 0, c.hidden};
+  if (c.arch == SOMA_ARCH_BODY) m.blk = soma::body_block(c.hidden);
+  return m;
+}
+
 int launch_sgd(const soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_t step, const Rates& r,
                const float* coef, const unsigned* err, hipStream_t st) {
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st, theta,
-                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), c.probe, err);
+                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), law_map(c), err);
   return check_launch("k_update");
 }
 
@@ -907,7 +1031,7 @@ int launch_adam(const soma_ctx* ctx, float* theta, float* m, float* v, const uin
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update_adam, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
-                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), c.probe, err);
+                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), law_map(c), err);
   return check_launch("k_update_adam");
 }
 
@@ -992,7 +1116,7 @@ int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds, uint64_t step, 
   if (int rc = check_launch("k_zero_f64")) return rc;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_estimator_moments, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
-                     seeds, step, coef, ctx->lay.d, D, group, c.probe, out);
+                     seeds, step, coef, ctx->lay.d, D, group, law_map(c), out);
   if (int rc = check_launch("k_estimator_moments")) return rc;
   return ok();
 }
@@ -1043,6 +1167,7 @@ int soma_apply_adam(soma_ctx* ctx, float* theta, float* m, float* v, int64_t t, 
 int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, float* loss,
                    void* stream) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (int rc = check_head(ctx)) return rc;
   if (!theta || !bytes || !loss) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
   const soma_config& c = ctx->cfg;
@@ -1059,6 +1184,64 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
                      1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr),
                      static_cast<const unsigned*>(nullptr));
   if (int rc = check_launch("k_loss_reduce")) return rc;
+  return ok();
+}
+
+int soma_set_tied_head(soma_ctx* ctx, float* E, int64_t expert_stride) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  if (ctx->cfg.arch != SOMA_ARCH_BODY) return fail(SOMA_EINVAL, "the stacked LSTM has no tied matrix");
+  if (!E || !aligned(E, 16)) return fail(SOMA_EINVAL, "E must be a 16-byte aligned device pointer");
+  if (expert_stride < 0 || expert_stride % 4)
+    return fail(SOMA_EINVAL, "expert_stride must be >= 0 and a multiple of 4 floats");
+  if (expert_stride > 0 && expert_stride < int64_t(SOMA_VOCAB) * ctx->cfg.hidden)
+    return fail(SOMA_EINVAL, "experts' tied matrices must not overlap (stride %lld < %d)",
+                static_cast<long long>(expert_stride), SOMA_VOCAB * ctx->cfg.hidden);
+  ctx->head = E;
+  ctx->head_stride = expert_stride;
+  return ok();
+}
+
+int soma_head_delta(soma_ctx* ctx, const float* theta, const uint8_t* bytes, float lr, float* grad, float* loss,
+                    void* stream) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  const soma_config& c = ctx->cfg;
+  if (c.arch != SOMA_ARCH_BODY) return fail(SOMA_EINVAL, "the delta rule needs the paper's body (arch 1)");
+  if (int rc = check_head(ctx)) return rc;
+  if (!theta || !bytes) return fail(SOMA_EINVAL, "NULL device pointer");
+  if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
+  if ((grad && !aligned(grad, 4)) || (loss && !aligned(loss, 4))) return fail(SOMA_EINVAL, "misaligned output");
+  if (!std::isfinite(lr)) return fail(SOMA_EINVAL, "lr must be finite");
+  if (lr != 0.0f && ctx->head_stride == 0 && c.n_experts > 1)
+    return fail(SOMA_EINVAL, "updating E needs one tied matrix per expert (expert_stride != 0)");
+  const Layout& L = ctx->lay;
+  const hipStream_t st = as_stream(stream);
+  const bool timing = ctx->timing;
+  ctx->timing = false;
+  const int rc0 = run_body<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
+  ctx->timing = timing;
+  if (rc0) return rc0;
+  const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
+  if (loss) {
+    hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1, 1, 1, 1, 0,
+                       inv_rows, loss, static_cast<double*>(nullptr), static_cast<const unsigned*>(nullptr));
+    if (int rc = check_launch("k_loss_reduce")) return rc;
+  }
+  float* dpart = reinterpret_cast<float*>(ctx->ws + L.dpart);
+  const dim3 pgrid(L.delta_chunks, c.n_experts);
+  const float* fdec = reinterpret_cast<const float*>(ctx->ws + L.fdec);
+  const float* lse = reinterpret_cast<const float*>(ctx->ws + L.lse);
+  if (c.hidden == 32)
+    hipLaunchKernelGGL((soma::k_head_delta_part<2>), pgrid, dim3(256), 0, st, fdec, lse, bytes, ctx->head,
+                       ctx->head_stride, c.batch, c.seq_len, L.delta_chunks, dpart);
+  else
+    hipLaunchKernelGGL((soma::k_head_delta_part<1>), pgrid, dim3(256), 0, st, fdec, lse, bytes, ctx->head,
+                       ctx->head_stride, c.batch, c.seq_len, L.delta_chunks, dpart);
+  if (int rc = check_launch("k_head_delta_part")) return rc;
+  const int64_t vd = int64_t(SOMA_VOCAB) * c.hidden;
+  hipLaunchKernelGGL(soma::k_head_delta_reduce, dim3(unsigned((vd + 255) / 256), c.n_experts), dim3(256), 0, st,
+                     dpart, L.delta_chunks, vd, inv_rows, grad, ctx->head, ctx->head_stride, lr);
+  if (int rc = check_launch("k_head_delta_reduce")) return rc;
   return ok();
 }
 

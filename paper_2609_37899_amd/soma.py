@@ -18,11 +18,12 @@ LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
 PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
+ARCH_LSTM, ARCH_BODY = 0, 1
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_spsa_step_adam", "soma_eval_loss", "soma_coefficients",
            "soma_apply_update", "soma_apply_adam", "soma_spsa_step_adam_sched", "soma_schedule_init",
-           "soma_schedule_observe", "soma_estimator_moments",
+           "soma_schedule_observe", "soma_estimator_moments", "soma_set_tied_head", "soma_head_delta",
            "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
            "soma_get_phase_times",
            "soma_last_error")
@@ -68,7 +69,7 @@ SCHEDULE_ENTRY_BYTES = 16   # soma_schedule_entry: lr, eps, best (fp32), since (
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "pair_chunk", "flags", "probe", "accum")]
+        "pair_chunk", "flags", "probe", "accum", "arch")]
 
 
 _lib = None
@@ -101,6 +102,8 @@ def load():
             "soma_schedule_observe": (ctypes.c_int, [vp, ctypes.c_int32, vp, ctypes.c_int32,
                                                      ctypes.POINTER(Plateau), vp]),
             "soma_eval_loss": (ctypes.c_int, [vp, vp, vp, vp, vp]),
+            "soma_set_tied_head": (ctypes.c_int, [vp, vp, ctypes.c_int64]),
+            "soma_head_delta": (ctypes.c_int, [vp, vp, vp, f32, vp, vp, vp]),
             "soma_coefficients": (ctypes.c_int, [vp, vp, vp]),
             "soma_apply_update": (ctypes.c_int, [vp, vp, vp, u64, f32, vp, vp]),
             "soma_gaussian": (ctypes.c_int, [u64, u64, u32, u64, u64, vp, vp]),
@@ -155,11 +158,12 @@ class Shape:
     flags: int = 0
     probe: int = PROBE_GAUSSIAN
     accum: int = 1
+    arch: int = ARCH_LSTM
 
     def cfg(self) -> Config:
         return Config(self.n_experts, self.n_layers, self.embed, self.hidden, self.batch,
                       self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, self.flags,
-                      self.probe, self.accum)
+                      self.probe, self.accum, self.arch)
 
     @property
     def directions(self) -> int:
@@ -259,6 +263,24 @@ class Context:
         _check(load().soma_eval_loss(self._h, _dptr(theta, torch.float32, "theta"),
                                      _dptr(bytes_, torch.uint8, "bytes"),
                                      _dptr(loss, torch.float32, "loss"), _stream(stream)))
+
+    def set_tied_head(self, E, per_expert: bool = False):
+        """The tied matrix of a body context: E [V][d] shared by every expert,
+        or [N][V][d] one per expert (per_expert=True).  The context reads the
+        tensor's memory on every later call: keep it alive."""
+        import torch
+        stride = E.shape[-2] * E.shape[-1] if per_expert else 0
+        _check(load().soma_set_tied_head(self._h, _dptr(E, torch.float32, "E"), stride))
+        self._head = E
+
+    def head_delta(self, theta, bytes_, lr: float = 0.0, grad=None, loss=None, stream=None):
+        """The decoder-path delta rule: grad [N][V][d] and loss [N] (either may
+        be None); with lr != 0 the tied matrix is also moved by -lr grad."""
+        import torch
+        g = _dptr(grad, torch.float32, "grad") if grad is not None else None
+        lo = _dptr(loss, torch.float32, "loss") if loss is not None else None
+        _check(load().soma_head_delta(self._h, _dptr(theta, torch.float32, "theta"),
+                                      _dptr(bytes_, torch.uint8, "bytes"), float(lr), g, lo, _stream(stream)))
 
     def coefficients(self, coef, stream=None):
         import torch

@@ -142,6 +142,42 @@ def init_theta(n_experts: int, n_layers: int, embed: int, hidden: int, init_seed
     return np.stack(rows)
 
 
+def body_param_count(n_layers: int, d: int) -> int:
+    """Size of one expert's parameter vector under the paper's body: per
+    block g1[d], W[4d][2d], g2[d], W1[4d][d], W2[d][4d], then g_f[d]."""
+    return n_layers * (16 * d * d + 2 * d) + d
+
+
+def init_body(n_experts: int, n_layers: int, d: int, init_seed: int = 0, distinct: bool = False) -> np.ndarray:
+    """[N][d_e] float32 for the paper's body: gains 1 + 0.1 N(0, 1) (away
+    from 1 so that a gain that is skipped shows), matrices U(-a, a) with
+    a = 1 / sqrt(fan-in)."""
+    rows = []
+    for e in range(n_experts if distinct else 1):
+        ss = np.random.SeedSequence([int(init_seed), e, 7] if distinct else [int(init_seed), 7])
+        g = np.random.Generator(np.random.PCG64(ss))
+        parts = []
+        for _ in range(n_layers):
+            parts += [1.0 + 0.1 * g.standard_normal(d),
+                      g.uniform(-1, 1, 8 * d * d) / np.sqrt(2 * d),
+                      1.0 + 0.1 * g.standard_normal(d),
+                      g.uniform(-1, 1, 4 * d * d) / np.sqrt(d),
+                      g.uniform(-1, 1, 4 * d * d) / np.sqrt(4 * d)]
+        parts.append(1.0 + 0.1 * g.standard_normal(d))
+        rows.append(np.concatenate(parts).astype(np.float32))
+    if not distinct:
+        rows = rows * n_experts
+    return np.stack(rows)
+
+
+def init_tied_head(d: int, init_seed: int = 0, n_experts: int = 0, scale: float = 0.3) -> np.ndarray:
+    """The tied matrix E, N(0, scale^2) entries: [V][d] (shared), or
+    [n_experts][V][d] (one per expert) when n_experts > 0."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(init_seed), 11])))
+    shape = (n_experts, VOCAB, d) if n_experts > 0 else (VOCAB, d)
+    return (scale * g.standard_normal(shape)).astype(np.float32)
+
+
 def expert_seeds(n_experts: int, base: int = 0x50A10000) -> np.ndarray:
     """Per-expert perturbation stream seeds."""
     return np.arange(n_experts, dtype=np.uint64) + np.uint64(base)

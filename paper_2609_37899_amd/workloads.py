@@ -9,7 +9,7 @@ from __future__ import annotations
 
 from dataclasses import dataclass, field, replace
 
-from .synth import param_count
+from .synth import body_param_count, param_count
 
 
 @dataclass(frozen=True)
@@ -28,15 +28,24 @@ class Workload:
     cluster_seeds: tuple = field(default=())
     pool_clusters: bool = False
     init_seed: int = 0
+    arch: int = 0               # 0 stacked LSTM, 1 the paper's body (width embed = hidden)
+    probe: int = 0              # probe law: 0 Gaussian, 1 sparse Rademacher, 2 Rademacher
 
     @property
     def params_per_expert(self) -> int:
+        if self.arch == 1:
+            return body_param_count(self.n_layers, self.hidden)
         return param_count(self.n_layers, self.embed, self.hidden)
 
     @property
     def flops_per_token(self) -> int:
         """Contraction work per target token of one perturbed forward:
-        2 * sum_l (in_l + H) * 4H + 2 * H * V (elementwise work excluded)."""
+        2 * sum_l (in_l + H) * 4H + 2 * H * V for the stacked LSTM, and
+        2 * (D * 16 d^2 + d * V) for the paper's body (per block the gate
+        matrix 8 d^2, W1 4 d^2, W2 4 d^2; the decoder d V); elementwise work
+        excluded."""
+        if self.arch == 1:
+            return 2 * (self.n_layers * 16 * self.hidden * self.hidden + self.hidden * 256)
         f = 0
         for l in range(self.n_layers):
             f += 2 * ((self.embed if l == 0 else self.hidden) + self.hidden) * 4 * self.hidden
@@ -60,4 +69,10 @@ MONOLITH = Workload("monolith_l2_h704", 1, 2, 704, 704, 64, 256, 128,
 SOMA_N256 = Workload("soma_n256_l1_h64", 256, 1, 32, 64, 16, 256, 32,
                      cluster_seeds=tuple(1000 + c for c in range(256)))
 
-ALL = {w.name: w for w in (TINY, SOMA_N2, SOMA_N4, MONOLITH, SOMA_N256)}
+# The paper's width-32 expert (Appendix C: D = 2 blocks, d_t = 32, frozen
+# tied E; Appendix E: sparse Rademacher probes, n_pert = 64 directions, B = 64
+# sequences of 1,024 bytes), eight experts on the GPU at once.
+PAPER_BODY_N8 = Workload("paper_body_n8_d32", 8, 2, 32, 32, 64, 1024, 64,
+                         cluster_seeds=tuple(1000 + c for c in range(8)), arch=1, probe=1)
+
+ALL = {w.name: w for w in (TINY, SOMA_N2, SOMA_N4, MONOLITH, SOMA_N256, PAPER_BODY_N8)}

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
 
 def shape_of(w, **kw):
     s = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
-                   w.loss_mode)
+                   w.loss_mode, probe=w.probe, arch=w.arch)
     for k, v in kw.items():
         setattr(s, k, v)
     return s
