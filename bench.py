@@ -42,9 +42,9 @@ def parse():
     ap.add_argument("--optimizer", choices=("sgd", "adam"), default="sgd",
                     help="update: the plain step on the estimate, or the paper's Adam-style update "
                          "(beta 0.9/0.999, delta 1e-8, coupled decay 1e-4) with fp32 moments")
-    ap.add_argument("--probe", choices=sorted(PROBE_LAWS), default="gaussian",
-                    help="probe law: gaussian (the workload's), sparse (the paper's training law: "
-                         "0 w.p. 1/2, +-1 w.p. 1/4) or dense (+-1)")
+    ap.add_argument("--probe", choices=sorted(PROBE_LAWS), default=None,
+                    help="probe law (default: the workload's own): gaussian, sparse (the paper's "
+                         "training law: 0 w.p. 1/2, +-1 w.p. 1/4) or dense (+-1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-kernel HBM bytes from rocprofv3 counter runs (JSON), if present")
@@ -58,13 +58,14 @@ def parse():
 
 
 KERNEL_SOURCES = ("paper_2609_37899_amd/csrc/soma_kernels.hpp", "paper_2609_37899_amd/csrc/soma_rng.hpp")
+BODY_SOURCES = KERNEL_SOURCES + ("paper_2609_37899_amd/csrc/soma_body.hpp",)
 
 
-def kernel_source_hash() -> str:
-    """Hash of the kernel sources: stored traffic figures apply only to these."""
+def kernel_source_hash(kernel: str = "") -> str:
+    """Hash of a kernel's sources: stored traffic figures apply only to these."""
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in (BODY_SOURCES if kernel == "k_body" else KERNEL_SOURCES):
         h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -88,6 +89,8 @@ def kernel_flops(w):
                            w.n_layers)
     fwd = N * 2 * P                  # perturbed forwards
     tok = B * (T - 1)                # target tokens per forward
+    if w.arch == 1:                  # the paper's body: one fused kernel does every product
+        return {"rec": fwd * tok * w.flops_per_token, "proj": 0, "fold": 0, "head": 0}
     rec = fwd * tok * L * 2 * H * 4 * H
     proj = fwd * tok * (L - 1) * 2 * H * 4 * H
     emb_in = fwd * tok * 2 * E * 4 * H     # layer-1 input contraction (executed once per byte value)
@@ -95,13 +98,11 @@ def kernel_flops(w):
     return {"rec": rec, "proj": proj, "fold": emb_in, "head": head}
 
 
-def cpu_baseline(w, theta, data, seeds, probe=0):
+def cpu_baseline(w, theta, data, seeds, probe=0, tied_head=None):
     """Time the oracle on a bounded sample of the workload."""
-    import numpy as np
-
     import oracle
-    cfg = oracle.cfg_from(w)
-    cfg.probe = probe
+    cfg = oracle.make_cfg(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
+                          w.loss_mode, probe, arch=w.arch, tied_head=tied_head)
     threads = oracle.num_threads()
     if w.perturbed_tokens * w.flops_per_token < 2e10:
         t0 = time.perf_counter()
@@ -147,7 +148,12 @@ def main():
     if args.pairs:
         w = w.with_(n_pairs=args.pairs)
     # Inputs are drawn (with a worker pool) before anything touches the GPU.
-    theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
+    tied = None
+    if w.arch == 1:   # the paper's width-32 recipe: one frozen tied E shared by every expert
+        theta0 = synth.init_body(w.n_experts, w.n_layers, w.hidden, w.init_seed)
+        tied = synth.init_tied_head(w.hidden, init_seed=1)
+    else:
+        theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
     nb = max(1, min(args.steps + args.warmup, 3))
     batches = [synth.expert_batches(w.cluster_seeds, w.batch, w.seq_len, data_seed=i,
                                     pool=w.pool_clusters,
@@ -156,11 +162,15 @@ def main():
     seeds_np = synth.expert_seeds(w.n_experts)
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    probe = PROBE_LAWS[args.probe]
+    probe = PROBE_LAWS[args.probe] if args.probe else w.probe
+    probe_name = {v: k for k, v in PROBE_LAWS.items()}[probe]
     shape = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
-                       w.loss_mode, args.pair_chunk, probe=probe)
+                       w.loss_mode, args.pair_chunk, probe=probe, arch=w.arch)
 
     ctx = soma.Context(shape, device=dev)
+    if tied is not None:
+        dtied = torch.from_numpy(tied).to(dev)
+        ctx.set_tied_head(dtied)
     theta = torch.from_numpy(theta0.copy()).to(dev)
     seeds = soma.seeds_tensor(seeds_np, dev)
     dbatches = [torch.from_numpy(b).to(dev) for b in batches]
@@ -212,12 +222,14 @@ def main():
     achieved = per_launch_flops / avg_launch_s / 1e12
     traffic = None
     kname = {"rec": "k_rec_step", "proj": "k_proj", "fold": "k_fold", "head": "k_head_ce"}[dom]
-    if dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
+    if w.arch == 1:
+        kname = "k_body"          # the whole perturbed forward, one launch per direction chunk
+    elif dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
         kname = "k_rec_persist"   # one persistent launch per layer and direction chunk
     if os.path.exists(args.traffic):
         try:
             ent = json.load(open(args.traffic)).get(w.name, {}).get(kname)
-            if ent and ent.get("source_hash") == kernel_source_hash():
+            if ent and ent.get("source_hash") == kernel_source_hash(kname):
                 traffic = ent["hbm_bytes_per_launch"]
         except (OSError, ValueError, KeyError):
             traffic = None
@@ -225,7 +237,7 @@ def main():
             "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_FP32_MFMA_TFLOPS, 4), "traffic": traffic,
             "flops_per_launch": per_launch_flops, "avg_launch_ms": round(avg_launch_s * 1e3, 4),
-            "launches_per_step": launches[dom], "kernel_source_hash": kernel_source_hash()}
+            "launches_per_step": launches[dom], "kernel_source_hash": kernel_source_hash(kname)}
     total_flops = w.perturbed_tokens * w.flops_per_token
     out = {
         "metric": METRIC,
@@ -246,7 +258,9 @@ def main():
                    "n_pairs": w.n_pairs, "forwards_per_expert": 2 * w.n_pairs,
                    "params_per_expert": w.params_per_expert, "eps": w.eps, "lr": w.lr,
                    "loss_mode": "summed" if w.loss_mode else "independent",
-                   "probe": args.probe, "optimizer": args.optimizer,
+                   "probe": probe_name, "optimizer": args.optimizer,
+                   "architecture": "paper body (pre-norm residual LSTM + GELU MLP, frozen tied E)"
+                   if w.arch == 1 else "stacked LSTM, untied head",
                    "parallelism": "single GPU, all experts and directions in each launch"},
         "algorithmic_tflops": round(total_flops / sec / 1e12, 3),
         "phase_ms": {k: round(v, 3) for k, v in ms.items()},
@@ -254,7 +268,7 @@ def main():
         "mean_loss": float(np.mean(lv)),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, theta0, batches[0], seeds_np, probe)
+        out["cpu_baseline"] = cpu_baseline(w, theta0, batches[0], seeds_np, probe, tied)
     print(json.dumps(out), flush=True)
 
 

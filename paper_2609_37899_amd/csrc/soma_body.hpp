@@ -11,25 +11,37 @@
 // once per block while the weights are written to LDS, and HBM sees only the
 // input bytes and one loss sum per block.
 //
-// Register layout.  Each wave owns 16 sequences (MFMA columns).  A length-n
-// activation vector of sequence c lives in lanes c, c+16, c+32, c+48: lane
-// group g = lane / 16 holds elements 16 m + 4 g + i in register i of f32x4
-// number m.  That is exactly the layout of a V_MFMA_F32_16X16X4_F32 result
-// block (rows 16 m .. 16 m + 15), and it is also a valid B operand when the
-// K index of MFMA (m, i) is taken as 16 m + 4 g + i: every product below
-// consumes the previous one's accumulators in place, with no data movement.
-// LayerNorm and softmax statistics are summed over the four lane groups with
-// the permlane swaps (no LDS).
+// Matrix products.  The fp32 matrix instructions of gfx950 share their
+// datapath with the vector ALU, and this kernel's vector work (LayerNorm,
+// gate nonlinearities, GELU, softmax) is of the same order as its products,
+// so on fp32 matrix cores the two would run back to back.  The products run
+// instead on the fp16 matrix cores (V_MFMA_F32_16X16X32_F16), which execute
+// alongside the vector ALU, with every fp32 operand split into two fp16
+// parts, x = hi + lo (hi = x rounded toward zero to fp16, lo = the remainder
+// rounded toward zero), and each product formed as
+//   A B = A_lo B_hi + A_hi B_lo + A_hi B_hi   (the lo * lo term dropped),
+// accumulated in fp32: about 21 significant bits per operand.  The weights
+// are split once per block (hi and lo take the 4 bytes of the fp32 weight);
+// the activations are split each step.
 //
-// LDS layout ("fragment order"): the A operand of MFMA (mb, m, i) for lane l
-// is W[16 mb + l % 16][16 m + 4 (l / 16) + i]; the four i of one (mb, m, l)
-// are one float4 at slot (mb * KM + m) * 64 + l, KM = K / 16, so a wave
-// reads one conflict-free b128 per four MFMAs.  Per block l:
-//   gate matrix [4d][2d]  (columns [LN input | recurrent]), 512 DW^2 slots
-//   W1 [4d][d]                                             , 256 DW^2 slots
-//   W2 [d][4d]                                             , 256 DW^2 slots
-// then E [256][d] (1024 DW slots).  The LayerNorm gains g1 and g2 are folded
-// into the columns of the matrix that reads the normalised vector,
+// Register layout.  Each wave owns 16 sequences (the MFMA columns).  A
+// length-n activation vector of sequence c lives in lanes c, c+16, c+32,
+// c+48: lane group g = lane / 16 holds elements 16 m + 4 g + i in register i
+// of f32x4 number m -- the layout of an MFMA result block (rows
+// 16 m .. 16 m + 15).  An fp16 MFMA contracts 32 K values, 8 per lane; K
+// chunk p takes, in lane group g, the elements 32 p + 16 (j / 4) + 4 g + j % 4
+// (j = 0..7), i.e. registers 0..3 of result blocks 2p and 2p+1.  With the
+// weights' columns laid out in the same order, each product consumes the
+// previous one's accumulators in place.  LayerNorm and softmax statistics
+// are summed over the four lane groups with the permlane swaps (no LDS).
+//
+// LDS layout ("fragment order"): for output block mb and K chunk p, lane l
+// reads the 8 weights W[16 mb + l % 16][col(p, l / 16, j)] as one 16-byte hi
+// fragment and one 16-byte lo fragment, slot (mb * KC + p), 2 KB per slot.
+// Per block l: the gate matrix [4d][2d] (columns [LN input | recurrent]),
+// W1 [4d][d], W2 [d][4d]; then E [256][d].  K is zero-padded to 32 where a
+// matrix has only 16 columns (d = 16).  The LayerNorm gains g1 and g2 are
+// folded into the columns of the matrix that reads the normalised vector,
 // W diag(g) n = W (g * n); the final gain multiplies f in registers.
 #pragma once
 
@@ -41,6 +53,8 @@ constexpr int kBodyThreads = 256;   // 4 waves x 16 sequences
 constexpr int kBodySeqs = 64;       // sequences per block
 constexpr float kLnEps = 1e-5f;     // LayerNorm's variance offset
 constexpr float kLog2e = 1.4426950408889634f;
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 
 struct BodyArgs {
   const float* theta;     // [N][d]
@@ -71,14 +85,19 @@ __host__ __device__ constexpr int body_gain_law(int law) {
 //   g1 [d] | W [4d][2d] | g2 [d] | W1 [4d][d] | W2 [d][4d];  g_f [d] after D blocks.
 __host__ __device__ constexpr int64_t body_block(int64_t dm) { return 16 * dm * dm + 2 * dm; }
 
+// Fragment slots (2 KB each: hi then lo) of one block and of E.
 template <int DW, int D>
 struct BodyLds {
-  static constexpr int kGate = 512 * DW * DW;
-  static constexpr int kW1 = 256 * DW * DW;
-  static constexpr int kW2 = 256 * DW * DW;
+  static constexpr int kGateKC = DW;                 // K = 2d in chunks of 32
+  static constexpr int kW1KC = 1;                    // K = d (padded to 32 when d = 16)
+  static constexpr int kW2KC = 2 * DW;               // K = 4d
+  static constexpr int kGate = 4 * DW * kGateKC;     // output blocks x chunks
+  static constexpr int kW1 = 4 * DW * kW1KC;
+  static constexpr int kW2 = DW * kW2KC;
   static constexpr int kLayer = kGate + kW1 + kW2;
-  static constexpr int kE = 1024 * DW;
-  static constexpr int kTotal = D * kLayer + kE;   // float4 slots
+  static constexpr int kE = 16;                      // 256 rows, one chunk
+  static constexpr int kSlots = D * kLayer + kE;
+  static constexpr int kUint4 = kSlots * 128;        // 64 lanes x (hi, lo)
 };
 
 // theta[k4 .. k4+3] +- eps z (one rounding, as every other perturbed weight).
@@ -134,46 +153,223 @@ __device__ __forceinline__ void layer_norm0(const f32x4 (&x)[DW], f32x4 (&n)[DW]
     for (int i = 0; i < 4; ++i) n[m][i] *= inv;
 }
 
-// GELU(u) = u Phi(u), Phi(u) = (1 + erf(u / sqrt 2)) / 2, with erf from
-// Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7 on erf):
-//   1 - erf(a) = t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) e^{-a^2},
-//   t = 1 / (1 + p a), a >= 0.
+// GELU(u) = u Phi(u) = max(u, 0) - |u| erfc(|u| / sqrt 2) / 2 (u erf(u / sqrt 2)
+// is even in u), with erfc from Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7):
+//   erfc(a) = t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) e^{-a^2},
+//   t = 1 / (1 + p a), a = |u| / sqrt 2 >= 0;
+// the halving is folded into the coefficients and 1 / sqrt 2 into p and the
+// exponent.
 __device__ __forceinline__ float gelu_f(float u) {
-  constexpr float p = 0.3275911f, a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f,
-                  a4 = -1.453152027f, a5 = 1.061405429f;
-  const float a = __builtin_fabsf(u) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(p, a, 1.0f));
-  float poly = __builtin_fmaf(t, a5, a4);
-  poly = __builtin_fmaf(t, poly, a3);
-  poly = __builtin_fmaf(t, poly, a2);
-  poly = __builtin_fmaf(t, poly, a1);
-  poly *= t;
-  const float tail = 0.5f * poly * __builtin_amdgcn_exp2f(-(a * a) * kLog2e);   // (1 - erf(a)) / 2
-  return u * (u >= 0.0f ? 1.0f - tail : tail);
+  constexpr float kP = 0.3275911f * 0.70710678118654752f;
+  constexpr float a1 = 0.5f * 0.254829592f, a2 = 0.5f * -0.284496736f, a3 = 0.5f * 1.421413741f,
+                  a4 = 0.5f * -1.453152027f, a5 = 0.5f * 1.061405429f;
+  constexpr float kE = -0.5f * kLog2e;                  // e^{-u^2/2} = 2^{kE u^2}
+  const float au = __builtin_fabsf(u);
+  const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(kP, au, 1.0f));
+  float q = __builtin_fmaf(t, a5, a4);
+  q = __builtin_fmaf(t, q, a3);
+  q = __builtin_fmaf(t, q, a2);
+  q = __builtin_fmaf(t, q, a1);
+  const float tail = q * t * __builtin_amdgcn_exp2f((u * u) * kE);   // erfc(a) / 2
+  return __builtin_fmaf(-au, tail, fmaxf(u, 0.0f));
 }
 
-// An LDS slot offset the compiler cannot see through.  The weights do not
-// change inside the time loop, so without this every LDS read of the step
-// (hundreds of registers' worth) would be hoisted out of the loop and
-// spilled; laundering the offset once per sublayer keeps each read next to
-// its MFMAs.
+// The gate rows are stored pre-scaled so that each nonlinearity needs one
+// exp2: sigmoid(a) = 1 / (1 + 2^{-a log2 e}) for i, f, o and
+// tanh(a) = 1 - 2 / (2^{2 a log2 e} + 1) for g.
+constexpr float kGateScaleSig = -kLog2e;
+constexpr float kGateScaleTanh = 2.0f * kLog2e;
+
+__device__ __forceinline__ float sigmoid_pre(float a) { return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(a)); }
+__device__ __forceinline__ float tanh_pre(float a) {
+  return __builtin_fmaf(-2.0f, __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(a) + 1.0f), 1.0f);
+}
+
+// An LDS offset the compiler cannot see through.  The weights do not change
+// inside the time loop, so without this every LDS read of the loop
+// (hundreds of registers' worth) would be hoisted out of it and spilled.
 __device__ __forceinline__ int opaque_offset(int off) {
   asm volatile("" : "+s"(off));
   return off;
 }
 
-// acc += A(float4 along the four MFMAs of one (mb, m)) . B(f32x4).
-__device__ __forceinline__ f32x4 mfma_frag(const float4& a, const f32x4& b, f32x4 acc) {
-  acc = mfma4(a.x, b[0], acc);
-  acc = mfma4(a.y, b[1], acc);
-  acc = mfma4(a.z, b[2], acc);
-  acc = mfma4(a.w, b[3], acc);
-  return acc;
+// Two fp32 values -> their fp16 parts, rounded toward zero: hi = (h(x0), h(x1)),
+// lo = (h(x0 - hi0), h(x1 - hi1)).  x - hi is exact in fp32.
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const auto h = __builtin_amdgcn_cvt_pkrtz(x0, x1);
+  const float r0 = x0 - static_cast<float>(h[0]), r1 = x1 - static_cast<float>(h[1]);
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(r0, r1));
+}
+
+// The 8 K values of a lane for one chunk: registers 0..3 of blocks a and b.
+__device__ __forceinline__ void split8(const f32x4& a, const f32x4& b, h8& hi, h8& lo) {
+  uint4 H, L;
+  split2(a[0], a[1], H.x, L.x);
+  split2(a[2], a[3], H.y, L.y);
+  split2(b[0], b[1], H.z, L.z);
+  split2(b[2], b[3], H.w, L.w);
+  hi = __builtin_bit_cast(h8, H);
+  lo = __builtin_bit_cast(h8, L);
+}
+
+// acc += A B over one K chunk, A from LDS slot `slot` (hi, lo), B split.
+__device__ __forceinline__ f32x4 mfma_split(const uint4* w16, int slot, int lane, const h8& bh, const h8& bl,
+                                            f32x4 acc) {
+  const h8 ah = __builtin_bit_cast(h8, w16[slot * 128 + lane]);
+  const h8 al = __builtin_bit_cast(h8, w16[slot * 128 + 64 + lane]);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl, acc, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh, acc, 0, 0, 0);
 }
 
 // Expert e's batch for direction j0 + jl (its accumulation batch).
 __device__ __forceinline__ const uint8_t* bytes_of_body(const BodyArgs& a, int e, int jl) {
   return a.bytes + static_cast<int64_t>((a.j0 + jl) / a.ppb) * a.bstride + static_cast<int64_t>(e) * a.B * a.T;
+}
+
+// One residual block for one time step of a wave's 16 sequences:
+//   x <- x + h,  h = LSTM(LN(x), h)    (the gains folded into the weights)
+//   x <- x + W2 GELU(W1 LN(x)).
+// W points at the block's first slot.  With act false the recurrent state
+// is left as it was (the pipeline's fill steps, whose results are discarded).
+template <int DW>
+__device__ __forceinline__ void body_block_step(const uint4* w16, int s0, int lane, f32x4 (&x)[DW], f32x4 (&h)[DW],
+                                                f32x4 (&c)[DW], bool act) {
+  using Lds = BodyLds<DW, 1>;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  f32x4 n[DW];
+  layer_norm0<DW>(x, n);
+  // K of the gate matrix: [n | h], 2 DW blocks, chunk p = blocks 2p, 2p+1.
+  f32x4 kin[2 * DW];
+#pragma unroll
+  for (int m = 0; m < DW; ++m) {
+    kin[m] = n[m];
+    kin[DW + m] = h[m];
+  }
+  f32x4 acc[4 * DW];
+#pragma unroll
+  for (int mb = 0; mb < 4 * DW; ++mb) acc[mb] = zero;
+#pragma unroll
+  for (int p = 0; p < Lds::kGateKC; ++p) {
+    h8 bh, bl;
+    split8(kin[2 * p], kin[2 * p + 1], bh, bl);
+#pragma unroll
+    for (int mb = 0; mb < 4 * DW; ++mb) acc[mb] = mfma_split(w16, s0 + mb * Lds::kGateKC + p, lane, bh, bl, acc[mb]);
+  }
+  // Unit 16 m + 4 g + i has gate q in block q DW + m, register i.
+#pragma unroll
+  for (int m = 0; m < DW; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ig = sigmoid_pre(acc[m][i]), fg = sigmoid_pre(acc[DW + m][i]);
+      const float gg = tanh_pre(acc[2 * DW + m][i]), og = sigmoid_pre(acc[3 * DW + m][i]);
+      const float c1 = __builtin_fmaf(fg, c[m][i], ig * gg);
+      const float h1 = og * tanh_pre(c1 * kGateScaleTanh);
+      c[m][i] = act ? c1 : c[m][i];
+      h[m][i] = act ? h1 : h[m][i];
+      x[m][i] += h1;
+    }
+  layer_norm0<DW>(x, n);
+  f32x4 u[4 * DW];
+#pragma unroll
+  for (int mb = 0; mb < 4 * DW; ++mb) u[mb] = zero;
+  {
+    h8 bh, bl;
+    split8(n[0], DW > 1 ? n[DW - 1] : zero, bh, bl);
+    const int s1 = s0 + Lds::kGate;
+#pragma unroll
+    for (int mb = 0; mb < 4 * DW; ++mb) u[mb] = mfma_split(w16, s1 + mb, lane, bh, bl, u[mb]);
+  }
+#pragma unroll
+  for (int mb = 0; mb < 4 * DW; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) u[mb][i] = gelu_f(u[mb][i]);
+  const int s2 = s0 + Lds::kGate + Lds::kW1;
+#pragma unroll
+  for (int p = 0; p < Lds::kW2KC; ++p) {
+    h8 bh, bl;
+    split8(u[2 * p], u[2 * p + 1], bh, bl);
+#pragma unroll
+    for (int mb = 0; mb < DW; ++mb) x[mb] = mfma_split(w16, s2 + mb * Lds::kW2KC + p, lane, bh, bl, x[mb]);
+  }
+}
+
+// The decoder for one time step: f = g_f * LN(x), logits = E f; returns the
+// cross entropy against the target whose E row (this lane's features) is
+// ey, and the log-sum-exp and f for the delta rule.
+template <int DW>
+__device__ __forceinline__ float body_decode_step(const uint4* w16, int se0, int lane, const f32x4 (&x)[DW],
+                                                  const f32x4 (&gf)[DW], const float4 (&ey)[DW], f32x4 (&f)[DW],
+                                                  float& lse) {
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  layer_norm0<DW>(x, f);
+#pragma unroll
+  for (int m = 0; m < DW; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f[m][i] *= gf[m][i];
+  h8 bh, bl;
+  split8(f[0], DW > 1 ? f[DW - 1] : zero, bh, bl);
+  f32x4 lo[16];
+#pragma unroll
+  for (int mb = 0; mb < 16; ++mb) lo[mb] = mfma_split(w16, se0 + mb, lane, bh, bl, zero);
+  float mx = lo[0][0];
+#pragma unroll
+  for (int mb = 0; mb < 16; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lo[mb][i]);
+  mx = xmax4(mx);
+  const float ms = mx * kLog2e;
+  float se = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < 16; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) se += __builtin_amdgcn_exp2f(__builtin_fmaf(lo[mb][i], kLog2e, -ms));
+  lse = __logf(xsum4(se)) + mx;
+  float yl = 0.0f;
+#pragma unroll
+  for (int m = 0; m < DW; ++m) {
+    yl = __builtin_fmaf(ey[m].x, f[m][0], yl);
+    yl = __builtin_fmaf(ey[m].y, f[m][1], yl);
+    yl = __builtin_fmaf(ey[m].z, f[m][2], yl);
+    yl = __builtin_fmaf(ey[m].w, f[m][3], yl);
+  }
+  return lse - xsum4(yl);
+}
+
+// One weight fragment: lane `ln` of slot (mb, p) of a matrix with row stride
+// `ld` (floats) and `ncol` columns, starting at canonical offset `base`;
+// columns col(p, g, j) = 32 p + 16 (j / 4) + 4 g + j % 4 beyond ncol are zero.
+// Columns below `gcol` are multiplied by the gain at canonical offset kg +
+// column; the row's scale is applied; the fp32 weight is then split into
+// (hi, lo).
+template <bool kPert>
+__device__ __forceinline__ void body_fragment(const float* th, int64_t base, int ld, int ncol, int row, int p,
+                                              int ln, int64_t kg, int gcol, float scale, int wlaw, int glaw,
+                                              uint2 key, uint32_t pair, uint32_t step_lo, float seps, uint4& hi,
+                                              uint4& lo) {
+  float w[8];
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int c0 = 32 * p + 16 * half + 4 * (ln >> 4);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c0 < ncol) {
+      v = body_weight4<kPert>(th, base + static_cast<int64_t>(row) * ld + c0, wlaw, key, pair, step_lo, seps);
+      if (c0 < gcol) {
+        const float4 g = body_weight4<kPert>(th, kg + c0, glaw, key, pair, step_lo, seps);
+        v = make_float4(v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w);
+      }
+      v = make_float4(v.x * scale, v.y * scale, v.z * scale, v.w * scale);
+    }
+    w[4 * half] = v.x;
+    w[4 * half + 1] = v.y;
+    w[4 * half + 2] = v.z;
+    w[4 * half + 3] = v.w;
+  }
+  split2(w[0], w[1], hi.x, lo.x);
+  split2(w[2], w[3], hi.y, lo.y);
+  split2(w[4], w[5], hi.z, lo.z);
+  split2(w[6], w[7], hi.w, lo.w);
 }
 
 // ---------------------------------------------------------------------------
@@ -182,13 +378,21 @@ __device__ __forceinline__ const uint8_t* bytes_of_body(const BodyArgs& a, int e
 // of its T-1 next-byte cross entropies; the block writes their fp64 sum to
 // part[slot][tile].  Evaluation also writes the decoder inputs f and the
 // log-sum-exp of every position (the inputs of the delta rule).
+//
+// The time loop is pipelined over the D + 1 stages (block 1, ..., block D,
+// decoder): iteration i runs block l on step i - l and the decoder on step
+// i - D, each on what the stage before it produced in iteration i - 1.  The
+// stages of one iteration are independent, so the matrix products of one
+// can run on the matrix cores while the vector ALU works on another.  The
+// first D iterations fill the pipeline and the last D drain it; their extra
+// results are discarded.
 // ---------------------------------------------------------------------------
 template <int DW, int D, bool kPert>
 __global__ __launch_bounds__(kBodyThreads, 1) void k_body(BodyArgs a) {
   using Lds = BodyLds<DW, D>;
   constexpr int dm = 16 * DW;
   constexpr int NS = kPert ? 2 : 1;
-  __shared__ float4 w4[Lds::kTotal];
+  __shared__ uint4 w16[Lds::kUint4];
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, lg = lane >> 4;
   const int bt = blockIdx.x % a.btiles;
@@ -204,37 +408,36 @@ __global__ __launch_bounds__(kBodyThreads, 1) void k_body(BodyArgs a) {
   const int wlaw = a.probe, glaw = body_gain_law(a.probe);
   constexpr int64_t blk = body_block(dm);
 
-  // Perturbed weights into LDS in fragment order, gains folded in.
-  for (int q = threadIdx.x; q < D * Lds::kLayer; q += kBodyThreads) {
-    const int l = q / Lds::kLayer, r = q % Lds::kLayer, ln = r & 63;
-    const int64_t base = l * blk;
-    int64_t k, kg = -1;
-    if (r < Lds::kGate) {
-      const int mb = r / (128 * DW), m = (r >> 6) % (2 * DW);
-      const int row = 16 * mb + (ln & 15), c0 = 16 * m + 4 * (ln >> 4);
-      k = base + dm + static_cast<int64_t>(row) * 2 * dm + c0;
-      if (m < DW) kg = base + c0;                                       // g1 on the LN input
-    } else if (r < Lds::kGate + Lds::kW1) {
-      const int rr = r - Lds::kGate, mb = rr / (64 * DW), m = (rr >> 6) % DW;
-      const int row = 16 * mb + (ln & 15), c0 = 16 * m + 4 * (ln >> 4);
-      k = base + 2 * dm + 8 * dm * dm + static_cast<int64_t>(row) * dm + c0;
-      kg = base + dm + 8 * dm * dm + c0;                                 // g2
+  // Perturbed weights into LDS as split fragments, gains folded in, gate
+  // rows pre-scaled for their nonlinearity.  One (slot, lane) per iteration.
+  for (int q = threadIdx.x; q < Lds::kSlots * 64; q += kBodyThreads) {
+    const int slot = q >> 6, ln = q & 63, r16 = ln & 15;
+    uint4 hi, lo;
+    if (slot < D * Lds::kLayer) {
+      const int l = slot / Lds::kLayer, r = slot % Lds::kLayer;
+      const int64_t base = l * blk;
+      if (r < Lds::kGate) {
+        // columns [0, d) read LN(x) (gain g1), [d, 2d) the recurrent state
+        const int mb = r / Lds::kGateKC, p = r % Lds::kGateKC, row = 16 * mb + r16;
+        const float scale = row / dm == 2 ? kGateScaleTanh : kGateScaleSig;
+        body_fragment<kPert>(th, base + dm, 2 * dm, 2 * dm, row, p, ln, base, dm, scale, wlaw, glaw, key, pair,
+                             step_lo, seps, hi, lo);
+      } else if (r < Lds::kGate + Lds::kW1) {
+        const int mb = r - Lds::kGate, row = 16 * mb + r16;
+        body_fragment<kPert>(th, base + 2 * dm + 8 * dm * dm, dm, dm, row, 0, ln, base + dm + 8 * dm * dm, dm, 1.0f,
+                             wlaw, glaw, key, pair, step_lo, seps, hi, lo);
+      } else {
+        const int rr = r - Lds::kGate - Lds::kW1, mb = rr / Lds::kW2KC, p = rr % Lds::kW2KC, row = 16 * mb + r16;
+        body_fragment<kPert>(th, base + 2 * dm + 12 * dm * dm, 4 * dm, 4 * dm, row, p, ln, 0, 0, 1.0f, wlaw, glaw,
+                             key, pair, step_lo, seps, hi, lo);
+      }
     } else {
-      const int rr = r - Lds::kGate - Lds::kW1, mb = rr / (256 * DW), m = (rr >> 6) % (4 * DW);
-      const int row = 16 * mb + (ln & 15), c0 = 16 * m + 4 * (ln >> 4);
-      k = base + 2 * dm + 12 * dm * dm + static_cast<int64_t>(row) * 4 * dm + c0;
+      // E (frozen, not perturbed): rows 16 mb + r16, columns as above.
+      const int mb = slot - D * Lds::kLayer, row = 16 * mb + r16;
+      body_fragment<false>(Ee, 0, dm, dm, row, 0, ln, 0, 0, 1.0f, 0, 0, key, pair, step_lo, 0.0f, hi, lo);
     }
-    float4 w = body_weight4<kPert>(th, k, wlaw, key, pair, step_lo, seps);
-    if (kg >= 0) {
-      const float4 g = body_weight4<kPert>(th, kg, glaw, key, pair, step_lo, seps);
-      w = make_float4(w.x * g.x, w.y * g.y, w.z * g.z, w.w * g.w);
-    }
-    w4[q] = w;
-  }
-  for (int q = threadIdx.x; q < Lds::kE; q += kBodyThreads) {
-    const int ln = q & 63, m = (q >> 6) % DW, mb = q / (64 * DW);
-    w4[D * Lds::kLayer + q] =
-        *reinterpret_cast<const float4*>(Ee + (16 * mb + (ln & 15)) * dm + 16 * m + 4 * (ln >> 4));
+    w16[slot * 128 + ln] = hi;
+    w16[slot * 128 + 64 + ln] = lo;
   }
   f32x4 gf[DW];
 #pragma unroll
@@ -253,127 +456,75 @@ __global__ __launch_bounds__(kBodyThreads, 1) void k_body(BodyArgs a) {
                              : a.bytes + (static_cast<int64_t>(e) * B + b) * T;
   double ce_sum = 0.0;
   if (live) {
-    f32x4 h[D][DW], cs[D][DW];
+    f32x4 h[D][DW], cs[D][DW], xs[D + 1][DW];   // xs[l]: the input of stage l this iteration
 #pragma unroll
     for (int l = 0; l < D; ++l)
 #pragma unroll
       for (int m = 0; m < DW; ++m) h[l][m] = cs[l][m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float4 er[DW];   // E row of the current input byte, this lane's features
+#pragma unroll
+    for (int l = 0; l <= D; ++l)
+#pragma unroll
+      for (int m = 0; m < DW; ++m) xs[l][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // rows[k] = E[byte_{i-k}] (this lane's features); the decoder's target at
+    // iteration i is byte_{i-D+1}, i.e. rows[D-1].
+    float4 rows[D][DW];
     {
-      const int v = seq[0];
+      const int v0 = seq[0];
 #pragma unroll
-      for (int m = 0; m < DW; ++m) er[m] = *reinterpret_cast<const float4*>(Ee + v * dm + 16 * m + 4 * lg);
+      for (int m = 0; m < DW; ++m) rows[0][m] = *reinterpret_cast<const float4*>(Ee + v0 * dm + 16 * m + 4 * lg);
+#pragma unroll
+      for (int k = 1; k < D; ++k)
+#pragma unroll
+        for (int m = 0; m < DW; ++m) rows[k][m] = rows[0][m];
     }
-    for (int t = 0; t + 1 < T; ++t) {
-      const int y = seq[t + 1];
-      float4 ey[DW];   // E row of the target: its logit now, the next input's embedding after
+    int vnext = seq[1 < T - 1 ? 1 : T - 1];
+    for (int i = 0; i < T - 1 + D; ++i) {
+      // Prefetch: the byte after next, and the E row of the next byte.
+      const int vnn = seq[i + 2 < T - 1 ? i + 2 : T - 1];
+      float4 rnext[DW];
 #pragma unroll
-      for (int m = 0; m < DW; ++m) ey[m] = *reinterpret_cast<const float4*>(Ee + y * dm + 16 * m + 4 * lg);
-      f32x4 x[DW];
+      for (int m = 0; m < DW; ++m) rnext[m] = *reinterpret_cast<const float4*>(Ee + vnext * dm + 16 * m + 4 * lg);
+      const uint4* W = w16 + opaque_offset(0);
 #pragma unroll
-      for (int m = 0; m < DW; ++m) x[m] = f32x4{er[m].x, er[m].y, er[m].z, er[m].w};
+      for (int m = 0; m < DW; ++m) xs[0][m] = f32x4{rows[0][m].x, rows[0][m].y, rows[0][m].z, rows[0][m].w};
 
+      f32x4 out[D][DW];
 #pragma unroll
       for (int l = 0; l < D; ++l) {
-        const float4* Wg = w4 + opaque_offset(l * Lds::kLayer);
-        f32x4 n[DW];
-        layer_norm0<DW>(x, n);
-        // LSTM sublayer: gate pre-activations W' [n; h] (rows i, f, g, o).
-        f32x4 acc[4 * DW];
 #pragma unroll
-        for (int mb = 0; mb < 4 * DW; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 0; m < 2 * DW; ++m) {
-          const f32x4 bv = m < DW ? n[m] : h[l][m - DW];
-#pragma unroll
-          for (int mb = 0; mb < 4 * DW; ++mb) acc[mb] = mfma_frag(Wg[(mb * 2 * DW + m) * 64 + lane], bv, acc[mb]);
-        }
-        // Unit 16 m + 4 g + i has gate q in block q DW + m, register i.
-#pragma unroll
-        for (int m = 0; m < DW; ++m)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float ig = sigmoid_f(acc[m][i]), fg = sigmoid_f(acc[DW + m][i]);
-            const float gg = tanh_f(acc[2 * DW + m][i]), og = sigmoid_f(acc[3 * DW + m][i]);
-            const float c1 = __builtin_fmaf(fg, cs[l][m][i], ig * gg);
-            cs[l][m][i] = c1;
-            h[l][m][i] = og * tanh_f(c1);
-            x[m][i] += h[l][m][i];
-          }
-        // MLP sublayer: x += W2 GELU(W1' LN(x)), the residual as W2's accumulator.
-        layer_norm0<DW>(x, n);
-        const float4* W1 = w4 + opaque_offset(l * Lds::kLayer + Lds::kGate);
-        const float4* W2 = W1 + Lds::kW1;
-        f32x4 u[4 * DW];
-#pragma unroll
-        for (int mb = 0; mb < 4 * DW; ++mb) u[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 0; m < DW; ++m)
-#pragma unroll
-          for (int mb = 0; mb < 4 * DW; ++mb) u[mb] = mfma_frag(W1[(mb * DW + m) * 64 + lane], n[m], u[mb]);
-#pragma unroll
-        for (int mb = 0; mb < 4 * DW; ++mb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) u[mb][i] = gelu_f(u[mb][i]);
-#pragma unroll
-        for (int m = 0; m < 4 * DW; ++m)
-#pragma unroll
-          for (int mb = 0; mb < DW; ++mb) x[mb] = mfma_frag(W2[(mb * 4 * DW + m) * 64 + lane], u[m], x[mb]);
+        for (int m = 0; m < DW; ++m) out[l][m] = xs[l][m];
+        body_block_step<DW>(W, l * Lds::kLayer, lane, out[l], h[l], cs[l], i >= l);
       }
-
-      // Decoder: f = g_f * LN(x), logits = E f, cross entropy against y.
       f32x4 f[DW];
-      layer_norm0<DW>(x, f);
-#pragma unroll
-      for (int m = 0; m < DW; ++m)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) f[m][i] *= gf[m][i];
-      const float4* Ef = w4 + opaque_offset(D * Lds::kLayer);
-      f32x4 lo[16];
-#pragma unroll
-      for (int mb = 0; mb < 16; ++mb) lo[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int m = 0; m < DW; ++m)
-#pragma unroll
-        for (int mb = 0; mb < 16; ++mb) lo[mb] = mfma_frag(Ef[(mb * DW + m) * 64 + lane], f[m], lo[mb]);
-      float mx = lo[0][0];
-#pragma unroll
-      for (int mb = 0; mb < 16; ++mb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, lo[mb][i]);
-      mx = xmax4(mx);
-      const float ms = mx * kLog2e;
-      float se = 0.0f;
-#pragma unroll
-      for (int mb = 0; mb < 16; ++mb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) se += __builtin_amdgcn_exp2f(__builtin_fmaf(lo[mb][i], kLog2e, -ms));
-      const float lse = __logf(xsum4(se)) + mx;
-      float yl = 0.0f;
-#pragma unroll
-      for (int m = 0; m < DW; ++m) {
-        yl = __builtin_fmaf(ey[m].x, f[m][0], yl);
-        yl = __builtin_fmaf(ey[m].y, f[m][1], yl);
-        yl = __builtin_fmaf(ey[m].z, f[m][2], yl);
-        yl = __builtin_fmaf(ey[m].w, f[m][3], yl);
-      }
-      yl = xsum4(yl);
-      if (lg == 0 && valid) ce_sum += static_cast<double>(lse - yl);
-      if (!kPert && valid) {
-        const int64_t pos = (static_cast<int64_t>(e) * B + b) * (T - 1) + t;
+      float lse;
+      const float ce = body_decode_step<DW>(W, D * Lds::kLayer, lane, xs[D], gf, rows[D - 1], f, lse);
+      const int td = i - D;                       // the decoder's time step
+      const bool scored = td >= 0 && td + 1 < T;
+      ce_sum += (scored && valid && lg == 0) ? static_cast<double>(ce) : 0.0;
+      if (!kPert && scored && valid) {
+        const int64_t pos = (static_cast<int64_t>(e) * B + b) * (T - 1) + td;
 #pragma unroll
         for (int m = 0; m < DW; ++m)
           *reinterpret_cast<float4*>(a.fdec + pos * dm + 16 * m + 4 * lg) = make_float4(f[m][0], f[m][1], f[m][2], f[m][3]);
         if (lg == 0) a.lse[pos] = lse;
       }
 #pragma unroll
-      for (int m = 0; m < DW; ++m) er[m] = ey[m];
+      for (int l = 0; l < D; ++l)
+#pragma unroll
+        for (int m = 0; m < DW; ++m) xs[l + 1][m] = out[l][m];
+#pragma unroll
+      for (int k = D - 1; k > 0; --k)
+#pragma unroll
+        for (int m = 0; m < DW; ++m) rows[k][m] = rows[k - 1][m];
+#pragma unroll
+      for (int m = 0; m < DW; ++m) rows[0][m] = rnext[m];
+      vnext = vnn;
     }
   }
 
   // Per-block sum of the 64 sequence losses in a fixed order.
   __syncthreads();   // every wave is past its loop: the weight region is free
-  double* red = reinterpret_cast<double*>(w4);
+  double* red = reinterpret_cast<double*>(w16);
   if (lg == 0) red[wave * 16 + col] = ce_sum;
   __syncthreads();
   if (threadIdx.x == 0) {
