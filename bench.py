@@ -64,7 +64,9 @@ BODY_SOURCES = KERNEL_SOURCES + ("paper_2609_37899_amd/csrc/soma_body.hpp",)
 def kernel_source_hash(kernel: str = "") -> str:
     """Hash of a kernel's sources: stored traffic figures apply only to these."""
     import hashlib
+    from paper_2609_37899_amd.build import HIPCC_FLAGS
     h = hashlib.sha256()
+    h.update(" ".join(HIPCC_FLAGS).encode())
     for f in (BODY_SOURCES if kernel == "k_body" else KERNEL_SOURCES):
         h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
