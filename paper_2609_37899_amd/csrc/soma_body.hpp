@@ -54,8 +54,6 @@ constexpr int kBodySeqs = 64;       // sequences per block
 constexpr float kLnEps = 1e-5f;     // LayerNorm's variance offset
 constexpr float kLog2e = 1.4426950408889634f;
 
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-
 struct BodyArgs {
   const float* theta;     // [N][d]
   const uint8_t* bytes;   // [A][N][B][T] (perturbed) or [N][B][T] (evaluation)
@@ -191,15 +189,6 @@ __device__ __forceinline__ float tanh_pre(float a) {
 __device__ __forceinline__ int opaque_offset(int off) {
   asm volatile("" : "+s"(off));
   return off;
-}
-
-// Two fp32 values -> their fp16 parts, rounded toward zero: hi = (h(x0), h(x1)),
-// lo = (h(x0 - hi0), h(x1 - hi1)).  x - hi is exact in fp32.
-__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
-  const auto h = __builtin_amdgcn_cvt_pkrtz(x0, x1);
-  const float r0 = x0 - static_cast<float>(h[0]), r1 = x1 - static_cast<float>(h[1]);
-  hi = __builtin_bit_cast(uint32_t, h);
-  lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(r0, r1));
 }
 
 // The 8 K values of a lane for one chunk: registers 0..3 of blocks a and b.

@@ -55,6 +55,63 @@ __device__ __forceinline__ f32x4 mfma_k16(const float4& w, const float4& x, f32x
   return acc;
 }
 
+// ---------------------------------------------------------------------------
+// Split fp16 products.  gfx950's fp32 matrix instructions share their
+// datapath with the vector ALU (one wave's or two waves' fp32 MFMAs and
+// vector instructions take the sum of their times), while its fp16 matrix
+// cores (V_MFMA_F32_16X16X32_F16) run alongside the vector ALU at 16 times
+// the fp32 matrix rate.  The streaming and persistent kernels therefore form
+// their fp32 products there: each fp32 operand is split into two fp16 parts,
+// x = hi + lo (hi = x rounded toward zero to fp16; lo = the remainder, exact
+// in fp32, rounded toward zero), and
+//   A B = A_lo B_hi + A_hi B_lo + A_hi B_hi   (the lo * lo term dropped)
+// is accumulated in fp32: about 21 significant bits per operand.  K runs in
+// chunks of 32; lane group g = lane / 16 supplies the 8 consecutive K values
+// 32 p + 8 g .. + 7 of chunk p for both operands, and its 16 lanes the rows
+// (A) or columns (B); the result block is laid out as for the fp32 MFMA.
+// ---------------------------------------------------------------------------
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+
+// Two fp32 values -> their fp16 parts: hi = (h(x0), h(x1)), lo = (h(x0 -
+// hi0), h(x1 - hi1)), both rounded toward zero; x - hi is exact in fp32.
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const auto h = __builtin_amdgcn_cvt_pkrtz(x0, x1);
+  const float r0 = x0 - static_cast<float>(h[0]), r1 = x1 - static_cast<float>(h[1]);
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(r0, r1));
+}
+
+// Four consecutive fp32 values -> 8 bytes of hi parts and 8 bytes of lo parts.
+__device__ __forceinline__ void split4(const float4& v, uint2& hi, uint2& lo) {
+  split2(v.x, v.y, hi.x, lo.x);
+  split2(v.z, v.w, hi.y, lo.y);
+}
+
+// Eight consecutive fp32 values (two float4) -> one 8-half fragment each.
+__device__ __forceinline__ void split8v(const float4& a, const float4& b, uint4& hi, uint4& lo) {
+  uint2 h0, l0, h1, l1;
+  split4(a, h0, l0);
+  split4(b, h1, l1);
+  hi = make_uint4(h0.x, h0.y, h1.x, h1.y);
+  lo = make_uint4(l0.x, l0.y, l1.x, l1.y);
+}
+
+// acc += A B over one 32-wide K chunk from split fragments (8 halves per lane).
+__device__ __forceinline__ f32x4 mfma3(const uint4& ah, const uint4& al, const uint4& bh, const uint4& bl,
+                                       f32x4 acc) {
+  const h8 AH = __builtin_bit_cast(h8, ah), AL = __builtin_bit_cast(h8, al);
+  const h8 BH = __builtin_bit_cast(h8, bh), BL = __builtin_bit_cast(h8, bl);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AL, BH, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, BL, acc, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, BH, acc, 0, 0, 0);
+}
+
+// Pieces of K = 64 NCH staged per pass of the streaming and persistent
+// kernels, each 64 or 128 wide (a whole number of 32-wide chunks).
+__host__ __device__ constexpr int split_quarters(int nch) {
+  return nch <= 4 ? nch : (nch % 4 == 0 ? 4 : (nch % 3 == 0 ? 3 : nch));
+}
+
 __device__ __forceinline__ float4 fma4(float a, const float4& z, const float4& t) {
   return make_float4(__builtin_fmaf(a, z.x, t.x), __builtin_fmaf(a, z.y, t.y),
                      __builtin_fmaf(a, z.z, t.z), __builtin_fmaf(a, z.w, t.w));
@@ -687,20 +744,73 @@ __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, con
   __syncthreads();
 }
 
+// The same rows as split fragments for the fp16 products: lane (wave, lr, lg)
+// keeps row r0 + 16 wave + lr, columns col0 + 32 c + 8 lg .. + 7 as (wh[c],
+// wl[c]), KC = K / 32 chunks; w = theta + seps z is formed in fp32 and then
+// split.  The probes are drawn as in resident_weights.
+template <int KC, bool kGateRows, bool kRad>
+__device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&wl)[KC], float* zs, const float* th,
+                                                       int64_t off_l, int ld, int col0, int H, int r0, int law,
+                                                       uint2 key, uint32_t pair, uint32_t step_lo, float seps) {
+  constexpr int kPiece = kZpiece / 32;   // chunks per probe piece
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  auto canon = [&](int r) { return kGateRows ? (r & 3) * H + (r >> 2) : r; };
+  const int prow = r0 + wave * 16 + lr;
+  const int64_t wrow = off_l + static_cast<int64_t>(canon(prow)) * ld + col0;
+#pragma unroll
+  for (int piece = 0; piece < (KC + kPiece - 1) / kPiece; ++piece) {
+    const int kc0 = piece * kPiece;
+    const int nc = (KC - kc0 < kPiece ? KC - kc0 : kPiece);
+    __syncthreads();
+    for (int q = threadIdx.x; q < 128 * nc * 8; q += blockDim.x) {
+      const int m = q / (nc * 8), k4 = q % (nc * 8);
+      const int pr = r0 + m;
+      const uint64_t kk = static_cast<uint64_t>(off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 32 * kc0 + 4 * k4);
+      *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) =
+          kRad ? rademacher_quad(key, pair, step_lo, kk, law == kProbeRademacher) : gauss_quad(key, pair, step_lo, kk >> 2);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c2 = 0; c2 < kPiece; ++c2) {
+      const int c = kc0 + c2;
+      if (c < KC) {
+        const float* zr = &zs[(wave * 16 + lr) * kZld + 32 * c2 + 8 * lg];
+        const float* tr = th + wrow + 32 * c + 8 * lg;
+        const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
+        const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+        split8v(w0, w1, wh[c], wl[c]);
+      }
+    }
+  }
+  __syncthreads();
+}
+
 template <int NB, int NCH, bool kRad>
 __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
-  constexpr int KQ = 4 * NCH;                           // 16-wide k groups: H = 64 NCH
-  constexpr int NQ = NCH >= 4 ? 4 : NCH;                // staging quarters of K
-  constexpr int QG = KQ / NQ;                           // k groups per quarter
+  constexpr int KC = 2 * NCH;                           // 32-wide k chunks: H = 64 NCH
+  // Staging pieces of K, each the largest of 256, 128, 64 that divides H:
+  // long enough that a piece's products outlast the loads of the next, and
+  // a whole number of 16-lane row segments per wave load.
+  constexpr int KWQ = (64 * NCH) % 256 == 0 ? 256 : ((64 * NCH) % 128 == 0 ? 128 : 64);   // k per piece
+  constexpr int NQ = 64 * NCH / KWQ;
+  constexpr int QC = KWQ / 32;                          // k chunks per piece
   constexpr int ROWS = NB * 16;
-  constexpr int QF4 = ROWS * QG * 4;                    // float4 per quarter (16 k per group = 4 float4)
-  constexpr int PT = (QF4 + kPersistThreads - 1) / kPersistThreads;
-  constexpr int LDS_FLOATS = (ROWS * kHsld > 128 * kZld) ? ROWS * kHsld : 128 * kZld;
-  __shared__ float hs[LDS_FLOATS];                      // staged h_{t-1} [ROWS][kHsld]; probe piece at job start
+  constexpr int HS = kRecMaxH + 16;                     // padded LDS row in halves (an odd multiple of 32 bytes)
+  constexpr int CW4 = KWQ / 4;                          // float4 per row of a piece: 16, 32 or 64
+  constexpr int RPW = 64 / CW4;                         // rows per wave load
+  constexpr int PT = ROWS >= 8 * RPW ? ROWS / (8 * RPW) : 1;   // wave loads per piece (8 waves)
+  constexpr bool kAllWaves = ROWS >= 8 * RPW;           // else waves past the rows stage nothing
+  constexpr int STAGE_BYTES = 2 * ROWS * HS * 2;        // [hi, lo][ROWS][HS] halves
+  constexpr int LDS_BYTES = STAGE_BYTES > 128 * kZld * 4 ? STAGE_BYTES : 128 * kZld * 4;
+  // staged h_{t-1} split into fp16 parts; the probe piece at job start
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
   __shared__ float ht[ROWS * kHtld];                    // h_t of the block's units, transposed for stores
+  _Float16* hs_hi = reinterpret_cast<_Float16*>(lds);
+  _Float16* hs_lo = hs_hi + ROWS * HS;
   __shared__ unsigned abort_flag;
   const FwdArgs& a = p.a;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform (scalar) from here on
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T, in = a.in_l;
   const int UT = H / kRecUnits;                         // blocks per group
   const int g = blockIdx.x % p.groups;
@@ -728,9 +838,11 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     const __amdgpu_buffer_rsrc_t bbuf =
         buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
 
-    // Perturbed recurrent weights of this lane, drawn once for the sequence.
-    float4 w[KQ];
-    resident_weights<KQ, true, kRad>(w, hs, th, a.off_l, in + H, in, H, utile * 128, a.probe, key, pair, step_lo, seps);
+    // Perturbed recurrent weights of this lane, drawn once for the sequence
+    // and held as split fragments.
+    uint4 wh[KC], wl[KC];
+    resident_weights_split<KC, true, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H, in, H,
+                                           utile * 128, a.probe, key, pair, step_lo, seps);
     // Rows past the batch compute on the last row's inputs and h (a column
     // of the product depends only on the same column of h, so no stored
     // output depends on them) and are never stored.  So the step has no
@@ -751,9 +863,10 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     }
 
     for (int t = 0; t + 1 < T; ++t) {
-      // Gate inputs of step t, loaded while the last quarter of K runs.
-      // Layer 1 reads its folded inputs by byte value; the bytes of step
-      // t + 1 (t + 1 < T) are fetched one step ahead.
+      // Gate inputs of step t, loaded with the first piece of h_{t-1}; they
+      // seed the accumulators, which the products then add to.  Layer 1
+      // reads its folded inputs by byte value; the bytes of step t + 1
+      // (t + 1 < T) are fetched one step ahead.
       float4 gi[NB];
       auto load_inputs = [&]() {
         if (a.layer == 0) {
@@ -772,13 +885,14 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         }
       };
       f32x4 acc[NB];
+      auto seed = [&]() {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{gi[nb].x, gi[nb].y, gi[nb].z, gi[nb].w};
+      };
       // Cell update of row tile nb: c_t = f c_{t-1} + i g, h_t = o tanh(c_t),
       // written to the transposed tile that is published below.
       auto cell = [&](int nb) {
-        const float ai = acc[nb][0] + gi[nb].x, af = acc[nb][1] + gi[nb].y;
-        const float ag = acc[nb][2] + gi[nb].z, ao = acc[nb][3] + gi[nb].w;
+        const float ai = acc[nb][0], af = acc[nb][1], ag = acc[nb][2], ao = acc[nb][3];
         const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
         cs[nb] = c;
         ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = sigmoid_f(ao) * tanh_f(c);
@@ -787,63 +901,77 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       if (t == 0) {
         load_inputs();
         wait_vmem();
+        seed();
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) cell(nb);
       } else {
         if (group_wait(bar, static_cast<unsigned>(UT) * done, p.err, p.spin_limit, &abort_flag)) return;
         const int row0 = (t - 1) * B;                    // rows of h_{t-1} in the slot
+        // Wave load i of a piece covers rows (wave + 8 i) RPW + lane / CW4,
+        // float4 lane % CW4 of the piece: a per-lane part and a scalar part.
+        // Rows past the batch (B < 64) read whatever follows h_{t-1} (zeros
+        // past the slot); their results are never stored.
+        const int lrow = lane / CW4, lc4 = lane % CW4;
+        const uint32_t lane_off = static_cast<uint32_t>((lrow * H + 4 * lc4) * 4);
         float4 pre[PT];
         auto gload = [&](int qq) {
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
-            const int idx = threadIdx.x + i * kPersistThreads;
-            const int c4 = idx % (QG * 4), n = brow_of(idx / (QG * 4), B);
-            if (idx < QF4) {
-              const uint32_t off = static_cast<uint32_t>(((row0 + n) * H + qq * QG * 16 + 4 * c4) * 4);
-              pre[i] = buffer_load_f4<kCoherent>(hbuf, off);
+            const int n0 = (wave + 8 * i) * RPW;
+            if (kAllWaves || n0 < ROWS) {                // wave-uniform
+              const uint32_t soff = static_cast<uint32_t>(((row0 + n0) * H + qq * KWQ) * 4);
+              typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+              const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hbuf, lane_off, soff, kCoherent);
+              pre[i] = make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
+                                   __uint_as_float(v[3]));
             }
           }
         };
+        // h_{t-1} is split into its fp16 parts as it is staged.
         auto sstore = [&](int qq) {
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
-            const int idx = threadIdx.x + i * kPersistThreads;
-            if (idx < QF4) {
-              const int c4 = idx % (QG * 4), n = idx / (QG * 4);
-              *reinterpret_cast<float4*>(&hs[n * kHsld + qq * QG * 16 + 4 * c4]) = pre[i];
-            }
+            if (!kAllWaves && (wave + 8 * i) * RPW >= ROWS) continue;   // wave-uniform
+            const int n = (wave + 8 * i) * RPW + lrow;
+            uint2 hi, lo;
+            split4(pre[i], hi, lo);
+            *reinterpret_cast<uint2*>(hs_hi + n * HS + qq * KWQ + 4 * lc4) = hi;
+            *reinterpret_cast<uint2*>(hs_lo + n * HS + qq * KWQ + 4 * lc4) = lo;
           }
         };
-        auto mfma_tile = [&](int nb, int kq) {
-          const float4 x = *reinterpret_cast<const float4*>(&hs[(nb * 16 + lr) * kHsld + 16 * kq + 4 * lg]);
-          acc[nb] = mfma_k16(w[kq], x, acc[nb]);
+        // Fragment (nb, kc) of this lane sits at a compile-time offset from
+        // one per-lane base per part (within the 16-bit LDS offset field).
+        const _Float16* bhi = hs_hi + lr * HS + 8 * lg;
+        const _Float16* blo = hs_lo + lr * HS + 8 * lg;
+        auto mfma_tile = [&](int nb, int kc) {
+          const int o = nb * 16 * HS + 32 * kc;
+          acc[nb] = mfma3(wh[kc], wl[kc], *reinterpret_cast<const uint4*>(bhi + o),
+                          *reinterpret_cast<const uint4*>(blo + o), acc[nb]);
         };
+        load_inputs();
         gload(0);
-        sstore(0);
+        sstore(0);                                       // its wait covers the inputs too
+        seed();
         __syncthreads();
 #pragma unroll
         for (int qq = 0; qq < NQ; ++qq) {
           if (qq + 1 < NQ) {
             gload(qq + 1);
 #pragma unroll
-            for (int gq = 0; gq < QG; ++gq)
+            for (int pq = 0; pq < QC; ++pq)
 #pragma unroll
-              for (int nb = 0; nb < NB; ++nb) mfma_tile(nb, qq * QG + gq);
+              for (int nb = 0; nb < NB; ++nb) mfma_tile(nb, qq * QC + pq);
             sstore(qq + 1);
             __syncthreads();
           } else {
-            // Last quarter, row tile by row tile: the cell update of a tile
-            // overlaps the MFMAs of the next (same k order per tile).  The
-            // inputs, issued here, have landed by the first update.
-            load_inputs();
+            // Last piece, row tile by row tile: the cell update of a tile
+            // overlaps the MFMAs of the next (same k order per tile).
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-              for (int gq = 0; gq < QG; ++gq) mfma_tile(nb, qq * QG + gq);
-              if (nb == 1) wait_vmem();
+              for (int pq = 0; pq < QC; ++pq) mfma_tile(nb, qq * QC + pq);
               if (nb >= 1) cell(nb - 1);
             }
-            if (NB == 1) wait_vmem();
             cell(NB - 1);
           }
         }
@@ -889,14 +1017,18 @@ constexpr int kProjThreads = 512;
 
 template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
-  constexpr int KQ = 4 * NCH;                 // 16-wide k groups: K = H = 64 NCH
-  constexpr int NQ = NCH >= 4 ? 4 : NCH;      // chunks per row tile
-  constexpr int QG = KQ / NQ;                 // k groups per chunk (<= 8)
-  constexpr int CW = QG * 16 + 8;             // padded LDS row of a chunk (an odd multiple of 8 floats)
-  constexpr int CF4 = 64 * QG * 4;            // float4 per chunk
+  constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
+  constexpr int NQ = split_quarters(NCH);     // ring chunks per row tile
+  constexpr int QC = KC / NQ;                 // k chunks per ring chunk
+  constexpr int KW = QC * 32;                 // k per ring chunk
+  constexpr int SW = KW + 16;                 // padded LDS row in halves (an odd multiple of 32 bytes)
+  constexpr int CF4 = 64 * KW / 4;            // float4 per ring chunk
   constexpr int PT = (CF4 + kProjThreads - 1) / kProjThreads;
-  constexpr int LDS_FLOATS = (2 * 64 * CW > 128 * kZld) ? 2 * 64 * CW : 128 * kZld;
-  __shared__ float xs[LDS_FLOATS];            // ring [2][64][CW]; probe scratch while forming weights
+  constexpr int RING_BYTES = 2 * 2 * 64 * SW * 2;
+  constexpr int LDS_BYTES = RING_BYTES > 128 * kZld * 4 ? RING_BYTES : 128 * kZld * 4;
+  // ring [buf][hi, lo][64][SW] halves; probe scratch while forming weights
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  _Float16* ring = reinterpret_cast<_Float16*>(lds);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T;
   const int R = (T - 1) * B;
@@ -928,20 +1060,22 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
   const __amdgpu_buffer_rsrc_t gbuf =
       buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(static_cast<int64_t>(R) * H4 * sizeof(float)));
 
-  float4 w[KQ];
-  resident_weights<KQ, true, kRad>(w, xs, th, a.off_l, a.in_l + H, 0, H, mb * 128, a.probe, key, pair, step_lo, seps);
+  uint4 wh[KC], wl[KC];
+  resident_weights_split<KC, true, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, a.in_l + H, 0, H,
+                                         mb * 128, a.probe, key, pair, step_lo, seps);
 
-  // Chunk c covers rows [64 (c / NQ), +64) and k [QG 16 (c % NQ), +QG 16);
-  // rows past R read row R - 1 and are never stored.
+  // Ring chunk c covers rows [64 (c / NQ), +64) and k [KW (c % NQ), +KW);
+  // rows past R read row R - 1 and are never stored.  h is split into its
+  // fp16 parts as it is staged.
   const int nchunks = ((R + 63) / 64) * NQ;
   float4 pre[PT];
   auto gload = [&](int c) {
-    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * QG * 16;
+    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * KW;
 #pragma unroll
     for (int i = 0; i < PT; ++i) {
       const int idx = threadIdx.x + i * kProjThreads;
       if (idx < CF4) {
-        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+        const int c4 = idx % (KW / 4), n = idx / (KW / 4);
         const int row = r0 + n < R ? r0 + n : R - 1;
         pre[i] = buffer_load_f4<0>(hbuf, static_cast<uint32_t>((row * H + k0 + 4 * c4) * 4));
       }
@@ -952,8 +1086,11 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
     for (int i = 0; i < PT; ++i) {
       const int idx = threadIdx.x + i * kProjThreads;
       if (idx < CF4) {
-        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
-        *reinterpret_cast<float4*>(&xs[(buf * 64 + n) * CW + 4 * c4]) = pre[i];
+        const int c4 = idx % (KW / 4), n = idx / (KW / 4);
+        uint2 hi, lo;
+        split4(pre[i], hi, lo);
+        *reinterpret_cast<uint2*>(ring + ((buf * 2) * 64 + n) * SW + 4 * c4) = hi;
+        *reinterpret_cast<uint2*>(ring + ((buf * 2 + 1) * 64 + n) * SW + 4 * c4) = lo;
       }
     }
   };
@@ -969,13 +1106,15 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
     const int buf = c & 1, qq = c % NQ;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      if (q == qq) {                           // compile-time register index into w
+      if (q == qq) {                           // compile-time register index into wh, wl
 #pragma unroll
-        for (int gq = 0; gq < QG; ++gq)
+        for (int pq = 0; pq < QC; ++pq)
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) {
-            const float4 x = *reinterpret_cast<const float4*>(&xs[(buf * 64 + nb * 16 + lr) * CW + 16 * gq + 4 * lg]);
-            acc[nb] = mfma_k16(w[q * QG + gq], x, acc[nb]);
+            const int o = (nb * 16 + lr) * SW + 32 * pq + 8 * lg;
+            const uint4 bh = *reinterpret_cast<const uint4*>(ring + (buf * 2) * 64 * SW + o);
+            const uint4 bl = *reinterpret_cast<const uint4*>(ring + (buf * 2 + 1) * 64 * SW + o);
+            acc[nb] = mfma3(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc[nb]);
           }
       }
     }
@@ -1013,15 +1152,18 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
 // ---------------------------------------------------------------------------
 template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int nslots, float2* hpart, float* htgt) {
-  constexpr int KQ = 4 * NCH;
-  constexpr int NQ = NCH >= 4 ? 4 : NCH;
-  constexpr int QG = KQ / NQ;
-  constexpr int CW = QG * 16 + 8;
-  constexpr int CF4 = 64 * QG * 4;
+  constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
+  constexpr int NQ = split_quarters(NCH);     // ring chunks per row tile
+  constexpr int QC = KC / NQ;
+  constexpr int KW = QC * 32;
+  constexpr int SW = KW + 16;                 // padded LDS row in halves (an odd multiple of 32 bytes)
+  constexpr int CF4 = 64 * KW / 4;
   constexpr int PT = (CF4 + kProjThreads - 1) / kProjThreads;
-  constexpr int LDS_FLOATS = (2 * 64 * CW > 128 * kZld) ? 2 * 64 * CW : 128 * kZld;
-  __shared__ float xs[LDS_FLOATS];
+  constexpr int RING_BYTES = 2 * 2 * 64 * SW * 2;
+  constexpr int LDS_BYTES = RING_BYTES > 128 * kZld * 4 ? RING_BYTES : 128 * kZld * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];   // ring [buf][hi, lo][64][SW]
   __shared__ float2 red[2][8][64];              // per-wave (m, s) of each row, by tile parity
+  _Float16* ring = reinterpret_cast<_Float16*>(lds);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T;
   const int R = (T - 1) * B;
@@ -1054,18 +1196,19 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
   float2* hp = hpart + (slot * 2 + vh) * R;
   float* tg = htgt + slot * R;
 
-  float4 w[KQ];
-  resident_weights<KQ, false, kRad>(w, xs, th, a.off_head, H, 0, H, vh * 128, a.probe, key, pair, step_lo, seps);
+  uint4 wh[KC], wl[KC];
+  resident_weights_split<KC, false, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_head, H, 0, H, vh * 128,
+                                          a.probe, key, pair, step_lo, seps);
 
   const int nchunks = ((R + 63) / 64) * NQ;
   float4 pre[PT];
   auto gload = [&](int c) {
-    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * QG * 16;
+    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * KW;
 #pragma unroll
     for (int i = 0; i < PT; ++i) {
       const int idx = threadIdx.x + i * kProjThreads;
       if (idx < CF4) {
-        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
+        const int c4 = idx % (KW / 4), n = idx / (KW / 4);
         const int row = r0 + n < R ? r0 + n : R - 1;
         pre[i] = buffer_load_f4<0>(hbuf, static_cast<uint32_t>((row * H + k0 + 4 * c4) * 4));
       }
@@ -1076,8 +1219,11 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
     for (int i = 0; i < PT; ++i) {
       const int idx = threadIdx.x + i * kProjThreads;
       if (idx < CF4) {
-        const int c4 = idx % (QG * 4), n = idx / (QG * 4);
-        *reinterpret_cast<float4*>(&xs[(buf * 64 + n) * CW + 4 * c4]) = pre[i];
+        const int c4 = idx % (KW / 4), n = idx / (KW / 4);
+        uint2 hi, lo;
+        split4(pre[i], hi, lo);
+        *reinterpret_cast<uint2*>(ring + ((buf * 2) * 64 + n) * SW + 4 * c4) = hi;
+        *reinterpret_cast<uint2*>(ring + ((buf * 2 + 1) * 64 + n) * SW + 4 * c4) = lo;
       }
     }
   };
@@ -1102,13 +1248,15 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
     }
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      if (q == qq) {                            // compile-time register index into w
+      if (q == qq) {                            // compile-time register index into wh, wl
 #pragma unroll
-        for (int gq = 0; gq < QG; ++gq)
+        for (int pq = 0; pq < QC; ++pq)
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) {
-            const float4 x = *reinterpret_cast<const float4*>(&xs[(buf * 64 + nb * 16 + lr) * CW + 16 * gq + 4 * lg]);
-            acc[nb] = mfma_k16(w[q * QG + gq], x, acc[nb]);
+            const int o = (nb * 16 + lr) * SW + 32 * pq + 8 * lg;
+            const uint4 bh = *reinterpret_cast<const uint4*>(ring + (buf * 2) * 64 * SW + o);
+            const uint4 bl = *reinterpret_cast<const uint4*>(ring + (buf * 2 + 1) * 64 * SW + o);
+            acc[nb] = mfma3(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc[nb]);
           }
       }
     }

@@ -136,9 +136,13 @@ def test_chunking_does_not_change_the_result():
 
 @pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("b64_h128", 0), ("b40_h384", 0),
                                         ("b64_h128", 1)])
-def test_persistent_and_per_step_recurrence_agree_bitwise(name, probe):
-    """The persistent recurrence (probe tile resident in LDS, group barriers)
-    and the per-step launches accumulate in the same order: identical bits."""
+def test_persistent_and_per_step_recurrence_agree(name, probe):
+    """The persistent recurrence (weights resident in registers, group
+    barriers, products on the fp16 matrix cores from split operands) against
+    the per-step launches (fp32 products): one launch per layer and chunk
+    against one per time step, and the same losses and update up to the
+    split's rounding (about 2^-21 per operand; each path is also held to the
+    oracle by the parity tests)."""
     torch = require_gpu()
     N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
     theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
@@ -160,19 +164,22 @@ def test_persistent_and_per_step_recurrence_agree_bitwise(name, probe):
     assert n0 == L * chunks      # one persistent launch per layer and chunk
     print(f"{name}: recurrence launches persistent={n0} per-step={n1}")
     assert np.all(np.isfinite(l0))
-    assert np.array_equal(l0, l1)
-    assert np.array_equal(t0, t1)
+    rel = np.abs(l0.astype(np.float64) - l1) / np.abs(l1)
+    print(f"{name} law {probe}: persistent vs per-step loss rel {rel.max():.2e}")
+    assert rel.max() <= 1e-5, rel.max()
+    assert_theta_close(t0, t1)
 
 
 @pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("b64_h128", 0), ("b40_h384", 0),
                                         ("h512_short", 1), ("b40_h384", 2)])
 def test_streaming_and_tiled_weights_agree(name, probe):
     """The streaming projection and head (weights resident in registers,
-    probes drawn once per 128 weight rows) against the tiled kernels (probes
-    regenerated per row tile).  The projections sum over k in the same order;
-    the streaming head merges the softmax of two vocabulary halves, so the
-    cross entropies agree up to fp32 rounding order (one ulp-level term per
-    token, 1e-6 relative on the per-pair mean).  The cases cover a ragged last
+    probes drawn once per 128 weight rows, products on the fp16 matrix cores
+    from split operands) against the tiled kernels (probes regenerated per row
+    tile, fp32 products).  The two product paths differ by the split's
+    rounding (about 2^-21 per operand), so the per-pair mean losses agree to
+    1e-5 relative and the updated weights to the parity tolerance; each path
+    is held to the oracle by the parity tests.  The cases cover a ragged last
     row tile (R = 80, 320) and slot counts that are and are not a multiple of
     8 (the two block-to-job mappings)."""
     torch = require_gpu()
@@ -191,7 +198,8 @@ def test_streaming_and_tiled_weights_agree(name, probe):
     (t0, l0), (t1, l1) = outs
     assert np.all(np.isfinite(l0))
     rel = np.abs(l0.astype(np.float64) - l1) / np.abs(l1)
-    assert rel.max() <= 1e-6, rel.max()
+    print(f"{name} law {probe}: streaming vs tiled loss rel {rel.max():.2e}")
+    assert rel.max() <= 1e-5, rel.max()
     assert_theta_close(t0, t1)
 
 
