@@ -1029,7 +1029,8 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
   // ring [buf][hi, lo][64][SW] halves; probe scratch while forming weights
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
   _Float16* ring = reinterpret_cast<_Float16*>(lds);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform (scalar)
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T;
   const int R = (T - 1) * B;
   const int H4 = 4 * H;
@@ -1068,33 +1069,36 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
   // rows past R read row R - 1 and are never stored.  h is split into its
   // fp16 parts as it is staged.
   const int nchunks = ((R + 63) / 64) * NQ;
+  // Wave load i of a ring chunk covers rows (wave + 8 i) RPW + lane / CW4,
+  // float4 lane % CW4 of the chunk: a per-lane part and a scalar part.
+  // Rows past R read zeros (past the slot's buffer) and are never stored.
+  constexpr int CW4 = KW / 4, RPW = 64 / CW4;
+  static_assert(CW4 * RPW == 64 && PT * 8 * RPW == 64, "ring chunk rows must split evenly over the waves");
+  const int lrow = lane / CW4, lc4 = lane % CW4;
+  const uint32_t lane_off = static_cast<uint32_t>((lrow * H + 4 * lc4) * 4);
   float4 pre[PT];
   auto gload = [&](int c) {
     const int r0 = (c / NQ) * 64, k0 = (c % NQ) * KW;
 #pragma unroll
     for (int i = 0; i < PT; ++i) {
-      const int idx = threadIdx.x + i * kProjThreads;
-      if (idx < CF4) {
-        const int c4 = idx % (KW / 4), n = idx / (KW / 4);
-        const int row = r0 + n < R ? r0 + n : R - 1;
-        pre[i] = buffer_load_f4<0>(hbuf, static_cast<uint32_t>((row * H + k0 + 4 * c4) * 4));
-      }
+      const uint32_t soff = static_cast<uint32_t>(((r0 + (wave + 8 * i) * RPW) * H + k0) * 4);
+      typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hbuf, lane_off, soff, 0);
+      pre[i] = make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < PT; ++i) {
-      const int idx = threadIdx.x + i * kProjThreads;
-      if (idx < CF4) {
-        const int c4 = idx % (KW / 4), n = idx / (KW / 4);
-        uint2 hi, lo;
-        split4(pre[i], hi, lo);
-        *reinterpret_cast<uint2*>(ring + ((buf * 2) * 64 + n) * SW + 4 * c4) = hi;
-        *reinterpret_cast<uint2*>(ring + ((buf * 2 + 1) * 64 + n) * SW + 4 * c4) = lo;
-      }
+      const int n = (wave + 8 * i) * RPW + lrow;
+      uint2 hi, lo;
+      split4(pre[i], hi, lo);
+      *reinterpret_cast<uint2*>(ring + ((buf * 2) * 64 + n) * SW + 4 * lc4) = hi;
+      *reinterpret_cast<uint2*>(ring + ((buf * 2 + 1) * 64 + n) * SW + 4 * lc4) = lo;
     }
   };
 
+  const _Float16* blane = ring + lr * SW + 8 * lg;   // this lane's B fragments sit at constant offsets from here
   f32x4 acc[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1111,9 +1115,9 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
         for (int pq = 0; pq < QC; ++pq)
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) {
-            const int o = (nb * 16 + lr) * SW + 32 * pq + 8 * lg;
-            const uint4 bh = *reinterpret_cast<const uint4*>(ring + (buf * 2) * 64 * SW + o);
-            const uint4 bl = *reinterpret_cast<const uint4*>(ring + (buf * 2 + 1) * 64 * SW + o);
+            const int o = nb * 16 * SW + 32 * pq;
+            const uint4 bh = *reinterpret_cast<const uint4*>(blane + (buf * 2) * 64 * SW + o);
+            const uint4 bl = *reinterpret_cast<const uint4*>(blane + (buf * 2 + 1) * 64 * SW + o);
             acc[nb] = mfma3(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc[nb]);
           }
       }
