@@ -362,7 +362,8 @@ int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds_dev, uint64_t st
 typedef struct soma_phase_times {
   float fold_ms;          /* layer-1 gate inputs per byte value (k_fold) */
   float proj_ms;          /* input projections of layers >= 2 (k_proj) */
-  float rec_ms;           /* recurrent time steps of all layers (k_rec_step) */
+  float rec_ms;           /* recurrent time steps of all layers (k_rec_step); for
+                             SOMA_ARCH_BODY the whole fused forward (k_body) */
   float head_ms;          /* head + softmax cross entropy (k_head_ce) */
   float reduce_ms;        /* loss sums and coefficients */
   float update_ms;        /* regenerate-and-update (k_update) */
