@@ -1018,7 +1018,7 @@ constexpr int kProjThreads = 512;
 template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
   constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
-  constexpr int NQ = split_quarters(NCH);     // ring chunks per row tile
+  constexpr int NQ = NCH % 4 == 0 ? NCH / 4 : split_quarters(NCH);   // ring chunks per row tile (256 k each where possible)
   constexpr int QC = KC / NQ;                 // k chunks per ring chunk
   constexpr int KW = QC * 32;                 // k per ring chunk
   constexpr int SW = KW + 16;                 // padded LDS row in halves (an odd multiple of 32 bytes)
