@@ -696,8 +696,13 @@ __device__ __forceinline__ float4 buffer_load_f4(__amdgpu_buffer_rsrc_t r, uint3
   return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
 }
 
-// Batch row of lane row b (rows past the batch read the last row).
-__device__ __forceinline__ int brow_of(int b, int B) { return b < B ? b : B - 1; }
+// float4 load at a per-lane plus a wave-uniform (scalar) offset.
+template <int kAux>
+__device__ __forceinline__ float4 buffer_load_f4s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kAux);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
 
 // Perturbed weights of the block's 128 rows r0 .. r0 + 127 over columns
 // col0 .. col0 + 16 KQ of a matrix at canonical offset off_l with row length
@@ -843,47 +848,54 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     uint4 wh[KC], wl[KC];
     resident_weights_split<KC, true, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H, in, H,
                                            utile * 128, a.probe, key, pair, step_lo, seps);
-    // Rows past the batch compute on the last row's inputs and h (a column
-    // of the product depends only on the same column of h, so no stored
-    // output depends on them) and are never stored.  So the step has no
-    // divergent branches: its loads issue together, and the stores of h, all
-    // at its end, are not waited on before the arrival.  (They do not read
-    // the rows that follow h_{t-1}, which are h_t and still being written:
-    // every h load happens after the wait that publishes its row.)
+    // Rows past the batch compute on whatever follows in the same buffers
+    // (finite inputs and h of later rows, possibly being rewritten, or zeros
+    // past a buffer's end): a column of the product depends only on the same
+    // column of h, so no stored output depends on them, and they are never
+    // stored.  So the step has no divergent branches: its loads issue
+    // together, and the stores of h, all at its end, are not waited on
+    // before the arrival.
     // All addresses of the step loop are 32-bit offsets into the buffers
     // above (a few VGPRs instead of one 64-bit pointer per row).
+    // Lane row lr of row tile nb is batch row 16 nb + lr: a per-lane offset
+    // plus a scalar one.  Rows past the batch (B < 16 NB) read the data that
+    // follows in the same buffer, or zeros past its end.
     float cs[NB];
     int vnext[NB];
+    const uint32_t byte_lane = static_cast<uint32_t>(lr * T);
+    const uint32_t gi_lane = static_cast<uint32_t>((lr * 4 * H + 4 * unit) * 4);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       cs[nb] = 0.0f;
       vnext[nb] = a.layer == 0
-                      ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, static_cast<uint32_t>(brow_of(nb * 16 + lr, B) * T), 0, 0)
+                      ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T), 0)
                       : 0;
     }
 
+    // Gate inputs of step tt; they seed the accumulators, which the
+    // products then add to.  Layer 1 reads its folded inputs by byte value
+    // (the byte of step tt + 1 is fetched along).  The inputs of step t + 1
+    // are requested as soon as step t has arrived, so their HBM latency
+    // overlaps the group barrier instead of the staging of h_t.
+    float4 gi[NB];
+    auto load_inputs = [&](int tt) {
+      if (a.layer == 0) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          gi[nb] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vnext[nb] * 4 * H + 4 * unit) * 4));
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          vnext[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane,
+                                                          static_cast<uint32_t>(nb * 16 * T + tt + 1), 0);
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          gi[nb] = buffer_load_f4s<0>(gbuf, gi_lane, static_cast<uint32_t>((tt * B + nb * 16) * 4 * H * 4));
+      }
+    };
+    load_inputs(0);
+
     for (int t = 0; t + 1 < T; ++t) {
-      // Gate inputs of step t, loaded with the first piece of h_{t-1}; they
-      // seed the accumulators, which the products then add to.  Layer 1
-      // reads its folded inputs by byte value; the bytes of step t + 1
-      // (t + 1 < T) are fetched one step ahead.
-      float4 gi[NB];
-      auto load_inputs = [&]() {
-        if (a.layer == 0) {
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            gi[nb] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vnext[nb] * 4 * H + 4 * unit) * 4));
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            vnext[nb] = __builtin_amdgcn_raw_buffer_load_b8(
-                bbuf, static_cast<uint32_t>(brow_of(nb * 16 + lr, B) * T + t + 1), 0, 0);
-        } else {
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            gi[nb] = buffer_load_f4<0>(
-                gbuf, static_cast<uint32_t>(((t * B + brow_of(nb * 16 + lr, B)) * 4 * H + 4 * unit) * 4));
-        }
-      };
       f32x4 acc[NB];
       auto seed = [&]() {
 #pragma unroll
@@ -899,7 +911,6 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       };
 
       if (t == 0) {
-        load_inputs();
         wait_vmem();
         seed();
 #pragma unroll
@@ -948,7 +959,6 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
           acc[nb] = mfma3(wh[kc], wl[kc], *reinterpret_cast<const uint4*>(bhi + o),
                           *reinterpret_cast<const uint4*>(blo + o), acc[nb]);
         };
-        load_inputs();
         gload(0);
         sstore(0);                                       // its wait covers the inputs too
         seed();
@@ -996,6 +1006,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       // group moves on: group_arrive's barrier orders the next step's staging.
       group_arrive(bar);
       ++done;
+      if (t + 2 < T) load_inputs(t + 1);
     }
   }
 }
