@@ -875,8 +875,11 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     // Gate inputs of step tt; they seed the accumulators, which the
     // products then add to.  Layer 1 reads its folded inputs by byte value
     // (the byte of step tt + 1 is fetched along).  The inputs of step t + 1
-    // are requested as soon as step t has arrived, so their HBM latency
-    // overlaps the group barrier instead of the staging of h_t.
+    // are requested at the start of step t's last piece of products (the
+    // staging registers are free by then), so their HBM latency is hidden
+    // by the products and the cell updates; by the arrival only the stores
+    // of h_t are outstanding, and the barrier polls, which return in order
+    // behind earlier loads of the same wave, are not held up.
     float4 gi[NB];
     auto load_inputs = [&](int tt) {
       if (a.layer == 0) {
@@ -913,6 +916,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       if (t == 0) {
         wait_vmem();
         seed();
+        if (t + 2 < T) load_inputs(t + 1);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) cell(nb);
       } else {
@@ -976,6 +980,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
           } else {
             // Last piece, row tile by row tile: the cell update of a tile
             // overlaps the MFMAs of the next (same k order per tile).
+            if (t + 2 < T) load_inputs(t + 1);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
@@ -1006,7 +1011,6 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       // group moves on: group_arrive's barrier orders the next step's staging.
       group_arrive(bar);
       ++done;
-      if (t + 2 < T) load_inputs(t + 1);
     }
   }
 }
