@@ -611,8 +611,8 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
 // H/32 co-resident blocks carries one (expert, direction, sign) through time:
 // after step t every block publishes its slice of h_t and arrives on the
 // group's counter; before step t+1 it waits for all H/32 arrivals, then
-// stages the whole h_{t-1} of its sign (B x H) in LDS, a quarter of K at a
-// time, overlapping the next quarter's loads with the current quarter's
+// stages the whole h_{t-1} of its sign (B x H) in LDS, 128 columns of K at
+// a time, overlapping the next piece's loads with the current piece's
 // MFMAs.  Groups take jobs round-robin; the cell state stays in registers.
 // One block per CU (two waves per SIMD).
 //
@@ -793,10 +793,11 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
 template <int NB, int NCH, bool kRad>
 __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
   constexpr int KC = 2 * NCH;                           // 32-wide k chunks: H = 64 NCH
-  // Staging pieces of K, each the largest of 256, 128, 64 that divides H:
-  // long enough that a piece's products outlast the loads of the next, and
-  // a whole number of 16-lane row segments per wave load.
-  constexpr int KWQ = (64 * NCH) % 256 == 0 ? 256 : ((64 * NCH) % 128 == 0 ? 128 : 64);   // k per piece
+  // Staging pieces of K, 128 wide where H allows, else 64: the first piece,
+  // whose loads nothing hides, stays short, while a piece's products still
+  // outlast the loads of the next (measured at H = 512: 256-wide pieces cost
+  // 7% more time per step, 64-wide ones 8%).
+  constexpr int KWQ = (64 * NCH) % 128 == 0 ? 128 : 64;   // k per piece
   constexpr int NQ = 64 * NCH / KWQ;
   constexpr int QC = KWQ / 32;                          // k chunks per piece
   constexpr int ROWS = NB * 16;
