@@ -96,14 +96,25 @@ __device__ __forceinline__ void split8v(const float4& a, const float4& b, uint4&
   lo = make_uint4(l0.x, l0.y, l1.x, l1.y);
 }
 
-// acc += A B over one 32-wide K chunk from split fragments (8 halves per lane).
-__device__ __forceinline__ f32x4 mfma3(const uint4& ah, const uint4& al, const uint4& bh, const uint4& bl,
-                                       f32x4 acc) {
+// acc[nb] += A B_nb over one 32-wide K chunk from split fragments (8 halves
+// per lane: A = A_hi + A_lo, B = B_hi + B_lo, the lo x lo product dropped)
+// for NT row tiles that share the A fragments; the B fragments of every
+// tile are read beforehand.  Each pass runs over the tiles, so neighbouring
+// MFMAs use independent accumulators: one tile at a time would serialise
+// the three passes behind each other and behind the tile's LDS reads.
+template <int NT>
+__device__ __forceinline__ void mfma3_batch(const uint4& ah, const uint4& al, const uint4 (&bh)[NT],
+                                            const uint4 (&bl)[NT], f32x4 (&acc)[NT]) {
   const h8 AH = __builtin_bit_cast(h8, ah), AL = __builtin_bit_cast(h8, al);
-  const h8 BH = __builtin_bit_cast(h8, bh), BL = __builtin_bit_cast(h8, bl);
-  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AL, BH, acc, 0, 0, 0);
-  acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, BL, acc, 0, 0, 0);
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, BH, acc, 0, 0, 0);
+#pragma unroll
+  for (int nb = 0; nb < NT; ++nb)
+    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(AL, __builtin_bit_cast(h8, bh[nb]), acc[nb], 0, 0, 0);
+#pragma unroll
+  for (int nb = 0; nb < NT; ++nb)
+    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, __builtin_bit_cast(h8, bl[nb]), acc[nb], 0, 0, 0);
+#pragma unroll
+  for (int nb = 0; nb < NT; ++nb)
+    acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, __builtin_bit_cast(h8, bh[nb]), acc[nb], 0, 0, 0);
 }
 
 // Pieces of K = 64 NCH staged per pass of the streaming and persistent
@@ -959,10 +970,14 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         // one per-lane base per part (within the 16-bit LDS offset field).
         const _Float16* bhi = hs_hi + lr * HS + 8 * lg;
         const _Float16* blo = hs_lo + lr * HS + 8 * lg;
-        auto mfma_tile = [&](int nb, int kc) {
-          const int o = nb * 16 * HS + 32 * kc;
-          acc[nb] = mfma3(wh[kc], wl[kc], *reinterpret_cast<const uint4*>(bhi + o),
-                          *reinterpret_cast<const uint4*>(blo + o), acc[nb]);
+        auto mfma_chunk = [&](int kc) {
+          uint4 bh[NB], bl[NB];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * HS + 32 * kc);
+            bl[nb] = *reinterpret_cast<const uint4*>(blo + nb * 16 * HS + 32 * kc);
+          }
+          mfma3_batch<NB>(wh[kc], wl[kc], bh, bl, acc);
         };
         gload(0);
         sstore(0);                                       // its wait covers the inputs too
@@ -973,22 +988,15 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
           if (qq + 1 < NQ) {
             gload(qq + 1);
 #pragma unroll
-            for (int pq = 0; pq < QC; ++pq)
-#pragma unroll
-              for (int nb = 0; nb < NB; ++nb) mfma_tile(nb, qq * QC + pq);
+            for (int pq = 0; pq < QC; ++pq) mfma_chunk(qq * QC + pq);
             sstore(qq + 1);
             __syncthreads();
           } else {
-            // Last piece, row tile by row tile: the cell update of a tile
-            // overlaps the MFMAs of the next (same k order per tile).
             if (t + 2 < T) load_inputs(t + 1);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
+            for (int pq = 0; pq < QC; ++pq) mfma_chunk(qq * QC + pq);
 #pragma unroll
-              for (int pq = 0; pq < QC; ++pq) mfma_tile(nb, qq * QC + pq);
-              if (nb >= 1) cell(nb - 1);
-            }
-            cell(NB - 1);
+            for (int nb = 0; nb < NB; ++nb) cell(nb);
           }
         }
       }
@@ -1128,14 +1136,16 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
     for (int q = 0; q < NQ; ++q) {
       if (q == qq) {                           // compile-time register index into wh, wl
 #pragma unroll
-        for (int pq = 0; pq < QC; ++pq)
+        for (int pq = 0; pq < QC; ++pq) {
+          uint4 bh[4], bl[4];
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) {
             const int o = nb * 16 * SW + 32 * pq;
-            const uint4 bh = *reinterpret_cast<const uint4*>(blane + (buf * 2) * 64 * SW + o);
-            const uint4 bl = *reinterpret_cast<const uint4*>(blane + (buf * 2 + 1) * 64 * SW + o);
-            acc[nb] = mfma3(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc[nb]);
+            bh[nb] = *reinterpret_cast<const uint4*>(blane + (buf * 2) * 64 * SW + o);
+            bl[nb] = *reinterpret_cast<const uint4*>(blane + (buf * 2 + 1) * 64 * SW + o);
           }
+          mfma3_batch<4>(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc);
+        }
       }
     }
     if (qq == NQ - 1) {
@@ -1270,14 +1280,16 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
     for (int q = 0; q < NQ; ++q) {
       if (q == qq) {                            // compile-time register index into wh, wl
 #pragma unroll
-        for (int pq = 0; pq < QC; ++pq)
+        for (int pq = 0; pq < QC; ++pq) {
+          uint4 bh[4], bl[4];
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) {
             const int o = (nb * 16 + lr) * SW + 32 * pq + 8 * lg;
-            const uint4 bh = *reinterpret_cast<const uint4*>(ring + (buf * 2) * 64 * SW + o);
-            const uint4 bl = *reinterpret_cast<const uint4*>(ring + (buf * 2 + 1) * 64 * SW + o);
-            acc[nb] = mfma3(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc[nb]);
+            bh[nb] = *reinterpret_cast<const uint4*>(ring + (buf * 2) * 64 * SW + o);
+            bl[nb] = *reinterpret_cast<const uint4*>(ring + (buf * 2 + 1) * 64 * SW + o);
           }
+          mfma3_batch<4>(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc);
+        }
       }
     }
     if (qq == NQ - 1) {
