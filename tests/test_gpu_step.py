@@ -15,6 +15,7 @@ CASES = {
     "ragged_l2_summed": (2, 2, 48, 32, 20, 37, 3, 1e-3, 1e-2, 1, 2),
     "l3_b70": (3, 3, 16, 80, 70, 9, 2, 2e-3, 5e-3, 0, 0),
     "h512_short": (1, 2, 512, 512, 16, 6, 2, 1e-3, 1e-3, 0, 0),
+    "h512_b50": (1, 2, 64, 512, 50, 7, 2, 1e-3, 1e-3, 0, 0),   # split-h ring, rows 50..63 never written
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
 }
@@ -134,8 +135,8 @@ def test_chunking_does_not_change_the_result():
         assert np.array_equal(th, outs[0][0]) and np.array_equal(ls, outs[0][1])
 
 
-@pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("b64_h128", 0), ("b40_h384", 0),
-                                        ("b64_h128", 1)])
+@pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("h512_b50", 0), ("b64_h128", 0),
+                                        ("b40_h384", 0), ("b64_h128", 1)])
 def test_persistent_and_per_step_recurrence_agree(name, probe):
     """The persistent recurrence (weights resident in registers, group
     barriers, products on the fp16 matrix cores from split operands) against
