@@ -15,7 +15,9 @@ CASES = {
     "ragged_l2_summed": (2, 2, 48, 32, 20, 37, 3, 1e-3, 1e-2, 1, 2),
     "l3_b70": (3, 3, 16, 80, 70, 9, 2, 2e-3, 5e-3, 0, 0),
     "h512_short": (1, 2, 512, 512, 16, 6, 2, 1e-3, 1e-3, 0, 0),
-    "h512_b50": (1, 2, 64, 512, 50, 7, 2, 1e-3, 1e-3, 0, 0),   # split-h ring, rows 50..63 never written
+    "h512_b50": (1, 2, 64, 512, 50, 7, 2, 1e-3, 1e-3, 0, 0),   # four row tiles, rows 50..63 past the batch
+    "t2_b1_p1": (1, 2, 32, 64, 1, 2, 1, 1e-3, 1e-2, 0, 0),    # one target per sequence: a single recurrence step
+    "h16_fallback": (2, 2, 16, 16, 5, 11, 2, 1e-3, 1e-2, 0, 0),  # H % 64 != 0: per-step and tiled kernels
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
 }
