@@ -374,6 +374,15 @@ typedef struct soma_phase_times {
 /* Turn phase timing on (enable != 0) or off for later steps on ctx. */
 int soma_set_phase_timing(soma_ctx* ctx, int enable);
 
+/* Polls a block of the persistent recurrence makes at one group barrier
+ * before it gives up, for later steps on ctx (default 2^20, about a second;
+ * 0 restores the default).  A block that gives up sets the step's sticky
+ * abort flag, every block that sees it leaves, the launch drains and the
+ * step is aborted as an invalid rate is: the losses read NaN and theta (and
+ * the Adam moments) are left untouched.  A tiny limit exercises that path;
+ * it is not a tuning knob.  Errors: SOMA_EINVAL for a NULL ctx. */
+int soma_set_spin_limit(soma_ctx* ctx, uint32_t polls);
+
 /* Wait for the last timed step's events and report its phase times.
  * Returns SOMA_EINVAL if no step ran with timing enabled. */
 int soma_get_phase_times(soma_ctx* ctx, soma_phase_times* out);

@@ -187,6 +187,7 @@ struct soma_ctx {
   bool have_coef;
   // phase timing
   bool timing;
+  unsigned spin_limit;              // polls per group barrier of the persistent recurrence
   bool have_times;
   // device facts for the persistent recurrence
   int coop_blocks;                  // co-resident k_rec_persist blocks (0: path unavailable)
@@ -260,7 +261,7 @@ __global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs,
   const double* p = part + ((int64_t(e) * PC + jl) * NS + s) * row_tiles;
   double tot = 0.0;
   for (int k = 0; k < row_tiles; ++k) tot += p[k];
-  if (err && *err) tot = __builtin_nan("");   // an aborted persistent launch voids the step
+  if (err && *err) tot = __builtin_nan("");   // an aborted step (k_coef voids earlier chunks too)
   const int64_t o = (int64_t(e) * P + j0 + jl) * NS + s;
   losses[o] = static_cast<float>(tot * inv_rows);
   if (lossd) lossd[o] = tot * inv_rows;
@@ -268,11 +269,20 @@ __global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs,
 
 // c[e][j] = (L+ - L-) / (2 eps P) from the fp64 means, rounded once to fp32;
 // summed mode: the differences of all experts added in expert order, the
-// same coefficient for every expert.
+// same coefficient for every expert.  It runs once after every direction
+// chunk: if the step was aborted (the flag may have been set in a later
+// chunk than some losses were reduced in), every loss and coefficient of
+// the step reads NaN.
 __global__ void k_coef(const double* lossd, int N, int P, int summed, const float* eps_v, int eps_stride,
-                       float* coef) {
+                       float* coef, float* losses, const unsigned* err) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= N * P) return;
+  if (*err) {
+    losses[2 * int64_t(i)] = __builtin_nanf("");
+    losses[2 * int64_t(i) + 1] = __builtin_nanf("");
+    coef[i] = __builtin_nanf("");
+    return;
+  }
   const int j = i % P, e = i / P;
   auto inv_denom = [&](int x) { return 1.0 / (2.0 * double(eps_v[int64_t(x) * eps_stride]) * double(P)); };
   double c;
@@ -756,7 +766,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       p.err = p.bar + kMaxGroups;
       p.groups = groups;
       p.jobs = 2 * N * pcs;   // (expert, direction, sign)
-      p.spin_limit = kSpinLimit;
+      p.spin_limit = ctx->spin_limit;
       // Counters restart at zero for every launch; the abort flag is kept
       // (zeroed once per step) so that a failure anywhere in the step sticks.
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
@@ -847,6 +857,7 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
   ctx->head = nullptr;
   ctx->head_stride = 0;
   ctx->timing = false;
+  ctx->spin_limit = kSpinLimit;
   ctx->have_times = false;
   ctx->nmarks = 0;
   ctx->rec_launches = ctx->proj_launches = 0;
@@ -863,6 +874,12 @@ void soma_destroy(soma_ctx* ctx) {
 int soma_set_phase_timing(soma_ctx* ctx, int enable) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
   ctx->timing = enable != 0;
+  return ok();
+}
+
+int soma_set_spin_limit(soma_ctx* ctx, uint32_t polls) {
+  if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
+  ctx->spin_limit = polls == 0 ? kSpinLimit : polls;
   return ok();
 }
 
@@ -978,7 +995,7 @@ int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t*
   const int nc = c.n_experts * D;
   hipLaunchKernelGGL(soma::k_coef, dim3((nc + 255) / 256), dim3(256), 0, st,
                      reinterpret_cast<const double*>(ctx->ws + L.lossd), c.n_experts, D,
-                     c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, r.eps_v, r.eps_stride, coef);
+                     c.loss_mode == SOMA_LOSS_SUMMED ? 1 : 0, r.eps_v, r.eps_stride, coef, losses, err);
   if (int rc = check_launch("k_coef")) return rc;
   if (int rc = mark(ctx, kPhaseReduce, st)) return rc;
   *err_out = err;

@@ -25,7 +25,7 @@ EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destr
            "soma_apply_update", "soma_apply_adam", "soma_spsa_step_adam_sched", "soma_schedule_init",
            "soma_schedule_observe", "soma_estimator_moments", "soma_set_tied_head", "soma_head_delta",
            "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
-           "soma_get_phase_times",
+           "soma_get_phase_times", "soma_set_spin_limit",
            "soma_last_error")
 
 
@@ -111,6 +111,7 @@ def load():
             "soma_philox": (ctypes.c_int, [vp, vp, vp, u64, vp]),
             "soma_box_muller": (ctypes.c_int, [vp, vp, vp, vp, u64, vp]),
             "soma_set_phase_timing": (ctypes.c_int, [vp, ctypes.c_int]),
+            "soma_set_spin_limit": (ctypes.c_int, [vp, ctypes.c_uint32]),
             "soma_get_phase_times": (ctypes.c_int, [vp, ctypes.POINTER(PhaseTimes)]),
             "soma_last_error": (ctypes.c_char_p, []),
         }
@@ -252,6 +253,10 @@ class Context:
 
     def set_phase_timing(self, enable: bool = True):
         _check(load().soma_set_phase_timing(self._h, 1 if enable else 0))
+
+    def set_spin_limit(self, polls: int):
+        """Polls per group barrier of the persistent recurrence (0: default)."""
+        _check(load().soma_set_spin_limit(self._h, int(polls)))
 
     def phase_times(self) -> dict:
         out = PhaseTimes()

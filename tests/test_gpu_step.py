@@ -272,3 +272,32 @@ def test_accumulated_step_matches_oracle(oracle_mod, name, A, pc):
     # the batches differ, so the accumulated losses are not one batch's repeated
     lg = losses.cpu().numpy()
     assert not np.array_equal(lg[:, :P], lg[:, P:2 * P])
+
+
+def test_persistent_barrier_timeout_aborts_the_step():
+    """A persistent recurrence whose group barrier gives up (a spin limit of
+    one poll, forced from the host) aborts the whole step: every block leaves
+    through its own bounded wait, the losses read NaN and theta is left as it
+    was.  The next step on the same context, with the default limit, runs
+    normally (the abort flag is cleared per step)."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES["b64_h128"]
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = torch.from_numpy(synth.expert_batches([100 + e for e in range(N)], B, T)).cuda()
+    seeds = soma.seeds_tensor(synth.expert_seeds(N))
+    ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc))
+    ctx.set_phase_timing(True)
+    th = torch.from_numpy(theta.copy()).cuda()
+    losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+    ctx.set_spin_limit(1)
+    ctx.spsa_step(th, seeds, 0, eps, lr, data, losses)
+    torch.cuda.synchronize()
+    chunks = (P + pc - 1) // pc
+    assert ctx.phase_times()["rec_launches"] == L * chunks   # the persistent path ran
+    assert torch.isnan(losses).all()
+    assert np.array_equal(th.cpu().numpy(), theta)
+    ctx.set_spin_limit(0)
+    ctx.spsa_step(th, seeds, 0, eps, lr, data, losses)
+    torch.cuda.synchronize()
+    assert torch.isfinite(losses).all()
+    assert not np.array_equal(th.cpu().numpy(), theta)
