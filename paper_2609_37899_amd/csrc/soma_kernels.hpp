@@ -1016,7 +1016,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
               static_cast<uint32_t>(((t * B + n) * H + utile * kRecUnits + 4 * c4) * 4), 0, kCoherent);
         }
       }
-      // Every wave is done reading hs (its last quarter) and ht before the
+      // Every wave is done reading hs (its last piece) and ht before the
       // group moves on: group_arrive's barrier orders the next step's staging.
       group_arrive(bar);
       ++done;
@@ -1031,8 +1031,9 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 // direction, sign) slot: it forms their perturbed weights in registers once
 // (the probes are drawn once per job instead of once per row tile) and
 // streams all R = B (T-1) rows of the slot's h through a double-buffered LDS
-// ring of 64-row x K/4 chunks, one barrier per chunk; each lane stores the
-// four gates of one unit for its rows after every 64-row tile.
+// ring of 64-row chunks of 256 K values where H allows (else 128 or 64), one
+// barrier per chunk; each lane stores the four gates of one unit for its rows
+// after every 64-row tile.
 // Grid: slots * mblocks blocks of 512 threads; where the slot count is a
 // multiple of 8 the 16 row blocks of a slot run on one XCD (blocks are dealt
 // to XCDs round-robin), so they share its L2 while streaming the same h.
