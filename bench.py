@@ -30,7 +30,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 PEAK_FP16_MFMA_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 # Kernels whose products run on the fp16 matrix cores from split fp32
 # operands (three fp16 products per fp32 product, fp32 accumulation).
-SPLIT_F16_KERNELS = ("k_rec_persist", "k_proj_stream", "k_head_stream", "k_body")
+SPLIT_F16_KERNELS = ("k_rec_persist", "k_rec_local", "k_proj_stream", "k_head_stream", "k_body")
 PEAK_HBM_GBS = 8000.0
 PROBE_LAWS = {"gaussian": 0, "sparse": 1, "dense": 2}
 
@@ -227,11 +227,19 @@ def main():
     avg_launch_s = ms[dom] / 1e3 / launches[dom]
     achieved = per_launch_flops / avg_launch_s / 1e12
     traffic = None
-    kname = {"rec": "k_rec_step", "proj": "k_proj", "fold": "k_fold", "head": "k_head_ce"}[dom]
+    # The kernels the library picks for this shape (see soma_api.hip):
+    # streaming projection and head where H % 64 == 0, H <= 512 and one
+    # slot's gate inputs stay under 2^31 bytes; the recurrence one block per
+    # job at H = 64, else persistent (one launch per layer and chunk) unless
+    # it ran per time step.
+    streams = (w.hidden % 64 == 0 and w.hidden <= 512
+               and (w.seq_len - 1) * w.batch * 4 * w.hidden * 4 < 2 ** 31)
+    kname = {"rec": "k_rec_step", "proj": "k_proj_stream" if streams else "k_proj", "fold": "k_fold",
+             "head": "k_head_stream" if streams else "k_head_ce"}[dom]
     if w.arch == 1:
         kname = "k_body"          # the whole perturbed forward, one launch per direction chunk
     elif dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
-        kname = "k_rec_persist"   # one persistent launch per layer and direction chunk
+        kname = "k_rec_local" if w.hidden == 64 else "k_rec_persist"
     if os.path.exists(args.traffic):
         try:
             ent = json.load(open(args.traffic)).get(w.name, {}).get(kname)

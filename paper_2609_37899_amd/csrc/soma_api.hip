@@ -643,6 +643,34 @@ void launch_proj_stream(const soma::FwdArgs& a, int nslots, hipStream_t st) {
     launch_proj_stream_t<true>(a, nslots, st);
 }
 
+// H = 64 (and the persistent path's other conditions: B <= 64, one slot's
+// gate inputs under 2^31 bytes): the recurrence runs one block per job with
+// h kept in LDS between steps (k_rec_local).
+bool local_recurrence(const soma_config& c) {
+  if (c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) return false;
+  const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
+  return c.arch == SOMA_ARCH_LSTM && c.hidden == 64 && c.batch <= 64 && gin_slot_bytes < (int64_t(1) << 31);
+}
+
+template <bool kRad>
+void launch_local_t(const soma::FwdArgs& a, int jobs, int B, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(jobs)), block(soma::kLocalThreads);
+  if (B <= 16)
+    hipLaunchKernelGGL((soma::k_rec_local<1, kRad>), grid, block, 0, st, a, jobs);
+  else if (B <= 32)
+    hipLaunchKernelGGL((soma::k_rec_local<2, kRad>), grid, block, 0, st, a, jobs);
+  else
+    hipLaunchKernelGGL((soma::k_rec_local<4, kRad>), grid, block, 0, st, a, jobs);
+}
+
+int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, hipStream_t st) {
+  if (probe == SOMA_PROBE_GAUSSIAN)
+    launch_local_t<false>(a, jobs, B, st);
+  else
+    launch_local_t<true>(a, jobs, B, st);
+  return check_launch("k_rec_local");
+}
+
 int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, hipStream_t st) {
   void* args[] = {const_cast<soma::PersistArgs*>(&p)};
   const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(soma::kPersistThreads), args, 0, st);
@@ -759,7 +787,12 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       ++ctx->proj_launches;
     }
     const int groups = kPert ? persistent_groups(ctx, 2 * N * pcs) : 0;
-    if (groups > 0) {
+    if (kPert && local_recurrence(c)) {
+      // H = 64: one block per job, h kept in the block between steps.
+      const int jobs = 2 * N * pcs;   // (expert, direction, sign)
+      if (int rc = launch_local(a, jobs, c.batch, c.probe, st)) return rc;
+      ctx->rec_launches += 1;
+    } else if (groups > 0) {
       soma::PersistArgs p{};
       p.a = a;
       p.bar = reinterpret_cast<unsigned*>(ctx->ws + L.sync);

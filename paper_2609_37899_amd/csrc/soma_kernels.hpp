@@ -1025,6 +1025,172 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 }
 
 // ---------------------------------------------------------------------------
+// Recurrence of one layer for H = 64 (perturbed step only), one block per
+// (expert, direction, sign) job.  All 4H = 256 gate rows of a job fit one
+// block's registers (each of the 8 waves keeps 32 rows, two MFMA row tiles,
+// as split fragments: 32 VGPRs at K = 64), so h never leaves the block
+// between steps: the cell updates of step t write h_t, split into fp16
+// parts, into one of two LDS buffers while the products of step t read
+// h_{t-1} from the other, and one block barrier separates the steps -- no
+// group counter, no cross-CU exchange, no cooperative launch; several jobs
+// share a compute unit.  h_t is also stored to the slot's hseq rows for the
+// next layer and the head.  Lane (wave, lr, lg) owns units 8 wave + 4 m + lg
+// (m < 2) of batch rows 16 nb + lr; rows past the batch compute on whatever
+// follows in the input buffers and are never stored.  Probes and weights
+// are those of k_rec_persist (same canonical indices, same order of
+// operations), the products the same three split passes.
+// ---------------------------------------------------------------------------
+constexpr int kLocalThreads = 512;
+
+template <int NB, bool kRad>
+__global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs) {
+  constexpr int H = 64, G = 4 * H;                      // gate rows of a job
+  constexpr int KC = H / 32;                            // 32-wide k chunks
+  constexpr int MT = G / (16 * 8);                      // row tiles per wave
+  constexpr int ROWS = NB * 16;
+  constexpr int HSW = H + 16;                           // LDS row of staged h in halves (160 B: an odd multiple of 32)
+  constexpr int kZw = H + 8;                            // probe scratch row in floats (288 B)
+  constexpr int PART = ROWS * HSW;                      // halves per fp16 part of one buffer
+  constexpr int ST_BYTES = 2 * 2 * PART * 2;            // [buffer][hi, lo][ROWS][HSW] halves
+  constexpr int ZS_BYTES = 128 * kZw * 4;
+  constexpr int LDS_BYTES = ST_BYTES > ZS_BYTES ? ST_BYTES : ZS_BYTES;
+  static_assert(MT == 2 && KC == 2, "H = 64");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  _Float16* hs = reinterpret_cast<_Float16*>(lds);      // buffer b, part q at hs + (2 b + q) PART
+  float* zs = reinterpret_cast<float*>(lds);
+  const int job = blockIdx.x;
+  if (job >= jobs) return;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int B = a.B, T = a.T, in = a.in_l;
+  const int64_t R = static_cast<int64_t>(T - 1) * B;
+  const int sg = job & 1, pj = job >> 1;
+  const int e = pj / a.pcs, jl = pj % a.pcs;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = stream_key(a.seeds[e], a.step);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+  const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(R * H * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t gbuf =
+      a.layer == 0 ? buffer_of(a.U + slot * kVocab * G, static_cast<uint32_t>(kVocab * G * sizeof(float)))
+                   : buffer_of(a.gin + slot * R * G, static_cast<uint32_t>(R * G * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t bbuf = buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
+
+  // Weights: rows 32 wave + 16 m + lr (gate-interleaved order, row 4u + g
+  // is gate g of unit u, canonical row g H + u), the recurrent columns.
+  uint4 wh[MT][KC], wl[MT][KC];
+  auto canon = [&](int r) { return (r & 3) * H + (r >> 2); };
+#pragma unroll
+  for (int rg = 0; rg < G / 128; ++rg) {
+    __syncthreads();
+    for (int q = threadIdx.x; q < 128 * (H / 4); q += kLocalThreads) {
+      const int m = q / (H / 4), k4 = q % (H / 4);
+      const uint64_t kk =
+          static_cast<uint64_t>(a.off_l + static_cast<int64_t>(canon(128 * rg + m)) * (in + H) + in + 4 * k4);
+      *reinterpret_cast<float4*>(&zs[m * kZw + 4 * k4]) =
+          kRad ? rademacher_quad(key, pair, step_lo, kk, a.probe == kProbeRademacher)
+               : gauss_quad(key, pair, step_lo, kk >> 2);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const int row0 = 32 * wave + 16 * m;              // wave-uniform
+      if (row0 / 128 != rg) continue;
+      const int row = row0 + lr;
+      const int64_t wrow = a.off_l + static_cast<int64_t>(canon(row)) * (in + H) + in;
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const float* zr = &zs[(row - 128 * rg) * kZw + 32 * c + 8 * lg];
+        const float* tr = th + wrow + 32 * c + 8 * lg;
+        const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
+        const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+        split8v(w0, w1, wh[m][c], wl[m][c]);
+      }
+    }
+  }
+  __syncthreads();                                      // the scratch becomes the h buffers
+
+  float cs[MT][NB];
+  int vnext[NB];
+  const uint32_t byte_lane = static_cast<uint32_t>(lr * T);
+  const int unit0 = 8 * wave + lg;                      // unit of row tile 0; row tile m: unit0 + 4 m
+  const uint32_t gi_lane = static_cast<uint32_t>((lr * G + 4 * unit0) * 4);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) cs[m][nb] = 0.0f;
+    vnext[nb] = a.layer == 0
+                    ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T), 0)
+                    : 0;
+  }
+  float4 gi[MT][NB];
+  auto load_inputs = [&](int tt) {
+    if (a.layer == 0) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+          gi[m][nb] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vnext[nb] * G + 4 * (unit0 + 4 * m)) * 4));
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        vnext[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T + tt + 1), 0);
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+          gi[m][nb] = buffer_load_f4s<0>(gbuf, gi_lane + 64 * m, static_cast<uint32_t>((tt * B + nb * 16) * G * 4));
+    }
+  };
+  load_inputs(0);
+
+  for (int t = 0; t + 1 < T; ++t) {
+    f32x4 acc[MT][NB];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[m][nb] = f32x4{gi[m][nb].x, gi[m][nb].y, gi[m][nb].z, gi[m][nb].w};
+    if (t + 2 < T) load_inputs(t + 1);                  // overlaps this step (h_{-1} = 0 at t = 0)
+    if (t > 0) {
+      const _Float16* bhi = hs + (2 * ((t - 1) & 1)) * PART + lr * HSW + 8 * lg;
+      const _Float16* blo = bhi + PART;
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        uint4 bh[NB], bl[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * HSW + 32 * kc);
+          bl[nb] = *reinterpret_cast<const uint4*>(blo + nb * 16 * HSW + 32 * kc);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) mfma3_batch<NB>(wh[m][kc], wl[m][kc], bh, bl, acc[m]);
+      }
+    }
+    // Cell updates; h_t into buffer t & 1 (split) and to the slot's rows.
+    _Float16* dhi = hs + (2 * (t & 1)) * PART;
+    _Float16* dlo = dhi + PART;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const float ai = acc[m][nb][0], af = acc[m][nb][1], ag = acc[m][nb][2], ao = acc[m][nb][3];
+        const float c = sigmoid_f(af) * cs[m][nb] + sigmoid_f(ai) * tanh_f(ag);
+        cs[m][nb] = c;
+        const float h = sigmoid_f(ao) * tanh_f(c);
+        const int n = nb * 16 + lr, u = unit0 + 4 * m;
+        const _Float16 hh = static_cast<_Float16>(__builtin_amdgcn_cvt_pkrtz(h, 0.0f)[0]);
+        dhi[n * HSW + u] = hh;
+        dlo[n * HSW + u] = static_cast<_Float16>(__builtin_amdgcn_cvt_pkrtz(h - static_cast<float>(hh), 0.0f)[0]);
+        if (n < B)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), hbuf,
+                                                static_cast<uint32_t>(((t * B + n) * H + u) * 4), 0, 0);
+      }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Input projection of layer l >= 2 with register-resident weights:
 //   gin[slot][row][4u+g] = sum_{k<H} W_l+-[g H + u][k] h_{l-1}[slot][row][k]
 // A block owns one job, the 128 gate rows [128 mb, +128) of one (expert,

@@ -18,6 +18,8 @@ CASES = {
     "h512_b50": (1, 2, 64, 512, 50, 7, 2, 1e-3, 1e-3, 0, 0),   # four row tiles, rows 50..63 past the batch
     "t2_b1_p1": (1, 2, 32, 64, 1, 2, 1, 1e-3, 1e-2, 0, 0),    # one target per sequence: a single recurrence step
     "h16_fallback": (2, 2, 16, 16, 5, 11, 2, 1e-3, 1e-2, 0, 0),  # H % 64 != 0: per-step and tiled kernels
+    "h64_b50_l2": (2, 2, 32, 64, 50, 9, 3, 1e-3, 1e-2, 0, 2),   # one block per job, four row tiles, ragged
+    "h64_b20": (1, 1, 48, 64, 20, 13, 2, 1e-3, 1e-2, 0, 0),      # one block per job, two row tiles
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
 }
@@ -138,7 +140,7 @@ def test_chunking_does_not_change_the_result():
 
 
 @pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("h512_b50", 0), ("b64_h128", 0),
-                                        ("b40_h384", 0), ("b64_h128", 1)])
+                                        ("b40_h384", 0), ("b64_h128", 1), ("h64_b50_l2", 1), ("h64_b20", 0)])
 def test_persistent_and_per_step_recurrence_agree(name, probe):
     """The persistent recurrence (weights resident in registers, group
     barriers, products on the fp16 matrix cores from split operands) against
