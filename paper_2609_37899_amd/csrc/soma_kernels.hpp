@@ -763,12 +763,15 @@ __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, con
 // The same rows as split fragments for the fp16 products: lane (wave, lr, lg)
 // keeps row r0 + 16 wave + lr, columns col0 + 32 c + 8 lg .. + 7 as (wh[c],
 // wl[c]), KC = K / 32 chunks; w = theta + seps z is formed in fp32 and then
-// split.  The probes are drawn as in resident_weights.
-template <int KC, bool kGateRows, bool kRad>
+// split.  The probes are drawn as in resident_weights, ZW columns at a time
+// into the LDS scratch zs (128 x (ZW + 8) floats).
+template <int KC, bool kGateRows, bool kRad, int ZW = kZpiece>
 __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&wl)[KC], float* zs, const float* th,
                                                        int64_t off_l, int ld, int col0, int H, int r0, int law,
                                                        uint2 key, uint32_t pair, uint32_t step_lo, float seps) {
-  constexpr int kPiece = kZpiece / 32;   // chunks per probe piece
+  static_assert(ZW % 32 == 0 && ZW <= kZpiece, "probe pieces of whole chunks");
+  constexpr int kPiece = ZW / 32;        // chunks per probe piece
+  constexpr int ZLD = ZW + 8;            // scratch row in floats (an odd multiple of 32 bytes)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   auto canon = [&](int r) { return kGateRows ? (r & 3) * H + (r >> 2) : r; };
   const int prow = r0 + wave * 16 + lr;
@@ -782,7 +785,7 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
       const int m = q / (nc * 8), k4 = q % (nc * 8);
       const int pr = r0 + m;
       const uint64_t kk = static_cast<uint64_t>(off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 32 * kc0 + 4 * k4);
-      *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) =
+      *reinterpret_cast<float4*>(&zs[m * ZLD + 4 * k4]) =
           kRad ? rademacher_quad(key, pair, step_lo, kk, law == kProbeRademacher) : gauss_quad(key, pair, step_lo, kk >> 2);
     }
     __syncthreads();
@@ -790,7 +793,7 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
     for (int c2 = 0; c2 < kPiece; ++c2) {
       const int c = kc0 + c2;
       if (c < KC) {
-        const float* zr = &zs[(wave * 16 + lr) * kZld + 32 * c2 + 8 * lg];
+        const float* zr = &zs[(wave * 16 + lr) * ZLD + 32 * c2 + 8 * lg];
         const float* tr = th + wrow + 32 * c + 8 * lg;
         const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
         const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
@@ -1207,7 +1210,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
 constexpr int kProjThreads = 512;
 
 template <int NCH, bool kRad>
-__global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
+__global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
   constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
   constexpr int NQ = NCH % 4 == 0 ? NCH / 4 : split_quarters(NCH);   // ring chunks per row tile (256 k each where possible)
   constexpr int QC = KC / NQ;                 // k chunks per ring chunk
@@ -1216,7 +1219,9 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
   constexpr int CF4 = 64 * KW / 4;            // float4 per ring chunk
   constexpr int PT = (CF4 + kProjThreads - 1) / kProjThreads;
   constexpr int RING_BYTES = 2 * 2 * 64 * SW * 2;
-  constexpr int LDS_BYTES = RING_BYTES > 128 * kZld * 4 ? RING_BYTES : 128 * kZld * 4;
+  constexpr int ZW = KC * 32 < kZpiece ? KC * 32 : kZpiece;   // probe piece width
+  constexpr int ZS_BYTES = 128 * (ZW + 8) * 4;
+  constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
   // ring [buf][hi, lo][64][SW] halves; probe scratch while forming weights
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
   _Float16* ring = reinterpret_cast<_Float16*>(lds);
@@ -1253,7 +1258,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
       buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(static_cast<int64_t>(R) * H4 * sizeof(float)));
 
   uint4 wh[KC], wl[KC];
-  resident_weights_split<KC, true, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, a.in_l + H, 0, H,
+  resident_weights_split<KC, true, kRad, ZW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, a.in_l + H, 0, H,
                                          mb * 128, a.probe, key, pair, step_lo, seps);
 
   // Ring chunk c covers rows [64 (c / NQ), +64) and k [KW (c % NQ), +KW);
@@ -1347,8 +1352,12 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_proj_stream(FwdArgs a, int 
 // that the loss reduction reads).
 // Partials: hpart[slot][half][R] float2 (m, s); htgt[slot][R].
 // ---------------------------------------------------------------------------
+// At H <= 128 the probe scratch is sized by K and the block asks for four
+// waves per SIMD (at most 128 VGPRs), so two blocks share a compute unit and
+// cover each other's per-tile reductions and barriers.
 template <int NCH, bool kRad>
-__global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int nslots, float2* hpart, float* htgt) {
+__global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(FwdArgs a, int nslots,
+                                                                             float2* hpart, float* htgt) {
   constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
   constexpr int NQ = split_quarters(NCH);     // ring chunks per row tile
   constexpr int QC = KC / NQ;
@@ -1357,7 +1366,9 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
   constexpr int CF4 = 64 * KW / 4;
   constexpr int PT = (CF4 + kProjThreads - 1) / kProjThreads;
   constexpr int RING_BYTES = 2 * 2 * 64 * SW * 2;
-  constexpr int LDS_BYTES = RING_BYTES > 128 * kZld * 4 ? RING_BYTES : 128 * kZld * 4;
+  constexpr int ZW = KC * 32 < kZpiece ? KC * 32 : kZpiece;   // probe piece width
+  constexpr int ZS_BYTES = 128 * (ZW + 8) * 4;
+  constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];   // ring [buf][hi, lo][64][SW]
   __shared__ float2 red[2][8][64];              // per-wave (m, s) of each row, by tile parity
   _Float16* ring = reinterpret_cast<_Float16*>(lds);
@@ -1394,7 +1405,7 @@ __global__ __launch_bounds__(kProjThreads, 1) void k_head_stream(FwdArgs a, int 
   float* tg = htgt + slot * R;
 
   uint4 wh[KC], wl[KC];
-  resident_weights_split<KC, false, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_head, H, 0, H, vh * 128,
+  resident_weights_split<KC, false, kRad, ZW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_head, H, 0, H, vh * 128,
                                           a.probe, key, pair, step_lo, seps);
 
   const int nchunks = ((R + 63) / 64) * NQ;
