@@ -652,22 +652,43 @@ bool local_recurrence(const soma_config& c) {
   return c.arch == SOMA_ARCH_LSTM && c.hidden == 64 && c.batch <= 64 && gin_slot_bytes < (int64_t(1) << 31);
 }
 
-template <bool kRad>
+// Layer 1 of the local recurrence forms its gate inputs in the block from
+// LDS copies of the perturbed embedding table (E = 32 or 64) and of the
+// job's bytes (B T <= kLocalBytes): no fold.
+bool local_embedding(const soma_config& c) {
+  return local_recurrence(c) && (c.embed == 32 || c.embed == 64) &&
+         int64_t(c.batch) * c.seq_len <= soma::kLocalBytes;
+}
+
+template <bool kRad, int KX>
 void launch_local_t(const soma::FwdArgs& a, int jobs, int B, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(jobs)), block(soma::kLocalThreads);
   if (B <= 16)
-    hipLaunchKernelGGL((soma::k_rec_local<1, kRad>), grid, block, 0, st, a, jobs);
+    hipLaunchKernelGGL((soma::k_rec_local<1, kRad, KX>), grid, block, 0, st, a, jobs);
   else if (B <= 32)
-    hipLaunchKernelGGL((soma::k_rec_local<2, kRad>), grid, block, 0, st, a, jobs);
+    hipLaunchKernelGGL((soma::k_rec_local<2, kRad, KX>), grid, block, 0, st, a, jobs);
   else
-    hipLaunchKernelGGL((soma::k_rec_local<4, kRad>), grid, block, 0, st, a, jobs);
+    hipLaunchKernelGGL((soma::k_rec_local<4, kRad, KX>), grid, block, 0, st, a, jobs);
 }
 
-int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, hipStream_t st) {
-  if (probe == SOMA_PROBE_GAUSSIAN)
-    launch_local_t<false>(a, jobs, B, st);
+// kx: 32-wide chunks of the embedding formed in the block (0: gate inputs
+// read from U or gin).
+template <bool kRad>
+void launch_local_k(const soma::FwdArgs& a, int jobs, int B, int kx, hipStream_t st) {
+  if (kx == 0)
+    launch_local_t<kRad, 0>(a, jobs, B, st);
+  else if (kx == 1)
+    launch_local_t<kRad, 1>(a, jobs, B, st);
   else
-    launch_local_t<true>(a, jobs, B, st);
+    launch_local_t<kRad, 2>(a, jobs, B, st);
+}
+
+int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, int kx, hipStream_t st) {
+  if (kx < 0 || kx > 2) return fail(SOMA_EINVAL, "k_rec_local: embedding chunks %d", kx);
+  if (probe == SOMA_PROBE_GAUSSIAN)
+    launch_local_k<false>(a, jobs, B, kx, st);
+  else
+    launch_local_k<true>(a, jobs, B, kx, st);
   return check_launch("k_rec_local");
 }
 
@@ -763,9 +784,12 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   a.layer = 0;
   a.in_l = c.embed;
   a.off_l = L.off_layer[0];
-  hipLaunchKernelGGL((soma::k_fold<kPert>), dim3(4 * H / 64, SOMA_VOCAB / 64, N * pcs),
-                     dim3(soma::kThreads), 0, st, a);
-  if (int rc = check_launch("k_fold")) return rc;
+  const bool emb_local = kPert && local_embedding(c);
+  if (!emb_local) {
+    hipLaunchKernelGGL((soma::k_fold<kPert>), dim3(4 * H / 64, SOMA_VOCAB / 64, N * pcs),
+                       dim3(soma::kThreads), 0, st, a);
+    if (int rc = check_launch("k_fold")) return rc;
+  }
   if (int rc = mark(ctx, kPhaseFold, st)) return rc;
   const int rb = rec_row_block(c.batch);
   const int bgroups = (c.batch + rb - 1) / rb;
@@ -790,7 +814,8 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     if (kPert && local_recurrence(c)) {
       // H = 64: one block per job, h kept in the block between steps.
       const int jobs = 2 * N * pcs;   // (expert, direction, sign)
-      if (int rc = launch_local(a, jobs, c.batch, c.probe, st)) return rc;
+      const int kx = l == 0 && emb_local ? c.embed / 32 : 0;
+      if (int rc = launch_local(a, jobs, c.batch, c.probe, kx, st)) return rc;
       ctx->rec_launches += 1;
     } else if (groups > 0) {
       soma::PersistArgs p{};

@@ -1042,24 +1042,43 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 // follows in the input buffers and are never stored.  Probes and weights
 // are those of k_rec_persist (same canonical indices, same order of
 // operations), the products the same three split passes.
+//
+// Gate inputs.  KX = 0: read per step, from the slot's gin rows (layers
+// >= 2) or gathered from the folded table U by byte value (layer 1).
+// KX = E / 32 > 0 (layer 1 only, E = 32 or 64, B T <= kLocalBytes): the
+// block forms them itself.  It keeps the input columns of W_1+- as split
+// fragments beside the recurrent ones, and in LDS the whole perturbed
+// embedding table Emb+- (256 x E, split into fp16 parts: E KiB) and the
+// job's B x T bytes, and adds x_t W_1x+-^T with KX more chunks of the same
+// three passes, x_t being the table row of byte b_t: the fold's 256-row
+// table per slot and its per-step row gathers from HBM are never formed,
+// and the loop issues no vector-memory load (a wait for one would also wait
+// for the h stores before it: loads and stores share one counter).
 // ---------------------------------------------------------------------------
 constexpr int kLocalThreads = 512;
+constexpr int kLocalBytes = 16384;                      // largest B T kept in LDS (KX > 0)
 
-template <int NB, bool kRad>
+template <int NB, bool kRad, int KX>
 __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs) {
   constexpr int H = 64, G = 4 * H;                      // gate rows of a job
   constexpr int KC = H / 32;                            // 32-wide k chunks
   constexpr int MT = G / (16 * 8);                      // row tiles per wave
   constexpr int ROWS = NB * 16;
+  constexpr int EW = 32 * KX;                           // embedding width held in LDS (KX > 0)
   constexpr int HSW = H + 16;                           // LDS row of staged h in halves (160 B: an odd multiple of 32)
   constexpr int kZw = H + 8;                            // probe scratch row in floats (288 B)
   constexpr int PART = ROWS * HSW;                      // halves per fp16 part of one buffer
-  constexpr int ST_BYTES = 2 * 2 * PART * 2;            // [buffer][hi, lo][ROWS][HSW] halves
+  constexpr int EMB_BYTES = 2 * kVocab * EW * 2;        // [hi, lo][256][EW] halves
+  constexpr int BT_BYTES = KX > 0 ? kLocalBytes : 0;    // the job's bytes [B][T]
+  constexpr int ST_BYTES = EMB_BYTES + BT_BYTES + 2 * 2 * PART * 2;  // + [buffer][hi, lo][ROWS][HSW] halves
   constexpr int ZS_BYTES = 128 * kZw * 4;
   constexpr int LDS_BYTES = ST_BYTES > ZS_BYTES ? ST_BYTES : ZS_BYTES;
   static_assert(MT == 2 && KC == 2, "H = 64");
+  static_assert(KX >= 0 && KX <= 2 && EW <= kZw, "E = 32 or 64");
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
-  _Float16* hs = reinterpret_cast<_Float16*>(lds);      // buffer b, part q at hs + (2 b + q) PART
+  _Float16* et = reinterpret_cast<_Float16*>(lds);     // Emb+- parts: hi at et, lo at et + 256 EW
+  unsigned char* bts = lds + EMB_BYTES;                 // bytes of row n, step t at bts[n T + t]
+  _Float16* hs = reinterpret_cast<_Float16*>(lds + EMB_BYTES + BT_BYTES);   // buffer b, part q at hs + (2 b + q) PART
   float* zs = reinterpret_cast<float*>(lds);
   const int job = blockIdx.x;
   if (job >= jobs) return;
@@ -1075,103 +1094,113 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
   const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
   const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
   const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(R * H * sizeof(float)));
-  const __amdgpu_buffer_rsrc_t gbuf =
-      a.layer == 0 ? buffer_of(a.U + slot * kVocab * G, static_cast<uint32_t>(kVocab * G * sizeof(float)))
-                   : buffer_of(a.gin + slot * R * G, static_cast<uint32_t>(R * G * sizeof(float)));
   const __amdgpu_buffer_rsrc_t bbuf = buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
+  auto probe4 = [&](uint64_t kk) {
+    return kRad ? rademacher_quad(key, pair, step_lo, kk, a.probe == kProbeRademacher)
+                : gauss_quad(key, pair, step_lo, kk >> 2);
+  };
 
   // Weights: rows 32 wave + 16 m + lr (gate-interleaved order, row 4u + g
-  // is gate g of unit u, canonical row g H + u), the recurrent columns.
+  // is gate g of unit u, canonical row g H + u); the recurrent columns
+  // [in, in + H) into wh/wl, with KX > 0 also the input columns [0, E) into
+  // xh/xl.  The probes of 128 rows of one column segment are drawn into the
+  // LDS scratch at a time.
   uint4 wh[MT][KC], wl[MT][KC];
+  uint4 xh[MT][KX > 0 ? KX : 1], xl[MT][KX > 0 ? KX : 1];
   auto canon = [&](int r) { return (r & 3) * H + (r >> 2); };
 #pragma unroll
   for (int rg = 0; rg < G / 128; ++rg) {
-    __syncthreads();
-    for (int q = threadIdx.x; q < 128 * (H / 4); q += kLocalThreads) {
-      const int m = q / (H / 4), k4 = q % (H / 4);
-      const uint64_t kk =
-          static_cast<uint64_t>(a.off_l + static_cast<int64_t>(canon(128 * rg + m)) * (in + H) + in + 4 * k4);
-      *reinterpret_cast<float4*>(&zs[m * kZw + 4 * k4]) =
-          kRad ? rademacher_quad(key, pair, step_lo, kk, a.probe == kProbeRademacher)
-               : gauss_quad(key, pair, step_lo, kk >> 2);
-    }
-    __syncthreads();
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const int row0 = 32 * wave + 16 * m;              // wave-uniform
-      if (row0 / 128 != rg) continue;
-      const int row = row0 + lr;
-      const int64_t wrow = a.off_l + static_cast<int64_t>(canon(row)) * (in + H) + in;
+    for (int seg = 0; seg < (KX > 0 ? 2 : 1); ++seg) {
+      const int c0 = seg == 0 ? in : 0;                 // first column of the segment
+      const int W4 = seg == 0 ? H / 4 : EW / 4;         // its width in quads
+      __syncthreads();
+      for (int q = threadIdx.x; q < 128 * W4; q += kLocalThreads) {
+        const int m = q / W4, k4 = q % W4;
+        const uint64_t kk = static_cast<uint64_t>(a.off_l + static_cast<int64_t>(canon(128 * rg + m)) * (in + H) +
+                                                  c0 + 4 * k4);
+        *reinterpret_cast<float4*>(&zs[m * kZw + 4 * k4]) = probe4(kk);
+      }
+      __syncthreads();
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        const float* zr = &zs[(row - 128 * rg) * kZw + 32 * c + 8 * lg];
-        const float* tr = th + wrow + 32 * c + 8 * lg;
-        const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
-        const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
-        split8v(w0, w1, wh[m][c], wl[m][c]);
+      for (int m = 0; m < MT; ++m) {
+        const int row0 = 32 * wave + 16 * m;            // wave-uniform
+        if (row0 / 128 != rg) continue;
+        const int row = row0 + lr;
+        const int64_t wrow = a.off_l + static_cast<int64_t>(canon(row)) * (in + H) + c0;
+#pragma unroll
+        for (int c = 0; c < (seg == 0 ? KC : KX); ++c) {
+          const float* zr = &zs[(row - 128 * rg) * kZw + 32 * c + 8 * lg];
+          const float* tr = th + wrow + 32 * c + 8 * lg;
+          const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
+          const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+          if (seg == 0)
+            split8v(w0, w1, wh[m][c], wl[m][c]);
+          else
+            split8v(w0, w1, xh[m][c], xl[m][c]);
+        }
       }
     }
   }
-  __syncthreads();                                      // the scratch becomes the h buffers
+  __syncthreads();                                      // the scratch becomes the embedding table and the h buffers
+
+  if constexpr (KX > 0) {
+    // Emb+-[v][k] = theta[v E + k] +- eps z (canonical offset 0), split.
+    for (int q = threadIdx.x; q < kVocab * EW / 4; q += kLocalThreads) {
+      const int kk = 4 * q;                             // = v EW + 4 k4
+      const float4 w = fma4(seps, probe4(static_cast<uint64_t>(kk)), *reinterpret_cast<const float4*>(th + kk));
+      uint2 hi, lo;
+      split4(w, hi, lo);
+      *reinterpret_cast<uint2*>(&et[kk]) = hi;
+      *reinterpret_cast<uint2*>(&et[kVocab * EW + kk]) = lo;
+    }
+    // The job's bytes (B T <= kLocalBytes, checked by the host), eight
+    // loads in flight per thread (past the end they read 0 and are dropped).
+    for (int q0 = 0; q0 < B * T; q0 += 8 * kLocalThreads) {
+      int v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        v[i] = __builtin_amdgcn_raw_buffer_load_b8(
+            bbuf, static_cast<uint32_t>(q0 + i * kLocalThreads + threadIdx.x), 0, 0);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int q = q0 + i * kLocalThreads + threadIdx.x;
+        if (q < B * T) bts[q] = static_cast<unsigned char>(v[i]);
+      }
+    }
+    __syncthreads();
+  }
 
   float cs[MT][NB];
-  int vnext[NB];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) cs[m][nb] = 0.0f;
   const uint32_t byte_lane = static_cast<uint32_t>(lr * T);
   const int unit0 = 8 * wave + lg;                      // unit of row tile 0; row tile m: unit0 + 4 m
-  const uint32_t gi_lane = static_cast<uint32_t>((lr * G + 4 * unit0) * 4);
+  auto load_byte = [&](int nb, int tt) {
+    return static_cast<int>(
+        __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T + tt), 0));
+  };
+  // acc += h_{t-1} W_h+-^T, h_{t-1} read from buffer b.
+  auto h_products = [&](f32x4 (&acc)[MT][NB], int b) {
+    const _Float16* bhi = hs + (2 * b) * PART + lr * HSW + 8 * lg;
+    const _Float16* blo = bhi + PART;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
+    for (int kc = 0; kc < KC; ++kc) {
+      uint4 bh[NB], bl[NB];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) cs[m][nb] = 0.0f;
-    vnext[nb] = a.layer == 0
-                    ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T), 0)
-                    : 0;
-  }
-  float4 gi[MT][NB];
-  auto load_inputs = [&](int tt) {
-    if (a.layer == 0) {
+      for (int nb = 0; nb < NB; ++nb) {
+        bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * HSW + 32 * kc);
+        bl[nb] = *reinterpret_cast<const uint4*>(blo + nb * 16 * HSW + 32 * kc);
+      }
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int m = 0; m < MT; ++m)
-          gi[m][nb] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vnext[nb] * G + 4 * (unit0 + 4 * m)) * 4));
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        vnext[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T + tt + 1), 0);
-    } else {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int m = 0; m < MT; ++m)
-          gi[m][nb] = buffer_load_f4s<0>(gbuf, gi_lane + 64 * m, static_cast<uint32_t>((tt * B + nb * 16) * G * 4));
+      for (int m = 0; m < MT; ++m) mfma3_batch<NB>(wh[m][kc], wl[m][kc], bh, bl, acc[m]);
     }
   };
-  load_inputs(0);
-
-  for (int t = 0; t + 1 < T; ++t) {
-    f32x4 acc[MT][NB];
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[m][nb] = f32x4{gi[m][nb].x, gi[m][nb].y, gi[m][nb].z, gi[m][nb].w};
-    if (t + 2 < T) load_inputs(t + 1);                  // overlaps this step (h_{-1} = 0 at t = 0)
-    if (t > 0) {
-      const _Float16* bhi = hs + (2 * ((t - 1) & 1)) * PART + lr * HSW + 8 * lg;
-      const _Float16* blo = bhi + PART;
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        uint4 bh[NB], bl[NB];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * HSW + 32 * kc);
-          bl[nb] = *reinterpret_cast<const uint4*>(blo + nb * 16 * HSW + 32 * kc);
-        }
-#pragma unroll
-        for (int m = 0; m < MT; ++m) mfma3_batch<NB>(wh[m][kc], wl[m][kc], bh, bl, acc[m]);
-      }
-    }
-    // Cell updates; h_t into buffer t & 1 (split) and to the slot's rows.
-    _Float16* dhi = hs + (2 * (t & 1)) * PART;
+  // Cell updates of step t; h_t into buffer b (split) and to the slot's rows.
+  auto cells = [&](const f32x4 (&acc)[MT][NB], int t, int b) {
+    _Float16* dhi = hs + (2 * b) * PART;
     _Float16* dlo = dhi + PART;
 #pragma unroll
     for (int m = 0; m < MT; ++m)
@@ -1189,7 +1218,110 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
           __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), hbuf,
                                                 static_cast<uint32_t>(((t * B + n) * H + u) * 4), 0, 0);
       }
-    __syncthreads();
+  };
+
+  if constexpr (KX == 0) {
+    const __amdgpu_buffer_rsrc_t gbuf =
+        a.layer == 0 ? buffer_of(a.U + slot * kVocab * G, static_cast<uint32_t>(kVocab * G * sizeof(float)))
+                     : buffer_of(a.gin + slot * R * G, static_cast<uint32_t>(R * G * sizeof(float)));
+    // The gate inputs of step t + 2 are requested at step t, into the ring
+    // slot (t & 1) that step t's own inputs just left (a step here is well
+    // under the latency of those loads).  Layer 1 gathers them by byte
+    // value: the byte of step t + 2 was requested at step t - 2, right after
+    // that step's gate inputs, so waiting for it waits for nothing the step
+    // does not need anyway (one wave's loads complete in order).
+    int vb[2][NB];                                      // bytes of steps t + 2 (slot t & 1)
+    float4 gi[2][MT][NB];                               // gate inputs of steps t, t + 1 (slot t & 1)
+    const uint32_t gi_lane = static_cast<uint32_t>((lr * G + 4 * unit0) * 4);
+    auto load_inputs = [&](float4 (&g)[MT][NB], const int (&v)[NB], int tt) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+          g[m][nb] = a.layer == 0
+                         ? buffer_load_f4<0>(gbuf, static_cast<uint32_t>((v[nb] * G + 4 * (unit0 + 4 * m)) * 4))
+                         : buffer_load_f4s<0>(gbuf, gi_lane + 64 * m,
+                                              static_cast<uint32_t>((tt * B + nb * 16) * G * 4));
+    };
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      vb[0][nb] = a.layer == 0 ? load_byte(nb, 0) : 0;
+      vb[1][nb] = a.layer == 0 && T > 2 ? load_byte(nb, 1) : 0;
+    }
+    load_inputs(gi[0], vb[0], 0);
+    if (T > 2) load_inputs(gi[1], vb[1], 1);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      vb[0][nb] = a.layer == 0 && T > 3 ? load_byte(nb, 2) : 0;
+      vb[1][nb] = a.layer == 0 && T > 4 ? load_byte(nb, 3) : 0;
+    }
+    // One step; P = t & 1 selects the ring slots at compile time.
+    auto step = [&](int t, auto Pc) {
+      constexpr int P = decltype(Pc)::value;
+      f32x4 acc[MT][NB];
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[m][nb] = f32x4{gi[P][m][nb].x, gi[P][m][nb].y, gi[P][m][nb].z, gi[P][m][nb].w};
+      if (t + 3 < T) {
+        load_inputs(gi[P], vb[P], t + 2);
+        if (a.layer == 0 && t + 5 < T) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) vb[P][nb] = load_byte(nb, t + 4);
+        }
+      }
+      if (t > 0) h_products(acc, P ^ 1);                // h_{t-1}: buffer (t - 1) & 1
+      cells(acc, t, P);
+      __syncthreads();
+    };
+    for (int t = 0; t + 1 < T; t += 2) {
+      step(t, std::integral_constant<int, 0>{});
+      if (t + 2 < T) step(t + 1, std::integral_constant<int, 1>{});
+    }
+  } else {
+    // acc = x_t W_1x+-^T for the byte v of each of the lane's rows: B
+    // operand rows of the embedding table.
+    auto x_products = [&](f32x4 (&acc)[MT][NB], const int (&v)[NB]) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[m][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kx = 0; kx < KX; ++kx) {
+        uint4 bh[NB], bl[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const _Float16* er = et + v[nb] * EW + 32 * kx + 8 * lg;
+          bh[nb] = *reinterpret_cast<const uint4*>(er);
+          bl[nb] = *reinterpret_cast<const uint4*>(er + kVocab * EW);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) mfma3_batch<NB>(xh[m][kx], xl[m][kx], bh, bl, acc[m]);
+      }
+    };
+    // The input product of step t + 1 is formed at the end of step t, off
+    // the path through the barrier.  Rows past the batch take byte 0.
+    auto bytes_at = [&](int (&v)[NB], int tt) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int n = nb * 16 + lr;
+        v[nb] = n < B ? bts[n * T + tt] : 0;
+      }
+    };
+    int vb[NB];
+    f32x4 acc[MT][NB];
+    bytes_at(vb, 0);
+    x_products(acc, vb);
+    for (int t = 0; t + 1 < T; ++t) {
+      if (t > 0) h_products(acc, (t & 1) ^ 1);          // h_{t-1}: buffer (t - 1) & 1
+      cells(acc, t, t & 1);
+      if (t + 2 < T) {                                  // step t + 1 exists
+        bytes_at(vb, t + 1);
+        x_products(acc, vb);
+      }
+      __syncthreads();
+    }
   }
 }
 

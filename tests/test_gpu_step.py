@@ -20,6 +20,7 @@ CASES = {
     "h16_fallback": (2, 2, 16, 16, 5, 11, 2, 1e-3, 1e-2, 0, 0),  # H % 64 != 0: per-step and tiled kernels
     "h64_b50_l2": (2, 2, 32, 64, 50, 9, 3, 1e-3, 1e-2, 0, 2),   # one block per job, four row tiles, ragged
     "h64_b20": (1, 1, 48, 64, 20, 13, 2, 1e-3, 1e-2, 0, 0),      # one block per job, two row tiles
+    "h64_e64_b33": (1, 2, 64, 64, 33, 10, 2, 1e-3, 1e-2, 0, 0),  # one block per job, embedding in LDS (two chunks)
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
 }
@@ -65,7 +66,7 @@ def test_step_matches_oracle(oracle_mod, name):
 
 
 @pytest.mark.parametrize("probe", [1, 2])
-@pytest.mark.parametrize("name", ["tiny", "ragged_l2_summed", "l3_b70", "b64_h128", "b40_h384"])
+@pytest.mark.parametrize("name", ["tiny", "ragged_l2_summed", "l3_b70", "h64_e64_b33", "b64_h128", "b40_h384"])
 def test_rademacher_step_matches_oracle(oracle_mod, name, probe):
     """Whole steps under the paper's sparse Rademacher law (1) and the dense
     law (2): the tiled kernels (H = 32, 80), the persistent recurrence and the
@@ -140,7 +141,8 @@ def test_chunking_does_not_change_the_result():
 
 
 @pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("h512_b50", 0), ("b64_h128", 0),
-                                        ("b40_h384", 0), ("b64_h128", 1), ("h64_b50_l2", 1), ("h64_b20", 0)])
+                                        ("b40_h384", 0), ("b64_h128", 1), ("h64_b50_l2", 1), ("h64_b20", 0),
+                                        ("h64_e64_b33", 2)])
 def test_persistent_and_per_step_recurrence_agree(name, probe):
     """The persistent recurrence (weights resident in registers, group
     barriers, products on the fp16 matrix cores from split operands) against
