@@ -216,6 +216,13 @@ def main():
 
     # Dominant kernel and its roofline.
     fl = kernel_flops(w)
+    # At H = 64 with E = 32 or 64 and B T <= 16 KiB the recurrence block
+    # forms layer 1's input product itself (no fold launch).
+    local_rec = (w.arch == 0 and w.hidden == 64 and w.batch <= 64
+                 and (w.seq_len - 1) * w.batch * 4 * w.hidden * 4 < 2 ** 31)
+    if local_rec and w.embed in (32, 64) and w.batch * w.seq_len <= 16384:
+        fl["rec"] += fl["fold"]
+        fl["fold"] = 0
     K = args.steps
     ms = {"rec": phases["rec_ms"] / K, "proj": phases["proj_ms"] / K, "fold": phases["fold_ms"] / K,
           "head": phases["head_ms"] / K, "reduce": phases["reduce_ms"] / K,
@@ -239,7 +246,7 @@ def main():
     if w.arch == 1:
         kname = "k_body"          # the whole perturbed forward, one launch per direction chunk
     elif dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
-        kname = "k_rec_local" if w.hidden == 64 else "k_rec_persist"
+        kname = "k_rec_local" if local_rec else "k_rec_persist"
     if os.path.exists(args.traffic):
         try:
             ent = json.load(open(args.traffic)).get(w.name, {}).get(kname)

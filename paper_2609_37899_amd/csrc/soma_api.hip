@@ -551,6 +551,11 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
   if (gin_slot_bytes >= (int64_t(1) << 31)) return 0;
   const int ut = c.hidden / soma::kRecUnits;
   int groups = std::min(ctx->coop_blocks / ut, jobs);
+  // Group g owns blocks g + k groups and blocks are dealt to the 8 XCDs
+  // round-robin, so with a multiple of 8 groups every group sits on one XCD
+  // and exchanges h through its L2; other counts spread each group over
+  // every XCD (about twice the time per step), so round down.
+  if (groups > 8) groups -= groups % 8;
   groups = std::min(groups, kMaxGroups);
   return groups >= 1 ? groups : 0;
 }

@@ -52,7 +52,6 @@ namespace soma {
 constexpr int kBodyThreads = 256;   // 4 waves x 16 sequences
 constexpr int kBodySeqs = 64;       // sequences per block
 constexpr float kLnEps = 1e-5f;     // LayerNorm's variance offset
-constexpr float kLog2e = 1.4426950408889634f;
 
 struct BodyArgs {
   const float* theta;     // [N][d]

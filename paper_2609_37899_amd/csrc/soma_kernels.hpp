@@ -128,8 +128,50 @@ __device__ __forceinline__ float4 fma4(float a, const float4& z, const float4& t
                      __builtin_fmaf(a, z.z, t.z), __builtin_fmaf(a, z.w, t.w));
 }
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// 2^x on the transcendental unit.
+__device__ __forceinline__ float exp2_f(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ float sigmoid_f(float x) {
   return __builtin_amdgcn_rcpf(1.0f + __expf(-x));
+}
+
+// Max and sum over the four lane groups (lanes l, l ^ 16, l ^ 32, l ^ 48),
+// every lane receiving the result, on the vector ALU: with both operands
+// holding x, permlane16_swap leaves x of the lane and of lane ^ 16 in the
+// pair (odd 16-lane rows of one operand trade places with even rows of the
+// other), permlane32_swap likewise for lane ^ 32.  Both lanes of a pair add
+// the same two values in the same order, so every lane holds the same sum.
+__device__ __forceinline__ float group4_max(float v) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float group4_sum(float v) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// One LSTM cell from its gate pre-activations (i, f, g, o):
+//   c <- sigma(f) c + sigma(i) tanh(g),  h = sigma(o) tanh(c),
+// with sigma(x) = 1 / (1 + e^{-x}) and tanh(x) = sgn(x) (1 - e^{-2|x|}) /
+// (1 + e^{-2|x|}), each product of a sigmoid and a tanh over one common
+// denominator: five exponentials and three reciprocals.  No exponent is
+// positive except those of sigma, whose overflow to +inf gives 0 (a
+// denominator of +inf), never NaN.
+__device__ __forceinline__ void lstm_cell(float ai, float af, float ag, float ao, float& c, float& h) {
+  const float ef = exp2_f(-kLog2e * af), ei = exp2_f(-kLog2e * ai), eo = exp2_f(-kLog2e * ao);
+  const float eg = exp2_f(-2.0f * kLog2e * __builtin_fabsf(ag));
+  const float sf = __builtin_amdgcn_rcpf(1.0f + ef);
+  const float ig = __builtin_copysignf((1.0f - eg) * __builtin_amdgcn_rcpf((1.0f + ei) * (1.0f + eg)), ag);
+  c = __builtin_fmaf(sf, c, ig);
+  const float ec = exp2_f(-2.0f * kLog2e * __builtin_fabsf(c));
+  h = __builtin_copysignf((1.0f - ec) * __builtin_amdgcn_rcpf((1.0f + eo) * (1.0f + ec)), c);
 }
 
 __device__ __forceinline__ float tanh_f(float x) {
@@ -1037,9 +1079,10 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
 // h_{t-1} from the other, and one block barrier separates the steps -- no
 // group counter, no cross-CU exchange, no cooperative launch; several jobs
 // share a compute unit.  h_t is also stored to the slot's hseq rows for the
-// next layer and the head.  Lane (wave, lr, lg) owns units 8 wave + 4 m + lg
-// (m < 2) of batch rows 16 nb + lr; rows past the batch compute on whatever
-// follows in the input buffers and are never stored.  Probes and weights
+// next layer and the head.  Lane (wave, lr, lg) owns units 8 wave + 2 lg + m
+// (m < 2: adjacent units, stored as pairs) of batch rows 16 nb + lr; rows
+// past the batch compute on whatever follows in the input buffers and are
+// never stored.  Probes and weights
 // are those of k_rec_persist (same canonical indices, same order of
 // operations), the products the same three split passes.
 //
@@ -1100,11 +1143,13 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
                 : gauss_quad(key, pair, step_lo, kk >> 2);
   };
 
-  // Weights: rows 32 wave + 16 m + lr (gate-interleaved order, row 4u + g
-  // is gate g of unit u, canonical row g H + u); the recurrent columns
-  // [in, in + H) into wh/wl, with KX > 0 also the input columns [0, E) into
-  // xh/xl.  The probes of 128 rows of one column segment are drawn into the
-  // LDS scratch at a time.
+  // Weights: MFMA row lr of row tile m is gate lr & 3 of unit 8 wave +
+  // 2 (lr >> 2) + m, gate-interleaved row 32 wave + 8 (lr >> 2) + 4 m +
+  // (lr & 3) (row 4u + g is gate g of unit u, canonical row g H + u), so the
+  // result lane (lr, lg) holds all four gates of units 8 wave + 2 lg + m;
+  // the recurrent columns [in, in + H) into wh/wl, with KX > 0 also the
+  // input columns [0, E) into xh/xl.  The probes of 128 rows of one column
+  // segment are drawn into the LDS scratch at a time.
   uint4 wh[MT][KC], wl[MT][KC];
   uint4 xh[MT][KX > 0 ? KX : 1], xl[MT][KX > 0 ? KX : 1];
   auto canon = [&](int r) { return (r & 3) * H + (r >> 2); };
@@ -1124,9 +1169,8 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
       __syncthreads();
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
-        const int row0 = 32 * wave + 16 * m;            // wave-uniform
-        if (row0 / 128 != rg) continue;
-        const int row = row0 + lr;
+        if ((32 * wave) / 128 != rg) continue;         // wave-uniform
+        const int row = 32 * wave + 8 * (lr >> 2) + 4 * m + (lr & 3);
         const int64_t wrow = a.off_l + static_cast<int64_t>(canon(row)) * (in + H) + c0;
 #pragma unroll
         for (int c = 0; c < (seg == 0 ? KC : KX); ++c) {
@@ -1177,7 +1221,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) cs[m][nb] = 0.0f;
   const uint32_t byte_lane = static_cast<uint32_t>(lr * T);
-  const int unit0 = 8 * wave + lg;                      // unit of row tile 0; row tile m: unit0 + 4 m
+  const int unit0 = 8 * wave + 2 * lg;                  // unit of row tile 0; row tile m: unit0 + m
   auto load_byte = [&](int nb, int tt) {
     return static_cast<int>(
         __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T + tt), 0));
@@ -1198,26 +1242,29 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
       for (int m = 0; m < MT; ++m) mfma3_batch<NB>(wh[m][kc], wl[m][kc], bh, bl, acc[m]);
     }
   };
-  // Cell updates of step t; h_t into buffer b (split) and to the slot's rows.
+  // Cell updates of step t; h_t into buffer b (split) and to the slot's
+  // rows, the lane's two adjacent units as one word per fp16 part and one
+  // 8-byte store.
   auto cells = [&](const f32x4 (&acc)[MT][NB], int t, int b) {
     _Float16* dhi = hs + (2 * b) * PART;
     _Float16* dlo = dhi + PART;
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+    for (int nb = 0; nb < NB; ++nb) {
+      float h[MT];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const float ai = acc[m][nb][0], af = acc[m][nb][1], ag = acc[m][nb][2], ao = acc[m][nb][3];
-        const float c = sigmoid_f(af) * cs[m][nb] + sigmoid_f(ai) * tanh_f(ag);
-        cs[m][nb] = c;
-        const float h = sigmoid_f(ao) * tanh_f(c);
-        const int n = nb * 16 + lr, u = unit0 + 4 * m;
-        const _Float16 hh = static_cast<_Float16>(__builtin_amdgcn_cvt_pkrtz(h, 0.0f)[0]);
-        dhi[n * HSW + u] = hh;
-        dlo[n * HSW + u] = static_cast<_Float16>(__builtin_amdgcn_cvt_pkrtz(h - static_cast<float>(hh), 0.0f)[0]);
-        if (n < B)
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), hbuf,
-                                                static_cast<uint32_t>(((t * B + n) * H + u) * 4), 0, 0);
+      for (int m = 0; m < MT; ++m)
+        lstm_cell(acc[m][nb][0], acc[m][nb][1], acc[m][nb][2], acc[m][nb][3], cs[m][nb], h[m]);
+      const int n = nb * 16 + lr;
+      uint32_t hi, lo;
+      split2(h[0], h[1], hi, lo);
+      *reinterpret_cast<uint32_t*>(dhi + n * HSW + unit0) = hi;
+      *reinterpret_cast<uint32_t*>(dlo + n * HSW + unit0) = lo;
+      if (n < B) {
+        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(h[0]), __float_as_uint(h[1])}, hbuf,
+                                              static_cast<uint32_t>(((t * B + n) * H + unit0) * 4), 0, 0);
       }
+    }
   };
 
   if constexpr (KX == 0) {
@@ -1239,8 +1286,8 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
 #pragma unroll
         for (int m = 0; m < MT; ++m)
           g[m][nb] = a.layer == 0
-                         ? buffer_load_f4<0>(gbuf, static_cast<uint32_t>((v[nb] * G + 4 * (unit0 + 4 * m)) * 4))
-                         : buffer_load_f4s<0>(gbuf, gi_lane + 64 * m,
+                         ? buffer_load_f4<0>(gbuf, static_cast<uint32_t>((v[nb] * G + 4 * (unit0 + m)) * 4))
+                         : buffer_load_f4s<0>(gbuf, gi_lane + 16 * m,
                                               static_cast<uint32_t>((tt * B + nb * 16) * G * 4));
     };
 #pragma unroll
@@ -1572,6 +1619,11 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   int y[4];                                     // target bytes of this lane's rows in the current tile
+  // Row r0 + lr = ytt B + yb of the tile, advanced by 64 rows a tile; rows
+  // 16 nb further on add the wave-uniform quotient and remainder of 16 nb
+  // by B (rows past R read past the batch: 0 from the buffer, never stored).
+  int ytt = lr / B, yb = lr - (lr / B) * B;
+  const int q64 = 64 / B, r64 = 64 % B;
   gload(0);
   sstore(0);
   __syncthreads();
@@ -1581,9 +1633,19 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
     if (qq == NQ - 1) {
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
-        const int row = r0 + nb * 16 + lr < R ? r0 + nb * 16 + lr : R - 1;
-        const int tt = row / B, b = row - tt * B;
-        y[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, static_cast<uint32_t>(b * T + tt + 1), 0, 0);
+        const int qn = (16 * nb) / B, rn = 16 * nb - qn * B;   // wave-uniform
+        int bn = yb + rn, tn = ytt + qn;
+        if (bn >= B) {
+          bn -= B;
+          ++tn;
+        }
+        y[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, static_cast<uint32_t>(bn * T + tn + 1), 0, 0);
+      }
+      yb += r64;
+      ytt += q64;
+      if (yb >= B) {
+        yb -= B;
+        ++ytt;
       }
     }
 #pragma unroll
@@ -1608,13 +1670,13 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
       // 8 waves.
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
-        float m = fmaxf(fmaxf(acc[nb][0], acc[nb][1]), fmaxf(acc[nb][2], acc[nb][3]));
-        m = fmaxf(m, __shfl_xor(m, 16));
-        m = fmaxf(m, __shfl_xor(m, 32));
-        float sum = ((__expf(acc[nb][0] - m) + __expf(acc[nb][1] - m)) + __expf(acc[nb][2] - m)) +
-                    __expf(acc[nb][3] - m);
-        sum += __shfl_xor(sum, 16);
-        sum += __shfl_xor(sum, 32);
+        const float m = group4_max(fmaxf(fmaxf(acc[nb][0], acc[nb][1]), fmaxf(acc[nb][2], acc[nb][3])));
+        // e^{x - m} = 2^{x log2 e - m log2 e}: one fma per logit.
+        const float ml = -m * kLog2e;
+        const float sum = group4_sum(
+            ((exp2_f(__builtin_fmaf(acc[nb][0], kLog2e, ml)) + exp2_f(__builtin_fmaf(acc[nb][1], kLog2e, ml))) +
+             exp2_f(__builtin_fmaf(acc[nb][2], kLog2e, ml))) +
+            exp2_f(__builtin_fmaf(acc[nb][3], kLog2e, ml)));
         if (lg == 0) red[(c / NQ) & 1][wave][nb * 16 + lr] = make_float2(m, sum);
         const int row = r0 + nb * 16 + lr;
         const int yo = y[nb] - vbase;
