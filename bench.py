@@ -235,11 +235,11 @@ def main():
     achieved = per_launch_flops / avg_launch_s / 1e12
     traffic = None
     # The kernels the library picks for this shape (see soma_api.hip):
-    # streaming projection and head where H % 64 == 0, H <= 512 and one
+    # streaming projection and head where H % 64 == 0, H <= 704 and one
     # slot's gate inputs stay under 2^31 bytes; the recurrence one block per
     # job at H = 64, else persistent (one launch per layer and chunk) unless
     # it ran per time step.
-    streams = (w.hidden % 64 == 0 and w.hidden <= 512
+    streams = (w.hidden % 64 == 0 and w.hidden <= 704
                and (w.seq_len - 1) * w.batch * 4 * w.hidden * 4 < 2 ** 31)
     kname = {"rec": "k_rec_step", "proj": "k_proj_stream" if streams else "k_proj", "fold": "k_fold",
              "head": "k_head_stream" if streams else "k_head_ce"}[dom]

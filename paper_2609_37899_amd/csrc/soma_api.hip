@@ -594,13 +594,13 @@ const void* persist_kernel_for(int B, int H, int probe) {
   return probe == SOMA_PROBE_GAUSSIAN ? persist_kernel_for<false>(B, H) : persist_kernel_for<true>(B, H);
 }
 
-// The streaming input projection and head apply for H % 64 == 0, H <= 512
-// and one slot's gate inputs under 2^31 bytes (32-bit offsets), unless the
-// tiled kernels are asked for.
+// The streaming input projection and head apply for H % 64 == 0,
+// H <= kStreamMaxH and one slot's gate inputs under 2^31 bytes (32-bit
+// offsets), unless the tiled kernels are asked for.
 bool stream_weights(const soma_config& c) {
   if (c.flags & SOMA_FLAG_TILED_WEIGHTS) return false;
   const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
-  return c.hidden % 64 == 0 && c.hidden <= 512 && gin_slot_bytes < (int64_t(1) << 31);
+  return c.hidden % 64 == 0 && c.hidden <= soma::kStreamMaxH && gin_slot_bytes < (int64_t(1) << 31);
 }
 
 template <bool kRad>
@@ -614,7 +614,10 @@ void launch_head_stream_t(const soma::FwdArgs& a, int nslots, float2* hpart, flo
     case 5: hipLaunchKernelGGL((soma::k_head_stream<5, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
     case 6: hipLaunchKernelGGL((soma::k_head_stream<6, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
     case 7: hipLaunchKernelGGL((soma::k_head_stream<7, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
-    default: hipLaunchKernelGGL((soma::k_head_stream<8, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 8: hipLaunchKernelGGL((soma::k_head_stream<8, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 9: hipLaunchKernelGGL((soma::k_head_stream<9, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    case 10: hipLaunchKernelGGL((soma::k_head_stream<10, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
+    default: hipLaunchKernelGGL((soma::k_head_stream<11, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;   // H = 704 (stream_weights)
   }
 }
 
@@ -637,7 +640,10 @@ void launch_proj_stream_t(const soma::FwdArgs& a, int nslots, hipStream_t st) {
     case 5: hipLaunchKernelGGL((soma::k_proj_stream<5, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
     case 6: hipLaunchKernelGGL((soma::k_proj_stream<6, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
     case 7: hipLaunchKernelGGL((soma::k_proj_stream<7, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
-    default: hipLaunchKernelGGL((soma::k_proj_stream<8, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 8: hipLaunchKernelGGL((soma::k_proj_stream<8, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 9: hipLaunchKernelGGL((soma::k_proj_stream<9, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 10: hipLaunchKernelGGL((soma::k_proj_stream<10, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    default: hipLaunchKernelGGL((soma::k_proj_stream<11, kRad>), grid, block, 0, st, a, mblocks, nslots); break;   // H = 704 (stream_weights)
   }
 }
 

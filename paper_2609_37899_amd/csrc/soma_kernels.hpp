@@ -1387,11 +1387,13 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
 // to XCDs round-robin), so they share its L2 while streaming the same h.
 // ---------------------------------------------------------------------------
 constexpr int kProjThreads = 512;
+constexpr int kStreamMaxH = 704;      // resident rows of K = 704: 176 VGPRs of split fragments per lane
 
 template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_stream(FwdArgs a, int mblocks, int nslots) {
   constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
-  constexpr int NQ = NCH % 4 == 0 ? NCH / 4 : split_quarters(NCH);   // ring chunks per row tile (256 k each where possible)
+  // ring chunks per row tile: 256 k each where possible, else 128 or 64
+  constexpr int NQ = NCH % 4 == 0 ? NCH / 4 : (NCH > 8 ? (NCH % 2 == 0 ? NCH / 2 : NCH) : split_quarters(NCH));
   constexpr int QC = KC / NQ;                 // k chunks per ring chunk
   constexpr int KW = QC * 32;                 // k per ring chunk
   constexpr int SW = KW + 16;                 // padded LDS row in halves (an odd multiple of 32 bytes)

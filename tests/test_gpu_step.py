@@ -23,6 +23,7 @@ CASES = {
     "h64_e64_b33": (1, 2, 64, 64, 33, 10, 2, 1e-3, 1e-2, 0, 0),  # one block per job, embedding in LDS (two chunks)
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
+    "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0, 0),    # streaming projection and head at H = 704
 }
 
 
@@ -178,7 +179,7 @@ def test_persistent_and_per_step_recurrence_agree(name, probe):
 
 
 @pytest.mark.parametrize("name,probe", [("tiny", 0), ("h512_short", 0), ("b64_h128", 0), ("b40_h384", 0),
-                                        ("h512_short", 1), ("b40_h384", 2)])
+                                        ("h512_short", 1), ("b40_h384", 2), ("h704_b12", 1)])
 def test_streaming_and_tiled_weights_agree(name, probe):
     """The streaming projection and head (weights resident in registers,
     probes drawn once per 128 weight rows, products on the fp16 matrix cores
