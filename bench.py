@@ -30,7 +30,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 PEAK_FP16_MFMA_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 # Kernels whose products run on the fp16 matrix cores from split fp32
 # operands (three fp16 products per fp32 product, fp32 accumulation).
-SPLIT_F16_KERNELS = ("k_rec_persist", "k_rec_local", "k_proj_stream", "k_head_stream", "k_body")
+SPLIT_F16_KERNELS = ("k_rec_persist", "k_rec_local", "k_proj_stream", "k_head_stream", "k_head_fused", "k_body")
 PEAK_HBM_GBS = 8000.0
 PROBE_LAWS = {"gaussian": 0, "sparse": 1, "dense": 2}
 
@@ -141,8 +141,8 @@ def main():
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; "
-                                   f"--gpus {args.gpus} is not supported (experts shard across "
-                                   "GPUs with no communication; see DESIGN.md)"}))
+                                   f"--gpus {args.gpus} is not supported (experts would shard "
+                                   "across GPUs with no communication between them)"}))
         sys.exit(2)
 
     import numpy as np
@@ -242,7 +242,7 @@ def main():
     streams = (w.hidden % 64 == 0 and w.hidden <= 704
                and (w.seq_len - 1) * w.batch * 4 * w.hidden * 4 < 2 ** 31)
     kname = {"rec": "k_rec_step", "proj": "k_proj_stream" if streams else "k_proj", "fold": "k_fold",
-             "head": "k_head_stream" if streams else "k_head_ce"}[dom]
+             "head": ("k_head_fused" if w.hidden <= 128 else "k_head_stream") if streams else "k_head_ce"}[dom]
     if w.arch == 1:
         kname = "k_body"          # the whole perturbed forward, one launch per direction chunk
     elif dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):

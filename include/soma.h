@@ -360,15 +360,17 @@ int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds_dev, uint64_t st
  * default; enabling adds one event record per phase boundary).  Times are
  * summed over direction chunks. */
 typedef struct soma_phase_times {
-  float fold_ms;          /* layer-1 gate inputs per byte value (k_fold) */
+  float fold_ms;          /* layer-1 gate inputs per byte value (k_fold; 0 where
+                             the H = 64 recurrence forms them in the block) */
   float proj_ms;          /* input projections of layers >= 2 (k_proj_stream, or
                              the tiled k_proj) */
-  float rec_ms;           /* recurrent time steps of all layers (k_rec_persist, one
-                             launch per layer and chunk, or k_rec_step, one per
-                             time step); for SOMA_ARCH_BODY the whole fused
-                             forward (k_body) */
-  float head_ms;          /* head + softmax cross entropy (k_head_stream and
-                             k_ce_combine, or the tiled k_head_ce) */
+  float rec_ms;           /* recurrent time steps of all layers (k_rec_persist or,
+                             at H = 64, k_rec_local: one launch per layer and
+                             chunk; or k_rec_step, one per time step); for
+                             SOMA_ARCH_BODY the whole fused forward (k_body) */
+  float head_ms;          /* head + softmax cross entropy (k_head_fused at
+                             H <= 128, k_head_stream and k_ce_combine above, or
+                             the tiled k_head_ce) */
   float reduce_ms;        /* loss sums and coefficients */
   float update_ms;        /* regenerate-and-update (k_update) */
   int32_t rec_launches;   /* recurrence launches in the step */

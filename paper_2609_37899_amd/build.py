@@ -22,7 +22,8 @@ HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
     # The probe generator is specified operation by operation: no contraction.
     "-ffp-contract=off",
-    # Packed fp32 VALU instructions stay off (build notes).
+    # Packed fp32 VALU instructions (v_pk_*_f32) stay off: plain fp32 code
+    # is compiled to single-lane instructions only.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # The instruction scheduler's ILP strategy: the body kernel runs one wave
     # per SIMD, so its latencies are hidden only by independent instructions

@@ -621,6 +621,23 @@ void launch_head_stream_t(const soma::FwdArgs& a, int nslots, float2* hpart, flo
   }
 }
 
+// H <= 128: the whole head and cross entropy of a slot in one block.
+template <bool kRad>
+void launch_head_fused_t(const soma::FwdArgs& a, int nslots, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(nslots)), block(soma::kHeadFusedThreads);
+  if (a.H == 64)
+    hipLaunchKernelGGL((soma::k_head_fused<1, kRad>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((soma::k_head_fused<2, kRad>), grid, block, 0, st, a);
+}
+
+void launch_head_fused(const soma::FwdArgs& a, int nslots, hipStream_t st) {
+  if (a.probe == SOMA_PROBE_GAUSSIAN)
+    launch_head_fused_t<false>(a, nslots, st);
+  else
+    launch_head_fused_t<true>(a, nslots, st);
+}
+
 void launch_head_stream(const soma::FwdArgs& a, int nslots, float2* hpart, float* htgt, hipStream_t st) {
   if (a.probe == SOMA_PROBE_GAUSSIAN)
     launch_head_stream_t<false>(a, nslots, hpart, htgt, st);
@@ -854,7 +871,10 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     }
     if (int rc = mark(ctx, kPhaseRec, st)) return rc;
   }
-  if (kPert && stream_weights(c)) {
+  if (kPert && stream_weights(c) && H <= 128) {
+    launch_head_fused(a, 2 * N * pcs, st);
+    if (int rc = check_launch("k_head_fused")) return rc;
+  } else if (kPert && stream_weights(c)) {
     float2* hpart = reinterpret_cast<float2*>(ctx->ws + L.hpart);
     float* htgt = reinterpret_cast<float*>(ctx->ws + L.htgt);
     launch_head_stream(a, 2 * N * pcs, hpart, htgt, st);

@@ -964,10 +964,9 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       // Cell update of row tile nb: c_t = f c_{t-1} + i g, h_t = o tanh(c_t),
       // written to the transposed tile that is published below.
       auto cell = [&](int nb) {
-        const float ai = acc[nb][0], af = acc[nb][1], ag = acc[nb][2], ao = acc[nb][3];
-        const float c = sigmoid_f(af) * cs[nb] + sigmoid_f(ai) * tanh_f(ag);
-        cs[nb] = c;
-        ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = sigmoid_f(ao) * tanh_f(c);
+        float h;
+        lstm_cell(acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3], cs[nb], h);
+        ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = h;
       };
 
       if (t == 0) {
@@ -1708,6 +1707,236 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
       hp[r0 + n] = make_float2(M, S);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Output head and cross entropy in one pass for H <= 128: a block of 16
+// waves owns one (expert, direction, sign) slot and all 256 rows of Whead
+// (wave w keeps rows 16 w .. + 15 as split fragments: 16 or 32 VGPRs), so
+// each row's cross entropy is finished in the block:
+//   ce = M + ln(sum_w s_w e^{m_w - M}) - logit_target,  M = max_w m_w,
+// from the 16 waves' (m_w, s_w) = (max, sum exp(logit - max)) over their 16
+// vocabulary rows.  All R rows of the slot's top-layer h stream once through
+// a double-buffered LDS ring of 64-row tiles (staged and split by all 1024
+// threads); the next tile is requested at the start of a tile.  Waves 0..3
+// (one per SIMD) combine a tile's partials, 16 rows each, while the next
+// tile's products run, and keep fp64 sums per lane; the slot's total goes
+// to the first of its per-tile loss partials at the end (the others are
+// zeroed: the loss reduction sums them).  The loop issues no store, so
+// waiting for the staged tile waits for nothing else.
+// ---------------------------------------------------------------------------
+constexpr int kHeadFusedThreads = 1024;
+constexpr float kNoShiftL1 = 64.0f;
+
+template <int NCH, bool kRad>
+__global__ __launch_bounds__(kHeadFusedThreads) void k_head_fused(FwdArgs a) {
+  constexpr int H = 64 * NCH;                 // 64 or 128
+  constexpr int KC = 2 * NCH;                 // 32-wide k chunks
+  constexpr int SW = H + 16;                  // ring row in halves (160 or 288 bytes: odd multiples of 32)
+  constexpr int PT = 64 * H / 4 / kHeadFusedThreads;   // float4 per thread per tile: 1 or 2
+  constexpr int ZLD = H + 8;                  // probe scratch row in floats
+  constexpr int RING_BYTES = 2 * 2 * 64 * SW * 2;
+  constexpr int ZS_BYTES = 128 * ZLD * 4;
+  constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
+  static_assert(NCH == 1 || NCH == 2, "H = 64 or 128");
+  static_assert(PT * kHeadFusedThreads * 4 == 64 * H, "a tile splits evenly over the threads");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];   // ring [buf][hi, lo][64][SW]
+  __shared__ float2 red[2][16][64];             // per-wave (m, s) of each row, by tile parity
+  __shared__ float tgl[2][64];                  // target logit of each row, by tile parity
+  __shared__ double dsum[64];
+  __shared__ unsigned wide;                     // some row of Whead+- has L1 norm >= kNoShiftL1
+  _Float16* ring = reinterpret_cast<_Float16*>(lds);
+  float* zs = reinterpret_cast<float*>(lds);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int B = a.B, T = a.T;
+  const int R = (T - 1) * B;
+  const int ps = blockIdx.x;                  // slot of this pass
+  const int sg = ps & 1, pj = ps >> 1;
+  const int e = pj / a.pcs, jl = pj % a.pcs;
+  const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = stream_key(a.seeds[e], a.step);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+  const int vbase = wave * 16 + 4 * lg;       // vocabulary rows vbase .. +3 of this lane
+  // 32-bit offsets: R H floats < 2^31 bytes (host check).
+  const __amdgpu_buffer_rsrc_t hbuf =
+      buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(static_cast<int64_t>(R) * H * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t bbuf = buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
+
+  // Whead+- rows 16 wave + lr, drawn 128 rows (one vocabulary half) at a time.
+  uint4 wh[KC], wl[KC];
+  float l1 = 0.0f;                            // this lane's part of its row's L1 norm
+  if (threadIdx.x == 0) wide = 0u;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    __syncthreads();
+    for (int q = threadIdx.x; q < 128 * (H / 4); q += kHeadFusedThreads) {
+      const int m = q / (H / 4), k4 = q % (H / 4);
+      const uint64_t kk = static_cast<uint64_t>(a.off_head + static_cast<int64_t>(128 * half + m) * H + 4 * k4);
+      *reinterpret_cast<float4*>(&zs[m * ZLD + 4 * k4]) =
+          kRad ? rademacher_quad(key, pair, step_lo, kk, a.probe == kProbeRademacher) : gauss_quad(key, pair, step_lo, kk >> 2);
+    }
+    __syncthreads();
+    if ((wave >> 3) == half) {
+      const int row = wave * 16 + lr;
+      const float* tr = th + a.off_head + static_cast<int64_t>(row) * H;
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const float* zr = &zs[(row - 128 * half) * ZLD + 32 * c + 8 * lg];
+        const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr + 32 * c + 8 * lg));
+        const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 32 * c + 8 * lg + 4));
+        split8v(w0, w1, wh[c], wl[c]);
+        l1 += ((fabsf(w0.x) + fabsf(w0.y)) + (fabsf(w0.z) + fabsf(w0.w))) +
+              ((fabsf(w1.x) + fabsf(w1.y)) + (fabsf(w1.z) + fabsf(w1.w)));
+      }
+    }
+  }
+  if (group4_sum(l1) >= kNoShiftL1) wide = 1u;
+  __syncthreads();                            // the scratch becomes the ring
+  // |h| <= 1, so |logit_v| <= ||Whead+-[v]||_1: below kNoShiftL1 for every v,
+  // e^logit neither overflows nor underflows in fp32 (a row's sum stays in
+  // [256 e^-64, 256 e^64]) and the maximum need not be subtracted.
+  const bool shift = wide != 0u;              // block-uniform
+
+  const int ntiles = (R + 63) / 64;
+  // Thread load i of a tile covers float4 (threadIdx.x + 1024 i) of its 64 x H
+  // block: row n = idx / (H / 4), quad idx % (H / 4).  Rows past R read zeros
+  // (past the buffer) and are never used.
+  float4 pre[PT];
+  auto gload = [&](int c) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kHeadFusedThreads;
+      pre[i] = buffer_load_f4<0>(hbuf, static_cast<uint32_t>(((c * 64 + idx / (H / 4)) * H + 4 * (idx % (H / 4))) * 4));
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int idx = threadIdx.x + i * kHeadFusedThreads;
+      const int n = idx / (H / 4), c4 = idx % (H / 4);
+      uint2 hi, lo;
+      split4(pre[i], hi, lo);
+      *reinterpret_cast<uint2*>(ring + ((buf * 2) * 64 + n) * SW + 4 * c4) = hi;
+      *reinterpret_cast<uint2*>(ring + ((buf * 2 + 1) * 64 + n) * SW + 4 * c4) = lo;
+    }
+  };
+
+  // Row r0 + lr = ytt B + yb of the tile, advanced by 64 rows a tile; rows
+  // 16 nb further on add the wave-uniform quotient and remainder of 16 nb
+  // by B (rows past R read past the batch: 0 from the buffer, never used).
+  int ytt = lr / B, yb = lr - (lr / B) * B;
+  const int q64 = 64 / B, r64 = 64 % B;
+  double cacc = 0.0;                          // this combining lane's ce sum (rows 16 wave + lane of every tile)
+  f32x4 acc[4];
+  // Rows of tile cc from the 16 waves' partials (waves 0..3, one per SIMD,
+  // 16 rows each), summed, logged and the target subtracted in fp64: a loss
+  // of one token then carries the rounding of the fp32 exponentials and
+  // partial sums only.
+  auto combine = [&](int cc) {
+    const int cb = cc & 1;
+    if (wave < 4 && lane < 16 && cc * 64 + wave * 16 + lane < R) {
+      const int n = wave * 16 + lane;
+      float M = 0.0f;
+      double S = 0.0;
+      if (shift) {
+        M = red[cb][0][n].x;
+#pragma unroll
+        for (int w = 1; w < 16; ++w) M = fmaxf(M, red[cb][w][n].x);
+        const float ML = -M * kLog2e;
+#pragma unroll
+        for (int w = 0; w < 16; ++w)
+          S += static_cast<double>(red[cb][w][n].y * exp2_f(__builtin_fmaf(red[cb][w][n].x, kLog2e, ML)));
+      } else {
+#pragma unroll
+        for (int w = 0; w < 16; ++w) S += static_cast<double>(red[cb][w][n].y);
+      }
+      cacc += (log(S) + static_cast<double>(M)) - static_cast<double>(tgl[cb][n]);
+    }
+  };
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int c = 0; c < ntiles; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < ntiles) gload(c + 1);
+    int y[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      const int qn = (16 * nb) / B, rn = 16 * nb - qn * B;   // wave-uniform
+      int bn = yb + rn, tn = ytt + qn;
+      if (bn >= B) {
+        bn -= B;
+        ++tn;
+      }
+      y[nb] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, static_cast<uint32_t>(bn * T + tn + 1), 0, 0);
+    }
+    yb += r64;
+    ytt += q64;
+    if (yb >= B) {
+      yb -= B;
+      ++ytt;
+    }
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      uint4 bh[4], bl[4];
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int o = (nb * 16 + lr) * SW + 32 * kc + 8 * lg;
+        bh[nb] = *reinterpret_cast<const uint4*>(ring + (buf * 2) * 64 * SW + o);
+        bl[nb] = *reinterpret_cast<const uint4*>(ring + (buf * 2 + 1) * 64 * SW + o);
+      }
+      mfma3_batch<4>(wh[kc], wl[kc], bh, bl, acc);
+    }
+    // The previous tile's rows, while the products run: its partials (the
+    // other parity) were written before the last barrier and are next
+    // written in tile c + 1, behind the next barrier.
+    if (c > 0) combine(c - 1);
+    // Lane (lr, lg) holds the logits of vocabulary rows vbase .. +3 for tile
+    // rows nb*16 + lr: reduce over the 4 lane groups; the lane holding a
+    // row's target logit records it.
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      float m = 0.0f, sum;
+      if (shift) {
+        m = group4_max(fmaxf(fmaxf(acc[nb][0], acc[nb][1]), fmaxf(acc[nb][2], acc[nb][3])));
+        const float ml = -m * kLog2e;
+        sum = group4_sum(
+            ((exp2_f(__builtin_fmaf(acc[nb][0], kLog2e, ml)) + exp2_f(__builtin_fmaf(acc[nb][1], kLog2e, ml))) +
+             exp2_f(__builtin_fmaf(acc[nb][2], kLog2e, ml))) +
+            exp2_f(__builtin_fmaf(acc[nb][3], kLog2e, ml)));
+      } else {
+        sum = group4_sum(((exp2_f(acc[nb][0] * kLog2e) + exp2_f(acc[nb][1] * kLog2e)) + exp2_f(acc[nb][2] * kLog2e)) +
+                         exp2_f(acc[nb][3] * kLog2e));
+      }
+      if (lg == 0) red[buf][wave][nb * 16 + lr] = make_float2(m, sum);
+      const int yo = y[nb] - vbase;
+      if (yo >= 0 && yo < 4) {
+        float v = acc[nb][0];
+#pragma unroll
+        for (int r = 1; r < 4; ++r)
+          if (yo == r) v = acc[nb][r];
+        tgl[buf][nb * 16 + lr] = v;
+      }
+    }
+    if (c + 1 < ntiles) sstore(buf ^ 1);
+    __syncthreads();
+  }
+  combine(ntiles - 1);
+  // The slot's total into its first tile partial, zeros in the others.
+  if (wave < 4 && lane < 16) dsum[wave * 16 + lane] = cacc;
+  __syncthreads();
+  double* part = a.part + slot * a.row_tiles;
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+    for (int n = 0; n < 64; ++n) tot += dsum[n];
+    part[0] = tot;
+  }
+  for (int k = 1 + static_cast<int>(threadIdx.x); k < a.row_tiles; k += kHeadFusedThreads) part[k] = 0.0;
 }
 
 // ce of every row from the two vocabulary halves, summed per 64-row tile in

@@ -27,11 +27,13 @@ CASES = {
 }
 
 
-def run_case(name, distinct=True, data=None, probe=0):
+def run_case(name, distinct=True, data=None, probe=0, head_scale=1.0):
     torch = require_gpu()
     N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
     shape = soma.Shape(N, L, E, H, B, T, P, mode, pc, probe=probe)
     theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=distinct)
+    if head_scale != 1.0:                      # Whead is the last 256 H parameters of each expert
+        theta[:, -256 * H:] *= np.float32(head_scale)
     if data is None:
         data = synth.expert_batches([100 + e for e in range(N)], B, T)
     seeds = synth.expert_seeds(N)
@@ -64,6 +66,23 @@ def test_step_matches_oracle(oracle_mod, name):
     cerr = np.abs(r["coef"] - o["coef"]).max() / np.abs(o["coef"]).max()
     print(f"{name}: loss rel {lerr:.2e}  theta rel {terr:.2e}  update rel {uerr:.2e}  coef rel {cerr:.2e}")
     assert not np.array_equal(r["theta"], r["theta0"])
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64_h128"])
+def test_large_head_weights_match_oracle(oracle_mod, name):
+    """Whead scaled 200-fold (row L1 norms near 1000): the one-pass head at
+    H <= 128 then subtracts each row's maximum logit before exponentiating
+    (below a row L1 norm of 64 on every row it need not, since |h| <= 1
+    bounds every logit by it; the other tests run that path)."""
+    N, L, E, H = CASES[name][:4]
+    r = run_case(name, head_scale=200.0)
+    l1 = np.abs(r["theta0"][:, -256 * H:].reshape(N, 256, H)).sum(axis=2).max()
+    assert l1 > 64.0
+    o = oracle_step(oracle_mod, r)
+    lerr = assert_losses_close(r["losses"], o["losses"])
+    terr = assert_theta_close(r["theta"], o["theta"])
+    print(f"{name} head x200 (row L1 up to {l1:.0f}): loss {r['losses'].mean():.3f}, rel {lerr:.2e}  "
+          f"theta rel {terr:.2e}")
 
 
 @pytest.mark.parametrize("probe", [1, 2])
