@@ -21,6 +21,7 @@ CASES = {
     "h64_b50_l2": (2, 2, 32, 64, 50, 9, 3, 1e-3, 1e-2, 0, 2),   # one block per job, four row tiles, ragged
     "h64_b20": (1, 1, 48, 64, 20, 13, 2, 1e-3, 1e-2, 0, 0),      # one block per job, two row tiles
     "h64_e64_b33": (1, 2, 64, 64, 33, 10, 2, 1e-3, 1e-2, 0, 0),  # one block per job, embedding in LDS (two chunks)
+    "h64_bt_big": (1, 1, 32, 64, 64, 257, 1, 1e-3, 1e-2, 0, 0),  # B T = 16448 > 16 KiB: the fold and per-step gathers
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
     "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0, 0),    # streaming projection and head at H = 704
