@@ -132,7 +132,7 @@ enum soma_arch {
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;
  * embed and hidden positive multiples of 16; batch >= 1; seq_len >= 2;
  * accum >= 0; pair_chunk in [0, D] (0 picks a chunk that keeps the workspace
- * under 24 GiB; the step processes its D directions in chunks of this many,
+ * under 64 GiB; the step processes its D directions in chunks of this many,
  * which changes memory use but not the result); flags: enum soma_flags.
  *
  * Accumulation (Appendix E): with A = accum > 1 an update averages the

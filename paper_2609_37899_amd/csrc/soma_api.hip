@@ -47,7 +47,7 @@ int ok() {
 constexpr size_t kAlign = 256;
 constexpr int kMaxGroups = 1024;              // persistent-recurrence groups (counters in the workspace)
 constexpr unsigned kSpinLimit = 1u << 20;     // polls (~1 s) before a persistent launch gives up
-constexpr size_t kAutoBudget = size_t(24) << 30;  // automatic pair_chunk keeps the workspace below this
+constexpr size_t kAutoBudget = size_t(64) << 30;  // automatic pair_chunk keeps the workspace below this
 
 size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -136,6 +136,9 @@ Layout layout_for_body(const soma_config& c, int pc) {
   return L;
 }
 
+bool stream_weights(const soma_config& c);
+bool local_embedding(const soma_config& c);
+
 Layout layout_for(const soma_config& c, int pc) {
   if (c.arch == SOMA_ARCH_BODY) return layout_for_body(c, pc);
   Layout L;
@@ -156,11 +159,16 @@ Layout layout_for(const soma_config& c, int pc) {
   L.coef = at; at += round_up(sizeof(float) * N * dirs(c));
   L.lossd = at; at += round_up(sizeof(double) * N * dirs(c) * 2);
   L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
-  L.U = at;    at += round_up(sizeof(float) * slots * SOMA_VOCAB * 4 * H);
+  // U: the perturbed slots' folded inputs, or only the N unperturbed ones
+  // of an evaluation where the H = 64 recurrence forms them in the block.
+  const size_t uslots = local_embedding(c) ? N : slots;
+  L.U = at;    at += round_up(sizeof(float) * uslots * SOMA_VOCAB * 4 * H);
   L.hseq = at; at += round_up(sizeof(float) * slots * R * H);
   L.cst = at;  at += round_up(sizeof(float) * slots * B * H);
-  L.hpart = at; at += round_up(sizeof(float) * 2 * slots * 2 * R);   // (m, s) per vocabulary half
-  L.htgt = at; at += round_up(sizeof(float) * slots * R);
+  // Head partials of k_head_stream only (H > 128; k_head_fused keeps its own).
+  const size_t hslots = stream_weights(c) && H > 128 ? slots : 0;
+  L.hpart = at; at += round_up(sizeof(float) * 2 * hslots * 2 * R);   // (m, s) per vocabulary half
+  L.htgt = at; at += round_up(sizeof(float) * hslots * R);
   L.gin = at;
   if (c.n_layers > 1) at += round_up(sizeof(float) * slots * R * 4 * H);
   L.total = at;
