@@ -52,8 +52,13 @@ def test_workspace_size_and_auto_chunk(lib):
     assert 0 < ws < 24 * 2**30
     s1 = shape_of(workloads.SOMA_N2, pair_chunk=1)
     assert soma.workspace_size(s1) < ws
-    big = shape_of(workloads.MONOLITH.with_(n_pairs=512))
-    assert soma.workspace_size(big) <= 24 * 2**30
+    # The automatic chunk keeps the workspace within 64 GiB: the monolith's
+    # 128 directions fit in one chunk, its 512 do not.
+    mono = workloads.MONOLITH
+    assert soma.workspace_size(shape_of(mono)) == soma.workspace_size(shape_of(mono, pair_chunk=mono.n_pairs))
+    big = shape_of(mono.with_(n_pairs=512))
+    assert soma.workspace_size(big) <= 64 * 2**30
+    assert soma.workspace_size(big) < soma.workspace_size(shape_of(mono.with_(n_pairs=512), pair_chunk=512))
 
 
 @pytest.mark.parametrize("field,value,code", [
