@@ -544,6 +544,19 @@ int launch_rec(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
   return SOMA_OK;
 }
 
+// The per-step recurrence with split fp16 products (perturbed step, H % 32
+// == 0, the per-step path chosen by the shape rather than by the flag).
+int launch_rec_split(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
+  const int B = a.B;
+  if (B <= 16)
+    hipLaunchKernelGGL((soma::k_rec_step_split<1>), grid, dim3(soma::kThreads), 0, st, a);
+  else if (B <= 32)
+    hipLaunchKernelGGL((soma::k_rec_step_split<2>), grid, dim3(soma::kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((soma::k_rec_step_split<4>), grid, dim3(soma::kThreads), 0, st, a);
+  return SOMA_OK;
+}
+
 int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 
 // Groups of H/32 blocks that the persistent recurrence can run at once
@@ -870,11 +883,15 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       ctx->rec_launches += 1;
     } else {
       const dim3 grid((H / 16) * bgroups, pcs, N);
+      const bool split = kPert && !(c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) && H % 32 == 0;
       for (int t = 0; t + 1 < c.seq_len; ++t) {
         a.t = t;
-        launch_rec<kPert>(a, grid, st);
+        if (split)
+          launch_rec_split(a, grid, st);
+        else
+          launch_rec<kPert>(a, grid, st);
       }
-      if (int rc = check_launch("k_rec_step")) return rc;
+      if (int rc = check_launch(split ? "k_rec_step_split" : "k_rec_step")) return rc;
       ctx->rec_launches += c.seq_len - 1;
     }
     if (int rc = mark(ctx, kPhaseRec, st)) return rc;

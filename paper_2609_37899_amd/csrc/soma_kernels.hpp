@@ -509,6 +509,127 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// One time step t, as k_rec_step (same grid, blocks, probes and cell update)
+// but with the products of both signs on the fp16 matrix cores from split
+// operands: h_{t-1} of both signs is split into its fp16 parts as it is
+// staged (32 K per chunk), and each lane forms W+- for its gate row and 8 K
+// values of a chunk from two probe quads, splits both signs and runs the
+// three passes over the row tiles.  The fp32 products of k_rec_step share
+// the vector ALU's datapath with the probe generation; these run beside it.
+// Used where the shape rules out the persistent recurrence (H > 512 or
+// H % 64 != 0, B > 64) and H % 32 == 0; SOMA_FLAG_PER_STEP_RECURRENCE keeps
+// the fp32 k_rec_step.
+// ---------------------------------------------------------------------------
+constexpr int kStepSw = 32 + 16;   // staged row in halves (96 bytes: an odd multiple of 32)
+
+template <int NB>
+__global__ __launch_bounds__(kThreads) void k_rec_step_split(FwdArgs a) {
+  constexpr int NS = 2, ROWS = NB * 16;
+  constexpr int F4 = NS * ROWS * 8;                     // float4 of h per chunk (both signs)
+  constexpr int PT = F4 / kThreads;
+  static_assert(PT * kThreads == F4, "a chunk splits evenly over the threads");
+  __shared__ __attribute__((aligned(16))) _Float16 hs[2][NS][2][ROWS][kStepSw];   // [buf][sign][hi, lo][row][k]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T, in = a.in_l, t = a.t;
+  const int ntile = H / 16;
+  const int utile = blockIdx.x % ntile, b0 = (blockIdx.x / ntile) * ROWS;
+  const int jl = blockIdx.y, e = blockIdx.z;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const int64_t R = static_cast<int64_t>(T - 1) * B;
+  const int64_t slot0 = (static_cast<int64_t>(e) * a.PC + jl) * NS;
+
+  f32x4 acc[NS][NB];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (t > 0) {
+    const uint2 key = stream_key(a.seeds[e], a.step);
+    const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+    const float eps = eps_of(a, e);
+    const int prow = utile * 64 + wave * 16 + lr;
+    const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H) + in;
+    const float* hprev = a.hseq + static_cast<int64_t>(t - 1) * B * H;
+    const int nch = H / 32;
+    float4 pre[PT];
+    // Thread load i of a chunk: float4 c4 = idx & 7 of row n = (idx >> 3) % ROWS
+    // of sign s = idx / (8 ROWS); rows past the batch stage zeros.
+    auto gload = [&](int c) {
+#pragma unroll
+      for (int i = 0; i < PT; ++i) {
+        const int idx = threadIdx.x + i * kThreads;
+        const int c4 = idx & 7, n = (idx >> 3) % ROWS, s = idx / (8 * ROWS);
+        const int b = b0 + n;
+        pre[i] = b < B ? *reinterpret_cast<const float4*>(hprev + ((slot0 + s) * R + b) * H + 32 * c + 4 * c4)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < PT; ++i) {
+        const int idx = threadIdx.x + i * kThreads;
+        const int c4 = idx & 7, n = (idx >> 3) % ROWS, s = idx / (8 * ROWS);
+        uint2 hi, lo;
+        split4(pre[i], hi, lo);
+        *reinterpret_cast<uint2*>(&hs[buf][s][0][n][4 * c4]) = hi;
+        *reinterpret_cast<uint2*>(&hs[buf][s][1][n][4 * c4]) = lo;
+      }
+    };
+    gload(0);
+    sstore(0);
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      if (c + 1 < nch) gload(c + 1);
+      const int buf = c & 1;
+      const int64_t kk = wrow + 32 * c + 8 * lg;
+      const float4 t0 = *reinterpret_cast<const float4*>(th + kk);
+      const float4 t1 = *reinterpret_cast<const float4*>(th + kk + 4);
+      const float4 z0 = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk));
+      const float4 z1 = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk + 4));
+      uint4 wh[NS], wl[NS];
+      split8v(fma4(eps, z0, t0), fma4(eps, z1, t1), wh[0], wl[0]);
+      split8v(fma4(-eps, z0, t0), fma4(-eps, z1, t1), wh[1], wl[1]);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        uint4 bh[NB], bl[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          bh[nb] = *reinterpret_cast<const uint4*>(&hs[buf][s][0][nb * 16 + lr][8 * lg]);
+          bl[nb] = *reinterpret_cast<const uint4*>(&hs[buf][s][1][nb * 16 + lr][8 * lg]);
+        }
+        mfma3_batch<NB>(wh[s], wl[s], bh, bl, acc[s]);
+      }
+      if (c + 1 < nch) sstore(buf ^ 1);
+      __syncthreads();
+    }
+  }
+
+  const int unit = utile * 16 + wave * 4 + lg;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int b = b0 + nb * 16 + lr;
+      if (b >= B) continue;
+      const int64_t slot = slot0 + s;
+      float4 gi;
+      if (a.layer == 0) {
+        const int v = bytes_of(a, e, jl)[static_cast<int64_t>(b) * T + t];
+        gi = *reinterpret_cast<const float4*>(a.U + (slot * kVocab + v) * (4 * static_cast<int64_t>(H)) + 4 * unit);
+      } else {
+        gi = *reinterpret_cast<const float4*>(
+            a.gin + (slot * R + static_cast<int64_t>(t) * B + b) * (4 * static_cast<int64_t>(H)) + 4 * unit);
+      }
+      float* cp = a.cst + (slot * B + b) * static_cast<int64_t>(H) + unit;
+      float c = t > 0 ? *cp : 0.0f, h;
+      lstm_cell(acc[s][nb][0] + gi.x, acc[s][nb][1] + gi.y, acc[s][nb][2] + gi.z, acc[s][nb][3] + gi.w, c, h);
+      *cp = c;
+      a.hseq[(slot * R + static_cast<int64_t>(t) * B + b) * H + unit] = h;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Head and fused softmax cross entropy over 256 byte values.
 //   logits[row][v] = sum_k Whead+-[v][k] h[slot][row][k];
 //   ce = log sum_v exp(logits - max) + max - logits[target]

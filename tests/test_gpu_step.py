@@ -25,6 +25,7 @@ CASES = {
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
     "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0, 0),    # streaming projection and head at H = 704
+    "h96_b70": (1, 2, 32, 96, 70, 7, 2, 1e-3, 1e-2, 0, 0),      # per-step split products, two batch groups
 }
 
 
@@ -194,6 +195,38 @@ def test_persistent_and_per_step_recurrence_agree(name, probe):
     assert np.all(np.isfinite(l0))
     rel = np.abs(l0.astype(np.float64) - l1) / np.abs(l1)
     print(f"{name} law {probe}: persistent vs per-step loss rel {rel.max():.2e}")
+    assert rel.max() <= 1e-5, rel.max()
+    assert_theta_close(t0, t1)
+
+
+@pytest.mark.parametrize("name,probe", [("h704_b12", 0), ("h96_b70", 2)])
+def test_split_and_fp32_per_step_recurrence_agree(name, probe):
+    """Where the shape rules out the persistent recurrence (H > 512, or
+    H % 64 != 0 with B > 64) the per-step launches form their products on the
+    fp16 matrix cores from split operands; the per-step flag keeps fp32
+    products.  Same launches, per-pair mean losses within 1e-5, the updated
+    weights to the parity tolerance (each path is also held to the oracle)."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = soma.seeds_tensor(synth.expert_seeds(N))
+    outs = []
+    for flags in (0, soma.FLAG_PER_STEP_RECURRENCE):
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags, probe))
+        ctx.set_phase_timing(True)
+        th = torch.from_numpy(theta.copy()).cuda()
+        losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+        ctx.spsa_step(th, seeds, 2, eps, lr, torch.from_numpy(data).cuda(), losses)
+        launches = ctx.phase_times()["rec_launches"]
+        torch.cuda.synchronize()
+        outs.append((th.cpu().numpy(), losses.cpu().numpy(), launches))
+    (t0, l0, n0), (t1, l1, n1) = outs
+    chunks = (P + (pc or P) - 1) // (pc or P)
+    assert n0 == n1 == L * (T - 1) * chunks
+    assert np.all(np.isfinite(l0))
+    rel = np.abs(l0.astype(np.float64) - l1) / np.abs(l1)
+    print(f"{name} law {probe}: split vs fp32 per-step loss rel {rel.max():.2e}")
     assert rel.max() <= 1e-5, rel.max()
     assert_theta_close(t0, t1)
 
