@@ -94,14 +94,18 @@ enum soma_probe_law {
 
 /* Execution flags (soma_config.flags). */
 enum soma_flags {
-  /* Run the recurrence as one launch per time step even where the persistent
-   * kernel applies (the result is the same up to fp32 rounding order). */
+  /* Run the recurrence as one launch per time step with fp32 matrix
+   * products (probes regenerated per step), even where the persistent, the
+   * one-block (H = 64) or the split-product per-step kernel applies.  Those
+   * form each fp32 product from fp16 parts (x = hi + lo, three products,
+   * about 2^-21 relative per operand), so results agree within that
+   * rounding; this path is the fp32 reference. */
   SOMA_FLAG_PER_STEP_RECURRENCE = 1,
   /* Run the input projections of layers 2..L and the output head as row
-   * tiles that regenerate their probes per tile, even where the streaming
-   * kernels (probes drawn once per 128 weight rows, weights held in
-   * registers) apply.  The projections agree bit for bit; the head's cross
-   * entropy agrees up to fp32 rounding order. */
+   * tiles with fp32 matrix products that regenerate their probes per tile,
+   * even where the streaming kernels (probes drawn once per 128 weight rows,
+   * weights held in registers, split fp16 products) apply.  Results agree
+   * within the split products' rounding. */
   SOMA_FLAG_TILED_WEIGHTS = 2
 };
 
