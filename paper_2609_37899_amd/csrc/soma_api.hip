@@ -625,11 +625,10 @@ bool stream_weights(const soma_config& c) {
 }
 
 template <bool kRad>
+// H > 128 (k_head_fused takes H <= 128), H % 64 == 0, H <= kStreamMaxH.
 void launch_head_stream_t(const soma::FwdArgs& a, int nslots, float2* hpart, float* htgt, hipStream_t st) {
   const dim3 grid(unsigned(nslots * 2)), block(soma::kProjThreads);
   switch (a.H / 64) {
-    case 1: hipLaunchKernelGGL((soma::k_head_stream<1, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
-    case 2: hipLaunchKernelGGL((soma::k_head_stream<2, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
     case 3: hipLaunchKernelGGL((soma::k_head_stream<3, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
     case 4: hipLaunchKernelGGL((soma::k_head_stream<4, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;
     case 5: hipLaunchKernelGGL((soma::k_head_stream<5, kRad>), grid, block, 0, st, a, nslots, hpart, htgt); break;

@@ -1653,9 +1653,9 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_stream(
 // that the loss reduction reads).
 // Partials: hpart[slot][half][R] float2 (m, s); htgt[slot][R].
 // ---------------------------------------------------------------------------
-// At H <= 128 the probe scratch is sized by K and the block asks for four
-// waves per SIMD (at most 128 VGPRs), so two blocks share a compute unit and
-// cover each other's per-tile reductions and barriers.
+// The library launches it for H > 128 (k_head_fused covers H <= 128); at
+// H <= 128 the probe scratch would be sized by K and the block would ask for
+// four waves per SIMD, so that two blocks share a compute unit.
 template <int NCH, bool kRad>
 __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(FwdArgs a, int nslots,
                                                                              float2* hpart, float* htgt) {
