@@ -174,6 +174,22 @@ __device__ __forceinline__ void lstm_cell(float ai, float af, float ag, float ao
   h = __builtin_copysignf((1.0f - ec) * __builtin_amdgcn_rcpf((1.0f + eo) * (1.0f + ec)), c);
 }
 
+// The cell update from pre-activations already multiplied by gate_scale(g)
+// (-log2 e for the gates i, f, o; 2 log2 e for the candidate g): the
+// exponentials' arguments come straight from the products, |x| and the sign
+// of the candidate being source modifiers.  Same formulas as lstm_cell.
+__host__ __device__ constexpr float gate_scale(int g) { return g == 2 ? 2.0f * kLog2e : -kLog2e; }
+
+__device__ __forceinline__ void lstm_cell_scaled(float pi, float pf, float pg, float po, float& c, float& h) {
+  const float ef = exp2_f(pf), ei = exp2_f(pi), eo = exp2_f(po);
+  const float eg = exp2_f(-__builtin_fabsf(pg));
+  const float sf = __builtin_amdgcn_rcpf(1.0f + ef);
+  const float ig = __builtin_copysignf((1.0f - eg) * __builtin_amdgcn_rcpf((1.0f + ei) * (1.0f + eg)), pg);
+  c = __builtin_fmaf(sf, c, ig);
+  const float ec = exp2_f(-2.0f * kLog2e * __builtin_fabsf(c));
+  h = __builtin_copysignf((1.0f - ec) * __builtin_amdgcn_rcpf((1.0f + eo) * (1.0f + ec)), c);
+}
+
 __device__ __forceinline__ float tanh_f(float x) {
   // 1 - 2 / (e^{2x} + 1), saturating correctly for large |x|.
   return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * x) + 1.0f);
@@ -1296,8 +1312,11 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
         for (int c = 0; c < (seg == 0 ? KC : KX); ++c) {
           const float* zr = &zs[(row - 128 * rg) * kZw + 32 * c + 8 * lg];
           const float* tr = th + wrow + 32 * c + 8 * lg;
-          const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
-          const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+          float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
+          float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+          const float gs = gate_scale(lr & 3);
+          w0 = make_float4(w0.x * gs, w0.y * gs, w0.z * gs, w0.w * gs);
+          w1 = make_float4(w1.x * gs, w1.y * gs, w1.z * gs, w1.w * gs);
           if (seg == 0)
             split8v(w0, w1, wh[m][c], wl[m][c]);
           else
@@ -1373,7 +1392,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
       float h[MT];
 #pragma unroll
       for (int m = 0; m < MT; ++m)
-        lstm_cell(acc[m][nb][0], acc[m][nb][1], acc[m][nb][2], acc[m][nb][3], cs[m][nb], h[m]);
+        lstm_cell_scaled(acc[m][nb][0], acc[m][nb][1], acc[m][nb][2], acc[m][nb][3], cs[m][nb], h[m]);
       const int n = nb * 16 + lr;
       uint32_t hi, lo;
       split2(h[0], h[1], hi, lo);
@@ -1430,7 +1449,8 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
       for (int m = 0; m < MT; ++m)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
-          acc[m][nb] = f32x4{gi[P][m][nb].x, gi[P][m][nb].y, gi[P][m][nb].z, gi[P][m][nb].w};
+          acc[m][nb] = f32x4{gi[P][m][nb].x * gate_scale(0), gi[P][m][nb].y * gate_scale(1),
+                             gi[P][m][nb].z * gate_scale(2), gi[P][m][nb].w * gate_scale(3)};
       if (t + 3 < T) {
         load_inputs(gi[P], vb[P], t + 2);
         if (a.layer == 0 && t + 5 < T) {
