@@ -556,7 +556,7 @@ __global__ __launch_bounds__(256) void k_head_delta_part(const float* fdec, cons
     __syncthreads();
     for (int i = threadIdx.x; i < n * dm; i += 256)
       fs[i / dm][i % dm] = fdec[(static_cast<int64_t>(e) * R + r0) * dm + i];
-    if (threadIdx.x < n) {
+    if (static_cast<int>(threadIdx.x) < n) {
       const int64_t r = r0 + threadIdx.x;
       const int64_t bb = r / (T - 1), tt = r % (T - 1);
       ls[threadIdx.x] = lse[static_cast<int64_t>(e) * R + r];
