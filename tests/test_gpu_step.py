@@ -23,6 +23,7 @@ CASES = {
     "h64_e64_b33": (1, 2, 64, 64, 33, 10, 2, 1e-3, 1e-2, 0, 0),  # one block per job, embedding in LDS (two chunks)
     "h64_bt_big": (1, 1, 32, 64, 64, 257, 1, 1e-3, 1e-2, 0, 0),  # B T = 16448 > 16 KiB: the fold and per-step gathers
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 0, 2),
+    "h128_b10": (1, 1, 32, 128, 10, 9, 2, 1e-3, 1e-2, 0, 0),     # one-pass head at H = 128, R = 80: a ragged tile
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
     "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0, 0),    # streaming projection and head at H = 704
     "h96_b70": (1, 2, 32, 96, 70, 7, 2, 1e-3, 1e-2, 0, 0),      # per-step split products, two batch groups
@@ -70,7 +71,7 @@ def test_step_matches_oracle(oracle_mod, name):
     assert not np.array_equal(r["theta"], r["theta0"])
 
 
-@pytest.mark.parametrize("name", ["tiny", "b64_h128"])
+@pytest.mark.parametrize("name", ["tiny", "b64_h128", "h128_b10"])
 def test_large_head_weights_match_oracle(oracle_mod, name):
     """Whead scaled 200-fold (row L1 norms near 1000): the one-pass head at
     H <= 128 then subtracts each row's maximum logit before exponentiating
