@@ -27,6 +27,8 @@ CASES = {
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0, 0),
     "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0, 0),    # streaming projection and head at H = 704
     "h96_b70": (1, 2, 32, 96, 70, 7, 2, 1e-3, 1e-2, 0, 0),      # per-step split products, two batch groups
+    "h96_b24": (2, 1, 32, 96, 24, 6, 2, 1e-3, 1e-2, 0, 0),      # per-step split products, two row tiles
+    "h64_e64_b12": (1, 1, 64, 64, 12, 11, 2, 1e-3, 1e-2, 0, 0),  # one block per job, embedding in LDS, one row tile
 }
 
 
@@ -200,7 +202,7 @@ def test_persistent_and_per_step_recurrence_agree(name, probe):
     assert_theta_close(t0, t1)
 
 
-@pytest.mark.parametrize("name,probe", [("h704_b12", 0), ("h96_b70", 2)])
+@pytest.mark.parametrize("name,probe", [("h704_b12", 0), ("h96_b70", 2), ("h96_b24", 1)])
 def test_split_and_fp32_per_step_recurrence_agree(name, probe):
     """Where the shape rules out the persistent recurrence (H > 512, or
     H % 64 != 0 with B > 64) the per-step launches form their products on the
