@@ -42,7 +42,8 @@ def build(force: bool = False) -> str:
 class OracleCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "probe", "accum", "arch")] + [("tied_head", ctypes.c_void_p), ("head_stride", ctypes.c_int64)]
+        "probe", "accum", "arch")] + [("tied_head", ctypes.c_void_p), ("head_stride", ctypes.c_int64),
+                                      ("perturb_mask", ctypes.c_uint32)]
 
 
 def _load():
@@ -86,6 +87,8 @@ def _load():
                 "oracle_spsa_step": (ctypes.c_int, [cfgp, f32p, u64p, ctypes.c_uint64,
                                                     ctypes.c_float, ctypes.c_float, u8p, f32p,
                                                     f64p, f32p, f64p]),
+                "oracle_spsa_step_rates": (ctypes.c_int, [cfgp, f32p, u64p, ctypes.c_uint64, f32p, f32p,
+                                                          u8p, f32p, f64p, f32p, f64p]),
                 "oracle_eval_loss": (ctypes.c_int, [cfgp, f32p, u8p, f64p]),
                 "oracle_num_threads": (ctypes.c_int, []),
                 "oracle_head_delta": (ctypes.c_double, [cfgp, f32p, u8p, f64p]),
@@ -107,14 +110,18 @@ PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 
 
 ARCH_LSTM, ARCH_PAPER_BODY = 0, 1
+# perturb_mask bits: the parameter groups that are perturbed and updated
+# (0 = all of them).
+PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD = 1, 2, 4
 
 
 def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode=0,
-             probe=PROBE_GAUSSIAN, accum=1, arch=ARCH_LSTM, tied_head=None):
+             probe=PROBE_GAUSSIAN, accum=1, arch=ARCH_LSTM, tied_head=None, perturb_mask=0):
     """tied_head (arch 1): the frozen tied matrix E, [V][d] (shared by all
-    experts) or [N][V][d] (one per expert); the configuration keeps it alive."""
+    experts) or [N][V][d] (one per expert); the configuration keeps it alive.
+    perturb_mask: PERTURB_* bits of the perturbed and updated groups (0: all)."""
     cfg = OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe, accum,
-                    arch, None, 0)
+                    arch, None, 0, perturb_mask)
     if tied_head is not None:
         h = np.ascontiguousarray(tied_head, dtype=np.float32)
         cfg._head_ref = h
@@ -128,7 +135,8 @@ def cfg_from(shape) -> OracleCfg:
     return make_cfg(shape.n_experts, shape.n_layers, shape.embed, shape.hidden, shape.batch,
                     shape.seq_len, shape.n_pairs, getattr(shape, "loss_mode", 0),
                     getattr(shape, "probe", PROBE_GAUSSIAN), getattr(shape, "accum", 1),
-                    getattr(shape, "arch", ARCH_LSTM), getattr(shape, "tied_head", None))
+                    getattr(shape, "arch", ARCH_LSTM), getattr(shape, "tied_head", None),
+                    getattr(shape, "perturb_mask", 0))
 
 
 def head_delta(cfg: OracleCfg, theta_e, bytes_e):
@@ -306,11 +314,13 @@ def apply_adam(cfg: OracleCfg, theta_e, m_e, v_e, t: int, seed: int, step: int, 
     return (to, mo, vo, gh) if want_ghat else (to, mo, vo)
 
 
-def spsa_step(cfg: OracleCfg, theta: np.ndarray, seeds, step: int, eps: float, lr: float,
+def spsa_step(cfg: OracleCfg, theta: np.ndarray, seeds, step: int, eps, lr,
               bytes_all: np.ndarray, want_ghat: bool = False):
     """Full oracle step.  bytes_all is [N][B][T], or [A][N][B][T] with A =
-    cfg.accum accumulation batches.  Returns dict(losses [N,D,2] f32, coef
-    [N,D] f64, theta [N,d] f32, ghat [N,d] f64 or None), D = A P directions."""
+    cfg.accum accumulation batches.  eps and lr are scalars, or [N] arrays
+    (one radius and learning rate per expert).  Returns dict(losses [N,D,2]
+    f32, coef [N,D] f64, theta [N,d] f32, ghat [N,d] f64 or None), D = A P
+    directions."""
     A = max(1, cfg.accum)
     N, P = cfg.n_experts, cfg.n_pairs * A
     d = param_count(cfg)
@@ -321,11 +331,21 @@ def spsa_step(cfg: OracleCfg, theta: np.ndarray, seeds, step: int, eps: float, l
     coef = np.empty((N, P), dtype=np.float64)
     out = np.empty_like(t)
     gh = np.empty((N, d), dtype=np.float64) if want_ghat else None
-    rc = _load().oracle_spsa_step(ctypes.byref(cfg), _ptr(t, ctypes.c_float),
-                                  _ptr(sd, ctypes.c_uint64), int(step), float(eps), float(lr),
-                                  _ptr(b, ctypes.c_uint8), _ptr(losses, ctypes.c_float),
-                                  _ptr(coef, ctypes.c_double), _ptr(out, ctypes.c_float),
-                                  _ptr(gh, ctypes.c_double) if want_ghat else None)
+    if np.ndim(eps) == 0 and np.ndim(lr) == 0:
+        rc = _load().oracle_spsa_step(ctypes.byref(cfg), _ptr(t, ctypes.c_float),
+                                      _ptr(sd, ctypes.c_uint64), int(step), float(eps), float(lr),
+                                      _ptr(b, ctypes.c_uint8), _ptr(losses, ctypes.c_float),
+                                      _ptr(coef, ctypes.c_double), _ptr(out, ctypes.c_float),
+                                      _ptr(gh, ctypes.c_double) if want_ghat else None)
+    else:
+        ev = np.ascontiguousarray(np.broadcast_to(np.asarray(eps, np.float32), (N,)))
+        lv = np.ascontiguousarray(np.broadcast_to(np.asarray(lr, np.float32), (N,)))
+        rc = _load().oracle_spsa_step_rates(ctypes.byref(cfg), _ptr(t, ctypes.c_float),
+                                            _ptr(sd, ctypes.c_uint64), int(step), _ptr(ev, ctypes.c_float),
+                                            _ptr(lv, ctypes.c_float), _ptr(b, ctypes.c_uint8),
+                                            _ptr(losses, ctypes.c_float), _ptr(coef, ctypes.c_double),
+                                            _ptr(out, ctypes.c_float),
+                                            _ptr(gh, ctypes.c_double) if want_ghat else None)
     if rc != 0:
         raise ValueError("oracle_spsa_step rejected the configuration")
     return {"losses": losses, "coef": coef, "theta": out, "ghat": gh}

@@ -74,6 +74,8 @@ typedef struct {
   int32_t arch;      /* 0: stacked LSTM + linear head; 1: the paper's expert body (see below) */
   const float *tied_head; /* arch 1: the frozen tied embedding/decoder E [V][d] of expert 0 */
   int64_t head_stride;    /* floats from one expert's E to the next (0: one shared E) */
+  uint32_t perturb_mask;  /* perturbed parameter groups: bit 0 embedding, bit 1 LSTM layers (the
+                             whole body for arch 1), bit 2 head; 0 means all of them */
 } oracle_cfg;
 
 /* Directions per update: P per batch, A batches. */
@@ -117,6 +119,19 @@ static int body_is_gain(const oracle_cfg *c, int64_t k) {
   if (k >= c->n_layers * blk) return 1;               /* g_f */
   const int64_t r = k % blk;
   return r < d || (r >= d + 8 * d * d && r < 2 * d + 8 * d * d);
+}
+
+/* Whether coordinate k is perturbed and updated (cfg.perturb_mask).  The
+ * paper keeps parts of the model out of the search: its decoder/embedding E
+ * is never perturbed and only the body is (Section 4; Appendix E).  For the
+ * stacked LSTM the groups are the embedding (bit 0), the LSTM layers (bit 1)
+ * and the head (bit 2); the body of arch 1 is one group (bit 1).  A masked
+ * coordinate keeps its value in every perturbed forward and in the update. */
+static int coord_perturbed(const oracle_cfg *c, int64_t k) {
+  const uint32_t m = c->perturb_mask ? c->perturb_mask : 7u;
+  if (c->arch == 1) return (int)((m >> 1) & 1u);
+  const int grp = k < (int64_t)VOCAB * c->embed ? 0 : (k < off_layer(c, c->n_layers) ? 1 : 2);
+  return (int)((m >> grp) & 1u);
 }
 
 /* The probe law of coordinate k: under the paper's sparse law its
@@ -561,7 +576,7 @@ void oracle_perturb(const oracle_cfg *c, const float *theta, uint64_t seed, uint
     probe_quad(law_of(c, 4 * q), seed, step, pair, (uint64_t)q, z);
     for (int i = 0; i < 4 && 4 * q + i < d; ++i) {
       int64_t k = 4 * q + i;
-      w_out[k] = fmaf(sign_eps, z[i], theta[k]);
+      w_out[k] = coord_perturbed(c, k) ? fmaf(sign_eps, z[i], theta[k]) : theta[k];
     }
   }
 }
@@ -593,6 +608,11 @@ void oracle_apply_update(const oracle_cfg *c, const float *theta, uint64_t seed,
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i) {
     const int64_t k = ks ? ks[i] : i;
+    if (!coord_perturbed(c, k)) {          /* masked: no estimate, no update */
+      theta_out[i] = theta[k];
+      if (ghat) ghat[i] = 0.0;
+      continue;
+    }
     double g = 0.0;
     for (int j = 0; j < P; ++j) {
       float z[4];
@@ -621,6 +641,13 @@ void oracle_apply_adam(const oracle_cfg *c, const float *theta, const float *m, 
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i) {
     const int64_t k = ks ? ks[i] : i;
+    if (!coord_perturbed(c, k)) {          /* masked: theta and both moments stay */
+      theta_out[i] = theta[k];
+      m_out[i] = m[k];
+      v_out[i] = v[k];
+      if (ghat) ghat[i] = 0.0;
+      continue;
+    }
     double gh = 0.0;
     for (int j = 0; j < P; ++j) {
       float z[4];
@@ -642,21 +669,31 @@ void oracle_apply_adam(const oracle_cfg *c, const float *theta, const float *m, 
  * sampled batches (Appendix E): direction j of the D = A P directions is
  * evaluated on batch j / P, and the estimate averages all D directions,
  *   g_hat = (1/A) sum_a (1/P) sum_{j in batch a} ... = (1/D) sum_j ...
+ * Each expert has its own perturbation radius eps[e] and learning rate
+ * lr[e] (the paper's per-expert schedule, Section 4).
  *   theta   [N][d]   fp32, read only
  *   seeds   [N]      per-expert Philox stream seeds
+ *   eps, lr [N]
  *   bytes   [A][N][B][T]
- *   losses  [N][D][2] out: [e][j][0] = L(theta_e + eps z), [1] = L(theta_e - eps z)
+ *   losses  [N][D][2] out: [e][j][0] = L(theta_e + eps_e z), [1] = L(theta_e - eps_e z)
  *   coef    [N][D]    out (may be NULL): the coefficient applied to z_{e,j}
  *   theta_out [N][d]  out
  *   ghat    [N][d]    out (may be NULL): the estimate, fp64
+ * Coefficients: independent losses c_{e,j} = (L_{e,j,+} - L_{e,j,-}) /
+ * (2 eps_e D) (Section 4, Eq. main-spsa per expert).  Summed loss (Appendix
+ * J): the joint direction perturbs expert e by eps_e z_{e,j}, the shared loss
+ * F = sum_e L_e changes by dF_j = sum_e (L_{e,j,+} - L_{e,j,-}), and Eq.
+ * main-spsa applied to F gives expert e the coefficient dF_j / (2 eps_e D)
+ * (one scalar loss difference shared by every expert, divided by the radius
+ * along that expert's coordinates).
  * Returns 0, or -1 on an invalid configuration. */
-int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *seeds, uint64_t step,
-                     float eps, float lr, const uint8_t *bytes, float *losses, double *coef,
-                     float *theta_out, double *ghat) {
+int oracle_spsa_step_rates(const oracle_cfg *c, const float *theta, const uint64_t *seeds, uint64_t step,
+                           const float *eps, const float *lr, const uint8_t *bytes, float *losses, double *coef,
+                           float *theta_out, double *ghat) {
   const int N = c->n_experts, P = total_dirs(c), Pb = c->n_pairs;
   if (N < 1 || Pb < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
       c->seq_len < 2 || c->probe < 0 || c->probe > 2 || c->accum < 0 || c->arch < 0 || c->arch > 1 ||
-      (c->arch == 1 && (c->embed != c->hidden || !c->tied_head)))
+      c->perturb_mask > 7u || (c->arch == 1 && (c->embed != c->hidden || !c->tied_head)))
     return -1;
   const int64_t d = oracle_param_count(c);
   const size_t bstride = (size_t)c->batch * c->seq_len;
@@ -670,12 +707,11 @@ int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *se
       for (int s = 0; s < 2; ++s)
         L[((size_t)e * P + j) * 2 + s] =
             oracle_perturbed_loss(&ce, theta + (size_t)e * d, seeds[e], step, (uint32_t)j,
-                                  s == 0 ? +1 : -1, eps,
+                                  s == 0 ? +1 : -1, eps[e],
                                   bytes + ((size_t)(j / Pb) * N + e) * bstride);
   }
   /* 5: coefficients. */
   double *cf = (double *)malloc(sizeof(double) * (size_t)N * P);
-  const double denom = 2.0 * (double)eps * (double)P;
   for (int e = 0; e < N; ++e)
     for (int j = 0; j < P; ++j) {
       double diff;
@@ -686,11 +722,11 @@ int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *se
       } else {
         diff = L[((size_t)e * P + j) * 2 + 0] - L[((size_t)e * P + j) * 2 + 1];
       }
-      cf[(size_t)e * P + j] = diff / denom;
+      cf[(size_t)e * P + j] = diff / (2.0 * (double)eps[e] * (double)P);
     }
   /* 6: update. */
   for (int e = 0; e < N; ++e)
-    oracle_apply_update(c, theta + (size_t)e * d, seeds[e], step, lr, cf + (size_t)e * P, NULL, 0,
+    oracle_apply_update(c, theta + (size_t)e * d, seeds[e], step, lr[e], cf + (size_t)e * P, NULL, 0,
                         theta_out + (size_t)e * d, ghat ? ghat + (size_t)e * d : NULL);
   /* 7: outputs. */
   for (size_t i = 0; i < (size_t)N * P * 2; ++i) losses[i] = (float)L[i];
@@ -699,6 +735,22 @@ int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *se
   free(cf);
   free(L);
   return 0;
+}
+
+/* The step with one radius and one learning rate for every expert. */
+int oracle_spsa_step(const oracle_cfg *c, const float *theta, const uint64_t *seeds, uint64_t step,
+                     float eps, float lr, const uint8_t *bytes, float *losses, double *coef,
+                     float *theta_out, double *ghat) {
+  if (c->n_experts < 1) return -1;
+  float *ev = (float *)malloc(sizeof(float) * 2 * (size_t)c->n_experts);
+  for (int e = 0; e < c->n_experts; ++e) {
+    ev[e] = eps;
+    ev[c->n_experts + e] = lr;
+  }
+  const int rc = oracle_spsa_step_rates(c, theta, seeds, step, ev, ev + c->n_experts, bytes, losses, coef,
+                                        theta_out, ghat);
+  free(ev);
+  return rc;
 }
 
 /* Unperturbed mean cross entropy of every expert on its own batch. */
