@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--probe", choices=sorted(PROBE_LAWS), default=None,
                     help="probe law (default: the workload's own): gaussian, sparse (the paper's "
                          "training law: 0 w.p. 1/2, +-1 w.p. 1/4) or dense (+-1)")
+    ap.add_argument("--loss-mode", choices=("independent", "summed"), default=None,
+                    help="coefficients from each expert's own loss (Section 4) or from the summed loss "
+                         "(Appendix J); default: the workload's own")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-kernel HBM bytes from rocprofv3 counter runs (JSON), if present")
@@ -154,6 +157,8 @@ def main():
     w = workloads.ALL[args.workload]
     if args.pairs:
         w = w.with_(n_pairs=args.pairs)
+    if args.loss_mode:
+        w = w.with_(loss_mode=1 if args.loss_mode == "summed" else 0)
     # Inputs are drawn (with a worker pool) before anything touches the GPU.
     tied = None
     if w.arch == 1:   # the paper's width-32 recipe: one frozen tied E shared by every expert
@@ -279,7 +284,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": ("f32 (matrix products as three fp16 products of split fp32 operands, fp32 accumulation)"
+                  if split else "f32"),
         "data": "synthetic: order-2 Markov byte chains, Dirichlet(0.1) rows, one chain per expert",
         "config": {"workload": w.name, "n_experts": w.n_experts, "n_layers": w.n_layers,
                    "embed": w.embed, "hidden": w.hidden, "batch": w.batch, "seq_len": w.seq_len,
@@ -295,6 +301,12 @@ def main():
         "roofline": roof,
         "mean_loss": float(np.mean(lv)),
     }
+    # Deterministic teardown: the context's events and the device buffers are
+    # released while the runtime is alive, not by the interpreter's exit.
+    torch.cuda.synchronize()
+    ctx.close()
+    del ctx, theta, dbatches, losses
+    torch.cuda.synchronize()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, theta0, batches[0], seeds_np, probe, tied)
     print(json.dumps(out), flush=True)

@@ -10,9 +10,10 @@
  *      on the expert's own batch, all directions and both signs sharing it
  *      (Section 4; Appendix E, Eq. localspsa);
  *   3. form the coefficients c_{e,j} = (L_{e,j,+} - L_{e,j,-}) / (2 eps P)
- *      (Section 4, Eq. main-spsa), or in SUMMED mode
- *      c_j = sum_e (L_{e,j,+} - L_{e,j,-}) / (2 eps P) for every expert
- *      (Appendix J, independent vs summed losses);
+ *      (Section 4, Eq. main-spsa), or in SUMMED mode, from the one shared
+ *      loss difference dF_j = sum_e (L_{e,j,+} - L_{e,j,-}),
+ *      c_{e,j} = dF_j / (2 eps P) for every expert (Appendix J, independent
+ *      vs summed losses);
  *   4. apply theta_e <- theta_e - lr * sum_j c_{e,j} z_{e,j}, regenerating
  *      every z_{e,j} from its counter instead of storing it.
  *
@@ -109,6 +110,21 @@ enum soma_flags {
   SOMA_FLAG_TILED_WEIGHTS = 2
 };
 
+/* Parameter groups that soma_config.perturb_mask names.  A masked group
+ * gets neither perturbation nor update: its weights enter every perturbed
+ * forward unchanged and keep their values (and Adam moments) through the
+ * step.  The paper keeps its decoder/embedding E out of the search and
+ * perturbs the body only, which lowers the search dimension (Section 4;
+ * Appendix E); for the stacked LSTM the three groups can be left out in any
+ * combination.  For SOMA_ARCH_BODY theta is one group (SOMA_PERTURB_LSTM),
+ * which the mask must include. */
+enum soma_perturb_group {
+  SOMA_PERTURB_EMBEDDING = 1,  /* Emb[256][E] */
+  SOMA_PERTURB_LSTM = 2,       /* W_1 .. W_L (SOMA_ARCH_BODY: the whole body) */
+  SOMA_PERTURB_HEAD = 4,       /* Whead[256][H] */
+  SOMA_PERTURB_ALL = 7
+};
+
 /* Expert architectures (soma_config.arch). */
 enum soma_arch {
   /* The stacked LSTM with a perturbed byte embedding and an untied linear
@@ -159,6 +175,8 @@ typedef struct soma_config {
   int32_t probe;      /* enum soma_probe_law, 0 (Gaussian) by default */
   int32_t accum;      /* A accumulation batches per update (0 or 1: one batch), see below */
   int32_t arch;       /* enum soma_arch, 0 (stacked LSTM) by default */
+  uint32_t perturb_mask; /* enum soma_perturb_group bits of the perturbed and updated
+                            groups; 0 means SOMA_PERTURB_ALL */
 } soma_config;
 
 typedef struct soma_ctx soma_ctx;
@@ -178,7 +196,13 @@ int soma_create(const soma_config* cfg, void* workspace_dev, size_t workspace_by
 void soma_destroy(soma_ctx* ctx);
 
 /* One SPSA step (Section 4, Eq. main-spsa; Appendix E, Eq. localspsa, with
- * a plain step theta <- theta - lr g_hat in place of Adam).
+ * a plain step theta <- theta - lr g_hat in place of Adam).  This is the
+ * soma_spsa_step(experts, seeds, eps, lr, byte_batches) of the method with
+ * three choices of form: the experts' parameters are one contiguous [N][d]
+ * device array rather than N device pointers, so one launch covers every
+ * expert; the seeds are a device array, so a step enqueues no host-to-device
+ * copy and can be replayed without host work; and the step counter that keys
+ * the probe stream is explicit.
  * Where the shape allows (H <= 512, B <= 64, a device that supports
  * cooperative launches), each layer's recurrence runs as one persistent
  * launch whose blocks synchronise per time step through bounded waits; if a
@@ -267,8 +291,10 @@ int soma_schedule_observe(soma_schedule_entry* sched_dev, int32_t n, const float
 
 /* soma_spsa_step_adam with each expert's eps and lr read from its schedule
  * entry, sched_dev [N] (device).  The coefficients use the expert's own
- * radius, c_{e,j} = (L+ - L-) / (2 eps_e P); in SUMMED mode
- * c_j = sum_e (L_{e,j,+} - L_{e,j,-}) / (2 eps_e P).  A step with an entry
+ * radius, c_{e,j} = (L+ - L-) / (2 eps_e P); in SUMMED mode the joint
+ * direction moves expert e by eps_e z_{e,j}, and Eq. main-spsa applied to the
+ * summed loss gives c_{e,j} = dF_j / (2 eps_e P) with the shared difference
+ * dF_j = sum_e' (L_{e',j,+} - L_{e',j,-}).  A step with an entry
  * whose eps is not finite and > 0 or whose lr is not finite is aborted on the
  * device: its losses read NaN and theta, m and v stay untouched. */
 int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta_dev, float* m_dev, float* v_dev, int64_t t,

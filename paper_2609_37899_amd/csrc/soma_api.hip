@@ -68,6 +68,13 @@ struct Layout {
 // Directions per update: n_pairs per accumulation batch, accum batches.
 int dirs(const soma_config& c) { return c.n_pairs * (c.accum > 1 ? c.accum : 1); }
 
+static_assert(SOMA_PERTURB_EMBEDDING == soma::kGroupEmb && SOMA_PERTURB_LSTM == soma::kGroupLstm &&
+                  SOMA_PERTURB_HEAD == soma::kGroupHead,
+              "the mask bits of the boundary are the kernels' group bits");
+
+// The perturbed parameter groups of a configuration (0 in the config: all).
+unsigned group_mask(const soma_config& c) { return c.perturb_mask ? c.perturb_mask : unsigned(SOMA_PERTURB_ALL); }
+
 int64_t param_count_of(const soma_config& c) {
   if (c.arch == SOMA_ARCH_BODY) return c.n_layers * soma::body_block(c.hidden) + c.hidden;
   int64_t d = int64_t(SOMA_VOCAB) * c.embed;
@@ -99,6 +106,10 @@ int validate(const soma_config* c) {
     return fail(SOMA_EINVAL, "probe must be 0 (Gaussian), 1 (sparse Rademacher) or 2 (Rademacher)");
   if (c->arch != SOMA_ARCH_LSTM && c->arch != SOMA_ARCH_BODY)
     return fail(SOMA_EINVAL, "arch must be 0 (stacked LSTM) or 1 (the paper's body)");
+  if (c->perturb_mask > SOMA_PERTURB_ALL)
+    return fail(SOMA_EINVAL, "perturb_mask must be a combination of SOMA_PERTURB_* bits (got %u)", c->perturb_mask);
+  if (c->arch == SOMA_ARCH_BODY && !(group_mask(*c) & SOMA_PERTURB_LSTM))
+    return fail(SOMA_EINVAL, "the body's parameters are one group: perturb_mask must include SOMA_PERTURB_LSTM");
   if (c->arch == SOMA_ARCH_BODY) {
     if (c->embed != c->hidden || (c->hidden != 16 && c->hidden != 32) || c->n_layers > 2)
       return fail(SOMA_ESHAPE, "the body needs embed = hidden in {16, 32} and n_layers in {1, 2} (got %d, %d, %d)",
@@ -275,9 +286,11 @@ __global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs,
   if (lossd) lossd[o] = tot * inv_rows;
 }
 
-// c[e][j] = (L+ - L-) / (2 eps P) from the fp64 means, rounded once to fp32;
-// summed mode: the differences of all experts added in expert order, the
-// same coefficient for every expert.  It runs once after every direction
+// c[e][j] = (L+ - L-) / (2 eps_e P) from the fp64 means, rounded once to fp32;
+// summed mode: the loss differences of all experts added in expert order
+// (the shared loss difference), divided by expert e's own radius: Eq.
+// main-spsa applied to the summed loss, whose joint direction moves expert e
+// by eps_e z_{e,j}.  It runs once after every direction
 // chunk: if the step was aborted (the flag may have been set in a later
 // chunk than some losses were reduced in), every loss and coefficient of
 // the step reads NaN.
@@ -295,9 +308,9 @@ __global__ void k_coef(const double* lossd, int N, int P, int summed, const floa
   auto inv_denom = [&](int x) { return 1.0 / (2.0 * double(eps_v[int64_t(x) * eps_stride]) * double(P)); };
   double c;
   if (summed) {
-    c = 0.0;
-    for (int e2 = 0; e2 < N; ++e2)
-      c += (lossd[(int64_t(e2) * P + j) * 2] - lossd[(int64_t(e2) * P + j) * 2 + 1]) * inv_denom(e2);
+    double dF = 0.0;   // the shared loss difference sum_e2 (L_{e2,j,+} - L_{e2,j,-})
+    for (int e2 = 0; e2 < N; ++e2) dF += lossd[(int64_t(e2) * P + j) * 2] - lossd[(int64_t(e2) * P + j) * 2 + 1];
+    c = dF * inv_denom(e);
   } else {
     c = (lossd[(int64_t(e) * P + j) * 2] - lossd[(int64_t(e) * P + j) * 2 + 1]) * inv_denom(e);
   }
@@ -331,9 +344,19 @@ __global__ void k_check_rates(const float* eps_v, int eps_stride, const float* l
 struct LawMap {
   int law;
   int layers;
-  int64_t blk;  // parameters per body block; 0: every coordinate has `law`
-  int64_t dm;   // body width
+  int64_t blk;         // parameters per body block; 0: every coordinate has `law`
+  int64_t dm;          // body width
+  int64_t emb_end;     // first coordinate of the LSTM layers (the embedding precedes it)
+  int64_t head_start;  // first coordinate of the head
+  unsigned mask;       // perturbed groups (kGroup* bits)
 };
+
+// Whether the probe quad at coordinate k4 belongs to a perturbed group.
+// Group boundaries are multiples of 4, so a quad never straddles two.
+__device__ __forceinline__ bool quad_perturbed(const LawMap& m, int64_t k4) {
+  const unsigned g = k4 < m.emb_end ? kGroupEmb : (k4 < m.head_start ? kGroupLstm : kGroupHead);
+  return (m.mask & g) != 0u;
+}
 
 __device__ __forceinline__ int law_at(const LawMap& m, int64_t k4) {
   if (m.blk == 0 || m.law != kProbeSparseRademacher) return m.law;
@@ -364,6 +387,7 @@ __global__ __launch_bounds__(256) void k_update(float* theta, const uint64_t* se
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
   if (err && *err) return;   // the step was aborted: theta stays as it was
+  if (!quad_perturbed(lm, 4 * q)) return;   // a masked group: no estimate, no update
   const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
                                    coef + int64_t(e) * P, P, law_at(lm, 4 * q), q);
   const float lr = lr_v[int64_t(e) * lr_stride];
@@ -398,6 +422,7 @@ __global__ __launch_bounds__(256) void k_update_adam(float* theta, float* m, flo
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   if (4 * q >= d) return;
   if (err && *err) return;   // the step was aborted: theta, m, v stay as they were
+  if (!quad_perturbed(lm, 4 * q)) return;   // a masked group: theta, m, v stay as they were
   const float4 acc = estimate_quad(stream_key(seeds[e], step), static_cast<uint32_t>(step),
                                    coef + int64_t(e) * P, P, law_at(lm, 4 * q), q);
   const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
@@ -428,7 +453,7 @@ __global__ __launch_bounds__(256) void k_estimator_moments(const uint64_t* seeds
   const int e = blockIdx.y;
   const int64_t q = blockIdx.x * int64_t(blockDim.x) + threadIdx.x;
   double s0 = 0.0, s1 = 0.0;
-  if (4 * q < d) {
+  if (4 * q < d && quad_perturbed(lm, 4 * q)) {   // masked coordinates have no estimate
     const uint2 key = stream_key(seeds[e], step);
     const uint32_t step_lo = static_cast<uint32_t>(step);
     const float* c = coef + int64_t(e) * D;
@@ -781,6 +806,7 @@ int run_body(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
   a.pcs = pcs;
   a.j0 = j0;
   a.btiles = L.row_tiles;
+  a.err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
   const unsigned blocks = unsigned(L.row_tiles) * unsigned(c.n_experts) * unsigned(pcs) * (kPert ? 2u : 1u);
   const bool wide = c.hidden == 32, deep = c.n_layers == 2;
   if (wide && deep) launch_body_t<2, 2, kPert>(a, blocks, st);
@@ -814,6 +840,8 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   a.step = step;
   a.eps_v = eps_v;
   a.eps_stride = eps_stride;
+  a.pmask = group_mask(c);
+  a.err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
   a.ppb = kPert ? c.n_pairs : 1;
   a.bstride = kPert ? int64_t(c.n_experts) * c.batch * c.seq_len : 0;
   a.probe = c.probe;
@@ -1141,9 +1169,14 @@ int check_state(const float* m, const float* v) {
   return SOMA_OK;
 }
 
-soma::LawMap law_map(const soma_config& c) {
-  soma::LawMap m{c.probe, c.n_layers, 0, c.hidden};
-  if (c.arch == SOMA_ARCH_BODY) m.blk = soma::body_block(c.hidden);
+soma::LawMap law_map(const soma_config& c, const Layout& L) {
+  soma::LawMap m{c.probe, c.n_layers, 0, c.hidden, 0, L.d, group_mask(c)};
+  if (c.arch == SOMA_ARCH_BODY) {
+    m.blk = soma::body_block(c.hidden);   // the whole body is the LSTM group
+  } else {
+    m.emb_end = L.off_layer[0];
+    m.head_start = L.off_head;
+  }
   return m;
 }
 
@@ -1152,7 +1185,7 @@ int launch_sgd(const soma_ctx* ctx, float* theta, const uint64_t* seeds, uint64_
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st, theta,
-                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), law_map(c), err);
+                     seeds, step, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), law_map(c, ctx->lay), err);
   return check_launch("k_update");
 }
 
@@ -1161,7 +1194,7 @@ int launch_adam(const soma_ctx* ctx, float* theta, float* m, float* v, const uin
   const soma_config& c = ctx->cfg;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_update_adam, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
-                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), law_map(c), err);
+                     theta, m, v, seeds, step, h, r.lr_v, r.lr_stride, coef, ctx->lay.d, dirs(c), law_map(c, ctx->lay), err);
   return check_launch("k_update_adam");
 }
 
@@ -1246,7 +1279,7 @@ int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds, uint64_t step, 
   if (int rc = check_launch("k_zero_f64")) return rc;
   const int64_t quads = (ctx->lay.d + 3) / 4;
   hipLaunchKernelGGL(soma::k_estimator_moments, dim3(unsigned((quads + 255) / 256), c.n_experts), dim3(256), 0, st,
-                     seeds, step, coef, ctx->lay.d, D, group, law_map(c), out);
+                     seeds, step, coef, ctx->lay.d, D, group, law_map(c, ctx->lay), out);
   if (int rc = check_launch("k_estimator_moments")) return rc;
   return ok();
 }
@@ -1305,14 +1338,18 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
   const hipStream_t st = as_stream(stream);
   const bool timing = ctx->timing;
   ctx->timing = false;  // evaluation is not part of the step's phase record
+  // The abort flag, set by a kernel that meets a weight outside the range of
+  // its split products, makes the losses NaN.
+  unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
+  hipLaunchKernelGGL(soma::k_zero_u32, dim3(1), dim3(64), 0, st, err, 1);
+  if (int rc = check_launch("k_zero_u32")) return rc;
   const int rc0 = run_forward<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
   ctx->timing = timing;
   if (rc0) return rc0;
   const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
   hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
                      reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1,
-                     1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr),
-                     static_cast<const unsigned*>(nullptr));
+                     1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr), err);
   if (int rc = check_launch("k_loss_reduce")) return rc;
   return ok();
 }
@@ -1347,6 +1384,9 @@ int soma_head_delta(soma_ctx* ctx, const float* theta, const uint8_t* bytes, flo
   const hipStream_t st = as_stream(stream);
   const bool timing = ctx->timing;
   ctx->timing = false;
+  unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
+  hipLaunchKernelGGL(soma::k_zero_u32, dim3(1), dim3(64), 0, st, err, 1);
+  if (int rc = check_launch("k_zero_u32")) return rc;
   const int rc0 = run_body<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
   ctx->timing = timing;
   if (rc0) return rc0;
@@ -1354,7 +1394,7 @@ int soma_head_delta(soma_ctx* ctx, const float* theta, const uint8_t* bytes, flo
   if (loss) {
     hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
                        reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1, 1, 1, 1, 0,
-                       inv_rows, loss, static_cast<double*>(nullptr), static_cast<const unsigned*>(nullptr));
+                       inv_rows, loss, static_cast<double*>(nullptr), err);
     if (int rc = check_launch("k_loss_reduce")) return rc;
   }
   float* dpart = reinterpret_cast<float*>(ctx->ws + L.dpart);

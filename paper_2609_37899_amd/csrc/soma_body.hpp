@@ -70,7 +70,18 @@ struct BodyArgs {
   int ppb;                // directions per accumulation batch
   int64_t bstride;        // bytes per accumulation batch, N B T
   int N, B, T, PC, pcs, j0, btiles;
+  unsigned* err;          // the step's sticky abort flag (a weight out of the split's range sets kAbortRange)
 };
+
+// Ranges the split products need (kSplitMax per operand).  The normalised
+// vector has |n_i| <= sqrt(d - 1) (zero mean, sum of squares <= d), so with
+// every folded matrix weight (gains and gate scales folded in) at most
+// kBodyWeightMax, a GELU input is at most kBodyWeightMax d = 8192 at d = 32,
+// and with |g_f| <= kBodyGainMax the decoder input f = g_f n stays below
+// 4096 sqrt(31) < 23000; h is bounded by 1.  A block that forms a weight
+// outside these bounds (or NaN) aborts the step.
+constexpr float kBodyWeightMax = 256.0f;
+constexpr float kBodyGainMax = 4096.0f;
 
 // Under the paper's sparse law the normalisation gains draw dense +-1
 // (Appendix E); under the other laws they follow the weights.
@@ -335,7 +346,7 @@ template <bool kPert>
 __device__ __forceinline__ void body_fragment(const float* th, int64_t base, int ld, int ncol, int row, int p,
                                               int ln, int64_t kg, int gcol, float scale, int wlaw, int glaw,
                                               uint2 key, uint32_t pair, uint32_t step_lo, float seps, uint4& hi,
-                                              uint4& lo) {
+                                              uint4& lo, float bound, bool& in_range) {
   float w[8];
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
@@ -348,6 +359,7 @@ __device__ __forceinline__ void body_fragment(const float* th, int64_t base, int
         v = make_float4(v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w);
       }
       v = make_float4(v.x * scale, v.y * scale, v.z * scale, v.w * scale);
+      in_range &= split_range_ok(v, bound);
     }
     w[4 * half] = v.x;
     w[4 * half + 1] = v.y;
@@ -398,6 +410,7 @@ __global__ __launch_bounds__(kBodyThreads, 1) void k_body(BodyArgs a) {
 
   // Perturbed weights into LDS as split fragments, gains folded in, gate
   // rows pre-scaled for their nonlinearity.  One (slot, lane) per iteration.
+  bool in_range = true;
   for (int q = threadIdx.x; q < Lds::kSlots * 64; q += kBodyThreads) {
     const int slot = q >> 6, ln = q & 63, r16 = ln & 15;
     uint4 hi, lo;
@@ -409,20 +422,21 @@ __global__ __launch_bounds__(kBodyThreads, 1) void k_body(BodyArgs a) {
         const int mb = r / Lds::kGateKC, p = r % Lds::kGateKC, row = 16 * mb + r16;
         const float scale = row / dm == 2 ? kGateScaleTanh : kGateScaleSig;
         body_fragment<kPert>(th, base + dm, 2 * dm, 2 * dm, row, p, ln, base, dm, scale, wlaw, glaw, key, pair,
-                             step_lo, seps, hi, lo);
+                             step_lo, seps, hi, lo, kBodyWeightMax, in_range);
       } else if (r < Lds::kGate + Lds::kW1) {
         const int mb = r - Lds::kGate, row = 16 * mb + r16;
         body_fragment<kPert>(th, base + 2 * dm + 8 * dm * dm, dm, dm, row, 0, ln, base + dm + 8 * dm * dm, dm, 1.0f,
-                             wlaw, glaw, key, pair, step_lo, seps, hi, lo);
+                             wlaw, glaw, key, pair, step_lo, seps, hi, lo, kBodyWeightMax, in_range);
       } else {
         const int rr = r - Lds::kGate - Lds::kW1, mb = rr / Lds::kW2KC, p = rr % Lds::kW2KC, row = 16 * mb + r16;
         body_fragment<kPert>(th, base + 2 * dm + 12 * dm * dm, 4 * dm, 4 * dm, row, p, ln, 0, 0, 1.0f, wlaw, glaw,
-                             key, pair, step_lo, seps, hi, lo);
+                             key, pair, step_lo, seps, hi, lo, kBodyWeightMax, in_range);
       }
     } else {
       // E (frozen, not perturbed): rows 16 mb + r16, columns as above.
       const int mb = slot - D * Lds::kLayer, row = 16 * mb + r16;
-      body_fragment<false>(Ee, 0, dm, dm, row, 0, ln, 0, 0, 1.0f, 0, 0, key, pair, step_lo, 0.0f, hi, lo);
+      body_fragment<false>(Ee, 0, dm, dm, row, 0, ln, 0, 0, 1.0f, 0, 0, key, pair, step_lo, 0.0f, hi, lo, kSplitMax,
+                           in_range);
     }
     w16[slot * 128 + ln] = hi;
     w16[slot * 128 + 64 + ln] = lo;
@@ -431,8 +445,10 @@ __global__ __launch_bounds__(kBodyThreads, 1) void k_body(BodyArgs a) {
 #pragma unroll
   for (int m = 0; m < DW; ++m) {
     const float4 g = body_weight4<kPert>(th, D * blk + 16 * m + 4 * lg, glaw, key, pair, step_lo, seps);
+    in_range &= split_range_ok(g, kBodyGainMax);
     gf[m] = f32x4{g.x, g.y, g.z, g.w};
   }
+  report_split_range(a.err, in_range);
   __syncthreads();
 
   const int B = a.B, T = a.T;

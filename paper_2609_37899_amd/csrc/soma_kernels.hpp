@@ -81,6 +81,29 @@ __device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_
   lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(r0, r1));
 }
 
+// Range of the split.  hi saturates at 65504, the largest finite fp16 (the
+// conversion rounds toward zero), so an operand is represented only for
+// |x| <= kSplitMax; below 2^-3 lo, and below 2^-14 hi too, fall into fp16's
+// subnormals, whose spacing 2^-24 bounds the absolute error there.  So the
+// split keeps |x - (hi + lo)| <= 2^-21 |x| + 2^-24 for |x| <= kSplitMax: about
+// 21 significant bits from |x| = 2^-3 up, fewer below.  Activations of the
+// stacked LSTM are bounded by 1 (h = o tanh(c)); every kernel that forms a
+// split weight checks it against kSplitMax (NaN included) and aborts the step
+// through the sticky flag (bit kAbortRange) if one is outside.
+constexpr float kSplitMax = 65504.0f;
+constexpr unsigned kAbortRange = 2u;
+
+__device__ __forceinline__ bool split_range_ok(const float4& v, float bound = kSplitMax) {
+  // false for NaN as well
+  return __builtin_fabsf(v.x) <= bound && __builtin_fabsf(v.y) <= bound && __builtin_fabsf(v.z) <= bound &&
+         __builtin_fabsf(v.w) <= bound;
+}
+
+// Sets the step's abort flag if this lane formed a weight outside the range.
+__device__ __forceinline__ void report_split_range(unsigned* err, bool ok) {
+  if (!ok && err) __hip_atomic_fetch_or(err, kAbortRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Four consecutive fp32 values -> 8 bytes of hi parts and 8 bytes of lo parts.
 __device__ __forceinline__ void split4(const float4& v, uint2& hi, uint2& lo) {
   split2(v.x, v.y, hi.x, lo.x);
@@ -211,6 +234,8 @@ struct FwdArgs {
   uint64_t step;
   const float* eps_v;     // perturbation radius of expert e: eps_v[e * eps_stride]
   int eps_stride;
+  unsigned pmask;         // perturbed parameter groups (kGroup* bits; all three when nothing is masked)
+  unsigned* err;          // the step's sticky abort flag (a split weight out of range sets kAbortRange)
   int probe;              // probe law (kProbe*)
   int ppb;                // directions per accumulation batch (direction j reads batch j / ppb)
   int64_t bstride;        // bytes per accumulation batch, N B T
@@ -223,7 +248,15 @@ struct FwdArgs {
   int row_tiles;          // head row tiles per slot
 };
 
-__device__ __forceinline__ float eps_of(const FwdArgs& a, int e) { return a.eps_v[int64_t(e) * a.eps_stride]; }
+// Parameter groups of the stacked LSTM that the perturbation mask names: the
+// embedding, the LSTM layers and the head.  A masked group is formed with
+// radius 0, i.e. theta itself (fma(0, z, theta) == theta for finite z).
+constexpr unsigned kGroupEmb = 1, kGroupLstm = 2, kGroupHead = 4;
+
+// The radius of expert e for the weights of parameter group `group`.
+__device__ __forceinline__ float eps_of(const FwdArgs& a, int e, unsigned group) {
+  return (a.pmask & group) ? a.eps_v[int64_t(e) * a.eps_stride] : 0.0f;
+}
 
 // Expert e's batch [B][T] for direction j0 + jl of the pass (its
 // accumulation batch).
@@ -250,7 +283,8 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
   const int E = a.E, H = a.H;
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
-  const float eps = kPert ? eps_of(a, e) : 0.0f;
+  const float eps_e = kPert ? eps_of(a, e, kGroupEmb) : 0.0f;    // the embedding rows
+  const float eps = kPert ? eps_of(a, e, kGroupLstm) : 0.0f;     // the input columns of W_1
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
   const int prow = mtile * 64 + wave * 16 + lr;
   const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (E + H);
@@ -270,8 +304,8 @@ __global__ __launch_bounds__(kThreads) void k_fold(FwdArgs a) {
       const float4 t4 = *reinterpret_cast<const float4*>(th + kk);
       if (kPert) {
         const float4 z = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk));
-        *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = fma4(eps, z, t4);
-        *reinterpret_cast<float4*>(&es[NS - 1][n][4 * c4]) = fma4(-eps, z, t4);
+        *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = fma4(eps_e, z, t4);
+        *reinterpret_cast<float4*>(&es[NS - 1][n][4 * c4]) = fma4(-eps_e, z, t4);
       } else {
         *reinterpret_cast<float4*>(&es[0][n][4 * c4]) = t4;
       }
@@ -438,7 +472,7 @@ __global__ __launch_bounds__(kThreads) void k_proj(FwdArgs a) {
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   };
   perturbed_mainloop<NS, 1, NBP, kPert>(acc, xs, th, wrow, in, a.probe, key, pair, step_lo,
-        kPert ? eps_of(a, e) : 0.0f, act);
+        kPert ? eps_of(a, e, kGroupLstm) : 0.0f, act);
 
   const int p = mtile * 64 + wave * 16 + 4 * lg;
 #pragma unroll
@@ -495,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void k_rec_step(FwdArgs a) {
                    : make_float4(0.f, 0.f, 0.f, 0.f);
     };
     perturbed_mainloop<NS, 1, NB, kPert>(acc, hs, th, wrow, H, a.probe, key, pair, step_lo,
-        kPert ? eps_of(a, e) : 0.0f, act);
+        kPert ? eps_of(a, e, kGroupLstm) : 0.0f, act);
   }
 
   const int unit = utile * 16 + wave * 4 + lg;
@@ -563,7 +597,7 @@ __global__ __launch_bounds__(kThreads) void k_rec_step_split(FwdArgs a) {
   if (t > 0) {
     const uint2 key = stream_key(a.seeds[e], a.step);
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-    const float eps = eps_of(a, e);
+    const float eps = eps_of(a, e, kGroupLstm);
     const int prow = utile * 64 + wave * 16 + lr;
     const int64_t wrow = a.off_l + static_cast<int64_t>((prow & 3) * H + (prow >> 2)) * (in + H) + in;
     const float* hprev = a.hseq + static_cast<int64_t>(t - 1) * B * H;
@@ -592,6 +626,7 @@ __global__ __launch_bounds__(kThreads) void k_rec_step_split(FwdArgs a) {
         *reinterpret_cast<uint2*>(&hs[buf][s][1][n][4 * c4]) = lo;
       }
     };
+    bool in_range = true;
     gload(0);
     sstore(0);
     __syncthreads();
@@ -604,8 +639,10 @@ __global__ __launch_bounds__(kThreads) void k_rec_step_split(FwdArgs a) {
       const float4 z0 = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk));
       const float4 z1 = probe_quad(a.probe, key, pair, step_lo, static_cast<uint64_t>(kk + 4));
       uint4 wh[NS], wl[NS];
-      split8v(fma4(eps, z0, t0), fma4(eps, z1, t1), wh[0], wl[0]);
-      split8v(fma4(-eps, z0, t0), fma4(-eps, z1, t1), wh[1], wl[1]);
+      const float4 wp0 = fma4(eps, z0, t0), wp1 = fma4(eps, z1, t1), wm0 = fma4(-eps, z0, t0), wm1 = fma4(-eps, z1, t1);
+      in_range &= (split_range_ok(wp0) && split_range_ok(wp1)) && (split_range_ok(wm0) && split_range_ok(wm1));
+      split8v(wp0, wp1, wh[0], wl[0]);
+      split8v(wm0, wm1, wh[1], wl[1]);
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         uint4 bh[NB], bl[NB];
@@ -619,6 +656,7 @@ __global__ __launch_bounds__(kThreads) void k_rec_step_split(FwdArgs a) {
       if (c + 1 < nch) sstore(buf ^ 1);
       __syncthreads();
     }
+    report_split_range(a.err, in_range);
   }
 
   const int unit = utile * 16 + wave * 4 + lg;
@@ -691,7 +729,7 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
                    : make_float4(0.f, 0.f, 0.f, 0.f);
   };
   perturbed_mainloop<NS, 4, NBH, kPert>(acc, xs, th, wrow, H, a.probe, key, pair, step_lo,
-        kPert ? eps_of(a, e) : 0.0f, act);
+        kPert ? eps_of(a, e, kGroupHead) : 0.0f, act);
 
   // Row maxima: lane-local over 16 logits, then across the 4 lane groups.
   float mx[NS][NBH];
@@ -947,7 +985,9 @@ __device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, con
 template <int KC, bool kGateRows, bool kRad, int ZW = kZpiece>
 __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&wl)[KC], float* zs, const float* th,
                                                        int64_t off_l, int ld, int col0, int H, int r0, int law,
-                                                       uint2 key, uint32_t pair, uint32_t step_lo, float seps) {
+                                                       uint2 key, uint32_t pair, uint32_t step_lo, float seps,
+                                                       unsigned* err) {
+  bool in_range = true;
   static_assert(ZW % 32 == 0 && ZW <= kZpiece, "probe pieces of whole chunks");
   constexpr int kPiece = ZW / 32;        // chunks per probe piece
   constexpr int ZLD = ZW + 8;            // scratch row in floats (an odd multiple of 32 bytes)
@@ -976,10 +1016,12 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
         const float* tr = th + wrow + 32 * c + 8 * lg;
         const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
         const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+        in_range = in_range && split_range_ok(w0) && split_range_ok(w1);
         split8v(w0, w1, wh[c], wl[c]);
       }
     }
   }
+  report_split_range(err, in_range);
   __syncthreads();
 }
 
@@ -1028,7 +1070,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     const uint2 key = stream_key(a.seeds[e], a.step);
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
     const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
-    const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+    const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
     const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
     // Gate inputs of layer 1 (folded, per byte value) or of a later layer.
     const __amdgpu_buffer_rsrc_t gbuf =
@@ -1041,7 +1083,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     // and held as split fragments.
     uint4 wh[KC], wl[KC];
     resident_weights_split<KC, true, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H, in, H,
-                                           utile * 128, a.probe, key, pair, step_lo, seps);
+                                           utile * 128, a.probe, key, pair, step_lo, seps, p.err);
     // Rows past the batch compute on whatever follows in the same buffers
     // (finite inputs and h of later rows, possibly being rewritten, or zeros
     // past a buffer's end): a column of the product depends only on the same
@@ -1271,7 +1313,8 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
   const uint2 key = stream_key(a.seeds[e], a.step);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
   const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
-  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+  const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
+  const float seps_emb = sg == 0 ? eps_of(a, e, kGroupEmb) : -eps_of(a, e, kGroupEmb);
   const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, static_cast<uint32_t>(R * H * sizeof(float)));
   const __amdgpu_buffer_rsrc_t bbuf = buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
   auto probe4 = [&](uint64_t kk) {
@@ -1288,6 +1331,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
   // segment are drawn into the LDS scratch at a time.
   uint4 wh[MT][KC], wl[MT][KC];
   uint4 xh[MT][KX > 0 ? KX : 1], xl[MT][KX > 0 ? KX : 1];
+  bool in_range = true;                                 // every split weight within the split's range
   auto canon = [&](int r) { return (r & 3) * H + (r >> 2); };
 #pragma unroll
   for (int rg = 0; rg < G / 128; ++rg) {
@@ -1317,6 +1361,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
           const float gs = gate_scale(lr & 3);
           w0 = make_float4(w0.x * gs, w0.y * gs, w0.z * gs, w0.w * gs);
           w1 = make_float4(w1.x * gs, w1.y * gs, w1.z * gs, w1.w * gs);
+          in_range = in_range && split_range_ok(w0) && split_range_ok(w1);   // the scaled weight is split
           if (seg == 0)
             split8v(w0, w1, wh[m][c], wl[m][c]);
           else
@@ -1331,7 +1376,8 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
     // Emb+-[v][k] = theta[v E + k] +- eps z (canonical offset 0), split.
     for (int q = threadIdx.x; q < kVocab * EW / 4; q += kLocalThreads) {
       const int kk = 4 * q;                             // = v EW + 4 k4
-      const float4 w = fma4(seps, probe4(static_cast<uint64_t>(kk)), *reinterpret_cast<const float4*>(th + kk));
+      const float4 w = fma4(seps_emb, probe4(static_cast<uint64_t>(kk)), *reinterpret_cast<const float4*>(th + kk));
+      in_range &= split_range_ok(w);
       uint2 hi, lo;
       split4(w, hi, lo);
       *reinterpret_cast<uint2*>(&et[kk]) = hi;
@@ -1354,6 +1400,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
     __syncthreads();
   }
 
+  report_split_range(a.err, in_range);
   float cs[MT][NB];
 #pragma unroll
   for (int m = 0; m < MT; ++m)
@@ -1570,7 +1617,7 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_stream(
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = stream_key(a.seeds[e], a.step);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+  const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
   const int unit = mb * 32 + wave * 4 + lg;   // output unit of this lane
   // 32-bit offsets: R 4H floats < 2^31 bytes (host check).
   const __amdgpu_buffer_rsrc_t hbuf =
@@ -1580,7 +1627,7 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_stream(
 
   uint4 wh[KC], wl[KC];
   resident_weights_split<KC, true, kRad, ZW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, a.in_l + H, 0, H,
-                                         mb * 128, a.probe, key, pair, step_lo, seps);
+                                         mb * 128, a.probe, key, pair, step_lo, seps, a.err);
 
   // Ring chunk c covers rows [64 (c / NQ), +64) and k [KW (c % NQ), +KW);
   // rows past R read row R - 1 and are never stored.  h is split into its
@@ -1715,7 +1762,7 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = stream_key(a.seeds[e], a.step);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+  const float seps = sg == 0 ? eps_of(a, e, kGroupHead) : -eps_of(a, e, kGroupHead);
   const int vbase = vh * 128 + wave * 16 + 4 * lg;   // vocabulary rows vbase .. +3 of this lane
   // 32-bit offsets: R H floats < 2^31 bytes (host check).
   const __amdgpu_buffer_rsrc_t hbuf =
@@ -1727,7 +1774,7 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
 
   uint4 wh[KC], wl[KC];
   resident_weights_split<KC, false, kRad, ZW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_head, H, 0, H, vh * 128,
-                                          a.probe, key, pair, step_lo, seps);
+                                          a.probe, key, pair, step_lo, seps, a.err);
 
   const int nchunks = ((R + 63) / 64) * NQ;
   float4 pre[PT];
@@ -1899,7 +1946,7 @@ __global__ __launch_bounds__(kHeadFusedThreads) void k_head_fused(FwdArgs a) {
   const float* th = a.theta + static_cast<int64_t>(e) * a.d;
   const uint2 key = stream_key(a.seeds[e], a.step);
   const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-  const float seps = sg == 0 ? eps_of(a, e) : -eps_of(a, e);
+  const float seps = sg == 0 ? eps_of(a, e, kGroupHead) : -eps_of(a, e, kGroupHead);
   const int vbase = wave * 16 + 4 * lg;       // vocabulary rows vbase .. +3 of this lane
   // 32-bit offsets: R H floats < 2^31 bytes (host check).
   const __amdgpu_buffer_rsrc_t hbuf =
@@ -1909,6 +1956,7 @@ __global__ __launch_bounds__(kHeadFusedThreads) void k_head_fused(FwdArgs a) {
   // Whead+- rows 16 wave + lr, drawn 128 rows (one vocabulary half) at a time.
   uint4 wh[KC], wl[KC];
   float l1 = 0.0f;                            // this lane's part of its row's L1 norm
+  bool in_range = true;
   if (threadIdx.x == 0) wide = 0u;
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
@@ -1928,12 +1976,14 @@ __global__ __launch_bounds__(kHeadFusedThreads) void k_head_fused(FwdArgs a) {
         const float* zr = &zs[(row - 128 * half) * ZLD + 32 * c + 8 * lg];
         const float4 w0 = fma4(seps, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr + 32 * c + 8 * lg));
         const float4 w1 = fma4(seps, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 32 * c + 8 * lg + 4));
+        in_range = in_range && split_range_ok(w0) && split_range_ok(w1);
         split8v(w0, w1, wh[c], wl[c]);
         l1 += ((fabsf(w0.x) + fabsf(w0.y)) + (fabsf(w0.z) + fabsf(w0.w))) +
               ((fabsf(w1.x) + fabsf(w1.y)) + (fabsf(w1.z) + fabsf(w1.w)));
       }
     }
   }
+  report_split_range(a.err, in_range);
   if (group4_sum(l1) >= kNoShiftL1) wide = 1u;
   __syncthreads();                            // the scratch becomes the ring
   // |h| <= 1, so |logit_v| <= ||Whead+-[v]||_1: below kNoShiftL1 for every v,

@@ -19,6 +19,7 @@ PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
 ARCH_LSTM, ARCH_BODY = 0, 1
+PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD, PERTURB_ALL = 1, 2, 4, 7
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
            "soma_spsa_step", "soma_spsa_step_adam", "soma_eval_loss", "soma_coefficients",
@@ -69,7 +70,7 @@ SCHEDULE_ENTRY_BYTES = 16   # soma_schedule_entry: lr, eps, best (fp32), since (
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_experts", "n_layers", "embed", "hidden", "batch", "seq_len", "n_pairs", "loss_mode",
-        "pair_chunk", "flags", "probe", "accum", "arch")]
+        "pair_chunk", "flags", "probe", "accum", "arch")] + [("perturb_mask", ctypes.c_uint32)]
 
 
 _lib = None
@@ -160,11 +161,12 @@ class Shape:
     probe: int = PROBE_GAUSSIAN
     accum: int = 1
     arch: int = ARCH_LSTM
+    perturb_mask: int = 0        # PERTURB_* bits of the perturbed groups; 0 = all
 
     def cfg(self) -> Config:
         return Config(self.n_experts, self.n_layers, self.embed, self.hidden, self.batch,
                       self.seq_len, self.n_pairs, self.loss_mode, self.pair_chunk, self.flags,
-                      self.probe, self.accum, self.arch)
+                      self.probe, self.accum, self.arch, self.perturb_mask)
 
     @property
     def directions(self) -> int:

@@ -65,7 +65,7 @@ def test_workspace_size_and_auto_chunk(lib):
     ("embed", 24, soma.SOMA_ESHAPE), ("hidden", 0, soma.SOMA_ESHAPE), ("seq_len", 1, soma.SOMA_ESHAPE),
     ("n_pairs", 0, soma.SOMA_ESHAPE), ("loss_mode", 2, soma.SOMA_EINVAL),
     ("pair_chunk", 99, soma.SOMA_ESHAPE), ("flags", 4, soma.SOMA_EINVAL), ("probe", 3, soma.SOMA_EINVAL),
-    ("probe", -1, soma.SOMA_EINVAL), ("accum", -1, soma.SOMA_ESHAPE)])
+    ("probe", -1, soma.SOMA_EINVAL), ("accum", -1, soma.SOMA_ESHAPE), ("perturb_mask", 8, soma.SOMA_EINVAL)])
 def test_invalid_shapes_are_rejected(lib, field, value, code):
     s = shape_of(workloads.TINY)
     cfg = s.cfg()
@@ -73,6 +73,21 @@ def test_invalid_shapes_are_rejected(lib, field, value, code):
     out = ctypes.c_size_t()
     assert lib.soma_workspace_size(ctypes.byref(cfg), ctypes.byref(out)) == code
     assert lib.soma_last_error()
+
+
+def test_perturb_mask_is_checked(lib):
+    """Any combination of the three groups is accepted for the stacked LSTM
+    (0 meaning all); the body's parameters are one group, which a mask must
+    include."""
+    out = ctypes.c_size_t()
+    for mask in range(8):
+        cfg = shape_of(workloads.TINY, perturb_mask=mask).cfg()
+        assert lib.soma_workspace_size(ctypes.byref(cfg), ctypes.byref(out)) == soma.SOMA_OK
+    body = workloads.PAPER_BODY_N8
+    for mask, code in ((0, soma.SOMA_OK), (soma.PERTURB_LSTM, soma.SOMA_OK), (soma.PERTURB_ALL, soma.SOMA_OK),
+                       (soma.PERTURB_EMBEDDING | soma.PERTURB_HEAD, soma.SOMA_EINVAL)):
+        cfg = shape_of(body, perturb_mask=mask).cfg()
+        assert lib.soma_workspace_size(ctypes.byref(cfg), ctypes.byref(out)) == code
 
 
 def test_create_checks_workspace(lib):

@@ -1,66 +1,117 @@
 """Full-size parity in the benchmark's launch configuration.
 
 At these sizes the oracle cannot run a whole step in seconds, so the test
-compares sampled outputs it can compute one by one: individual perturbed
-losses L(theta_e +- eps z_{e,j}) at the workload's full B and T.  Properties
-that hold at any size are checked on the whole output: every loss is finite
-and near ln 256 at initialisation, separability holds bit for bit, and the
-step leaves the experts of independent runs identical where their inputs are.
+compares outputs it can compute one by one: individual perturbed losses
+L(theta_e +- eps z_{e,j}) at the workload's full B and T, the coefficients of
+the directions whose both signs it evaluated, and updated weights at sampled
+coordinates.  Properties that hold at any size are checked on the whole
+output: every loss is finite and near ln 256 at initialisation, separability
+holds bit for bit, and the summed-loss step shares the independent step's
+forwards bit for bit.
+
+Updated weights.  theta'_k = theta_k - lr sum_j c_j z_{j,k} needs every
+coefficient of the expert.  Where the oracle can evaluate all of an expert's
+directions in seconds (the N=256 workload's small experts) it supplies all
+of them and the comparison is the oracle's alone.  For the larger experts it
+evaluates a sample of directions (both signs): those coefficients are the
+oracle's, the rest are the step's own (soma_coefficients), and theta' at
+sampled coordinates is compared with oracle.apply_update fed that mix.
 """
 import gc
 
 import numpy as np
 import pytest
 
-from gpu_common import assert_losses_close, require_gpu
+from gpu_common import assert_losses_close, assert_theta_close, require_gpu
 from paper_2609_37899_amd import soma, synth, workloads
 
 pytestmark = pytest.mark.gpu
 
-SAMPLES = {   # (expert, direction, sign) checked against the oracle
-    "soma_n2_l2_h512": [(0, 0, 0), (1, 31, 1)],
-    "soma_n4_l2_h384": [(0, 5, 1), (3, 31, 0)],
-    "monolith_l2_h704": [(0, 127, 0), (0, 60, 1)],   # 128 directions: the last chunk is ragged
-    "soma_n256_l1_h64": [(0, 0, 0), (255, 31, 1), (131, 7, 0)],
+# (expert, direction) pairs evaluated at both signs.  N=2: jobs 0..15 are
+# (expert 0, directions 0..7, both signs), one job in each of the 16
+# persistent groups (groups take jobs round-robin).
+SAMPLES = {
+    "soma_n2_l2_h512": [(0, j) for j in range(8)] + [(1, 31)],
+    "soma_n4_l2_h384": [(0, 5), (3, 31)],
+    "monolith_l2_h704": [(0, 127), (0, 60)],
+    "soma_n256_l1_h64": [(0, 0), (255, 31), (131, 7)],
 }
+# Experts whose every coefficient the oracle supplies (all directions).
+FULL_EXPERTS = {"soma_n256_l1_h64": (0, 131)}
 
 
-def run_full(w, data=None):
+def shape_of(w, **kw):
+    args = dict(loss_mode=w.loss_mode)
+    args.update(kw)
+    return soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
+                      args.pop("loss_mode"), 0, **args)
+
+
+def run_full(w, data=None, shape=None):
     torch = require_gpu()
-    shape = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
-                       w.loss_mode, 0)
+    shape = shape or shape_of(w)
     theta = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
     if data is None:
         data = synth.expert_batches_in_child(w.cluster_seeds, w.batch, w.seq_len, pool=w.pool_clusters)
     seeds = synth.expert_seeds(w.n_experts)
     ctx = soma.Context(shape)
     th = torch.from_numpy(theta.copy()).cuda()
-    losses = torch.zeros((w.n_experts, w.n_pairs, 2), dtype=torch.float32, device="cuda")
+    D = shape.directions
+    losses = torch.zeros((w.n_experts, D, 2), dtype=torch.float32, device="cuda")
     ctx.spsa_step(th, soma.seeds_tensor(seeds), 0, w.eps, w.lr, torch.from_numpy(data).cuda(), losses)
+    coef = torch.zeros((w.n_experts, D), dtype=torch.float32, device="cuda")
+    ctx.coefficients(coef)
     torch.cuda.synchronize()
-    out = dict(theta0=theta, data=data, seeds=seeds, theta=th.cpu().numpy(), losses=losses.cpu().numpy())
-    del ctx, th, losses
+    out = dict(theta0=theta, data=data, seeds=seeds, theta=th.cpu().numpy(), losses=losses.cpu().numpy(),
+               coef=coef.cpu().numpy())
+    ctx.close()
+    del ctx, th, losses, coef
     gc.collect()
     torch.cuda.empty_cache()
     return out
 
 
+def oracle_pair(oracle_mod, cfg, r, w, e, j):
+    """L(theta_e + eps z_{e,j}) and L(theta_e - eps z_{e,j}) by the oracle."""
+    print(f"{w.name}: oracle forwards e={e} j={j}", flush=True)
+    return [oracle_mod.perturbed_loss(cfg, r["theta0"][e], int(r["seeds"][e]), 0, j, s, w.eps, r["data"][e])
+            for s in (+1, -1)]
+
+
 @pytest.mark.parametrize("wname", list(SAMPLES))
-def test_full_size_sampled_losses(oracle_mod, wname):
+def test_full_size_sampled_losses_and_update(oracle_mod, wname):
     w = workloads.ALL[wname]
     r = run_full(w)
     L = r["losses"]
     assert np.all(np.isfinite(L))
     assert np.all(np.abs(L - np.log(256.0)) < 0.1)
     cfg = oracle_mod.cfg_from(w)
+    P = w.n_pairs
+    denom = 2.0 * np.float64(np.float32(w.eps)) * P
+    coef_mix = r["coef"].astype(np.float64)
     got, ref = [], []
-    for (e, j, s) in SAMPLES[wname]:
-        print(f"{wname}: oracle forward e={e} j={j} sign={'+-'[s]}", flush=True)
-        ref.append(oracle_mod.perturbed_loss(cfg, r["theta0"][e], int(r["seeds"][e]), 0, j,
-                                             +1 if s == 0 else -1, w.eps, r["data"][e]))
-        got.append(L[e, j, s])
+    for (e, j) in SAMPLES[wname]:
+        lp, lm = oracle_pair(oracle_mod, cfg, r, w, e, j)
+        got += [L[e, j, 0], L[e, j, 1]]
+        ref += [lp, lm]
+        coef_mix[e, j] = (lp - lm) / denom
     err = assert_losses_close(got, ref)
-    print(f"{wname}: sampled loss rel err {err:.2e}")
+    cerr = np.max(np.abs(coef_mix - r["coef"]) / np.abs(coef_mix).max(axis=1, keepdims=True))
+    print(f"{wname}: {len(got)} sampled losses, rel err {err:.2e}; sampled coefficients rel {cerr:.2e}")
+    assert cerr <= 2e-2
+    d = r["theta0"].shape[1]
+    ks = np.random.default_rng(0).choice(d, 3000, replace=False)
+    full = FULL_EXPERTS.get(wname, ())
+    for e in full:
+        for j in range(P):
+            lp, lm = [oracle_mod.perturbed_loss(cfg, r["theta0"][e], int(r["seeds"][e]), 0, j, s, w.eps,
+                                                r["data"][e]) for s in (+1, -1)]
+            coef_mix[e, j] = (lp - lm) / denom
+    for e in sorted({e for (e, _) in SAMPLES[wname]} | set(full)):
+        want = oracle_mod.apply_update(cfg, r["theta0"][e], int(r["seeds"][e]), 0, w.lr, coef_mix[e], ks)
+        terr = assert_theta_close(r["theta"][e][ks], want)
+        kind = "oracle coefficients only" if e in full else "oracle coefficients for the sampled directions"
+        print(f"{wname}: expert {e} theta' at {ks.size} coordinates ({kind}): rel {terr:.2e}")
     assert not np.array_equal(r["theta"], r["theta0"])
 
 
@@ -74,3 +125,65 @@ def test_full_size_separability_bit_identity():
     assert np.array_equal(a["theta"][0], b["theta"][0])
     assert np.array_equal(a["losses"][0], b["losses"][0])
     assert not np.array_equal(a["theta"][1], b["theta"][1])
+
+
+def test_full_size_summed_loss_shares_the_forwards(oracle_mod):
+    """The N=4 workload with the summed loss (Appendix J) on the same seeds
+    and data as the independent run: the losses are the same forwards, bit
+    for bit; every expert's coefficient is the shared loss difference over
+    2 eps P, i.e. the sum over experts of the independent coefficients; a
+    sampled loss and updated weights at sampled coordinates against the
+    oracle."""
+    w = workloads.SOMA_N4
+    data = synth.expert_batches_in_child(w.cluster_seeds, w.batch, w.seq_len)
+    ind = run_full(w, data)
+    summ = run_full(w, data, shape_of(w, loss_mode=1))
+    assert np.array_equal(ind["losses"], summ["losses"])
+    total = ind["coef"].astype(np.float64).sum(axis=0)
+    scale = np.abs(total).max()
+    for e in range(w.n_experts):
+        # each side rounds its fp64 coefficients to fp32 once
+        assert np.abs(summ["coef"][e] - total).max() <= 4 * np.spacing(np.float32(scale)) * w.n_experts
+    cfg = oracle_mod.cfg_from(w.with_(loss_mode=1))
+    lp, lm = oracle_pair(oracle_mod, cfg, summ, w, 2, 17)
+    assert_losses_close([summ["losses"][2, 17, 0], summ["losses"][2, 17, 1]], [lp, lm])
+    ks = np.random.default_rng(1).choice(summ["theta0"].shape[1], 3000, replace=False)
+    for e in (0, 3):
+        want = oracle_mod.apply_update(cfg, summ["theta0"][e], int(summ["seeds"][e]), 0, w.lr,
+                                       summ["coef"][e].astype(np.float64), ks)
+        assert_theta_close(summ["theta"][e][ks], want)
+    assert not np.array_equal(summ["theta"], ind["theta"])
+
+
+def auto_chunk(shape, budget=64 * 2 ** 30):
+    """The direction chunk the library picks (the largest whose workspace
+    fits the 64 GiB budget), found from soma_workspace_size."""
+    pc = shape.directions
+    while pc > 1 and soma.workspace_size(soma.Shape(**{**shape.__dict__, "pair_chunk": pc})) > budget:
+        pc -= 1
+    return pc
+
+
+def test_full_size_monolith_1024_perturbations(oracle_mod):
+    """The monolith at 1,024 perturbed forwards (512 directions), in the
+    automatic chunking the benchmark uses: the last chunk is ragged; sampled
+    losses in the first and the last chunk against the oracle."""
+    w = workloads.MONOLITH.with_(n_pairs=512)
+    shape = shape_of(w)
+    pc = auto_chunk(shape)
+    assert w.n_pairs % pc != 0, pc
+    last0 = (w.n_pairs // pc) * pc
+    print(f"{w.name} P=512: chunks of {pc}, the last of {w.n_pairs - last0}", flush=True)
+    r = run_full(w, shape=shape)
+    L = r["losses"]
+    assert np.all(np.isfinite(L)) and np.all(np.abs(L - np.log(256.0)) < 0.1)
+    cfg = oracle_mod.cfg_from(w)
+    got, ref = [], []
+    for (j, s) in ((0, 0), (last0, 1), (511, 0)):
+        print(f"{w.name}: oracle forward j={j} sign={'+-'[s]}", flush=True)
+        ref.append(oracle_mod.perturbed_loss(cfg, r["theta0"][0], int(r["seeds"][0]), 0, j, 1 - 2 * s, w.eps,
+                                             r["data"][0]))
+        got.append(L[0, j, s])
+    err = assert_losses_close(got, ref)
+    print(f"{w.name} P=512: sampled loss rel err {err:.2e}")
+    assert not np.array_equal(r["theta"], r["theta0"])

@@ -1,0 +1,191 @@
+"""GPU parity of the perturbation mask (soma_config.perturb_mask) against the
+oracle, on every kernel that forms or updates weights, and of the range
+guard of the split products.
+
+The paper keeps parts of the model out of the search (its E is never
+perturbed; Section 4, Appendix E).  Masked groups enter every perturbed
+forward unchanged and keep their values, and their Adam moments, through the
+step; the unmasked ones follow the oracle's step at the 1e-4 bar.
+"""
+import numpy as np
+import pytest
+
+from gpu_common import assert_losses_close, assert_theta_close, require_gpu
+from paper_2609_37899_amd import soma, synth
+
+pytestmark = pytest.mark.gpu
+EMB, LSTM, HEAD = soma.PERTURB_EMBEDDING, soma.PERTURB_LSTM, soma.PERTURB_HEAD
+
+# name: (N, L, E, H, B, T, P, eps, lr, pair_chunk) -- the kernels each shape selects
+SHAPES = {
+    "tiny": (1, 1, 32, 64, 8, 64, 4, 1e-3, 1e-2, 0),          # one block per job, embedding in the block, one-pass head
+    "h64_b20": (1, 1, 48, 64, 20, 13, 2, 1e-3, 1e-2, 0),      # fold, one block per job
+    "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 2),    # fold, persistent recurrence, streaming projection
+    "ragged_l2": (2, 2, 48, 32, 20, 37, 3, 1e-3, 1e-2, 2),    # tiled kernels (H = 32)
+    "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0),     # per-step split recurrence, streaming head
+    "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0),     # persistent, streaming head (H > 128)
+}
+
+
+def groups(N, L, E, H):
+    d = 256 * E + sum(4 * H * ((E if l == 0 else H) + H) for l in range(L)) + 256 * H
+    return {EMB: np.arange(0, 256 * E), LSTM: np.arange(256 * E, d - 256 * H), HEAD: np.arange(d - 256 * H, d)}, d
+
+
+def run(name, mask, probe=0, flags=0):
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, pc = SHAPES[name]
+    shape = soma.Shape(N, L, E, H, B, T, P, 0, pc, flags, probe, perturb_mask=mask)
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = synth.expert_seeds(N)
+    ctx = soma.Context(shape)
+    th = torch.from_numpy(theta.copy()).cuda()
+    losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+    ctx.spsa_step(th, soma.seeds_tensor(seeds), 0, eps, lr, torch.from_numpy(data).cuda(), losses)
+    torch.cuda.synchronize()
+    out = dict(theta0=theta, data=data, seeds=seeds, theta=th.cpu().numpy(), losses=losses.cpu().numpy(),
+               shape=shape, eps=eps, lr=lr)
+    ctx.close()
+    return out
+
+
+@pytest.mark.parametrize("name,mask,probe", [
+    ("tiny", LSTM, 0), ("tiny", EMB | HEAD, 1), ("h64_b20", HEAD, 0), ("h64_b20", EMB, 2),
+    ("b64_h128", LSTM, 0), ("b64_h128", EMB | LSTM, 1), ("ragged_l2", LSTM | HEAD, 0), ("ragged_l2", EMB, 0),
+    ("h704_b12", LSTM, 0), ("b40_h384", HEAD, 0)])
+def test_masked_step_matches_oracle(oracle_mod, name, mask, probe):
+    r = run(name, mask, probe)
+    o = oracle_mod.spsa_step(oracle_mod.cfg_from(r["shape"]), r["theta0"], r["seeds"], 0, r["eps"], r["lr"],
+                             r["data"])
+    lerr = assert_losses_close(r["losses"], o["losses"])
+    terr = assert_theta_close(r["theta"], o["theta"])
+    N, L, E, H = r["shape"].n_experts, r["shape"].n_layers, r["shape"].embed, r["shape"].hidden
+    grp, d = groups(N, L, E, H)
+    on = np.concatenate([grp[b] for b in (EMB, LSTM, HEAD) if mask & b])
+    off = np.setdiff1d(np.arange(d), on)
+    assert np.array_equal(r["theta"][:, off], r["theta0"][:, off])      # masked: bit for bit
+    assert not np.array_equal(r["theta"][:, on], r["theta0"][:, on])
+    print(f"{name} mask {mask} law {probe}: loss rel {lerr:.2e}  theta rel {terr:.2e}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64_h128"])
+def test_fully_masked_lstm_equals_frozen_layers(name):
+    """With the LSTM group masked, the fp32-product reference kernels and the
+    split-product kernels see the same unperturbed recurrent weights: the
+    losses of the per-step fp32 path and the default path agree to the
+    split's rounding."""
+    a = run(name, EMB | HEAD)
+    b = run(name, EMB | HEAD, flags=soma.FLAG_PER_STEP_RECURRENCE | soma.FLAG_TILED_WEIGHTS)
+    rel = np.abs(a["losses"].astype(np.float64) - b["losses"]) / np.abs(b["losses"])
+    assert rel.max() <= 1e-5, rel.max()
+
+
+def test_masked_adam_keeps_the_moments(oracle_mod):
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, pc = SHAPES["b64_h128"]
+    mask = LSTM
+    shape = soma.Shape(N, L, E, H, B, T, P, 0, pc, perturb_mask=mask)
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = synth.expert_seeds(N)
+    ctx = soma.Context(shape)
+    th = torch.from_numpy(theta.copy()).cuda()
+    m = torch.full_like(th, 0.25)
+    v = torch.full_like(th, 0.5)
+    losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+    ctx.spsa_step_adam(th, m, v, 2, soma.Adam(), soma.seeds_tensor(seeds), 0, eps, lr, torch.from_numpy(data).cuda(),
+                       losses)
+    torch.cuda.synchronize()
+    grp, d = groups(N, L, E, H)
+    off = np.concatenate([grp[EMB], grp[HEAD]])
+    got_t, got_m, got_v = th.cpu().numpy(), m.cpu().numpy(), v.cpu().numpy()
+    assert np.array_equal(got_t[:, off], theta[:, off])
+    assert np.all(got_m[:, off] == 0.25) and np.all(got_v[:, off] == 0.5)
+    assert not np.any(got_m[:, grp[LSTM]] == 0.25)
+    o = oracle_mod.spsa_step(oracle_mod.cfg_from(shape), theta, seeds, 0, eps, lr, data)
+    assert_losses_close(losses.cpu().numpy(), o["losses"])
+    ctx.close()
+
+
+def test_masked_estimator_moments_skip_masked_coordinates(oracle_mod):
+    """The variance harness sums only over perturbed coordinates: with the
+    head masked its moments equal numpy's over the other coordinates."""
+    torch = require_gpu()
+    N, L, E, H, B, T = 1, 1, 32, 64, 8, 16
+    D, G = 8, 2
+    mask = EMB | LSTM
+    shape = soma.Shape(N, L, E, H, B, T, D, perturb_mask=mask)
+    seeds = synth.expert_seeds(1)
+    coef = (np.random.default_rng(3).standard_normal((1, D)) * 1e-2).astype(np.float32)
+    ctx = soma.Context(shape)
+    out = torch.zeros((1, 2), dtype=torch.float64, device="cuda")
+    ctx.estimator_moments(soma.seeds_tensor(seeds), 2, torch.from_numpy(coef).cuda(), D // G, out)
+    torch.cuda.synchronize()
+    grp, d = groups(N, L, E, H)
+    keep = np.concatenate([grp[EMB], grp[LSTM]])
+    X = np.stack([D * np.float64(coef[0, j]) * oracle_mod.probe(0, int(seeds[0]), 2, j, 0, d).astype(np.float64)
+                  for j in range(D)])[:, keep]
+    s0 = np.sum(X.reshape(G, D // G, keep.size).sum(axis=1) ** 2)
+    s1 = np.sum(X.sum(axis=0) ** 2)
+    np.testing.assert_allclose(out.cpu().numpy()[0], [s0, s1], rtol=1e-12)
+    ctx.close()
+
+
+# ---------------------------------------------------------------------------
+# Range of the split products: every operand is represented to about 2^-21
+# relative from |x| = 2^-3 up to 65504, and to 2^-24 absolute below; the
+# parity bar holds with every weight scaled down or up by 100, and a weight
+# beyond the range aborts the step.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "b64_h128", "b40_h384", "h704_b12"])
+@pytest.mark.parametrize("scale", [1e-2, 1e2])
+def test_scaled_weights_match_oracle(oracle_mod, name, scale):
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, pc = SHAPES[name]
+    shape = soma.Shape(N, L, E, H, B, T, P, 0, pc)
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True) * np.float32(scale)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = synth.expert_seeds(N)
+    e_rel = eps * scale            # the radius scales with the weights
+    ctx = soma.Context(shape)
+    th = torch.from_numpy(theta.copy()).cuda()
+    losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+    ctx.spsa_step(th, soma.seeds_tensor(seeds), 0, e_rel, lr * scale, torch.from_numpy(data).cuda(), losses)
+    torch.cuda.synchronize()
+    o = oracle_mod.spsa_step(oracle_mod.cfg_from(shape), theta, seeds, 0, e_rel, lr * scale, data)
+    lerr = assert_losses_close(losses.cpu().numpy(), o["losses"])
+    terr = assert_theta_close(th.cpu().numpy(), o["theta"])
+    print(f"{name} weights x{scale:g}: loss {float(o['losses'].mean()):.4f}, rel {lerr:.2e}  theta rel {terr:.2e}")
+    ctx.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "b64_h128", "h704_b12"])
+def test_weight_beyond_the_split_range_aborts_the_step(name):
+    """One recurrent weight set to 1e5 on the host (beyond 65504): the kernel
+    that forms it reports it, the losses read NaN and theta is untouched;
+    the same weight at 2e4 is within range for every kernel (the H = 64
+    kernel splits it multiplied by its gate scale, at most 2 log2 e) and the
+    step runs."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, pc = SHAPES[name]
+    shape = soma.Shape(N, L, E, H, B, T, P, 0, pc)
+    base = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    k = 256 * E + (4 * H) * (E + H) // 2 + E + 3        # a recurrent column of W_1
+    data = torch.from_numpy(synth.expert_batches([100 + e for e in range(N)], B, T)).cuda()
+    seeds = soma.seeds_tensor(synth.expert_seeds(N))
+    for value, aborted in ((1e5, True), (2e4, False)):
+        theta = base.copy()
+        theta[0, k] = value
+        ctx = soma.Context(shape)
+        th = torch.from_numpy(theta.copy()).cuda()
+        losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+        ctx.spsa_step(th, seeds, 0, eps, lr, data, losses)
+        torch.cuda.synchronize()
+        if aborted:
+            assert torch.isnan(losses).all()
+            assert np.array_equal(th.cpu().numpy(), theta)
+        else:
+            assert torch.isfinite(losses).all()
+            assert not np.array_equal(th.cpu().numpy(), theta)
+        ctx.close()

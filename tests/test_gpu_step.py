@@ -267,46 +267,83 @@ def test_streaming_and_tiled_weights_agree(name, probe):
     assert_theta_close(t0, t1)
 
 
-@pytest.mark.parametrize("name,probe", [("ragged_l2", 1), ("b64_h128", 0)])
+def seeded_moments(ghat, seed=7):
+    """Adam moments for a whole-step comparison: m ~ N(0, rms(g_hat)/10),
+    v ~ U(0.5, 1.5) 30 mean(g_hat^2) (as after earlier, larger estimates).
+    With v above g_hat^2 the update lr m_hat / (sqrt(v_hat) + delta) is smooth
+    in g_hat (unlike the first step from zero moments, lr sign(g)), so the
+    GPU's estimate, which differs from the oracle's by the fp32 noise in
+    L+ - L-, gives theta' within the parity bar of the oracle's own step
+    (checked on the CPU: coefficients off by 2e-2 of their largest value move
+    theta' by at most 8e-5 of the bar's scale), while the update itself is
+    about 3e-3 of theta, 30 times the bar."""
+    rng = np.random.default_rng(seed)
+    g2 = float(np.mean(ghat ** 2))
+    m = (rng.standard_normal(ghat.shape) * 0.1 * np.sqrt(g2)).astype(np.float32)
+    v = (rng.uniform(0.5, 1.5, ghat.shape) * 30.0 * g2).astype(np.float32)
+    return m, v
+
+
+def adam_oracle_step(oracle_mod, cfg, theta, seeds, step, eps, lr, data, m0, v0, t, adam):
+    """The oracle's whole Adam step: its own forwards and coefficients, then
+    its Adam update from (m0, v0) -- nothing from the GPU."""
+    o = oracle_mod.spsa_step(cfg, theta, seeds, step, eps, lr, data)
+    hp = dict(beta1=float(adam.beta1), beta2=float(adam.beta2), delta=float(adam.delta),
+              weight_decay=float(adam.weight_decay))
+    outs = [oracle_mod.apply_adam(cfg, theta[e], m0[e], v0[e], t, int(seeds[e]), step,
+                                  float(np.float32(np.broadcast_to(lr, (len(seeds),))[e])), o["coef"][e], **hp)
+            for e in range(len(seeds))]
+    return o, [np.stack([x[i] for x in outs]) for i in range(3)]
+
+
+def assert_moments_close(got, ref, scale, rtol=2e-2):
+    """Adam moments carry the estimate itself, whose GPU-vs-oracle difference
+    is the fp32 forward noise in L+ - L- (coefficients agree to ~1e-3..2e-2 of
+    their largest value), so they are held to that bar relative to the
+    moment's scale; theta' is held to the 1e-4 parity bar."""
+    err = np.abs(np.asarray(got, np.float64) - ref).max() / scale
+    assert err <= rtol, err
+    return err
+
+
+@pytest.mark.parametrize("name,probe", [("ragged_l2", 1), ("b64_h128", 0), ("tiny", 0)])
 def test_adam_step_matches_oracle(oracle_mod, name, probe):
-    """A whole step with the Adam-style update from zero moments: losses and
-    coefficients against the oracle's step; theta', m', v' against the
-    oracle's update applied to the GPU's coefficients (so that fp32 forward
-    noise in L+ - L- does not enter the comparison of the update)."""
-    from test_gpu_update import _adam_compare
+    """A whole step with the Adam-style update (update number 3, seeded
+    moments) against the oracle's whole step: losses, coefficients and theta'
+    at the parity bar, the moments at the coefficients' bar."""
     torch = require_gpu()
     N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
     shape = soma.Shape(N, L, E, H, B, T, P, mode, pc, probe=probe)
     theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
     data = synth.expert_batches([100 + e for e in range(N)], B, T)
     seeds = synth.expert_seeds(N)
+    cfg = oracle_mod.cfg_from(shape)
+    ghat = oracle_mod.spsa_step(cfg, theta, seeds, 0, eps, lr, data, want_ghat=True)["ghat"]
+    m0, v0 = seeded_moments(ghat)
     adam = soma.Adam()
     ctx = soma.Context(shape)
     th = torch.from_numpy(theta.copy()).cuda()
-    m = torch.zeros_like(th)
-    v = torch.zeros_like(th)
+    m = torch.from_numpy(m0.copy()).cuda()
+    v = torch.from_numpy(v0.copy()).cuda()
     losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
-    ctx.spsa_step_adam(th, m, v, 1, adam, soma.seeds_tensor(seeds), 0, eps, lr, torch.from_numpy(data).cuda(),
+    ctx.spsa_step_adam(th, m, v, 3, adam, soma.seeds_tensor(seeds), 0, eps, lr, torch.from_numpy(data).cuda(),
                        losses)
     coef = torch.zeros((N, P), dtype=torch.float32, device="cuda")
     ctx.coefficients(coef)
     torch.cuda.synchronize()
-    r = dict(theta0=theta, data=data, seeds=seeds, shape=shape, eps=eps, lr=lr)
-    o = oracle_step(oracle_mod, r)
+    o, (to, mo, vo) = adam_oracle_step(oracle_mod, cfg, theta, seeds, 0, eps, lr, data, m0, v0, 3, adam)
     assert_losses_close(losses.cpu().numpy(), o["losses"])
-    cg = coef.cpu().numpy()
-    assert np.abs(cg - o["coef"]).max() <= 2e-2 * np.abs(o["coef"]).max()
-    cfg = oracle_mod.cfg_from(shape)
-    hp = dict(beta1=float(adam.beta1), beta2=float(adam.beta2), delta=float(adam.delta),
-              weight_decay=float(adam.weight_decay))
-    got = [x.cpu().numpy() for x in (th, m, v)]
-    for e in range(N):
-        to, mo, vo, gh = oracle_mod.apply_adam(cfg, theta[e], np.zeros_like(theta[e]), np.zeros_like(theta[e]), 1,
-                                               int(seeds[e]), 0, float(np.float32(lr)), cg[e].astype(np.float64),
-                                               want_ghat=True, **hp)
-        g = gh + hp["weight_decay"] * theta[e].astype(np.float64)
-        _adam_compare([x[e] for x in got], (to, mo, vo), theta[e].astype(np.float64), g, float(np.float32(lr)),
-                      1, True)
+    cerr = np.abs(coef.cpu().numpy() - o["coef"]).max() / np.abs(o["coef"]).max()
+    assert cerr <= 2e-2
+    terr = assert_theta_close(th.cpu().numpy(), to)
+    uerr = update_rel_error(theta, th.cpu().numpy(), to)
+    assert uerr <= 5e-2        # the Adam update vector itself, at the coefficients' bar
+    merr = assert_moments_close(m.cpu().numpy(), mo, np.abs(mo).max())
+    verr = assert_moments_close(v.cpu().numpy(), vo, np.abs(vo).max())
+    print(f"{name} law {probe}: coef rel {cerr:.2e}  theta rel {terr:.2e}  update rel {uerr:.2e}  "
+          f"m rel {merr:.2e}  v rel {verr:.2e}")
+    assert not np.array_equal(th.cpu().numpy(), theta)
+    ctx.close()
 
 
 @pytest.mark.parametrize("name,A,pc", [("ragged_l2", 3, 2), ("b64_h128", 2, 0), ("tiny", 2, 3)])

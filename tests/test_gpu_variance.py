@@ -70,3 +70,81 @@ def test_single_probe_covariance_and_averaging_law(probe, q):
     assert abs(traces[1] / pred - 1) < 0.3
     slope = np.polyfit(np.log([1, 2, 4, 8, 16]), np.log([traces[n] for n in (1, 2, 4, 8, 16)]), 1)[0]
     assert abs(slope + 1) < 0.25, slope
+
+
+def _c3_traces(torch, B, T, D, probe=0):
+    """One independent-loss and one summed-loss step of the N = 4 experts of
+    width 384 (two layers) at fixed weights (lr = 0), on the same seeds and
+    data; returns the coefficients and the tr Cov of the single-direction
+    estimates of every expert from soma_estimator_moments (group 1)."""
+    w = workloads.SOMA_N4
+    theta = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed) * np.float32(3.0)
+    data = synth.expert_batches_in_child(w.cluster_seeds, B, T)
+    seeds = soma.seeds_tensor(synth.expert_seeds(w.n_experts, base=4321))
+    out = {}
+    for mode in (0, 1):
+        shape = soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, B, T, D, mode, probe=probe)
+        ctx = soma.Context(shape)
+        th = torch.from_numpy(theta.copy()).cuda()
+        losses = torch.zeros((w.n_experts, D, 2), dtype=torch.float32, device="cuda")
+        ctx.spsa_step(th, seeds, 0, w.eps, 0.0, torch.from_numpy(data).cuda(), losses)
+        coef = torch.zeros((w.n_experts, D), dtype=torch.float32, device="cuda")
+        ctx.coefficients(coef)
+        mom = torch.zeros((w.n_experts, 2), dtype=torch.float64, device="cuda")
+        ctx.estimator_moments(seeds, 0, coef, 1, mom)
+        torch.cuda.synchronize()
+        out[mode] = (coef.cpu().numpy().astype(np.float64), soma.group_covariance_trace(mom.cpu().numpy(), D, 1),
+                     losses.cpu().numpy())
+        ctx.close()
+    d = soma.param_count(shape)
+    return out, d, w.n_experts
+
+
+def _ratio_and_error(c_ind, c_sum, rng):
+    """sum_e tr Cov(summed) / sum_e tr Cov(independent) from the coefficients
+    (|X_j|^2 = D^2 c_j^2 |z_j|^2 and |z_j|^2 = d (1 + O(d^-1/2))), and its
+    bootstrap standard error over directions."""
+    def ratio(idx):
+        return np.sum(c_sum[:, idx] ** 2) / np.sum(c_ind[:, idx] ** 2)
+    D = c_ind.shape[1]
+    boots = [ratio(rng.integers(0, D, D)) for _ in range(400)]
+    return ratio(np.arange(D)), float(np.std(boots))
+
+
+@pytest.mark.parametrize("probe", [0, 2])
+def test_summed_to_independent_variance_ratio(probe):
+    """Appendix J's independent-vs-summed comparison (Section 5: summing the
+    experts' losses puts every expert's probe noise into each estimate) on
+    the N = 4 experts of width 384 at a reduced batch: with M = N d perturbed
+    coordinates the summed loss's estimate has (M + 1) / (d + 1) (Gaussian
+    probes) or (M - 1) / (d - 1) (dense Rademacher; Prop. 1's law) times the
+    independent one's total single-direction variance -- 4.0 here.  The paper
+    measures 4.02 against 4.00 predicted.  The forwards of the two runs are
+    the same bit for bit."""
+    torch = require_gpu()
+    D = 1024
+    out, d, N = _c3_traces(torch, 4, 16, D, probe)
+    assert np.array_equal(out[0][2], out[1][2])
+    (c_i, tr_i, _), (c_s, tr_s, _) = out[0], out[1]
+    pred = (N * d + 1) / (d + 1) if probe == 0 else (N * d - 1) / (d - 1)
+    measured = float(np.sum(tr_s) / np.sum(tr_i))
+    from_coef, se = _ratio_and_error(c_i, c_s, np.random.default_rng(0))
+    print(f"law {probe}: d = {d}, D = {D}: tr Cov summed / independent = {measured:.3f} "
+          f"(coefficients: {from_coef:.3f} +- {se:.3f}), predicted {pred:.5f}")
+    assert abs(measured / from_coef - 1) < 0.02      # the moments and the coefficients agree
+    assert abs(measured - pred) < 4 * se + 0.02, (measured, pred, se)
+
+
+def test_summed_to_independent_variance_ratio_full_size():
+    """The same comparison at the N = 4 workload's full batch (32 sequences
+    of 512 bytes) with 256 directions per expert."""
+    torch = require_gpu()
+    D = 256
+    out, d, N = _c3_traces(torch, 32, 512, D)
+    (c_i, tr_i, _), (c_s, tr_s, _) = out[0], out[1]
+    pred = (N * d + 1) / (d + 1)
+    measured = float(np.sum(tr_s) / np.sum(tr_i))
+    from_coef, se = _ratio_and_error(c_i, c_s, np.random.default_rng(1))
+    print(f"full size: tr Cov summed / independent = {measured:.3f} (coefficients: {from_coef:.3f} +- {se:.3f}), "
+          f"predicted {pred:.5f}")
+    assert abs(measured - pred) < 4 * se + 0.02, (measured, pred, se)
