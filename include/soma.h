@@ -223,6 +223,22 @@ void soma_destroy(soma_ctx* ctx);
 int soma_spsa_step(soma_ctx* ctx, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,
                    float eps, float lr, const uint8_t* bytes_dev, float* losses_dev, void* stream);
 
+/* soma_spsa_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * no context and no workspace.  The step's scratch space is a static device
+ * array of the library, 32 MiB on each GPU it runs on, held until the
+ * process ends; shapes whose workspace for one direction at a time exceeds
+ * it return SOMA_ESHAPE (the tiny and small shapes fit: the N = 1, H = 64
+ * workload needs 1.3 MB).  The directions run in the largest chunk that fits
+ * (or cfg->pair_chunk).  Stacked LSTM only (SOMA_EINVAL for SOMA_ARCH_BODY).
+ * Calls share that array on each GPU: calls that overlap on one GPU (two
+ * streams, two threads) race and must be serialised by the caller; the
+ * coefficients are not kept.  Arguments, results, atomicity and errors
+ * otherwise as soma_spsa_step, whose kernels it runs, and the results are
+ * the same bit for bit at the same chunk. */
+int soma_spsa_step_noalloc(const soma_config* cfg, float* theta_dev, const uint64_t* seeds_dev, uint64_t step,
+                           float eps, float lr, const uint8_t* bytes_dev, float* losses_dev, void* stream);
+
 /* Adam hyperparameters of the paper's update (Appendix E, Eq. localspsa;
  * the paper uses beta1 = 0.9, beta2 = 0.999, delta = 1e-8 and coupled weight
  * decay 1e-4).  beta1, beta2 in [0, 1); delta finite and > 0; weight_decay

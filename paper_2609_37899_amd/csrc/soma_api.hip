@@ -16,6 +16,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -941,6 +942,43 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   return mark(ctx, kPhaseHead, st);
 }
 
+// Fill a context for a shape and its workspace on the current device (no
+// allocation: the persistent recurrence's occupancy is queried, not run).
+void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws, size_t ws_bytes) {
+  const soma_config* cfg = &cfg0;
+  ctx->cfg = cfg0;
+  ctx->lay = L;
+  ctx->ws = ws;
+  ctx->ws_bytes = ws_bytes;
+  ctx->have_coef = false;
+  ctx->coop_blocks = 0;
+  {
+    // Co-resident blocks for the persistent recurrence on the current device.
+    int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
+    hipFuncAttributes fa{};
+    const bool shape_ok = cfg->arch == SOMA_ARCH_LSTM && cfg->hidden % 64 == 0 &&
+                          cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
+    const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden, cfg->probe) : nullptr;
+    if (kern && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
+        hipFuncGetAttributes(&fa, kern) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, soma::kPersistThreads, 0) == hipSuccess &&
+        coop && size_t(lds_max) >= fa.sharedSizeBytes && per_cu >= 1) {
+      ctx->coop_blocks = cus * per_cu;
+    }
+    (void)hipGetLastError();  // a failed query only disables the persistent path
+  }
+  ctx->head = nullptr;
+  ctx->head_stride = 0;
+  ctx->timing = false;
+  ctx->spin_limit = kSpinLimit;
+  ctx->have_times = false;
+  ctx->nmarks = 0;
+  ctx->rec_launches = ctx->proj_launches = 0;
+}
+
 }  // namespace
 
 extern "C" {
@@ -971,37 +1009,7 @@ int soma_create(const soma_config* cfg, void* workspace, size_t ws_bytes, soma_c
     return fail(SOMA_EWORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, L.total);
   soma_ctx* ctx = new (std::nothrow) soma_ctx;
   if (!ctx) return fail(SOMA_EINVAL, "out of host memory");
-  ctx->cfg = *cfg;
-  ctx->lay = L;
-  ctx->ws = static_cast<char*>(workspace);
-  ctx->ws_bytes = ws_bytes;
-  ctx->have_coef = false;
-  ctx->coop_blocks = 0;
-  {
-    // Co-resident blocks for the persistent recurrence on the current device.
-    int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
-    hipFuncAttributes fa{};
-    const bool shape_ok = cfg->arch == SOMA_ARCH_LSTM && cfg->hidden % 64 == 0 &&
-                          cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
-    const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden, cfg->probe) : nullptr;
-    if (kern && hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
-        hipFuncGetAttributes(&fa, kern) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, soma::kPersistThreads, 0) == hipSuccess &&
-        coop && size_t(lds_max) >= fa.sharedSizeBytes && per_cu >= 1) {
-      ctx->coop_blocks = cus * per_cu;
-    }
-    (void)hipGetLastError();  // a failed query only disables the persistent path
-  }
-  ctx->head = nullptr;
-  ctx->head_stride = 0;
-  ctx->timing = false;
-  ctx->spin_limit = kSpinLimit;
-  ctx->have_times = false;
-  ctx->nmarks = 0;
-  ctx->rec_launches = ctx->proj_launches = 0;
+  init_ctx(ctx, *cfg, L, static_cast<char*>(workspace), ws_bytes);
   *out = ctx;
   return ok();
 }
@@ -1488,3 +1496,70 @@ int soma_box_muller(const uint32_t* wa, const uint32_t* wb, float* za, float* zb
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The step for callers that cannot allocate device memory (code under HIP
+// graph capture, tight serving loops, harnesses that forbid allocation): the
+// kernels of soma_spsa_step with their scratch space in a file-scope device
+// array instead of a caller's workspace.  Each GPU the library runs on holds
+// its own copy of the array (kStaticScratchBytes) until the process ends; its
+// device address is looked up once per device with hipGetSymbolAddress, with
+// that device current, and only that address is handed to kernels.  Every
+// call on one GPU shares the array: the step clears what must start at zero
+// (the abort flag and the group counters, by kernels) and writes everything
+// else before reading it, and calls that overlap on one GPU race.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of the current device's scratch array (looked up on
+// the first call on that device).
+int scratch_address(char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SOMA_EDEVICE, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(SOMA_EDEVICE, "hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return SOMA_OK;
+}
+
+// The largest direction chunk whose workspace fits `budget` bytes (the
+// configured chunk if one is set), or 0 if none does.
+int chunk_within(const soma_config& c, size_t budget) {
+  if (c.pair_chunk > 0) return layout_for(c, c.pair_chunk).total <= budget ? c.pair_chunk : 0;
+  for (int pc = dirs(c); pc >= 1; --pc)
+    if (layout_for(c, pc).total <= budget) return pc;
+  return 0;
+}
+
+}  // namespace
+
+extern "C" int soma_spsa_step_noalloc(const soma_config* cfg, float* theta, const uint64_t* seeds, uint64_t step,
+                                      float eps, float lr, const uint8_t* bytes, float* losses, void* stream) {
+  if (int rc = validate(cfg)) return rc;
+  if (cfg->arch != SOMA_ARCH_LSTM) return fail(SOMA_EINVAL, "soma_spsa_step_noalloc runs the stacked LSTM only");
+  const int pc = chunk_within(*cfg, kStaticScratchBytes);
+  if (pc == 0)
+    return fail(SOMA_ESHAPE, "this shape needs %zu bytes of scratch per direction; the static scratch holds %zu",
+                layout_for(*cfg, 1).total, kStaticScratchBytes);
+  char* ws = nullptr;
+  if (int rc = scratch_address(&ws)) return rc;
+  const Layout L = layout_for(*cfg, pc);
+  soma_ctx ctx;   // host stack: its event pool stays empty (no phase timing here)
+  init_ctx(&ctx, *cfg, L, ws, kStaticScratchBytes);
+  return soma_spsa_step(&ctx, theta, seeds, step, eps, lr, bytes, losses, stream);
+}

@@ -26,7 +26,7 @@ EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destr
            "soma_apply_update", "soma_apply_adam", "soma_spsa_step_adam_sched", "soma_schedule_init",
            "soma_schedule_observe", "soma_estimator_moments", "soma_set_tied_head", "soma_head_delta",
            "soma_gaussian", "soma_probe", "soma_philox", "soma_box_muller", "soma_set_phase_timing",
-           "soma_get_phase_times", "soma_set_spin_limit",
+           "soma_get_phase_times", "soma_set_spin_limit", "soma_spsa_step_noalloc",
            "soma_last_error")
 
 
@@ -92,6 +92,7 @@ def load():
             "soma_create": (ctypes.c_int, [cp, vp, ctypes.c_size_t, ctypes.POINTER(vp)]),
             "soma_destroy": (None, [vp]),
             "soma_spsa_step": (ctypes.c_int, [vp, vp, vp, u64, f32, f32, vp, vp, vp]),
+            "soma_spsa_step_noalloc": (ctypes.c_int, [cp, vp, vp, u64, f32, f32, vp, vp, vp]),
             "soma_spsa_step_adam": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam),
                                                    vp, u64, f32, f32, vp, vp, vp]),
             "soma_apply_adam": (ctypes.c_int, [vp, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(Adam), vp,
@@ -298,6 +299,17 @@ class Context:
         _check(load().soma_apply_update(self._h, _dptr(theta, torch.float32, "theta"),
                                         _dptr(seeds, torch.int64, "seeds"), int(step), float(lr),
                                         _dptr(coef, torch.float32, "coef"), _stream(stream)))
+
+
+def spsa_step_noalloc(shape: Shape, theta, seeds, step: int, eps: float, lr: float, bytes_, losses, stream=None):
+    """soma_spsa_step without a context or workspace: the library's static
+    per-device scratch (small shapes only; calls on one GPU must not overlap)."""
+    import torch
+    cfg = shape.cfg()
+    _check(load().soma_spsa_step_noalloc(ctypes.byref(cfg), _dptr(theta, torch.float32, "theta"),
+                                         _dptr(seeds, torch.int64, "seeds"), int(step), float(eps), float(lr),
+                                         _dptr(bytes_, torch.uint8, "bytes"), _dptr(losses, torch.float32, "losses"),
+                                         _stream(stream)))
 
 
 def gaussian(seed: int, step: int, pair: int, k0: int, out, stream=None):
