@@ -585,8 +585,8 @@ int launch_rec_split(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
 
 int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 
-// Groups of H/32 blocks that the persistent recurrence can run at once
-// (0 when the shape or the device rules it out).  The kernel addresses one
+// Groups of H / (4 NW) blocks that the persistent recurrence can run at once
+// (0 when the shape or the device rules it out; NW = persist_waves(H)).  The kernel addresses one
 // slot's gate inputs with 32-bit offsets, so B (T-1) 4H floats must stay
 // below 2^31 bytes.
 int persistent_groups(const soma_ctx* ctx, int jobs) {
@@ -596,7 +596,7 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
     return 0;
   const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
   if (gin_slot_bytes >= (int64_t(1) << 31)) return 0;
-  const int ut = c.hidden / soma::kRecUnits;
+  const int ut = c.hidden / (4 * soma::persist_waves(c.hidden));
   int groups = std::min(ctx->coop_blocks / ut, jobs);
   // Group g owns blocks g + k groups and blocks are dealt to the 8 XCDs
   // round-robin, so with a multiple of 8 groups every group sits on one XCD
@@ -609,7 +609,7 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
 
 template <int NB, int NCH, bool kRad>
 const void* persist_kernel() {
-  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH, kRad>);
+  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH, kRad, soma::persist_waves(64 * NCH)>);
 }
 
 template <int NB, bool kRad>
@@ -623,6 +623,9 @@ const void* persist_kernel_for(int nch) {
     case 6: return persist_kernel<NB, 6, kRad>();
     case 7: return persist_kernel<NB, 7, kRad>();
     case 8: return persist_kernel<NB, 8, kRad>();
+    case 9: return persist_kernel<NB, 9, kRad>();
+    case 10: return persist_kernel<NB, 10, kRad>();
+    case 11: return persist_kernel<NB, 11, kRad>();
     default: return nullptr;
   }
 }
@@ -636,7 +639,7 @@ const void* persist_kernel_for(int B, int H) {
 }
 
 // The persistent recurrence kernel for batch B, hidden width H (H % 64 == 0,
-// H <= 512) and the generator family of probe law `probe`.
+// H <= kRecMaxH) and the generator family of probe law `probe`.
 const void* persist_kernel_for(int B, int H, int probe) {
   return probe == SOMA_PROBE_GAUSSIAN ? persist_kernel_for<false>(B, H) : persist_kernel_for<true>(B, H);
 }
@@ -766,9 +769,9 @@ int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, int kx, hip
   return check_launch("k_rec_local");
 }
 
-int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, hipStream_t st) {
+int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, int threads, hipStream_t st) {
   void* args[] = {const_cast<soma::PersistArgs*>(&p)};
-  const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(soma::kPersistThreads), args, 0, st);
+  const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), args, 0, st);
   if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipLaunchCooperativeKernel: %s", hipGetErrorString(e));
   return SOMA_OK;
 }
@@ -906,8 +909,9 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       // (zeroed once per step) so that a failure anywhere in the step sticks.
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
       if (int rc = check_launch("k_zero_u32")) return rc;
-      const int blocks = groups * (H / soma::kRecUnits);
-      if (int rc = launch_persist(persist_kernel_for(c.batch, H, c.probe), p, blocks, st)) return rc;
+      const int nw = soma::persist_waves(H);
+      const int blocks = groups * (H / (4 * nw));
+      if (int rc = launch_persist(persist_kernel_for(c.batch, H, c.probe), p, blocks, 64 * nw, st)) return rc;
       ctx->rec_launches += 1;
     } else {
       const dim3 grid((H / 16) * bgroups, pcs, N);
@@ -964,7 +968,8 @@ void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws,
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
         hipFuncGetAttributes(&fa, kern) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, soma::kPersistThreads, 0) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * soma::persist_waves(cfg->hidden), 0) ==
+            hipSuccess &&
         coop && size_t(lds_max) >= fa.sharedSizeBytes && per_cu >= 1) {
       ctx->coop_blocks = cus * per_cu;
     }

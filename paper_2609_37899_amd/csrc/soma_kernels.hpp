@@ -832,17 +832,19 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
 // ---------------------------------------------------------------------------
 // Persistent recurrence of one layer (perturbed step only).
 //
-// A block of 8 waves owns 32 units (128 gate rows) of one (expert, direction,
-// sign): wave w keeps the perturbed recurrent weights of gate rows
-// [16 w, +16) IN REGISTERS for the whole sequence -- the probes are drawn once
-// per (expert, direction, sign) instead of once per time step.  A group of
-// H/32 co-resident blocks carries one (expert, direction, sign) through time:
-// after step t every block publishes its slice of h_t and arrives on the
-// group's counter; before step t+1 it waits for all H/32 arrivals, then
-// stages the whole h_{t-1} of its sign (B x H) in LDS, 128 columns of K at
-// a time, overlapping the next piece's loads with the current piece's
-// MFMAs.  Groups take jobs round-robin; the cell state stays in registers.
-// One block per CU (two waves per SIMD).
+// A block of NW waves (8, or 12 where persist_waves says so) owns 4 NW units
+// (16 NW gate rows) of one (expert, direction, sign): wave w keeps the
+// perturbed recurrent weights of gate rows [16 w, +16) IN REGISTERS for the
+// whole sequence -- the probes are drawn once per (expert, direction, sign)
+// instead of once per time step.  A group of H / (4 NW) co-resident blocks
+// carries one (expert, direction, sign) through time: after step t every
+// block publishes its slice of h_t and arrives on the group's counter;
+// before step t+1 it waits for all the group's arrivals, then streams h_{t-1}
+// of its sign (B x H) through a ring of two LDS pieces of 128 (or 64) columns
+// of K, splitting it into fp16 parts as it is stored and overlapping the next
+// piece's loads with the current piece's MFMAs.  Groups take jobs
+// round-robin; the cell state stays in registers.  One block per CU (two or
+// three waves per SIMD).
 //
 // h is exchanged with device-coherent (sc1) stores and loads, so no cache
 // writeback or invalidation is needed: a block's stores complete
@@ -854,14 +856,9 @@ __global__ __launch_bounds__(kThreads) void k_head_ce(FwdArgs a) {
 // always drains; the update kernel then leaves theta untouched and the
 // losses read NaN.
 // ---------------------------------------------------------------------------
-constexpr int kPersistThreads = 512;   // 8 waves x 16 gate rows
-constexpr int kRecMaxH = 512;          // H <= 512 (h_{t-1} of one sign fits in LDS)
-constexpr int kRecUnits = 32;          // units per block (128 gate rows)
-constexpr int kHsld = kRecMaxH + 8;    // padded LDS row of staged h (odd multiple of 8 floats)
+constexpr int kRecMaxH = 704;          // H <= 704: 176 VGPRs of split fragments per lane (K = H)
 constexpr int kCoherent = 16;          // cache policy: device scope (sc1)
 constexpr int kZpiece = 256;           // k per cooperatively drawn probe piece
-constexpr int kZld = kZpiece + 8;      // its padded LDS row
-constexpr int kHtld = kRecUnits + 4;   // LDS row of the transposed h_t tile (conflict-free word writes)
 
 struct PersistArgs {
   FwdArgs a;
@@ -932,65 +929,28 @@ __device__ __forceinline__ float4 buffer_load_f4s(__amdgpu_buffer_rsrc_t r, uint
   return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
 }
 
-// Perturbed weights of the block's 128 rows r0 .. r0 + 127 over columns
-// col0 .. col0 + 16 KQ of a matrix at canonical offset off_l with row length
-// ld, one sign:  w = theta + seps z.  With kGateRows the rows are a layer's
-// gate rows in interleaved order (row 4u + g is gate g of unit u, canonical
-// row g H + u); otherwise row r is canonical row r.
-// Lane (wave, lr, lg) keeps row r0 + 16 wave + lr, columns col0 + 16 c + 4 lg
-// .. + 3 in w[c].  The block draws the probes cooperatively, 256 columns at a
-// time, into the LDS scratch zs (128 x kZld floats); it is free again on return.
-// The generator is fixed at compile time (kRad: a Rademacher law, `law` then
-// telling sparse from dense; else Gaussian): a run-time choice between the
-// two costs these register-resident kernels spills.
-template <int KQ, bool kGateRows, bool kRad>
-__device__ __forceinline__ void resident_weights(float4 (&w)[KQ], float* zs, const float* th, int64_t off_l,
-                                                 int ld, int col0, int H, int r0, int law, uint2 key,
-                                                 uint32_t pair, uint32_t step_lo, float seps) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
-  auto canon = [&](int r) { return kGateRows ? (r & 3) * H + (r >> 2) : r; };
-  const int prow = r0 + wave * 16 + lr;
-  const int64_t wrow = off_l + static_cast<int64_t>(canon(prow)) * ld + col0;
-#pragma unroll
-  for (int piece = 0; piece < (KQ + 15) / 16; ++piece) {
-    const int kq0 = piece * 16;
-    const int nq = (KQ - kq0 < 16 ? KQ - kq0 : 16);
-    __syncthreads();
-    for (int q = threadIdx.x; q < 128 * nq * 4; q += blockDim.x) {
-      const int m = q / (nq * 4), k4 = q % (nq * 4);
-      const int pr = r0 + m;
-      const uint64_t kk = static_cast<uint64_t>(off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 16 * kq0 + 4 * k4);
-      *reinterpret_cast<float4*>(&zs[m * kZld + 4 * k4]) =
-          kRad ? rademacher_quad(key, pair, step_lo, kk, law == kProbeRademacher) : gauss_quad(key, pair, step_lo, kk >> 2);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int c2 = 0; c2 < 16; ++c2) {
-      const int c = kq0 + c2;
-      if (c < KQ) {
-        const float4 t4 = *reinterpret_cast<const float4*>(th + wrow + 16 * c + 4 * lg);
-        const float4 z = *reinterpret_cast<const float4*>(&zs[(wave * 16 + lr) * kZld + 16 * c2 + 4 * lg]);
-        w[c] = fma4(seps, z, t4);
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// The same rows as split fragments for the fp16 products: lane (wave, lr, lg)
-// keeps row r0 + 16 wave + lr, columns col0 + 32 c + 8 lg .. + 7 as (wh[c],
-// wl[c]), KC = K / 32 chunks; w = theta + seps z is formed in fp32 and then
-// split.  The probes are drawn as in resident_weights, ZW columns at a time
-// into the LDS scratch zs (128 x (ZW + 8) floats).
-template <int KC, bool kGateRows, bool kRad, int ZW = kZpiece>
+// Perturbed weights of NR rows r0 .. r0 + NR - 1 (16 per wave) over columns
+// col0 .. col0 + 32 KC of a matrix at canonical offset off_l with row length
+// ld, one sign, as split fragments for the fp16 products:  w = theta + seps z
+// is formed in fp32 and split.  With kGateRows the rows are a layer's gate
+// rows in interleaved order (row 4u + g is gate g of unit u, canonical row
+// g H + u); otherwise row r is canonical row r.  Lane (wave, lr, lg) keeps
+// row r0 + 16 wave + lr, columns col0 + 32 c + 8 lg .. + 7 as (wh[c],
+// wl[c]).  The block draws the probes cooperatively, ZW columns at a time,
+// into the LDS scratch zs (NR x (ZW + 8) floats), which is free again on
+// return.  The generator is fixed at compile time (kRad: a Rademacher law,
+// `law` then telling sparse from dense; else Gaussian): a run-time choice
+// between the two costs these register-resident kernels spills.  A weight
+// outside the split's range sets the step's abort flag.
+template <int KC, bool kGateRows, bool kRad, int ZW = kZpiece, int NR = 128>
 __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&wl)[KC], float* zs, const float* th,
                                                        int64_t off_l, int ld, int col0, int H, int r0, int law,
                                                        uint2 key, uint32_t pair, uint32_t step_lo, float seps,
                                                        unsigned* err) {
-  bool in_range = true;
   static_assert(ZW % 32 == 0 && ZW <= kZpiece, "probe pieces of whole chunks");
   constexpr int kPiece = ZW / 32;        // chunks per probe piece
   constexpr int ZLD = ZW + 8;            // scratch row in floats (an odd multiple of 32 bytes)
+  bool in_range = true;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   auto canon = [&](int r) { return kGateRows ? (r & 3) * H + (r >> 2) : r; };
   const int prow = r0 + wave * 16 + lr;
@@ -1000,7 +960,7 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
     const int kc0 = piece * kPiece;
     const int nc = (KC - kc0 < kPiece ? KC - kc0 : kPiece);
     __syncthreads();
-    for (int q = threadIdx.x; q < 128 * nc * 8; q += blockDim.x) {
+    for (int q = threadIdx.x; q < NR * nc * 8; q += blockDim.x) {
       const int m = q / (nc * 8), k4 = q % (nc * 8);
       const int pr = r0 + m;
       const uint64_t kk = static_cast<uint64_t>(off_l + static_cast<int64_t>(canon(pr)) * ld + col0 + 32 * kc0 + 4 * k4);
@@ -1025,8 +985,16 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
   __syncthreads();
 }
 
-template <int NB, int NCH, bool kRad>
-__global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs p) {
+// Waves per block of the persistent recurrence for hidden width H: 12 (192
+// gate rows, 48 units) where H is 192 or 384, so that a group of H/48 blocks
+// fits one XCD in groups of a multiple of 8 across all 256 compute units (at
+// H = 384: 32 groups of 8 blocks instead of 16 groups of 12 blocks, a quarter
+// of the chip idle); else 8 (128 gate rows, 32 units).
+__host__ __device__ constexpr int persist_waves(int H) { return (H == 192 || H == 384) ? 12 : 8; }
+
+template <int NB, int NCH, bool kRad, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
+  constexpr int NU = 4 * NW;                            // units per block (16 NW gate rows, 16 per wave)
   constexpr int KC = 2 * NCH;                           // 32-wide k chunks: H = 64 NCH
   // Staging pieces of K, 128 wide where H allows, else 64: the first piece,
   // whose loads nothing hides, stays short, while a piece's products still
@@ -1036,29 +1004,34 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
   constexpr int NQ = 64 * NCH / KWQ;
   constexpr int QC = KWQ / 32;                          // k chunks per piece
   constexpr int ROWS = NB * 16;
-  constexpr int HS = kRecMaxH + 16;                     // padded LDS row in halves (an odd multiple of 32 bytes)
-  constexpr int CW4 = KWQ / 4;                          // float4 per row of a piece: 16, 32 or 64
+  constexpr int SW = KWQ + 16;                          // ring row in halves (an odd multiple of 32 bytes)
+  constexpr int CW4 = KWQ / 4;                          // float4 per row of a piece: 16 or 32
   constexpr int RPW = 64 / CW4;                         // rows per wave load
-  constexpr int PT = ROWS >= 8 * RPW ? ROWS / (8 * RPW) : 1;   // wave loads per piece (8 waves)
-  constexpr bool kAllWaves = ROWS >= 8 * RPW;           // else waves past the rows stage nothing
-  constexpr int STAGE_BYTES = 2 * ROWS * HS * 2;        // [hi, lo][ROWS][HS] halves
-  constexpr int LDS_BYTES = STAGE_BYTES > 128 * kZld * 4 ? STAGE_BYTES : 128 * kZld * 4;
-  // staged h_{t-1} split into fp16 parts; the probe piece at job start
+  constexpr int WL = ROWS / RPW;                        // wave loads per piece
+  constexpr int PT = (WL + NW - 1) / NW;                // of them per wave
+  constexpr bool kAllWaves = WL % NW == 0;              // else the waves past the rows stage nothing
+  constexpr int RING_BYTES = 2 * 2 * ROWS * SW * 2;     // [buffer][hi, lo][ROWS][SW] halves
+  constexpr int ZW = NW > 8 ? 128 : kZpiece;            // probe piece: 16 NW rows x (ZW + 8) floats
+  constexpr int ZS_BYTES = 16 * NW * (ZW + 8) * 4;
+  constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
+  constexpr int HTLD = NU + 4;                          // LDS row of the transposed h_t tile
+  static_assert(WL * RPW == ROWS, "a piece's rows split into whole wave loads");
+  // a ring of two staged pieces of h_{t-1}, split into fp16 parts; the probe
+  // piece at job start
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
-  __shared__ float ht[ROWS * kHtld];                    // h_t of the block's units, transposed for stores
-  _Float16* hs_hi = reinterpret_cast<_Float16*>(lds);
-  _Float16* hs_lo = hs_hi + ROWS * HS;
+  __shared__ __attribute__((aligned(16))) float ht[ROWS * HTLD];   // h_t of the block's units, transposed for stores
+  _Float16* ring = reinterpret_cast<_Float16*>(lds);    // buffer b: hi at ring + 2 b ROWS SW, lo one part later
   __shared__ unsigned abort_flag;
   const FwdArgs& a = p.a;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform (scalar) from here on
   const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int H = a.H, B = a.B, T = a.T, in = a.in_l;
-  const int UT = H / kRecUnits;                         // blocks per group
+  const int UT = H / NU;                                // blocks per group
   const int g = blockIdx.x % p.groups;
   const int utile = blockIdx.x / p.groups;              // < UT: the grid is groups * UT blocks
   const int64_t R = static_cast<int64_t>(T - 1) * B;
   const int64_t H4 = 4 * static_cast<int64_t>(H);
-  const int unit = utile * kRecUnits + wave * 4 + lg;   // output unit of this lane
+  const int unit = utile * NU + wave * 4 + lg;          // output unit of this lane
   const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));   // < 2^31 (host check)
   unsigned* bar = p.bar + g;
   unsigned done = 0;                                    // steps this block has published
@@ -1082,8 +1055,9 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
     // Perturbed recurrent weights of this lane, drawn once for the sequence
     // and held as split fragments.
     uint4 wh[KC], wl[KC];
-    resident_weights_split<KC, true, kRad>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H, in, H,
-                                           utile * 128, a.probe, key, pair, step_lo, seps, p.err);
+    resident_weights_split<KC, true, kRad, ZW, 16 * NW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H,
+                                                        in, H, utile * 16 * NW, a.probe, key, pair, step_lo, seps,
+                                                        p.err);
     // Rows past the batch compute on whatever follows in the same buffers
     // (finite inputs and h of later rows, possibly being rewritten, or zeros
     // past a buffer's end): a column of the product depends only on the same
@@ -1145,7 +1119,7 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       auto cell = [&](int nb) {
         float h;
         lstm_cell(acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3], cs[nb], h);
-        ht[(nb * 16 + lr) * kHtld + wave * 4 + lg] = h;
+        ht[(nb * 16 + lr) * HTLD + wave * 4 + lg] = h;
       };
 
       if (t == 0) {
@@ -1157,17 +1131,20 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
       } else {
         if (group_wait(bar, static_cast<unsigned>(UT) * done, p.err, p.spin_limit, &abort_flag)) return;
         const int row0 = (t - 1) * B;                    // rows of h_{t-1} in the slot
-        // Wave load i of a piece covers rows (wave + 8 i) RPW + lane / CW4,
+        // Wave load i of a piece covers rows (wave + NW i) RPW + lane / CW4,
         // float4 lane % CW4 of the piece: a per-lane part and a scalar part.
         // Rows past the batch (B < 64) read whatever follows h_{t-1} (zeros
-        // past the slot); their results are never stored.
+        // past the slot); their results are never stored.  Piece qq is staged
+        // into ring buffer qq & 1: the products of piece qq - 1, the buffer's
+        // previous contents, were finished before the block barrier that
+        // ends their iteration.
         const int lrow = lane / CW4, lc4 = lane % CW4;
         const uint32_t lane_off = static_cast<uint32_t>((lrow * H + 4 * lc4) * 4);
         float4 pre[PT];
         auto gload = [&](int qq) {
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
-            const int n0 = (wave + 8 * i) * RPW;
+            const int n0 = (wave + NW * i) * RPW;
             if (kAllWaves || n0 < ROWS) {                // wave-uniform
               const uint32_t soff = static_cast<uint32_t>(((row0 + n0) * H + qq * KWQ) * 4);
               typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -1179,28 +1156,30 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
         };
         // h_{t-1} is split into its fp16 parts as it is staged.
         auto sstore = [&](int qq) {
+          _Float16* hi_part = ring + (2 * (qq & 1)) * ROWS * SW;
 #pragma unroll
           for (int i = 0; i < PT; ++i) {
-            if (!kAllWaves && (wave + 8 * i) * RPW >= ROWS) continue;   // wave-uniform
-            const int n = (wave + 8 * i) * RPW + lrow;
+            if (!kAllWaves && (wave + NW * i) * RPW >= ROWS) continue;   // wave-uniform
+            const int n = (wave + NW * i) * RPW + lrow;
             uint2 hi, lo;
             split4(pre[i], hi, lo);
-            *reinterpret_cast<uint2*>(hs_hi + n * HS + qq * KWQ + 4 * lc4) = hi;
-            *reinterpret_cast<uint2*>(hs_lo + n * HS + qq * KWQ + 4 * lc4) = lo;
+            *reinterpret_cast<uint2*>(hi_part + n * SW + 4 * lc4) = hi;
+            *reinterpret_cast<uint2*>(hi_part + ROWS * SW + n * SW + 4 * lc4) = lo;
           }
         };
-        // Fragment (nb, kc) of this lane sits at a compile-time offset from
-        // one per-lane base per part (within the 16-bit LDS offset field).
-        const _Float16* bhi = hs_hi + lr * HS + 8 * lg;
-        const _Float16* blo = hs_lo + lr * HS + 8 * lg;
-        auto mfma_chunk = [&](int kc) {
+        // Fragment (nb, chunk pq of piece qq) of this lane sits at a
+        // compile-time offset from one per-lane base (within the 16-bit LDS
+        // offset field).
+        const _Float16* blane = ring + lr * SW + 8 * lg;
+        auto mfma_chunk = [&](int qq, int pq) {
+          const _Float16* bhi = blane + (2 * (qq & 1)) * ROWS * SW;
           uint4 bh[NB], bl[NB];
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
-            bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * HS + 32 * kc);
-            bl[nb] = *reinterpret_cast<const uint4*>(blo + nb * 16 * HS + 32 * kc);
+            bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * SW + 32 * pq);
+            bl[nb] = *reinterpret_cast<const uint4*>(bhi + ROWS * SW + nb * 16 * SW + 32 * pq);
           }
-          mfma3_batch<NB>(wh[kc], wl[kc], bh, bl, acc);
+          mfma3_batch<NB>(wh[qq * QC + pq], wl[qq * QC + pq], bh, bl, acc);
         };
         gload(0);
         sstore(0);                                       // its wait covers the inputs too
@@ -1211,32 +1190,32 @@ __global__ __launch_bounds__(kPersistThreads, 1) void k_rec_persist(PersistArgs 
           if (qq + 1 < NQ) {
             gload(qq + 1);
 #pragma unroll
-            for (int pq = 0; pq < QC; ++pq) mfma_chunk(qq * QC + pq);
+            for (int pq = 0; pq < QC; ++pq) mfma_chunk(qq, pq);
             sstore(qq + 1);
             __syncthreads();
           } else {
             if (t + 2 < T) load_inputs(t + 1);
 #pragma unroll
-            for (int pq = 0; pq < QC; ++pq) mfma_chunk(qq * QC + pq);
+            for (int pq = 0; pq < QC; ++pq) mfma_chunk(qq, pq);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) cell(nb);
           }
         }
       }
 
-      // Publish h_t: the block's 32 units of one row are one 128-byte line;
-      // transposed through LDS (cell() wrote this lane's words), each thread
-      // stores a float4 and the block writes whole lines instead of
-      // scattered words.
+      // Publish h_t: the block's NU units of one row are 128 or 192
+      // contiguous bytes; transposed through LDS (cell() wrote this lane's
+      // words), each thread stores a float4, so the block writes whole lines
+      // instead of scattered words.
       __syncthreads();
-      if (threadIdx.x < ROWS * 8) {
-        const int n = threadIdx.x >> 3, c4 = threadIdx.x & 7;
+      if (threadIdx.x < ROWS * (NU / 4)) {
+        const int n = threadIdx.x / (NU / 4), c4 = threadIdx.x % (NU / 4);
         if (n < B) {
           typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-          const float4 v = *reinterpret_cast<const float4*>(&ht[n * kHtld + 4 * c4]);
+          const float4 v = *reinterpret_cast<const float4*>(&ht[n * HTLD + 4 * c4]);
           __builtin_amdgcn_raw_buffer_store_b128(
               __builtin_bit_cast(u32x4, v), hbuf,
-              static_cast<uint32_t>(((t * B + n) * H + utile * kRecUnits + 4 * c4) * 4), 0, kCoherent);
+              static_cast<uint32_t>(((t * B + n) * H + utile * NU + 4 * c4) * 4), 0, kCoherent);
         }
       }
       // Every wave is done reading hs (its last piece) and ht before the

@@ -22,7 +22,7 @@ SHAPES = {
     "h64_b20": (1, 1, 48, 64, 20, 13, 2, 1e-3, 1e-2, 0),      # fold, one block per job
     "b64_h128": (2, 2, 64, 128, 64, 20, 3, 1e-3, 1e-2, 2),    # fold, persistent recurrence, streaming projection
     "ragged_l2": (2, 2, 48, 32, 20, 37, 3, 1e-3, 1e-2, 2),    # tiled kernels (H = 32)
-    "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0),     # per-step split recurrence, streaming head
+    "h704_b12": (1, 2, 32, 704, 12, 5, 1, 1e-3, 1e-3, 0),     # persistent recurrence at H = 704, streaming head
     "b40_h384": (1, 2, 32, 384, 40, 9, 2, 1e-3, 1e-2, 0),     # persistent, streaming head (H > 128)
 }
 
