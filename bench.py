@@ -229,6 +229,9 @@ def main():
     if local_rec and w.embed in (32, 64) and w.batch * w.seq_len <= 16384:
         fl["rec"] += fl["fold"]
         fl["fold"] = 0
+        if w.n_layers == 1:          # and the head and cross entropy too (no head launch)
+            fl["rec"] += fl["head"]
+            fl["head"] = 0
     K = args.steps
     ms = {"rec": phases["rec_ms"] / K, "proj": phases["proj_ms"] / K, "fold": phases["fold_ms"] / K,
           "head": phases["head_ms"] / K, "reduce": phases["reduce_ms"] / K,

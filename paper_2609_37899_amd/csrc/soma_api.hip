@@ -586,7 +586,7 @@ int launch_rec_split(const soma::FwdArgs& a, dim3 grid, hipStream_t st) {
 int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 
 // Groups of H / (4 NW) blocks that the persistent recurrence can run at once
-// (0 when the shape or the device rules it out; NW = persist_waves(H)).  The kernel addresses one
+// (0 when the shape or the device rules it out; NW = persist_waves(H, B)).  The kernel addresses one
 // slot's gate inputs with 32-bit offsets, so B (T-1) 4H floats must stay
 // below 2^31 bytes.
 int persistent_groups(const soma_ctx* ctx, int jobs) {
@@ -596,7 +596,7 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
     return 0;
   const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
   if (gin_slot_bytes >= (int64_t(1) << 31)) return 0;
-  const int ut = c.hidden / (4 * soma::persist_waves(c.hidden));
+  const int ut = c.hidden / (4 * soma::persist_waves(c.hidden, c.batch));
   int groups = std::min(ctx->coop_blocks / ut, jobs);
   // Group g owns blocks g + k groups and blocks are dealt to the 8 XCDs
   // round-robin, so with a multiple of 8 groups every group sits on one XCD
@@ -609,7 +609,7 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
 
 template <int NB, int NCH, bool kRad>
 const void* persist_kernel() {
-  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH, kRad, soma::persist_waves(64 * NCH)>);
+  return reinterpret_cast<const void*>(&soma::k_rec_persist<NB, NCH, kRad, soma::persist_waves(64 * NCH, 16 * NB)>);
 }
 
 template <int NB, bool kRad>
@@ -737,35 +737,40 @@ bool local_embedding(const soma_config& c) {
          int64_t(c.batch) * c.seq_len <= soma::kLocalBytes;
 }
 
-template <bool kRad, int KX>
+template <bool kRad, int KX, bool kHead>
 void launch_local_t(const soma::FwdArgs& a, int jobs, int B, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(jobs)), block(soma::kLocalThreads);
   if (B <= 16)
-    hipLaunchKernelGGL((soma::k_rec_local<1, kRad, KX>), grid, block, 0, st, a, jobs);
+    hipLaunchKernelGGL((soma::k_rec_local<1, kRad, KX, kHead>), grid, block, 0, st, a, jobs);
   else if (B <= 32)
-    hipLaunchKernelGGL((soma::k_rec_local<2, kRad, KX>), grid, block, 0, st, a, jobs);
+    hipLaunchKernelGGL((soma::k_rec_local<2, kRad, KX, kHead>), grid, block, 0, st, a, jobs);
   else
-    hipLaunchKernelGGL((soma::k_rec_local<4, kRad, KX>), grid, block, 0, st, a, jobs);
+    hipLaunchKernelGGL((soma::k_rec_local<4, kRad, KX, kHead>), grid, block, 0, st, a, jobs);
 }
 
 // kx: 32-wide chunks of the embedding formed in the block (0: gate inputs
-// read from U or gin).
+// read from U or gin); head: the head and cross entropy fused into the block
+// (kx > 0 only: the targets are read from the job's bytes in LDS).
 template <bool kRad>
-void launch_local_k(const soma::FwdArgs& a, int jobs, int B, int kx, hipStream_t st) {
+void launch_local_k(const soma::FwdArgs& a, int jobs, int B, int kx, bool head, hipStream_t st) {
   if (kx == 0)
-    launch_local_t<kRad, 0>(a, jobs, B, st);
+    launch_local_t<kRad, 0, false>(a, jobs, B, st);
+  else if (kx == 1 && head)
+    launch_local_t<kRad, 1, true>(a, jobs, B, st);
   else if (kx == 1)
-    launch_local_t<kRad, 1>(a, jobs, B, st);
+    launch_local_t<kRad, 1, false>(a, jobs, B, st);
+  else if (head)
+    launch_local_t<kRad, 2, true>(a, jobs, B, st);
   else
-    launch_local_t<kRad, 2>(a, jobs, B, st);
+    launch_local_t<kRad, 2, false>(a, jobs, B, st);
 }
 
-int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, int kx, hipStream_t st) {
-  if (kx < 0 || kx > 2) return fail(SOMA_EINVAL, "k_rec_local: embedding chunks %d", kx);
+int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, int kx, bool head, hipStream_t st) {
+  if (kx < 0 || kx > 2 || (head && kx == 0)) return fail(SOMA_EINVAL, "k_rec_local: embedding chunks %d", kx);
   if (probe == SOMA_PROBE_GAUSSIAN)
-    launch_local_k<false>(a, jobs, B, kx, st);
+    launch_local_k<false>(a, jobs, B, kx, head, st);
   else
-    launch_local_k<true>(a, jobs, B, kx, st);
+    launch_local_k<true>(a, jobs, B, kx, head, st);
   return check_launch("k_rec_local");
 }
 
@@ -865,6 +870,10 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   a.in_l = c.embed;
   a.off_l = L.off_layer[0];
   const bool emb_local = kPert && local_embedding(c);
+  // One layer at H = 64 with the embedding in the block: the head and the
+  // cross entropy run in the recurrence block too (no h in HBM, no head
+  // launch), unless the tiled reference kernels are asked for.
+  const bool fused_head = emb_local && c.n_layers == 1 && stream_weights(c);
   if (!emb_local) {
     hipLaunchKernelGGL((soma::k_fold<kPert>), dim3(4 * H / 64, SOMA_VOCAB / 64, N * pcs),
                        dim3(soma::kThreads), 0, st, a);
@@ -895,7 +904,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       // H = 64: one block per job, h kept in the block between steps.
       const int jobs = 2 * N * pcs;   // (expert, direction, sign)
       const int kx = l == 0 && emb_local ? c.embed / 32 : 0;
-      if (int rc = launch_local(a, jobs, c.batch, c.probe, kx, st)) return rc;
+      if (int rc = launch_local(a, jobs, c.batch, c.probe, kx, fused_head, st)) return rc;
       ctx->rec_launches += 1;
     } else if (groups > 0) {
       soma::PersistArgs p{};
@@ -909,7 +918,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       // (zeroed once per step) so that a failure anywhere in the step sticks.
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
       if (int rc = check_launch("k_zero_u32")) return rc;
-      const int nw = soma::persist_waves(H);
+      const int nw = soma::persist_waves(H, c.batch);
       const int blocks = groups * (H / (4 * nw));
       if (int rc = launch_persist(persist_kernel_for(c.batch, H, c.probe), p, blocks, 64 * nw, st)) return rc;
       ctx->rec_launches += 1;
@@ -928,7 +937,9 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     }
     if (int rc = mark(ctx, kPhaseRec, st)) return rc;
   }
-  if (kPert && stream_weights(c) && H <= 128) {
+  if (fused_head) {
+    // formed by the recurrence block
+  } else if (kPert && stream_weights(c) && H <= 128) {
     launch_head_fused(a, 2 * N * pcs, st);
     if (int rc = check_launch("k_head_fused")) return rc;
   } else if (kPert && stream_weights(c)) {
@@ -968,7 +979,7 @@ void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws,
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
         hipFuncGetAttributes(&fa, kern) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * soma::persist_waves(cfg->hidden), 0) ==
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * soma::persist_waves(cfg->hidden, cfg->batch), 0) ==
             hipSuccess &&
         coop && size_t(lds_max) >= fa.sharedSizeBytes && per_cu >= 1) {
       ctx->coop_blocks = cus * per_cu;

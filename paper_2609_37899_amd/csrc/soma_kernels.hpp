@@ -985,12 +985,16 @@ __device__ __forceinline__ void resident_weights_split(uint4 (&wh)[KC], uint4 (&
   __syncthreads();
 }
 
-// Waves per block of the persistent recurrence for hidden width H: 12 (192
-// gate rows, 48 units) where H is 192 or 384, so that a group of H/48 blocks
-// fits one XCD in groups of a multiple of 8 across all 256 compute units (at
-// H = 384: 32 groups of 8 blocks instead of 16 groups of 12 blocks, a quarter
-// of the chip idle); else 8 (128 gate rows, 32 units).
-__host__ __device__ constexpr int persist_waves(int H) { return (H == 192 || H == 384) ? 12 : 8; }
+// Waves per block of the persistent recurrence for hidden width H and batch
+// B: 12 (192 gate rows, 48 units) where H is 192 or 384 and B <= 32, so that
+// a group of H/48 blocks fits one XCD in groups of a multiple of 8 across all
+// 256 compute units (at H = 384: 32 groups of 8 blocks instead of 16 groups
+// of 12 blocks, a quarter of the chip idle); else 8 (128 gate rows, 32
+// units).  With 12 waves (three per SIMD, 168 registers each) four row tiles
+// do not fit.
+__host__ __device__ constexpr int persist_waves(int H, int B) {
+  return (H == 192 || H == 384) && B <= 32 ? 12 : 8;
+}
 
 template <int NB, int NCH, bool kRad, int NW>
 __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
@@ -1016,6 +1020,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
   constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
   constexpr int HTLD = NU + 4;                          // LDS row of the transposed h_t tile
   static_assert(WL * RPW == ROWS, "a piece's rows split into whole wave loads");
+  // Registers per lane: weights 8 KC, accumulators and gate inputs 8 NB, the
+  // B fragments of a chunk 8 NB, staging 4 PT, about 40 more.  Where that
+  // exceeds the 256 that two waves per SIMD leave each wave (H >= 576 with
+  // four row tiles), the fragments are read one row tile at a time
+  // (measured on the monolith workload: its recurrence 210 -> 192 ms per
+  // step; with three waves per SIMD at H = 384 the serialised passes cost
+  // more than the spills they avoid).
+  constexpr bool kLeanFrag = NW == 8 && 8 * KC + 16 * NB + 4 * PT + 40 > 256;
   // a ring of two staged pieces of h_{t-1}, split into fp16 parts; the probe
   // piece at job start
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
@@ -1173,13 +1185,24 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
         const _Float16* blane = ring + lr * SW + 8 * lg;
         auto mfma_chunk = [&](int qq, int pq) {
           const _Float16* bhi = blane + (2 * (qq & 1)) * ROWS * SW;
-          uint4 bh[NB], bl[NB];
+          if constexpr (kLeanFrag) {
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * SW + 32 * pq);
-            bl[nb] = *reinterpret_cast<const uint4*>(bhi + ROWS * SW + nb * 16 * SW + 32 * pq);
+            for (int nb = 0; nb < NB; ++nb) {
+              uint4 bh[1] = {*reinterpret_cast<const uint4*>(bhi + nb * 16 * SW + 32 * pq)};
+              uint4 bl[1] = {*reinterpret_cast<const uint4*>(bhi + ROWS * SW + nb * 16 * SW + 32 * pq)};
+              f32x4 a1[1] = {acc[nb]};
+              mfma3_batch<1>(wh[qq * QC + pq], wl[qq * QC + pq], bh, bl, a1);
+              acc[nb] = a1[0];
+            }
+          } else {
+            uint4 bh[NB], bl[NB];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+              bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * SW + 32 * pq);
+              bl[nb] = *reinterpret_cast<const uint4*>(bhi + ROWS * SW + nb * 16 * SW + 32 * pq);
+            }
+            mfma3_batch<NB>(wh[qq * QC + pq], wl[qq * QC + pq], bh, bl, acc);
           }
-          mfma3_batch<NB>(wh[qq * QC + pq], wl[qq * QC + pq], bh, bl, acc);
         };
         gload(0);
         sstore(0);                                       // its wait covers the inputs too
@@ -1256,10 +1279,15 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
 // for the h stores before it: loads and stores share one counter).
 // ---------------------------------------------------------------------------
 constexpr int kLocalThreads = 512;
+// Below this L1 norm of every perturbed head row, |logit| < 64 (|h| < 1), so
+// e^logit neither overflows nor underflows in fp32 and the row maximum need
+// not be subtracted before exponentiating.
+constexpr float kNoShiftL1 = 64.0f;
 constexpr int kLocalBytes = 16384;                      // largest B T kept in LDS (KX > 0)
 
-template <int NB, bool kRad, int KX>
-__global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs) {
+template <int NB, bool kRad, int KX, bool kHead>
+__global__ __launch_bounds__(kLocalThreads) __attribute__((amdgpu_waves_per_eu(kHead && NB == 1 ? 4 : 1)))
+void k_rec_local(FwdArgs a, int jobs) {
   constexpr int H = 64, G = 4 * H;                      // gate rows of a job
   constexpr int KC = H / 32;                            // 32-wide k chunks
   constexpr int MT = G / (16 * 8);                      // row tiles per wave
@@ -1270,15 +1298,24 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
   constexpr int PART = ROWS * HSW;                      // halves per fp16 part of one buffer
   constexpr int EMB_BYTES = 2 * kVocab * EW * 2;        // [hi, lo][256][EW] halves
   constexpr int BT_BYTES = KX > 0 ? kLocalBytes : 0;    // the job's bytes [B][T]
-  constexpr int ST_BYTES = EMB_BYTES + BT_BYTES + 2 * 2 * PART * 2;  // + [buffer][hi, lo][ROWS][HSW] halves
+  constexpr int H_BYTES = 2 * 2 * PART * 2;            // [buffer][hi, lo][ROWS][HSW] halves
+  // the fused head's per-wave partials (max, sum exp) and target logits of
+  // each row, by step parity: [2][8][ROWS] float2, [2][ROWS] float
+  constexpr int HEAD_BYTES = kHead ? 2 * 8 * ROWS * 8 + 2 * ROWS * 4 : 0;
+  constexpr int ST_BYTES = EMB_BYTES + BT_BYTES + H_BYTES + HEAD_BYTES;
   constexpr int ZS_BYTES = 128 * kZw * 4;
   constexpr int LDS_BYTES = ST_BYTES > ZS_BYTES ? ST_BYTES : ZS_BYTES;
   static_assert(MT == 2 && KC == 2, "H = 64");
   static_assert(KX >= 0 && KX <= 2 && EW <= kZw, "E = 32 or 64");
+  static_assert(!kHead || KX > 0, "the fused head reads the targets from the job's bytes in LDS");
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
   _Float16* et = reinterpret_cast<_Float16*>(lds);     // Emb+- parts: hi at et, lo at et + 256 EW
   unsigned char* bts = lds + EMB_BYTES;                 // bytes of row n, step t at bts[n T + t]
   _Float16* hs = reinterpret_cast<_Float16*>(lds + EMB_BYTES + BT_BYTES);   // buffer b, part q at hs + (2 b + q) PART
+  float2* red = reinterpret_cast<float2*>(lds + EMB_BYTES + BT_BYTES + H_BYTES);   // [parity][wave][row]
+  float* tgl = reinterpret_cast<float*>(lds + EMB_BYTES + BT_BYTES + H_BYTES + 2 * 8 * ROWS * 8);   // [parity][row]
+  __shared__ double dsum[ROWS];                         // the fused head's per-row cross-entropy sums
+  __shared__ unsigned wide;                             // some head row has L1 norm >= kNoShiftL1
   float* zs = reinterpret_cast<float*>(lds);
   const int job = blockIdx.x;
   if (job >= jobs) return;
@@ -1349,7 +1386,50 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
       }
     }
   }
+  // Head (kHead): wave w keeps vocabulary rows 32 w + 16 m + lr (m < 2) of
+  // Whead+- over all 64 columns as split fragments, the same layout as the
+  // recurrent rows, so the head's products take the same B fragments.  The
+  // rows' L1 norms decide whether the row maxima must be subtracted before
+  // exponentiating (as in k_head_fused: |h| < 1 bounds each logit by its
+  // row's L1 norm).
+  uint4 vh[kHead ? MT : 1][KC], vl[kHead ? MT : 1][KC];
+  if constexpr (kHead) {
+    const float seps_head = sg == 0 ? eps_of(a, e, kGroupHead) : -eps_of(a, e, kGroupHead);
+    float l1[MT] = {0.0f, 0.0f};
+    if (threadIdx.x == 0) wide = 0u;
+#pragma unroll
+    for (int rg = 0; rg < kVocab / 128; ++rg) {
+      __syncthreads();
+      for (int q = threadIdx.x; q < 128 * (H / 4); q += kLocalThreads) {
+        const int m = q / (H / 4), k4 = q % (H / 4);
+        *reinterpret_cast<float4*>(&zs[m * kZw + 4 * k4]) =
+            probe4(static_cast<uint64_t>(a.off_head + static_cast<int64_t>(128 * rg + m) * H + 4 * k4));
+      }
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const int row = 32 * wave + 16 * m + lr;
+        if (row / 128 != rg) continue;                 // wave-uniform
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+          const float* zr = &zs[(row - 128 * rg) * kZw + 32 * c + 8 * lg];
+          const float* tr = th + a.off_head + static_cast<int64_t>(row) * H + 32 * c + 8 * lg;
+          const float4 w0 = fma4(seps_head, *reinterpret_cast<const float4*>(zr), *reinterpret_cast<const float4*>(tr));
+          const float4 w1 =
+              fma4(seps_head, *reinterpret_cast<const float4*>(zr + 4), *reinterpret_cast<const float4*>(tr + 4));
+          in_range = in_range && split_range_ok(w0) && split_range_ok(w1);
+          split8v(w0, w1, vh[m][c], vl[m][c]);
+          l1[m] += ((fabsf(w0.x) + fabsf(w0.y)) + (fabsf(w0.z) + fabsf(w0.w))) +
+                   ((fabsf(w1.x) + fabsf(w1.y)) + (fabsf(w1.z) + fabsf(w1.w)));
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      if (group4_sum(l1[m]) >= kNoShiftL1) wide = 1u;
+  }
   __syncthreads();                                      // the scratch becomes the embedding table and the h buffers
+  const bool shift = !kHead || wide != 0u;              // block-uniform
 
   if constexpr (KX > 0) {
     // Emb+-[v][k] = theta[v E + k] +- eps z (canonical offset 0), split.
@@ -1391,10 +1471,19 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
     return static_cast<int>(
         __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(nb * 16 * T + tt), 0));
   };
-  // acc += h_{t-1} W_h+-^T, h_{t-1} read from buffer b.
-  auto h_products = [&](f32x4 (&acc)[MT][NB], int b) {
+  // acc += h_{t-1} W_h+-^T, h_{t-1} read from buffer b; with the fused head
+  // also hacc = h_{t-1} Whead+-^T (the logits of step t - 1) from the same
+  // fragments.  rec = false: the head's products alone (after the last step).
+  f32x4 hacc[kHead ? MT : 1][NB];
+  auto h_products = [&](f32x4 (&acc)[MT][NB], int b, bool rec) {
     const _Float16* bhi = hs + (2 * b) * PART + lr * HSW + 8 * lg;
     const _Float16* blo = bhi + PART;
+    if constexpr (kHead) {
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) hacc[m][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       uint4 bh[NB], bl[NB];
@@ -1403,8 +1492,76 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
         bh[nb] = *reinterpret_cast<const uint4*>(bhi + nb * 16 * HSW + 32 * kc);
         bl[nb] = *reinterpret_cast<const uint4*>(blo + nb * 16 * HSW + 32 * kc);
       }
+      if (rec) {
 #pragma unroll
-      for (int m = 0; m < MT; ++m) mfma3_batch<NB>(wh[m][kc], wl[m][kc], bh, bl, acc[m]);
+        for (int m = 0; m < MT; ++m) mfma3_batch<NB>(wh[m][kc], wl[m][kc], bh, bl, acc[m]);
+      }
+      if constexpr (kHead) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m) mfma3_batch<NB>(vh[m][kc], vl[m][kc], bh, bl, hacc[m]);
+      }
+    }
+  };
+  // Fused head, step tau's logits in hacc: this wave's (max, sum exp) over
+  // its 32 vocabulary rows for each batch row, into red[parity][wave], and
+  // the target logit of each row from the lane that holds it.
+  auto head_partials = [&](int tau, int par) {
+    if constexpr (kHead) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float m = 0.0f;
+      if (shift) {
+        m = fmaxf(fmaxf(fmaxf(hacc[0][nb][0], hacc[0][nb][1]), fmaxf(hacc[0][nb][2], hacc[0][nb][3])),
+                  fmaxf(fmaxf(hacc[1][nb][0], hacc[1][nb][1]), fmaxf(hacc[1][nb][2], hacc[1][nb][3])));
+        m = group4_max(m);
+      }
+      const float ml = -m * kLog2e;
+      float sum = 0.0f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sum += exp2_f(__builtin_fmaf(hacc[mt][nb][r], kLog2e, ml));
+      sum = group4_sum(sum);
+      const int n = nb * 16 + lr;
+      if (lg == 0) red[(par * 8 + wave) * ROWS + n] = make_float2(m, sum);
+      const int y = n < B ? bts[n * T + tau + 1] : 0;
+      if (n < B && (y >> 5) == wave && ((y >> 2) & 3) == lg) {
+        const int ym = (y >> 4) & 1, yr = y & 3;
+        float v = 0.0f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (mt == ym && r == yr) v = hacc[mt][nb][r];
+        tgl[par * ROWS + n] = v;
+      }
+    }
+    }
+  };
+  // The cross entropy of each batch row at one step from the 8 waves'
+  // partials (threads 0 .. B-1, one row each), merged, logged and the target
+  // subtracted in fp64, summed per row in fp64.
+  double cacc = 0.0;
+  auto head_combine = [&](int par) {
+    const int n = threadIdx.x;
+    if (kHead && n < B) {
+      float M = 0.0f;
+      double S = 0.0;
+      if (shift) {
+        M = red[par * 8 * ROWS + n].x;
+#pragma unroll
+        for (int w = 1; w < 8; ++w) M = fmaxf(M, red[(par * 8 + w) * ROWS + n].x);
+        const float ML = -M * kLog2e;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const float2 rw = red[(par * 8 + w) * ROWS + n];
+          S += static_cast<double>(rw.y * exp2_f(__builtin_fmaf(rw.x, kLog2e, ML)));
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 8; ++w) S += static_cast<double>(red[(par * 8 + w) * ROWS + n].y);
+      }
+      cacc += (log(S) + static_cast<double>(M)) - static_cast<double>(tgl[par * ROWS + n]);
     }
   };
   // Cell updates of step t; h_t into buffer b (split) and to the slot's
@@ -1424,7 +1581,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
       split2(h[0], h[1], hi, lo);
       *reinterpret_cast<uint32_t*>(dhi + n * HSW + unit0) = hi;
       *reinterpret_cast<uint32_t*>(dlo + n * HSW + unit0) = lo;
-      if (n < B) {
+      if (!kHead && n < B) {                            // the fused head needs no h in HBM
         typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
         __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(h[0]), __float_as_uint(h[1])}, hbuf,
                                               static_cast<uint32_t>(((t * B + n) * H + unit0) * 4), 0, 0);
@@ -1484,7 +1641,7 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
           for (int nb = 0; nb < NB; ++nb) vb[P][nb] = load_byte(nb, t + 4);
         }
       }
-      if (t > 0) h_products(acc, P ^ 1);                // h_{t-1}: buffer (t - 1) & 1
+      if (t > 0) h_products(acc, P ^ 1, true);          // h_{t-1}: buffer (t - 1) & 1
       cells(acc, t, P);
       __syncthreads();
     };
@@ -1526,14 +1683,39 @@ __global__ __launch_bounds__(kLocalThreads) void k_rec_local(FwdArgs a, int jobs
     f32x4 acc[MT][NB];
     bytes_at(vb, 0);
     x_products(acc, vb);
+    // With the fused head, step t also forms the logits of step t - 1 from
+    // h_{t-1} (its partials into parity t & 1) and merges those of step t - 2
+    // (parity (t - 1) & 1, written before the previous barrier).
     for (int t = 0; t + 1 < T; ++t) {
-      if (t > 0) h_products(acc, (t & 1) ^ 1);          // h_{t-1}: buffer (t - 1) & 1
+      if (t > 0) h_products(acc, (t & 1) ^ 1, true);    // h_{t-1}: buffer (t - 1) & 1
+      if constexpr (kHead) {
+        if (t > 1) head_combine((t - 1) & 1);
+        if (t > 0) head_partials(t - 1, t & 1);
+      }
       cells(acc, t, t & 1);
       if (t + 2 < T) {                                  // step t + 1 exists
         bytes_at(vb, t + 1);
         x_products(acc, vb);
       }
       __syncthreads();
+    }
+    if constexpr (kHead) {
+      // The last step's logits (h_{T-2}, buffer (T - 2) & 1), then the
+      // block's cross-entropy sum: part[slot][0], the other tiles 0.
+      const int tl = T - 2;
+      if (tl > 0) head_combine(tl & 1);
+      h_products(acc, tl & 1, false);
+      head_partials(tl, (tl + 1) & 1);
+      __syncthreads();
+      head_combine((tl + 1) & 1);
+      if (threadIdx.x < ROWS) dsum[threadIdx.x] = cacc;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        double tot = 0.0;
+        for (int n = 0; n < ROWS; ++n) tot += dsum[n];
+        a.part[slot * a.row_tiles] = tot;
+      }
+      for (int i = 1 + static_cast<int>(threadIdx.x); i < a.row_tiles; i += kLocalThreads) a.part[slot * a.row_tiles + i] = 0.0;
     }
   }
 }
@@ -1893,7 +2075,6 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_head_stream(
 // waiting for the staged tile waits for nothing else.
 // ---------------------------------------------------------------------------
 constexpr int kHeadFusedThreads = 1024;
-constexpr float kNoShiftL1 = 64.0f;
 
 template <int NCH, bool kRad>
 __global__ __launch_bounds__(kHeadFusedThreads) void k_head_fused(FwdArgs a) {
