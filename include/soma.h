@@ -98,9 +98,17 @@ enum soma_flags {
   /* Run the recurrence as one launch per time step with fp32 matrix
    * products (probes regenerated per step), even where the persistent, the
    * one-block (H = 64) or the split-product per-step kernel applies.  Those
-   * form each fp32 product from fp16 parts (x = hi + lo, three products,
-   * about 2^-21 relative per operand), so results agree within that
-   * rounding; this path is the fp32 reference. */
+   * form each fp32 product from fp16 parts: x = hi + lo, both rounded toward
+   * zero, and a b = a_hi b_lo + a_lo b_hi + a_hi b_hi with fp32
+   * accumulation.  For |x| <= 65504 the split's error is at most
+   * 2^-21 |x| + 2^-24 (about 21 significant bits from |x| = 2^-3 up, fewer
+   * below, where the parts fall into fp16's subnormals), so results agree
+   * within that rounding; this path is the fp32 reference.  A perturbed
+   * weight outside +-65504, or NaN, aborts the step on the device (losses
+   * read NaN, theta and the Adam moments are left untouched); activations
+   * are bounded by the cell (|h| < 1).  For SOMA_ARCH_BODY every folded
+   * matrix weight must stay within +-256 and every decoder gain within
+   * +-4096, which keeps each split operand of the body within +-65504. */
   SOMA_FLAG_PER_STEP_RECURRENCE = 1,
   /* Run the input projections of layers 2..L and the output head as row
    * tiles with fp32 matrix products that regenerate their probes per tile,

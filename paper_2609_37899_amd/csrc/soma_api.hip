@@ -1,14 +1,28 @@
 // soma_api.hip -- C ABI of the SOMA SPSA hot path on gfx950 (see soma.h).
 //
-// One step enqueues, per chunk of directions (all experts at once):
-//   k_fold        layer-1 gate inputs per byte value, both signs
-//   per layer l:  k_proj (l >= 2) then T-1 launches of k_rec_step
-//   k_head_ce     head + softmax cross entropy, per-tile sums
-//   k_loss_reduce fixed-order sums -> L_{e,j,+-}
+// A step of the stacked LSTM enqueues, per chunk of directions (all experts
+// at once, both signs of each direction side by side):
+//   k_fold          layer-1 gate inputs per byte value (embedding times the
+//                   input weights, perturbed rows formed on the fly)
+//   per layer l:    k_proj_stream (l >= 2: h^(l-1) times the input weights,
+//                   weights held in registers) then the recurrence:
+//                   k_rec_persist (one cooperative launch; blocks of a group
+//                   share the recurrent weights and exchange h each step),
+//                   k_rec_local (H = 64: one block per perturbed model, h in
+//                   LDS, for L = 1 with the head and cross entropy fused), or
+//                   one launch per time step (k_rec_step_split / k_rec_step)
+//   k_head_stream + k_ce_combine   head and softmax cross entropy (unless
+//                   fused into the recurrence)
+//   k_loss_reduce   fixed-order sums -> L_{e,j,+-} (fp64 means)
 // and then, once for the step:
-//   k_coef        c_{e,j} (independent) or c_j (summed)
-//   k_update      theta -= lr sum_j c_j z_j, regenerating every z_j
-// The step writes theta only in k_update, after every loss exists.
+//   k_coef          c_{e,j} (independent) or dF_j / (2 eps_e P) (summed)
+//   k_update / k_update_adam   theta -= lr sum_j c_j z_j, regenerating z_j
+// The paper's width-32 body (SOMA_ARCH_BODY) runs its whole perturbed
+// forward in k_body (soma_body.hpp).  Every kernel that forms split fp16
+// weights checks their range and the persistent recurrence bounds its waits:
+// either failure sets a sticky flag, and the step is then aborted on the
+// device (NaN losses, theta untouched).  The step writes theta only in the
+// update kernel, after every loss exists.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
