@@ -109,7 +109,7 @@ VOCAB = 256
 PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 
 
-ARCH_LSTM, ARCH_PAPER_BODY = 0, 1
+ARCH_LSTM, ARCH_PAPER_BODY, ARCH_WIDE = 0, 1, 2
 # perturb_mask bits: the parameter groups that are perturbed and updated
 # (0 = all of them).
 PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD = 1, 2, 4
@@ -117,8 +117,9 @@ PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD = 1, 2, 4
 
 def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode=0,
              probe=PROBE_GAUSSIAN, accum=1, arch=ARCH_LSTM, tied_head=None, perturb_mask=0):
-    """tied_head (arch 1): the frozen tied matrix E, [V][d] (shared by all
-    experts) or [N][V][d] (one per expert); the configuration keeps it alive.
+    """tied_head (arch 1, 2): the tied matrix E, [V][w] (shared by all
+    experts) or [N][V][w] (one per expert), w = hidden for arch 1 and
+    w = embed for arch 2; the configuration keeps it alive.
     perturb_mask: PERTURB_* bits of the perturbed and updated groups (0: all)."""
     cfg = OracleCfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_mode, probe, accum,
                     arch, None, 0, perturb_mask)
@@ -126,7 +127,7 @@ def make_cfg(n_experts, n_layers, embed, hidden, batch, seq_len, n_pairs, loss_m
         h = np.ascontiguousarray(tied_head, dtype=np.float32)
         cfg._head_ref = h
         cfg.tied_head = h.ctypes.data
-        cfg.head_stride = 0 if h.ndim == 2 else VOCAB * hidden
+        cfg.head_stride = 0 if h.ndim == 2 else VOCAB * (embed if arch == ARCH_WIDE else hidden)
     return cfg
 
 
@@ -140,12 +141,12 @@ def cfg_from(shape) -> OracleCfg:
 
 
 def head_delta(cfg: OracleCfg, theta_e, bytes_e):
-    """(mean CE, dE [V][d] fp64): the decoder-path derivative of the
-    unperturbed loss with respect to the tied matrix (arch 1; one expert,
-    cfg.tied_head pointing at its E)."""
+    """(mean CE, dE [V][w] fp64): the decoder-path derivative of the
+    unperturbed loss with respect to the tied matrix (arch 1 or 2; one
+    expert, cfg.tied_head pointing at its E)."""
     t = np.ascontiguousarray(theta_e, dtype=np.float32)
     b = np.ascontiguousarray(bytes_e, dtype=np.uint8)
-    g = np.empty((VOCAB, cfg.hidden), dtype=np.float64)
+    g = np.empty((VOCAB, cfg.embed if cfg.arch == ARCH_WIDE else cfg.hidden), dtype=np.float64)
     loss = _load().oracle_head_delta(ctypes.byref(cfg), _ptr(t, ctypes.c_float), _ptr(b, ctypes.c_uint8),
                                      _ptr(g, ctypes.c_double))
     return float(loss), g

@@ -20,7 +20,14 @@
  *   - a plain stacked LSTM byte model: embedding -> LSTM_1 -> ... -> LSTM_L ->
  *     linear head (the experts' recurrent body, Section 3 and Appendix C),
  *     bias-free as in Appendix C, gates in the order i, f, g, o;
- *   - the update theta' = theta - lr * g_hat (plain SGD step on g_hat).
+ *   - the paper's expert body (arch 1: pre-norm residual LSTM and GELU-MLP
+ *     blocks with gain-only LayerNorm and the frozen tied E, Appendix C) and
+ *     the body of its wider fixed-size controls (arch 2: the same blocks at
+ *     width d_t between input and output projections to the head width d_E,
+ *     with each expert's own tied E, Appendix C and E), and the decoder-path
+ *     delta rule for E (Appendix E, Eq. delta);
+ *   - the update theta' = theta - lr * g_hat (plain SGD step on g_hat) and the
+ *     paper's Adam-style update with coupled weight decay (Appendix E).
  *
  * Probe laws (cfg.probe), all from counter-based Philox4x32-10 (Salmon,
  * Moraes, Dror, Shaw, SC'11, "Parallel random numbers: as easy as 1, 2, 3"):
@@ -30,8 +37,8 @@
  *      operations, reproducible bit for bit on any conforming machine.
  *   1  sparse Rademacher, the paper's training law (Appendix E): each
  *      coordinate is 0 with probability 1/2 and -1 or +1 with probability
- *      1/4 each (the paper's normalization gains, which are always +-1, do
- *      not occur in this model).
+ *      1/4 each; the normalization gains of arch 1 and 2 are always +-1
+ *      (Appendix E).
  *   2  dense Rademacher, the law of the paper's variance theory (Section 4,
  *      Eq. main-spsa; Appendix F, Prop. block-variance): -1 or +1 with
  *      probability 1/2 each.
@@ -71,8 +78,9 @@ typedef struct {
   int32_t loss_mode; /* 0: independent per-expert losses, 1: summed loss */
   int32_t probe;     /* probe law: 0 Gaussian, 1 sparse Rademacher, 2 dense Rademacher */
   int32_t accum;     /* A accumulation batches per update (0 or 1: one batch) */
-  int32_t arch;      /* 0: stacked LSTM + linear head; 1: the paper's expert body (see below) */
-  const float *tied_head; /* arch 1: the frozen tied embedding/decoder E [V][d] of expert 0 */
+  int32_t arch;      /* 0: stacked LSTM + linear head; 1: the paper's expert body; 2: the body of
+                        the wide controls (both below) */
+  const float *tied_head; /* arch 1, 2: the tied embedding/decoder E [V][head width] of expert 0 */
   int64_t head_stride;    /* floats from one expert's E to the next (0: one shared E) */
   uint32_t perturb_mask;  /* perturbed parameter groups: bit 0 embedding, bit 1 LSTM layers (the
                              whole body for arch 1), bit 2 head; 0 means all of them */
@@ -108,13 +116,46 @@ static int64_t off_layer(const oracle_cfg *c, int l) {
 
 static int64_t body_block(int64_t d) { return 16 * d * d + 2 * d; }
 
+/* The body of the wider fixed-size controls (arch 2; Appendix C, counting
+ * rules and Table fixed-parameter-counts): the same D blocks at width
+ * d_t = hidden, between input and output projections to the head width
+ * d_E = embed, so the count is 16 D d_t^2 + (2D + 1) d_t + 2 d_E d_t.  The
+ * head E [V][d_E] is tied between input and output within an expert, local
+ * to it and never perturbed (Appendix E): x_0 = P_in E[byte]; the blocks as
+ * in arch 1; f = LayerNorm(x; g_f); the decoder input is u = P_out f and the
+ * logits are E u.  Where the projections sit is fixed only by the count; the
+ * reading here puts them at the two ends of the body.
+ * Layout (canonical k; every matrix row a multiple of 4 long, so that a probe
+ * quad never straddles two rows):
+ *   P_in [d_t][d_E]             x_0[c] = sum_q P_in[c][q] E[byte][q]
+ *   per block l:
+ *     A_l [d_t][4 d_t]          LSTM input weights, a[j] = sum_c n[c] A_l[c][j]
+ *     R_l [d_t][4 d_t]          LSTM recurrent weights, a[j] += sum_c h[c] R_l[c][j]
+ *                               (j = gate g d_t + unit, gates i, f, g, o)
+ *     U_l [d_t][4 d_t]          MLP up, m[j] = GELU(sum_c n[c] U_l[c][j])
+ *     V_l [d_t][4 d_t]          MLP down, x[c] += sum_j V_l[c][j] m[j]
+ *   P_out [d_t][d_E]            u[q] = sum_c f[c] P_out[c][q]
+ *   gains: g1_l, g2_l for l = 1..D, then g_f (each d_t long)            */
+static int64_t wide_off_block(const oracle_cfg *c, int l) {
+  const int64_t d = c->hidden;
+  return d * c->embed + (int64_t)l * 16 * d * d;
+}
+static int64_t wide_off_gain(const oracle_cfg *c) {
+  return wide_off_block(c, c->n_layers) + (int64_t)c->hidden * c->embed;
+}
+
 int64_t oracle_param_count(const oracle_cfg *c) {
   if (c->arch == 1) return c->n_layers * body_block(c->hidden) + c->hidden;
+  if (c->arch == 2) return wide_off_gain(c) + (2LL * c->n_layers + 1) * c->hidden;
   return off_layer(c, c->n_layers) + (int64_t)VOCAB * c->hidden;
 }
 
+/* Width of the tied head E: d = d_t for arch 1, d_E for arch 2. */
+static int head_width(const oracle_cfg *c) { return c->arch == 2 ? c->embed : c->hidden; }
+
 /* Whether coordinate k of the body is a LayerNorm gain. */
 static int body_is_gain(const oracle_cfg *c, int64_t k) {
+  if (c->arch == 2) return k >= wide_off_gain(c);
   const int64_t d = c->hidden, blk = body_block(d);
   if (k >= c->n_layers * blk) return 1;               /* g_f */
   const int64_t r = k % blk;
@@ -125,11 +166,12 @@ static int body_is_gain(const oracle_cfg *c, int64_t k) {
  * paper keeps parts of the model out of the search: its decoder/embedding E
  * is never perturbed and only the body is (Section 4; Appendix E).  For the
  * stacked LSTM the groups are the embedding (bit 0), the LSTM layers (bit 1)
- * and the head (bit 2); the body of arch 1 is one group (bit 1).  A masked
- * coordinate keeps its value in every perturbed forward and in the update. */
+ * and the head (bit 2); the body of arch 1 or 2 is one group (bit 1).  A
+ * masked coordinate keeps its value in every perturbed forward and in the
+ * update. */
 static int coord_perturbed(const oracle_cfg *c, int64_t k) {
   const uint32_t m = c->perturb_mask ? c->perturb_mask : 7u;
-  if (c->arch == 1) return (int)((m >> 1) & 1u);
+  if (c->arch != 0) return (int)((m >> 1) & 1u);
   const int grp = k < (int64_t)VOCAB * c->embed ? 0 : (k < off_layer(c, c->n_layers) ? 1 : 2);
   return (int)((m >> grp) & 1u);
 }
@@ -137,7 +179,7 @@ static int coord_perturbed(const oracle_cfg *c, int64_t k) {
 /* The probe law of coordinate k: under the paper's sparse law its
  * normalization gains are dense +-1 (Appendix E); otherwise the configured law. */
 static int law_of(const oracle_cfg *c, int64_t k) {
-  return (c->arch == 1 && c->probe == 1 && body_is_gain(c, k)) ? 2 : c->probe;
+  return (c->arch != 0 && c->probe == 1 && body_is_gain(c, k)) ? 2 : c->probe;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -497,29 +539,121 @@ static double sequence_ce_sum_body(const oracle_cfg *c, const double *w, const d
   return total;
 }
 
+/* Sum of next-byte cross entropies of one sequence under the wide controls'
+ * body (arch 2), E the expert's tied matrix [V][d_E] (fp64).  When dE != NULL
+ * the decoder-path derivative (p - onehot(y)) u^T of every target, u the
+ * decoder input, is added to dE [V][d_E] (Appendix E, Eq. delta). */
+static double sequence_ce_sum_wide(const oracle_cfg *c, const double *w, const double *E, const uint8_t *seq,
+                                   double *scratch, double *dE) {
+  const int D = c->n_layers, d = c->hidden, dE_ = c->embed, T = c->seq_len;
+  const int64_t d4 = 4 * (int64_t)d;
+  double *h = scratch;                  /* [D][d] */
+  double *cs = h + (size_t)D * d;       /* [D][d] */
+  double *x = cs + (size_t)D * d;       /* [d] */
+  double *n = x + d;                    /* [d] */
+  double *a = n + d;                    /* [4d] */
+  double *m = a + d4;                   /* [4d] */
+  double *u = m + d4;                   /* [d_E] */
+  double *logits = u + dE_;             /* [V] */
+  memset(h, 0, sizeof(double) * 2 * (size_t)D * d);
+  const double *Pin = w, *Pout = w + wide_off_block(c, D), *gains = w + wide_off_gain(c);
+  const double *gf = gains + 2 * (size_t)D * d;
+  double total = 0.0;
+  for (int t = 0; t + 1 < T; ++t) {
+    const double *ey = E + (size_t)seq[t] * dE_;
+    for (int k = 0; k < d; ++k) {                               /* input projection */
+      double acc = 0.0;
+      for (int q = 0; q < dE_; ++q) acc += Pin[(size_t)k * dE_ + q] * ey[q];
+      x[k] = acc;
+    }
+    for (int l = 0; l < D; ++l) {
+      const double *A = w + wide_off_block(c, l), *R = A + d4 * d, *U = R + d4 * d, *Vd = U + d4 * d;
+      const double *g1 = gains + 2 * (size_t)l * d, *g2 = g1 + d;
+      double *hl = h + (size_t)l * d, *cl = cs + (size_t)l * d;
+      layer_norm(x, g1, d, n);                                   /* LSTM sublayer */
+      for (int64_t j = 0; j < d4; ++j) {
+        double acc = 0.0;
+        for (int k = 0; k < d; ++k) acc += n[k] * A[(size_t)k * d4 + j];
+        for (int k = 0; k < d; ++k) acc += hl[k] * R[(size_t)k * d4 + j];
+        a[j] = acc;
+      }
+      for (int q = 0; q < d; ++q) {
+        const double ig = sigmoid(a[q]), fg = sigmoid(a[d + q]), gg = tanh(a[2 * d + q]),
+                     og = sigmoid(a[3 * d + q]);
+        cl[q] = fg * cl[q] + ig * gg;
+        hl[q] = og * tanh(cl[q]);
+      }
+      for (int k = 0; k < d; ++k) x[k] += hl[k];                 /* residual */
+      layer_norm(x, g2, d, n);                                   /* MLP sublayer */
+      for (int64_t j = 0; j < d4; ++j) {
+        double acc = 0.0;
+        for (int k = 0; k < d; ++k) acc += n[k] * U[(size_t)k * d4 + j];
+        m[j] = gelu(acc);
+      }
+      for (int k = 0; k < d; ++k) {
+        double acc = 0.0;
+        for (int64_t j = 0; j < d4; ++j) acc += Vd[(size_t)k * d4 + j] * m[j];
+        x[k] += acc;                                             /* residual */
+      }
+    }
+    layer_norm(x, gf, d, n);                                     /* f */
+    for (int q = 0; q < dE_; ++q) {                              /* output projection: u */
+      double acc = 0.0;
+      for (int k = 0; k < d; ++k) acc += n[k] * Pout[(size_t)k * dE_ + q];
+      u[q] = acc;
+    }
+    double mx = -INFINITY;
+    for (int v = 0; v < VOCAB; ++v) {
+      double acc = 0.0;
+      for (int q = 0; q < dE_; ++q) acc += E[(size_t)v * dE_ + q] * u[q];
+      logits[v] = acc;
+      if (acc > mx) mx = acc;
+    }
+    double se = 0.0;
+    for (int v = 0; v < VOCAB; ++v) se += exp(logits[v] - mx);
+    const int y = seq[t + 1];
+    total += log(se) + mx - logits[y];
+    if (dE)
+      for (int v = 0; v < VOCAB; ++v) {
+        const double pv = exp(logits[v] - mx) / se - (v == y ? 1.0 : 0.0);
+        for (int q = 0; q < dE_; ++q) dE[(size_t)v * dE_ + q] += pv * u[q];
+      }
+  }
+  return total;
+}
+
+static double sequence_ce_sum_head(const oracle_cfg *c, const double *w, const double *E, const uint8_t *seq,
+                                   double *scratch, double *dE) {
+  return c->arch == 2 ? sequence_ce_sum_wide(c, w, E, seq, scratch, dE)
+                      : sequence_ce_sum_body(c, w, E, seq, scratch, dE);
+}
+
+static size_t scratch_doubles(const oracle_cfg *c);
+
 static double *head_f64(const oracle_cfg *c) {
-  const size_t nE = (size_t)VOCAB * c->hidden;
+  const size_t nE = (size_t)VOCAB * head_width(c);
   double *E = (double *)malloc(sizeof(double) * nE);
   for (size_t i = 0; i < nE; ++i) E[i] = (double)c->tied_head[i];
   return E;
 }
 
 /* The decoder-path derivative of the unperturbed mean cross entropy with
- * respect to the tied matrix (Appendix E, Eq. delta), one expert (arch 1):
+ * respect to the tied matrix (Appendix E, Eq. delta), one expert (arch 1 or 2):
  *   dE = (1 / (B (T-1))) sum_{b,t} (p_{b,t} - onehot(y_{b,t+1})) f_{b,t}^T,
- * holding the decoder inputs f fixed.  grad [V][d] fp64 out.  Returns the
- * mean cross entropy, or NaN for a configuration that is not arch 1. */
+ * holding the decoder inputs f fixed (f = LayerNorm(x; g_f) for arch 1, the
+ * output projection u for arch 2).  grad [V][head width] fp64 out.  Returns
+ * the mean cross entropy, or NaN for a configuration without a tied head. */
 double oracle_head_delta(const oracle_cfg *c, const float *theta, const uint8_t *bytes, double *grad) {
-  if (c->arch != 1 || !c->tied_head) return NAN;
-  const int B = c->batch, T = c->seq_len, d = c->hidden;
+  if ((c->arch != 1 && c->arch != 2) || !c->tied_head) return NAN;
+  const int B = c->batch, T = c->seq_len, d = head_width(c);
   const int64_t nd = oracle_param_count(c);
   double *w = (double *)malloc(sizeof(double) * (size_t)nd);
   for (int64_t k = 0; k < nd; ++k) w[k] = (double)theta[k];
   double *E = head_f64(c);
-  double *scratch = (double *)malloc(sizeof(double) * (4 * (size_t)c->n_layers * d + 12 * (size_t)d + VOCAB));
+  double *scratch = (double *)malloc(sizeof(double) * scratch_doubles(c));
   memset(grad, 0, sizeof(double) * (size_t)VOCAB * d);
   double total = 0.0;
-  for (int b = 0; b < B; ++b) total += sequence_ce_sum_body(c, w, E, bytes + (size_t)b * T, scratch, grad);
+  for (int b = 0; b < B; ++b) total += sequence_ce_sum_head(c, w, E, bytes + (size_t)b * T, scratch, grad);
   const double inv = 1.0 / ((double)B * (double)(T - 1));
   for (size_t i = 0; i < (size_t)VOCAB * d; ++i) grad[i] *= inv;
   free(scratch);
@@ -531,6 +665,7 @@ double oracle_head_delta(const oracle_cfg *c, const float *theta, const uint8_t 
 static size_t scratch_doubles(const oracle_cfg *c) {
   const size_t L = c->n_layers, E = c->embed, H = c->hidden;
   if (c->arch == 1) return 2 * L * H + 10 * H + VOCAB;
+  if (c->arch == 2) return 2 * L * H + 10 * H + E + VOCAB;
   return 2 * L * H + (E > H ? E : H) + 4 * H + VOCAB;
 }
 
@@ -541,13 +676,13 @@ double oracle_forward_loss_f64(const oracle_cfg *c, const double *w, const uint8
   const int B = c->batch, T = c->seq_len;
   double *seq_sum = (double *)malloc(sizeof(double) * (size_t)B);
   const size_t ns = scratch_doubles(c);
-  double *E = c->arch == 1 ? head_f64(c) : NULL;
+  double *E = c->arch != 0 ? head_f64(c) : NULL;
 #pragma omp parallel
   {
     double *scratch = (double *)malloc(sizeof(double) * ns);
 #pragma omp for schedule(dynamic, 1)
     for (int b = 0; b < B; ++b)
-      seq_sum[b] = c->arch == 1 ? sequence_ce_sum_body(c, w, E, bytes + (size_t)b * T, scratch, NULL)
+      seq_sum[b] = c->arch != 0 ? sequence_ce_sum_head(c, w, E, bytes + (size_t)b * T, scratch, NULL)
                                 : sequence_ce_sum(c, w, bytes + (size_t)b * T, scratch);
     free(scratch);
   }
@@ -692,8 +827,9 @@ int oracle_spsa_step_rates(const oracle_cfg *c, const float *theta, const uint64
                            float *theta_out, double *ghat) {
   const int N = c->n_experts, P = total_dirs(c), Pb = c->n_pairs;
   if (N < 1 || Pb < 1 || c->n_layers < 1 || c->embed < 1 || c->hidden < 1 || c->batch < 1 ||
-      c->seq_len < 2 || c->probe < 0 || c->probe > 2 || c->accum < 0 || c->arch < 0 || c->arch > 1 ||
-      c->perturb_mask > 7u || (c->arch == 1 && (c->embed != c->hidden || !c->tied_head)))
+      c->seq_len < 2 || c->probe < 0 || c->probe > 2 || c->accum < 0 || c->arch < 0 || c->arch > 2 ||
+      c->perturb_mask > 7u || (c->arch == 1 && (c->embed != c->hidden || !c->tied_head)) ||
+      (c->arch == 2 && (c->embed % 4 != 0 || !c->tied_head)))
     return -1;
   const int64_t d = oracle_param_count(c);
   const size_t bstride = (size_t)c->batch * c->seq_len;
@@ -701,7 +837,7 @@ int oracle_spsa_step_rates(const oracle_cfg *c, const float *theta, const uint64
   /* 1-4: perturbed forwards, each on its expert's own batch (batch j / Pb of
    * the update for direction j). */
   for (int e = 0; e < N; ++e) {
-    oracle_cfg ce = *c;                      /* expert e's tied head (arch 1) */
+    oracle_cfg ce = *c;                      /* expert e's tied head (arch 1, 2) */
     if (c->tied_head) ce.tied_head = c->tied_head + e * c->head_stride;
     for (int j = 0; j < P; ++j)
       for (int s = 0; s < 2; ++s)

@@ -170,6 +170,37 @@ def init_body(n_experts: int, n_layers: int, d: int, init_seed: int = 0, distinc
     return np.stack(rows)
 
 
+def wide_param_count(n_layers: int, d_t: int, d_e: int) -> int:
+    """Size of one expert's perturbed vector for the wide controls' body:
+    16 D d_t^2 + (2D + 1) d_t + 2 d_E d_t (the head E is separate)."""
+    return 16 * n_layers * d_t * d_t + (2 * n_layers + 1) * d_t + 2 * d_e * d_t
+
+
+def init_wide(n_experts: int, n_layers: int, d_t: int, d_e: int, init_seed: int = 0,
+              distinct: bool = False) -> np.ndarray:
+    """[N][params] float32 for the wide controls' body, in its canonical order
+    (P_in [d_t][d_E]; per block A, R, U, V [d_t][4 d_t]; P_out [d_t][d_E];
+    gains g1, g2 per block and g_f): matrices U(-a, a) with a = 1 / sqrt(fan-in),
+    gains 1 + 0.1 N(0, 1)."""
+    rows = []
+    d4 = 4 * d_t
+    for e in range(n_experts if distinct else 1):
+        ss = np.random.SeedSequence([int(init_seed), e, 13] if distinct else [int(init_seed), 13])
+        g = np.random.Generator(np.random.PCG64(ss))
+        parts = [g.uniform(-1, 1, d_t * d_e) / np.sqrt(d_e)]
+        for _ in range(n_layers):
+            parts += [g.uniform(-1, 1, d_t * d4) / np.sqrt(2 * d_t),     # A (input half of the gates)
+                      g.uniform(-1, 1, d_t * d4) / np.sqrt(2 * d_t),     # R (recurrent half)
+                      g.uniform(-1, 1, d_t * d4) / np.sqrt(d_t),         # U
+                      g.uniform(-1, 1, d_t * d4) / np.sqrt(d4)]          # V
+        parts.append(g.uniform(-1, 1, d_t * d_e) / np.sqrt(d_t))
+        parts.append(1.0 + 0.1 * g.standard_normal((2 * n_layers + 1) * d_t))
+        rows.append(np.concatenate(parts).astype(np.float32))
+    if not distinct:
+        rows = rows * n_experts
+    return np.stack(rows)
+
+
 def init_tied_head(d: int, init_seed: int = 0, n_experts: int = 0, scale: float = 0.3) -> np.ndarray:
     """The tied matrix E, N(0, scale^2) entries: [V][d] (shared), or
     [n_experts][V][d] (one per expert) when n_experts > 0."""
