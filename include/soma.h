@@ -154,11 +154,34 @@ enum soma_arch {
    * +-1 (Appendix E); every other coordinate follows soma_config.probe.
    * Supported: d in {16, 32}, D in {1, 2} (one perturbed body and E fit in
    * one compute unit's LDS); flags must be 0. */
-  SOMA_ARCH_BODY = 1
+  SOMA_ARCH_BODY = 1,
+  /* The body of the paper's wider fixed-size controls (Appendix C, counting
+   * rules and Table fixed-parameter-counts; Appendix E): the blocks of
+   * SOMA_ARCH_BODY at width d_t = hidden between an input projection from
+   * the head width d_E = embed and an output projection back to it,
+   *   x_0 = P_in E[byte];  the D blocks;  f = LN(x; g_f);  u = P_out f;
+   *   logits = u E^T,
+   * with each expert's own tied matrix E [256][d_E] (soma_set_tied_head with
+   * a nonzero stride), which the perturbation never touches and only the
+   * delta rule updates (soma_head_delta; u is the decoder input).  Parameters
+   * of one expert, canonical order (every matrix row a multiple of 4 long,
+   * so that a probe quad lies in one row of one matrix):
+   *   P_in[d_t][d_E]; per block A[d_t][4 d_t] (LSTM input weights, column
+   *   g d_t + u for gate g = i, f, g, o of unit u), R[d_t][4 d_t] (recurrent
+   *   weights, same columns), U[d_t][4 d_t] (MLP up), V[d_t][4 d_t] (MLP
+   *   down, row = output feature); P_out[d_t][d_E]; then the gains g1, g2
+   *   of every block and g_f, d_t each:
+   *   d_e = 16 D d_t^2 + (2 D + 1) d_t + 2 d_E d_t.
+   * Under the sparse probe law the gains draw dense +-1.  The whole body is
+   * one group (SOMA_PERTURB_LSTM).  Supported: d_E = 32, 4 <= d_t <= 512
+   * (padded inside to a multiple of 64), batch <= 64, one slot's gate inputs
+   * B (T-1) 4 d_p floats under 2^31 bytes; flags must be 0; the recurrence
+   * needs a device with cooperative launches (SOMA_EDEVICE otherwise). */
+  SOMA_ARCH_WIDE = 2
 };
 
 /* Shape of one SPSA step.  Constraints: n_experts, n_layers, n_pairs >= 1;
- * embed and hidden positive multiples of 16; batch >= 1; seq_len >= 2;
+ * embed and hidden positive multiples of 16 (SOMA_ARCH_WIDE: see there); batch >= 1; seq_len >= 2;
  * accum >= 0; pair_chunk in [0, D] (0 picks a chunk that keeps the workspace
  * under 64 GiB; the step processes its D directions in chunks of this many,
  * which changes memory use but not the result); flags: enum soma_flags.
@@ -332,27 +355,31 @@ int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta_dev, float* m_dev, flo
 int soma_eval_loss(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev,
                    float* loss_dev, void* stream);
 
-/* The tied matrix E of an SOMA_ARCH_BODY context (Appendix C): expert e
- * reads E_dev + e * expert_stride, [256][d] fp32 row-major (device, 16-byte
- * aligned, expert_stride a multiple of 4 floats; 0 = one E shared by every
- * expert, the paper's frozen width-32 head).  The context keeps the pointer,
- * not a copy: the memory must stay valid and unchanged while any step or
+/* The tied matrix E of an SOMA_ARCH_BODY or SOMA_ARCH_WIDE context
+ * (Appendix C): expert e reads E_dev + e * expert_stride, [256][w] fp32
+ * row-major with w = d (SOMA_ARCH_BODY) or w = d_E = embed (SOMA_ARCH_WIDE)
+ * (device, 16-byte aligned, expert_stride a multiple of 4 floats; 0 = one E
+ * shared by every expert, the paper's frozen width-32 head; the wide
+ * controls give every expert its own).  The context keeps the pointer, not
+ * a copy: the memory must stay valid and unchanged while any step or
  * evaluation that reads it runs.  Every step, evaluation and
- * soma_head_delta() on an SOMA_ARCH_BODY context returns SOMA_EINVAL until
- * it is set; SOMA_EINVAL on an SOMA_ARCH_LSTM context. */
+ * soma_head_delta() on such a context returns SOMA_EINVAL until it is set;
+ * SOMA_EINVAL on an SOMA_ARCH_LSTM context. */
 int soma_set_tied_head(soma_ctx* ctx, float* E_dev, int64_t expert_stride);
 
-/* The decoder-path delta rule of an SOMA_ARCH_BODY context (Appendix E,
- * Eq. delta): with the decoder inputs f_{b,t} of the unperturbed body held
- * fixed, for every expert
+/* The decoder-path delta rule of an SOMA_ARCH_BODY or SOMA_ARCH_WIDE
+ * context (Appendix E, Eq. delta): with the decoder inputs f_{b,t} of the
+ * unperturbed body held fixed (f = LN(x; g_f), or u = P_out f for the wide
+ * body), for every expert
  *   grad_e = (1 / (B (T-1))) sum_{b,t} (softmax(E_e f_{b,t}) - onehot(y_{b,t+1})) f_{b,t}^T,
- * a [256][d] matrix; the indirect path through the input embedding and the
- * body is deliberately left out.
+ * a [256][w] matrix (w as in soma_set_tied_head); the indirect path through
+ * the input embedding and the body is deliberately left out.  The wide
+ * controls apply it to every expert's own head (Appendix E).
  *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8 (device).
  *   lr        if nonzero, also E_e <- E_e - lr grad_e in place (plain
  *             descent on the rule; each expert must then own its E:
  *             expert_stride != 0 or N = 1).
- *   grad_dev  [N][256][d] fp32 out, or NULL.
+ *   grad_dev  [N][256][w] fp32 out, or NULL.
  *   loss_dev  [N] fp32 out (the unperturbed mean cross entropy, as
  *             soma_eval_loss), or NULL. */
 int soma_head_delta(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev, float lr, float* grad_dev,

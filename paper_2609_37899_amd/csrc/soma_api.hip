@@ -38,6 +38,7 @@
 #include "soma.h"
 #include "soma_kernels.hpp"
 #include "soma_body.hpp"
+#include "soma_wide.hpp"
 
 namespace {
 
@@ -74,10 +75,15 @@ struct Layout {
   int row_tiles = 0;   // head tiles per slot
   size_t sync = 0, rates = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, hpart = 0, htgt = 0,
          total = 0;
-  // the paper's body (SOMA_ARCH_BODY): decoder inputs, log-sum-exps and
-  // delta-rule partials of an evaluation pass
+  // the paper's body (SOMA_ARCH_BODY) and the wide controls' body
+  // (SOMA_ARCH_WIDE): decoder inputs, log-sum-exps and delta-rule partials
+  // of an evaluation pass
   size_t fdec = 0, lse = 0, dpart = 0;
   int delta_chunks = 0;
+  // SOMA_ARCH_WIDE: pre-formed weights and the residual stream per slot
+  // (hseq holds the normalised rows and the recurrence's h, gin the gate
+  // inputs and the MLP hidden layer)
+  size_t wform = 0, xres = 0;
 };
 
 // Directions per update: n_pairs per accumulation batch, accum batches.
@@ -92,6 +98,8 @@ unsigned group_mask(const soma_config& c) { return c.perturb_mask ? c.perturb_ma
 
 int64_t param_count_of(const soma_config& c) {
   if (c.arch == SOMA_ARCH_BODY) return c.n_layers * soma::body_block(c.hidden) + c.hidden;
+  if (c.arch == SOMA_ARCH_WIDE)
+    return 16LL * c.n_layers * c.hidden * c.hidden + (2LL * c.n_layers + 1) * c.hidden + 2LL * c.embed * c.hidden;
   int64_t d = int64_t(SOMA_VOCAB) * c.embed;
   for (int l = 0; l < c.n_layers; ++l)
     d += 4LL * c.hidden * ((l == 0 ? c.embed : c.hidden) + c.hidden);
@@ -104,9 +112,14 @@ int validate(const soma_config* c) {
     return fail(SOMA_ESHAPE, "n_experts, n_layers, n_pairs and batch must be >= 1");
   if (c->n_layers > 64) return fail(SOMA_ESHAPE, "at most 64 layers");
   if (c->seq_len < 2) return fail(SOMA_ESHAPE, "seq_len must be >= 2 (T-1 targets)");
-  if (c->embed < 16 || c->embed % 16 || c->hidden < 16 || c->hidden % 16)
+  if (c->arch == SOMA_ARCH_WIDE) {
+    if (c->embed != soma::kWideHeadWidth || c->hidden < 4 || c->hidden > 512)
+      return fail(SOMA_ESHAPE, "the wide body needs embed = %d and 4 <= hidden <= 512 (got %d, %d)",
+                  soma::kWideHeadWidth, c->embed, c->hidden);
+  } else if (c->embed < 16 || c->embed % 16 || c->hidden < 16 || c->hidden % 16) {
     return fail(SOMA_ESHAPE, "embed and hidden must be positive multiples of 16 (got %d, %d)",
                 c->embed, c->hidden);
+  }
   if (c->loss_mode != SOMA_LOSS_INDEPENDENT && c->loss_mode != SOMA_LOSS_SUMMED)
     return fail(SOMA_EINVAL, "loss_mode must be 0 (independent) or 1 (summed)");
   if (c->accum < 0) return fail(SOMA_ESHAPE, "accum must be >= 0 (0 or 1: one batch)");
@@ -119,11 +132,11 @@ int validate(const soma_config* c) {
   if (c->probe != SOMA_PROBE_GAUSSIAN && c->probe != SOMA_PROBE_SPARSE_RADEMACHER &&
       c->probe != SOMA_PROBE_RADEMACHER)
     return fail(SOMA_EINVAL, "probe must be 0 (Gaussian), 1 (sparse Rademacher) or 2 (Rademacher)");
-  if (c->arch != SOMA_ARCH_LSTM && c->arch != SOMA_ARCH_BODY)
-    return fail(SOMA_EINVAL, "arch must be 0 (stacked LSTM) or 1 (the paper's body)");
+  if (c->arch != SOMA_ARCH_LSTM && c->arch != SOMA_ARCH_BODY && c->arch != SOMA_ARCH_WIDE)
+    return fail(SOMA_EINVAL, "arch must be 0 (stacked LSTM), 1 (the paper's body) or 2 (the wide controls' body)");
   if (c->perturb_mask > SOMA_PERTURB_ALL)
     return fail(SOMA_EINVAL, "perturb_mask must be a combination of SOMA_PERTURB_* bits (got %u)", c->perturb_mask);
-  if (c->arch == SOMA_ARCH_BODY && !(group_mask(*c) & SOMA_PERTURB_LSTM))
+  if (c->arch != SOMA_ARCH_LSTM && !(group_mask(*c) & SOMA_PERTURB_LSTM))
     return fail(SOMA_EINVAL, "the body's parameters are one group: perturb_mask must include SOMA_PERTURB_LSTM");
   if (c->arch == SOMA_ARCH_BODY) {
     if (c->embed != c->hidden || (c->hidden != 16 && c->hidden != 32) || c->n_layers > 2)
@@ -133,6 +146,13 @@ int validate(const soma_config* c) {
     const int64_t blocks = int64_t((c->batch + soma::kBodySeqs - 1) / soma::kBodySeqs) * c->n_experts * 2 *
                            (int64_t(c->n_pairs) * (c->accum > 1 ? c->accum : 1));
     if (blocks >= (int64_t(1) << 31)) return fail(SOMA_ESHAPE, "too many body blocks in one step");
+  }
+  if (c->arch == SOMA_ARCH_WIDE) {
+    if (c->flags) return fail(SOMA_EINVAL, "flags select stacked-LSTM kernels and must be 0 for the wide body");
+    if (c->batch > 64) return fail(SOMA_ESHAPE, "the wide body's recurrence takes batch <= 64 (got %d)", c->batch);
+    const int64_t dp = soma::wide_padded(c->hidden);
+    if (int64_t(c->seq_len - 1) * c->batch * 4 * dp * int64_t(sizeof(float)) >= (int64_t(1) << 31))
+      return fail(SOMA_ESHAPE, "one slot's gate inputs, B (T-1) 4 d_p floats, must stay below 2^31 bytes");
   }
   const int64_t d = param_count_of(*c);
   if (d >= (int64_t(1) << 40)) return fail(SOMA_ESHAPE, "expert too large (d >= 2^40)");
@@ -162,11 +182,44 @@ Layout layout_for_body(const soma_config& c, int pc) {
   return L;
 }
 
+// The wide controls' body: per slot of a pass its pre-formed weights, the
+// per-byte input projection U, the residual stream x, the normalised rows
+// (shared with the recurrence's h: each reader is done before the next
+// writer) and the gate inputs (shared with the MLP hidden layer).
+Layout layout_for_wide(const soma_config& c, int pc) {
+  Layout L;
+  L.d = param_count_of(c);
+  L.pc = pc;
+  const size_t N = c.n_experts, R = size_t(c.seq_len - 1) * c.batch, dp = soma::wide_padded(c.hidden);
+  L.row_tiles = int((R + soma::kWideHeadRows - 1) / soma::kWideHeadRows);
+  L.delta_chunks = int((R + soma::kDeltaChunk - 1) / soma::kDeltaChunk);
+  const size_t slots = std::max(N * size_t(pc) * 2, N);
+  const size_t form = size_t(soma::wide_form_layout(int(dp), c.n_layers).total);
+  const size_t E = soma::kWideHeadWidth;
+  size_t at = 0;
+  L.sync = at; at += round_up(sizeof(unsigned) * (kMaxGroups + 1));
+  L.rates = at; at += round_up(sizeof(float) * 2 * N);
+  L.coef = at; at += round_up(sizeof(float) * N * dirs(c));
+  L.lossd = at; at += round_up(sizeof(double) * N * dirs(c) * 2);
+  L.part = at; at += round_up(sizeof(double) * slots * L.row_tiles);
+  L.wform = at; at += round_up(sizeof(float) * slots * form);
+  L.U = at; at += round_up(sizeof(float) * slots * SOMA_VOCAB * dp);
+  L.xres = at; at += round_up(sizeof(float) * slots * R * dp);
+  L.hseq = at; at += round_up(sizeof(float) * slots * R * dp);
+  L.gin = at; at += round_up(sizeof(float) * slots * R * 4 * dp);
+  L.fdec = at; at += round_up(sizeof(float) * N * R * E);
+  L.lse = at; at += round_up(sizeof(float) * N * R);
+  L.dpart = at; at += round_up(sizeof(float) * N * L.delta_chunks * SOMA_VOCAB * E);
+  L.total = at;
+  return L;
+}
+
 bool stream_weights(const soma_config& c);
 bool local_embedding(const soma_config& c);
 
 Layout layout_for(const soma_config& c, int pc) {
   if (c.arch == SOMA_ARCH_BODY) return layout_for_body(c, pc);
+  if (c.arch == SOMA_ARCH_WIDE) return layout_for_wide(c, pc);
   Layout L;
   L.d = param_count_of(c);
   int64_t off = int64_t(SOMA_VOCAB) * c.embed;
@@ -225,7 +278,7 @@ struct soma_ctx {
   bool have_times;
   // device facts for the persistent recurrence
   int coop_blocks;                  // co-resident k_rec_persist blocks (0: path unavailable)
-  float* head;                      // SOMA_ARCH_BODY: the tied matrix E of expert 0 (caller owned)
+  float* head;                      // SOMA_ARCH_BODY, SOMA_ARCH_WIDE: the tied matrix E of expert 0 (caller owned)
   int64_t head_stride;              // floats from one expert's E to the next
   std::vector<hipEvent_t> events;   // pool, grows on demand
   std::vector<int> phase;           // phase closed by events[i]
@@ -364,6 +417,7 @@ struct LawMap {
   int64_t emb_end;     // first coordinate of the LSTM layers (the embedding precedes it)
   int64_t head_start;  // first coordinate of the head
   unsigned mask;       // perturbed groups (kGroup* bits)
+  int64_t gain0;       // the wide controls' body: first gain (all gains follow); 0: none
 };
 
 // Whether the probe quad at coordinate k4 belongs to a perturbed group.
@@ -374,7 +428,9 @@ __device__ __forceinline__ bool quad_perturbed(const LawMap& m, int64_t k4) {
 }
 
 __device__ __forceinline__ int law_at(const LawMap& m, int64_t k4) {
-  if (m.blk == 0 || m.law != kProbeSparseRademacher) return m.law;
+  if (m.law != kProbeSparseRademacher) return m.law;
+  if (m.gain0 > 0) return k4 >= m.gain0 ? kProbeRademacher : m.law;   // gains at the end (a multiple of 4)
+  if (m.blk == 0) return m.law;
   const int64_t l = k4 / m.blk;
   if (l >= m.layers) return kProbeRademacher;                 // g_f
   const int64_t r = k4 - l * m.blk, w = 8 * m.dm * m.dm;
@@ -603,14 +659,14 @@ int rec_row_block(int B) { return B <= 16 ? 16 : (B <= 32 ? 32 : 64); }
 // (0 when the shape or the device rules it out; NW = persist_waves(H, B)).  The kernel addresses one
 // slot's gate inputs with 32-bit offsets, so B (T-1) 4H floats must stay
 // below 2^31 bytes.
-int persistent_groups(const soma_ctx* ctx, int jobs) {
+int persistent_groups_h(const soma_ctx* ctx, int jobs, int H) {
   const soma_config& c = ctx->cfg;
   if (c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) return 0;
-  if (ctx->coop_blocks <= 0 || c.hidden > soma::kRecMaxH || c.hidden % 64 != 0 || c.batch > 64)
+  if (ctx->coop_blocks <= 0 || H > soma::kRecMaxH || H % 64 != 0 || c.batch > 64)
     return 0;
-  const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * c.hidden * int64_t(sizeof(float));
+  const int64_t gin_slot_bytes = int64_t(c.seq_len - 1) * c.batch * 4 * H * int64_t(sizeof(float));
   if (gin_slot_bytes >= (int64_t(1) << 31)) return 0;
-  const int ut = c.hidden / (4 * soma::persist_waves(c.hidden, c.batch));
+  const int ut = H / (4 * soma::persist_waves(H, c.batch));
   int groups = std::min(ctx->coop_blocks / ut, jobs);
   // Group g owns blocks g + k groups and blocks are dealt to the 8 XCDs
   // round-robin, so with a multiple of 8 groups every group sits on one XCD
@@ -620,6 +676,8 @@ int persistent_groups(const soma_ctx* ctx, int jobs) {
   groups = std::min(groups, kMaxGroups);
   return groups >= 1 ? groups : 0;
 }
+
+int persistent_groups(const soma_ctx* ctx, int jobs) { return persistent_groups_h(ctx, jobs, ctx->cfg.hidden); }
 
 template <int NB, int NCH, bool kRad>
 const void* persist_kernel() {
@@ -656,6 +714,34 @@ const void* persist_kernel_for(int B, int H) {
 // H <= kRecMaxH) and the generator family of probe law `probe`.
 const void* persist_kernel_for(int B, int H, int probe) {
   return probe == SOMA_PROBE_GAUSSIAN ? persist_kernel_for<false>(B, H) : persist_kernel_for<true>(B, H);
+}
+
+// Its instantiation on pre-formed weights (the wide controls' body, d_p <= 512).
+template <int NB, int NCH>
+const void* persist_pre_kernel() {
+  return reinterpret_cast<const void*>(
+      &soma::k_rec_persist<NB, NCH, false, soma::persist_waves(64 * NCH, 16 * NB), true>);
+}
+
+template <int NB>
+const void* persist_pre_kernel_for(int nch) {
+  switch (nch) {
+    case 1: return persist_pre_kernel<NB, 1>();
+    case 2: return persist_pre_kernel<NB, 2>();
+    case 3: return persist_pre_kernel<NB, 3>();
+    case 4: return persist_pre_kernel<NB, 4>();
+    case 5: return persist_pre_kernel<NB, 5>();
+    case 6: return persist_pre_kernel<NB, 6>();
+    case 7: return persist_pre_kernel<NB, 7>();
+    case 8: return persist_pre_kernel<NB, 8>();
+    default: return nullptr;
+  }
+}
+
+const void* persist_pre_kernel_for(int B, int H) {
+  if (B <= 16) return persist_pre_kernel_for<1>(H / 64);
+  if (B <= 32) return persist_pre_kernel_for<2>(H / 64);
+  return persist_pre_kernel_for<4>(H / 64);
 }
 
 // The streaming input projection and head apply for H % 64 == 0,
@@ -841,6 +927,196 @@ int run_body(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
   return mark(ctx, kPhaseRec, st);
 }
 
+// The wide controls' body: one pass of the kernels listed in soma_wide.hpp
+// over the pass's slots (expert, direction, sign), or over the experts
+// unperturbed (!kPert).
+int launch_wide_mm(int epi, const soma::MmArgs& m, int slots, hipStream_t st) {
+  const dim3 grid(unsigned((m.N + 127) / 128), unsigned((m.M + 127) / 128), unsigned(slots));
+  if (epi == soma::kEpiGelu)
+    hipLaunchKernelGGL((soma::k_wide_mm<soma::kEpiGelu>), grid, dim3(256), 0, st, m);
+  else if (epi == soma::kEpiAdd)
+    hipLaunchKernelGGL((soma::k_wide_mm<soma::kEpiAdd>), grid, dim3(256), 0, st, m);
+  else
+    hipLaunchKernelGGL((soma::k_wide_mm<soma::kEpiStore>), grid, dim3(256), 0, st, m);
+  return check_launch("k_wide_mm");
+}
+
+template <bool kPert>
+int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t step, const float* eps_v,
+             int eps_stride, const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
+  const soma_config& c = ctx->cfg;
+  const Layout& L = ctx->lay;
+  const int N = c.n_experts, D = c.n_layers, dt = c.hidden, dp = soma::wide_padded(dt);
+  const int NS = kPert ? 2 : 1, PC = kPert ? L.pc : 1;
+  const int slots = N * pcs * NS;
+  const int64_t R = int64_t(c.seq_len - 1) * c.batch;
+  const soma::WideForm F = soma::wide_form_layout(dp, D);
+  const int64_t mp = 4 * int64_t(dp) * dp;
+  unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
+  const int groups = persistent_groups_h(ctx, slots, dp);
+  if (groups <= 0) return fail(SOMA_EDEVICE, "the wide body needs the persistent recurrence (cooperative launch)");
+
+  soma::WideArgs a{};
+  a.theta = theta;
+  a.seeds = seeds;
+  a.bytes = bytes;
+  a.E = ctx->head;
+  a.e_stride = ctx->head_stride;
+  a.wform = reinterpret_cast<float*>(ctx->ws + L.wform);
+  a.U = reinterpret_cast<float*>(ctx->ws + L.U);
+  a.x = reinterpret_cast<float*>(ctx->ws + L.xres);
+  a.n = reinterpret_cast<float*>(ctx->ws + L.hseq);
+  a.gin = reinterpret_cast<float*>(ctx->ws + L.gin);
+  a.part = reinterpret_cast<double*>(ctx->ws + L.part);
+  a.fdec = reinterpret_cast<float*>(ctx->ws + L.fdec);
+  a.lse = reinterpret_cast<float*>(ctx->ws + L.lse);
+  a.d = L.d;
+  a.step = step;
+  a.eps_v = eps_v;
+  a.eps_stride = eps_stride;
+  a.err = err;
+  a.probe = c.probe;
+  a.ppb = kPert ? c.n_pairs : 1;
+  a.bstride = kPert ? int64_t(N) * c.batch * c.seq_len : 0;
+  a.N = N;
+  a.D = D;
+  a.dt = dt;
+  a.dp = dp;
+  a.B = c.batch;
+  a.T = c.seq_len;
+  a.PC = PC;
+  a.pcs = pcs;
+  a.j0 = j0;
+  a.NS = NS;
+  a.row_tiles = L.row_tiles;
+
+  // Pre-formed weights; padded entries are zero (the form kernel writes only
+  // the real ones).
+  const int64_t form_floats = int64_t(N) * PC * NS * F.total;
+  if (dp != dt) {
+    hipLaunchKernelGGL(soma::k_fill_f32, dim3(4096), dim3(256), 0, st, a.wform, form_floats);
+    if (int rc = check_launch("k_fill_f32")) return rc;
+  }
+  const int64_t mat_quads = (L.d - (2LL * D + 1) * dt) / 4;
+  hipLaunchKernelGGL((soma::k_wide_form<kPert>), dim3(unsigned((mat_quads + 255) / 256), unsigned(slots)), dim3(256),
+                     0, st, a);
+  if (int rc = check_launch("k_wide_form")) return rc;
+  if (int rc = mark(ctx, kPhaseFold, st)) return rc;
+
+  soma::MmArgs m{};
+  m.pcs = pcs;
+  m.PC = PC;
+  m.NS = NS;
+  m.err = err;
+  m.w_slot = F.total;
+  // U = E P_in^T: the input projection of every byte value.
+  m.A = ctx->head;
+  m.a_slot = ctx->head_stride;
+  m.a_expert = 1;
+  m.W = a.wform + F.pin;
+  m.C = a.U;
+  m.c_slot = int64_t(SOMA_VOCAB) * dp;
+  m.M = SOMA_VOCAB;
+  m.N = dp;
+  m.K = soma::kWideHeadWidth;
+  if (int rc = launch_wide_mm(soma::kEpiStore, m, slots, st)) return rc;
+  const dim3 ln_grid(unsigned((R + 3) / 4), unsigned(slots));
+  hipLaunchKernelGGL((soma::k_wide_ln<0>), ln_grid, dim3(256), 0, st, a);
+  if (int rc = check_launch("k_wide_ln")) return rc;
+  if (int rc = mark(ctx, kPhaseFold, st)) return rc;
+
+  m.a_expert = 0;
+  m.M = int(R);
+  for (int l = 0; l < D; ++l) {
+    const float* blk = a.wform + F.blk0 + l * F.blk_stride;
+    // gate inputs gin = n A'^T (rows interleaved per unit)
+    m.A = a.n;
+    m.a_slot = R * dp;
+    m.W = blk;
+    m.C = a.gin;
+    m.c_slot = R * 4 * dp;
+    m.N = 4 * dp;
+    m.K = dp;
+    if (int rc = launch_wide_mm(soma::kEpiStore, m, slots, st)) return rc;
+    if (int rc = mark(ctx, kPhaseProj, st)) return rc;
+    ++ctx->proj_launches;
+    // the recurrence on the pre-formed R; h into the n buffer
+    soma::FwdArgs f{};
+    f.theta = theta;
+    f.bytes = bytes;
+    f.seeds = seeds;
+    f.gin = a.gin;
+    f.hseq = a.n;
+    f.d = L.d;
+    f.step = step;
+    f.eps_v = eps_v;
+    f.eps_stride = eps_stride;
+    f.pmask = group_mask(c);
+    f.err = err;
+    f.probe = c.probe;
+    f.ppb = a.ppb;
+    f.bstride = a.bstride;
+    f.N = N;
+    f.E = dp;
+    f.H = dp;
+    f.B = c.batch;
+    f.T = c.seq_len;
+    f.PC = PC;
+    f.pcs = pcs;
+    f.j0 = j0;
+    f.layer = 1;        // gate inputs from gin
+    f.in_l = dp;
+    f.wpre = blk + mp;
+    f.wpre_slot = F.total;
+    f.ns = NS;
+    soma::PersistArgs p{};
+    p.a = f;
+    p.bar = reinterpret_cast<unsigned*>(ctx->ws + L.sync);
+    p.err = err;
+    p.groups = groups;
+    p.jobs = slots;
+    p.spin_limit = ctx->spin_limit;
+    hipLaunchKernelGGL(soma::k_zero_u32, dim3((groups + 255) / 256), dim3(256), 0, st, p.bar, groups);
+    if (int rc = check_launch("k_zero_u32")) return rc;
+    const int nw = soma::persist_waves(dp, c.batch);
+    const void* kern = persist_pre_kernel_for(c.batch, dp);
+    if (!kern) return fail(SOMA_ESHAPE, "no persistent recurrence for d_p = %d", dp);
+    if (int rc = launch_persist(kern, p, groups * (dp / (4 * nw)), 64 * nw, st)) return rc;
+    ctx->rec_launches += 1;
+    if (int rc = mark(ctx, kPhaseRec, st)) return rc;
+    // x += h; n = LN(x); m = GELU(n U'^T); x += m V^T
+    hipLaunchKernelGGL((soma::k_wide_ln<1>), ln_grid, dim3(256), 0, st, a);
+    if (int rc = check_launch("k_wide_ln")) return rc;
+    m.A = a.n;
+    m.a_slot = R * dp;
+    m.W = blk + 2 * mp;
+    m.C = a.gin;
+    m.c_slot = R * 4 * dp;
+    m.N = 4 * dp;
+    m.K = dp;
+    if (int rc = launch_wide_mm(soma::kEpiGelu, m, slots, st)) return rc;
+    m.A = a.gin;
+    m.a_slot = R * 4 * dp;
+    m.W = blk + 3 * mp;
+    m.C = a.x;
+    m.c_slot = R * dp;
+    m.N = dp;
+    m.K = 4 * dp;
+    if (int rc = launch_wide_mm(soma::kEpiAdd, m, slots, st)) return rc;
+    if (l + 1 < D) {
+      hipLaunchKernelGGL((soma::k_wide_ln<2>), ln_grid, dim3(256), 0, st, a);
+      if (int rc = check_launch("k_wide_ln")) return rc;
+    }
+    if (int rc = mark(ctx, kPhaseProj, st)) return rc;
+    ctx->proj_launches += 2;
+  }
+  hipLaunchKernelGGL((soma::k_wide_ln<2>), ln_grid, dim3(256), 0, st, a);
+  if (int rc = check_launch("k_wide_ln")) return rc;
+  hipLaunchKernelGGL((soma::k_wide_head<!kPert>), dim3(unsigned(L.row_tiles), unsigned(slots)), dim3(256), 0, st, a);
+  if (int rc = check_launch("k_wide_head")) return rc;
+  return mark(ctx, kPhaseHead, st);
+}
+
 // Forward passes of `pcs` directions starting at j0 (kPert) or of the
 // unperturbed experts (!kPert, pcs = 1), ending with per-tile loss sums.
 template <bool kPert>
@@ -848,6 +1124,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
                 int eps_stride, const uint8_t* bytes, int j0, int pcs, hipStream_t st) {
   const soma_config& c = ctx->cfg;
   if (c.arch == SOMA_ARCH_BODY) return run_body<kPert>(ctx, theta, seeds, step, eps_v, eps_stride, bytes, j0, pcs, st);
+  if (c.arch == SOMA_ARCH_WIDE) return run_wide<kPert>(ctx, theta, seeds, step, eps_v, eps_stride, bytes, j0, pcs, st);
   const Layout& L = ctx->lay;
   soma::FwdArgs a{};
   a.theta = theta;
@@ -985,15 +1262,20 @@ void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws,
     // Co-resident blocks for the persistent recurrence on the current device.
     int dev = 0, coop = 0, cus = 0, per_cu = 0, lds_max = 0;
     hipFuncAttributes fa{};
-    const bool shape_ok = cfg->arch == SOMA_ARCH_LSTM && cfg->hidden % 64 == 0 &&
-                          cfg->hidden <= soma::kRecMaxH && cfg->batch <= 64;
-    const void* kern = shape_ok ? persist_kernel_for(cfg->batch, cfg->hidden, cfg->probe) : nullptr;
+    // The wide body's recurrence runs at the padded width on pre-formed
+    // weights (the kernel's generator family is then unused).
+    const int rec_h = cfg->arch == SOMA_ARCH_WIDE ? soma::wide_padded(cfg->hidden) : cfg->hidden;
+    const bool shape_ok = cfg->arch != SOMA_ARCH_BODY && rec_h % 64 == 0 && rec_h <= soma::kRecMaxH &&
+                          cfg->batch <= 64;
+    const void* kern = !shape_ok ? nullptr
+                       : cfg->arch == SOMA_ARCH_WIDE ? persist_pre_kernel_for(cfg->batch, rec_h)
+                                                     : persist_kernel_for(cfg->batch, rec_h, cfg->probe);
     if (kern && hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess &&
         hipFuncGetAttributes(&fa, kern) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * soma::persist_waves(cfg->hidden, cfg->batch), 0) ==
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64 * soma::persist_waves(rec_h, cfg->batch), 0) ==
             hipSuccess &&
         coop && size_t(lds_max) >= fa.sharedSizeBytes && per_cu >= 1) {
       ctx->coop_blocks = cus * per_cu;
@@ -1117,7 +1399,7 @@ Rates schedule_rates(const soma_schedule_entry* sched) {
 
 // The paper's body decodes through the caller's tied matrix: it must be set.
 int check_head(const soma_ctx* ctx) {
-  if (ctx->cfg.arch == SOMA_ARCH_BODY && !ctx->head)
+  if (ctx->cfg.arch != SOMA_ARCH_LSTM && !ctx->head)
     return fail(SOMA_EINVAL, "no tied matrix E: call soma_set_tied_head first");
   return SOMA_OK;
 }
@@ -1208,9 +1490,11 @@ int check_state(const float* m, const float* v) {
 }
 
 soma::LawMap law_map(const soma_config& c, const Layout& L) {
-  soma::LawMap m{c.probe, c.n_layers, 0, c.hidden, 0, L.d, group_mask(c)};
+  soma::LawMap m{c.probe, c.n_layers, 0, c.hidden, 0, L.d, group_mask(c), 0};
   if (c.arch == SOMA_ARCH_BODY) {
     m.blk = soma::body_block(c.hidden);   // the whole body is the LSTM group
+  } else if (c.arch == SOMA_ARCH_WIDE) {
+    m.gain0 = L.d - (2LL * c.n_layers + 1) * c.hidden;   // the whole body is the LSTM group
   } else {
     m.emb_end = L.off_layer[0];
     m.head_start = L.off_head;
@@ -1394,13 +1678,14 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
 
 int soma_set_tied_head(soma_ctx* ctx, float* E, int64_t expert_stride) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
-  if (ctx->cfg.arch != SOMA_ARCH_BODY) return fail(SOMA_EINVAL, "the stacked LSTM has no tied matrix");
+  if (ctx->cfg.arch == SOMA_ARCH_LSTM) return fail(SOMA_EINVAL, "the stacked LSTM has no tied matrix");
   if (!E || !aligned(E, 16)) return fail(SOMA_EINVAL, "E must be a 16-byte aligned device pointer");
   if (expert_stride < 0 || expert_stride % 4)
     return fail(SOMA_EINVAL, "expert_stride must be >= 0 and a multiple of 4 floats");
-  if (expert_stride > 0 && expert_stride < int64_t(SOMA_VOCAB) * ctx->cfg.hidden)
+  const int width = ctx->cfg.arch == SOMA_ARCH_WIDE ? ctx->cfg.embed : ctx->cfg.hidden;
+  if (expert_stride > 0 && expert_stride < int64_t(SOMA_VOCAB) * width)
     return fail(SOMA_EINVAL, "experts' tied matrices must not overlap (stride %lld < %d)",
-                static_cast<long long>(expert_stride), SOMA_VOCAB * ctx->cfg.hidden);
+                static_cast<long long>(expert_stride), SOMA_VOCAB * width);
   ctx->head = E;
   ctx->head_stride = expert_stride;
   return ok();
@@ -1410,7 +1695,7 @@ int soma_head_delta(soma_ctx* ctx, const float* theta, const uint8_t* bytes, flo
                     void* stream) {
   if (!ctx) return fail(SOMA_EINVAL, "ctx is NULL");
   const soma_config& c = ctx->cfg;
-  if (c.arch != SOMA_ARCH_BODY) return fail(SOMA_EINVAL, "the delta rule needs the paper's body (arch 1)");
+  if (c.arch == SOMA_ARCH_LSTM) return fail(SOMA_EINVAL, "the delta rule needs a tied head (arch 1 or 2)");
   if (int rc = check_head(ctx)) return rc;
   if (!theta || !bytes) return fail(SOMA_EINVAL, "NULL device pointer");
   if (!aligned(theta, 16)) return fail(SOMA_EINVAL, "theta must be 16-byte aligned");
@@ -1425,10 +1710,12 @@ int soma_head_delta(soma_ctx* ctx, const float* theta, const uint8_t* bytes, flo
   unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
   hipLaunchKernelGGL(soma::k_zero_u32, dim3(1), dim3(64), 0, st, err, 1);
   if (int rc = check_launch("k_zero_u32")) return rc;
-  const int rc0 = run_body<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
+  const int rc0 = c.arch == SOMA_ARCH_WIDE ? run_wide<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st)
+                                           : run_body<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
   ctx->timing = timing;
   if (rc0) return rc0;
   const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
+  const int width = c.arch == SOMA_ARCH_WIDE ? c.embed : c.hidden;
   if (loss) {
     hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
                        reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1, 1, 1, 1, 0,
@@ -1439,14 +1726,14 @@ int soma_head_delta(soma_ctx* ctx, const float* theta, const uint8_t* bytes, flo
   const dim3 pgrid(L.delta_chunks, c.n_experts);
   const float* fdec = reinterpret_cast<const float*>(ctx->ws + L.fdec);
   const float* lse = reinterpret_cast<const float*>(ctx->ws + L.lse);
-  if (c.hidden == 32)
+  if (width == 32)
     hipLaunchKernelGGL((soma::k_head_delta_part<2>), pgrid, dim3(256), 0, st, fdec, lse, bytes, ctx->head,
                        ctx->head_stride, c.batch, c.seq_len, L.delta_chunks, dpart);
   else
     hipLaunchKernelGGL((soma::k_head_delta_part<1>), pgrid, dim3(256), 0, st, fdec, lse, bytes, ctx->head,
                        ctx->head_stride, c.batch, c.seq_len, L.delta_chunks, dpart);
   if (int rc = check_launch("k_head_delta_part")) return rc;
-  const int64_t vd = int64_t(SOMA_VOCAB) * c.hidden;
+  const int64_t vd = int64_t(SOMA_VOCAB) * width;
   hipLaunchKernelGGL(soma::k_head_delta_reduce, dim3(unsigned((vd + 255) / 256), c.n_experts), dim3(256), 0, st,
                      dpart, L.delta_chunks, vd, inv_rows, grad, ctx->head, ctx->head_stride, lr);
   if (int rc = check_launch("k_head_delta_reduce")) return rc;

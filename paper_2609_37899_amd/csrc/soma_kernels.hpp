@@ -246,6 +246,14 @@ struct FwdArgs {
   int in_l;               // input width of the current layer
   int t;                  // time step (rec kernel)
   int row_tiles;          // head row tiles per slot
+  // The persistent recurrence's pre-formed instantiation only: perturbed
+  // recurrent weights formed beforehand, slot s's matrix at wpre + s *
+  // wpre_slot, [4H][H] with row 4 u + g = gate g of unit u; and the signs
+  // per direction of the pass (1: one unperturbed job per expert, else both
+  // signs).
+  const float* wpre;
+  int64_t wpre_slot;
+  int ns;
 };
 
 // Parameter groups of the stacked LSTM that the perturbation mask names: the
@@ -996,7 +1004,10 @@ __host__ __device__ constexpr int persist_waves(int H, int B) {
   return (H == 192 || H == 384) && B <= 32 ? 12 : 8;
 }
 
-template <int NB, int NCH, bool kRad, int NW>
+// kPre: the recurrent weights come pre-formed (a.wpre) and a pass may run
+// one sign per direction (a.ns == 1); a separate instantiation, so that the
+// kernels that form their weights from the probes keep their registers.
+template <int NB, int NCH, bool kRad, int NW, bool kPre = false>
 __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
   constexpr int NU = 4 * NW;                            // units per block (16 NW gate rows, 16 per wave)
   constexpr int KC = 2 * NCH;                           // 32-wide k chunks: H = 64 NCH
@@ -1048,14 +1059,15 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
   unsigned* bar = p.bar + g;
   unsigned done = 0;                                    // steps this block has published
 
+  const bool one_sign = kPre && a.ns == 1;
   for (int job = g; job < p.jobs; job += p.groups) {
-    const int sg = job & 1, pj = job >> 1;
+    const int sg = one_sign ? 0 : job & 1, pj = one_sign ? job : job >> 1;
     const int e = pj / a.pcs, jl = pj % a.pcs;
     const float* th = a.theta + static_cast<int64_t>(e) * a.d;
-    const uint2 key = stream_key(a.seeds[e], a.step);
+    const uint2 key = kPre ? make_uint2(0u, 0u) : stream_key(a.seeds[e], a.step);   // no seeds for pre-formed weights
     const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
-    const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
-    const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
+    const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * (one_sign ? 1 : 2) + sg;
+    const float seps = kPre ? 0.0f : (sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm));
     const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
     // Gate inputs of layer 1 (folded, per byte value) or of a later layer.
     const __amdgpu_buffer_rsrc_t gbuf =
@@ -1067,9 +1079,20 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
     // Perturbed recurrent weights of this lane, drawn once for the sequence
     // and held as split fragments.
     uint4 wh[KC], wl[KC];
-    resident_weights_split<KC, true, kRad, ZW, 16 * NW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H,
-                                                        in, H, utile * 16 * NW, a.probe, key, pair, step_lo, seps,
-                                                        p.err);
+    if constexpr (kPre) {
+      // Rows of the pre-formed matrix: this lane's gate row, 8 consecutive
+      // k per 32-wide chunk (the formed weights' range is checked where they
+      // were formed).
+      const float* wr = a.wpre + slot * a.wpre_slot + static_cast<int64_t>(utile * 16 * NW + wave * 16 + lr) * H + 8 * lg;
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        split8v(*reinterpret_cast<const float4*>(wr + 32 * c), *reinterpret_cast<const float4*>(wr + 32 * c + 4),
+                wh[c], wl[c]);
+    } else {
+      resident_weights_split<KC, true, kRad, ZW, 16 * NW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H,
+                                                          in, H, utile * 16 * NW, a.probe, key, pair, step_lo, seps,
+                                                          p.err);
+    }
     // Rows past the batch compute on whatever follows in the same buffers
     // (finite inputs and h of later rows, possibly being rewritten, or zeros
     // past a buffer's end): a column of the product depends only on the same

@@ -1,0 +1,481 @@
+// soma_wide.hpp -- the body of the paper's wider fixed-size controls
+// (SOMA_ARCH_WIDE; Appendix C, counting rules and Table
+// fixed-parameter-counts; Appendix E): D pre-norm residual blocks (a
+// bias-free LSTM and a GELU MLP of hidden width 4 d_t, gain-only LayerNorm)
+// at width d_t, between an input projection P_in from the head width d_E and
+// an output projection P_out back to it, decoded by the expert's own tied
+// matrix E [256][d_E], which is never perturbed.
+//
+// Canonical parameter order of one expert (every matrix row a multiple of 4
+// long, so that a probe quad lies in one row of one matrix):
+//   P_in [d_t][d_E]; per block A, R, U, V [d_t][4 d_t] (LSTM input and
+//   recurrent weights with columns j = g d_t + u for gates g = i, f, g, o;
+//   MLP up weights; MLP down weights, row = output feature); P_out [d_t][d_E];
+//   gains g1, g2 per block, then g_f (each d_t long).
+//
+// A pass of this body runs, for every slot (expert, direction, sign):
+//   k_wide_form   perturbed weights, gains folded into the matrices that
+//                 read a normalised vector, zero-padded to d_p = 64 ceil(d_t
+//                 / 64) and laid out for the kernels below (once per pass)
+//   k_wide_mm     U = E P_in^T (the input projection per byte value)
+//   k_wide_ln     x = U[byte], n = LN(x)   (the gain sits in the weights)
+//   per block:    k_wide_mm gin = n A'      (gate inputs, units interleaved)
+//                 k_rec_persist h           (recurrent weights pre-formed)
+//                 k_wide_ln x += h, n = LN(x)
+//                 k_wide_mm m = GELU(n U')
+//                 k_wide_mm x += m V^T
+//   k_wide_ln     n = LN(x)
+//   k_wide_head   u = n P_out', logits = u E^T, cross entropy
+// Padded units have zero weights and zero gate inputs, so their cell state
+// and h stay exactly 0 and every padded column of x stays 0.
+#pragma once
+
+#include "soma_kernels.hpp"
+#include "soma_body.hpp"
+
+namespace soma {
+
+constexpr int kWideHeadWidth = 32;   // d_E of the GPU path (the paper's head width)
+constexpr int kWidePad = 64;         // d_p: d_t rounded up to a multiple of this
+
+__host__ __device__ constexpr int wide_padded(int dt) { return (dt + kWidePad - 1) / kWidePad * kWidePad; }
+
+// Floats of one slot's pre-formed weights and their offsets.
+struct WideForm {
+  int64_t pin, blk0, blk_stride, pout, total;   // blk_stride: one block's four matrices
+};
+
+__host__ __device__ inline WideForm wide_form_layout(int dp, int D) {
+  WideForm f{};
+  const int64_t m = 4 * int64_t(dp) * dp;
+  // Every matrix a product reads is stored output-major, [n][k]: the rows
+  // of the gate matrices are interleaved (row 4 u + g is gate g of unit u).
+  f.pin = 0;                                   // P_in   [d_p][32]
+  f.blk0 = int64_t(dp) * kWideHeadWidth;       // per block: A' [4 d_p][d_p], R [4 d_p][d_p],
+  f.blk_stride = 4 * m;                        //   U' [4 d_p][d_p], V [d_p][4 d_p]
+  f.pout = f.blk0 + int64_t(D) * f.blk_stride; // P_out' [d_p][32]: feature c, output q
+  f.total = f.pout + int64_t(dp) * kWideHeadWidth;
+  return f;
+}
+
+struct WideArgs {
+  const float* theta;     // [N][d]
+  const uint64_t* seeds;  // [N]
+  const uint8_t* bytes;   // [A][N][B][T]
+  const float* E;         // tied matrices, expert e at E + e * e_stride, [256][32]
+  int64_t e_stride;
+  float* wform;           // pre-formed weights, [slots][WideForm::total]
+  float* U;               // [slots][256][d_p]
+  float* x;               // [slots][R][d_p] residual stream
+  float* n;               // [slots][R][d_p] normalised x (also h of the recurrence)
+  float* gin;             // [slots][R][4 d_p] gate inputs, then the MLP hidden layer
+  double* part;           // [slots][row_tiles] cross-entropy sums
+  float* fdec;            // evaluation: decoder inputs u [N][B][T-1][32] (position b (T-1) + t)
+  float* lse;             // evaluation: log-sum-exps [N][B][T-1]
+  int64_t d;              // parameters per expert
+  uint64_t step;
+  const float* eps_v;     // radius of expert e: eps_v[e * eps_stride]
+  int eps_stride;
+  unsigned* err;          // the step's sticky abort flag
+  int probe;
+  int ppb;                // directions per accumulation batch
+  int64_t bstride;        // bytes per accumulation batch, N B T
+  int N, D, dt, dp, B, T, PC, pcs, j0, NS;   // NS: signs per direction (2; 1 for an evaluation)
+  int row_tiles;          // 64-row tiles of the head per slot
+};
+
+// Sum and max over the 64 lanes of a wave (butterfly; every lane gets the
+// same value, each pair adding its two values in either order).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Orders a wave's LDS writes before its later LDS reads of other lanes'
+// words (a wave's LDS accesses execute in order; this keeps the compiler
+// from moving them).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Slot s of the pass: (expert, direction in the pass, sign).
+__device__ __forceinline__ void wide_slot(const WideArgs& a, int s, int& e, int& jl, int& sg) {
+  sg = s % a.NS;
+  const int pj = s / a.NS;
+  jl = pj % a.pcs;
+  e = pj / a.pcs;
+}
+
+__device__ __forceinline__ int64_t wide_slot_index(const WideArgs& a, int e, int jl, int sg) {
+  return (int64_t(e) * a.PC + jl) * a.NS + sg;
+}
+
+// The perturbed value of canonical coordinate k of expert e (one probe quad
+// drawn for it): theta_k + seps z_k.
+__device__ __forceinline__ float wide_coord(const float* th, int64_t k, int64_t gain0, int law, uint2 key,
+                                            uint32_t pair, uint32_t step_lo, float seps) {
+  if (seps == 0.0f) return th[k];
+  const int lw = (k >= gain0 && law == kProbeSparseRademacher) ? kProbeRademacher : law;
+  const float4 z = probe_quad(lw, key, pair, step_lo, static_cast<uint64_t>(k & ~int64_t(3)));
+  const float zz[4] = {z.x, z.y, z.z, z.w};
+  return __builtin_fmaf(seps, zz[k & 3], th[k]);
+}
+
+// ---------------------------------------------------------------------------
+// Pre-formed weights of every slot: one canonical probe quad per thread
+// (grid: quads of the matrices, slots).  The gains are not stored: each
+// matrix quad that reads a normalised vector multiplies by the perturbed gain
+// of its row (one more probe quad).  Padded entries are zeroed beforehand
+// (k_fill_f32).  A formed weight outside the split products' range, or NaN,
+// sets the step's abort flag.
+// ---------------------------------------------------------------------------
+template <bool kPert>
+__global__ __launch_bounds__(256) void k_wide_form(WideArgs a) {
+  const int dt = a.dt, dp = a.dp, D = a.D;
+  const int64_t dt4 = 4 * int64_t(dt), mat = dt4 * dt;
+  const int64_t blk0 = int64_t(dt) * kWideHeadWidth, pout0 = blk0 + D * 4 * mat;
+  const int64_t gain0 = pout0 + int64_t(dt) * kWideHeadWidth;
+  const int64_t k = 4 * (blockIdx.x * int64_t(blockDim.x) + threadIdx.x);
+  if (k >= gain0) return;
+  int e, jl, sg;
+  wide_slot(a, blockIdx.y, e, jl, sg);
+  const int64_t slot = wide_slot_index(a, e, jl, sg);
+  const float* th = a.theta + int64_t(e) * a.d;
+  const uint2 key = kPert ? stream_key(a.seeds[e], a.step) : make_uint2(0u, 0u);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const float eps = kPert ? a.eps_v[int64_t(e) * a.eps_stride] : 0.0f;
+  const float seps = sg == 0 ? eps : -eps;
+  float w[4];
+  if (kPert) {
+    const int lw = a.probe;   // matrices follow the configured law
+    const float4 z = probe_quad(lw, key, pair, step_lo, static_cast<uint64_t>(k));
+    w[0] = __builtin_fmaf(seps, z.x, th[k]);
+    w[1] = __builtin_fmaf(seps, z.y, th[k + 1]);
+    w[2] = __builtin_fmaf(seps, z.z, th[k + 2]);
+    w[3] = __builtin_fmaf(seps, z.w, th[k + 3]);
+  } else {
+    w[0] = th[k]; w[1] = th[k + 1]; w[2] = th[k + 2]; w[3] = th[k + 3];
+  }
+  const WideForm F = wide_form_layout(dp, D);
+  float* out = a.wform + slot * F.total;
+  const int64_t dp4 = 4 * int64_t(dp);
+  bool ok = true;
+  float* dst = out;
+  auto put = [&](int64_t at, float v) {
+    ok = ok && __builtin_fabsf(v) <= kSplitMax;
+    dst[at] = v;
+  };
+  if (k < blk0) {                                     // P_in [c][q]
+    const int64_t c = k / kWideHeadWidth, q = k % kWideHeadWidth;
+    for (int i = 0; i < 4; ++i) put(F.pin + c * kWideHeadWidth + q + i, w[i]);
+  } else if (k < pout0) {
+    const int64_t r = k - blk0;
+    const int l = static_cast<int>(r / (4 * mat));
+    const int which = static_cast<int>((r / mat) % 4);
+    const int64_t rr = r % mat, c = rr / dt4, j = rr % dt4;
+    dst = out + F.blk0 + l * F.blk_stride;
+    const int64_t mp = 4 * int64_t(dp) * dp;
+    float g = 1.0f;
+    if (which == 0 || which == 2)                     // A reads LN(x; g1), U reads LN(x; g2)
+      g = wide_coord(th, gain0 + (2 * l + (which == 2 ? 1 : 0)) * int64_t(dt) + c, gain0, a.probe, key, pair,
+                     step_lo, seps);
+    for (int i = 0; i < 4; ++i) {
+      const int64_t jj = j + i;
+      if (which <= 1) {                               // gate column g dt + u -> row 4 u + g
+        const int64_t gate = jj / dt, u = jj % dt;
+        const float v = which == 0 ? w[i] * g : w[i];
+        put(which * mp + (4 * u + gate) * dp + c, v); // A' at +0, R at +4 dp^2
+      } else if (which == 2) {                        // U'[j][c]
+        put(2 * mp + jj * dp + c, w[i] * g);
+      } else {                                        // V[c][j]: row = output feature
+        put(3 * mp + c * dp4 + jj, w[i]);
+      }
+    }
+  } else {                                            // P_out' [c][q] = P_out[c][q] g_f[c]
+    const int64_t r = k - pout0, c = r / kWideHeadWidth, q = r % kWideHeadWidth;
+    const float g = wide_coord(th, gain0 + 2 * int64_t(D) * dt + c, gain0, a.probe, key, pair, step_lo, seps);
+    for (int i = 0; i < 4; ++i) put(F.pout + c * kWideHeadWidth + q + i, w[i] * g);   // not split: no bound needed
+  }
+  report_split_range(a.err, ok);
+}
+
+// out[i] = 0 for i < n (a fill kernel, so that callers may capture it).
+__global__ void k_fill_f32(float* out, int64_t n) {
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+    out[i] = 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Batched products on the fp16 matrix cores from split fp32 operands:
+//   C[s][m][n] (= | += | GELU of) sum_k A[s][m][k] W[s][n][k]
+// A row-major [M][K] per slot, or per expert (the tied matrix); W
+// output-major [N][K].  blockIdx.z runs over the pass's slots (expert,
+// direction, sign), whose buffers sit at (e PC + jl) NS + sg.
+// Block tile 128 (n) x 128 (m), four waves of 64 x 64; K in 32-wide chunks
+// (K % 32 == 0, N % 4 == 0), staged through LDS as fp16 hi/lo parts, the
+// next chunk's global loads issued before the current chunk's products.
+// ---------------------------------------------------------------------------
+enum WideEpi { kEpiStore = 0, kEpiGelu = 1, kEpiAdd = 2 };
+
+struct MmArgs {
+  const float* A;
+  int64_t a_slot;     // floats between consecutive A matrices (slots, or experts)
+  int a_expert;       // A is per expert rather than per slot
+  const float* W;
+  int64_t w_slot;
+  float* C;
+  int64_t c_slot;
+  int M, N, K;
+  int pcs, PC, NS;    // the pass's slots
+  unsigned* err;
+};
+
+constexpr int kMmLd = 48;   // LDS row in halves: 32 + 16 (an odd multiple of 32 bytes)
+
+template <int kEpi>
+__global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
+  __shared__ __attribute__((aligned(16))) _Float16 sa[2][128 * kMmLd];   // activations (hi, lo)
+  __shared__ __attribute__((aligned(16))) _Float16 sw[2][128 * kMmLd];   // weights (hi, lo)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int n0 = blockIdx.x * 128, m0 = blockIdx.y * 128;
+  const int sg = blockIdx.z % p.NS, jl = (blockIdx.z / p.NS) % p.pcs, e = blockIdx.z / (p.NS * p.pcs);
+  const int64_t s = (int64_t(e) * p.PC + jl) * p.NS + sg;
+  const float* A = p.A + (p.a_expert ? int64_t(e) : s) * p.a_slot;
+  const float* W = p.W + s * p.w_slot;
+  float* C = p.C + s * p.c_slot;
+  const int M = p.M, N = p.N, K = p.K;
+  bool ok = true;
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  float4 pa[4], pw[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = threadIdx.x + 256 * i;
+      const int row = idx >> 3, k4 = idx & 7;          // activations: 128 rows x 8 float4
+      const int m = m0 + row;
+      pa[i] = m < M ? *reinterpret_cast<const float4*>(A + int64_t(m) * K + k0 + 4 * k4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int n = n0 + row;                          // weights: 128 rows x 8 float4 along k
+      pw[i] = n < N ? *reinterpret_cast<const float4*>(W + int64_t(n) * K + k0 + 4 * k4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = threadIdx.x + 256 * i;
+      const int row = idx >> 3, k4 = idx & 7;
+      uint2 hi, lo;
+      ok = ok && split_range_ok(pa[i]);
+      split4(pa[i], hi, lo);
+      *reinterpret_cast<uint2*>(&sa[0][row * kMmLd + 4 * k4]) = hi;
+      *reinterpret_cast<uint2*>(&sa[1][row * kMmLd + 4 * k4]) = lo;
+      ok = ok && split_range_ok(pw[i]);
+      split4(pw[i], hi, lo);
+      *reinterpret_cast<uint2*>(&sw[0][row * kMmLd + 4 * k4]) = hi;
+      *reinterpret_cast<uint2*>(&sw[1][row * kMmLd + 4 * k4]) = lo;
+    }
+  };
+
+  gload(0);
+  for (int k0 = 0; k0 < K; k0 += 32) {
+    __syncthreads();                 // the previous chunk's fragments have been read
+    sstore();
+    __syncthreads();
+    if (k0 + 32 < K) gload(k0 + 32);
+    uint4 bh[4], bl[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int row = wm * 64 + 16 * mt + lr;
+      bh[mt] = *reinterpret_cast<const uint4*>(&sa[0][row * kMmLd + 8 * lg]);
+      bl[mt] = *reinterpret_cast<const uint4*>(&sa[1][row * kMmLd + 8 * lg]);
+    }
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const int row = wn * 64 + 16 * nt + lr;
+      const uint4 wh = *reinterpret_cast<const uint4*>(&sw[0][row * kMmLd + 8 * lg]);
+      const uint4 wl = *reinterpret_cast<const uint4*>(&sw[1][row * kMmLd + 8 * lg]);
+      mfma3_batch<4>(wh, wl, bh, bl, acc[nt]);
+    }
+  }
+  report_split_range(p.err, ok);
+
+  // acc[nt][mt][i] = C[m0 + 64 wm + 16 mt + lr][n0 + 64 wn + 16 nt + 4 lg + i]
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) {
+    const int n = n0 + wn * 64 + 16 * nt + 4 * lg;
+    if (n >= N) continue;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int m = m0 + wm * 64 + 16 * mt + lr;
+      if (m >= M) continue;
+      float4* c = reinterpret_cast<float4*>(C + int64_t(m) * N + n);
+      float4 v = make_float4(acc[nt][mt][0], acc[nt][mt][1], acc[nt][mt][2], acc[nt][mt][3]);
+      if (kEpi == kEpiGelu) {
+        v = make_float4(gelu_f(v.x), gelu_f(v.y), gelu_f(v.z), gelu_f(v.w));
+      } else if (kEpi == kEpiAdd) {
+        const float4 o = *c;
+        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+      }
+      *c = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Gain-free LayerNorm of every row of x, one wave per row (four per block):
+//   kMode 0: x = U[byte]          (the embedding's projection per byte value)
+//   kMode 1: x += h               (the LSTM sublayer's residual; h in n)
+//   kMode 2: x as it is
+// then n = (x - mean) / sqrt(var + 1e-5) over the first d_t features (biased
+// variance), 0 on the padded ones.  Rows are r = t B + b.
+// ---------------------------------------------------------------------------
+template <int kMode>
+__global__ __launch_bounds__(256) void k_wide_ln(WideArgs a) {
+  constexpr int kMaxC = 8;   // d_p <= 512
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t R = int64_t(a.T - 1) * a.B;
+  const int64_t r = int64_t(blockIdx.x) * 4 + wave;
+  if (r >= R) return;
+  const int s = blockIdx.y;
+  int e, jl, sg;
+  wide_slot(a, s, e, jl, sg);
+  const int64_t slot = wide_slot_index(a, e, jl, sg);
+  const int dp = a.dp, dt = a.dt, nc = dp / 64;
+  float* xr = a.x + (slot * R + r) * dp;
+  float* nr = a.n + (slot * R + r) * dp;
+  float v[kMaxC];
+  if (kMode == 0) {
+    const int64_t t = r / a.B, b = r % a.B;
+    const uint8_t* by = a.bytes + int64_t((a.j0 + jl) / a.ppb) * a.bstride + (int64_t(e) * a.B + b) * a.T;
+    const float* ur = a.U + (slot * kVocab + by[t]) * dp;
+#pragma unroll
+    for (int i = 0; i < kMaxC; ++i)
+      if (i < nc) {
+        v[i] = ur[64 * i + lane];
+        xr[64 * i + lane] = v[i];
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kMaxC; ++i)
+      if (i < nc) {
+        v[i] = xr[64 * i + lane];
+        if (kMode == 1) {
+          v[i] += nr[64 * i + lane];
+          xr[64 * i + lane] = v[i];
+        }
+      }
+  }
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kMaxC; ++i)
+    if (i < nc && 64 * i + lane < dt) sum += v[i];
+  sum = wave_sum(sum);
+  const float mean = sum / static_cast<float>(dt);
+  float sq = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kMaxC; ++i)
+    if (i < nc && 64 * i + lane < dt) {
+      const float c = v[i] - mean;
+      sq = __builtin_fmaf(c, c, sq);
+    }
+  sq = wave_sum(sq);
+  const float inv = 1.0f / __builtin_sqrtf(sq / static_cast<float>(dt) + 1e-5f);
+#pragma unroll
+  for (int i = 0; i < kMaxC; ++i)
+    if (i < nc) nr[64 * i + lane] = 64 * i + lane < dt ? (v[i] - mean) * inv : 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// The decoder: u = n P_out' (32 features, the final gain folded in), logits
+// = u E^T over the 256 byte values, cross entropy against the next byte.
+// One wave per row, 64 rows per block (a 64-row tile of the slot); the
+// tile's sum of cross entropies goes to part[slot][tile] (fp64, rows in
+// order).  Evaluations also write u and the log-sum-exp per position
+// b (T-1) + t for the delta rule.  fp32 products on the vector ALU.
+// ---------------------------------------------------------------------------
+constexpr int kWideHeadRows = 64;
+
+template <bool kEval>
+__global__ __launch_bounds__(256) void k_wide_head(WideArgs a) {
+  constexpr int EW = kWideHeadWidth, ELD = EW + 1;
+  __shared__ float ps[512 * ELD];            // P_out' [d_p][32], rows padded
+  __shared__ float es[kVocab * ELD];         // E [256][32], rows padded
+  __shared__ float ns[4][512];               // a wave's row of n
+  __shared__ float us[4][EW];                // a wave's decoder input
+  __shared__ double ce_w[4];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tile = blockIdx.x, s = blockIdx.y;
+  int e, jl, sg;
+  wide_slot(a, s, e, jl, sg);
+  const int64_t slot = wide_slot_index(a, e, jl, sg);
+  const int dp = a.dp;
+  const int64_t R = int64_t(a.T - 1) * a.B;
+  const WideForm F = wide_form_layout(dp, a.D);
+  const float* P = a.wform + slot * F.total + F.pout;
+  const float* Ee = a.E + int64_t(e) * a.e_stride;
+  for (int i = threadIdx.x; i < dp * EW; i += 256) ps[(i / EW) * ELD + i % EW] = P[i];
+  for (int i = threadIdx.x; i < kVocab * EW; i += 256) es[(i / EW) * ELD + i % EW] = Ee[i];
+  const uint8_t* by = a.bytes + int64_t((a.j0 + jl) / a.ppb) * a.bstride + int64_t(e) * a.B * a.T;
+  __syncthreads();
+  double ce_sum = 0.0;
+  const int q = lane & 31, half = lane >> 5;
+  for (int i = 0; i < kWideHeadRows / 4; ++i) {
+    const int64_t r = int64_t(tile) * kWideHeadRows + wave * (kWideHeadRows / 4) + i;
+    if (r >= R) break;                                 // wave-uniform
+    const float* nr = a.n + (slot * R + r) * dp;
+    wave_lds_sync();                                   // the previous row's reads are done
+    for (int c = lane; c < dp; c += 64) ns[wave][c] = nr[c];
+    wave_lds_sync();
+    // u[q]: lanes q and q + 32 each sum half of the features, then add.
+    float u = 0.0f;
+    for (int c = half; c < dp; c += 2) u = __builtin_fmaf(ns[wave][c], ps[c * ELD + q], u);
+    u += __shfl_xor(u, 32);
+    if (lane < EW) us[wave][lane] = u;
+    wave_lds_sync();
+    float lg[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int v = lane + 64 * j;
+      float acc = 0.0f;
+#pragma unroll
+      for (int k = 0; k < EW; ++k) acc = __builtin_fmaf(es[v * ELD + k], us[wave][k], acc);
+      lg[j] = acc;
+    }
+    float mx = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
+    mx = wave_max(mx);
+    float se = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) se += __expf(lg[j] - mx);
+    se = wave_sum(se);
+    const float lse = __logf(se) + mx;
+    const int64_t t = r / a.B, b = r % a.B;
+    const int y = by[b * a.T + t + 1];
+    const float ly = __shfl(lg[y >> 6], y & 63);
+    ce_sum += static_cast<double>(lse - ly);
+    if (kEval) {
+      const int64_t pos = int64_t(e) * R + b * (a.T - 1) + t;
+      if (lane < EW) a.fdec[pos * EW + lane] = u;
+      if (lane == 0) a.lse[pos] = lse;
+    }
+  }
+  if (lane == 0) ce_w[wave] = ce_sum;
+  __syncthreads();
+  if (threadIdx.x == 0) a.part[slot * a.row_tiles + tile] = ((ce_w[0] + ce_w[1]) + ce_w[2]) + ce_w[3];
+}
+
+}  // namespace soma

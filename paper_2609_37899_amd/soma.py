@@ -18,7 +18,7 @@ LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
 PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
-ARCH_LSTM, ARCH_BODY = 0, 1
+ARCH_LSTM, ARCH_BODY, ARCH_WIDE = 0, 1, 2
 PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD, PERTURB_ALL = 1, 2, 4, 7
 
 EXPORTS = ("soma_param_count", "soma_workspace_size", "soma_create", "soma_destroy",
@@ -273,9 +273,10 @@ class Context:
                                      _dptr(loss, torch.float32, "loss"), _stream(stream)))
 
     def set_tied_head(self, E, per_expert: bool = False):
-        """The tied matrix of a body context: E [V][d] shared by every expert,
-        or [N][V][d] one per expert (per_expert=True).  The context reads the
-        tensor's memory on every later call: keep it alive."""
+        """The tied matrix of a body context: E [V][w] shared by every expert,
+        or [N][V][w] one per expert (per_expert=True); w = d, or d_E for the
+        wide body.  The context reads the tensor's memory on every later
+        call: keep it alive."""
         import torch
         stride = E.shape[-2] * E.shape[-1] if per_expert else 0
         _check(load().soma_set_tied_head(self._h, _dptr(E, torch.float32, "E"), stride))
