@@ -31,7 +31,7 @@ PEAK_FP16_MFMA_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 # Kernels whose products run on the fp16 matrix cores from split fp32
 # operands (three fp16 products per fp32 product, fp32 accumulation).
 SPLIT_F16_KERNELS = ("k_rec_persist", "k_rec_local", "k_rec_step_split", "k_proj_stream", "k_head_stream",
-                     "k_head_fused", "k_body")
+                     "k_head_fused", "k_body", "k_wide_mm")
 PEAK_HBM_GBS = 8000.0
 PROBE_LAWS = {"gaussian": 0, "sparse": 1, "dense": 2}
 
@@ -67,6 +67,7 @@ def parse():
 
 KERNEL_SOURCES = ("paper_2609_37899_amd/csrc/soma_kernels.hpp", "paper_2609_37899_amd/csrc/soma_rng.hpp")
 BODY_SOURCES = KERNEL_SOURCES + ("paper_2609_37899_amd/csrc/soma_body.hpp",)
+WIDE_SOURCES = BODY_SOURCES + ("paper_2609_37899_amd/csrc/soma_wide.hpp",)
 
 
 def kernel_source_hash(kernel: str = "") -> str:
@@ -75,7 +76,8 @@ def kernel_source_hash(kernel: str = "") -> str:
     from paper_2609_37899_amd.build import HIPCC_FLAGS
     h = hashlib.sha256()
     h.update(" ".join(HIPCC_FLAGS).encode())
-    for f in (BODY_SOURCES if kernel == "k_body" else KERNEL_SOURCES):
+    srcs = BODY_SOURCES if kernel == "k_body" else (WIDE_SOURCES if kernel.startswith("k_wide") else KERNEL_SOURCES)
+    for f in srcs:
         h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -101,11 +103,20 @@ def kernel_flops(w):
     tok = B * (T - 1)                # target tokens per forward
     if w.arch == 1:                  # the paper's body: one fused kernel does every product
         return {"rec": fwd * tok * w.flops_per_token, "proj": 0, "fold": 0, "head": 0}
+    if w.arch == 2:                  # the wide body: recurrence; A, U, V products; projections + decoder
+        return {"rec": fwd * tok * L * 2 * H * 4 * H, "proj": fwd * tok * L * 3 * 2 * H * 4 * H,
+                "fold": fwd * tok * 2 * E * H, "head": fwd * tok * 2 * (H * E + E * 256)}
     rec = fwd * tok * L * 2 * H * 4 * H
     proj = fwd * tok * (L - 1) * 2 * H * 4 * H
     emb_in = fwd * tok * 2 * E * 4 * H     # layer-1 input contraction (executed once per byte value)
     head = fwd * tok * 2 * H * 256
     return {"rec": rec, "proj": proj, "fold": emb_in, "head": head}
+
+
+def cfg_batch(oracle, w, batch, probe, tied_head):
+    """The oracle's configuration of workload w with `batch` sequences."""
+    return oracle.make_cfg(w.n_experts, w.n_layers, w.embed, w.hidden, batch, w.seq_len, w.n_pairs,
+                           w.loss_mode, probe, arch=w.arch, tied_head=tied_head)
 
 
 def cpu_baseline(w, theta, data, seeds, probe=0, tied_head=None):
@@ -114,6 +125,25 @@ def cpu_baseline(w, theta, data, seeds, probe=0, tied_head=None):
     cfg = oracle.make_cfg(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs,
                           w.loss_mode, probe, arch=w.arch, tied_head=tied_head)
     threads = oracle.num_threads()
+    seq_flops = 2 * (w.seq_len - 1) * w.flops_per_token      # one sequence, both signs
+    if w.batch * seq_flops > 4e11:
+        # One perturbed forward (direction 0, + sign) of expert 0 on its first
+        # b sequences, b sized to about 10 s of oracle work.
+        t0 = time.perf_counter()
+        oracle.perturbed_loss(cfg_batch(oracle, w, 1, probe, tied_head), theta[0], int(seeds[0]), 0, 0, 1,
+                              w.eps, data[0][:1])
+        one = time.perf_counter() - t0
+        b = int(max(1, min(w.batch, 10.0 // max(one, 1e-3))))
+        t0 = time.perf_counter()
+        oracle.perturbed_loss(cfg_batch(oracle, w, b, probe, tied_head), theta[0], int(seeds[0]), 0, 0, 1,
+                              w.eps, data[0][:b])
+        dt = time.perf_counter() - t0
+        tokens = b * (w.seq_len - 1)
+        sample = (f"expert 0, direction 0, + sign, its first {b} of {w.batch} sequences at T={w.seq_len} "
+                  f"({tokens} perturbed tokens of {w.perturbed_tokens} per step; "
+                  f"full step extrapolates to {dt * w.perturbed_tokens / tokens:.0f} s)")
+        return {"value": tokens / dt, "unit": "perturbed tokens/s", "cores": threads, "kind": "oracle",
+                "sample": sample, "seconds": dt}
     if w.perturbed_tokens * w.flops_per_token < 2e10:
         t0 = time.perf_counter()
         oracle.spsa_step(cfg, theta, seeds, 0, w.eps, w.lr, data)
@@ -164,6 +194,9 @@ def main():
     if w.arch == 1:   # the paper's width-32 recipe: one frozen tied E shared by every expert
         theta0 = synth.init_body(w.n_experts, w.n_layers, w.hidden, w.init_seed)
         tied = synth.init_tied_head(w.hidden, init_seed=1)
+    elif w.arch == 2:  # the wide controls: every expert its own tied E
+        theta0 = synth.init_wide(w.n_experts, w.n_layers, w.hidden, w.embed, w.init_seed)
+        tied = synth.init_tied_head(w.embed, init_seed=1, n_experts=w.n_experts)
     else:
         theta0 = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, w.init_seed)
     nb = max(1, min(args.steps + args.warmup, 3))
@@ -182,7 +215,7 @@ def main():
     ctx = soma.Context(shape, device=dev)
     if tied is not None:
         dtied = torch.from_numpy(tied).to(dev)
-        ctx.set_tied_head(dtied)
+        ctx.set_tied_head(dtied, per_expert=w.arch == 2)
     theta = torch.from_numpy(theta0.copy()).to(dev)
     seeds = soma.seeds_tensor(seeds_np, dev)
     dbatches = [torch.from_numpy(b).to(dev) for b in batches]
@@ -255,6 +288,8 @@ def main():
              "head": ("k_head_fused" if w.hidden <= 128 else "k_head_stream") if streams else "k_head_ce"}[dom]
     if w.arch == 1:
         kname = "k_body"          # the whole perturbed forward, one launch per direction chunk
+    elif w.arch == 2:
+        kname = {"rec": "k_rec_persist", "proj": "k_wide_mm", "fold": "k_wide_form", "head": "k_wide_head"}[dom]
     elif dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
         kname = "k_rec_local" if local_rec else "k_rec_persist"
     if os.path.exists(args.traffic):
@@ -296,8 +331,9 @@ def main():
                    "params_per_expert": w.params_per_expert, "eps": w.eps, "lr": w.lr,
                    "loss_mode": "summed" if w.loss_mode else "independent",
                    "probe": probe_name, "optimizer": args.optimizer,
-                   "architecture": "paper body (pre-norm residual LSTM + GELU MLP, frozen tied E)"
-                   if w.arch == 1 else "stacked LSTM, untied head",
+                   "architecture": {1: "paper body (pre-norm residual LSTM + GELU MLP, frozen tied E)",
+                                    2: "wide control body (residual LSTM + GELU MLP at d_t with input/output "
+                                       "projections to d_E, per-expert tied E)"}.get(w.arch, "stacked LSTM, untied head"),
                    "parallelism": "single GPU, all experts and directions in each launch"},
         "algorithmic_tflops": round(total_flops / sec / 1e12, 3),
         "phase_ms": {k: round(v, 3) for k, v in ms.items()},

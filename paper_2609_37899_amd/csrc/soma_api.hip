@@ -259,6 +259,13 @@ int choose_chunk(const soma_config& c) {
   if (c.arch == SOMA_ARCH_BODY) return dirs(c);   // no per-direction buffers
   int pc = dirs(c);
   while (pc > 1 && layout_for(c, pc).total > kAutoBudget) --pc;
+  if (c.arch == SOMA_ARCH_WIDE) {
+    // Chunks of equal size: each chunk's recurrence runs its jobs in rounds
+    // of the concurrent groups, and a small last chunk would leave most of
+    // them idle.
+    const int n = (dirs(c) + pc - 1) / pc;
+    pc = (dirs(c) + n - 1) / n;
+  }
   return pc;
 }
 

@@ -163,3 +163,49 @@ def test_wide_separability():
     assert np.array_equal(outs[0][0][0], outs[1][0][0])
     assert np.array_equal(outs[0][1][0], outs[1][1][0])
     assert not np.array_equal(outs[0][1][1], outs[1][1][1])
+
+
+def test_wide_fullsize_sampled(oracle_mod):
+    """The paper's N = 2 wide control (d_t = 361, B = 64, T = 1,024, 32
+    directions, sparse probes) in the benchmark's launch configuration: every
+    loss finite and near ln 256, one direction of expert 1 at both signs
+    against the oracle, its coefficient, and theta' at sampled coordinates of
+    expert 1 from oracle.apply_update fed the oracle's coefficient for that
+    direction and the step's own for the others."""
+    torch = require_gpu()
+    w = workloads.WIDE_N2
+    N, P = w.n_experts, w.n_pairs
+    theta = synth.init_wide(N, w.n_layers, w.hidden, w.embed, init_seed=w.init_seed)
+    E = synth.init_tied_head(w.embed, init_seed=1, n_experts=N)
+    data = synth.expert_batches_in_child(w.cluster_seeds, w.batch, w.seq_len)
+    seeds = synth.expert_seeds(N)
+    shape = soma.Shape(N, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, P, probe=w.probe, arch=w.arch)
+    print(f"{w.name}: step", flush=True)
+    ctx, _ = _context(torch, shape, E)
+    th = torch.from_numpy(theta.copy()).cuda()
+    losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+    ctx.spsa_step(th, soma.seeds_tensor(seeds), 0, w.eps, w.lr, torch.from_numpy(data).cuda(), losses)
+    coef = torch.zeros((N, P), dtype=torch.float32, device="cuda")
+    ctx.coefficients(coef)
+    torch.cuda.synchronize()
+    lg, cg, got = losses.cpu().numpy(), coef.cpu().numpy(), th.cpu().numpy()
+    ctx.close()
+    assert np.all(np.isfinite(lg)) and np.all(np.abs(lg - np.log(256.0)) < 0.5)
+    e, j = 1, 29
+    cfg = _oracle_cfg(oracle_mod, shape, E)
+    ce = oracle_mod.make_cfg(1, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, P, 0, w.probe,
+                             arch=oracle_mod.ARCH_WIDE, tied_head=E[e])
+    ref = []
+    for sgn in (1, -1):
+        print(f"{w.name}: oracle forward e={e} j={j} sign={sgn}", flush=True)
+        ref.append(oracle_mod.perturbed_loss(ce, theta[e], int(seeds[e]), 0, j, sgn, w.eps, data[e]))
+    err = assert_losses_close(lg[e, j], ref)
+    denom = 2.0 * np.float64(np.float32(w.eps)) * P
+    c_mix = cg[e].astype(np.float64)
+    c_mix[j] = (ref[0] - ref[1]) / denom
+    cerr = abs(c_mix[j] - cg[e, j]) / np.abs(c_mix).max()
+    assert cerr <= 2e-2
+    ks = np.random.default_rng(2).choice(theta.shape[1], 3000, replace=False)
+    want = oracle_mod.apply_update(cfg, theta[e], int(seeds[e]), 0, w.lr, c_mix, ks)
+    terr = assert_theta_close(got[e][ks], want)
+    print(f"{w.name}: loss rel {err:.2e}  coef rel {cerr:.2e}  theta' rel {terr:.2e}")
