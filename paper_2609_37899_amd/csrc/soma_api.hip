@@ -1119,7 +1119,17 @@ int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
   }
   hipLaunchKernelGGL((soma::k_wide_ln<2>), ln_grid, dim3(256), 0, st, a);
   if (int rc = check_launch("k_wide_ln")) return rc;
-  hipLaunchKernelGGL((soma::k_wide_head<!kPert>), dim3(unsigned(L.row_tiles), unsigned(slots)), dim3(256), 0, st, a);
+  // u = n P_out'^T into the (free) gate-input buffer, then the decoder.
+  m.A = a.n;
+  m.a_slot = R * dp;
+  m.W = a.wform + F.pout;
+  m.C = a.gin;
+  m.c_slot = R * 4 * dp;
+  m.N = soma::kWideHeadWidth;
+  m.K = dp;
+  if (int rc = launch_wide_mm(soma::kEpiStore, m, slots, st)) return rc;
+  hipLaunchKernelGGL((soma::k_wide_head<!kPert>), dim3(unsigned(L.row_tiles), unsigned(slots)), dim3(256), 0, st, a,
+                     a.gin, R * 4 * dp, soma::kWideHeadWidth);
   if (int rc = check_launch("k_wide_head")) return rc;
   return mark(ctx, kPhaseHead, st);
 }

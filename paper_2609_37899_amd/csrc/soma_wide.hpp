@@ -25,7 +25,8 @@
 //                 k_wide_mm m = GELU(n U')
 //                 k_wide_mm x += m V^T
 //   k_wide_ln     n = LN(x)
-//   k_wide_head   u = n P_out', logits = u E^T, cross entropy
+//   k_wide_mm     u = n P_out'^T (the final gain folded into P_out)
+//   k_wide_head   logits = u E^T, cross entropy
 // Padded units have zero weights and zero gate inputs, so their cell state
 // and h stay exactly 0 and every padded column of x stays 0.
 #pragma once
@@ -53,7 +54,7 @@ __host__ __device__ inline WideForm wide_form_layout(int dp, int D) {
   f.pin = 0;                                   // P_in   [d_p][32]
   f.blk0 = int64_t(dp) * kWideHeadWidth;       // per block: A' [4 d_p][d_p], R [4 d_p][d_p],
   f.blk_stride = 4 * m;                        //   U' [4 d_p][d_p], V [d_p][4 d_p]
-  f.pout = f.blk0 + int64_t(D) * f.blk_stride; // P_out' [d_p][32]: feature c, output q
+  f.pout = f.blk0 + int64_t(D) * f.blk_stride; // P_out' [32][d_p]
   f.total = f.pout + int64_t(dp) * kWideHeadWidth;
   return f;
 }
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(256) void k_wide_form(WideArgs a) {
   } else {                                            // P_out' [c][q] = P_out[c][q] g_f[c]
     const int64_t r = k - pout0, c = r / kWideHeadWidth, q = r % kWideHeadWidth;
     const float g = wide_coord(th, gain0 + 2 * int64_t(D) * dt + c, gain0, a.probe, key, pair, step_lo, seps);
-    for (int i = 0; i < 4; ++i) put(F.pout + c * kWideHeadWidth + q + i, w[i] * g);   // not split: no bound needed
+    for (int i = 0; i < 4; ++i) put(F.pout + (q + i) * dp + c, w[i] * g);
   }
   report_split_range(a.err, ok);
 }
@@ -401,60 +402,50 @@ __global__ __launch_bounds__(256) void k_wide_ln(WideArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// The decoder: u = n P_out' (32 features, the final gain folded in), logits
-// = u E^T over the 256 byte values, cross entropy against the next byte.
-// One wave per row, 64 rows per block (a 64-row tile of the slot); the
-// tile's sum of cross entropies goes to part[slot][tile] (fp64, rows in
+// The decoder: logits = u E^T over the 256 byte values and the cross entropy
+// against the next byte, u = n P_out'^T from the products above ([R][32] per
+// slot, row stride u_ld).  One wave per row; lane l keeps rows l, l + 64,
+// l + 128, l + 192 of the expert's E in registers, and u is broadcast from
+// the lanes that loaded it.  A block covers kWideHeadRows rows of a slot and
+// writes their sum of cross entropies to part[slot][tile] (fp64, rows in
 // order).  Evaluations also write u and the log-sum-exp per position
 // b (T-1) + t for the delta rule.  fp32 products on the vector ALU.
 // ---------------------------------------------------------------------------
-constexpr int kWideHeadRows = 64;
+constexpr int kWideHeadRows = 256;
 
 template <bool kEval>
-__global__ __launch_bounds__(256) void k_wide_head(WideArgs a) {
-  constexpr int EW = kWideHeadWidth, ELD = EW + 1;
-  __shared__ float ps[512 * ELD];            // P_out' [d_p][32], rows padded
-  __shared__ float es[kVocab * ELD];         // E [256][32], rows padded
-  __shared__ float ns[4][512];               // a wave's row of n
-  __shared__ float us[4][EW];                // a wave's decoder input
+__global__ __launch_bounds__(256) void k_wide_head(WideArgs a, const float* u_base, int64_t u_slot, int u_ld) {
+  constexpr int EW = kWideHeadWidth;
+  constexpr int RPW = kWideHeadRows / 4;     // rows per wave
   __shared__ double ce_w[4];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int tile = blockIdx.x, s = blockIdx.y;
   int e, jl, sg;
   wide_slot(a, s, e, jl, sg);
   const int64_t slot = wide_slot_index(a, e, jl, sg);
-  const int dp = a.dp;
   const int64_t R = int64_t(a.T - 1) * a.B;
-  const WideForm F = wide_form_layout(dp, a.D);
-  const float* P = a.wform + slot * F.total + F.pout;
   const float* Ee = a.E + int64_t(e) * a.e_stride;
-  for (int i = threadIdx.x; i < dp * EW; i += 256) ps[(i / EW) * ELD + i % EW] = P[i];
-  for (int i = threadIdx.x; i < kVocab * EW; i += 256) es[(i / EW) * ELD + i % EW] = Ee[i];
+  float ev[4][EW];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int k = 0; k < EW; k += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(Ee + (lane + 64 * j) * EW + k);
+      ev[j][k] = v.x; ev[j][k + 1] = v.y; ev[j][k + 2] = v.z; ev[j][k + 3] = v.w;
+    }
   const uint8_t* by = a.bytes + int64_t((a.j0 + jl) / a.ppb) * a.bstride + int64_t(e) * a.B * a.T;
-  __syncthreads();
+  const float* ub = u_base + slot * u_slot;
   double ce_sum = 0.0;
-  const int q = lane & 31, half = lane >> 5;
-  for (int i = 0; i < kWideHeadRows / 4; ++i) {
-    const int64_t r = int64_t(tile) * kWideHeadRows + wave * (kWideHeadRows / 4) + i;
+  for (int i = 0; i < RPW; ++i) {
+    const int64_t r = int64_t(tile) * kWideHeadRows + wave * RPW + i;
     if (r >= R) break;                                 // wave-uniform
-    const float* nr = a.n + (slot * R + r) * dp;
-    wave_lds_sync();                                   // the previous row's reads are done
-    for (int c = lane; c < dp; c += 64) ns[wave][c] = nr[c];
-    wave_lds_sync();
-    // u[q]: lanes q and q + 32 each sum half of the features, then add.
-    float u = 0.0f;
-    for (int c = half; c < dp; c += 2) u = __builtin_fmaf(ns[wave][c], ps[c * ELD + q], u);
-    u += __shfl_xor(u, 32);
-    if (lane < EW) us[wave][lane] = u;
-    wave_lds_sync();
-    float lg[4];
+    const float u = lane < EW ? ub[r * u_ld + lane] : 0.0f;
+    float lg[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int v = lane + 64 * j;
-      float acc = 0.0f;
+    for (int k = 0; k < EW; ++k) {
+      const float uk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(u), k));
 #pragma unroll
-      for (int k = 0; k < EW; ++k) acc = __builtin_fmaf(es[v * ELD + k], us[wave][k], acc);
-      lg[j] = acc;
+      for (int j = 0; j < 4; ++j) lg[j] = __builtin_fmaf(ev[j][k], uk, lg[j]);
     }
     float mx = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
     mx = wave_max(mx);
