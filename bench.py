@@ -251,6 +251,16 @@ def main():
     ctx.set_phase_timing(False)
     sec = (t1 - t0) / args.steps
     lv = losses.cpu().numpy()
+    # The unperturbed evaluation (the validation loss the plateau schedule
+    # reads), timed apart from the step.
+    eval_loss = torch.zeros(w.n_experts, dtype=torch.float32, device=dev)
+    ctx.eval_loss(theta, dbatches[0], eval_loss)
+    torch.cuda.synchronize()
+    te = time.perf_counter()
+    for _ in range(3):
+        ctx.eval_loss(theta, dbatches[0], eval_loss)
+    torch.cuda.synchronize()
+    eval_ms = (time.perf_counter() - te) / 3 * 1e3
     assert np.all(np.isfinite(lv)), "non-finite losses"
 
     # Dominant kernel and its roofline.
@@ -337,6 +347,7 @@ def main():
                    "parallelism": "single GPU, all experts and directions in each launch"},
         "algorithmic_tflops": round(total_flops / sec / 1e12, 3),
         "phase_ms": {k: round(v, 3) for k, v in ms.items()},
+        "eval_ms": round(eval_ms, 3),
         "roofline": roof,
         "mean_loss": float(np.mean(lv)),
     }

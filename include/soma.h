@@ -351,7 +351,13 @@ int soma_spsa_step_adam_sched(soma_ctx* ctx, float* theta_dev, float* m_dev, flo
 
 /* Unperturbed mean cross entropy of every expert on its own batch
  * (Appendix E, L_CE; the expert validation loss of Section 6).
- *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8, loss_dev [N] fp32 out. */
+ *   theta_dev [N][d] fp32, bytes_dev [N][B][T] uint8, loss_dev [N] fp32 out.
+ * The stacked LSTM runs the step's kernels with radius 0 (every weight
+ * formed as fma(+-0, z, theta) = theta; split fp16 products): one direction,
+ * both signs, the + sign's sum is the loss.  With soma_config.flags set it
+ * runs the reference kernels instead (fp32 products, one launch per time
+ * step, tiled weights).  A weight outside the split products' range makes
+ * the losses NaN. */
 int soma_eval_loss(soma_ctx* ctx, const float* theta_dev, const uint8_t* bytes_dev,
                    float* loss_dev, void* stream);
 

@@ -361,6 +361,20 @@ __global__ void k_loss_reduce(const double* part, int row_tiles, int N, int pcs,
   if (lossd) lossd[o] = tot * inv_rows;
 }
 
+// loss[e] = (sum over tiles in order) / (B (T-1)) of slot (e, direction 0,
+// sign +) of a pass with PC directions per expert and both signs: the
+// evaluation that runs the step's kernels at radius 0.
+__global__ void k_eval_reduce(const double* part, int row_tiles, int N, int PC, double inv_rows, float* loss,
+                              const unsigned* err) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= N) return;
+  const double* p = part + (int64_t(e) * PC * 2) * row_tiles;
+  double tot = 0.0;
+  for (int k = 0; k < row_tiles; ++k) tot += p[k];
+  if (*err) tot = __builtin_nan("");
+  loss[e] = static_cast<float>(tot * inv_rows);
+}
+
 // c[e][j] = (L+ - L-) / (2 eps_e P) from the fp64 means, rounded once to fp32;
 // summed mode: the loss differences of all experts added in expert order
 // (the shared loss difference), divided by expert e's own radius: Eq.
@@ -1682,10 +1696,29 @@ int soma_eval_loss(soma_ctx* ctx, const float* theta, const uint8_t* bytes, floa
   unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;
   hipLaunchKernelGGL(soma::k_zero_u32, dim3(1), dim3(64), 0, st, err, 1);
   if (int rc = check_launch("k_zero_u32")) return rc;
+  const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
+  if (c.arch == SOMA_ARCH_LSTM && c.flags == 0) {
+    // The step's kernels with radius 0: every weight is formed as
+    // fma(+-0, z, theta) = theta, so both signs of direction 0 are the
+    // unperturbed model (the probes are drawn and multiplied by zero; any
+    // seeds do, so the fp64 loss area serves as their memory).  The + sign's
+    // sum is the loss.
+    float* r = reinterpret_cast<float*>(ctx->ws + L.rates);
+    const int N = c.n_experts;
+    hipLaunchKernelGGL(soma::k_fill_rates, dim3((N + 255) / 256), dim3(256), 0, st, r, r + N, N, 0.0f, 0.0f);
+    if (int rc = check_launch("k_fill_rates")) return rc;
+    const uint64_t* any_seeds = reinterpret_cast<const uint64_t*>(ctx->ws + L.lossd);
+    const int rc0 = run_forward<true>(ctx, theta, any_seeds, 0, r, 1, bytes, 0, 1, st);
+    ctx->timing = timing;
+    if (rc0) return rc0;
+    hipLaunchKernelGGL(soma::k_eval_reduce, dim3((N + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, N, L.pc, inv_rows, loss, err);
+    if (int rc = check_launch("k_eval_reduce")) return rc;
+    return ok();
+  }
   const int rc0 = run_forward<false>(ctx, theta, nullptr, 0, nullptr, 0, bytes, 0, 1, st);
   ctx->timing = timing;
   if (rc0) return rc0;
-  const double inv_rows = 1.0 / double(int64_t(c.seq_len - 1) * c.batch);
   hipLaunchKernelGGL(soma::k_loss_reduce, dim3((c.n_experts + 255) / 256), dim3(256), 0, st,
                      reinterpret_cast<const double*>(ctx->ws + L.part), L.row_tiles, c.n_experts, 1,
                      1, 1, 1, 0, inv_rows, loss, static_cast<double*>(nullptr), err);

@@ -106,19 +106,48 @@ def test_rademacher_step_matches_oracle(oracle_mod, name, probe):
     assert not np.array_equal(r["theta"], r["theta0"])
 
 
-def test_eval_loss_matches_oracle(oracle_mod):
+@pytest.mark.parametrize("name", ["tiny", "ragged_l2", "l3_b70", "h64_b50_l2", "b64_h128", "b32_h384",
+                                  "h704_b12", "h96_b70"])
+def test_eval_loss_matches_oracle(oracle_mod, name):
+    """The evaluation runs the step's kernels at radius 0 (split fp16
+    products; persistent, one-block or per-step recurrence by shape); the
+    reference kernels (fp32 products, one launch per time step, tiled
+    weights) run under the execution flags.  Both against the oracle, and
+    against each other."""
     torch = require_gpu()
-    for name in ("tiny", "ragged_l2", "l3_b70"):
-        N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
-        shape = soma.Shape(N, L, E, H, B, T, P, mode, pc)
-        theta = synth.init_theta(N, L, E, H, init_seed=2, distinct=True) * np.float32(2.0)
-        data = synth.expert_batches([200 + e for e in range(N)], B, T)
-        ctx = soma.Context(shape)
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
+    theta = synth.init_theta(N, L, E, H, init_seed=2, distinct=True) * np.float32(2.0)
+    data = synth.expert_batches([200 + e for e in range(N)], B, T)
+    ref = oracle_mod.eval_loss(oracle_mod.make_cfg(N, L, E, H, B, T, P), theta, data)
+    out = []
+    for flags in (0, soma.FLAG_PER_STEP_RECURRENCE | soma.FLAG_TILED_WEIGHTS):
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags=flags))
         loss = torch.zeros(N, dtype=torch.float32, device="cuda")
         ctx.eval_loss(torch.from_numpy(theta).cuda(), torch.from_numpy(data).cuda(), loss)
         torch.cuda.synchronize()
-        ref = oracle_mod.eval_loss(oracle_mod.make_cfg(N, L, E, H, B, T, P), theta, data)
-        assert_losses_close(loss.cpu().numpy(), ref)
+        out.append(loss.cpu().numpy())
+        ctx.close()
+        err = assert_losses_close(out[-1], ref)
+        print(f"{name} flags {flags}: eval loss rel {err:.2e}")
+    np.testing.assert_allclose(out[0], out[1], rtol=2e-5)
+
+
+def test_eval_loss_full_size(oracle_mod):
+    """The N = 2 workload's evaluation at full size (B = 64, T = 256,
+    H = 512): both experts' losses against the oracle."""
+    torch = require_gpu()
+    w = workloads.SOMA_N2
+    theta = synth.init_theta(w.n_experts, w.n_layers, w.embed, w.hidden, init_seed=5, distinct=True) * np.float32(2.0)
+    data = synth.expert_batches_in_child(w.cluster_seeds, w.batch, w.seq_len)
+    ctx = soma.Context(soma.Shape(w.n_experts, w.n_layers, w.embed, w.hidden, w.batch, w.seq_len, w.n_pairs))
+    loss = torch.zeros(w.n_experts, dtype=torch.float32, device="cuda")
+    ctx.eval_loss(torch.from_numpy(theta).cuda(), torch.from_numpy(data).cuda(), loss)
+    torch.cuda.synchronize()
+    ctx.close()
+    print("oracle evaluation at full size", flush=True)
+    ref = oracle_mod.eval_loss(oracle_mod.cfg_from(w), theta, data)
+    err = assert_losses_close(loss.cpu().numpy(), ref)
+    print(f"full-size eval loss rel {err:.2e}")
 
 
 def test_zero_weights_give_ln256():
