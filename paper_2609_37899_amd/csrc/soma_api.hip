@@ -951,14 +951,22 @@ int run_body(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
 // The wide controls' body: one pass of the kernels listed in soma_wide.hpp
 // over the pass's slots (expert, direction, sign), or over the experts
 // unperturbed (!kPert).
-int launch_wide_mm(int epi, const soma::MmArgs& m, int slots, hipStream_t st) {
-  const dim3 grid(unsigned((m.N + 127) / 128), unsigned((m.M + 127) / 128), unsigned(slots));
-  if (epi == soma::kEpiGelu)
-    hipLaunchKernelGGL((soma::k_wide_mm<soma::kEpiGelu>), grid, dim3(256), 0, st, m);
+// epi: soma::WideEpi; a_split: A stored split (else fp32, split as staged).
+int launch_wide_mm(int epi, bool a_split, soma::MmArgs m, int slots, hipStream_t st) {
+  m.ntn = (m.N + 127) / 128;
+  m.ntm = (m.M + 127) / 128;
+  m.tiles = int64_t(m.ntn) * m.ntm * slots;
+  const int64_t blocks = (m.tiles + soma::kXcds - 1) / soma::kXcds * soma::kXcds;
+  if (blocks >= (int64_t(1) << 31)) return fail(SOMA_ESHAPE, "too many product tiles in one launch");
+  const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+  if (!a_split)
+    hipLaunchKernelGGL((soma::k_wide_mm<false, soma::kEpiStore>), grid, block, 0, st, m);
+  else if (epi == soma::kEpiGelu)
+    hipLaunchKernelGGL((soma::k_wide_mm<true, soma::kEpiGelu>), grid, block, 0, st, m);
   else if (epi == soma::kEpiAdd)
-    hipLaunchKernelGGL((soma::k_wide_mm<soma::kEpiAdd>), grid, dim3(256), 0, st, m);
+    hipLaunchKernelGGL((soma::k_wide_mm<true, soma::kEpiAdd>), grid, block, 0, st, m);
   else
-    hipLaunchKernelGGL((soma::k_wide_mm<soma::kEpiStore>), grid, dim3(256), 0, st, m);
+    hipLaunchKernelGGL((soma::k_wide_mm<true, soma::kEpiStore>), grid, block, 0, st, m);
   return check_launch("k_wide_mm");
 }
 
@@ -1040,7 +1048,7 @@ int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
   m.M = SOMA_VOCAB;
   m.N = dp;
   m.K = soma::kWideHeadWidth;
-  if (int rc = launch_wide_mm(soma::kEpiStore, m, slots, st)) return rc;
+  if (int rc = launch_wide_mm(soma::kEpiStore, false, m, slots, st)) return rc;
   const dim3 ln_grid(unsigned((R + 3) / 4), unsigned(slots));
   hipLaunchKernelGGL((soma::k_wide_ln<0>), ln_grid, dim3(256), 0, st, a);
   if (int rc = check_launch("k_wide_ln")) return rc;
@@ -1058,7 +1066,7 @@ int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
     m.c_slot = R * 4 * dp;
     m.N = 4 * dp;
     m.K = dp;
-    if (int rc = launch_wide_mm(soma::kEpiStore, m, slots, st)) return rc;
+    if (int rc = launch_wide_mm(soma::kEpiStore, true, m, slots, st)) return rc;
     if (int rc = mark(ctx, kPhaseProj, st)) return rc;
     ++ctx->proj_launches;
     // the recurrence on the pre-formed R; h into the n buffer
@@ -1115,7 +1123,7 @@ int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
     m.c_slot = R * 4 * dp;
     m.N = 4 * dp;
     m.K = dp;
-    if (int rc = launch_wide_mm(soma::kEpiGelu, m, slots, st)) return rc;
+    if (int rc = launch_wide_mm(soma::kEpiGelu, true, m, slots, st)) return rc;
     m.A = a.gin;
     m.a_slot = R * 4 * dp;
     m.W = blk + 3 * mp;
@@ -1123,7 +1131,7 @@ int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
     m.c_slot = R * dp;
     m.N = dp;
     m.K = 4 * dp;
-    if (int rc = launch_wide_mm(soma::kEpiAdd, m, slots, st)) return rc;
+    if (int rc = launch_wide_mm(soma::kEpiAdd, true, m, slots, st)) return rc;
     if (l + 1 < D) {
       hipLaunchKernelGGL((soma::k_wide_ln<2>), ln_grid, dim3(256), 0, st, a);
       if (int rc = check_launch("k_wide_ln")) return rc;
@@ -1141,7 +1149,7 @@ int run_wide(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64_t 
   m.c_slot = R * 4 * dp;
   m.N = soma::kWideHeadWidth;
   m.K = dp;
-  if (int rc = launch_wide_mm(soma::kEpiStore, m, slots, st)) return rc;
+  if (int rc = launch_wide_mm(soma::kEpiStore, true, m, slots, st)) return rc;
   hipLaunchKernelGGL((soma::k_wide_head<!kPert>), dim3(unsigned(L.row_tiles), unsigned(slots)), dim3(256), 0, st, a,
                      a.gin, R * 4 * dp, soma::kWideHeadWidth);
   if (int rc = check_launch("k_wide_head")) return rc;

@@ -248,7 +248,8 @@ struct FwdArgs {
   int row_tiles;          // head row tiles per slot
   // The persistent recurrence's pre-formed instantiation only: perturbed
   // recurrent weights formed beforehand, slot s's matrix at wpre + s *
-  // wpre_slot, [4H][H] with row 4 u + g = gate g of unit u; and the signs
+  // wpre_slot, [4H][2][H] halves (each row's hi parts, then its lo parts)
+  // with row 4 u + g = gate g of unit u; and the signs
   // per direction of the pass (1: one unperturbed job per expert, else both
   // signs).
   const float* wpre;
@@ -1080,14 +1081,16 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
     // and held as split fragments.
     uint4 wh[KC], wl[KC];
     if constexpr (kPre) {
-      // Rows of the pre-formed matrix: this lane's gate row, 8 consecutive
-      // k per 32-wide chunk (the formed weights' range is checked where they
-      // were formed).
-      const float* wr = a.wpre + slot * a.wpre_slot + static_cast<int64_t>(utile * 16 * NW + wave * 16 + lr) * H + 8 * lg;
+      // Rows of the pre-formed matrix, stored split (a row's H hi parts,
+      // then its H lo parts): this lane's gate row, 8 consecutive k per
+      // 32-wide chunk (the range was checked where the weights were formed).
+      const _Float16* wr = reinterpret_cast<const _Float16*>(a.wpre + slot * a.wpre_slot) +
+                           static_cast<int64_t>(utile * 16 * NW + wave * 16 + lr) * 2 * H + 8 * lg;
 #pragma unroll
-      for (int c = 0; c < KC; ++c)
-        split8v(*reinterpret_cast<const float4*>(wr + 32 * c), *reinterpret_cast<const float4*>(wr + 32 * c + 4),
-                wh[c], wl[c]);
+      for (int c = 0; c < KC; ++c) {
+        wh[c] = *reinterpret_cast<const uint4*>(wr + 32 * c);
+        wl[c] = *reinterpret_cast<const uint4*>(wr + H + 32 * c);
+      }
     } else {
       resident_weights_split<KC, true, kRad, ZW, 16 * NW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H,
                                                           in, H, utile * 16 * NW, a.probe, key, pair, step_lo, seps,

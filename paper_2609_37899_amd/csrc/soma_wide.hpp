@@ -49,8 +49,10 @@ struct WideForm {
 __host__ __device__ inline WideForm wide_form_layout(int dp, int D) {
   WideForm f{};
   const int64_t m = 4 * int64_t(dp) * dp;
-  // Every matrix a product reads is stored output-major, [n][k]: the rows
-  // of the gate matrices are interleaved (row 4 u + g is gate g of unit u).
+  // Every matrix is stored output-major and split, [n][2][k] halves (a
+  // row's hi parts, then its lo parts: the bytes of the fp32 matrix): the
+  // rows of the gate matrices are interleaved (row 4 u + g is gate g of
+  // unit u).
   f.pin = 0;                                   // P_in   [d_p][32]
   f.blk0 = int64_t(dp) * kWideHeadWidth;       // per block: A' [4 d_p][d_p], R [4 d_p][d_p],
   f.blk_stride = 4 * m;                        //   U' [4 d_p][d_p], V [d_p][4 d_p]
@@ -68,7 +70,7 @@ struct WideArgs {
   float* wform;           // pre-formed weights, [slots][WideForm::total]
   float* U;               // [slots][256][d_p]
   float* x;               // [slots][R][d_p] residual stream
-  float* n;               // [slots][R][d_p] normalised x (also h of the recurrence)
+  float* n;               // [slots][R][d_p] normalised x, split (also h of the recurrence, fp32)
   float* gin;             // [slots][R][4 d_p] gate inputs, then the MLP hidden layer
   double* part;           // [slots][row_tiles] cross-entropy sums
   float* fdec;            // evaluation: decoder inputs u [N][B][T-1][32] (position b (T-1) + t)
@@ -106,6 +108,14 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One fp32 value -> its fp16 parts, as split2 does for a pair (hi rounded
+// toward zero, lo the exact remainder rounded toward zero).
+__device__ __forceinline__ void split1(float v, _Float16& hi, _Float16& lo) {
+  const auto h = __builtin_amdgcn_cvt_pkrtz(v, 0.0f);
+  hi = h[0];
+  lo = __builtin_amdgcn_cvt_pkrtz(v - static_cast<float>(h[0]), 0.0f)[0];
 }
 
 // Slot s of the pass: (expert, direction in the pass, sign).
@@ -167,44 +177,46 @@ __global__ __launch_bounds__(256) void k_wide_form(WideArgs a) {
     w[0] = th[k]; w[1] = th[k + 1]; w[2] = th[k + 2]; w[3] = th[k + 3];
   }
   const WideForm F = wide_form_layout(dp, D);
-  float* out = a.wform + slot * F.total;
-  const int64_t dp4 = 4 * int64_t(dp);
+  _Float16* out = reinterpret_cast<_Float16*>(a.wform + slot * F.total);
   bool ok = true;
-  float* dst = out;
-  auto put = [&](int64_t at, float v) {
+  // Element (row, col) of a matrix at float offset base with rows of K
+  // values, stored split: row r is K hi parts then K lo parts.
+  auto put = [&](int64_t base, int64_t row, int64_t col, int64_t K, float v) {
     ok = ok && __builtin_fabsf(v) <= kSplitMax;
-    dst[at] = v;
+    _Float16 h, l;
+    split1(v, h, l);
+    _Float16* p = out + 2 * base + row * 2 * K + col;
+    p[0] = h;
+    p[K] = l;
   };
   if (k < blk0) {                                     // P_in [c][q]
     const int64_t c = k / kWideHeadWidth, q = k % kWideHeadWidth;
-    for (int i = 0; i < 4; ++i) put(F.pin + c * kWideHeadWidth + q + i, w[i]);
+    for (int i = 0; i < 4; ++i) put(F.pin, c, q + i, kWideHeadWidth, w[i]);
   } else if (k < pout0) {
     const int64_t r = k - blk0;
     const int l = static_cast<int>(r / (4 * mat));
     const int which = static_cast<int>((r / mat) % 4);
     const int64_t rr = r % mat, c = rr / dt4, j = rr % dt4;
-    dst = out + F.blk0 + l * F.blk_stride;
-    const int64_t mp = 4 * int64_t(dp) * dp;
+    const int64_t mp = 4 * int64_t(dp) * dp, base = F.blk0 + l * F.blk_stride + which * mp;
     float g = 1.0f;
     if (which == 0 || which == 2)                     // A reads LN(x; g1), U reads LN(x; g2)
       g = wide_coord(th, gain0 + (2 * l + (which == 2 ? 1 : 0)) * int64_t(dt) + c, gain0, a.probe, key, pair,
                      step_lo, seps);
     for (int i = 0; i < 4; ++i) {
       const int64_t jj = j + i;
-      if (which <= 1) {                               // gate column g dt + u -> row 4 u + g
+      if (which <= 1) {                               // gate column g dt + u -> row 4 u + g (A' and R)
         const int64_t gate = jj / dt, u = jj % dt;
-        const float v = which == 0 ? w[i] * g : w[i];
-        put(which * mp + (4 * u + gate) * dp + c, v); // A' at +0, R at +4 dp^2
+        put(base, 4 * u + gate, c, dp, which == 0 ? w[i] * g : w[i]);
       } else if (which == 2) {                        // U'[j][c]
-        put(2 * mp + jj * dp + c, w[i] * g);
+        put(base, jj, c, dp, w[i] * g);
       } else {                                        // V[c][j]: row = output feature
-        put(3 * mp + c * dp4 + jj, w[i]);
+        put(base, c, jj, 4 * int64_t(dp), w[i]);
       }
     }
-  } else {                                            // P_out' [c][q] = P_out[c][q] g_f[c]
+  } else {                                            // P_out'[q][c] = P_out[c][q] g_f[c]
     const int64_t r = k - pout0, c = r / kWideHeadWidth, q = r % kWideHeadWidth;
     const float g = wide_coord(th, gain0 + 2 * int64_t(D) * dt + c, gain0, a.probe, key, pair, step_lo, seps);
-    for (int i = 0; i < 4; ++i) put(F.pout + (q + i) * dp + c, w[i] * g);
+    for (int i = 0; i < 4; ++i) put(F.pout, q + i, c, dp, w[i] * g);
   }
   report_split_range(a.err, ok);
 }
@@ -218,43 +230,56 @@ __global__ void k_fill_f32(float* out, int64_t n) {
 // ---------------------------------------------------------------------------
 // Batched products on the fp16 matrix cores from split fp32 operands:
 //   C[s][m][n] (= | += | GELU of) sum_k A[s][m][k] W[s][n][k]
-// A row-major [M][K] per slot, or per expert (the tied matrix); W
-// output-major [N][K].  blockIdx.z runs over the pass's slots (expert,
-// direction, sign), whose buffers sit at (e PC + jl) NS + sg.
-// Block tile 128 (n) x 128 (m), four waves of 64 x 64; K in 32-wide chunks
-// (K % 32 == 0, N % 4 == 0), staged through LDS as fp16 hi/lo parts, the
-// next chunk's global loads issued before the current chunk's products.
+// W is stored split ([N][2][K] halves: per row its K hi parts, then its K lo
+// parts), as the form kernel writes it.  A is either stored split the same
+// way ([M][2][K], written so by LayerNorm and by the GELU epilogue) or fp32
+// [M][K], split as it is staged (the tied matrix of the input projection);
+// per slot, or per expert.  C is fp32 [M][N] (store, add), or split
+// [M][2][N] (GELU: the next product's A).  Block tile 128 (n) x 128 (m),
+// four waves of 64 x 64; K in 32-wide chunks (K % 32 == 0, N % 4 == 0)
+// staged through LDS, the next chunk's global loads issued before the
+// current chunk's products.  Tiles are dealt so that each XCD (blocks go to
+// the 8 XCDs round-robin) works through a contiguous range of them: the n
+// tiles of one m tile, and the m tiles of one slot, share its L2.
 // ---------------------------------------------------------------------------
 enum WideEpi { kEpiStore = 0, kEpiGelu = 1, kEpiAdd = 2 };
 
 struct MmArgs {
-  const float* A;
-  int64_t a_slot;     // floats between consecutive A matrices (slots, or experts)
+  const void* A;
+  int64_t a_slot;     // A elements (floats or split pairs) between consecutive A matrices (slots, or experts)
   int a_expert;       // A is per expert rather than per slot
-  const float* W;
-  int64_t w_slot;
-  float* C;
-  int64_t c_slot;
+  const void* W;      // split
+  int64_t w_slot;     // floats (split pairs) between slots' matrices
+  void* C;
+  int64_t c_slot;     // elements between slots' outputs
   int M, N, K;
   int pcs, PC, NS;    // the pass's slots
+  int ntn, ntm;       // n tiles, m tiles
+  int64_t tiles;      // ntn * ntm * slots
   unsigned* err;
 };
 
 constexpr int kMmLd = 48;   // LDS row in halves: 32 + 16 (an odd multiple of 32 bytes)
+constexpr int kXcds = 8;
 
-template <int kEpi>
+template <bool kASplit, int kEpi>
 __global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
   __shared__ __attribute__((aligned(16))) _Float16 sa[2][128 * kMmLd];   // activations (hi, lo)
   __shared__ __attribute__((aligned(16))) _Float16 sw[2][128 * kMmLd];   // weights (hi, lo)
+  const int64_t per_xcd = (p.tiles + kXcds - 1) / kXcds;
+  const int64_t tile = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (tile >= p.tiles) return;                          // block-uniform
+  const int nt = static_cast<int>(tile % p.ntn);
+  const int64_t rest = tile / p.ntn;
+  const int mtile = static_cast<int>(rest % p.ntm), z = static_cast<int>(rest / p.ntm);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
   const int wn = wave & 1, wm = wave >> 1;
-  const int n0 = blockIdx.x * 128, m0 = blockIdx.y * 128;
-  const int sg = blockIdx.z % p.NS, jl = (blockIdx.z / p.NS) % p.pcs, e = blockIdx.z / (p.NS * p.pcs);
+  const int n0 = nt * 128, m0 = mtile * 128;
+  const int sg = z % p.NS, jl = (z / p.NS) % p.pcs, e = z / (p.NS * p.pcs);
   const int64_t s = (int64_t(e) * p.PC + jl) * p.NS + sg;
-  const float* A = p.A + (p.a_expert ? int64_t(e) : s) * p.a_slot;
-  const float* W = p.W + s * p.w_slot;
-  float* C = p.C + s * p.c_slot;
+  const int64_t a_off = (p.a_expert ? int64_t(e) : s) * p.a_slot;
   const int M = p.M, N = p.N, K = p.K;
+  const _Float16* Wh = reinterpret_cast<const _Float16*>(p.W) + 2 * s * p.w_slot;
   bool ok = true;
 
   f32x4 acc[4][4];
@@ -263,32 +288,45 @@ __global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  float4 pa[4], pw[4];
+  // Staging: a split row chunk is 32 hi then 32 lo halves (4 uint4 each);
+  // an fp32 row chunk is 8 float4.  Thread idx = t + 256 i covers row
+  // idx >> 3 and piece idx & 7 of both operands.
+  uint4 pa[4], pw[4];
+  float4 pf[4];
   auto gload = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = threadIdx.x + 256 * i;
-      const int row = idx >> 3, k4 = idx & 7;          // activations: 128 rows x 8 float4
-      const int m = m0 + row;
-      pa[i] = m < M ? *reinterpret_cast<const float4*>(A + int64_t(m) * K + k0 + 4 * k4) : make_float4(0.f, 0.f, 0.f, 0.f);
-      const int n = n0 + row;                          // weights: 128 rows x 8 float4 along k
-      pw[i] = n < N ? *reinterpret_cast<const float4*>(W + int64_t(n) * K + k0 + 4 * k4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const int row = idx >> 3, pc = idx & 7, part = pc >> 2, q = pc & 3;
+      const int m = m0 + row, n = n0 + row;
+      if constexpr (kASplit) {
+        const _Float16* A = reinterpret_cast<const _Float16*>(p.A) + 2 * a_off;
+        pa[i] = m < M ? *reinterpret_cast<const uint4*>(A + int64_t(m) * 2 * K + part * K + k0 + 8 * q)
+                      : make_uint4(0u, 0u, 0u, 0u);
+      } else {
+        const float* A = reinterpret_cast<const float*>(p.A) + a_off;
+        pf[i] = m < M ? *reinterpret_cast<const float4*>(A + int64_t(m) * K + k0 + 4 * pc)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      pw[i] = n < N ? *reinterpret_cast<const uint4*>(Wh + int64_t(n) * 2 * K + part * K + k0 + 8 * q)
+                    : make_uint4(0u, 0u, 0u, 0u);
     }
   };
   auto sstore = [&]() {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = threadIdx.x + 256 * i;
-      const int row = idx >> 3, k4 = idx & 7;
-      uint2 hi, lo;
-      ok = ok && split_range_ok(pa[i]);
-      split4(pa[i], hi, lo);
-      *reinterpret_cast<uint2*>(&sa[0][row * kMmLd + 4 * k4]) = hi;
-      *reinterpret_cast<uint2*>(&sa[1][row * kMmLd + 4 * k4]) = lo;
-      ok = ok && split_range_ok(pw[i]);
-      split4(pw[i], hi, lo);
-      *reinterpret_cast<uint2*>(&sw[0][row * kMmLd + 4 * k4]) = hi;
-      *reinterpret_cast<uint2*>(&sw[1][row * kMmLd + 4 * k4]) = lo;
+      const int row = idx >> 3, pc = idx & 7, part = pc >> 2, q = pc & 3;
+      if constexpr (kASplit) {
+        *reinterpret_cast<uint4*>(&sa[part][row * kMmLd + 8 * q]) = pa[i];
+      } else {
+        uint2 hi, lo;
+        ok = ok && split_range_ok(pf[i]);
+        split4(pf[i], hi, lo);
+        *reinterpret_cast<uint2*>(&sa[0][row * kMmLd + 4 * pc]) = hi;
+        *reinterpret_cast<uint2*>(&sa[1][row * kMmLd + 4 * pc]) = lo;
+      }
+      *reinterpret_cast<uint4*>(&sw[part][row * kMmLd + 8 * q]) = pw[i];
     }
   };
 
@@ -306,35 +344,43 @@ __global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
       bl[mt] = *reinterpret_cast<const uint4*>(&sa[1][row * kMmLd + 8 * lg]);
     }
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      const int row = wn * 64 + 16 * nt + lr;
+    for (int ntl = 0; ntl < 4; ++ntl) {
+      const int row = wn * 64 + 16 * ntl + lr;
       const uint4 wh = *reinterpret_cast<const uint4*>(&sw[0][row * kMmLd + 8 * lg]);
       const uint4 wl = *reinterpret_cast<const uint4*>(&sw[1][row * kMmLd + 8 * lg]);
-      mfma3_batch<4>(wh, wl, bh, bl, acc[nt]);
+      mfma3_batch<4>(wh, wl, bh, bl, acc[ntl]);
     }
   }
-  report_split_range(p.err, ok);
 
-  // acc[nt][mt][i] = C[m0 + 64 wm + 16 mt + lr][n0 + 64 wn + 16 nt + 4 lg + i]
+  // acc[ntl][mt][i] = C[m0 + 64 wm + 16 mt + lr][n0 + 64 wn + 16 ntl + 4 lg + i]
 #pragma unroll
-  for (int nt = 0; nt < 4; ++nt) {
-    const int n = n0 + wn * 64 + 16 * nt + 4 * lg;
+  for (int ntl = 0; ntl < 4; ++ntl) {
+    const int n = n0 + wn * 64 + 16 * ntl + 4 * lg;
     if (n >= N) continue;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int m = m0 + wm * 64 + 16 * mt + lr;
       if (m >= M) continue;
-      float4* c = reinterpret_cast<float4*>(C + int64_t(m) * N + n);
-      float4 v = make_float4(acc[nt][mt][0], acc[nt][mt][1], acc[nt][mt][2], acc[nt][mt][3]);
-      if (kEpi == kEpiGelu) {
+      float4 v = make_float4(acc[ntl][mt][0], acc[ntl][mt][1], acc[ntl][mt][2], acc[ntl][mt][3]);
+      if constexpr (kEpi == kEpiGelu) {
         v = make_float4(gelu_f(v.x), gelu_f(v.y), gelu_f(v.z), gelu_f(v.w));
-      } else if (kEpi == kEpiAdd) {
-        const float4 o = *c;
-        v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+        ok = ok && split_range_ok(v);
+        uint2 hi, lo;
+        split4(v, hi, lo);
+        _Float16* C = reinterpret_cast<_Float16*>(p.C) + 2 * s * p.c_slot + int64_t(m) * 2 * N + n;
+        *reinterpret_cast<uint2*>(C) = hi;
+        *reinterpret_cast<uint2*>(C + N) = lo;
+      } else {
+        float4* c = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.C) + s * p.c_slot + int64_t(m) * N + n);
+        if constexpr (kEpi == kEpiAdd) {
+          const float4 o = *c;
+          v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+        }
+        *c = v;
       }
-      *c = v;
     }
   }
+  report_split_range(p.err, ok);
 }
 
 // ---------------------------------------------------------------------------
@@ -343,7 +389,8 @@ __global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
 //   kMode 1: x += h               (the LSTM sublayer's residual; h in n)
 //   kMode 2: x as it is
 // then n = (x - mean) / sqrt(var + 1e-5) over the first d_t features (biased
-// variance), 0 on the padded ones.  Rows are r = t B + b.
+// variance), 0 on the padded ones, written split (the row's hi parts, then
+// its lo parts) over the fp32 row of h it replaces.  Rows are r = t B + b.
 // ---------------------------------------------------------------------------
 template <int kMode>
 __global__ __launch_bounds__(256) void k_wide_ln(WideArgs a) {
@@ -396,9 +443,18 @@ __global__ __launch_bounds__(256) void k_wide_ln(WideArgs a) {
     }
   sq = wave_sum(sq);
   const float inv = 1.0f / __builtin_sqrtf(sq / static_cast<float>(dt) + 1e-5f);
+  // n, split into its fp16 parts: the row's dp hi parts, then its dp lo
+  // parts (the bytes of the fp32 row it replaces).
+  _Float16* ns = reinterpret_cast<_Float16*>(nr);
 #pragma unroll
   for (int i = 0; i < kMaxC; ++i)
-    if (i < nc) nr[64 * i + lane] = 64 * i + lane < dt ? (v[i] - mean) * inv : 0.0f;
+    if (i < nc) {
+      const float y = 64 * i + lane < dt ? (v[i] - mean) * inv : 0.0f;
+      _Float16 h, l;
+      split1(y, h, l);
+      ns[64 * i + lane] = h;
+      ns[dp + 64 * i + lane] = l;
+    }
 }
 
 // ---------------------------------------------------------------------------
