@@ -14,7 +14,8 @@ the HIP path and the CPU oracle receive.
   draws its uniforms from ``SeedSequence([data_seed, cs, step])``.
 * Initial weights are U(-1/sqrt(H), 1/sqrt(H)) from ``SeedSequence([init_seed])``,
   drawn in float64 and rounded to float32; every expert starts from the same
-  body ("branch: copy seed body", Section 4) unless ``distinct`` is set.
+  body (the paper's experts begin as copies of one seed body, Section 4)
+  unless ``distinct`` is set.
 """
 from __future__ import annotations
 

@@ -6,8 +6,8 @@ no normalization gains).  Law 2 is the dense Rademacher law of the paper's
 variance theory (Section 4, Eq. main-spsa; Appendix F, Prop. block-variance).
 
 Closed forms used, for small eps, with q = P(z_k != 0):
-  * one direction gives z z^T g + O(eps^2), whose mean is q g (no
-    inverse-probability rescaling, Appendix E);
+  * one direction gives z z^T g + O(eps^2), whose mean is q g (the paper
+    does not divide by the probability of a nonzero coordinate, Appendix E);
   * its centered variance is tr Cov(z z^T g) = q (1 + s - 2q) ||g||^2 with
     s = q d (the R_g prediction of Appendix estimator-iso, all coordinates
     ordinary): d/4 ||g||^2 for the sparse law, (d - 1) ||g||^2 for the dense
