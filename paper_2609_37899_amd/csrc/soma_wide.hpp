@@ -237,8 +237,9 @@ __global__ void k_fill_f32(float* out, int64_t n) {
 // per slot, or per expert.  C is fp32 [M][N] (store, add), or split
 // [M][2][N] (GELU: the next product's A).  Block tile 128 (n) x 128 (m),
 // four waves of 64 x 64; K in 32-wide chunks (K % 32 == 0, N % 4 == 0)
-// staged through LDS, the next chunk's global loads issued before the
-// current chunk's products.  Tiles are dealt so that each XCD (blocks go to
+// staged through two LDS buffers: chunk c + 1's global loads are in flight
+// during chunk c's products and stored into the other buffer after them,
+// one block barrier per chunk.  Tiles are dealt so that each XCD (blocks go to
 // the 8 XCDs round-robin) works through a contiguous range of them: the n
 // tiles of one m tile, and the m tiles of one slot, share its L2.
 // ---------------------------------------------------------------------------
@@ -259,13 +260,13 @@ struct MmArgs {
   unsigned* err;
 };
 
-constexpr int kMmLd = 48;   // LDS row in halves: 32 + 16 (an odd multiple of 32 bytes)
+constexpr int kMmLd = 80;   // LDS row in halves: 32 hi, 32 lo, 16 spare (160 bytes, an odd multiple of 32)
 constexpr int kXcds = 8;
 
 template <bool kASplit, int kEpi>
 __global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
-  __shared__ __attribute__((aligned(16))) _Float16 sa[2][128 * kMmLd];   // activations (hi, lo)
-  __shared__ __attribute__((aligned(16))) _Float16 sw[2][128 * kMmLd];   // weights (hi, lo)
+  __shared__ __attribute__((aligned(16))) _Float16 sa[2][128 * kMmLd];   // [buffer] activations, rows hi | lo
+  __shared__ __attribute__((aligned(16))) _Float16 sw[2][128 * kMmLd];   // [buffer] weights, rows hi | lo
   const int64_t per_xcd = (p.tiles + kXcds - 1) / kXcds;
   const int64_t tile = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
   if (tile >= p.tiles) return;                          // block-uniform
@@ -312,44 +313,49 @@ __global__ __launch_bounds__(256) void k_wide_mm(MmArgs p) {
                     : make_uint4(0u, 0u, 0u, 0u);
     }
   };
-  auto sstore = [&]() {
+  auto sstore = [&](int b) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = threadIdx.x + 256 * i;
       const int row = idx >> 3, pc = idx & 7, part = pc >> 2, q = pc & 3;
       if constexpr (kASplit) {
-        *reinterpret_cast<uint4*>(&sa[part][row * kMmLd + 8 * q]) = pa[i];
+        *reinterpret_cast<uint4*>(&sa[b][row * kMmLd + 32 * part + 8 * q]) = pa[i];
       } else {
         uint2 hi, lo;
         ok = ok && split_range_ok(pf[i]);
         split4(pf[i], hi, lo);
-        *reinterpret_cast<uint2*>(&sa[0][row * kMmLd + 4 * pc]) = hi;
-        *reinterpret_cast<uint2*>(&sa[1][row * kMmLd + 4 * pc]) = lo;
+        *reinterpret_cast<uint2*>(&sa[b][row * kMmLd + 4 * pc]) = hi;
+        *reinterpret_cast<uint2*>(&sa[b][row * kMmLd + 32 + 4 * pc]) = lo;
       }
-      *reinterpret_cast<uint4*>(&sw[part][row * kMmLd + 8 * q]) = pw[i];
+      *reinterpret_cast<uint4*>(&sw[b][row * kMmLd + 32 * part + 8 * q]) = pw[i];
     }
   };
 
   gload(0);
-  for (int k0 = 0; k0 < K; k0 += 32) {
-    __syncthreads();                 // the previous chunk's fragments have been read
-    sstore();
-    __syncthreads();
-    if (k0 + 32 < K) gload(k0 + 32);
+  sstore(0);
+  __syncthreads();
+  const int nk = K / 32;
+  for (int c = 0; c < nk; ++c) {
+    const int b = c & 1;
+    if (c + 1 < nk) gload(32 * (c + 1));
     uint4 bh[4], bl[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int row = wm * 64 + 16 * mt + lr;
-      bh[mt] = *reinterpret_cast<const uint4*>(&sa[0][row * kMmLd + 8 * lg]);
-      bl[mt] = *reinterpret_cast<const uint4*>(&sa[1][row * kMmLd + 8 * lg]);
+      bh[mt] = *reinterpret_cast<const uint4*>(&sa[b][row * kMmLd + 8 * lg]);
+      bl[mt] = *reinterpret_cast<const uint4*>(&sa[b][row * kMmLd + 32 + 8 * lg]);
     }
 #pragma unroll
     for (int ntl = 0; ntl < 4; ++ntl) {
       const int row = wn * 64 + 16 * ntl + lr;
-      const uint4 wh = *reinterpret_cast<const uint4*>(&sw[0][row * kMmLd + 8 * lg]);
-      const uint4 wl = *reinterpret_cast<const uint4*>(&sw[1][row * kMmLd + 8 * lg]);
+      const uint4 wh = *reinterpret_cast<const uint4*>(&sw[b][row * kMmLd + 8 * lg]);
+      const uint4 wl = *reinterpret_cast<const uint4*>(&sw[b][row * kMmLd + 32 + 8 * lg]);
       mfma3_batch<4>(wh, wl, bh, bl, acc[ntl]);
     }
+    // The other buffer was last read in chunk c - 1, before the barrier
+    // that ended it.
+    if (c + 1 < nk) sstore(b ^ 1);
+    __syncthreads();
   }
 
   // acc[ntl][mt][i] = C[m0 + 64 wm + 16 mt + lr][n0 + 64 wn + 16 ntl + 4 lg + i]
