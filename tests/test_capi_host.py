@@ -131,3 +131,34 @@ def test_step_rejects_bad_scalars_before_enqueueing(lib):
         assert lib.soma_apply_adam(h, p, p, p, 1, None, p, 0, 1e-3, p, None) == soma.SOMA_EINVAL
     finally:
         lib.soma_destroy(h)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("embed", 16, soma.SOMA_ESHAPE), ("hidden", 3, soma.SOMA_ESHAPE), ("hidden", 513, soma.SOMA_ESHAPE),
+    ("batch", 65, soma.SOMA_ESHAPE), ("flags", 1, soma.SOMA_EINVAL),
+    ("perturb_mask", soma.PERTURB_EMBEDDING | soma.PERTURB_HEAD, soma.SOMA_EINVAL)])
+def test_wide_body_limits(lib, field, value, code):
+    """The wide controls' body: head width 32, 4 <= d_t <= 512 at any width in
+    between (odd widths included), batch <= 64, no execution flags, the body
+    one group."""
+    w = workloads.WIDE_N2
+    out = ctypes.c_size_t()
+    for dt in (4, 13, 181, 361, 509, 512):
+        cfg = shape_of(w.with_(hidden=dt)).cfg()
+        assert lib.soma_workspace_size(ctypes.byref(cfg), ctypes.byref(out)) == soma.SOMA_OK, dt
+    cfg = shape_of(w).cfg()
+    setattr(cfg, field, value)
+    assert lib.soma_workspace_size(ctypes.byref(cfg), ctypes.byref(out)) == code
+    assert lib.soma_last_error()
+
+
+def test_wide_body_parameter_counts_and_chunks(lib):
+    """16 D d_t^2 + (2D + 1) d_t + 2 d_E d_t per expert at the table's widths,
+    and a workspace that the automatic chunking keeps within 64 GiB in equal
+    chunks (the N = 2 control: two chunks of 16 directions)."""
+    w = workloads.WIDE_N2
+    for dt, body in ((509, 8_325_713), (361, 4_195_181), (181, 1_060_841)):
+        assert soma.param_count(shape_of(w.with_(hidden=dt))) == body
+    ws = soma.workspace_size(shape_of(w))
+    assert ws <= 64 * 2**30
+    assert ws == soma.workspace_size(shape_of(w, pair_chunk=16))
