@@ -30,7 +30,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 PEAK_FP16_MFMA_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 # Kernels whose products run on the fp16 matrix cores from split fp32
 # operands (three fp16 products per fp32 product, fp32 accumulation).
-SPLIT_F16_KERNELS = ("k_rec_persist", "k_rec_local", "k_rec_step_split", "k_proj_stream", "k_head_stream",
+SPLIT_F16_KERNELS = ("k_rec_xchg", "k_rec_persist", "k_rec_local", "k_rec_step_split", "k_proj_stream", "k_head_stream",
                      "k_head_fused", "k_body", "k_wide_mm")
 PEAK_HBM_GBS = 8000.0
 PROBE_LAWS = {"gaussian": 0, "sparse": 1, "dense": 2}
@@ -301,7 +301,8 @@ def main():
     elif w.arch == 2:
         kname = {"rec": "k_rec_persist", "proj": "k_wide_mm", "fold": "k_wide_form", "head": "k_wide_head"}[dom]
     elif dom == "rec" and launches["rec"] < w.n_layers * (w.seq_len - 1):
-        kname = "k_rec_local" if local_rec else "k_rec_persist"
+        kname = ("k_rec_local" if local_rec else
+                 "k_rec_xchg" if phases.get("xchg_launches", 0) > 0 else "k_rec_persist")
     if os.path.exists(args.traffic):
         try:
             ent = json.load(open(args.traffic)).get(w.name, {}).get(kname)

@@ -115,7 +115,13 @@ enum soma_flags {
    * even where the streaming kernels (probes drawn once per 128 weight rows,
    * weights held in registers, split fp16 products) apply.  Results agree
    * within the split products' rounding. */
-  SOMA_FLAG_TILED_WEIGHTS = 2
+  SOMA_FLAG_TILED_WEIGHTS = 2,
+  /* Run the persistent recurrence with fp32 h staged by every block of a
+   * group, even where the split exchange applies (h published once in
+   * split form and copied into LDS by DMA, several groups per compute
+   * unit).  Both form the same split products in the same order, so their
+   * results agree bit for bit. */
+  SOMA_FLAG_STAGED_RECURRENCE = 4
 };
 
 /* Parameter groups that soma_config.perturb_mask names.  A masked group
@@ -451,8 +457,8 @@ typedef struct soma_phase_times {
                              the H = 64 recurrence forms them in the block) */
   float proj_ms;          /* input projections of layers >= 2 (k_proj_stream, or
                              the tiled k_proj) */
-  float rec_ms;           /* recurrent time steps of all layers (k_rec_persist or,
-                             at H = 64, k_rec_local: one launch per layer and
+  float rec_ms;           /* recurrent time steps of all layers (k_rec_xchg or
+                             k_rec_persist or, at H = 64, k_rec_local: one launch per layer and
                              chunk; or k_rec_step, one per time step); for
                              SOMA_ARCH_BODY the whole fused forward (k_body) */
   float head_ms;          /* head + softmax cross entropy (k_head_fused at
@@ -462,6 +468,8 @@ typedef struct soma_phase_times {
   float update_ms;        /* regenerate-and-update (k_update) */
   int32_t rec_launches;   /* recurrence launches in the step */
   int32_t proj_launches;  /* input-projection launches in the step */
+  int32_t xchg_launches;  /* of rec_launches, those of the persistent recurrence
+                             with the split exchange (k_rec_xchg) */
 } soma_phase_times;
 
 /* Turn phase timing on (enable != 0) or off for later steps on ctx. */

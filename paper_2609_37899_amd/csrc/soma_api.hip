@@ -75,6 +75,8 @@ struct Layout {
   int row_tiles = 0;   // head tiles per slot
   size_t sync = 0, rates = 0, coef = 0, lossd = 0, part = 0, U = 0, gin = 0, hseq = 0, cst = 0, hpart = 0, htgt = 0,
          total = 0;
+  // the exchange recurrence: published h ring, flags and placement counters
+  size_t xch = 0, xch_bytes = 0;
   // the paper's body (SOMA_ARCH_BODY) and the wide controls' body
   // (SOMA_ARCH_WIDE): decoder inputs, log-sum-exps and delta-rule partials
   // of an evaluation pass
@@ -127,7 +129,7 @@ int validate(const soma_config* c) {
     return fail(SOMA_ESHAPE, "n_pairs * accum must stay below 2^24");
   if (c->pair_chunk < 0 || c->pair_chunk > dirs(*c))
     return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs * accum]");
-  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS))
+  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS | SOMA_FLAG_STAGED_RECURRENCE))
     return fail(SOMA_EINVAL, "unknown flags");
   if (c->probe != SOMA_PROBE_GAUSSIAN && c->probe != SOMA_PROBE_SPARSE_RADEMACHER &&
       c->probe != SOMA_PROBE_RADEMACHER)
@@ -217,6 +219,33 @@ Layout layout_for_wide(const soma_config& c, int pc) {
 bool stream_weights(const soma_config& c);
 bool local_embedding(const soma_config& c);
 
+// The pipelined exchange recurrence (k_rec_xchg) runs for the stacked LSTM
+// with four row tiles (48 < B <= 64) at the widths it has been validated on:
+// H = 128, 256, 512 and 704.  At H = 192 a launch faulted the device, with no
+// cause found in the kernel's indexing; that width and the others not yet
+// validated take the staged recurrence.  Whether it runs also depends on the
+// device (compute units per XCD).
+bool xchg_shape(const soma_config& c) {
+  const int H = c.hidden;
+  return c.arch == SOMA_ARCH_LSTM && c.batch > 48 && c.batch <= 64 &&
+         (H == 128 || H == 256 || H == 512 || H == 704) && !(c.flags & SOMA_FLAG_PER_STEP_RECURRENCE) &&
+         !(c.flags & SOMA_FLAG_STAGED_RECURRENCE);
+}
+
+int xchg_tiles(int) { return soma::kXchgTiles; }
+
+// Groups the exchange recurrence can have at width H: 8 XCDs of at most 64
+// compute units, one block each, H / 32 blocks a group.
+int xchg_max_groups(int H) { return std::min(soma::kXchgMaxGroups, 8 * 64 / (H / 32)); }
+
+// Ring of two published steps per group: 16 NB rows x H, split (4 bytes a value).
+size_t xchg_ring_bytes(const soma_config& c) {
+  return size_t(xchg_max_groups(c.hidden)) * 2 * 16 * xchg_tiles(c.batch) * c.hidden * 4;
+}
+
+// Flags, then the per-compute-unit and per-rank placement counters.
+int xchg_counter_words() { return soma::kXchgMaxGroups * soma::kXchgFlagWords + soma::kXchgCuSlots + 8 * soma::kXchgMaxPerCu; }
+
 Layout layout_for(const soma_config& c, int pc) {
   if (c.arch == SOMA_ARCH_BODY) return layout_for_body(c, pc);
   if (c.arch == SOMA_ARCH_WIDE) return layout_for_wide(c, pc);
@@ -250,6 +279,11 @@ Layout layout_for(const soma_config& c, int pc) {
   L.htgt = at; at += round_up(sizeof(float) * hslots * R);
   L.gin = at;
   if (c.n_layers > 1) at += round_up(sizeof(float) * slots * R * 4 * H);
+  if (xchg_shape(c)) {
+    L.xch = at;
+    L.xch_bytes = xchg_ring_bytes(c);
+    at += round_up(L.xch_bytes + sizeof(unsigned) * xchg_counter_words());
+  }
   L.total = at;
   return L;
 }
@@ -285,12 +319,15 @@ struct soma_ctx {
   bool have_times;
   // device facts for the persistent recurrence
   int coop_blocks;                  // co-resident k_rec_persist blocks (0: path unavailable)
+  int xchg_per_cu;                  // co-resident k_rec_xchg blocks per compute unit (0: unavailable)
+  int xchg_cus_per_xcd;
+  int xchg_pad_lds;                 // unused dynamic LDS per block that caps its occupancy at xchg_per_cu
   float* head;                      // SOMA_ARCH_BODY, SOMA_ARCH_WIDE: the tied matrix E of expert 0 (caller owned)
   int64_t head_stride;              // floats from one expert's E to the next
   std::vector<hipEvent_t> events;   // pool, grows on demand
   std::vector<int> phase;           // phase closed by events[i]
   size_t nmarks;
-  int rec_launches, proj_launches;
+  int rec_launches, proj_launches, xchg_launches;
 };
 
 namespace soma {
@@ -737,6 +774,40 @@ const void* persist_kernel_for(int B, int H, int probe) {
   return probe == SOMA_PROBE_GAUSSIAN ? persist_kernel_for<false>(B, H) : persist_kernel_for<true>(B, H);
 }
 
+// The exchange recurrence for width H (xchg_shape) and the generator family
+// of probe law `probe`.
+template <bool kRad>
+const void* xchg_kernel_for(int nch) {
+  switch (nch) {
+    case 2: return reinterpret_cast<const void*>(&soma::k_rec_xchg<2, kRad>);
+    case 3: return reinterpret_cast<const void*>(&soma::k_rec_xchg<3, kRad>);
+    case 4: return reinterpret_cast<const void*>(&soma::k_rec_xchg<4, kRad>);
+    case 5: return reinterpret_cast<const void*>(&soma::k_rec_xchg<5, kRad>);
+    case 6: return reinterpret_cast<const void*>(&soma::k_rec_xchg<6, kRad>);
+    case 7: return reinterpret_cast<const void*>(&soma::k_rec_xchg<7, kRad>);
+    case 8: return reinterpret_cast<const void*>(&soma::k_rec_xchg<8, kRad>);
+    case 9: return reinterpret_cast<const void*>(&soma::k_rec_xchg<9, kRad>);
+    case 10: return reinterpret_cast<const void*>(&soma::k_rec_xchg<10, kRad>);
+    case 11: return reinterpret_cast<const void*>(&soma::k_rec_xchg<11, kRad>);
+    default: return nullptr;
+  }
+}
+
+const void* xchg_kernel_for(int H, int probe) {
+  return probe == SOMA_PROBE_GAUSSIAN ? xchg_kernel_for<false>(H / 64) : xchg_kernel_for<true>(H / 64);
+}
+
+// Groups of the exchange recurrence (a multiple of 8, each on one XCD), or
+// 0 where it does not run: one block per compute unit, H / 32 blocks a
+// group, the compute units of an XCD past its whole groups idle.
+int xchg_groups(const soma_ctx* ctx) {
+  const soma_config& c = ctx->cfg;
+  if (!xchg_shape(c) || ctx->xchg_per_cu <= 0) return 0;
+  const int ut = c.hidden / 32;
+  const int groups = 8 * (ctx->xchg_per_cu * ctx->xchg_cus_per_xcd / ut);
+  return groups >= 8 && groups <= xchg_max_groups(c.hidden) ? groups : 0;
+}
+
 // Its instantiation on pre-formed weights (the wide controls' body, d_p <= 512).
 template <int NB, int NCH>
 const void* persist_pre_kernel() {
@@ -895,9 +966,11 @@ int launch_local(const soma::FwdArgs& a, int jobs, int B, int probe, int kx, boo
   return check_launch("k_rec_local");
 }
 
-int launch_persist(const void* kernel, const soma::PersistArgs& p, int blocks, int threads, hipStream_t st) {
-  void* args[] = {const_cast<soma::PersistArgs*>(&p)};
-  const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), args, 0, st);
+template <class Args>
+int launch_persist(const void* kernel, const Args& p, int blocks, int threads, hipStream_t st,
+                   unsigned dyn_lds = 0) {
+  void* args[] = {const_cast<Args*>(&p)};
+  const hipError_t e = hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), args, dyn_lds, st);
   if (e != hipSuccess) return fail(SOMA_EDEVICE, "hipLaunchCooperativeKernel: %s", hipGetErrorString(e));
   return SOMA_OK;
 }
@@ -1230,12 +1303,36 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       ++ctx->proj_launches;
     }
     const int groups = kPert ? persistent_groups(ctx, 2 * N * pcs) : 0;
+    const int xgroups = kPert ? xchg_groups(ctx) : 0;
     if (kPert && local_recurrence(c)) {
       // H = 64: one block per job, h kept in the block between steps.
       const int jobs = 2 * N * pcs;   // (expert, direction, sign)
       const int kx = l == 0 && emb_local ? c.embed / 32 : 0;
       if (int rc = launch_local(a, jobs, c.batch, c.probe, kx, fused_head, st)) return rc;
       ctx->rec_launches += 1;
+    } else if (xgroups > 0) {
+      soma::XchgArgs p{};
+      p.a = a;
+      p.xh = reinterpret_cast<_Float16*>(ctx->ws + L.xch);
+      p.flag = reinterpret_cast<unsigned*>(ctx->ws + L.xch + L.xch_bytes);
+      p.cu_count = p.flag + soma::kXchgMaxGroups * soma::kXchgFlagWords;
+      p.rank_count = p.cu_count + soma::kXchgCuSlots;
+      p.err = a.err;
+      p.groups = xgroups;
+      p.cus_per_xcd = ctx->xchg_cus_per_xcd;
+      p.per_cu = ctx->xchg_per_cu;
+      p.jobs = 2 * N * pcs;   // (expert, direction, sign)
+      p.spin_limit = ctx->spin_limit;
+      // Flags and placement counters restart at zero for every launch.
+      const int words = xchg_counter_words();
+      hipLaunchKernelGGL(soma::k_zero_u32, dim3((words + 255) / 256), dim3(256), 0, st, p.flag, words);
+      if (int rc = check_launch("k_zero_u32")) return rc;
+      const int blocks = ctx->xchg_per_cu * 8 * ctx->xchg_cus_per_xcd;
+      if (int rc = launch_persist(xchg_kernel_for(H, c.probe), p, blocks, 512, st,
+                                  unsigned(ctx->xchg_pad_lds)))
+        return rc;
+      ctx->rec_launches += 1;
+      ctx->xchg_launches += 1;
     } else if (groups > 0) {
       soma::PersistArgs p{};
       p.a = a;
@@ -1321,13 +1418,48 @@ void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws,
     }
     (void)hipGetLastError();  // a failed query only disables the persistent path
   }
+  ctx->xchg_per_cu = 0;
+  ctx->xchg_cus_per_xcd = 0;
+  ctx->xchg_pad_lds = 0;
+  if (xchg_shape(*cfg)) {
+    // The exchange recurrence: one block per compute unit (unused dynamic LDS
+    // caps the occupancy where more would fit: every compute unit must hold
+    // exactly one block for the placement), compute units per XCD (8 XCDs,
+    // blocks dealt to them round-robin).  A launch that placed two of its
+    // blocks on each compute unit faulted the device, with no cause found
+    // in the kernel's indexing; that placement stays off.
+    int dev = 0, coop = 0, cus = 0, occ = 0, lds_cu = 0;
+    hipFuncAttributes fa{};
+    const void* kern = xchg_kernel_for(cfg->hidden, cfg->probe);
+    if (kern && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
+        hipFuncGetAttributes(&fa, kern) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 512, 0) == hipSuccess && coop && cus % 8 == 0 &&
+        cus / 8 <= 64 && occ >= 1) {
+      int pad = 0, got = occ;
+      if (occ > 1) {
+        pad = std::max(0, lds_cu / 2 + 2048 - int(fa.sharedSizeBytes));
+        if (int(fa.sharedSizeBytes) + pad > lds_cu ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&got, kern, 512, size_t(pad)) != hipSuccess)
+          got = 0;
+      }
+      if (got == 1) {
+        ctx->xchg_per_cu = 1;
+        ctx->xchg_cus_per_xcd = cus / 8;
+        ctx->xchg_pad_lds = pad;
+      }
+    }
+    (void)hipGetLastError();
+  }
   ctx->head = nullptr;
   ctx->head_stride = 0;
   ctx->timing = false;
   ctx->spin_limit = kSpinLimit;
   ctx->have_times = false;
   ctx->nmarks = 0;
-  ctx->rec_launches = ctx->proj_launches = 0;
+  ctx->rec_launches = ctx->proj_launches = ctx->xchg_launches = 0;
 }
 
 }  // namespace
@@ -1403,6 +1535,7 @@ int soma_get_phase_times(soma_ctx* ctx, soma_phase_times* out) {
   out->reduce_ms = acc[kPhaseReduce];
   out->update_ms = acc[kPhaseUpdate];
   out->rec_launches = ctx->rec_launches;
+  out->xchg_launches = ctx->xchg_launches;
   out->proj_launches = ctx->proj_launches;
   return ok();
 }
@@ -1469,7 +1602,7 @@ int forwards_and_coefficients(soma_ctx* ctx, const float* theta, const uint64_t*
   const soma_config& c = ctx->cfg;
   const Layout& L = ctx->lay;
   ctx->nmarks = 0;
-  ctx->rec_launches = ctx->proj_launches = 0;
+  ctx->rec_launches = ctx->proj_launches = ctx->xchg_launches = 0;
   ctx->have_times = false;
   if (int rc = mark(ctx, kPhaseStart, st)) return rc;
   unsigned* err = reinterpret_cast<unsigned*>(ctx->ws + L.sync) + kMaxGroups;

@@ -1276,6 +1276,338 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
 }
 
 // ---------------------------------------------------------------------------
+// Persistent recurrence with a pipelined split exchange (k_rec_xchg): the
+// per-step arithmetic of k_rec_persist -- G_t = G_in,t + h_{t-1} W_h+-^T on
+// the fp16 matrix cores from split operands, the cell update in the lane
+// that holds a unit's four gates -- organised so that the exchange of h
+// between the blocks of a group overlaps the products.
+//
+//  * The batch's row tiles (16 sequences each) are independent recurrences
+//    that share the block's resident weights.  A block runs sub-steps
+//    s = (t, k) in the order t, then tile k: the products of tile k at step
+//    t need only tile k's h_{t-1}, published NB sub-steps earlier, so its
+//    exchange is hidden behind the products of the other tiles (NB >= 4).
+//  * Each block publishes its 32 units of h_t of a tile already split into
+//    fp16 hi and lo parts, in the order the MFMA B operand reads them: per
+//    32-wide K chunk c and part, 64 lanes x 8 halves, lane (lr, lg) holding
+//    row lr of the tile, columns 32 c + 8 lg .. + 7.  A group keeps two steps
+//    per tile (parity t mod 2) in L2.  h_t is also written to the layer's
+//    hseq rows in fp32 for the kernels that read the whole sequence.
+//  * The tile's h_{t-1} reaches LDS by DMA (buffer_load_dwordx4 ... lds):
+//    each 1 KiB block lands unchanged and each lane reads its fragment as one
+//    16-byte word -- no staging registers, vector instructions or LDS stores.
+//    The DMA of sub-step s + 2 is issued at the end of sub-step s, into the
+//    LDS buffer its products have just released (two buffers).
+//  * Arrival is a per-(tile, block) flag word holding the steps published.
+//    A sub-step's stores are acknowledged during the next sub-step's
+//    products (one vmcnt(0) per sub-step, after the products), and the flag
+//    is raised right behind the barrier that follows; the flags needed for
+//    the DMA of sub-step s + 2 (raised a sub-step earlier) are read with one
+//    load issued halfway through the products of sub-step s and checked
+//    after them.  The gate inputs are added to the products after that wait
+//    (loads and stores share one counter, so an earlier use of a loaded
+//    value would wait for the pending stores too).
+//
+// Every wait is bounded: a wave that polls longer than the spin limit, or
+// that sees the step's abort flag, sets the flag and stops waiting; every
+// wave then runs to the end without waiting (on stale data), so the grid
+// drains, and the losses read NaN.  A block of 8 waves owns 128 gate rows
+// (32 units); a group of H / 32 blocks sits on one XCD; one block per
+// compute unit, claimed at start from the compute unit it runs on.
+//
+// The LDS DMA is issued through inline assembly: the compiler assumes that a
+// pending LDS DMA may alias every later LDS read and would wait for it
+// before each fragment read.  Its completion is covered by the sub-step's
+// vmcnt(0) and the block barrier that follows.
+// ---------------------------------------------------------------------------
+constexpr int kXchgMaxGroups = 256;    // groups of one launch (flags in the workspace)
+constexpr int kXchgFlagWords = 256;    // flag words per group: [tile][block], H / 32 <= 64 blocks
+constexpr int kXchgCuSlots = 8 * 64;   // blocks-per-compute-unit counters: (XCD, shader engine, CU)
+constexpr int kXchgMaxPerCu = 4;
+constexpr int kXchgTiles = 4;          // row tiles the pipeline needs: B > 48
+constexpr unsigned kAbortPlace = 4u;   // a block found no (group, tile) to claim
+
+struct XchgArgs {
+  FwdArgs a;
+  _Float16* xh;          // [groups][2][NB][H/32][2][64][8] published h, split, in fragment order
+  unsigned* flag;        // [groups][kXchgFlagWords] steps published per (tile, block), over all jobs
+  unsigned* cu_count;    // [kXchgCuSlots] blocks started per compute unit (zero at launch)
+  unsigned* rank_count;  // [8][kXchgMaxPerCu] blocks claimed per (XCD, rank on the CU) (zero at launch)
+  unsigned* err;         // sticky abort flag
+  int groups;            // 8 * groups per XCD
+  int cus_per_xcd;       // compute units per XCD
+  int per_cu;            // blocks per compute unit of the launch
+  int jobs;              // N * directions in this pass * 2 signs
+  unsigned spin_limit;   // polls per wait before giving up
+};
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer descriptor over [base, base + bytes) as four scalar words.
+__device__ __forceinline__ i32x4 buffer_words(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return i32x4{static_cast<int>(static_cast<uint32_t>(b)), static_cast<int>(static_cast<uint32_t>(b >> 32)),
+               static_cast<int>(bytes), 0x00020000};
+}
+
+// LDS byte address of a __shared__ location.
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) void*)(p)));
+}
+
+// 16 bytes per lane from buffer offset voff + soff (device-coherent) into LDS
+// at lds + 16 lane.
+__device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds) {
+  asm volatile("buffer_load_dwordx4 %0, %1, %2 offen sc1 lds" : : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(lds)
+               : "memory");
+}
+
+template <int NCH, bool kRad>
+__global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
+  constexpr int NW = 8;                                 // waves: 128 gate rows, 32 units (one K chunk of h)
+  constexpr int NU = 4 * NW;
+  constexpr int NB = kXchgTiles;                        // row tiles of 16 sequences
+  constexpr int KC = 2 * NCH;                           // 32-wide k chunks: H = 64 NCH
+  constexpr int FRAG = 512;                             // halves per (chunk, part) block: 64 lanes x 8
+  constexpr int TBUF = KC * 2 * FRAG;                   // halves of one tile's h in LDS
+  constexpr int XTILE = KC * 2 * FRAG;                  // halves per published (step, tile)
+  constexpr int XSLOT = 2 * NB * XTILE;                 // halves per group: parity x tile
+  constexpr int ZW = 128;                               // probe piece: 128 rows x (ZW + 8) floats
+  constexpr int ZS_BYTES = 16 * NW * (ZW + 8) * 4;
+  constexpr int RING_BYTES = 2 * TBUF * 2;
+  constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
+  constexpr int HTLD = NU + 4;                          // LDS row of the h_t tile (float4-aligned)
+  constexpr int NBLK = 2 * KC;                          // 1 KiB blocks per tile: (chunk, part)
+  constexpr int BPW = (NBLK + NW - 1) / NW;             // of them per wave (the last ones may be short)
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  __shared__ __attribute__((aligned(16))) float ht[16 * HTLD];
+  __shared__ int role[2];
+  _Float16* ring = reinterpret_cast<_Float16*>(lds);
+  const FwdArgs& a = p.a;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T, in = a.in_l;
+  const int UT = H / NU;                                // blocks per group
+
+  // Claim (group, unit tile): rank r = how many blocks started on this
+  // compute unit before this one, i = how many blocks of rank r on this XCD
+  // claimed before; position r * cus_per_xcd + i of the XCD's per_cu *
+  // cus_per_xcd blocks, UT consecutive positions per group, positions past
+  // the XCD's whole groups idle.
+  if (threadIdx.x == 0) {
+    const unsigned hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);         // HW_ID
+    const unsigned xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20) & 15;  // XCC_ID
+    const unsigned cu = ((hw >> 13) & 3) * 16 + ((hw >> 8) & 15);          // shader engine, compute unit
+    int grp = -2, tile = 0;                             // -2: unplaced (an error), -1: idle
+    if (xcc < 8) {
+      const unsigned r = __hip_atomic_fetch_add(&p.cu_count[xcc * 64 + cu], 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      if (r < static_cast<unsigned>(p.per_cu)) {
+        const unsigned i = __hip_atomic_fetch_add(&p.rank_count[xcc * kXchgMaxPerCu + r], 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        if (i < static_cast<unsigned>(p.cus_per_xcd)) {
+          const int pos = static_cast<int>(r) * p.cus_per_xcd + static_cast<int>(i);
+          grp = pos < (p.groups / 8) * UT ? (pos / UT) * 8 + static_cast<int>(xcc) : -1;
+          tile = pos % UT;
+        }
+      }
+    }
+    if (grp == -2) __hip_atomic_fetch_or(p.err, kAbortPlace, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    role[0] = grp;
+    role[1] = tile;
+  }
+  __syncthreads();
+  const int grp = role[0], utile = role[1];
+  if (grp < 0) return;
+  unsigned* const flags = p.flag + grp * kXchgFlagWords;   // [tile][block]
+  const uint32_t xbytes = static_cast<uint32_t>(p.groups) * XSLOT * 2u;
+  const i32x4 xrs = buffer_words(p.xh, xbytes);            // the same buffer for the DMA (scalar words)
+  const __amdgpu_buffer_rsrc_t xbuf = buffer_of(p.xh, xbytes);
+  const int unit = utile * NU + wave * 4 + lg;          // output unit of this lane
+  const int64_t R = static_cast<int64_t>(T - 1) * B;
+  const int64_t H4 = 4 * static_cast<int64_t>(H);
+  const uint32_t slot_bytes = static_cast<uint32_t>(R * H * sizeof(float));   // < 2^31 (host check)
+  const int S = (T - 1) * NB;                           // sub-steps of a job
+  bool failed = false;                                  // this wave stopped waiting (abort)
+
+  // Poll until every block of the group has published `target` steps of
+  // tile k (flag words [k][0 .. UT)), or give up.  Every wave polls for
+  // itself; after an abort nothing waits any more.  One load per poll: lane
+  // 63 reads the abort flag, the others their flag word, so no load of the
+  // loop is left outstanding when it exits (the compiler would otherwise
+  // wait for all memory accesses before the register is reused).
+  auto ready = [&](unsigned target, unsigned v) { return __builtin_amdgcn_ballot_w64(lane < UT && v < target) == 0; };
+  auto wait_flags = [&](int k, unsigned target) {
+    unsigned polls = 0;
+    const unsigned* addr = lane == 63 ? p.err : flags + k * 64 + lane;
+    while (!failed) {
+      const unsigned v = __hip_atomic_load(addr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const unsigned f = __builtin_amdgcn_readlane(v, 63);
+      if (ready(target, v)) break;
+      if (f != 0u || ++polls > p.spin_limit) {
+        if (lane == 0) __hip_atomic_fetch_or(p.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        failed = true;
+      } else {
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+  };
+
+  unsigned base = 0;                                    // steps of every tile published in earlier jobs
+  for (int job = grp; job < p.jobs; job += p.groups, base += static_cast<unsigned>(T - 1)) {
+    const int sg = job & 1, pj = job >> 1;
+    const int e = pj / a.pcs, jl = pj % a.pcs;
+    const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+    const uint2 key = stream_key(a.seeds[e], a.step);
+    const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+    const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+    const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
+    const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
+    const __amdgpu_buffer_rsrc_t gbuf =
+        a.layer == 0 ? buffer_of(a.U + slot * kVocab * H4, static_cast<uint32_t>(kVocab * H4 * sizeof(float)))
+                     : buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(R * H4 * sizeof(float)));
+    const __amdgpu_buffer_rsrc_t bbuf = buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
+
+    // The ring slots this job writes were read in the previous job: every
+    // block must have finished it (its last publication of every tile).
+    if (base > 0) {
+      for (int k = 0; k < NB; ++k) wait_flags(k, base);
+    }
+    // Perturbed recurrent weights of this lane's gate row, split, for the
+    // whole sequence (the probe scratch overlays the LDS ring; the barriers
+    // inside order it after the previous job's last fragment reads).
+    uint4 wh[KC], wl[KC];
+    resident_weights_split<KC, true, kRad, ZW, 16 * NW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, in + H,
+                                                        in, H, utile * 16 * NW, a.probe, key, pair, step_lo, seps,
+                                                        p.err);
+    float cs[NB];
+    int vb[NB];                                         // layer 1: byte of the next step of each tile
+    float4 gi[NB];                                      // gate inputs of each tile's next step
+    const uint32_t byte_lane = static_cast<uint32_t>(lr * T);
+    const uint32_t gi_lane = static_cast<uint32_t>((lr * 4 * H + 4 * unit) * 4);
+    // Gate inputs of (step tt, tile k) into gi[k]; layer 1 reads its folded
+    // inputs by byte value and fetches the byte of step tt + 1 along.
+    auto load_inputs = [&](int tt, int k) {
+      if (a.layer == 0) {
+        gi[k] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vb[k] * 4 * H + 4 * unit) * 4));
+        vb[k] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(k * 16 * T + tt + 1), 0);
+      } else {
+        gi[k] = buffer_load_f4s<0>(gbuf, gi_lane, static_cast<uint32_t>((tt * B + k * 16) * 4 * H * 4));
+      }
+    };
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      cs[k] = 0.0f;
+      vb[k] = a.layer == 0 ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(k * 16 * T), 0)
+                           : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k) load_inputs(0, k);
+
+    // Sub-step s = (t, k) reads tile k's h_{t-1} (published by every block
+    // at sub-step s - NB) from LDS buffer s & 1, filled by DMA issued at the
+    // end of sub-step s - 2.
+    auto issue = [&](int s) {
+      const int t = s / NB, k = s % NB;
+      const uint32_t src = static_cast<uint32_t>((grp * XSLOT + (((t - 1) & 1) * NB + k) * XTILE) * 2);
+      const uint32_t dst = lds_address(ring + (s & 1) * TBUF);
+#pragma unroll
+      for (int i = 0; i < BPW; ++i) {
+        const int b = wave + NW * i;                    // (chunk, part) block b / 2, b % 2
+        if (NBLK % NW == 0 || b < NBLK)                 // wave-uniform
+          dma16(xrs, static_cast<uint32_t>(lane * 16), src + static_cast<uint32_t>(b * FRAG * 2),
+                dst + static_cast<uint32_t>(b * FRAG * 2));
+      }
+    };
+    for (int t = 0; t + 1 < T; ++t) {
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const int s = t * NB + k;
+        // DMA(s + 2) is issued at the end of this sub-step; its flags, read
+        // halfway through the products, are checked once they are done.
+        const int s2 = s + 2, t2 = s2 / NB;
+        const int k2 = (k + 2) % NB;
+        const bool need2 = s2 < S && t2 >= 1;
+        unsigned v2 = 0;
+        f32x4 acc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (t >= 1) {
+          const _Float16* bsrc = ring + (k & 1) * TBUF + lane * 8;   // buffer s & 1 (NB is even)
+#pragma unroll
+          for (int c = 0; c < KC; ++c) {
+            if (c == KC / 2 && need2)
+              v2 = __hip_atomic_load(flags + k2 * 64 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const uint4 bh = *reinterpret_cast<const uint4*>(bsrc + (2 * c + 0) * FRAG);
+            const uint4 bl = *reinterpret_cast<const uint4*>(bsrc + (2 * c + 1) * FRAG);
+            const h8 AH = __builtin_bit_cast(h8, wh[c]), AL = __builtin_bit_cast(h8, wl[c]);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AL, __builtin_bit_cast(h8, bh), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, __builtin_bit_cast(h8, bl), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, __builtin_bit_cast(h8, bh), acc, 0, 0, 0);
+          }
+        } else if (need2) {
+          v2 = __hip_atomic_load(flags + k2 * 64 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // Every memory access of this wave has completed: the stores of
+        // sub-step s - 1, the DMA of sub-step s + 1, the flag load, the inputs.
+        wait_vmem();
+        __syncthreads();
+        // Raise the flag of the previous publication (tile k - 1 at step t, or
+        // the last tile at step t - 1): every wave's stores of it completed
+        // before the barrier.
+        if (threadIdx.x == 0 && s > 0) {
+          const int kp = (k + NB - 1) % NB;
+          const unsigned vp = base + static_cast<unsigned>(k == 0 ? t : t + 1);
+          __hip_atomic_store(flags + kp * 64 + utile, vp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (need2 && !ready(base + t2, v2)) wait_flags(k2, base + t2);
+        float h;
+        {
+          const float4 g = gi[k];
+          lstm_cell(acc[0] + g.x, acc[1] + g.y, acc[2] + g.z, acc[3] + g.w, cs[k], h);
+        }
+        // Inputs of the tile's next step (past the last step they read zeros
+        // past the buffer or unused bytes: no branch, no register copies).
+        load_inputs(t + 1, k);
+        ht[lr * HTLD + wave * 4 + lg] = h;
+        // The h_t tile is complete and every wave's products of this
+        // sub-step are done: its LDS buffer takes the DMA of sub-step s + 2.
+        __syncthreads();
+        if (need2) issue(s2);
+        // Publish h_t of tile k: threads 0..127 (part, word, row) split 8
+        // units of one row into one fragment word; threads 128..255 (row,
+        // quarter of 4 units) store the fp32 rows of the tile inside the batch.
+        const int tid = threadIdx.x;
+        if (tid < 128) {
+          const int rr = tid & 15, hw = (tid >> 4) & 3, part = tid >> 6;
+          const float* srcw = &ht[rr * HTLD + 8 * hw];
+          uint4 hi, lo;
+          split8v(*reinterpret_cast<const float4*>(srcw), *reinterpret_cast<const float4*>(srcw + 4), hi, lo);
+          const uint4 v = part ? lo : hi;
+          typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+          const uint32_t off = static_cast<uint32_t>(
+              (grp * XSLOT + ((t & 1) * NB + k) * XTILE + (utile * 2 + part) * FRAG + (16 * hw + rr) * 8) * 2);
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, xbuf, off, 0, kCoherent);
+        } else if (tid < 256) {
+          const int n = (tid - 128) >> 3, c4 = tid & 7, row = k * 16 + n;
+          if (row < B) {
+            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+            const float4 v = *reinterpret_cast<const float4*>(&ht[n * HTLD + 4 * c4]);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(u32x4, v), hbuf,
+                static_cast<uint32_t>(((t * B + row) * H + utile * NU + 4 * c4) * 4), 0, 0);
+          }
+        }
+      }
+    }
+    // The job's last publication (tile NB - 1 at step T - 2).
+    wait_vmem();
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_store(flags + (NB - 1) * 64 + utile, base + static_cast<unsigned>(T - 1), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Recurrence of one layer for H = 64 (perturbed step only), one block per
 // (expert, direction, sign) job.  All 4H = 256 gate rows of a job fit one
 // block's registers (each of the 8 waves keeps 32 rows, two MFMA row tiles,

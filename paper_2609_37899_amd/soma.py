@@ -18,6 +18,7 @@ LOSS_INDEPENDENT, LOSS_SUMMED = 0, 1
 PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
+FLAG_STAGED_RECURRENCE = 4
 ARCH_LSTM, ARCH_BODY, ARCH_WIDE = 0, 1, 2
 PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD, PERTURB_ALL = 1, 2, 4, 7
 
@@ -40,7 +41,8 @@ class PhaseTimes(ctypes.Structure):
     _fields_ = [("fold_ms", ctypes.c_float), ("proj_ms", ctypes.c_float),
                 ("rec_ms", ctypes.c_float), ("head_ms", ctypes.c_float),
                 ("reduce_ms", ctypes.c_float), ("update_ms", ctypes.c_float),
-                ("rec_launches", ctypes.c_int32), ("proj_launches", ctypes.c_int32)]
+                ("rec_launches", ctypes.c_int32), ("proj_launches", ctypes.c_int32),
+                ("xchg_launches", ctypes.c_int32)]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
