@@ -6,8 +6,10 @@
 //                   input weights, perturbed rows formed on the fly)
 //   per layer l:    k_proj_stream (l >= 2: h^(l-1) times the input weights,
 //                   weights held in registers) then the recurrence:
-//                   k_rec_persist (one cooperative launch; blocks of a group
-//                   share the recurrent weights and exchange h each step),
+//                   k_rec_xchg (one cooperative launch, four row tiles of
+//                   the batch pipelined, h exchanged pre-split by LDS DMA)
+//                   or k_rec_persist (one cooperative launch; blocks of a
+//                   group share the recurrent weights and stage h each step),
 //                   k_rec_local (H = 64: one block per perturbed model, h in
 //                   LDS, for L = 1 with the head and cross entropy fused), or
 //                   one launch per time step (k_rec_step_split / k_rec_step)
