@@ -778,25 +778,29 @@ const void* persist_kernel_for(int B, int H, int probe) {
 
 // The exchange recurrence for width H (xchg_shape) and the generator family
 // of probe law `probe`.
-template <bool kRad>
+template <bool kRad, bool kL1>
 const void* xchg_kernel_for(int nch) {
   switch (nch) {
-    case 2: return reinterpret_cast<const void*>(&soma::k_rec_xchg<2, kRad>);
-    case 3: return reinterpret_cast<const void*>(&soma::k_rec_xchg<3, kRad>);
-    case 4: return reinterpret_cast<const void*>(&soma::k_rec_xchg<4, kRad>);
-    case 5: return reinterpret_cast<const void*>(&soma::k_rec_xchg<5, kRad>);
-    case 6: return reinterpret_cast<const void*>(&soma::k_rec_xchg<6, kRad>);
-    case 7: return reinterpret_cast<const void*>(&soma::k_rec_xchg<7, kRad>);
-    case 8: return reinterpret_cast<const void*>(&soma::k_rec_xchg<8, kRad>);
-    case 9: return reinterpret_cast<const void*>(&soma::k_rec_xchg<9, kRad>);
-    case 10: return reinterpret_cast<const void*>(&soma::k_rec_xchg<10, kRad>);
-    case 11: return reinterpret_cast<const void*>(&soma::k_rec_xchg<11, kRad>);
+    case 2: return reinterpret_cast<const void*>(&soma::k_rec_xchg<2, kRad, kL1>);
+    case 3: return reinterpret_cast<const void*>(&soma::k_rec_xchg<3, kRad, kL1>);
+    case 4: return reinterpret_cast<const void*>(&soma::k_rec_xchg<4, kRad, kL1>);
+    case 5: return reinterpret_cast<const void*>(&soma::k_rec_xchg<5, kRad, kL1>);
+    case 6: return reinterpret_cast<const void*>(&soma::k_rec_xchg<6, kRad, kL1>);
+    case 7: return reinterpret_cast<const void*>(&soma::k_rec_xchg<7, kRad, kL1>);
+    case 8: return reinterpret_cast<const void*>(&soma::k_rec_xchg<8, kRad, kL1>);
+    case 9: return reinterpret_cast<const void*>(&soma::k_rec_xchg<9, kRad, kL1>);
+    case 10: return reinterpret_cast<const void*>(&soma::k_rec_xchg<10, kRad, kL1>);
+    case 11: return reinterpret_cast<const void*>(&soma::k_rec_xchg<11, kRad, kL1>);
     default: return nullptr;
   }
 }
 
-const void* xchg_kernel_for(int H, int probe) {
-  return probe == SOMA_PROBE_GAUSSIAN ? xchg_kernel_for<false>(H / 64) : xchg_kernel_for<true>(H / 64);
+// The instance for width H, the probe kind and the layer (layer 1 reads the
+// folded table).
+const void* xchg_kernel_for(int H, int probe, bool layer1) {
+  const bool rad = probe != SOMA_PROBE_GAUSSIAN;
+  if (layer1) return rad ? xchg_kernel_for<true, true>(H / 64) : xchg_kernel_for<false, true>(H / 64);
+  return rad ? xchg_kernel_for<true, false>(H / 64) : xchg_kernel_for<false, false>(H / 64);
 }
 
 // Groups of the exchange recurrence (a multiple of 8, each on one XCD), or
@@ -1330,7 +1334,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((words + 255) / 256), dim3(256), 0, st, p.flag, words);
       if (int rc = check_launch("k_zero_u32")) return rc;
       const int blocks = ctx->xchg_per_cu * 8 * ctx->xchg_cus_per_xcd;
-      if (int rc = launch_persist(xchg_kernel_for(H, c.probe), p, blocks, 512, st,
+      if (int rc = launch_persist(xchg_kernel_for(H, c.probe, l == 0), p, blocks, 512, st,
                                   unsigned(ctx->xchg_pad_lds)))
         return rc;
       ctx->rec_launches += 1;
@@ -1430,16 +1434,22 @@ void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws,
     // blocks dealt to them round-robin).  A launch that placed two of its
     // blocks on each compute unit faulted the device, with no cause found
     // in the kernel's indexing; that placement stays off.
-    int dev = 0, coop = 0, cus = 0, occ = 0, lds_cu = 0;
-    hipFuncAttributes fa{};
-    const void* kern = xchg_kernel_for(cfg->hidden, cfg->probe);
-    if (kern && hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
-        hipFuncGetAttributes(&fa, kern) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 512, 0) == hipSuccess && coop && cus % 8 == 0 &&
-        cus / 8 <= 64 && occ >= 1) {
+    // Both instances (layer 1, deeper layers) must take the same geometry.
+    int dev = 0, coop = 0, cus = 0, lds_cu = 0;
+    const bool dev_ok = hipGetDevice(&dev) == hipSuccess &&
+                        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
+                        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                        hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) ==
+                            hipSuccess &&
+                        coop && cus % 8 == 0 && cus / 8 <= 64;
+    int pad_of[2] = {-1, -1};
+    for (int l1 = 0; l1 < 2 && dev_ok; ++l1) {
+      const void* kern = xchg_kernel_for(cfg->hidden, cfg->probe, l1 == 1);
+      hipFuncAttributes fa{};
+      int occ = 0;
+      if (!kern || hipFuncGetAttributes(&fa, kern) != hipSuccess ||
+          hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 512, 0) != hipSuccess || occ < 1)
+        break;
       int pad = 0, got = occ;
       if (occ > 1) {
         pad = std::max(0, lds_cu / 2 + 2048 - int(fa.sharedSizeBytes));
@@ -1447,11 +1457,12 @@ void init_ctx(soma_ctx* ctx, const soma_config& cfg0, const Layout& L, char* ws,
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&got, kern, 512, size_t(pad)) != hipSuccess)
           got = 0;
       }
-      if (got == 1) {
-        ctx->xchg_per_cu = 1;
-        ctx->xchg_cus_per_xcd = cus / 8;
-        ctx->xchg_pad_lds = pad;
-      }
+      if (got == 1) pad_of[l1] = pad;
+    }
+    if (pad_of[0] >= 0 && pad_of[1] >= 0) {
+      ctx->xchg_per_cu = 1;
+      ctx->xchg_cus_per_xcd = cus / 8;
+      ctx->xchg_pad_lds = std::max(pad_of[0], pad_of[1]);
     }
     (void)hipGetLastError();
   }

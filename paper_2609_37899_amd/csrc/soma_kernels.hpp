@@ -1287,26 +1287,40 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
 //    s = (t, k) in the order t, then tile k: the products of tile k at step
 //    t need only tile k's h_{t-1}, published NB sub-steps earlier, so its
 //    exchange is hidden behind the products of the other tiles (NB >= 4).
-//  * Each block publishes its 32 units of h_t of a tile already split into
-//    fp16 hi and lo parts, in the order the MFMA B operand reads them: per
-//    32-wide K chunk c and part, 64 lanes x 8 halves, lane (lr, lg) holding
-//    row lr of the tile, columns 32 c + 8 lg .. + 7.  A group keeps two steps
-//    per tile (parity t mod 2) in L2.  h_t is also written to the layer's
-//    hseq rows in fp32 for the kernels that read the whole sequence.
+//  * Each block publishes its 32 units of h_t of a tile (one 32-wide K
+//    chunk) already split into fp16 hi and lo parts, in one of two layouts
+//    of the chunk's 2 KiB.  Fragment order (H <= 512): per part (hi, lo) 64
+//    lanes x 8 halves, lane (lr, lg) holding row lr, columns 8 lg .. + 7,
+//    read by the products as they are; the block transposes h_t through
+//    LDS (one more block barrier) and two waves store whole lines.  Words
+//    (H >= 640): per wave and row one 16-byte word, the four hi parts then
+//    the four lo parts, word (w, r) at index 64 (w & 1) + 16 (w >> 1) + r,
+//    stored straight from the lanes of the cell update (a wave holds 4 units
+//    of each row; three lane swaps bring them together); lane (lr, lg) reads
+//    the words at indices lane and 64 + lane and takes its fragments from
+//    them by register moves.  Either way every 128-byte line is written by
+//    one wave: halves of one word stored by two waves (device coherent) now
+//    and then left a half two steps old.  A group keeps two steps per tile
+//    (parity t mod 2) in L2.  h_t is also written to the layer's hseq rows
+//    in fp32 for the kernels that read the whole sequence.
 //  * The tile's h_{t-1} reaches LDS by DMA (buffer_load_dwordx4 ... lds):
-//    each 1 KiB block lands unchanged and each lane reads its fragment as one
-//    16-byte word -- no staging registers, vector instructions or LDS stores.
-//    The DMA of sub-step s + 2 is issued at the end of sub-step s, into the
-//    LDS buffer its products have just released (two buffers).
+//    each 1 KiB block lands unchanged -- no staging registers, vector
+//    instructions or LDS stores.  The DMA of sub-step s + 2 is issued after
+//    a block barrier of sub-step s, into the LDS buffer the products of
+//    sub-step s have released (two buffers).
 //  * Arrival is a per-(tile, block) flag word holding the steps published.
 //    A sub-step's stores are acknowledged during the next sub-step's
-//    products (one vmcnt(0) per sub-step, after the products), and the flag
-//    is raised right behind the barrier that follows; the flags needed for
-//    the DMA of sub-step s + 2 (raised a sub-step earlier) are read with one
-//    load issued halfway through the products of sub-step s and checked
-//    after them.  The gate inputs are added to the products after that wait
-//    (loads and stores share one counter, so an earlier use of a loaded
-//    value would wait for the pending stores too).
+//    products (one vmcnt(0) per sub-step, after the products: loads and
+//    stores share the counter and may complete out of order, so only a full
+//    wait is sound), and the flag is raised right behind the barrier that
+//    follows; the flags needed for the DMA of sub-step s + 2 (raised a
+//    sub-step earlier) are read with one load issued halfway through the
+//    products of sub-step s and checked after them.
+//  * The gate inputs of a tile's next step go out as early as the wait
+//    allows: at layer 1 (rows of the folded table gathered by byte value,
+//    often cache misses) right after the wait, for the next sub-step's
+//    tile; at deeper layers (a stream of the time-parallel gate inputs)
+//    right after the cell update, which measured faster there.
 //
 // Every wait is bounded: a wave that polls longer than the spin limit, or
 // that sees the step's abort flag, sets the flag and stops waiting; every
@@ -1329,7 +1343,7 @@ constexpr unsigned kAbortPlace = 4u;   // a block found no (group, tile) to clai
 
 struct XchgArgs {
   FwdArgs a;
-  _Float16* xh;          // [groups][2][NB][H/32][2][64][8] published h, split, in fragment order
+  _Float16* xh;          // [groups][2][NB][H/32][wave & 1][wave >> 1][16 rows][4 hi + 4 lo] published h, split
   unsigned* flag;        // [groups][kXchgFlagWords] steps published per (tile, block), over all jobs
   unsigned* cu_count;    // [kXchgCuSlots] blocks started per compute unit (zero at launch)
   unsigned* rank_count;  // [8][kXchgMaxPerCu] blocks claimed per (XCD, rank on the CU) (zero at launch)
@@ -1362,13 +1376,17 @@ __device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t voff, uint32_t soff, 
                : "memory");
 }
 
-template <int NCH, bool kRad>
+// kL1: the layer reads its inputs from the folded table by byte value (layer
+// 1) rather than from the time-parallel gate inputs; a template parameter so
+// that each instance loads its inputs on one path (the compiler would
+// otherwise merge the two paths' pending loads and wait for all of them).
+template <int NCH, bool kRad, bool kL1>
 __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
   constexpr int NW = 8;                                 // waves: 128 gate rows, 32 units (one K chunk of h)
   constexpr int NU = 4 * NW;
   constexpr int NB = kXchgTiles;                        // row tiles of 16 sequences
   constexpr int KC = 2 * NCH;                           // 32-wide k chunks: H = 64 NCH
-  constexpr int FRAG = 512;                             // halves per (chunk, part) block: 64 lanes x 8
+  constexpr int FRAG = 512;                             // halves per 1 KiB block (half a chunk of a tile)
   constexpr int TBUF = KC * 2 * FRAG;                   // halves of one tile's h in LDS
   constexpr int XTILE = KC * 2 * FRAG;                  // halves per published (step, tile)
   constexpr int XSLOT = 2 * NB * XTILE;                 // halves per group: parity x tile
@@ -1376,11 +1394,18 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
   constexpr int ZS_BYTES = 16 * NW * (ZW + 8) * 4;
   constexpr int RING_BYTES = 2 * TBUF * 2;
   constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
-  constexpr int HTLD = NU + 4;                          // LDS row of the h_t tile (float4-aligned)
-  constexpr int NBLK = 2 * KC;                          // 1 KiB blocks per tile: (chunk, part)
+  // Layout of the published h: 16-byte words per (wave, row) at H >= 640,
+  // published straight from the cell lanes (no LDS transpose, no second
+  // block barrier; measured 12% faster at H = 704, where the compiler also
+  // spills fewer registers: 13 against 25); else the MFMA fragment order,
+  // transposed through LDS, whose fragments need no register moves between
+  // the LDS reads and the products (faster at H = 512).
+  constexpr bool kWords = NCH >= 10;
+  constexpr int NBLK = 2 * KC;                          // 1 KiB blocks per tile: (chunk, half)
   constexpr int BPW = (NBLK + NW - 1) / NW;             // of them per wave (the last ones may be short)
   __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
-  __shared__ __attribute__((aligned(16))) float ht[16 * HTLD];
+  constexpr int HTLD = NU + 4;                          // LDS row of the h_t tile (float4-aligned)
+  __shared__ __attribute__((aligned(16))) float ht[kWords ? 4 : 16 * HTLD];
   __shared__ int role[2];
   _Float16* ring = reinterpret_cast<_Float16*>(lds);
   const FwdArgs& a = p.a;
@@ -1464,7 +1489,7 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
     const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
     const __amdgpu_buffer_rsrc_t hbuf = buffer_of(a.hseq + slot * R * H, slot_bytes);
     const __amdgpu_buffer_rsrc_t gbuf =
-        a.layer == 0 ? buffer_of(a.U + slot * kVocab * H4, static_cast<uint32_t>(kVocab * H4 * sizeof(float)))
+        kL1 ? buffer_of(a.U + slot * kVocab * H4, static_cast<uint32_t>(kVocab * H4 * sizeof(float)))
                      : buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(R * H4 * sizeof(float)));
     const __amdgpu_buffer_rsrc_t bbuf = buffer_of(bytes_of(a, e, jl), static_cast<uint32_t>(B * T));
 
@@ -1488,7 +1513,7 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
     // Gate inputs of (step tt, tile k) into gi[k]; layer 1 reads its folded
     // inputs by byte value and fetches the byte of step tt + 1 along.
     auto load_inputs = [&](int tt, int k) {
-      if (a.layer == 0) {
+      if constexpr (kL1) {
         gi[k] = buffer_load_f4<0>(gbuf, static_cast<uint32_t>((vb[k] * 4 * H + 4 * unit) * 4));
         vb[k] = __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(k * 16 * T + tt + 1), 0);
       } else {
@@ -1498,22 +1523,26 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
       cs[k] = 0.0f;
-      vb[k] = a.layer == 0 ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(k * 16 * T), 0)
+      vb[k] = kL1 ? __builtin_amdgcn_raw_buffer_load_b8(bbuf, byte_lane, static_cast<uint32_t>(k * 16 * T), 0)
                            : 0;
     }
+    if constexpr (kL1) {
+      load_inputs(0, 0);                                // the others go out one sub-step ahead
+    } else {
 #pragma unroll
-    for (int k = 0; k < NB; ++k) load_inputs(0, k);
+      for (int k = 0; k < NB; ++k) load_inputs(0, k);
+    }
 
     // Sub-step s = (t, k) reads tile k's h_{t-1} (published by every block
-    // at sub-step s - NB) from LDS buffer s & 1, filled by DMA issued at the
-    // end of sub-step s - 2.
+    // at sub-step s - NB) from LDS buffer s & 1, filled by DMA issued in
+    // sub-step s - 2.
     auto issue = [&](int s) {
       const int t = s / NB, k = s % NB;
       const uint32_t src = static_cast<uint32_t>((grp * XSLOT + (((t - 1) & 1) * NB + k) * XTILE) * 2);
       const uint32_t dst = lds_address(ring + (s & 1) * TBUF);
 #pragma unroll
       for (int i = 0; i < BPW; ++i) {
-        const int b = wave + NW * i;                    // (chunk, part) block b / 2, b % 2
+        const int b = wave + NW * i;                    // chunk b / 2, half b % 2
         if (NBLK % NW == 0 || b < NBLK)                 // wave-uniform
           dma16(xrs, static_cast<uint32_t>(lane * 16), src + static_cast<uint32_t>(b * FRAG * 2),
                 dst + static_cast<uint32_t>(b * FRAG * 2));
@@ -1523,7 +1552,7 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
 #pragma unroll
       for (int k = 0; k < NB; ++k) {
         const int s = t * NB + k;
-        // DMA(s + 2) is issued at the end of this sub-step; its flags, read
+        // DMA(s + 2) is issued after this sub-step's barrier; its flags, read
         // halfway through the products, are checked once they are done.
         const int s2 = s + 2, t2 = s2 / NB;
         const int k2 = (k + 2) % NB;
@@ -1531,13 +1560,19 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
         unsigned v2 = 0;
         f32x4 acc = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
         if (t >= 1) {
-          const _Float16* bsrc = ring + (k & 1) * TBUF + lane * 8;   // buffer s & 1 (NB is even)
+          // buffer s & 1 (NB is even): each read is one contiguous KiB over
+          // the wave's lanes
+          const _Float16* bsrc = ring + (k & 1) * TBUF + lane * 8;
 #pragma unroll
           for (int c = 0; c < KC; ++c) {
             if (c == KC / 2 && need2)
               v2 = __hip_atomic_load(flags + k2 * 64 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const uint4 bh = *reinterpret_cast<const uint4*>(bsrc + (2 * c + 0) * FRAG);
-            const uint4 bl = *reinterpret_cast<const uint4*>(bsrc + (2 * c + 1) * FRAG);
+            const uint4 w0 = *reinterpret_cast<const uint4*>(bsrc + c * 2 * FRAG);
+            const uint4 w1 = *reinterpret_cast<const uint4*>(bsrc + c * 2 * FRAG + FRAG);
+            // Words: lane (lr, lg) takes those of waves 2 lg and 2 lg + 1 for
+            // its row (K 8 lg .. + 3 and 8 lg + 4 .. + 7); fragments: as read.
+            const uint4 bh = kWords ? make_uint4(w0.x, w0.y, w1.x, w1.y) : w0;
+            const uint4 bl = kWords ? make_uint4(w0.z, w0.w, w1.z, w1.w) : w1;
             const h8 AH = __builtin_bit_cast(h8, wh[c]), AL = __builtin_bit_cast(h8, wl[c]);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AL, __builtin_bit_cast(h8, bh), acc, 0, 0, 0);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(AH, __builtin_bit_cast(h8, bl), acc, 0, 0, 0);
@@ -1548,7 +1583,15 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
         }
         // Every memory access of this wave has completed: the stores of
         // sub-step s - 1, the DMA of sub-step s + 1, the flag load, the inputs.
+        // (Loads and stores share the counter and may complete out of order,
+        // so only a full wait is sound here.)
         wait_vmem();
+        // Layer 1: the inputs of the next sub-step's tile, as early as they
+        // can go (the folded table's rows are gathered by byte value and often
+        // miss the cache; the next wait covers them, a whole sub-step on).
+        if constexpr (kL1) {
+          if (s + 1 < S) load_inputs(k + 1 < NB ? t : t + 1, (k + 1) % NB);
+        }
         __syncthreads();
         // Raise the flag of the previous publication (tile k - 1 at step t, or
         // the last tile at step t - 1): every wave's stores of it completed
@@ -1559,41 +1602,69 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
           __hip_atomic_store(flags + kp * 64 + utile, vp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         if (need2 && !ready(base + t2, v2)) wait_flags(k2, base + t2);
+        // Every wave's products of this sub-step are done: its LDS buffer
+        // takes the DMA of sub-step s + 2.
+        if (kWords && need2) issue(s2);
         float h;
         {
           const float4 g = gi[k];
           lstm_cell(acc[0] + g.x, acc[1] + g.y, acc[2] + g.z, acc[3] + g.w, cs[k], h);
         }
-        // Inputs of the tile's next step (past the last step they read zeros
-        // past the buffer or unused bytes: no branch, no register copies).
-        load_inputs(t + 1, k);
-        ht[lr * HTLD + wave * 4 + lg] = h;
-        // The h_t tile is complete and every wave's products of this
-        // sub-step are done: its LDS buffer takes the DMA of sub-step s + 2.
-        __syncthreads();
-        if (need2) issue(s2);
-        // Publish h_t of tile k: threads 0..127 (part, word, row) split 8
-        // units of one row into one fragment word; threads 128..255 (row,
-        // quarter of 4 units) store the fp32 rows of the tile inside the batch.
-        const int tid = threadIdx.x;
-        if (tid < 128) {
-          const int rr = tid & 15, hw = (tid >> 4) & 3, part = tid >> 6;
-          const float* srcw = &ht[rr * HTLD + 8 * hw];
-          uint4 hi, lo;
-          split8v(*reinterpret_cast<const float4*>(srcw), *reinterpret_cast<const float4*>(srcw + 4), hi, lo);
-          const uint4 v = part ? lo : hi;
-          typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-          const uint32_t off = static_cast<uint32_t>(
-              (grp * XSLOT + ((t & 1) * NB + k) * XTILE + (utile * 2 + part) * FRAG + (16 * hw + rr) * 8) * 2);
-          __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, xbuf, off, 0, kCoherent);
-        } else if (tid < 256) {
-          const int n = (tid - 128) >> 3, c4 = tid & 7, row = k * 16 + n;
-          if (row < B) {
-            typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-            const float4 v = *reinterpret_cast<const float4*>(&ht[n * HTLD + 4 * c4]);
-            __builtin_amdgcn_raw_buffer_store_b128(
-                __builtin_bit_cast(u32x4, v), hbuf,
-                static_cast<uint32_t>(((t * B + row) * H + utile * NU + 4 * c4) * 4), 0, 0);
+        // Deeper layers: the tile's inputs of the next step, streamed from
+        // the gate inputs (past the last step they read zeros past the
+        // buffer); issued here they cost less than right after the wait.
+        if constexpr (!kL1) load_inputs(t + 1, k);
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        if constexpr (kWords) {
+          // Publish h_t of tile k straight from the cell lanes.  Lane (lr, lg)
+          // holds unit 4 wave + lg of row lr; the swaps give every lane of
+          // the row all four units.  Lane group 0 stores the row's word (the
+          // four hi parts, then the four lo parts), lane group 2 the four
+          // fp32 values to the layer's sequence when the row is inside the
+          // batch.  Every 128-byte line of the ring is written by one wave.
+          const auto p16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(h), __float_as_uint(h), false, false);
+          const auto qa = __builtin_amdgcn_permlane32_swap(p16[0], p16[0], false, false);   // units 0, 2
+          const auto qb = __builtin_amdgcn_permlane32_swap(p16[1], p16[1], false, false);   // units 1, 3
+          const float4 hv = make_float4(__uint_as_float(qa[0]), __uint_as_float(qb[0]), __uint_as_float(qa[1]),
+                                        __uint_as_float(qb[1]));
+          if (lg == 0) {
+            uint2 hi, lo;
+            split4(hv, hi, lo);
+            const uint32_t off = static_cast<uint32_t>((grp * XSLOT + ((t & 1) * NB + k) * XTILE + utile * 2 * FRAG +
+                                                        (wave & 1) * FRAG + (16 * (wave >> 1) + lr) * 8) * 2);
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4{hi.x, hi.y, lo.x, lo.y}, xbuf, off, 0, kCoherent);
+          } else if (lg == 2 && k * 16 + lr < B) {
+            const uint32_t off = static_cast<uint32_t>(((t * B + k * 16 + lr) * H + utile * NU + 4 * wave) * 4);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, hv), hbuf, off, 0, 0);
+          }
+        } else {
+          // Fragment order: h_t of the tile is transposed through LDS, then
+          // threads 0..127 (part, word, row) split 8 units of one row into one
+          // fragment word, each wave storing whole lines; threads 128..255
+          // (row, quarter of 4 units) store the fp32 rows of the tile inside
+          // the batch.  (Halves of one word stored by two waves, device
+          // coherent, now and then left a half two steps old.)
+          ht[lr * HTLD + wave * 4 + lg] = h;
+          __syncthreads();
+          if (need2) issue(s2);
+          const int tid = threadIdx.x;
+          if (tid < 128) {
+            const int rr = tid & 15, hw = (tid >> 4) & 3, part = tid >> 6;
+            const float* srcw = &ht[rr * HTLD + 8 * hw];
+            uint4 hi, lo;
+            split8v(*reinterpret_cast<const float4*>(srcw), *reinterpret_cast<const float4*>(srcw + 4), hi, lo);
+            const uint4 v = part ? lo : hi;
+            const uint32_t off = static_cast<uint32_t>(
+                (grp * XSLOT + ((t & 1) * NB + k) * XTILE + (utile * 2 + part) * FRAG + (16 * hw + rr) * 8) * 2);
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, xbuf, off, 0, kCoherent);
+          } else if (tid < 256) {
+            const int n = (tid - 128) >> 3, c4 = tid & 7, row = k * 16 + n;
+            if (row < B) {
+              const float4 v = *reinterpret_cast<const float4*>(&ht[n * HTLD + 4 * c4]);
+              __builtin_amdgcn_raw_buffer_store_b128(
+                  __builtin_bit_cast(u32x4, v), hbuf,
+                  static_cast<uint32_t>(((t * B + row) * H + utile * NU + 4 * c4) * 4), 0, 0);
+            }
           }
         }
       }
