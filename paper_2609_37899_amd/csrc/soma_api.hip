@@ -918,6 +918,28 @@ void launch_proj_stream(const soma::FwdArgs& a, int nslots, hipStream_t st) {
     launch_proj_stream_t<true>(a, nslots, st);
 }
 
+// The projection from a pre-split sequence (k_proj_dma), for the widths at
+// which the exchange recurrence stores it (fragment order: H = 128, 256, 512).
+bool proj_dma_width(int H) { return H == 128 || H == 256 || H == 512; }
+
+template <bool kRad>
+void launch_proj_dma_t(const soma::FwdArgs& a, int nslots, hipStream_t st) {
+  const int mblocks = a.H / 32;
+  const dim3 grid(unsigned(nslots * mblocks)), block(soma::kProjThreads);
+  switch (a.H / 64) {
+    case 2: hipLaunchKernelGGL((soma::k_proj_dma<2, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    case 4: hipLaunchKernelGGL((soma::k_proj_dma<4, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+    default: hipLaunchKernelGGL((soma::k_proj_dma<8, kRad>), grid, block, 0, st, a, mblocks, nslots); break;
+  }
+}
+
+void launch_proj_dma(const soma::FwdArgs& a, int nslots, hipStream_t st) {
+  if (a.probe == SOMA_PROBE_GAUSSIAN)
+    launch_proj_dma_t<false>(a, nslots, st);
+  else
+    launch_proj_dma_t<true>(a, nslots, st);
+}
+
 // H = 64 (and the persistent path's other conditions: B <= 64, one slot's
 // gate inputs under 2^31 bytes): the recurrence runs one block per job with
 // h kept in LDS between steps (k_rec_local).
@@ -1291,12 +1313,16 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
   if (int rc = mark(ctx, kPhaseFold, st)) return rc;
   const int rb = rec_row_block(c.batch);
   const int bgroups = (c.batch + rb - 1) / rb;
+  bool split_h = false;   // hseq holds the previous layer's h split into fp16 parts
   for (int l = 0; l < c.n_layers; ++l) {
     a.layer = l;
     a.in_l = l == 0 ? c.embed : c.hidden;
     a.off_l = L.off_layer[l];
     if (l > 0) {
-      if (kPert && stream_weights(c)) {
+      if (split_h) {
+        launch_proj_dma(a, 2 * N * pcs, st);
+        if (int rc = check_launch("k_proj_dma")) return rc;
+      } else if (kPert && stream_weights(c)) {
         launch_proj_stream(a, 2 * N * pcs, st);
         if (int rc = check_launch("k_proj_stream")) return rc;
       } else {
@@ -1310,6 +1336,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
     }
     const int groups = kPert ? persistent_groups(ctx, 2 * N * pcs) : 0;
     const int xgroups = kPert ? xchg_groups(ctx) : 0;
+    bool out_split = false;   // this layer's recurrence stores its h split
     if (kPert && local_recurrence(c)) {
       // H = 64: one block per job, h kept in the block between steps.
       const int jobs = 2 * N * pcs;   // (expert, direction, sign)
@@ -1334,6 +1361,9 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       hipLaunchKernelGGL(soma::k_zero_u32, dim3((words + 255) / 256), dim3(256), 0, st, p.flag, words);
       if (int rc = check_launch("k_zero_u32")) return rc;
       const int blocks = ctx->xchg_per_cu * 8 * ctx->xchg_cus_per_xcd;
+      // The next layer's projection reads this layer's h pre-split (k_proj_dma).
+      p.split_out = l + 1 < c.n_layers && stream_weights(c) && proj_dma_width(H) && c.batch % 16 == 0 ? 1 : 0;
+      out_split = p.split_out != 0;
       if (int rc = launch_persist(xchg_kernel_for(H, c.probe, l == 0), p, blocks, 512, st,
                                   unsigned(ctx->xchg_pad_lds)))
         return rc;
@@ -1368,6 +1398,7 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       if (int rc = check_launch(split ? "k_rec_step_split" : "k_rec_step")) return rc;
       ctx->rec_launches += c.seq_len - 1;
     }
+    split_h = out_split;
     if (int rc = mark(ctx, kPhaseRec, st)) return rc;
   }
   if (fused_head) {

@@ -1302,7 +1302,10 @@ __global__ __launch_bounds__(64 * NW, 1) void k_rec_persist(PersistArgs p) {
 //    one wave: halves of one word stored by two waves (device coherent) now
 //    and then left a half two steps old.  A group keeps two steps per tile
 //    (parity t mod 2) in L2.  h_t is also written to the layer's hseq rows
-//    in fp32 for the kernels that read the whole sequence.
+//    for the kernels that read the whole sequence: in fp32, or (split_out:
+//    fragment order, B = 64, where the next layer's projection is
+//    k_proj_dma) as the same split words, in 1 KiB blocks [16-row tile][hi,
+//    lo][32-wide k chunk], word 16 lg + lr holding row lr, k 8 lg .. + 7.
 //  * The tile's h_{t-1} reaches LDS by DMA (buffer_load_dwordx4 ... lds):
 //    each 1 KiB block lands unchanged -- no staging registers, vector
 //    instructions or LDS stores.  The DMA of sub-step s + 2 is issued after
@@ -1353,6 +1356,7 @@ struct XchgArgs {
   int per_cu;            // blocks per compute unit of the launch
   int jobs;              // N * directions in this pass * 2 signs
   unsigned spin_limit;   // polls per wait before giving up
+  int split_out;         // store the layer's h to hseq split, in fragment-order blocks (for k_proj_dma)
 };
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -1658,12 +1662,30 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
                 (grp * XSLOT + ((t & 1) * NB + k) * XTILE + (utile * 2 + part) * FRAG + (16 * hw + rr) * 8) * 2);
             __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, xbuf, off, 0, kCoherent);
           } else if (tid < 256) {
-            const int n = (tid - 128) >> 3, c4 = tid & 7, row = k * 16 + n;
-            if (row < B) {
-              const float4 v = *reinterpret_cast<const float4*>(&ht[n * HTLD + 4 * c4]);
+            if (p.split_out) {
+              // The same words as the exchange's, into the sequence's
+              // fragment-order layout: 1 KiB block (row tile, part, k chunk
+              // = this block's units), word 16 hw + rr.  (B % 16 == 0, so a
+              // tile of the batch is one row tile of the sequence.)  16-byte
+              // stores: 8-byte stores whose data registers were rewritten by
+              // the next instruction stored corrupted values.
+              const int u = tid - 128, rr = u & 15, hw = (u >> 4) & 3, part = u >> 6;
+              const float* srcw = &ht[rr * HTLD + 8 * hw];
+              uint4 hi, lo;
+              split8v(*reinterpret_cast<const float4*>(srcw), *reinterpret_cast<const float4*>(srcw + 4), hi, lo);
+              const uint4 v = part ? lo : hi;
+              const int rt = (t * B) / 16 + k;
               __builtin_amdgcn_raw_buffer_store_b128(
-                  __builtin_bit_cast(u32x4, v), hbuf,
-                  static_cast<uint32_t>(((t * B + row) * H + utile * NU + 4 * c4) * 4), 0, 0);
+                  u32x4{v.x, v.y, v.z, v.w}, hbuf,
+                  static_cast<uint32_t>((((rt * 2 + part) * KC + utile) * FRAG + (16 * hw + rr) * 8) * 2), 0, 0);
+            } else {
+              const int n = (tid - 128) >> 3, c4 = tid & 7, row = k * 16 + n;
+              if (row < B) {
+                const float4 v = *reinterpret_cast<const float4*>(&ht[n * HTLD + 4 * c4]);
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    __builtin_bit_cast(u32x4, v), hbuf,
+                    static_cast<uint32_t>(((t * B + row) * H + utile * NU + 4 * c4) * 4), 0, 0);
+              }
             }
           }
         }
@@ -2293,6 +2315,139 @@ __global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_stream(
     }
     if (c + 1 < nchunks) sstore(buf ^ 1);
     __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The input projection of k_proj_stream from a pre-split sequence
+// (k_proj_dma): where the previous layer's recurrence stored its h already
+// split into fp16 parts, in MFMA fragment order -- hseq as 1 KiB blocks
+// [16-row tile][hi, lo][32-wide k chunk], word 16 lg + lr holding row lr,
+// k 8 lg .. + 7 (the same bytes as fp32) -- the ring is filled by LDS DMA
+// (buffer_load_dwordx4 ... lds), one contiguous block per instruction, and
+// the products read each fragment as one 16-byte word.  Staging
+// then takes no registers, vector instructions, LDS stores or waits beside
+// the products: the DMA of the next ring chunk is issued before the current
+// chunk's products, and one wait and one barrier close each chunk.  The
+// split is the one k_proj_stream applies while staging, so the products and
+// results are the same.  The gate inputs of a finished 64-row tile are
+// stored after the barrier, so the next wait finds them done.
+// ---------------------------------------------------------------------------
+template <int NCH, bool kRad>
+__global__ __launch_bounds__(kProjThreads, NCH <= 2 ? 4 : 1) void k_proj_dma(FwdArgs a, int mblocks, int nslots) {
+  constexpr int KC = 2 * NCH;                 // 32-wide k chunks: K = H = 64 NCH
+  constexpr int NQ = NCH % 4 == 0 ? NCH / 4 : (NCH > 8 ? (NCH % 2 == 0 ? NCH / 2 : NCH) : split_quarters(NCH));
+  constexpr int QC = KC / NQ;                 // k chunks per ring chunk
+  constexpr int KW = QC * 32;                 // k per ring chunk
+  constexpr int FRAG = 512;                   // halves per 1 KiB block
+  constexpr int NBLK = 2 * 4 * QC;            // blocks per ring chunk: (part, row tile, k chunk)
+  constexpr int BUF = NBLK * FRAG;            // halves per ring buffer
+  constexpr int BPW = (NBLK + 7) / 8;         // blocks per wave
+  constexpr int RING_BYTES = 2 * BUF * 2;
+  constexpr int ZW = KC * 32 < kZpiece ? KC * 32 : kZpiece;   // probe piece width
+  constexpr int ZS_BYTES = 128 * (ZW + 8) * 4;
+  constexpr int LDS_BYTES = RING_BYTES > ZS_BYTES ? RING_BYTES : ZS_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[LDS_BYTES];
+  _Float16* ring = reinterpret_cast<_Float16*>(lds);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, lr = lane & 15, lg = lane >> 4;
+  const int H = a.H, B = a.B, T = a.T;
+  const int R = (T - 1) * B;
+  const int H4 = 4 * H;
+
+  int ps, mb;                                 // slot of this pass, row block (as k_proj_stream)
+  {
+    const int b = blockIdx.x;
+    if (nslots % 8 == 0) {
+      const int i = b / 8;
+      mb = i % mblocks;
+      ps = (i / mblocks) * 8 + b % 8;
+    } else {
+      ps = b / mblocks;
+      mb = b % mblocks;
+    }
+  }
+  const int sg = ps & 1, pj = ps >> 1;
+  const int e = pj / a.pcs, jl = pj % a.pcs;
+  const int64_t slot = (static_cast<int64_t>(e) * a.PC + jl) * 2 + sg;
+  const float* th = a.theta + static_cast<int64_t>(e) * a.d;
+  const uint2 key = stream_key(a.seeds[e], a.step);
+  const uint32_t pair = static_cast<uint32_t>(a.j0 + jl), step_lo = static_cast<uint32_t>(a.step);
+  const float seps = sg == 0 ? eps_of(a, e, kGroupLstm) : -eps_of(a, e, kGroupLstm);
+  const int unit = mb * 32 + wave * 4 + lg;   // output unit of this lane
+  // 32-bit offsets: R 4H floats < 2^31 bytes (host check).  Every DMA offset
+  // is per lane (bounds-checked): row tiles past R (B % 16 == 0) read zeros
+  // and are never stored.
+  const i32x4 hrs = buffer_words(a.hseq + slot * R * H, static_cast<uint32_t>(static_cast<int64_t>(R) * H * 4));
+  const __amdgpu_buffer_rsrc_t gbuf =
+      buffer_of(a.gin + slot * R * H4, static_cast<uint32_t>(static_cast<int64_t>(R) * H4 * sizeof(float)));
+
+  uint4 wh[KC], wl[KC];
+  resident_weights_split<KC, true, kRad, ZW>(wh, wl, reinterpret_cast<float*>(lds), th, a.off_l, a.in_l + H, 0, H,
+                                         mb * 128, a.probe, key, pair, step_lo, seps, a.err);
+
+  // Ring chunk c covers rows [64 (c / NQ), +64) and k [KW (c % NQ), +KW);
+  // block b of it is (part b / (4 QC), row tile (b / QC) % 4, k chunk b % QC).
+  const int nchunks = ((R + 63) / 64) * NQ;
+  auto issue = [&](int c) {
+    const int r0 = (c / NQ) * 64, k0 = (c % NQ) * KW;
+    const uint32_t dst = lds_address(ring + (c & 1) * BUF);
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int b = wave + 8 * i;
+      if (NBLK % 8 == 0 || b < NBLK) {            // wave-uniform
+        const int part = b / (4 * QC), nb = (b / QC) % 4, pq = b % QC;
+        const int rt = r0 / 16 + nb, kc = k0 / 32 + pq;
+        const uint32_t voff = static_cast<uint32_t>((((rt * 2 + part) * KC + kc) * FRAG + lane * 8) * 2);
+        dma16(hrs, voff, 0u, dst + static_cast<uint32_t>(b * FRAG * 2));
+      }
+    }
+  };
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // The weights' probe scratch overlays the ring: the barriers inside the
+  // weight formation come before this first DMA.
+  issue(0);
+  wait_vmem();
+  __syncthreads();
+  for (int c = 0; c < nchunks; ++c) {
+    if (c + 1 < nchunks) issue(c + 1);           // into the buffer chunk c - 1 read
+    const int qq = c % NQ;
+    const _Float16* bl0 = ring + (c & 1) * BUF + lane * 8;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      if (q == qq) {                           // compile-time register index into wh, wl
+#pragma unroll
+        for (int pq = 0; pq < QC; ++pq) {
+          uint4 bh[4], bl[4];
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) {
+            bh[nb] = *reinterpret_cast<const uint4*>(bl0 + (nb * QC + pq) * FRAG);
+            bl[nb] = *reinterpret_cast<const uint4*>(bl0 + ((4 + nb) * QC + pq) * FRAG);
+          }
+          mfma3_batch<4>(wh[q * QC + pq], wl[q * QC + pq], bh, bl, acc);
+        }
+      }
+    }
+    // The DMA of chunk c + 1 and the stores of the previous tile are done,
+    // every wave's products of chunk c too (its buffer takes chunk c + 2).
+    wait_vmem();
+    __syncthreads();
+    if (qq == NQ - 1) {
+      const int r0 = (c / NQ) * 64;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int row = r0 + nb * 16 + lr;
+        if (row < R) {
+          typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[nb]), gbuf,
+                                                 static_cast<uint32_t>((row * H4 + 4 * unit) * 4), 0, 0);
+        }
+        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
   }
 }
 
