@@ -117,11 +117,17 @@ enum soma_flags {
    * within the split products' rounding. */
   SOMA_FLAG_TILED_WEIGHTS = 2,
   /* Run the persistent recurrence with fp32 h staged by every block of a
-   * group, even where the split exchange applies (h published once in
-   * split form and copied into LDS by DMA, several groups per compute
-   * unit).  Both form the same split products in the same order, so their
-   * results agree bit for bit. */
-  SOMA_FLAG_STAGED_RECURRENCE = 4
+   * group, even where the pipelined split exchange applies (four row tiles
+   * in flight, h published once in split form and copied into LDS by DMA).
+   * Both form the same split products; the exchange adds the gate inputs
+   * after them rather than before, so results agree within that rounding. */
+  SOMA_FLAG_STAGED_RECURRENCE = 4,
+  /* Store each layer's output sequence in fp32 and let the next layer's
+   * streaming projection split it while staging it, even where the
+   * exchange recurrence stores it pre-split in fragment order for the
+   * DMA-staged projection (B = 64, H = 128, 256, 512).  Both split the same
+   * fp32 values the same way, so results agree bit for bit. */
+  SOMA_FLAG_FP32_SEQUENCE = 8
 };
 
 /* Parameter groups that soma_config.perturb_mask names.  A masked group

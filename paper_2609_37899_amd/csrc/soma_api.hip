@@ -131,7 +131,8 @@ int validate(const soma_config* c) {
     return fail(SOMA_ESHAPE, "n_pairs * accum must stay below 2^24");
   if (c->pair_chunk < 0 || c->pair_chunk > dirs(*c))
     return fail(SOMA_ESHAPE, "pair_chunk must be in [0, n_pairs * accum]");
-  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS | SOMA_FLAG_STAGED_RECURRENCE))
+  if (c->flags & ~(SOMA_FLAG_PER_STEP_RECURRENCE | SOMA_FLAG_TILED_WEIGHTS | SOMA_FLAG_STAGED_RECURRENCE |
+                   SOMA_FLAG_FP32_SEQUENCE))
     return fail(SOMA_EINVAL, "unknown flags");
   if (c->probe != SOMA_PROBE_GAUSSIAN && c->probe != SOMA_PROBE_SPARSE_RADEMACHER &&
       c->probe != SOMA_PROBE_RADEMACHER)
@@ -1362,7 +1363,8 @@ int run_forward(soma_ctx* ctx, const float* theta, const uint64_t* seeds, uint64
       if (int rc = check_launch("k_zero_u32")) return rc;
       const int blocks = ctx->xchg_per_cu * 8 * ctx->xchg_cus_per_xcd;
       // The next layer's projection reads this layer's h pre-split (k_proj_dma).
-      p.split_out = l + 1 < c.n_layers && stream_weights(c) && proj_dma_width(H) && c.batch % 16 == 0 ? 1 : 0;
+      p.split_out = l + 1 < c.n_layers && stream_weights(c) && proj_dma_width(H) && c.batch % 16 == 0 &&
+                    !(c.flags & SOMA_FLAG_FP32_SEQUENCE) ? 1 : 0;
       out_split = p.split_out != 0;
       if (int rc = launch_persist(xchg_kernel_for(H, c.probe, l == 0), p, blocks, 512, st,
                                   unsigned(ctx->xchg_pad_lds)))

@@ -19,6 +19,7 @@ PROBE_GAUSSIAN, PROBE_SPARSE_RADEMACHER, PROBE_RADEMACHER = 0, 1, 2
 FLAG_PER_STEP_RECURRENCE = 1
 FLAG_TILED_WEIGHTS = 2
 FLAG_STAGED_RECURRENCE = 4
+FLAG_FP32_SEQUENCE = 8
 ARCH_LSTM, ARCH_BODY, ARCH_WIDE = 0, 1, 2
 PERTURB_EMBEDDING, PERTURB_LSTM, PERTURB_HEAD, PERTURB_ALL = 1, 2, 4, 7
 

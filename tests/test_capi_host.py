@@ -64,7 +64,7 @@ def test_workspace_size_and_auto_chunk(lib):
 @pytest.mark.parametrize("field,value,code", [
     ("embed", 24, soma.SOMA_ESHAPE), ("hidden", 0, soma.SOMA_ESHAPE), ("seq_len", 1, soma.SOMA_ESHAPE),
     ("n_pairs", 0, soma.SOMA_ESHAPE), ("loss_mode", 2, soma.SOMA_EINVAL),
-    ("pair_chunk", 99, soma.SOMA_ESHAPE), ("flags", 8, soma.SOMA_EINVAL), ("probe", 3, soma.SOMA_EINVAL),
+    ("pair_chunk", 99, soma.SOMA_ESHAPE), ("flags", 16, soma.SOMA_EINVAL), ("probe", 3, soma.SOMA_EINVAL),
     ("probe", -1, soma.SOMA_EINVAL), ("accum", -1, soma.SOMA_ESHAPE), ("perturb_mask", 8, soma.SOMA_EINVAL)])
 def test_invalid_shapes_are_rejected(lib, field, value, code):
     s = shape_of(workloads.TINY)

@@ -212,6 +212,35 @@ def test_exchange_recurrence_is_repeatable(name, probe):
         assert np.array_equal(r["theta"], runs[0]["theta"])
 
 
+@pytest.mark.parametrize("name,probe", [("b64_h128", 0), ("b64_h128", 2), ("h256_b64_jobs", 1)])
+def test_presplit_sequence_is_bit_identical(name, probe):
+    """Layer 1's exchange recurrence stores its h pre-split in fragment order
+    and layer 2's projection stages it by DMA (k_proj_dma); with
+    SOMA_FLAG_FP32_SEQUENCE the sequence stays fp32 and the streaming
+    projection splits it while staging.  Both split the same values the same
+    way: losses and weights agree bit for bit."""
+    torch = require_gpu()
+    N, L, E, H, B, T, P, eps, lr, mode, pc = CASES[name]
+    theta = synth.init_theta(N, L, E, H, init_seed=1, distinct=True)
+    data = synth.expert_batches([100 + e for e in range(N)], B, T)
+    seeds = soma.seeds_tensor(synth.expert_seeds(N))
+    outs = []
+    for flags in (0, soma.FLAG_FP32_SEQUENCE):
+        ctx = soma.Context(soma.Shape(N, L, E, H, B, T, P, mode, pc, flags, probe))
+        ctx.set_phase_timing(True)
+        th = torch.from_numpy(theta.copy()).cuda()
+        losses = torch.zeros((N, P, 2), dtype=torch.float32, device="cuda")
+        ctx.spsa_step(th, seeds, 2, eps, lr, torch.from_numpy(data).cuda(), losses)
+        pt = ctx.phase_times()
+        torch.cuda.synchronize()
+        outs.append((th.cpu().numpy(), losses.cpu().numpy(), pt["xchg_launches"]))
+    (t0, l0, x0), (t1, l1, x1) = outs
+    assert x0 > 0 and x1 > 0                  # both through the exchange recurrence
+    assert np.all(np.isfinite(l0))
+    assert np.array_equal(l0, l1)
+    assert np.array_equal(t0, t1)
+
+
 def test_chunking_does_not_change_the_result():
     torch = require_gpu()
     N, L, E, H, B, T, P = 2, 2, 32, 32, 8, 12, 5
