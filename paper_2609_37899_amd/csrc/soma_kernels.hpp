@@ -1667,8 +1667,10 @@ __global__ __launch_bounds__(512) void k_rec_xchg(XchgArgs p) {
               // fragment-order layout: 1 KiB block (row tile, part, k chunk
               // = this block's units), word 16 hw + rr.  (B % 16 == 0, so a
               // tile of the batch is one row tile of the sequence.)  16-byte
-              // stores: 8-byte stores whose data registers were rewritten by
-              // the next instruction stored corrupted values.
+              // stores: a version with two 8-byte stores per thread (whose
+              // data registers the next instruction rewrote) left non-finite
+              // values under the Rademacher laws at H = 128; its cause was
+              // not established.
               const int u = tid - 128, rr = u & 15, hw = (u >> 4) & 3, part = u >> 6;
               const float* srcw = &ht[rr * HTLD + 8 * hw];
               uint4 hi, lo;

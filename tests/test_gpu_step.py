@@ -212,6 +212,17 @@ def test_exchange_recurrence_is_repeatable(name, probe):
         assert np.array_equal(r["theta"], runs[0]["theta"])
 
 
+@pytest.mark.parametrize("name,probe", [("h64_b50_l2", 0), ("h64_b50_l2", 1), ("h64_e64_b33", 0)])
+def test_local_recurrence_is_repeatable(name, probe):
+    """The same step four times through the one-block recurrence at H = 64
+    (its h stored for the next layer's projection and the head) gives
+    bit-identical losses and weights."""
+    runs = [run_case(name, probe=probe) for _ in range(4)]
+    for r in runs[1:]:
+        assert np.array_equal(r["losses"], runs[0]["losses"])
+        assert np.array_equal(r["theta"], runs[0]["theta"])
+
+
 @pytest.mark.parametrize("name,probe", [("b64_h128", 0), ("b64_h128", 2), ("h256_b64_jobs", 1)])
 def test_presplit_sequence_is_bit_identical(name, probe):
     """Layer 1's exchange recurrence stores its h pre-split in fragment order
