@@ -30,7 +30,8 @@ PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
 PEAK_FP16_MFMA_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
 # Kernels whose products run on the fp16 matrix cores from split fp32
 # operands (three fp16 products per fp32 product, fp32 accumulation).
-SPLIT_F16_KERNELS = ("k_rec_xchg", "k_rec_persist", "k_rec_local", "k_rec_step_split", "k_proj_stream", "k_head_stream",
+SPLIT_F16_KERNELS = ("k_rec_xchg", "k_rec_persist", "k_rec_local", "k_rec_step_split", "k_proj_stream", "k_proj_dma",
+                     "k_head_stream",
                      "k_head_fused", "k_body", "k_wide_mm")
 PEAK_HBM_GBS = 8000.0
 PROBE_LAWS = {"gaussian": 0, "sparse": 1, "dense": 2}
@@ -288,13 +289,17 @@ def main():
     traffic = None
     # The kernels the library picks for this shape (see soma_api.hip):
     # streaming projection and head where H % 64 == 0, H <= 704 and one
-    # slot's gate inputs stay under 2^31 bytes; the recurrence one block per
-    # job at H = 64, else persistent (one launch per layer and chunk) unless
-    # it ran per time step (split fp16 products where H % 32 == 0).
+    # slot's gate inputs stay under 2^31 bytes (the projection from the
+    # pre-split sequence after the exchange recurrence in fragment order with
+    # B = 64); the recurrence one block per job at H = 64, else persistent (one
+    # launch per layer and chunk) unless it ran per time step (split fp16
+    # products where H % 32 == 0).
     streams = (w.hidden % 64 == 0 and w.hidden <= 704
                and (w.seq_len - 1) * w.batch * 4 * w.hidden * 4 < 2 ** 31)
+    presplit = (streams and phases.get("xchg_launches", 0) > 0 and w.batch == 64
+                and w.hidden in (128, 256, 512))
     kname = {"rec": "k_rec_step_split" if w.hidden % 32 == 0 else "k_rec_step",
-             "proj": "k_proj_stream" if streams else "k_proj", "fold": "k_fold",
+             "proj": ("k_proj_dma" if presplit else "k_proj_stream") if streams else "k_proj", "fold": "k_fold",
              "head": ("k_head_fused" if w.hidden <= 128 else "k_head_stream") if streams else "k_head_ce"}[dom]
     if w.arch == 1:
         kname = "k_body"          # the whole perturbed forward, one launch per direction chunk
