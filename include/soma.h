@@ -246,8 +246,8 @@ void soma_destroy(soma_ctx* ctx);
  * expert; the seeds are a device array, so a step enqueues no host-to-device
  * copy and can be replayed without host work; and the step counter that keys
  * the probe stream is explicit.
- * Where the shape allows (H <= 512, B <= 64, a device that supports
- * cooperative launches), each layer's recurrence runs as one persistent
+ * Where the shape allows (H <= 704 and a multiple of 64, B <= 64, a device
+ * that supports cooperative launches), each layer's recurrence runs as one persistent
  * launch whose blocks synchronise per time step through bounded waits; if a
  * wait ever times out, the step's losses are NaN and theta is left
  * unchanged.
@@ -461,8 +461,9 @@ int soma_estimator_moments(soma_ctx* ctx, const uint64_t* seeds_dev, uint64_t st
 typedef struct soma_phase_times {
   float fold_ms;          /* layer-1 gate inputs per byte value (k_fold; 0 where
                              the H = 64 recurrence forms them in the block) */
-  float proj_ms;          /* input projections of layers >= 2 (k_proj_stream, or
-                             the tiled k_proj) */
+  float proj_ms;          /* input projections of layers >= 2 (k_proj_dma from a
+                             pre-split sequence, k_proj_stream, or the tiled
+                             k_proj) */
   float rec_ms;           /* recurrent time steps of all layers (k_rec_xchg or
                              k_rec_persist or, at H = 64, k_rec_local: one launch per layer and
                              chunk; or k_rec_step, one per time step); for

@@ -4,8 +4,11 @@
 // at once, both signs of each direction side by side):
 //   k_fold          layer-1 gate inputs per byte value (embedding times the
 //                   input weights, perturbed rows formed on the fly)
-//   per layer l:    k_proj_stream (l >= 2: h^(l-1) times the input weights,
-//                   weights held in registers) then the recurrence:
+//   per layer l:    for l >= 2, h^(l-1) times the input weights, weights
+//                   held in registers: k_proj_dma where the previous layer's
+//                   k_rec_xchg stored its h pre-split (B % 16 = 0,
+//                   H = 128, 256, 512), else k_proj_stream; then the
+//                   recurrence:
 //                   k_rec_xchg (one cooperative launch, four row tiles of
 //                   the batch pipelined, h exchanged pre-split by LDS DMA)
 //                   or k_rec_persist (one cooperative launch; blocks of a
@@ -20,7 +23,10 @@
 //   k_coef          c_{e,j} (independent) or dF_j / (2 eps_e P) (summed)
 //   k_update / k_update_adam   theta -= lr sum_j c_j z_j, regenerating z_j
 // The paper's width-32 body (SOMA_ARCH_BODY) runs its whole perturbed
-// forward in k_body (soma_body.hpp).  Every kernel that forms split fp16
+// forward in k_body (soma_body.hpp); the wide controls' body
+// (SOMA_ARCH_WIDE) forms each slot's perturbed weights once (k_wide_form)
+// and runs split-fp16 products (k_wide_mm), LayerNorms and the decoder
+// (soma_wide.hpp) around k_rec_persist on the pre-formed weights.  Every kernel that forms split fp16
 // weights checks their range and the persistent recurrence bounds its waits:
 // either failure sets a sticky flag, and the step is then aborted on the
 // device (NaN losses, theta untouched).  The step writes theta only in the
