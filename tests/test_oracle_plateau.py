@@ -24,14 +24,25 @@ def torch_schedule(rate0, losses, patience, factor, threshold, floor):
     return np.array(out)
 
 
-@pytest.mark.parametrize("patience", [1, 3, 7])
-def test_plateau_equals_torch_reduce_on_plateau(oracle_mod, patience):
+# The paper's threshold (1e-8) is below fp32's spacing near a loss of 5, so
+# only the larger thresholds make the curves improve by less than the
+# threshold and test that such a step is no improvement.
+@pytest.mark.parametrize("patience,threshold", [(1, 1e-8), (3, 1e-8), (7, 1e-8), (3, 5e-4), (2, 2e-3)])
+def test_plateau_equals_torch_reduce_on_plateau(oracle_mod, patience, threshold):
     rng = np.random.default_rng(patience)
     n, steps = 3, 400
     # noisy decreasing curves with long flat stretches, per expert
     base = np.cumsum(rng.exponential(1e-3, (steps, n)) * (rng.random((steps, n)) < 0.2), axis=0)
     losses = (5.0 - base + rng.normal(0, 1e-4, (steps, n))).astype(np.float32)
-    sch = oracle_mod.Plateau(n, 1e-3, 2e-3, factor=0.5, patience=patience, threshold=1e-8, floor=1e-5)
+    if threshold > 1e-6:
+        # some improvements on the running best fall below the threshold
+        best, small = np.full(n, np.inf), 0
+        for t in range(steps):
+            gain = best - losses[t].astype(np.float64)
+            small += int(np.sum((gain > 0) & (gain <= threshold)))
+            best = np.minimum(best, losses[t])
+        assert small >= 5
+    sch = oracle_mod.Plateau(n, 1e-3, 2e-3, factor=0.5, patience=patience, threshold=threshold, floor=1e-5)
     lrs, epss = [], []
     for t in range(steps):
         sch.observe(losses[t])
@@ -40,8 +51,8 @@ def test_plateau_equals_torch_reduce_on_plateau(oracle_mod, patience):
         epss.append(eps)
     lrs, epss = np.array(lrs), np.array(epss)
     for e in range(n):
-        ref_lr = torch_schedule(1e-3, losses[:, e], patience, 0.5, 1e-8, 1e-5)
-        ref_eps = torch_schedule(2e-3, losses[:, e], patience, 0.5, 1e-8, 1e-5)
+        ref_lr = torch_schedule(1e-3, losses[:, e], patience, 0.5, threshold, 1e-5)
+        ref_eps = torch_schedule(2e-3, losses[:, e], patience, 0.5, threshold, 1e-5)
         np.testing.assert_array_equal(lrs[:, e].astype(np.float64), ref_lr.astype(np.float32).astype(np.float64))
         np.testing.assert_array_equal(epss[:, e].astype(np.float64), ref_eps.astype(np.float32).astype(np.float64))
     assert lrs.min() < 1e-3 and lrs.min() >= F(1e-5)       # decays happened, none below the floor
